@@ -1,0 +1,408 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Every check here uses something other than the oracle's own formulas: a
+hand-derived worked example, exact integer arithmetic, textbook closed forms
+(Sylvester-Hadamard codebooks, M = 1), invariants the paper states (Eq. 1-4,
+U^T U = I, x = U U^T x), brute-force exact rank over rationals, LAPACK
+(numpy.linalg) and scipy routines, and the paper's printed values.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+from paper_2608_01528_amd import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ------------------------------------------------------------------ helpers
+
+def exact_rank(rows) -> int:
+    """Rank over the rationals by Gaussian elimination with Fractions."""
+    A = [[Fraction(int(v)) for v in r] for r in rows]
+    m = len(A)
+    n = len(A[0]) if m else 0
+    rank = 0
+    for col in range(n):
+        piv = next((i for i in range(rank, m) if A[i][col] != 0), None)
+        if piv is None:
+            continue
+        A[rank], A[piv] = A[piv], A[rank]
+        for i in range(rank + 1, m):
+            if A[i][col] != 0:
+                f = A[i][col] / A[rank][col]
+                A[i] = [a - f * b for a, b in zip(A[i], A[rank])]
+        rank += 1
+        if rank == m:
+            break
+    return rank
+
+
+def greedy_kept(C) -> list:
+    """Rows that raise the exact rank when taken in index order."""
+    kept, r = [], 0
+    for i in range(C.shape[0]):
+        ri = exact_rank(C[: i + 1])
+        if ri > r:
+            kept.append(i)
+            r = ri
+    return kept
+
+
+def exact_gram(C) -> np.ndarray:
+    Ci = C.astype(np.int64)
+    return Ci @ Ci.T
+
+
+def read_worked():
+    lines = [l.split() for l in open(os.path.join(GOLDEN, "worked_rank2.txt"))
+             if l.strip() and not l.startswith("#")]
+    out, key, rows = {}, None, []
+    for t in lines:
+        if t[0] in ("codebook", "R", "Q"):
+            if key:
+                out[key] = np.array(rows, float)
+            key, rows = t[0], []
+        elif t[0] == "rank":
+            out[key] = np.array(rows, float)
+            key, rows = None, []
+            out["rank"] = int(t[1])
+        elif t[0] == "kept":
+            out["kept"] = [int(v) for v in t[1:]]
+        else:
+            rows.append([float(v) for v in t])
+    if key:
+        out[key] = np.array(rows, float)
+    return out
+
+
+def read_paper_values():
+    vals = {}
+    for l in open(os.path.join(GOLDEN, "paper_values.txt")):
+        if l.strip() and not l.startswith("#"):
+            k, v = l.split()[:2]
+            vals[k] = float(v)
+    return vals
+
+
+# --------------------------------------------------------------- compress
+
+def test_worked_example_rank2():
+    g = read_worked()
+    Q, R, kept, r = oracle.compress(g["codebook"])
+    assert r == g["rank"] == 2
+    assert list(kept) == g["kept"]
+    np.testing.assert_allclose(R, g["R"], atol=1e-15)
+    np.testing.assert_allclose(Q, g["Q"], atol=1e-15)
+
+
+@pytest.mark.parametrize("kind,M,D,seed", [
+    ("bipolar", 10, 1024, 1), ("bipolar", 22, 1024, 2), ("binary", 40, 512, 4),
+    ("bipolar", 64, 256, 7), ("binary", 96, 300, 8)])
+def test_orthonormal_and_exact_factorisation(kind, M, D, seed):
+    # P1 Q Q^T = I (Sec. 3.2, U^T U = I);  P2 C = R Q (Eq. 1, Eq. 4);
+    # P3 R R^T = C C^T computed exactly in integers.
+    C = (wl.bipolar_codebook if kind == "bipolar" else wl.binary_codebook)(M, D, seed)
+    Q, R, kept, r = oracle.compress(C)
+    assert r == M
+    assert np.abs(Q @ Q.T - np.eye(r)).max() <= 1e-12
+    RQ = R @ Q
+    assert np.abs(RQ - C).max() <= 1e-12 * np.abs(C).max()
+    assert np.array_equal(np.rint(RQ), C)
+    G = exact_gram(C).astype(np.float64)
+    assert np.abs(R @ R.T - G).max() <= 1e-12 * np.abs(G).max()
+    # lower echelon, positive pivots
+    for k, i in enumerate(kept):
+        assert R[i, k] > 0
+        assert np.all(R[i, k + 1:] == 0)
+
+
+def test_r_is_cholesky_factor_of_gram():
+    # Uniqueness: with rows kept in index order and positive pivots, the kept
+    # rows of R are the Cholesky factor of their exact Gram matrix (LAPACK).
+    C = wl.bipolar_codebook(48, 640, 11)
+    C[7] = C[3]
+    C[20] = -C[5]
+    Q, R, kept, r = oracle.compress(C)
+    K = list(kept)
+    L = np.linalg.cholesky(exact_gram(C[K]).astype(np.float64))
+    np.testing.assert_allclose(R[K], L, atol=1e-10, rtol=0)
+
+
+def test_q_matches_lapack_qr():
+    # Q^T equals the Q of LAPACK's Householder QR of W = C^T up to column
+    # signs, fixed by requiring a positive diagonal of the triangular factor.
+    C = wl.binary_codebook(30, 200, 12)
+    Q, R, kept, r = oracle.compress(C)
+    Ql, Rl = np.linalg.qr(C.T.astype(np.float64))
+    s = np.sign(np.diag(Rl))
+    np.testing.assert_allclose(Q, (Ql * s).T, atol=1e-12)
+    np.testing.assert_allclose(R, (Rl * s[:, None]).T, atol=1e-11)
+
+
+def _tiny_cases():
+    rng = np.random.default_rng(5)
+    cases = []
+    for t in range(12):
+        M = int(rng.integers(2, 13))
+        D = int(rng.integers(M, 65))
+        C = (2 * rng.integers(0, 2, (M, D)) - 1).astype(np.float64)
+        if t % 3 == 0:
+            C[M - 1] = C[0]                 # duplicate
+        if t % 3 == 1 and M > 2:
+            C[M - 1] = -C[1]                # negation
+        if t % 4 == 2 and M > 3:
+            C[M - 1] = C[0] + C[1] - C[2]   # integer combination
+        cases.append(C)
+    # binary rows with disjoint support and their sum
+    B = np.zeros((5, 24))
+    B[0, :8] = 1
+    B[1, 8:16] = 1
+    B[2, 16:] = 1
+    B[3] = B[0] + B[1]
+    B[4, ::2] = 1
+    cases.append(B)
+    # short and wide: more rows than linearly possible is excluded (D >= M),
+    # a zero row is dependent
+    Z = (2 * rng.integers(0, 2, (6, 16)) - 1).astype(np.float64)
+    Z[2] = 0
+    cases.append(Z)
+    return cases
+
+
+@pytest.mark.parametrize("idx", range(14))
+def test_rank_and_kept_brute_force(idx):
+    # P7: rank = algebraic rank (Sec. 3.2), checked by exact rational
+    # elimination; kept rows = first rows that raise the exact rank.
+    C = _tiny_cases()[idx]
+    Q, R, kept, r = oracle.compress(C)
+    assert r == exact_rank(C)
+    assert list(kept) == greedy_kept(C)
+    assert np.abs(R @ Q - C).max() <= 1e-12
+
+
+def test_hadamard_closed_form():
+    # P8: exactly orthogonal +-1 rows: R = sqrt(D) I, Q = C / sqrt(D),
+    # cos(c_i, c_j) = delta_ij.
+    D = 64
+    C = wl.hadamard_codebook(D)
+    Q, R, kept, r = oracle.compress(C)
+    assert r == D
+    np.testing.assert_allclose(R, math.sqrt(D) * np.eye(D), atol=1e-13)
+    np.testing.assert_allclose(Q, C / math.sqrt(D), atol=1e-15)
+    S = oracle.similarity(C, C, oracle.COSINE)
+    np.testing.assert_allclose(S, np.eye(D), atol=1e-15)
+
+
+@pytest.mark.parametrize("D", [1, 7, 1024])
+def test_single_vector(D):
+    # P14: M = 1 -> q = c/|c|, R = |c| (sqrt(D) for a bipolar vector).
+    c = wl.bipolar_codebook(1, D, 3)
+    Q, R, kept, r = oracle.compress(c)
+    assert r == 1 and list(kept) == [0]
+    assert abs(R[0, 0] - math.sqrt(D)) <= 1e-15 * math.sqrt(D)
+    np.testing.assert_allclose(Q[0], c[0] / math.sqrt(D), atol=1e-16)
+
+
+def test_dependent_row_coefficients():
+    # P15: duplicate -> same coordinates; negation -> negated; sum -> sum.
+    C = wl.bipolar_codebook(12, 128, 21).astype(np.float64)
+    C = np.vstack([C, C[4], -C[6], C[1] + C[9]])
+    Q, R, kept, r = oracle.compress(C)
+    assert r == 12 and list(kept) == list(range(12))
+    np.testing.assert_allclose(R[12], R[4], atol=1e-12)
+    np.testing.assert_allclose(R[13], -R[6], atol=1e-12)
+    np.testing.assert_allclose(R[14], R[1] + R[9], atol=1e-12)
+
+
+def test_duplicated_rows_rank_by_construction():
+    # 10 % duplicated rows of a 64 x 512 bipolar codebook: rank = 64 - 6.
+    C = wl.bipolar_codebook(64, 512, 5)
+    C2, targets, sources = wl.duplicate_rows(C, 0.1, 5)
+    assert len(targets) == 6
+    Q, R, kept, r = oracle.compress(C2)
+    assert r == 58 == np.linalg.matrix_rank(C2)
+    # every row whose copy occurs earlier is dependent
+    for i in range(64):
+        earlier = any(np.array_equal(C2[i], C2[j]) for j in range(i))
+        assert (i in set(kept)) != earlier
+
+
+@pytest.mark.parametrize("tau", [1e-12, 1e-10, 1e-6, 1e-3])
+def test_rank_stable_over_threshold(tau):
+    C = wl.binary_codebook(80, 256, 9).astype(np.float64)
+    C[40:50] = C[0:10] + C[10:20]
+    Q, R, kept, r = oracle.compress(C, tau=tau)
+    assert r == 70 == np.linalg.matrix_rank(C)
+
+
+def test_thread_count_does_not_change_bits():
+    C = wl.binary_codebook(60, 333, 13)
+    n0 = oracle.threads()
+    try:
+        oracle.set_threads(1)
+        a = oracle.compress(C)
+        P = wl.dirichlet_probs(50, 60, 0.3, 1)
+        s1 = oracle.similarity(oracle.prob2vec(P, C), C)
+        oracle.set_threads(4)
+        b = oracle.compress(C)
+        s4 = oracle.similarity(oracle.prob2vec(P, C), C)
+    finally:
+        oracle.set_threads(n0)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    assert np.array_equal(s1, s4)
+
+
+# ----------------------------------------------- dense operators vs library
+
+def test_dense_operators_match_numpy():
+    rng = np.random.default_rng(3)
+    C = rng.standard_normal((9, 70))
+    X = rng.standard_normal((13, 70))
+    P = rng.random((13, 9))
+    Q = rng.standard_normal((5, 70))
+    T = rng.standard_normal((13, 5))
+    np.testing.assert_allclose(oracle.prob2vec(P, C), P @ C, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.similarity(X, C, oracle.DOT, 0.5), 0.5 * X @ C.T,
+                               rtol=1e-13, atol=1e-13)
+    cos = (X @ C.T) / np.outer(np.linalg.norm(X, axis=1), np.linalg.norm(C, axis=1))
+    np.testing.assert_allclose(oracle.similarity(X, C, oracle.COSINE), cos, rtol=1e-13,
+                               atol=1e-15)
+    np.testing.assert_allclose(oracle.project(X, Q), X @ Q.T, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.reconstruct(T, Q), T @ Q, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(oracle.row_norms(X), np.linalg.norm(X, axis=1), rtol=1e-14)
+    np.testing.assert_array_equal(oracle.bind(X, C[:1].repeat(13, 0)), X * C[0])
+
+
+def test_softmax_properties():
+    # P10: rows sum to one; equal scores give 1/M; shift invariance; scipy.
+    rng = np.random.default_rng(4)
+    S = rng.standard_normal((20, 17)) * 3
+    for beta in (1.0, 16.0):
+        A = oracle.softmax(S, beta)
+        np.testing.assert_allclose(A.sum(1), 1.0, atol=1e-15)
+        np.testing.assert_allclose(A, scipy.special.softmax(beta * S, axis=1), rtol=1e-13)
+        np.testing.assert_allclose(oracle.softmax(S + 5.0, beta), A, rtol=1e-12)
+    np.testing.assert_allclose(oracle.softmax(np.full((3, 7), 2.5), 4.0), 1 / 7, rtol=1e-15)
+    # large beta: no overflow, mass on the maximum
+    A = oracle.softmax(np.array([[0.0, 1.0, 0.5]]), 1e4)
+    assert A[0, 1] == 1.0 and np.isfinite(A).all()
+
+
+def test_argmax_ties_lowest_index():
+    S = np.array([[1.0, 3.0, 3.0, 2.0], [5.0, 5.0, 5.0, 5.0], [-1.0, -2.0, -1.0, -0.5]])
+    assert list(oracle.argmax(S)) == [1, 0, 3]
+
+
+def test_cosine_zero_norm_is_zero():
+    C = np.array([[1.0, 0.0], [0.0, 0.0]])
+    X = np.array([[0.0, 0.0], [3.0, 4.0]])
+    S = oracle.similarity(X, C, oracle.COSINE)
+    np.testing.assert_array_equal(S, [[0.0, 0.0], [0.6, 0.0]])
+
+
+# ------------------------------------------- invariants of the paper's method
+
+def test_inner_products_preserved_eq2():
+    # P5 (Eq. 2): <x, c_j> = <U^T x, U^T c_j> = <Q x, R_j>; for x outside the
+    # span it still holds because c_j lies in it.
+    C = wl.bipolar_codebook(40, 512, 6)
+    Q, R, kept, r = oracle.compress(C)
+    rng = np.random.default_rng(6)
+    P = wl.dirichlet_probs(32, 40, 0.5, 6)
+    X_in = oracle.prob2vec(P, C)
+    X_out = X_in + rng.standard_normal(X_in.shape)
+    for X in (X_in, X_out):
+        dense = oracle.similarity(X, C, oracle.DOT)
+        coords = oracle.project(X, Q) @ R.T
+        assert np.abs(dense - coords).max() <= 1e-12 * np.abs(dense).max()
+
+
+def test_similarity_invariant_eq3_in_span():
+    # Eq. 3: cosine of in-span vectors equals the cosine of their Gram-locs.
+    C = wl.binary_codebook(25, 300, 8)
+    Q, R, kept, r = oracle.compress(C)
+    P = wl.dirichlet_probs(16, 25, 0.2, 8)
+    V = oracle.prob2vec(P, C)
+    T = oracle.project(V, Q)
+    np.testing.assert_allclose(oracle.similarity(T, R, oracle.COSINE),
+                               oracle.similarity(V, C, oracle.COSINE), atol=1e-13)
+
+
+def test_reconstruction_exact_in_span_eq4():
+    # P6 (Eq. 4, x = U U^T x): restore(project(v)) = v for v in the span, and
+    # the probability vector maps to P R in Gram-loc.
+    C = wl.bipolar_codebook(22, 1024, 2)
+    Q, R, kept, r = oracle.compress(C)
+    P = wl.softmax_probs(64, 22, math.sqrt(2), 2)
+    V = oracle.prob2vec(P, C)
+    T = oracle.project(V, Q)
+    np.testing.assert_allclose(T, P.astype(np.float64) @ R, atol=1e-12)
+    assert np.abs(oracle.reconstruct(T, Q) - V).max() <= 1e-12
+
+
+def test_one_hot_probabilities():
+    # P9: one-hot p selects its codebook vector exactly; cosine 1 with itself;
+    # argmax is its index.
+    C = wl.bipolar_codebook(10, 1024, 1)
+    Q, R, kept, r = oracle.compress(C)
+    P = np.eye(10)
+    V = oracle.prob2vec(P, C)
+    assert np.array_equal(V, C)
+    S = oracle.similarity(V, C, oracle.COSINE)
+    assert list(oracle.argmax(S)) == list(range(10))
+    np.testing.assert_allclose(np.diag(S), 1.0, atol=1e-15)
+    assert np.array_equal(np.rint(oracle.reconstruct(P @ R, Q)), C)
+
+
+def test_bipolar_self_binding_is_identity():
+    # P11: c (.) c = 1 for bipolar vectors; binding commutes.
+    C = wl.bipolar_codebook(4, 256, 3)
+    assert np.array_equal(oracle.bind(C, C), np.ones_like(C, dtype=np.float64))
+    assert np.array_equal(oracle.bind(C[:2], C[2:]), oracle.bind(C[2:], C[:2]))
+
+
+def test_table4_similarity_score_100_percent():
+    # P12: the reconstructed codebook R Q has cosine 1 with the original
+    # (Table 4: similarity score 100 %).
+    pv = read_paper_values()
+    for C in (wl.bipolar_codebook(40, 2048, 1), wl.binary_codebook(40, 256, 1)):
+        Q, R, kept, r = oracle.compress(C)
+        rec = oracle.reconstruct(R, Q)
+        cos = np.diag(oracle.similarity(rec, C, oracle.COSINE))
+        assert 100.0 * cos.min() >= pv["similarity_score_percent"] * (1 - 1e-12)
+
+
+def test_memory_model_paper_ratios():
+    # P13: D/k = 6.4 at M = 40, D = 256 (Sec. 3.1); 51x at D = 2048 (Table 4).
+    pv = read_paper_values()
+    C = wl.bipolar_codebook(40, 256, 1)
+    k = oracle.compress(C)[3]
+    assert oracle.memory_model(40, 256, k)["per_vector_ratio"] == pv["ratio_D256_k40"]
+    assert math.floor(oracle.memory_model(40, 2048, 40)["per_vector_ratio"]) == pv["ratio_table4"]
+    mm = oracle.memory_model(40, 256, 40)
+    assert mm["dense_bytes"] == 40 * 256 * 4 and mm["compressed_bytes"] == (256 + 40) * 40 * 4
+
+
+@pytest.mark.parametrize("D", [64, 1024])
+def test_rank_threshold_is_relative_residual(D):
+    # c1 = c0 + delta e_0: the part of c1 outside span{c0} has norm
+    # delta * sqrt(1 - 1/D) (closed form), so the relative residual is
+    # rho / |c1|.  A threshold just above it makes c1 dependent, just below
+    # keeps it (Sec. 3.2: rank is the algebraic rank up to the threshold).
+    c0 = wl.bipolar_codebook(1, D, 17)[0].astype(np.float64)
+    delta = 1e-6 * math.sqrt(D)
+    c1 = c0.copy()
+    c1[0] += delta
+    rel = delta * math.sqrt(1 - 1 / D) / np.linalg.norm(c1)
+    C = np.vstack([c0, c1])
+    assert oracle.compress(C, tau=rel * 1.01)[3] == 1
+    Q, R, kept, r = oracle.compress(C, tau=rel * 0.99)
+    assert r == 2
+    # the residual is a difference of vectors of norm |c1|: error ~ eps |c1|
+    assert abs(R[1, 1] - delta * math.sqrt(1 - 1 / D)) <= 1e-12 * np.linalg.norm(c1)
