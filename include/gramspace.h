@@ -1,0 +1,219 @@
+/*
+ * gramspace.h -- C ABI of the Gram-Space operator library for MI355X (gfx950).
+ *
+ * Gram-Space (Wang & Li, "Gram-Space: Structure-Preserving Codebook
+ * Compression for Memory-Efficient Neuro-Symbolic AI") factors a VSA codebook
+ * into an orthonormal basis and per-vector coordinates ("Gram-loc"), runs the
+ * matrix-space operators (probability vectorisation, similarity, attention
+ * score) on the coordinates, and restores vectors to the original domain only
+ * before component-wise operators such as binding.
+ *
+ * Notation.  The paper stores the codebook as W (D x M, one codebook vector
+ * per column), the basis as U (D x k) and the Gram-loc codebook as
+ * T = U^T W (Sec. 3.1, Eq. 1).  This library stores the transposes, row-major:
+ *   C  (M x D)  codebook, row j = codebook vector c_j       (= W^T)
+ *   Q  (r x D)  orthonormal basis, row k = basis vector q_k (= U^T)
+ *   R  (M x r)  Gram-loc of the codebook, C = R Q           (= T^T)
+ *   T  (B x r)  Gram-loc of a batch of B vectors, x_b = T_b Q
+ * r is the algebraic rank of C (Sec. 3.2).  All matrices are row-major with a
+ * leading dimension (elements between consecutive rows) ld >= columns.
+ *
+ * Memory and ownership.  Every matrix argument is a device pointer (HIP
+ * device memory of the current device) unless marked HOST.  The caller
+ * allocates every buffer, including workspace; the library allocates no
+ * device memory, keeps no state besides a thread-local error message, and
+ * never frees caller memory.  Inputs are read-only.  Outputs must not overlap
+ * inputs or each other (GS_ERR_ARG).
+ *
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
+ * Every call except gs_compress only enqueues work on that stream and returns
+ * without waiting.  gs_compress synchronises the stream before returning
+ * because the rank is returned in host memory.
+ *
+ * Element types.  GS_F32 and GS_BF16 (bfloat16 storage, fp32 arithmetic) for
+ * batch data and coordinates; GS_F64 additionally for compress input/outputs.
+ * Within one call, the two operands of a contraction have the same type.
+ * Scores and attention weights are always fp32.  Conversions to bf16 round to
+ * nearest even.
+ *
+ * Errors.  Every call returns a gs_status; gs_last_error() returns a text
+ * description of the last failure on the calling thread.  Arguments are
+ * validated before any device work; on a validation failure nothing is
+ * written.  A zero batch (B == 0) is valid and does nothing; its batch-sized
+ * buffers may then be NULL.  A failing launch
+ * returns GS_ERR_DEVICE and leaves outputs undefined.
+ */
+#ifndef GRAMSPACE_H
+#define GRAMSPACE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GS_ABI_VERSION 1
+
+typedef enum {
+    GS_OK = 0,
+    GS_ERR_ARG = 1,        /* null pointer, bad enum, negative size, overlap */
+    GS_ERR_SHAPE = 2,      /* inconsistent sizes or leading dimensions       */
+    GS_ERR_DTYPE = 3,      /* unsupported element-type combination          */
+    GS_ERR_ALIGN = 4,      /* pointer not aligned to its element size        */
+    GS_ERR_WORKSPACE = 5,  /* workspace missing or too small                 */
+    GS_ERR_NUMERIC = 6,    /* non-finite codebook entry                      */
+    GS_ERR_DEVICE = 7      /* no usable GPU, or a HIP call failed            */
+} gs_status;
+
+typedef enum { GS_F32 = 0, GS_BF16 = 1, GS_F64 = 2 } gs_dtype;
+
+/* Similarity function of Sec. 2.2: a scaled dot product, or the dot product
+   of the normalised vectors (cosine). */
+typedef enum { GS_SIM_DOT = 0, GS_SIM_COSINE = 1 } gs_sim_mode;
+
+/* Component-wise operator applied after restoring two vectors. */
+typedef enum { GS_BIND_NONE = 0, GS_BIND_MUL = 1 } gs_bind;
+
+/* ABI version of the loaded library (GS_ABI_VERSION of its build). */
+int gs_abi_version(void);
+
+/* Text of the last error on the calling thread ("" if none).  The pointer
+   stays valid until the next gs_* call on the same thread. */
+const char *gs_last_error(void);
+
+/*
+ * gs_compress_workspace -- bytes of device workspace gs_compress needs for an
+ * M x D codebook.  Returns 0 for invalid sizes.
+ */
+size_t gs_compress_workspace(int64_t M, int64_t D);
+
+/*
+ * gs_compress -- Gram-Space compression (Sec. 3.1 Eq. 1; rank Sec. 3.2;
+ * construction at initialisation Sec. 3.3).
+ *
+ * Builds an orthonormal basis Q of the row space of the codebook C and its
+ * coordinates R with C = R Q, by blocked modified Gram-Schmidt with one
+ * re-orthogonalisation pass, in fp64.  Codebook rows are taken in index
+ * order; row i is dependent (adds no basis vector) when the norm of its part
+ * outside the current span, after both passes, is <= tol * ||c_i||.  Kept rows
+ * are listed in `kept`, so basis vector k comes from codebook row kept[k].  R
+ * is lower-echelon: R[i, k] = <c_i, q_k> for basis vectors created before row
+ * i, R[kept[k], k] > 0, zero elsewhere.  With these rules Q and R are unique.
+ *
+ *   C      in   M x D, ct in {F32, BF16, F64}, leading dimension ldc >= D
+ *   M, D        1 <= M <= D (D < M needs the paper's partitioned bases, which
+ *               this library does not build: GS_ERR_SHAPE)
+ *   tol         relative rank threshold, 0 <= tol < 1 (1e-10 recommended)
+ *   Q      out  rank x D, qt in {F64, F32, BF16}, ldq >= D; rows rank..M-1
+ *               are zero-filled (capacity M rows)
+ *   R      out  M x rank, rt in {F64, F32, BF16}, ldr >= M; columns rank..M-1
+ *               are zero-filled (capacity M columns)
+ *   kept   out  int32[M] device, nullable; entries rank..M-1 set to -1
+ *   cnorm  out  float[M] device, nullable: ||c_i|| (used by cosine similarity)
+ *   rank   out  HOST int32
+ *   ws          device workspace of >= gs_compress_workspace(M, D) bytes,
+ *               256-byte aligned; contents on return are unspecified
+ *   stream      synchronised before return
+ * Errors: GS_ERR_NUMERIC if C holds a NaN or infinity (detected on the device;
+ * outputs are then undefined).
+ */
+gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
+                      double tol,
+                      void *Q, gs_dtype qt, int64_t ldq,
+                      void *R, gs_dtype rt, int64_t ldr,
+                      int32_t *kept, float *cnorm, int32_t *rank,
+                      void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * gs_project -- Gram-loc of a batch (Sec. 3.1: t = U^T x):  T = X Q^T.
+ *
+ *   X      in   B x D, xt in {F32, BF16}, ldx >= D
+ *   Q      in   r x D, qt == xt, ldq >= D
+ *   T      out  B x r, tt in {F32, BF16}, ldt >= r
+ *   xnorm2 out  float[B], nullable: ||x_b||^2 of the dense input, computed in
+ *               the same pass (needed for cosine similarity of vectors that
+ *               are not in the span of the codebook)
+ * fp32 accumulation.
+ */
+gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,
+                     const void *Q, gs_dtype qt, int64_t r, int64_t ldq,
+                     void *T, gs_dtype tt, int64_t ldt,
+                     float *xnorm2, void *stream);
+
+/*
+ * gs_prob2vec -- probability vectorisation on Gram-loc (Sec. 2.2, Sec. 3.1):
+ * the dense v_b = sum_j P[b, j] c_j is never formed; its Gram-loc is
+ * T = P R.
+ *
+ *   P      in   B x M, pt in {F32, BF16}, ldp >= M
+ *   R      in   M x r, rt == pt, ldr >= r
+ *   T      out  B x r, tt in {F32, BF16}, ldt >= r
+ * fp32 accumulation.
+ */
+gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t ldp,
+                      const void *R, gs_dtype rt, int64_t r, int64_t ldr,
+                      void *T, gs_dtype tt, int64_t ldt, void *stream);
+
+/*
+ * gs_similarity -- similarity of each batch vector with every codebook vector,
+ * on Gram-loc (Sec. 2.2; invariance Sec. 3.2 Eq. 2-3):
+ *   DOT:     S[b, j] = scale * <t_b, R_j>                       (= <x_b, c_j>)
+ *   COSINE:  S[b, j] = scale * <t_b, R_j> / (||x_b|| ||c_j||), 0 if a norm is 0
+ * with ||x_b||^2 = qnorm2[b] when given (e.g. from gs_project), else ||t_b||^2
+ * (exact for vectors in the span, such as prob2vec outputs), and
+ * ||c_j|| = cnorm[j] when given, else ||R_j||.
+ *
+ *   T      in   B x r, tt in {F32, BF16}, ldt >= r
+ *   R      in   M x r, rt == tt, ldr >= r
+ *   qnorm2 in   float[B], nullable;  cnorm in float[M], nullable
+ *   S      out  float B x M, nullable, lds >= M
+ *   argmax out  int32[B], nullable: index of the largest S[b, :], the lowest
+ *               index on an exact tie
+ * At least one of S and argmax must be given.  fp32 accumulation.
+ */
+gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                        const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                        const float *qnorm2, const float *cnorm,
+                        gs_sim_mode mode, float scale,
+                        float *S, int64_t lds, int32_t *argmax, void *stream);
+
+/*
+ * gs_attention -- attention score over the codebook (Sec. 2.2): the softmax
+ * over j of beta * S[b, j], with S as in gs_similarity (same T, R, qnorm2,
+ * cnorm, mode and scale), and optionally the attention-weighted sum of the
+ * codebook vectors in Gram-loc, O = A R (its dense form is sum_j A[b,j] c_j).
+ *
+ *   A      out  float B x M, lda >= M (required)
+ *   O      out  B x r, ot in {F32, BF16}, ldo >= r, nullable
+ */
+gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                       const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                       const float *qnorm2, const float *cnorm,
+                       gs_sim_mode mode, float scale, float beta,
+                       float *A, int64_t lda,
+                       void *O, gs_dtype ot, int64_t ldo, void *stream);
+
+/*
+ * gs_reconstruct -- restore vectors to the original domain (Sec. 3.1 and
+ * Sec. 3.3, the "decompose" step): X = T Q.  With bind == GS_BIND_MUL and a
+ * second coordinate batch T2, the two restored vectors are bound
+ * component-wise (Sec. 2.2; Table 1 "element-wise product") in the same pass:
+ * X = (T Q) .* (T2 Q).
+ *
+ *   T      in   B x r, tt in {F32, BF16}, ldt >= r
+ *   T2     in   B x r, same type as T, ldt2 >= r; required iff bind == MUL
+ *   Q      in   r x D, qt == tt, ldq >= D
+ *   X      out  B x D, xt in {F32, BF16}, ldx >= D
+ * fp32 accumulation.
+ */
+gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                         const void *T2, int64_t ldt2, gs_bind bind,
+                         const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
+                         void *X, gs_dtype xt, int64_t ldx, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRAMSPACE_H */

@@ -1,0 +1,303 @@
+// C-ABI entry points of the Gram-Space library: argument validation, error
+// reporting and dispatch to the kernels.  Every check runs on the host before
+// any HIP call, so a rejected call touches neither the device nor its outputs.
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <string>
+
+#include "gs_internal.h"
+
+using namespace gs;
+
+namespace {
+
+thread_local std::string g_err;
+
+gs_status fail(gs_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return st;
+}
+
+gs_status ok() {
+    g_err.clear();
+    return GS_OK;
+}
+
+size_t esize(gs_dtype t) { return t == GS_F64 ? 8 : (t == GS_F32 ? 4 : 2); }
+bool valid_dtype(int t) { return t == GS_F32 || t == GS_BF16 || t == GS_F64; }
+const char *dname(gs_dtype t) { return t == GS_F32 ? "f32" : (t == GS_BF16 ? "bf16" : "f64"); }
+
+// Byte range occupied by a rows x cols matrix with leading dimension ld.
+struct Span {
+    const char *lo = nullptr, *hi = nullptr;
+    const char *name = "";
+};
+
+Span span(const void *p, int64_t rows, int64_t cols, int64_t ld, size_t es, const char *name) {
+    Span s;
+    s.name = name;
+    if (!p || rows <= 0 || cols <= 0) return s;
+    s.lo = static_cast<const char *>(p);
+    s.hi = s.lo + ((rows - 1) * ld + cols) * (int64_t)es;
+    return s;
+}
+
+bool overlap(const Span &a, const Span &b) {
+    return a.lo && b.lo && a.lo < b.hi && b.lo < a.hi;
+}
+
+// Outputs must overlap neither inputs nor each other.
+gs_status check_overlaps(std::initializer_list<Span> in, std::initializer_list<Span> out) {
+    for (const Span &o : out) {
+        for (const Span &i : in)
+            if (overlap(o, i)) return fail(GS_ERR_ARG, "output %s overlaps input %s", o.name, i.name);
+        for (const Span &o2 : out)
+            if (&o2 != &o && overlap(o, o2)) return fail(GS_ERR_ARG, "outputs %s and %s overlap", o.name, o2.name);
+    }
+    return GS_OK;
+}
+
+gs_status check_aligned(const void *p, size_t es, const char *name) {
+    if (p && (reinterpret_cast<uintptr_t>(p) % es) != 0)
+        return fail(GS_ERR_ALIGN, "%s is not aligned to its %zu-byte element", name, es);
+    return GS_OK;
+}
+
+#define GS_CHECK(x) do { gs_status s_ = (x); if (s_ != GS_OK) return s_; } while (0)
+
+gs_status check_matrix(const void *p, const char *name, int64_t rows, int64_t cols, int64_t ld,
+                       gs_dtype t, bool nullable) {
+    if (!p) {
+        // an empty batch may come without storage
+        if (nullable || rows == 0) return GS_OK;
+        return fail(GS_ERR_ARG, "%s is null", name);
+    }
+    if (ld < cols) return fail(GS_ERR_SHAPE, "leading dimension of %s (%lld) is smaller than its %lld columns",
+                                name, (long long)ld, (long long)cols);
+    return check_aligned(p, esize(t), name);
+}
+
+gs_status check_device() {
+    static std::atomic<int> state{-1};   // -1 unknown, 0 none, 1 ok
+    int s = state.load();
+    if (s < 0) {
+        int n = 0;
+        hipError_t e = hipGetDeviceCount(&n);
+        s = (e == hipSuccess && n > 0) ? 1 : 0;
+        state.store(s);
+    }
+    if (!s) return fail(GS_ERR_DEVICE, "no HIP device is available");
+    return GS_OK;
+}
+
+gs_status launched(hipError_t e, const char *what) {
+    if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+    if (getenv("GS_DEBUG")) {
+        hipError_t e2 = hipDeviceSynchronize();
+        if (e2 != hipSuccess) return fail(GS_ERR_DEVICE, "%s (GS_DEBUG sync): %s", what, hipGetErrorString(e2));
+    }
+    return ok();
+}
+
+bool is_batch_type(gs_dtype t) { return t == GS_F32 || t == GS_BF16; }
+
+}  // namespace
+
+extern "C" {
+
+int gs_abi_version(void) { return GS_ABI_VERSION; }
+
+const char *gs_last_error(void) { return g_err.c_str(); }
+
+size_t gs_compress_workspace(int64_t M, int64_t D) {
+    if (M < 1 || D < 1 || M > D) return 0;
+    return compress_workspace(M, D);
+}
+
+gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                      void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
+                      int32_t *kept, float *cnorm, int32_t *rank, void *ws, size_t ws_bytes,
+                      void *stream) {
+    if (!valid_dtype(ct) || !valid_dtype(qt) || !valid_dtype(rt))
+        return fail(GS_ERR_DTYPE, "gs_compress: unknown element type");
+    if (!rank) return fail(GS_ERR_ARG, "gs_compress: rank (host) is null");
+    if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "gs_compress: M and D must be >= 1 (M=%lld, D=%lld)",
+                                    (long long)M, (long long)D);
+    if (M > D) return fail(GS_ERR_SHAPE, "gs_compress: M=%lld > D=%lld needs partitioned bases, not supported",
+                           (long long)M, (long long)D);
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "gs_compress: tol must be in [0, 1)");
+    GS_CHECK(check_matrix(C, "C", M, D, ldc, ct, false));
+    GS_CHECK(check_matrix(Q, "Q", M, D, ldq, qt, false));
+    GS_CHECK(check_matrix(R, "R", M, M, ldr, rt, false));
+    GS_CHECK(check_aligned(kept, 4, "kept"));
+    GS_CHECK(check_aligned(cnorm, 4, "cnorm"));
+    if (!ws) return fail(GS_ERR_WORKSPACE, "gs_compress: workspace is null");
+    if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+        return fail(GS_ERR_ALIGN, "gs_compress: workspace must be 256-byte aligned");
+    const size_t need = compress_workspace(M, D);
+    if (ws_bytes < need)
+        return fail(GS_ERR_WORKSPACE, "gs_compress: workspace of %zu bytes, %zu needed", ws_bytes, need);
+    const Span sC = span(C, M, D, ldc, esize(ct), "C");
+    const Span sW = span(ws, 1, (int64_t)need, (int64_t)need, 1, "workspace");
+    GS_CHECK(check_overlaps({sC, sW}, {span(Q, M, D, ldq, esize(qt), "Q"), span(R, M, M, ldr, esize(rt), "R"),
+                                       span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    GS_CHECK(check_device());
+    int nonfinite = 0;
+    int32_t r = 0;
+    hipError_t e = run_compress(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
+                                &nonfinite, ws, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(GS_ERR_DEVICE, "gs_compress: %s", hipGetErrorString(e));
+    if (nonfinite) return fail(GS_ERR_NUMERIC, "gs_compress: codebook holds a NaN or infinity");
+    *rank = r;
+    return ok();
+}
+
+gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,
+                     const void *Q, gs_dtype qt, int64_t r, int64_t ldq,
+                     void *T, gs_dtype tt, int64_t ldt, float *xnorm2, void *stream) {
+    if (!is_batch_type(xt) || qt != xt || !is_batch_type(tt))
+        return fail(GS_ERR_DTYPE, "gs_project: X/Q must be both f32 or both bf16 and T f32 or bf16 (got %s/%s/%s)",
+                    dname(xt), dname(qt), valid_dtype(tt) ? dname(tt) : "?");
+    if (B < 0 || D < 1 || r < 1) return fail(GS_ERR_SHAPE, "gs_project: need B >= 0, D >= 1, r >= 1");
+    GS_CHECK(check_matrix(X, "X", B, D, ldx, xt, false));
+    GS_CHECK(check_matrix(Q, "Q", r, D, ldq, qt, false));
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    GS_CHECK(check_aligned(xnorm2, 4, "xnorm2"));
+    GS_CHECK(check_overlaps({span(X, B, D, ldx, esize(xt), "X"), span(Q, r, D, ldq, esize(qt), "Q")},
+                            {span(T, B, r, ldt, esize(tt), "T"), span(xnorm2, 1, B, B, 4, "xnorm2")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    GemmArgs a{};
+    a.A = X; a.lda = ldx; a.B = Q; a.ldb = ldq; a.C = T; a.ldc = ldt;
+    a.M = B; a.N = r; a.K = D; a.rownorm2 = xnorm2;
+    return launched(launch_gemm(xt, qt, tt, false, EPI_STORE, a, (hipStream_t)stream), "gs_project");
+}
+
+gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t ldp,
+                      const void *R, gs_dtype rt, int64_t r, int64_t ldr,
+                      void *T, gs_dtype tt, int64_t ldt, void *stream) {
+    if (!is_batch_type(pt) || rt != pt || !is_batch_type(tt))
+        return fail(GS_ERR_DTYPE, "gs_prob2vec: P/R must be both f32 or both bf16 and T f32 or bf16");
+    if (B < 0 || M < 1 || r < 1 || r > M) return fail(GS_ERR_SHAPE, "gs_prob2vec: need B >= 0 and 1 <= r <= M");
+    GS_CHECK(check_matrix(P, "P", B, M, ldp, pt, false));
+    GS_CHECK(check_matrix(R, "R", M, r, ldr, rt, false));
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    GS_CHECK(check_overlaps({span(P, B, M, ldp, esize(pt), "P"), span(R, M, r, ldr, esize(rt), "R")},
+                            {span(T, B, r, ldt, esize(tt), "T")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+        SmallArgs a{};
+        a.In = P; a.ldin = ldp; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = T; a.ldout = ldt;
+        return launched(launch_small_prob2vec(pt, tt, a, (hipStream_t)stream), "gs_prob2vec");
+    }
+    GemmArgs a{};
+    a.A = P; a.lda = ldp; a.B = R; a.ldb = ldr; a.C = T; a.ldc = ldt; a.M = B; a.N = r; a.K = M;
+    return launched(launch_gemm(pt, rt, tt, true, EPI_STORE, a, (hipStream_t)stream), "gs_prob2vec");
+}
+
+static gs_status check_sim_common(const char *fn, const void *T, gs_dtype tt, int64_t B, int64_t r,
+                                  int64_t ldt, const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                                  const float *qnorm2, const float *cnorm, int mode) {
+    if (!is_batch_type(tt) || rt != tt)
+        return fail(GS_ERR_DTYPE, "%s: T/R must be both f32 or both bf16", fn);
+    if (mode != GS_SIM_DOT && mode != GS_SIM_COSINE) return fail(GS_ERR_ARG, "%s: unknown similarity mode", fn);
+    if (B < 0 || M < 1 || r < 1 || r > M) return fail(GS_ERR_SHAPE, "%s: need B >= 0 and 1 <= r <= M", fn);
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    GS_CHECK(check_matrix(R, "R", M, r, ldr, rt, false));
+    GS_CHECK(check_aligned(qnorm2, 4, "qnorm2"));
+    GS_CHECK(check_aligned(cnorm, 4, "cnorm"));
+    return GS_OK;
+}
+
+gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                        const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                        const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
+                        float *S, int64_t lds, int32_t *argmax, void *stream) {
+    GS_CHECK(check_sim_common("gs_similarity", T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
+    if (!S && !argmax) return fail(GS_ERR_ARG, "gs_similarity: S and argmax are both null");
+    GS_CHECK(check_matrix(S, "S", B, M, lds, GS_F32, true));
+    GS_CHECK(check_aligned(argmax, 4, "argmax"));
+    GS_CHECK(check_overlaps({span(T, B, r, ldt, esize(tt), "T"), span(R, M, r, ldr, esize(rt), "R"),
+                             span(qnorm2, 1, B, B, 4, "qnorm2"), span(cnorm, 1, M, M, 4, "cnorm")},
+                            {span(S, B, M, lds, 4, "S"), span(argmax, 1, B, B, 4, "argmax")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+        SmallArgs a{};
+        a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = S; a.ldout = lds;
+        a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale; a.argmax = argmax;
+        return launched(launch_small_similarity(tt, a, (hipStream_t)stream), "gs_similarity");
+    }
+    GemmArgs a{};
+    a.A = T; a.lda = ldt; a.B = R; a.ldb = ldr; a.C = S; a.ldc = lds; a.M = B; a.N = M; a.K = r;
+    a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale;
+    a.argmax = argmax; a.write_out = S != nullptr;
+    return launched(launch_gemm(tt, rt, GS_F32, false, EPI_SIM, a, (hipStream_t)stream), "gs_similarity");
+}
+
+gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                       const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                       const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
+                       float beta, float *A, int64_t lda, void *O, gs_dtype ot, int64_t ldo,
+                       void *stream) {
+    GS_CHECK(check_sim_common("gs_attention", T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
+    GS_CHECK(check_matrix(A, "A", B, M, lda, GS_F32, false));
+    if (O && !is_batch_type(ot)) return fail(GS_ERR_DTYPE, "gs_attention: O must be f32 or bf16");
+    if (O) GS_CHECK(check_matrix(O, "O", B, r, ldo, ot, false));
+    GS_CHECK(check_overlaps({span(T, B, r, ldt, esize(tt), "T"), span(R, M, r, ldr, esize(rt), "R"),
+                             span(qnorm2, 1, B, B, 4, "qnorm2"), span(cnorm, 1, M, M, 4, "cnorm")},
+                            {span(A, B, M, lda, 4, "A"), span(O, B, r, ldo, O ? esize(ot) : 1, "O")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    hipStream_t s = (hipStream_t)stream;
+    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+        SmallArgs a{};
+        a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = A; a.ldout = lda;
+        a.O = O; a.ldo = ldo; a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE;
+        a.scale = scale; a.beta = beta;
+        return launched(launch_small_attention(tt, O ? ot : GS_F32, a, s), "gs_attention");
+    }
+    GemmArgs a{};
+    a.A = T; a.lda = ldt; a.B = R; a.ldb = ldr; a.C = A; a.ldc = lda; a.M = B; a.N = M; a.K = r;
+    a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale; a.beta = beta;
+    gs_status st = launched(launch_gemm(tt, rt, GS_F32, false, EPI_SOFTMAX, a, s), "gs_attention");
+    if (st != GS_OK || !O) return st;
+    GemmArgs o{};
+    o.A = A; o.lda = lda; o.B = R; o.ldb = ldr; o.C = O; o.ldc = ldo; o.M = B; o.N = r; o.K = M;
+    return launched(launch_gemm(GS_F32, rt, ot, true, EPI_STORE, o, s), "gs_attention (weighted sum)");
+}
+
+gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                         const void *T2, int64_t ldt2, gs_bind bind,
+                         const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
+                         void *X, gs_dtype xt, int64_t ldx, void *stream) {
+    if (!is_batch_type(tt) || qt != tt || !is_batch_type(xt))
+        return fail(GS_ERR_DTYPE, "gs_reconstruct: T/Q must be both f32 or both bf16 and X f32 or bf16");
+    if (bind != GS_BIND_NONE && bind != GS_BIND_MUL) return fail(GS_ERR_ARG, "gs_reconstruct: unknown bind");
+    if (B < 0 || r < 1 || D < 1) return fail(GS_ERR_SHAPE, "gs_reconstruct: need B >= 0, r >= 1, D >= 1");
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    if (bind == GS_BIND_MUL) GS_CHECK(check_matrix(T2, "T2", B, r, ldt2, tt, false));
+    else if (T2) return fail(GS_ERR_ARG, "gs_reconstruct: T2 given without a bind operator");
+    GS_CHECK(check_matrix(Q, "Q", r, D, ldq, qt, false));
+    GS_CHECK(check_matrix(X, "X", B, D, ldx, xt, false));
+    GS_CHECK(check_overlaps({span(T, B, r, ldt, esize(tt), "T"), span(T2, B, r, ldt2, esize(tt), "T2"),
+                             span(Q, r, D, ldq, esize(qt), "Q")},
+                            {span(X, B, D, ldx, esize(xt), "X")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    GemmArgs a{};
+    a.A = T; a.lda = ldt; a.A2 = T2; a.lda2 = ldt2; a.B = Q; a.ldb = ldq; a.C = X; a.ldc = ldx;
+    a.M = B; a.N = D; a.K = r;
+    return launched(launch_gemm(tt, qt, xt, true, bind == GS_BIND_MUL ? EPI_BIND : EPI_STORE, a,
+                                (hipStream_t)stream), "gs_reconstruct");
+}
+
+}  // extern "C"

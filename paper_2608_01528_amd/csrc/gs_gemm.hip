@@ -1,0 +1,488 @@
+// Dense contractions of the Gram-Space operators on CDNA4 matrix cores.
+//
+//   project      T = X Q^T          (A = X,  B = Q stored N x K)
+//   reconstruct  X = T Q            (A = T,  B = Q stored K x N)
+//   bind         X = (T Q) .* (T2 Q)
+//   prob2vec     T = P R            (A = P,  B = R stored K x N)
+//   similarity   S = scale * T R^T  (A = T,  B = R stored N x K), cosine
+//                normalisation and row argmax fused in the epilogue
+//   attention    A = softmax(beta * S) fused, two passes over the row block
+//
+// Work-group tile 128 x 128, K-step 32, 256 threads = 4 waves in a 2 x 2
+// arrangement, each wave owning a 64 x 64 sub-tile as 2 x 2 blocks of the
+// 32x32x2 fp32 MFMA.  Both operands are staged through LDS k-major
+// ([k][m] / [k][n]), so every MFMA operand read is one conflict-free
+// ds_read_b32 per lane; bf16 operands are widened to fp32 on the way in.
+// The next K-step is fetched into registers while the current one is
+// multiplied (double-buffered LDS, one barrier per K-step).
+#include "gs_internal.h"
+
+namespace gs {
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int NTHR = 256;
+constexpr int LDS_STRIDE = BM + 4;            // floats per k-row of a staged tile
+constexpr int TILE_FLOATS = BK * LDS_STRIDE;  // one staged operand tile
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- loading
+// Each thread moves 16 elements of a tile per K-step.
+
+// Row-oriented operand (A, or B stored N x K): 128 rows x 32 k.  Lane l of
+// wave w takes row (l % 32) + 32 w and the 16 contiguous k starting at
+// 16 (l / 32).
+template <typename T>
+__device__ __forceinline__ void load_rows(const T *__restrict__ base, int64_t ld, int64_t row0,
+                                          int64_t nrows, int64_t k0, int64_t K, bool vec,
+                                          float v[16]) {
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t row = row0 + (l & 31) + 32 * w;
+    const int64_t kb = k0 + 16 * (l >> 5);
+    if (row >= nrows) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = 0.f;
+        return;
+    }
+    const T *p = base + row * ld + kb;
+    if constexpr (sizeof(T) == 4) {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (kb + 4 * q < K) {
+                    f4v t = *reinterpret_cast<const f4v *>(p + 4 * q);
+                    v[4 * q] = t[0]; v[4 * q + 1] = t[1]; v[4 * q + 2] = t[2]; v[4 * q + 3] = t[3];
+                } else {
+                    v[4 * q] = v[4 * q + 1] = v[4 * q + 2] = v[4 * q + 3] = 0.f;
+                }
+            }
+            return;
+        }
+    } else {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                if (kb + 8 * q < K) {
+                    uint4 t = *reinterpret_cast<const uint4 *>(p + 8 * q);
+                    uint32_t ww[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[8 * q + 2 * e] = __uint_as_float(ww[e] << 16);
+                        v[8 * q + 2 * e + 1] = __uint_as_float(ww[e] & 0xffff0000u);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[8 * q + e] = 0.f;
+                }
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = (kb + i < K) ? ld_f32<T>(p, i) : 0.f;
+}
+
+__device__ __forceinline__ void store_rows(float *tile, const float v[16]) {
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int m = (l & 31) + 32 * w;
+    const int kb = 16 * (l >> 5);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tile[(kb + i) * LDS_STRIDE + m] = v[i];
+}
+
+// K-major operand (B stored K x N): 32 k-rows x 128 columns.  Thread t takes
+// k-row t / 8 and the 16 contiguous columns starting at 16 (t % 8).
+template <typename T>
+__device__ __forceinline__ void load_kmajor(const T *__restrict__ base, int64_t ld, int64_t k0,
+                                            int64_t K, int64_t n0, int64_t N, bool vec,
+                                            float v[16]) {
+    const int t = threadIdx.x;
+    const int64_t k = k0 + (t >> 3);
+    const int64_t nb = n0 + 16 * (t & 7);
+    if (k >= K) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v[i] = 0.f;
+        return;
+    }
+    const T *p = base + k * ld + nb;
+    if constexpr (sizeof(T) == 4) {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (nb + 4 * q < N) {
+                    f4v x = *reinterpret_cast<const f4v *>(p + 4 * q);
+                    v[4 * q] = x[0]; v[4 * q + 1] = x[1]; v[4 * q + 2] = x[2]; v[4 * q + 3] = x[3];
+                } else {
+                    v[4 * q] = v[4 * q + 1] = v[4 * q + 2] = v[4 * q + 3] = 0.f;
+                }
+            }
+            return;
+        }
+    } else {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                if (nb + 8 * q < N) {
+                    uint4 x = *reinterpret_cast<const uint4 *>(p + 8 * q);
+                    uint32_t ww[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[8 * q + 2 * e] = __uint_as_float(ww[e] << 16);
+                        v[8 * q + 2 * e + 1] = __uint_as_float(ww[e] & 0xffff0000u);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[8 * q + e] = 0.f;
+                }
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = (nb + i < N) ? ld_f32<T>(p, i) : 0.f;
+}
+
+__device__ __forceinline__ void store_kmajor(float *tile, const float v[16]) {
+    const int t = threadIdx.x;
+    float *p = tile + (t >> 3) * LDS_STRIDE + 16 * (t & 7);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<f4v *>(p + 4 * q) = f4v{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+}
+
+// Row of the output held by accumulator register g of a 32x32 block, for lane l.
+__device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 * (l >> 5) + (g & 3); }
+
+// ------------------------------------------------------------- main loop
+//
+// Computes the 128 x 128 block (m0, n0) of A * Bop into acc (and A2 * Bop into
+// acc2 when TWO).  On return LDS is free for reuse by the caller (a barrier
+// has been passed after the last MFMA read).
+//
+// When SQA, every thread t < 128 also accumulates sum_k A[m0 + t, k]^2 into
+// *sqa; when SQB, every thread t < 128 accumulates sum_k Bop[k, n0 + t]^2.
+template <typename TA, typename TB, bool BNN, bool TWO>
+__device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t n0, bool veca,
+                                          bool vecb, float *lds, f16v acc[2][2], f16v acc2[2][2],
+                                          bool sqa, float *sqa_out, bool sqb, float *sqb_out) {
+    const TA *A = static_cast<const TA *>(g.A);
+    const TA *A2 = static_cast<const TA *>(g.A2);
+    const TB *B = static_cast<const TB *>(g.B);
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+    const int nstage = TWO ? 3 : 2;   // operand tiles per buffer
+    float *buf[2] = {lds, lds + nstage * TILE_FLOATS};
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            acc[i][j] = f16v{};
+            if (TWO) acc2[i][j] = f16v{};
+        }
+    float sa = 0.f, sb = 0.f;
+
+    float va[16], vb[16], va2[16];
+    const int64_t nk = (g.K + BK - 1) / BK;
+    auto fetch = [&](int64_t kt) {
+        load_rows<TA>(A, g.lda, m0, g.M, kt * BK, g.K, veca, va);
+        if (TWO) load_rows<TA>(A2, g.lda2, m0, g.M, kt * BK, g.K, veca, va2);
+        if (BNN) load_kmajor<TB>(B, g.ldb, kt * BK, g.K, n0, g.N, vecb, vb);
+        else load_rows<TB>(B, g.ldb, n0, g.N, kt * BK, g.K, vecb, vb);
+    };
+    auto stash = [&](float *b) {
+        store_rows(b, va);
+        if (BNN) store_kmajor(b + TILE_FLOATS, vb);
+        else store_rows(b + TILE_FLOATS, vb);
+        if (TWO) store_rows(b + 2 * TILE_FLOATS, va2);
+    };
+
+    fetch(0);
+    stash(buf[0]);
+    __syncthreads();
+    for (int64_t kt = 0; kt < nk; ++kt) {
+        float *cur = buf[kt & 1];
+        if (kt + 1 < nk) fetch(kt + 1);
+        const float *As = cur, *Bs = cur + TILE_FLOATS, *As2 = cur + 2 * TILE_FLOATS;
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const int kr = (kk + (l >> 5)) * LDS_STRIDE;
+            float a0 = As[kr + wm + (l & 31)], a1 = As[kr + wm + 32 + (l & 31)];
+            float b0 = Bs[kr + wn + (l & 31)], b1 = Bs[kr + wn + 32 + (l & 31)];
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            if (TWO) {
+                float c0 = As2[kr + wm + (l & 31)], c1 = As2[kr + wm + 32 + (l & 31)];
+                acc2[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(c0, b0, acc2[0][0], 0, 0, 0);
+                acc2[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(c0, b1, acc2[0][1], 0, 0, 0);
+                acc2[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(c1, b0, acc2[1][0], 0, 0, 0);
+                acc2[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(c1, b1, acc2[1][1], 0, 0, 0);
+            }
+        }
+        if (threadIdx.x < 128) {
+            if (sqa) {
+#pragma unroll 8
+                for (int k = 0; k < BK; ++k) { float x = As[k * LDS_STRIDE + threadIdx.x]; sa += x * x; }
+            }
+            if (sqb) {
+#pragma unroll 8
+                for (int k = 0; k < BK; ++k) { float x = Bs[k * LDS_STRIDE + threadIdx.x]; sb += x * x; }
+            }
+        }
+        if (kt + 1 < nk) stash(buf[(kt + 1) & 1]);
+        __syncthreads();
+    }
+    if (threadIdx.x < 128) {
+        if (sqa) *sqa_out = sa;
+        if (sqb) *sqb_out = sb;
+    }
+}
+
+// XCD-aware tile order: work-group ids are dealt to the 8 XCDs round-robin,
+// so logical tile L is given to ids that share an XCD for consecutive L.
+// Consecutive logical tiles share their A row block (n varies fastest), which
+// then stays in that XCD's L2.
+__device__ __forceinline__ int64_t logical_tile(int64_t total) {
+    const int64_t per = (total + 7) / 8;
+    const int64_t w = blockIdx.x;
+    return (w & 7) * per + (w >> 3);
+}
+
+// --------------------------------------------------------- epilogue: store
+
+template <typename TA, typename TB, typename TO, bool BNN, bool BIND>
+__global__ void __launch_bounds__(NTHR) gemm_store_kernel(GemmArgs g, int veca, int vecb) {
+    extern __shared__ float lds[];
+    const int64_t nM = (g.M + BM - 1) / BM, nN = (g.N + BN - 1) / BN;
+    const int64_t L = logical_tile(nM * nN);
+    if (L >= nM * nN) return;
+    const int64_t m0 = (L / nN) * BM, n0 = (L % nN) * BN;
+    f16v acc[2][2], acc2[2][2];
+    const bool sqa = (g.rownorm2 != nullptr) && (n0 == 0);
+    float sa = 0.f, sb = 0.f;
+    block_mma<TA, TB, BNN, BIND>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
+    if (sqa && threadIdx.x < 128 && m0 + threadIdx.x < g.M) g.rownorm2[m0 + threadIdx.x] = sa;
+
+    TO *C = static_cast<TO *>(g.C);
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t col = n0 + wn + 32 * j + (l & 31);
+            if (col >= g.N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t row = m0 + wm + 32 * i + acc_row(r, l);
+                if (row < g.M) {
+                    float v = acc[i][j][r];
+                    if (BIND) v *= acc2[i][j][r];
+                    st_f32<TO>(C, row * g.ldc + col, v);
+                }
+            }
+        }
+}
+
+// ---------------------------------------- epilogue: similarity / softmax
+//
+// One work-group owns a 128-row block and sweeps every 128-column block of
+// the codebook.  Scores of a column block are parked in LDS, where one pair
+// of threads per row folds them into the row's running state: (max, argmax)
+// for similarity, (max, sum of exp) for softmax.  Softmax rows are finished
+// by a second sweep over the row block's outputs, which that same work-group
+// has just written (still in L2).
+
+constexpr int SS_STRIDE = BN + 1;
+
+template <typename TA, typename TB, bool SOFTMAX>
+__global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int veca, int vecb) {
+    extern __shared__ float lds[];
+    float *ss = lds + 2 * 2 * TILE_FLOATS;         // scores [BM][SS_STRIDE]
+    float *rq = ss + BM * SS_STRIDE;               // 1 / ||x|| per row (or 1)
+    float *cn = rq + BM;                           // 1 / ||c|| per column (or 1)
+    const int64_t nM = (g.M + BM - 1) / BM;
+    const int64_t L = logical_tile(nM);
+    if (L >= nM) return;
+    const int64_t m0 = L * BM;
+    const int64_t nN = (g.N + BN - 1) / BN;
+    const int t = threadIdx.x;
+    const int l = t & 63, w = t >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+    float *out = static_cast<float *>(g.C);
+
+    // running row state, identical in both threads of a pair
+    const int prow = t >> 1, half = t & 1;
+    float run_max = -INFINITY, run_sum = 0.f;
+    int run_idx = 0;
+
+    for (int64_t nt = 0; nt < nN; ++nt) {
+        const int64_t n0 = nt * BN;
+        f16v acc[2][2], acc2[2][2];
+        const bool sqa = g.cosine && g.qnorm2 == nullptr && nt == 0;
+        const bool sqb = g.cosine && g.cnorm == nullptr;
+        float sa = 0.f, sb = 0.f;
+        block_mma<TA, TB, false, false>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, sqb, &sb);
+        if (t < 128) {
+            if (nt == 0) {
+                float q = 1.f;
+                if (g.cosine) {
+                    float n2 = g.qnorm2 ? ((m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f) : sa;
+                    q = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+                }
+                rq[t] = q;
+            }
+            float c = 1.f;
+            if (g.cosine) {
+                float cc = g.cnorm ? ((n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f) : sqrtf(sb);
+                c = (cc > 0.f) ? 1.f / cc : 0.f;
+            }
+            cn[t] = c;
+        }
+        __syncthreads();
+        // scores -> LDS and (optionally) global
+        const float mul = SOFTMAX ? g.scale * g.beta : g.scale;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int cl = wn + 32 * j + (l & 31);
+                const int64_t col = n0 + cl;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int rl = wm + 32 * i + acc_row(r, l);
+                    const int64_t row = m0 + rl;
+                    float v = mul * acc[i][j][r] * rq[rl] * cn[cl];
+                    ss[rl * SS_STRIDE + cl] = (col < g.N) ? v : -INFINITY;
+                    if ((SOFTMAX || g.write_out) && row < g.M && col < g.N)
+                        out[row * g.ldc + col] = v;
+                }
+            }
+        __syncthreads();
+        // fold this column block into the running row state
+        const int ncols = (int)((g.N - n0 < BN) ? (g.N - n0) : BN);
+        float bm = -INFINITY, bs = 0.f;
+        int bi = 0;
+        for (int c = half; c < ncols; c += 2) {
+            float v = ss[prow * SS_STRIDE + c];
+            if (v > bm) { bm = v; bi = c; }
+        }
+        if (SOFTMAX) {
+            for (int c = half; c < ncols; c += 2) bs += __expf(ss[prow * SS_STRIDE + c] - bm);
+        }
+        float om = __shfl_xor(bm, 1), os = __shfl_xor(bs, 1);
+        int oi = __shfl_xor(bi, 1);
+        if (SOFTMAX) {
+            float nm = fmaxf(bm, om);
+            float tsum = (bm == -INFINITY ? 0.f : bs * __expf(bm - nm)) +
+                         (om == -INFINITY ? 0.f : os * __expf(om - nm));
+            float m2 = fmaxf(run_max, nm);
+            run_sum = (run_max == -INFINITY ? 0.f : run_sum * __expf(run_max - m2)) +
+                      (nm == -INFINITY ? 0.f : tsum * __expf(nm - m2));
+            run_max = m2;
+        } else {
+            // lowest column index wins a tie
+            if (om > bm || (om == bm && oi < bi)) { bm = om; bi = oi; }
+            if (bm > run_max) { run_max = bm; run_idx = (int)(n0 + bi); }
+        }
+        __syncthreads();   // ss and the staged tiles are reused by the next block
+    }
+
+    if (!SOFTMAX) {
+        if (g.argmax && half == 0 && m0 + prow < g.M) g.argmax[m0 + prow] = run_idx;
+        return;
+    }
+    // second sweep: normalise the row block
+    float *rmax = rq, *rinv = cn;   // reuse
+    if (half == 0) {
+        rmax[prow] = run_max;
+        rinv[prow] = 1.f / run_sum;
+    }
+    __threadfence_block();
+    __syncthreads();
+    const int64_t rows = (g.M - m0 < BM) ? (g.M - m0) : BM;
+    for (int64_t r = 0; r < rows; ++r) {
+        float *orow = out + (m0 + r) * g.ldc;
+        const float mx = rmax[r], iv = rinv[r];
+        for (int64_t c = t; c < g.N; c += NTHR) orow[c] = __expf(orow[c] - mx) * iv;
+    }
+}
+
+// Kernels whose dynamic LDS exceeds the default 64 KiB limit must raise it
+// once before their first launch.
+template <typename K>
+hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const GemmArgs &a, int veca,
+                           int vecb) {
+    if (lds > 65536) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kernel, grid, dim3(NTHR), lds, s, a, veca, vecb);
+    return hipGetLastError();
+}
+
+template <typename TA, typename TB, typename TO>
+hipError_t dispatch_store(bool b_nn, bool bind, const GemmArgs &a, bool veca, bool vecb,
+                          hipStream_t s) {
+    const int64_t nM = (a.M + BM - 1) / BM, nN = (a.N + BN - 1) / BN;
+    const int64_t total = nM * nN;
+    const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
+    const size_t lds = (size_t)2 * (bind ? 3 : 2) * TILE_FLOATS * sizeof(float);
+    if (b_nn) {
+        if (bind) return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, true>, grid, lds, s, a, veca, vecb);
+        return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, false>, grid, lds, s, a, veca, vecb);
+    }
+    if (bind) return launch_with_lds(gemm_store_kernel<TA, TB, TO, false, true>, grid, lds, s, a, veca, vecb);
+    return launch_with_lds(gemm_store_kernel<TA, TB, TO, false, false>, grid, lds, s, a, veca, vecb);
+}
+
+template <typename TA, typename TB>
+hipError_t dispatch_rowsweep(bool softmax, const GemmArgs &a, bool veca, bool vecb, hipStream_t s) {
+    const int64_t nM = (a.M + BM - 1) / BM;
+    const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
+    const size_t lds = ((size_t)4 * TILE_FLOATS + BM * SS_STRIDE + 2 * BM) * sizeof(float);
+    if (softmax) return launch_with_lds(gemm_rowsweep_kernel<TA, TB, true>, grid, lds, s, a, veca, vecb);
+    return launch_with_lds(gemm_rowsweep_kernel<TA, TB, false>, grid, lds, s, a, veca, vecb);
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Vector loads along the contiguous dimension need a 16-byte aligned base, a
+// leading dimension that keeps every row 16-byte aligned, and a contiguous
+// extent that is a whole number of vectors.
+bool vec_ok(const void *p, gs_dtype t, int64_t ld, int64_t extent) {
+    const int64_t per = (t == GS_BF16) ? 8 : 4;
+    return aligned16(p) && (ld % per == 0) && (extent % per == 0);
+}
+
+}  // namespace
+
+hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,
+                       const GemmArgs &a, hipStream_t s) {
+    if (a.M == 0 || a.N == 0) return hipSuccess;
+    bool veca = vec_ok(a.A, ta, a.lda, a.K);
+    if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
+    const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);
+    const bool bf_a = ta == GS_BF16, bf_b = tb == GS_BF16, bf_o = tout == GS_BF16;
+    if (epi == EPI_STORE || epi == EPI_BIND) {
+        const bool bind = epi == EPI_BIND;
+        if (!bf_a && !bf_b && !bf_o) return dispatch_store<float, float, float>(b_nn, bind, a, veca, vecb, s);
+        if (!bf_a && !bf_b && bf_o) return dispatch_store<float, float, bf16_t>(b_nn, bind, a, veca, vecb, s);
+        if (bf_a && bf_b && !bf_o) return dispatch_store<bf16_t, bf16_t, float>(b_nn, bind, a, veca, vecb, s);
+        if (bf_a && bf_b && bf_o) return dispatch_store<bf16_t, bf16_t, bf16_t>(b_nn, bind, a, veca, vecb, s);
+        if (!bf_a && bf_b && !bf_o) return dispatch_store<float, bf16_t, float>(b_nn, bind, a, veca, vecb, s);
+        if (!bf_a && bf_b && bf_o) return dispatch_store<float, bf16_t, bf16_t>(b_nn, bind, a, veca, vecb, s);
+        return hipErrorInvalidValue;
+    }
+    const bool sm = epi == EPI_SOFTMAX;
+    if (!bf_a && !bf_b) return dispatch_rowsweep<float, float>(sm, a, veca, vecb, s);
+    if (bf_a && bf_b) return dispatch_rowsweep<bf16_t, bf16_t>(sm, a, veca, vecb, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace gs

@@ -1,0 +1,103 @@
+// Internal declarations shared by the HIP translation units of the Gram-Space
+// library.  Not part of the public ABI (that is include/gramspace.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gramspace.h"
+
+namespace gs {
+
+// ------------------------------------------------------------ element types
+
+// bfloat16 is carried as its 16-bit pattern; arithmetic is always fp32.
+struct bf16_t { uint16_t bits; };
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// fp64 -> bf16, round to nearest even in one rounding: narrow to fp32 toward
+// zero, fold the discarded bits into the last fp32 bit (round to odd), then
+// round that to bf16.  fp32 keeps 16 more bits than bf16, so the result equals
+// the correctly rounded fp64 -> bf16 conversion.
+__device__ __forceinline__ uint16_t f64_to_bf16(double d) {
+    float f = __double2float_rz(d);
+    if ((double)f != d) f = __uint_as_float(__float_as_uint(f) | 1u);
+    return f32_to_bf16(f);
+}
+
+template <typename T> __device__ __forceinline__ float ld_f32(const T *p, int64_t i);
+template <> __device__ __forceinline__ float ld_f32<float>(const float *p, int64_t i) { return p[i]; }
+template <> __device__ __forceinline__ float ld_f32<bf16_t>(const bf16_t *p, int64_t i) {
+    return bf16_to_f32(p[i].bits);
+}
+
+template <typename T> __device__ __forceinline__ void st_f32(T *p, int64_t i, float v);
+template <> __device__ __forceinline__ void st_f32<float>(float *p, int64_t i, float v) { p[i] = v; }
+template <> __device__ __forceinline__ void st_f32<bf16_t>(bf16_t *p, int64_t i, float v) {
+    p[i].bits = f32_to_bf16(v);
+}
+
+// --------------------------------------------------------- launch plumbing
+
+enum Epi { EPI_STORE = 0, EPI_BIND = 1, EPI_SIM = 2, EPI_SOFTMAX = 3 };
+
+// One dense contraction  out[m, n] = sum_k A[m, k] * Bop[k, n]  with fp32
+// accumulation on MFMA.  B is stored either N x K (b_nn = false: Bop = B^T)
+// or K x N (b_nn = true).  The epilogue decides what is written.
+struct GemmArgs {
+    const void *A; int64_t lda;
+    const void *A2; int64_t lda2;      // second left operand (EPI_BIND)
+    const void *B; int64_t ldb;
+    void *C; int64_t ldc;              // output (float for SIM / SOFTMAX)
+    int64_t M, N, K;
+    float *rownorm2;                   // EPI_STORE: sum_k A[m,k]^2, nullable
+    const float *qnorm2;               // SIM / SOFTMAX, nullable
+    const float *cnorm;                // SIM / SOFTMAX, nullable
+    int cosine;
+    float scale;
+    float beta;
+    int32_t *argmax;                   // EPI_SIM, nullable
+    int write_out;                     // EPI_SIM: write scores to C
+};
+
+hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,
+                       const GemmArgs &a, hipStream_t s);
+
+// Small-codebook streaming kernels (M <= SMALL_MAX and r <= SMALL_MAX).
+constexpr int SMALL_MAX = 32;
+
+struct SmallArgs {
+    const void *In; int64_t ldin;      // P (prob2vec) or T (similarity / attention)
+    const void *R; int64_t ldr;        // M x r
+    int64_t B, M, r;
+    void *Out; int64_t ldout;          // T (prob2vec); S (similarity); A (attention)
+    void *O; int64_t ldo;              // attention weighted sum, nullable
+    const float *qnorm2, *cnorm;
+    int cosine;
+    float scale, beta;
+    int32_t *argmax;
+};
+
+hipError_t launch_small_prob2vec(gs_dtype tin, gs_dtype tout, const SmallArgs &a, hipStream_t s);
+hipError_t launch_small_similarity(gs_dtype tin, const SmallArgs &a, hipStream_t s);
+hipError_t launch_small_attention(gs_dtype tin, gs_dtype to, const SmallArgs &a, hipStream_t s);
+
+// Compression.
+size_t compress_workspace(int64_t M, int64_t D);
+hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                        void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
+                        int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite,
+                        void *ws, hipStream_t s);
+
+}  // namespace gs

@@ -1,0 +1,235 @@
+"""Thin ctypes binding of the Gram-Space C ABI (include/gramspace.h).
+
+Two layers with the C names:
+
+* `lib()` returns the loaded shared library; its `gs_*` functions take raw
+  pointers exactly as declared in the header.
+* `gs_compress`, `gs_project`, `gs_prob2vec`, `gs_similarity`,
+  `gs_attention`, `gs_reconstruct` below take torch tensors on the current
+  GPU, allocate the outputs with torch, and pass pointers, sizes and the
+  current stream to the library.  They only marshal arguments: every step of
+  the computation runs in the library's HIP kernels.
+
+Loading fails loudly (GramSpaceError) when libgramspace.so has not been
+built; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgramspace.so")
+
+GS_OK, GS_ERR_ARG, GS_ERR_SHAPE, GS_ERR_DTYPE, GS_ERR_ALIGN, GS_ERR_WORKSPACE, \
+    GS_ERR_NUMERIC, GS_ERR_DEVICE = range(8)
+STATUS_NAMES = ["GS_OK", "GS_ERR_ARG", "GS_ERR_SHAPE", "GS_ERR_DTYPE", "GS_ERR_ALIGN",
+                "GS_ERR_WORKSPACE", "GS_ERR_NUMERIC", "GS_ERR_DEVICE"]
+GS_F32, GS_BF16, GS_F64 = 0, 1, 2
+GS_SIM_DOT, GS_SIM_COSINE = 0, 1
+GS_BIND_NONE, GS_BIND_MUL = 0, 1
+
+_DT = {torch.float32: GS_F32, torch.bfloat16: GS_BF16, torch.float64: GS_F64}
+
+
+class GramSpaceError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        self.status = status
+        name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__("%s: %s" % (name, msg))
+
+
+_lib = None
+
+_vp, _i64, _i32p, _fp = ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p
+_SIGS = {
+    "gs_abi_version": ([], ctypes.c_int),
+    "gs_last_error": ([], ctypes.c_char_p),
+    "gs_compress_workspace": ([_i64, _i64], ctypes.c_size_t),
+    "gs_compress": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double,
+                     _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
+                     _vp, _vp, _i32p, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "gs_project": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                    _vp, ctypes.c_int, _i64, _vp, _vp], ctypes.c_int),
+    "gs_prob2vec": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                     _vp, ctypes.c_int, _i64, _vp], ctypes.c_int),
+    "gs_similarity": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                       _vp, _vp, ctypes.c_int, ctypes.c_float, _vp, _i64, _vp, _vp], ctypes.c_int),
+    "gs_attention": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                      _vp, _vp, ctypes.c_int, ctypes.c_float, ctypes.c_float, _vp, _i64,
+                      _vp, ctypes.c_int, _i64, _vp], ctypes.c_int),
+    "gs_reconstruct": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ctypes.c_int,
+                        _vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _i64, _vp], ctypes.c_int),
+}
+
+
+def lib():
+    """The loaded libgramspace.so (raises GramSpaceError if it is not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise GramSpaceError(GS_ERR_DEVICE, "libgramspace.so is not built (run "
+                                 "paper_2608_01528_amd/build.py or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != GS_OK:
+        raise GramSpaceError(status, lib().gs_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _mat(t: torch.Tensor, name: str):
+    if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
+        raise ValueError("%s must be a 2-D row-major tensor (unit column stride)" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must be on the GPU" % name)
+    if t.dtype not in _DT:
+        raise ValueError("%s: unsupported dtype %s" % (name, t.dtype))
+    return _DT[t.dtype], max(t.stride(0), t.size(1))
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _mode(mode):
+    if mode in ("cosine", GS_SIM_COSINE):
+        return GS_SIM_COSINE
+    if mode in ("dot", GS_SIM_DOT):
+        return GS_SIM_DOT
+    raise ValueError("mode must be 'cosine' or 'dot'")
+
+
+def compress_workspace_bytes(M: int, D: int) -> int:
+    return int(lib().gs_compress_workspace(M, D))
+
+
+def gs_compress(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dtype=torch.float64,
+                workspace: torch.Tensor | None = None):
+    """Compress codebook C (M x D).  Returns (Q, R, rank, kept, cnorm) with
+    Q rank x D, R M x rank, kept int32[rank], cnorm float32[M] (all views of
+    full-capacity buffers)."""
+    ct, ldc = _mat(C, "C")
+    M, D = C.shape
+    dev = C.device
+    Q = torch.empty((M, D), dtype=q_dtype, device=dev)
+    R = torch.empty((M, M), dtype=r_dtype, device=dev)
+    kept = torch.empty(M, dtype=torch.int32, device=dev)
+    cnorm = torch.empty(M, dtype=torch.float32, device=dev)
+    need = compress_workspace_bytes(M, D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1) + 256, dtype=torch.uint8, device=dev)
+    base = workspace.data_ptr()
+    off = (-base) % 256
+    rank = ctypes.c_int32(0)
+    _check(lib().gs_compress(_ptr(C), ct, M, D, ldc, float(tol), _ptr(Q), _DT[q_dtype], D,
+                             _ptr(R), _DT[r_dtype], M, _ptr(kept), _ptr(cnorm), ctypes.byref(rank),
+                             ctypes.c_void_p(base + off), workspace.numel() - off, _stream()))
+    r = rank.value
+    return Q[:r], R[:, :r], r, kept[:r], cnorm
+
+
+def gs_project(X: torch.Tensor, Q: torch.Tensor, out_dtype=None, xnorm2: bool = False,
+               out: torch.Tensor | None = None, xnorm2_out: torch.Tensor | None = None):
+    """T = X Q^T (and ||x_b||^2 if xnorm2)."""
+    xt, ldx = _mat(X, "X")
+    qt, ldq = _mat(Q, "Q")
+    B, D = X.shape
+    r = Q.shape[0]
+    if out is None:
+        out = torch.empty((B, r), dtype=out_dtype or X.dtype, device=X.device)
+    tt, ldt = _mat(out, "T")
+    xn = None
+    if xnorm2:
+        xn = xnorm2_out if xnorm2_out is not None else torch.empty(B, dtype=torch.float32, device=X.device)
+    _check(lib().gs_project(_ptr(X), xt, B, D, ldx, _ptr(Q), qt, r, ldq, _ptr(out), tt, ldt,
+                            _ptr(xn), _stream()))
+    return (out, xn) if xnorm2 else out
+
+
+def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Tensor | None = None):
+    """T = P R: Gram-loc of sum_j P[b, j] c_j."""
+    pt, ldp = _mat(P, "P")
+    rt, ldr = _mat(R, "R")
+    B, M = P.shape
+    r = R.shape[1]
+    if out is None:
+        out = torch.empty((B, r), dtype=out_dtype or P.dtype, device=P.device)
+    tt, ldt = _mat(out, "T")
+    _check(lib().gs_prob2vec(_ptr(P), pt, B, M, ldp, _ptr(R), rt, r, ldr, _ptr(out), tt, ldt, _stream()))
+    return out
+
+
+def gs_similarity(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode="cosine",
+                  scale: float = 1.0, scores: bool = True, argmax: bool = True,
+                  out: torch.Tensor | None = None, argmax_out: torch.Tensor | None = None):
+    """Scores S (B x M, fp32) and row argmax (int32) of T against R."""
+    tt, ldt = _mat(T, "T")
+    rt, ldr = _mat(R, "R")
+    B, r = T.shape
+    M = R.shape[0]
+    S = None
+    if scores:
+        S = out if out is not None else torch.empty((B, M), dtype=torch.float32, device=T.device)
+    idx = None
+    if argmax:
+        idx = argmax_out if argmax_out is not None else torch.empty(B, dtype=torch.int32, device=T.device)
+    lds = _mat(S, "S")[1] if S is not None else M
+    _check(lib().gs_similarity(_ptr(T), tt, B, r, ldt, _ptr(R), rt, M, ldr, _ptr(qnorm2), _ptr(cnorm),
+                               _mode(mode), float(scale), _ptr(S), lds, _ptr(idx), _stream()))
+    return S, idx
+
+
+def gs_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode="cosine",
+                 scale: float = 1.0, beta: float = 1.0, weighted_sum: bool = False, out_dtype=None,
+                 out: torch.Tensor | None = None, o_out: torch.Tensor | None = None):
+    """Attention weights A = softmax(beta * S) (B x M, fp32) and optionally the
+    weighted sum O = A R (B x r)."""
+    tt, ldt = _mat(T, "T")
+    rt, ldr = _mat(R, "R")
+    B, r = T.shape
+    M = R.shape[0]
+    A = out if out is not None else torch.empty((B, M), dtype=torch.float32, device=T.device)
+    _, lda = _mat(A, "A")
+    O, ot, ldo = None, GS_F32, r
+    if weighted_sum:
+        O = o_out if o_out is not None else torch.empty((B, r), dtype=out_dtype or T.dtype, device=T.device)
+        ot, ldo = _mat(O, "O")
+    _check(lib().gs_attention(_ptr(T), tt, B, r, ldt, _ptr(R), rt, M, ldr, _ptr(qnorm2), _ptr(cnorm),
+                              _mode(mode), float(scale), float(beta), _ptr(A), lda, _ptr(O), ot, ldo,
+                              _stream()))
+    return A, O
+
+
+def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = None, bind=None,
+                   out_dtype=None, out: torch.Tensor | None = None):
+    """X = T Q, or (T Q) .* (T2 Q) with bind='mul'."""
+    tt, ldt = _mat(T, "T")
+    qt, ldq = _mat(Q, "Q")
+    B, r = T.shape
+    D = Q.shape[1]
+    b = GS_BIND_NONE
+    ldt2 = r
+    if bind in ("mul", GS_BIND_MUL):
+        b = GS_BIND_MUL
+        _, ldt2 = _mat(T2, "T2")
+    elif bind not in (None, "none", GS_BIND_NONE):
+        raise ValueError("bind must be None or 'mul'")
+    if out is None:
+        out = torch.empty((B, D), dtype=out_dtype or T.dtype, device=T.device)
+    xt, ldx = _mat(out, "X")
+    _check(lib().gs_reconstruct(_ptr(T), tt, B, r, ldt, _ptr(T2), ldt2, b, _ptr(Q), qt, D, ldq,
+                                _ptr(out), xt, ldx, _stream()))
+    return out

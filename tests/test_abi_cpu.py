@@ -1,0 +1,184 @@
+"""Host-side tests of the C ABI: the library loads, exports every function the
+header declares, and rejects invalid arguments before any device work.
+
+Fake pointers are used only for calls that must fail validation (or, with no
+GPU present, the device check), so nothing here ever reaches a kernel.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2608_01528_amd import gramspace as gsm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gramspace.h")
+
+P = ctypes.c_void_p
+A1 = P(0x10000)       # distinct, well-aligned fake addresses
+A2 = P(0x20000000)
+A3 = P(0x40000000)
+A4 = P(0x60000000)
+WS = P(0x80000000)
+NULL = None
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(gs_\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return gsm.lib()
+
+
+def err(L):
+    return L.gs_last_error().decode()
+
+
+def test_exports_every_declared_function(L):
+    names = header_functions()
+    assert set(names) >= {"gs_compress", "gs_project", "gs_prob2vec", "gs_similarity",
+                          "gs_attention", "gs_reconstruct", "gs_last_error", "gs_abi_version",
+                          "gs_compress_workspace"}
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_abi_version_matches_header(L):
+    v = int(re.search(r"#define GS_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert L.gs_abi_version() == v
+
+
+def test_workspace_size(L):
+    assert L.gs_compress_workspace(0, 10) == 0
+    assert L.gs_compress_workspace(11, 10) == 0          # D < M unsupported
+    a = L.gs_compress_workspace(10, 1024)
+    b = L.gs_compress_workspace(2048, 16384)
+    assert 0 < a < b
+    assert b >= 2048 * 16384 * 8                          # fp64 master basis
+
+
+def compress(L, C=A1, ct=gsm.GS_F32, M=10, D=64, ldc=64, tol=1e-10, Q=A2, qt=gsm.GS_F64, ldq=64,
+             R=A3, rt=gsm.GS_F64, ldr=10, kept=NULL, cnorm=NULL, rank=True, ws=WS, wsb=None):
+    rk = ctypes.c_int32(0)
+    if wsb is None:
+        wsb = L.gs_compress_workspace(M, D) if 1 <= M <= D else 1 << 20
+    return L.gs_compress(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm,
+                         ctypes.byref(rk) if rank else None, ws, wsb, None)
+
+
+def test_compress_validation(L):
+    assert compress(L, ct=7) == gsm.GS_ERR_DTYPE
+    assert compress(L, rank=False) == gsm.GS_ERR_ARG
+    assert compress(L, M=0) == gsm.GS_ERR_SHAPE
+    assert compress(L, M=65, ldr=65) == gsm.GS_ERR_SHAPE and "partitioned" in err(L)
+    assert compress(L, tol=1.5) == gsm.GS_ERR_ARG
+    assert compress(L, tol=float("nan")) == gsm.GS_ERR_ARG
+    assert compress(L, C=NULL) == gsm.GS_ERR_ARG and "C" in err(L)
+    assert compress(L, ldc=63) == gsm.GS_ERR_SHAPE
+    assert compress(L, ldr=9) == gsm.GS_ERR_SHAPE and "R" in err(L)
+    assert compress(L, Q=P(0x20000004)) == gsm.GS_ERR_ALIGN            # f64 needs 8 bytes
+    assert compress(L, ws=NULL) == gsm.GS_ERR_WORKSPACE
+    assert compress(L, ws=P(0x80000010)) == gsm.GS_ERR_ALIGN
+    assert compress(L, wsb=100) == gsm.GS_ERR_WORKSPACE and "needed" in err(L)
+    assert compress(L, Q=A1) == gsm.GS_ERR_ARG and "overlaps" in err(L)   # output aliases input
+    assert compress(L, kept=P(0x20000000 + 8)) == gsm.GS_ERR_ARG            # kept inside Q
+
+
+def test_project_validation(L):
+    f = L.gs_project
+    # dtype mismatch X f32 / Q bf16
+    assert f(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_BF16, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_DTYPE
+    assert f(A1, gsm.GS_F64, 4, 8, 8, A2, gsm.GS_F64, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_DTYPE
+    assert f(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 0, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_SHAPE
+    assert f(A1, gsm.GS_F32, 4, 8, 7, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_SHAPE
+    assert f(NULL, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_ARG
+    assert f(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 2, 8, P(0x10004), gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_ARG
+    assert f(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, P(0x40000002), NULL) == gsm.GS_ERR_ALIGN
+    # xnorm2 overlapping T
+    assert f(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, P(0x40000008), NULL) == gsm.GS_ERR_ARG
+    # empty batch is a valid no-op that touches nothing
+    assert f(A1, gsm.GS_F32, 0, 8, 8, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_OK
+    assert err(L) == ""
+
+
+def test_prob2vec_validation(L):
+    f = L.gs_prob2vec
+    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 6, 6, A3, gsm.GS_F32, 6, NULL) == gsm.GS_ERR_SHAPE  # r > M
+    assert f(A1, gsm.GS_BF16, 4, 5, 5, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE
+    assert f(A1, gsm.GS_F32, 4, 5, 4, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_SHAPE
+    assert f(A1, gsm.GS_F32, -1, 5, 5, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_SHAPE
+    assert f(A1, gsm.GS_F32, 0, 5, 5, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_OK
+
+
+def test_similarity_validation(L):
+    f = L.gs_similarity
+    ok = dict(T=A1, tt=gsm.GS_F32, B=4, r=5, ldt=5, R=A2, rt=gsm.GS_F32, M=5, ldr=5, qn=NULL, cn=NULL,
+              mode=gsm.GS_SIM_COSINE, scale=1.0, S=A3, lds=5, am=A4)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["T"], a["tt"], a["B"], a["r"], a["ldt"], a["R"], a["rt"], a["M"], a["ldr"], a["qn"],
+                 a["cn"], a["mode"], a["scale"], a["S"], a["lds"], a["am"], NULL)
+
+    assert call(mode=3) == gsm.GS_ERR_ARG
+    assert call(S=NULL, am=NULL) == gsm.GS_ERR_ARG
+    assert call(lds=4) == gsm.GS_ERR_SHAPE
+    assert call(am=P(0x60000001)) == gsm.GS_ERR_ALIGN
+    assert call(am=P(0x40000004)) == gsm.GS_ERR_ARG          # argmax inside S
+    assert call(S=A1) == gsm.GS_ERR_ARG                      # S aliases T
+    assert call(r=6) == gsm.GS_ERR_SHAPE
+    assert call(B=0) == gsm.GS_OK
+
+
+def test_attention_and_reconstruct_validation(L):
+    f = L.gs_attention
+    base = [A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0, 2.0]
+    assert f(*base, NULL, 5, NULL, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_ARG           # A required
+    assert f(*base, A3, 5, A4, gsm.GS_F64, 5, NULL) == gsm.GS_ERR_DTYPE            # O f64
+    assert f(*base, A3, 5, A4, gsm.GS_F32, 4, NULL) == gsm.GS_ERR_SHAPE            # ldo < r
+    assert f(*base, A3, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_ARG              # O aliases A
+    g = L.gs_reconstruct
+    assert g(A1, gsm.GS_F32, 4, 5, 5, NULL, 5, gsm.GS_BIND_MUL, A2, gsm.GS_F32, 16, 16, A3, gsm.GS_F32, 16,
+             NULL) == gsm.GS_ERR_ARG                                               # T2 missing
+    assert g(A1, gsm.GS_F32, 4, 5, 5, A4, 5, gsm.GS_BIND_NONE, A2, gsm.GS_F32, 16, 16, A3, gsm.GS_F32, 16,
+             NULL) == gsm.GS_ERR_ARG                                               # T2 without bind
+    assert g(A1, gsm.GS_F32, 4, 5, 5, NULL, 5, 9, A2, gsm.GS_F32, 16, 16, A3, gsm.GS_F32, 16,
+             NULL) == gsm.GS_ERR_ARG
+    assert g(A1, gsm.GS_F32, 4, 5, 5, NULL, 5, gsm.GS_BIND_NONE, A2, gsm.GS_BF16, 16, 16, A3, gsm.GS_F32, 16,
+             NULL) == gsm.GS_ERR_DTYPE
+    assert g(A1, gsm.GS_F32, 4, 5, 5, NULL, 5, gsm.GS_BIND_NONE, A2, gsm.GS_F32, 16, 16, A3, gsm.GS_F32, 15,
+             NULL) == gsm.GS_ERR_SHAPE
+
+
+def test_errors_are_per_thread(L):
+    import threading
+    assert compress(L, ct=7) == gsm.GS_ERR_DTYPE
+    seen = []
+
+    def other():
+        seen.append(err(L))
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen == [""] and "element type" in err(L)
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a GPU is present: valid fake pointers would reach a kernel")
+def test_no_device_is_reported(L):
+    # every argument valid: the only thing missing is a GPU
+    assert L.gs_project(A1, gsm.GS_F32, 4, 8, 8, A2, gsm.GS_F32, 2, 8, A3, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_ERR_DEVICE
+    assert "device" in err(L)
+    assert compress(L) == gsm.GS_ERR_DEVICE
+
+
+def test_python_wrapper_raises_with_status():
+    e = gsm.GramSpaceError(gsm.GS_ERR_SHAPE, "boom")
+    assert e.status == gsm.GS_ERR_SHAPE and "GS_ERR_SHAPE" in str(e)

@@ -1,0 +1,365 @@
+"""GPU parity of every C-ABI call against the fp64 oracle.
+
+Inputs are seeded and synthetic; the oracle's own outputs (Q, R) are fed to
+the GPU calls that need a basis, so each call is checked on its own, and the
+chained cases check the GPU's compress output end to end.  Sizes span several
+128-wide tiles with ragged tails, strided leading dimensions, leading
+dimensions that force the scalar load path, r = 1, B = 1, and B = 0.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_01528_amd import gramspace as gsm
+from paper_2608_01528_amd import workloads as wl
+from tests.gpu_util import TOL_BF16, TOL_F32, check_argmax, dev, host, rowrel
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gsm.lib()
+
+
+def padded(a, pad, dtype=torch.float32):
+    """Device copy of a with `pad` extra columns of leading dimension (a view)."""
+    a = np.asarray(a)
+    full = np.zeros((a.shape[0], a.shape[1] + pad), a.dtype)
+    full[:, : a.shape[1]] = a
+    return dev(full, dtype)[:, : a.shape[1]]
+
+
+def rq_codebook(kind, M, D, seed, dup=0.0):
+    C = (wl.bipolar_codebook if kind == "bipolar" else wl.binary_codebook)(M, D, seed)
+    if dup:
+        C, _, _ = wl.duplicate_rows(C, dup, seed)
+    return C
+
+
+# ---------------------------------------------------------------- compress
+
+COMPRESS = [
+    ("tiny", lambda: rq_codebook("bipolar", 10, 1024, 1)),
+    ("vsa22", lambda: wl.codebook(wl.WORKLOADS["vsa"], 3)),
+    ("bipolar64x2048", lambda: rq_codebook("bipolar", 64, 2048, 3)),
+    ("binary120x1000", lambda: rq_codebook("binary", 120, 1000, 4)),
+    ("dup100x700", lambda: rq_codebook("bipolar", 100, 700, 5, dup=0.1)),
+    ("hadamard64", lambda: wl.hadamard_codebook(64)),
+    ("single", lambda: rq_codebook("bipolar", 1, 100, 6)),
+]
+
+
+def special_rows():
+    C = rq_codebook("binary", 40, 256, 7).astype(np.float32)
+    C[3] = 0
+    C[10] = C[2]
+    C[20] = C[5] + C[6]
+    C[33] = C[1]
+    return C
+
+
+COMPRESS.append(("special_rows", special_rows))
+
+
+@pytest.mark.parametrize("name,make", COMPRESS, ids=[c[0] for c in COMPRESS])
+def test_compress_matches_oracle(name, make):
+    C = np.ascontiguousarray(make(), dtype=np.float32)
+    print("compress case", name, C.shape, flush=True)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    Q, R, r, kept, cnorm = gsm.gs_compress(dev(C))
+    torch.cuda.synchronize()
+    assert r == ro
+    assert list(host(kept).astype(int)) == list(kept_o)
+    Qg, Rg = host(Q), host(R)
+    assert np.abs(Qg - Qo).max() <= 1e-12
+    assert np.abs(Rg - Ro).max() <= 1e-12 * max(1.0, np.abs(Ro).max())
+    # invariants on the GPU's own output: Q Q^T = I, C = R Q
+    assert np.abs(Qg @ Qg.T - np.eye(r)).max() <= 1e-12
+    assert np.abs(Rg @ Qg - C).max() <= 1e-12 * np.abs(C).max()
+    np.testing.assert_allclose(host(cnorm), oracle.row_norms(C), rtol=1e-6)
+
+
+@pytest.mark.parametrize("qt,rt", [(torch.float32, torch.float32), (torch.bfloat16, torch.bfloat16),
+                                   (torch.float32, torch.float64)])
+def test_compress_output_types(qt, rt):
+    C = rq_codebook("binary", 50, 600, 8)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    Q, R, r, kept, cnorm = gsm.gs_compress(dev(C), q_dtype=qt, r_dtype=rt)
+    torch.cuda.synchronize()
+    assert r == ro
+    tq = 1e-6 if qt == torch.float32 else 4e-3
+    tr = 1e-6 if rt != torch.bfloat16 else 4e-3
+    assert rowrel(host(Q), Qo) <= tq
+    assert rowrel(host(R), Ro) <= tr
+
+
+def test_compress_capacity_is_zero_filled():
+    C = rq_codebook("bipolar", 20, 128, 9)
+    C[5] = C[4]
+    Cd = dev(C)
+    Q, R, r, kept, cnorm = gsm.gs_compress(Cd)
+    torch.cuda.synchronize()
+    assert r == 19
+    # the wrapper returns views of full M-row / M-column buffers
+    Qb = torch.as_strided(Q, (20, 128), (128, 1))
+    Rb = torch.as_strided(R, (20, 20), (20, 1))
+    assert float(Qb[19:].abs().max()) == 0.0
+    assert float(Rb[:, 19:].abs().max()) == 0.0
+
+
+def test_compress_rejects_nonfinite():
+    C = rq_codebook("bipolar", 8, 64, 1)
+    C[3, 7] = np.nan
+    with pytest.raises(gsm.GramSpaceError) as e:
+        gsm.gs_compress(dev(C))
+    assert e.value.status == gsm.GS_ERR_NUMERIC
+
+
+# ----------------------------------------------------------------- project
+
+def basis(r, D, seed):
+    C = rq_codebook("bipolar", r, D, seed)
+    Qo, Ro, kept, rr = oracle.compress(C)
+    assert rr == r
+    return C, Qo, Ro
+
+
+@pytest.mark.parametrize("B,D,r,dtype,pad", [
+    (300, 1000, 70, torch.float32, 0),
+    (257, 2048, 130, torch.float32, 8),
+    (64, 512, 1, torch.float32, 0),
+    (1, 96, 33, torch.float32, 0),
+    (333, 1030, 45, torch.float32, 1),     # odd leading dimension: scalar loads
+    (200, 1024, 64, torch.bfloat16, 0),
+    (129, 520, 140, torch.bfloat16, 3),
+])
+def test_project(B, D, r, dtype, pad):
+    print("project", B, D, r, dtype, pad, flush=True)
+    C, Qo, Ro = basis(r, D, 11)
+    X = np.random.default_rng(B).standard_normal((B, D)).astype(np.float32)
+    if dtype == torch.bfloat16:
+        Xin, Qin = wl.round_bf16(X), wl.round_bf16(Qo.astype(np.float32))
+    else:
+        Xin, Qin = X, Qo.astype(np.float32)
+    T, xn = gsm.gs_project(padded(Xin, pad, dtype), padded(Qin, pad, dtype), out_dtype=torch.float32,
+                           xnorm2=True)
+    torch.cuda.synchronize()
+    tol = TOL_F32 if dtype == torch.float32 else TOL_BF16
+    assert rowrel(host(T), oracle.project(X, Qo)) <= tol
+    np.testing.assert_allclose(host(xn), oracle.row_norms(X) ** 2, rtol=tol)
+
+
+def test_project_bf16_output():
+    C, Qo, Ro = basis(40, 700, 12)
+    X = np.random.default_rng(2).standard_normal((150, 700)).astype(np.float32)
+    T = gsm.gs_project(dev(X), dev(Qo), out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert rowrel(host(T), oracle.project(X, Qo)) <= TOL_BF16
+
+
+# ---------------------------------------------------------------- prob2vec
+
+@pytest.mark.parametrize("B,M,D,dup,dtype", [
+    (1000, 22, 1024, 0.0, torch.float32),    # small-codebook kernel
+    (129, 5, 1024, 0.0, torch.float32),
+    (333, 100, 512, 0.0, torch.float32),     # matrix-core path
+    (300, 160, 900, 0.1, torch.float32),     # rank-deficient, r < M
+    (250, 150, 800, 0.0, torch.bfloat16),
+    (260, 20, 256, 0.0, torch.bfloat16),
+])
+def test_prob2vec(B, M, D, dup, dtype):
+    print("prob2vec", B, M, D, dup, dtype, flush=True)
+    C = rq_codebook("bipolar", M, D, M, dup=dup)
+    Qo, Ro, kept, r = oracle.compress(C)
+    P = wl.dirichlet_probs(B, M, 0.5, M)
+    Pin, Rin = (P, Ro.astype(np.float32)) if dtype == torch.float32 else (wl.round_bf16(P), wl.round_bf16(Ro.astype(np.float32)))
+    T = gsm.gs_prob2vec(dev(Pin, dtype), dev(Rin, dtype), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    To = oracle.project(oracle.prob2vec(P, C), Qo)
+    assert rowrel(host(T), To) <= (TOL_F32 if dtype == torch.float32 else TOL_BF16)
+
+
+# -------------------------------------------------- similarity / attention
+
+SIM_CASES = [  # (B, M, D, dup, in_span)
+    (700, 10, 1024, 0.0, True),
+    (513, 22, 1024, 0.0, False),
+    (300, 100, 1000, 0.0, True),
+    (260, 300, 700, 0.1, False),    # r < M, three column blocks, ragged
+]
+
+
+def sim_inputs(B, M, D, dup, in_span, seed=0):
+    C = rq_codebook("bipolar", M, D, 100 + M, dup=dup)
+    Qo, Ro, kept, r = oracle.compress(C)
+    P = wl.dirichlet_probs(B, M, 0.5, seed + M)
+    X = oracle.prob2vec(P, C)
+    if not in_span:
+        X = X + np.sqrt(0.1) * np.random.default_rng(seed).standard_normal(X.shape)
+    To = oracle.project(X, Qo)
+    return C, Qo, Ro, X, To
+
+
+@pytest.mark.parametrize("B,M,D,dup,in_span", SIM_CASES)
+@pytest.mark.parametrize("mode", ["cosine", "dot"])
+def test_similarity(B, M, D, dup, in_span, mode):
+    print("similarity", B, M, D, dup, in_span, mode, flush=True)
+    C, Qo, Ro, X, To = sim_inputs(B, M, D, dup, in_span)
+    scale = 1.0 if mode == "cosine" else 1.0 / math.sqrt(D)
+    qn = dev(oracle.row_norms(X) ** 2) if (mode == "cosine" and not in_span) else None
+    cn = dev(oracle.row_norms(C)) if M > 50 else None
+    S, idx = gsm.gs_similarity(dev(To), dev(Ro), qnorm2=qn, cnorm=cn, mode=mode, scale=scale)
+    torch.cuda.synchronize()
+    So = oracle.similarity(X, C, oracle.COSINE if mode == "cosine" else oracle.DOT, scale)
+    assert rowrel(host(S), So) <= TOL_F32
+    check_argmax(host(idx), So)
+    # argmax alone (no score output) gives the same indices
+    _, idx2 = gsm.gs_similarity(dev(To), dev(Ro), qnorm2=qn, cnorm=cn, mode=mode, scale=scale, scores=False)
+    torch.cuda.synchronize()
+    assert torch.equal(idx, idx2)
+
+
+@pytest.mark.parametrize("B,M,D,dup,in_span", SIM_CASES)
+@pytest.mark.parametrize("beta", [1.0, 16.0])
+def test_attention(B, M, D, dup, in_span, beta):
+    print("attention", B, M, D, dup, in_span, beta, flush=True)
+    C, Qo, Ro, X, To = sim_inputs(B, M, D, dup, in_span, seed=1)
+    qn = dev(oracle.row_norms(X) ** 2) if not in_span else None
+    A, O = gsm.gs_attention(dev(To), dev(Ro), qnorm2=qn, mode="cosine", beta=beta, weighted_sum=True,
+                            out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    Ao = oracle.softmax(oracle.similarity(X, C, oracle.COSINE), beta)
+    assert rowrel(host(A), Ao) <= TOL_F32
+    np.testing.assert_allclose(host(A).sum(1), 1.0, atol=1e-5)
+    Oo = oracle.project(oracle.prob2vec(Ao, C), Qo)
+    assert rowrel(host(O), Oo) <= TOL_F32
+
+
+def test_similarity_bf16():
+    B, M, D = 400, 120, 600
+    C, Qo, Ro, X, To = sim_inputs(B, M, D, 0.0, False, seed=3)
+    qn = oracle.row_norms(X) ** 2
+    Tb, Rb = wl.round_bf16(To.astype(np.float32)), wl.round_bf16(Ro.astype(np.float32))
+    S, idx = gsm.gs_similarity(dev(Tb, torch.bfloat16), dev(Rb, torch.bfloat16), qnorm2=dev(qn), mode="cosine")
+    A, _ = gsm.gs_attention(dev(Tb, torch.bfloat16), dev(Rb, torch.bfloat16), qnorm2=dev(qn), beta=4.0)
+    torch.cuda.synchronize()
+    So = oracle.similarity(X, C, oracle.COSINE)
+    assert rowrel(host(S), So) <= TOL_BF16
+    assert rowrel(host(A), oracle.softmax(So, 4.0)) <= TOL_BF16
+    # argmax: exact against the oracle on the bf16-rounded inputs (coordinates)
+    cn = np.linalg.norm(Rb.astype(np.float64), axis=1)
+    Sb = (Tb.astype(np.float64) @ Rb.astype(np.float64).T) / np.sqrt(qn)[:, None] / cn[None, :]
+    check_argmax(host(idx), Sb)
+
+
+def test_argmax_ties_lowest_index():
+    # identical codebook coordinates give exact ties: the lowest index wins
+    M, r = 40, 8
+    R = np.zeros((M, r), np.float32)
+    R[:, 0] = 1.0
+    R[7:, 1] = 0.5
+    T = np.zeros((300, r), np.float32)
+    T[:, 0] = 1.0
+    for Mm in (M, 12):
+        _, idx = gsm.gs_similarity(dev(T), dev(R[:Mm]), mode="dot", scores=False)
+        torch.cuda.synchronize()
+        assert int(host(idx).max()) == 0
+
+
+# -------------------------------------------------------------- reconstruct
+
+@pytest.mark.parametrize("B,M,D,dtype,pad", [
+    (300, 100, 1000, torch.float32, 0),
+    (130, 33, 4100, torch.float32, 4),
+    (64, 1, 300, torch.float32, 0),
+    (200, 90, 1030, torch.float32, 1),
+    (250, 70, 1024, torch.bfloat16, 0),
+])
+def test_reconstruct(B, M, D, dtype, pad):
+    print("reconstruct", B, M, D, dtype, flush=True)
+    C = rq_codebook("bipolar", M, D, 200 + M)
+    Qo, Ro, kept, r = oracle.compress(C)
+    P = wl.dirichlet_probs(B, M, 0.3, 7)
+    To = P.astype(np.float64) @ Ro          # exact coordinates of P C
+    if dtype == torch.bfloat16:
+        Tin, Qin = wl.round_bf16(To.astype(np.float32)), wl.round_bf16(Qo.astype(np.float32))
+    else:
+        Tin, Qin = To.astype(np.float32), Qo.astype(np.float32)
+    X = gsm.gs_reconstruct(padded(Tin, pad, dtype), padded(Qin, pad, dtype), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert rowrel(host(X), oracle.prob2vec(P, C)) <= (TOL_F32 if dtype == torch.float32 else TOL_BF16)
+
+
+@pytest.mark.parametrize("kind", ["binary", "bipolar"])
+def test_bind_and_reproject(kind):
+    B, M, D = 260, 150, 1100
+    C = rq_codebook(kind, M, D, 300)
+    Qo, Ro, kept, r = oracle.compress(C)
+    Pa = wl.dirichlet_probs(B, M, 0.05, 1)
+    Pb = wl.dirichlet_probs(B, M, 0.05, 2)
+    Ta = dev(oracle.project(oracle.prob2vec(Pa, C), Qo))
+    Tb = dev(oracle.project(oracle.prob2vec(Pb, C), Qo))
+    Y = gsm.gs_reconstruct(Ta, dev(Qo), T2=Tb, bind="mul")
+    torch.cuda.synchronize()
+    Yo = oracle.bind(oracle.prob2vec(Pa, C), oracle.prob2vec(Pb, C))
+    assert rowrel(host(Y), Yo) <= TOL_F32
+    Ty = gsm.gs_project(Y, dev(Qo))
+    torch.cuda.synchronize()
+    assert rowrel(host(Ty), oracle.project(Yo, Qo)) <= TOL_F32
+
+
+def test_bipolar_self_binding_is_ones():
+    C = rq_codebook("bipolar", 30, 512, 5)
+    Qo, Ro, kept, r = oracle.compress(C)
+    T = dev(Ro)                      # coordinates of the codebook itself
+    Y = gsm.gs_reconstruct(T, dev(Qo), T2=T, bind="mul")
+    torch.cuda.synchronize()
+    assert np.abs(host(Y) - 1.0).max() <= 1e-4
+
+
+# ------------------------------------------------------------ end to end
+
+@pytest.mark.parametrize("wname", ["tiny"])
+def test_chain_tiny_workload(wname):
+    w = wl.WORKLOADS[wname]
+    C = wl.codebook(w)
+    P = wl.probabilities(w)
+    Q, R, r, kept, cnorm = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    T = gsm.gs_prob2vec(dev(P), R)
+    S, idx = gsm.gs_similarity(T, R, cnorm=cnorm, mode="cosine")
+    A, _ = gsm.gs_attention(T, R, cnorm=cnorm, beta=16.0)
+    X = gsm.gs_reconstruct(T, Q)
+    torch.cuda.synchronize()
+    V = oracle.prob2vec(P, C)
+    So = oracle.similarity(V, C, oracle.COSINE)
+    assert r == 10
+    assert rowrel(host(S), So) <= TOL_F32
+    check_argmax(host(idx), So)
+    assert rowrel(host(A), oracle.softmax(So, 16.0)) <= TOL_F32
+    assert rowrel(host(X), V) <= TOL_F32
+
+
+def test_empty_batch_is_noop():
+    R = dev(np.eye(4, dtype=np.float32))
+    T = gsm.gs_prob2vec(torch.empty((0, 4), device="cuda"), R)
+    S, idx = gsm.gs_similarity(torch.empty((0, 4), device="cuda"), R)
+    torch.cuda.synchronize()
+    assert T.shape == (0, 4) and S.shape == (0, 4) and idx.shape == (0,)
+
+
+def test_deterministic():
+    C = rq_codebook("binary", 70, 900, 12)
+    a = gsm.gs_compress(dev(C))
+    b = gsm.gs_compress(dev(C))
+    X = dev(np.random.default_rng(0).standard_normal((300, 900)).astype(np.float32))
+    t1 = gsm.gs_project(X, a[0].float())
+    t2 = gsm.gs_project(X, a[0].float())
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+    assert torch.equal(t1, t2)
