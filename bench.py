@@ -1,0 +1,345 @@
+"""Throughput benchmark of the Gram-Space hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload: four bipolar attribute codebooks with M = 5, 6, 10, 22 entries of
+dimension D = 1024 (the VSA-reasoning shape: attribute codebooks of a
+RAVEN-style problem), and for each a batch of 4096 problems x 16 panels =
+65536 probability rows (softmax of N(0, 2) logits).  The codebooks are
+compressed once before timing (compress time is reported).  One step runs,
+for every codebook, probability vectorisation, cosine similarity with argmax
+and the attention-score softmax (beta = 16) on Gram-loc: 262144 queries per
+step, in one fused launch (gs_soft_select).  The same step through the
+separate calls (gs_prob2vec, gs_similarity, gs_attention: 12 launches) is
+timed as well and reported under "extra".
+
+Inputs stay resident in HBM.  Steps cycle through several independent copies
+of the batch (inputs and outputs) so that the working set exceeds the 256 MiB
+Infinity Cache: every step reads its inputs from HBM.  The K timed steps are
+captured in one HIP graph and replayed once, bracketed by device
+synchronisation; each kernel launch inside it is bracketed by HIP events on
+the same stream, which give the kernel's mean launch duration for the
+roofline entry.
+
+The JSON line also carries the oracle's throughput on the host cores for a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "coord-space similarity+prob2vec queries/s and HBM GB/s vs peak; MFMA util"
+wl = None
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--sets", type=int, default=0, help="batch copies to cycle through (0: >= 1 GiB)")
+    ap.add_argument("--beta", type=float, default=16.0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-unfused", action="store_true", help="skip timing the 12-call path")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                    help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE counter CSVs (kernel run, copy calibration) "
+                         "into profiles/traffic_<kernel>_<workload>.json and exit")
+    ap.add_argument("--pmc-kernel", default="soft_select_kernel")
+    ap.add_argument("--pmc-copy-mib", type=int, default=512)
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_01528_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except ValueError:
+        return None
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+class VsaWorkload:
+    """Compressed attribute codebooks and `nsets` copies of the batch."""
+
+    def __init__(self, w, nsets, torch, gsm):
+        dev = torch.device("cuda:0")
+        self.w = w
+        self.books = []
+        self.compress_ms = []
+        for i, M in enumerate(w.Ms):
+            C = torch.from_numpy(wl.codebook(w, i)).to(dev)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=torch.float32, r_dtype=torch.float32)
+            torch.cuda.synchronize()
+            self.compress_ms.append((time.perf_counter() - t0) * 1e3)
+            R = R.contiguous()
+            P0 = torch.from_numpy(wl.probabilities(w, i)).to(dev)
+            B = P0.shape[0]
+            sets = []
+            for s in range(nsets):
+                sets.append({
+                    "P": P0 if s == 0 else P0.clone(),
+                    "T": torch.empty((B, r), dtype=torch.float32, device=dev),
+                    "S": torch.empty((B, M), dtype=torch.float32, device=dev),
+                    "argmax": torch.empty(B, dtype=torch.int32, device=dev),
+                    "A": torch.empty((B, M), dtype=torch.float32, device=dev),
+                })
+            self.books.append({"M": M, "r": r, "R": R, "cnorm": cnorm, "sets": sets, "B": B})
+        self.queries = sum(b["B"] for b in self.books)
+
+    def fused_bytes(self):
+        """Algorithmic bytes of one fused launch: read P, R, norms; write T, S,
+        argmax, A."""
+        tot = 0
+        for b in self.books:
+            B, M, r = b["B"], b["M"], b["r"]
+            tot += B * (4 * M + 4 * r + 4 * M + 4 + 4 * M) + 4 * M * r + 4 * M
+        return tot
+
+    def unfused_bytes(self):
+        """Algorithmic bytes of the 12 separate calls (T written, then read twice)."""
+        tot = 0
+        for b in self.books:
+            B, M, r = b["B"], b["M"], b["r"]
+            cb = 4 * M * r + 4 * M
+            tot += (4 * B * M + 4 * B * r + cb) + (4 * B * r + 4 * B * M + 4 * B + cb) + (4 * B * r + 4 * B * M + cb)
+        return tot
+
+
+def cpu_baseline_vsa(w, beta, seconds):
+    """Oracle (dense fp64 in D-space) on a bounded sample of the same workload."""
+    import oracle
+    cores = oracle.threads()
+    rows = 256
+    while True:
+        t0 = time.perf_counter()
+        for i, M in enumerate(w.Ms):
+            C = wl.codebook(w, i)
+            P = wl.probabilities(w, i, B=rows)
+            V = oracle.prob2vec(P, C)
+            S = oracle.similarity(V, C, oracle.COSINE)
+            oracle.argmax(S)
+            oracle.softmax(S, beta)
+        dt = time.perf_counter() - t0
+        if dt >= 0.2 * seconds or rows >= w.B:
+            break
+        rows = min(w.B, int(rows * max(2.0, 0.25 * seconds / max(dt, 1e-3))))
+    q = rows * len(w.Ms)
+    return {"value": q / dt, "unit": "queries/s", "cores": cores, "kind": "oracle",
+            "sample": "%d rows of each of the %d codebooks (%d queries): dense fp64 prob2vec, cosine "
+                      "similarity, argmax and softmax in D = %d; %.2f s" % (rows, len(w.Ms), q, w.D, dt)}
+
+
+def timed_graph(torch, steps, launch_step, stream):
+    """Capture `steps` steps into one HIP graph and replay it once, bracketed
+    by device synchronisation (wall clock) and by HIP events recorded on the
+    replay stream (GPU time).  Returns (wall seconds, GPU ms per step)."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for k in range(steps):
+            launch_step(k)
+    g.replay()                      # warm replay (uploads the graph)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    a.record(stream)
+    g.replay()
+    b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, a.elapsed_time(b) / steps
+
+
+def _counter_kib(path, name_part, counter):
+    """Mean per-dispatch value (KiB) of a counter for kernels whose name holds
+    name_part, from a rocprofv3 counter_collection CSV."""
+    import csv
+    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+            if name_part in r["Kernel_Name"] and r["Counter_Name"] == counter]
+    if not vals:
+        raise SystemExit("no %s records for kernels matching %r in %s" % (counter, name_part, path))
+    return float(np.mean(vals)), len(vals)
+
+
+def pmc_summary(args):
+    """HBM bytes per launch of the kernel: counter KiB x 1024, scaled by the
+    ratio of true to counted bytes of a plain copy of known size."""
+    fetch_csv, write_csv, cf_csv, cw_csv = args.pmc_summary
+    copy_bytes = args.pmc_copy_mib * (1 << 20)
+    f_kib, nf = _counter_kib(fetch_csv, args.pmc_kernel, "FETCH_SIZE")
+    w_kib, nw = _counter_kib(write_csv, args.pmc_kernel, "WRITE_SIZE")
+    cf_kib, _ = _counter_kib(cf_csv, "copy", "FETCH_SIZE")
+    cw_kib, _ = _counter_kib(cw_csv, "copy", "WRITE_SIZE")
+    f_scale = copy_bytes / (cf_kib * 1024.0)
+    w_scale = copy_bytes / (cw_kib * 1024.0)
+    read = f_kib * 1024.0 * f_scale
+    write = w_kib * 1024.0 * w_scale
+    out = {"kernel": args.pmc_kernel, "workload": "vsa", "source_hash": kernel_source_hash(),
+           "hbm_bytes_per_launch": read + write, "read_bytes_per_launch": read, "write_bytes_per_launch": write,
+           "fetch_kib_per_dispatch": f_kib, "write_kib_per_dispatch": w_kib, "dispatches": [nf, nw],
+           "copy_calibration": {"bytes": copy_bytes, "fetch_kib": cf_kib, "write_kib": cw_kib,
+                                "fetch_scale": f_scale, "write_scale": w_scale}}
+    path = os.path.join(ROOT, "profiles", "traffic_%s_vsa.json" % args.pmc_kernel)
+    json.dump(out, open(path, "w"), indent=1)
+    print(json.dumps(out))
+
+
+def main():
+    args = parse()
+    if args.pmc_summary:
+        pmc_summary(args)
+        return
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (--gpus %d requested)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_01528_amd import gramspace as gsm
+    global wl
+    from paper_2608_01528_amd import workloads as wl_mod
+    wl = wl_mod
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    gsm.lib()
+
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        a = torch.ones(n, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 5}))
+        return
+
+    w = wl.WORKLOADS["vsa"]
+    per_set = sum(w.B * (16 * M + 4) for M in w.Ms)
+    nsets = args.sets or max(1, int(np.ceil((1 << 30) / per_set)))
+    work = VsaWorkload(w, nsets, torch, gsm)
+    beta = args.beta
+
+    # fused step: one gs_soft_select launch over the four codebooks
+    prepared = []
+    for s in range(nsets):
+        groups = [{"P": b["sets"][s]["P"], "R": b["R"], "cnorm": b["cnorm"], "T": b["sets"][s]["T"],
+                   "S": b["sets"][s]["S"], "argmax": b["sets"][s]["argmax"], "A": b["sets"][s]["A"]}
+                  for b in work.books]
+        prepared.append(gsm.soft_groups(groups))
+
+    def fused_step(k):
+        gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[k % nsets])
+
+    def unfused_step(k):
+        for b in work.books:
+            d = b["sets"][k % nsets]
+            gsm.gs_prob2vec(d["P"], b["R"], out=d["T"])
+            gsm.gs_similarity(d["T"], b["R"], cnorm=b["cnorm"], mode="cosine", out=d["S"], argmax_out=d["argmax"])
+            gsm.gs_attention(d["T"], b["R"], cnorm=b["cnorm"], mode="cosine", beta=beta, out=d["A"])
+
+    stream = torch.cuda.current_stream()
+    for k in range(args.warmup):
+        fused_step(k)
+        if not args.no_unfused:
+            unfused_step(k)
+    torch.cuda.synchronize()
+
+    wall, launch_ms = timed_graph(torch, args.steps, fused_step, stream)
+    ms_per_step = wall * 1e3 / args.steps
+    qps = work.queries * args.steps / wall
+    bpl = float(work.fused_bytes())
+    achieved = bpl / (launch_ms * 1e-3) / 1e9
+
+    extra = {
+        "timing": "one HIP graph of K fused launches; events on the replay stream",
+        "fused_step_bytes": bpl,
+        "compress_ms": work.compress_ms,
+        "kernel_source_hash": kernel_source_hash(),
+        "buffer_copies": nsets,
+    }
+    if not args.no_unfused:
+        uwall, _ = timed_graph(torch, args.steps, unfused_step, stream)
+        extra["unfused_12_calls_ms_per_step"] = uwall * 1e3 / args.steps
+        extra["unfused_queries_per_s"] = work.queries * args.steps / uwall
+        extra["unfused_step_bytes"] = work.unfused_bytes()
+        extra["unfused_GBps"] = work.unfused_bytes() / (uwall / args.steps) / 1e9
+
+    # hot-cache reference: the fused step on one batch copy (cache resident)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for k in range(args.steps):
+            gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[0])
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    g.replay()
+    torch.cuda.synchronize()
+    extra["hot_cache_ms_per_step"] = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    cpu = None if args.no_cpu else cpu_baseline_vsa(w, beta, args.cpu_seconds)
+    out = {
+        "metric": METRIC,
+        "value": qps,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "vsa: 4 bipolar attribute codebooks M=5,6,10,22, D=1024; 4096 problems x 16 panels "
+                        "= 65536 probability rows each; prob2vec + cosine similarity/argmax + softmax(beta=%g)"
+                        % beta,
+            "codebooks_M": w.Ms, "D": w.D, "rows_per_codebook": w.B, "queries_per_step": work.queries,
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "soft_select_kernel", "call": "gs_soft_select",
+            "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": load_traffic("soft_select_kernel", "vsa"),
+            "bytes_per_launch": bpl, "avg_launch_us": launch_ms * 1e3,
+        },
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -212,6 +212,46 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
                          const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
                          void *X, gs_dtype xt, int64_t ldx, void *stream);
 
+/*
+ * gs_soft_select -- the soft-selection pass (Sec. 3.1: probabilities are
+ * turned into superposed vectors, which are then compared through attention
+ * scores; operators of Sec. 2.2) fused into one launch over up to eight small
+ * codebooks.  For every probability row p of group g:
+ *   t = p R_g                        (probability vectorisation on Gram-loc)
+ *   S[b, j] = scale * sim(t, R_g[j]) (DOT, or COSINE with ||x|| = ||t||: the
+ *                                     superposed vector lies in the span of
+ *                                     the codebook, Sec. 3.2)
+ *   argmax[b] = lowest index of the row maximum of S
+ *   A[b, j] = softmax over j of beta * S[b, j]
+ * It computes what gs_prob2vec, gs_similarity and gs_attention compute on the
+ * same inputs, without storing and re-reading the coordinates in between.
+ *
+ *   groups     HOST array of ngroups descriptors, 1 <= ngroups <= 8; in each,
+ *              1 <= r <= M <= 32, B >= 0, and
+ *     P        in   B x M probabilities, type pt (F32 or BF16), ldp >= M
+ *     R        in   M x r Gram-loc codebook, type pt, ldr >= r
+ *     cnorm    in   float[M] codebook norms (cosine), nullable: ||R_j||
+ *     T        out  B x r coordinates of the superposed vectors, type tt,
+ *                   ldt >= r, nullable
+ *     S        out  float B x M scores, lds >= M, nullable
+ *     argmax   out  int32[B], nullable
+ *     A        out  float B x M attention weights, lda >= M, nullable
+ *   Outputs of all groups must overlap neither each other nor any input.
+ */
+typedef struct {
+    const void *P; int64_t ldp;
+    const void *R; int64_t ldr;
+    const float *cnorm;
+    int64_t B, M, r;
+    void *T; int64_t ldt;
+    float *S; int64_t lds;
+    int32_t *argmax;
+    float *A; int64_t lda;
+} gs_soft_group;
+
+gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, gs_dtype tt,
+                         gs_sim_mode mode, float scale, float beta, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <string>
+#include <vector>
 
 #include "gs_internal.h"
 
@@ -54,12 +55,13 @@ bool overlap(const Span &a, const Span &b) {
 }
 
 // Outputs must overlap neither inputs nor each other.
-gs_status check_overlaps(std::initializer_list<Span> in, std::initializer_list<Span> out) {
-    for (const Span &o : out) {
+gs_status check_overlaps(const std::vector<Span> &in, const std::vector<Span> &out) {
+    for (size_t a = 0; a < out.size(); ++a) {
         for (const Span &i : in)
-            if (overlap(o, i)) return fail(GS_ERR_ARG, "output %s overlaps input %s", o.name, i.name);
-        for (const Span &o2 : out)
-            if (&o2 != &o && overlap(o, o2)) return fail(GS_ERR_ARG, "outputs %s and %s overlap", o.name, o2.name);
+            if (overlap(out[a], i)) return fail(GS_ERR_ARG, "output %s overlaps input %s", out[a].name, i.name);
+        for (size_t b = a + 1; b < out.size(); ++b)
+            if (overlap(out[a], out[b]))
+                return fail(GS_ERR_ARG, "outputs %s and %s overlap", out[a].name, out[b].name);
     }
     return GS_OK;
 }
@@ -95,6 +97,22 @@ gs_status check_device() {
     }
     if (!s) return fail(GS_ERR_DEVICE, "no HIP device is available");
     return GS_OK;
+}
+
+// Compute units of the current device (queried once per process).
+int cu_count() {
+    static std::atomic<int> n{0};
+    int v = n.load();
+    if (v == 0) {
+        int dev = 0, cus = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+            v = cus;
+        else
+            v = 256;
+        n.store(v);
+    }
+    return v;
 }
 
 gs_status launched(hipError_t e, const char *what) {
@@ -222,7 +240,7 @@ gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_
                         const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
                         float *S, int64_t lds, int32_t *argmax, void *stream) {
     GS_CHECK(check_sim_common("gs_similarity", T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
-    if (!S && !argmax) return fail(GS_ERR_ARG, "gs_similarity: S and argmax are both null");
+    if (!S && !argmax && B > 0) return fail(GS_ERR_ARG, "gs_similarity: S and argmax are both null");
     GS_CHECK(check_matrix(S, "S", B, M, lds, GS_F32, true));
     GS_CHECK(check_aligned(argmax, 4, "argmax"));
     GS_CHECK(check_overlaps({span(T, B, r, ldt, esize(tt), "T"), span(R, M, r, ldr, esize(rt), "R"),
@@ -298,6 +316,55 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
     a.M = B; a.N = D; a.K = r;
     return launched(launch_gemm(tt, qt, xt, true, bind == GS_BIND_MUL ? EPI_BIND : EPI_STORE, a,
                                 (hipStream_t)stream), "gs_reconstruct");
+}
+
+gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, gs_dtype tt,
+                         gs_sim_mode mode, float scale, float beta, void *stream) {
+    if (!groups) return fail(GS_ERR_ARG, "gs_soft_select: groups is null");
+    if (ngroups < 1 || ngroups > SOFT_MAX_GROUPS)
+        return fail(GS_ERR_ARG, "gs_soft_select: ngroups must be in [1, %d]", SOFT_MAX_GROUPS);
+    if (!is_batch_type(pt) || !is_batch_type(tt))
+        return fail(GS_ERR_DTYPE, "gs_soft_select: P/R and T must be f32 or bf16");
+    if (mode != GS_SIM_DOT && mode != GS_SIM_COSINE) return fail(GS_ERR_ARG, "gs_soft_select: unknown mode");
+    std::vector<Span> in, out;
+    SoftArgs a{};
+    a.ngroups = ngroups;
+    a.cosine = mode == GS_SIM_COSINE;
+    a.scale = scale;
+    a.beta = beta;
+    int64_t tiles = 0;
+    for (int i = 0; i < ngroups; ++i) {
+        const gs_soft_group &g = groups[i];
+        if (g.B < 0 || g.M < 1 || g.M > SMALL_MAX || g.r < 1 || g.r > g.M)
+            return fail(GS_ERR_SHAPE, "gs_soft_select: group %d needs B >= 0 and 1 <= r <= M <= %d", i, SMALL_MAX);
+        GS_CHECK(check_matrix(g.P, "P", g.B, g.M, g.ldp, pt, false));
+        GS_CHECK(check_matrix(g.R, "R", g.M, g.r, g.ldr, pt, false));
+        GS_CHECK(check_aligned(g.cnorm, 4, "cnorm"));
+        GS_CHECK(check_matrix(g.T, "T", g.B, g.r, g.ldt, tt, true));
+        GS_CHECK(check_matrix(g.S, "S", g.B, g.M, g.lds, GS_F32, true));
+        GS_CHECK(check_matrix(g.A, "A", g.B, g.M, g.lda, GS_F32, true));
+        GS_CHECK(check_aligned(g.argmax, 4, "argmax"));
+        in.push_back(span(g.P, g.B, g.M, g.ldp, esize(pt), "P"));
+        in.push_back(span(g.R, g.M, g.r, g.ldr, esize(pt), "R"));
+        in.push_back(span(g.cnorm, 1, g.M, g.M, 4, "cnorm"));
+        out.push_back(span(g.T, g.B, g.r, g.ldt, esize(tt), "T"));
+        out.push_back(span(g.S, g.B, g.M, g.lds, 4, "S"));
+        out.push_back(span(g.argmax, 1, g.B, g.B, 4, "argmax"));
+        out.push_back(span(g.A, g.B, g.M, g.lda, 4, "A"));
+        SoftGroup &d = a.g[i];
+        d.P = g.P; d.ldp = g.ldp; d.R = g.R; d.ldr = g.ldr; d.cnorm = g.cnorm;
+        d.B = g.B; d.M = g.M; d.r = g.r; d.T = g.T; d.ldt = g.ldt; d.S = g.S; d.lds = g.lds;
+        d.argmax = g.argmax; d.A = g.A; d.lda = g.lda;
+        a.tile_start[i] = tiles;
+        tiles += soft_select_tiles(g.B);
+        a.mb[i] = soft_select_pad(g.M);
+    }
+    a.tile_start[ngroups] = tiles;
+    a.ntiles = tiles;
+    GS_CHECK(check_overlaps(in, out));
+    if (tiles == 0) return ok();
+    GS_CHECK(check_device());
+    return launched(launch_soft_select(pt, tt, a, (hipStream_t)stream), "gs_soft_select");
 }
 
 }  // extern "C"

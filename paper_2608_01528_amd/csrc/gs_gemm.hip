@@ -15,6 +15,9 @@
 // ds_read_b32 per lane; bf16 operands are widened to fp32 on the way in.
 // The next K-step is fetched into registers while the current one is
 // multiplied (double-buffered LDS, one barrier per K-step).
+#include <mutex>
+#include <unordered_set>
+
 #include "gs_internal.h"
 
 namespace gs {
@@ -412,14 +415,23 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
     }
 }
 
-// Kernels whose dynamic LDS exceeds the default 64 KiB limit must raise it
-// once before their first launch.
+// Kernels whose dynamic LDS exceeds the default 64 KiB limit raise it once,
+// before their first launch (never inside a stream capture of a later call).
+hipError_t allow_lds(const void *kernel, size_t lds) {
+    static std::mutex mu;
+    static std::unordered_set<const void *> done;
+    std::lock_guard<std::mutex> lock(mu);
+    if (done.count(kernel)) return hipSuccess;
+    hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess) done.insert(kernel);
+    return e;
+}
+
 template <typename K>
 hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const GemmArgs &a, int veca,
                            int vecb) {
     if (lds > 65536) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipError_t e = allow_lds(reinterpret_cast<const void *>(kernel), lds);
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(kernel, grid, dim3(NTHR), lds, s, a, veca, vecb);

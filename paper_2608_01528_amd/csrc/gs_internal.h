@@ -93,6 +93,34 @@ hipError_t launch_small_prob2vec(gs_dtype tin, gs_dtype tout, const SmallArgs &a
 hipError_t launch_small_similarity(gs_dtype tin, const SmallArgs &a, hipStream_t s);
 hipError_t launch_small_attention(gs_dtype tin, gs_dtype to, const SmallArgs &a, hipStream_t s);
 
+// Fused soft selection over up to SOFT_MAX_GROUPS small codebooks.
+constexpr int SOFT_MAX_GROUPS = 8;
+
+struct SoftGroup {
+    const void *P; int64_t ldp;
+    const void *R; int64_t ldr;
+    const float *cnorm;
+    int64_t B, M, r;
+    void *T; int64_t ldt;
+    float *S; int64_t lds;
+    int32_t *argmax;
+    float *A; int64_t lda;
+};
+
+struct SoftArgs {
+    SoftGroup g[SOFT_MAX_GROUPS];
+    int64_t tile_start[SOFT_MAX_GROUPS + 1];    // first work-group (row block) of each group
+    int64_t ntiles;                             // work-groups in total
+    int mb[SOFT_MAX_GROUPS];                    // padded codebook size of each group
+    int ngroups;
+    int cosine;
+    float scale, beta;
+};
+
+int64_t soft_select_tiles(int64_t B);
+int soft_select_pad(int64_t M);
+hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s);
+
 // Compression.
 size_t compress_workspace(int64_t M, int64_t D);
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,

@@ -1,173 +1,503 @@
 // Streaming kernels for small codebooks (M <= 32, r <= 32): probability
-// vectorisation, similarity (+ argmax) and attention score on Gram-loc.
+// vectorisation, similarity (+ argmax), attention score, and the fused
+// soft-selection pass over several codebooks in one launch.
 //
-// At these sizes every output row costs at most M*r multiply-adds against
-// 4(M + r) bytes of traffic, so the kernels are bound by memory traffic and
-// latency, not arithmetic.  Each work-group stages the codebook coordinates R
-// (and their norms) in LDS once, streams a tile of ROWS batch rows through
-// LDS with coalesced loads, computes one row per thread from LDS, and writes
-// the output tile back through LDS with coalesced stores.
+// At these sizes an output row costs at most M*r multiply-adds against
+// 4(M + r) bytes of traffic.  One thread owns one batch row.  Batch tiles move
+// between HBM and LDS with coalesced (vector, when rows are contiguous)
+// accesses; each thread reads its own row from the tile.
+//
+// The codebook coordinates R are widened once per work-group into a
+// zero-padded fp32 MB x MB block in LDS and read as broadcast 16-byte
+// vectors (measured faster here than scalar loads into SGPRs, whose address
+// and latency overhead outweighed the saved LDS traffic).  Loops run to a
+// compile-time bound MB >= M (8, 16, 24 or 32) with padded terms contributing
+// exact zeros.
 #include "gs_internal.h"
 
 namespace gs {
 namespace {
 
-constexpr int ROWS = 128;   // batch rows per work-group = threads per work-group
-constexpr int MAXK = SMALL_MAX;
+constexpr int ROWS = 256;                 // batch rows per work-group (separate calls)
+#ifndef SOFT_RPT
+#define SOFT_RPT 1
+#endif
+constexpr int MAXK = SMALL_MAX;           // 32
 
 enum Mode { MODE_P2V = 0, MODE_SIM = 1, MODE_ATT = 2 };
 
-// Odd row stride of a staged tile of `w` columns: conflict-free when each
-// thread walks its own row.
-__device__ __forceinline__ int odd_stride(int64_t w) { return (int)(w | 1); }
+typedef float f4v __attribute__((ext_vector_type(4)));
 
-template <typename TI, typename TO, int MODE>
-__global__ void __launch_bounds__(ROWS) small_kernel(SmallArgs a) {
-    __shared__ float Rs[MAXK * MAXK];               // R, M x r
-    __shared__ float Rn[MAXK];                      // 1/||c_j|| (cosine) or 1
-    __shared__ float tile_in[ROWS * (MAXK + 1)];
-    __shared__ float tile_out[ROWS * (MAXK + 1)];
-    // attention-weighted sum of a row: written over the thread's own input row
-    // once that row is in registers (input and output rows share the stride)
-    float *tile_o = tile_in;
+__device__ __forceinline__ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Four consecutive elements as fp32 (16-byte aligned fp32, 8-byte aligned bf16).
+__device__ __forceinline__ f4v ld4(const float *p) { return *reinterpret_cast<const f4v *>(p); }
+__device__ __forceinline__ f4v ld4(const bf16_t *p) {
+    const uint2 u = *reinterpret_cast<const uint2 *>(p);
+    return f4v{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+               __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)};
+}
+__device__ __forceinline__ void st4(float *p, f4v v) { *reinterpret_cast<f4v *>(p) = v; }
+__device__ __forceinline__ void st4(bf16_t *p, f4v v) {
+    uint2 u;
+    u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+    u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+    *reinterpret_cast<uint2 *>(p) = u;
+}
+
+// Smallest supported padded size for a codebook of M entries.
+__host__ __device__ __forceinline__ int pad_of(int64_t M) { return M <= 8 ? 8 : M <= 16 ? 16 : M <= 24 ? 24 : 32; }
+
+// ------------------------------------------------------------- tile moves
+//
+// A tile holds rows [b0, b0 + nrow) x [0, w) densely (row stride w): tile
+// element e is matrix element (e / w, e % w).  With contiguous rows
+// (ld == w) and an aligned base, tile and matrix are one linear range moved
+// as 4-element vectors; otherwise element by element with the row and column
+// advanced incrementally.  NT is the number of threads taking part.
+
+template <typename T, int NT>
+__device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, int64_t b0, int nrow, int w,
+                                          float *tile) {
+    const int t = threadIdx.x;
+    const int n = nrow * w;
+    const T *base = g + b0 * ld;
+    if (ld == w && aligned16(base)) {
+        const int n4 = n >> 2;
+        constexpr int V = (NT * MAXK / 4 + NT - 1) / NT;
+        f4v v[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e4 = t + i * NT;
+            if (e4 < n4) v[i] = ld4(base + 4 * e4);
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e4 = t + i * NT;
+            if (e4 < n4) st4(tile + 4 * e4, v[i]);
+        }
+        const int e = 4 * n4 + t;
+        if (e < n) tile[e] = ld_f32<T>(base, e);
+        return;
+    }
+    int row = t / w, col = t - (t / w) * w;
+    const int dq = NT / w, dc = NT - (NT / w) * w;
+    for (int i0 = 0; i0 * NT < n; i0 += 8) {   // 8 loads in flight per chunk
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = t + (i0 + i) * NT;
+            v[i] = (e < n) ? ld_f32<T>(base, (int64_t)row * ld + col) : 0.f;
+            row += dq;
+            col += dc;
+            if (col >= w) { col -= w; ++row; }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = t + (i0 + i) * NT;
+            if (e < n) tile[e] = v[i];
+        }
+    }
+}
+
+template <typename T, int NT>
+__device__ __forceinline__ void tile_store(T *__restrict__ g, int64_t ld, int64_t b0, int nrow, int w,
+                                           const float *tile) {
+    const int t = threadIdx.x;
+    const int n = nrow * w;
+    T *base = g + b0 * ld;
+    if (ld == w && aligned16(base)) {
+        const int n4 = n >> 2;
+        for (int e4 = t; e4 < n4; e4 += NT) st4(base + 4 * e4, *reinterpret_cast<const f4v *>(tile + 4 * e4));
+        const int e = 4 * n4 + t;
+        if (e < n) st_f32<T>(base, e, tile[e]);
+        return;
+    }
+    int row = t / w, col = t - (t / w) * w;
+    const int dq = NT / w, dc = NT - (NT / w) * w;
+    for (int e = t; e < n; e += NT) {
+        st_f32<T>(base, (int64_t)row * ld + col, tile[e]);
+        row += dq;
+        col += dc;
+        if (col >= w) { col -= w; ++row; }
+    }
+}
+
+// --------------------------------------------------- codebook row sources
+
+// Zero-padded MB x MB fp32 block in LDS.
+template <int MB>
+struct LdsRows {
+    const float *Rs;
+    __device__ __forceinline__ void row(int j, float rr[MB]) const {
+        const f4v *p = reinterpret_cast<const f4v *>(Rs + j * MB);
+#pragma unroll
+        for (int q = 0; q < MB / 4; ++q) {
+            const f4v v = p[q];
+            rr[4 * q] = v[0]; rr[4 * q + 1] = v[1]; rr[4 * q + 2] = v[2]; rr[4 * q + 3] = v[3];
+        }
+    }
+};
+
+// Widen the codebook into the padded LDS block.
+template <typename T, int MB, int NT>
+__device__ __forceinline__ void stage_padded(const T *R, int64_t ldr, int M, int r, float *Rs) {
+    for (int e = threadIdx.x; e < MB * MB; e += NT) {
+        const int j = e / MB, k = e - (e / MB) * MB;
+        Rs[e] = (j < M && k < r) ? ld_f32<T>(R, (int64_t)j * ldr + k) : 0.f;
+    }
+}
+
+// Reciprocal codebook norms for cosine scores (ones for dot), zeros beyond M.
+// Without given norms they are ||R_j||, summed in fp32 from the source rows.
+template <typename T, int NT>
+__device__ __forceinline__ void stage_norms(const T *R, int64_t ldr, int M, int r, const float *cnorm,
+                                            bool cosine, int MB, float *Rn) {
+    for (int j = threadIdx.x; j < MB; j += NT) {
+        float c = 0.f;
+        if (j < M) {
+            c = 1.f;
+            if (cosine) {
+                float n;
+                if (cnorm) {
+                    n = cnorm[j];
+                } else {
+                    float s2 = 0.f;
+                    for (int k = 0; k < r; ++k) {
+                        const float v = ld_f32<T>(R, (int64_t)j * ldr + k);
+                        s2 += v * v;
+                    }
+                    n = sqrtf(s2);
+                }
+                c = (n > 0.f) ? 1.f / n : 0.f;
+            }
+        }
+        Rn[j] = c;
+    }
+}
+
+// ---------------------------------------------------------------- row ops
+
+// out[k] = sum_{j < M} p_j R[j, k], p_j read from the thread's own tile row.
+template <int MB, class Rows>
+__device__ __forceinline__ void row_prob2vec(const float *prow, int M, const Rows &R, float out[MB]) {
+#pragma unroll
+    for (int k = 0; k < MB; ++k) out[k] = 0.f;
+#pragma unroll 2
+    for (int j = 0; j < M; ++j) {
+        float rr[MB];
+        R.row(j, rr);
+        const float pj = prow[j];
+#pragma unroll
+        for (int k = 0; k < MB; ++k) out[k] += pj * rr[k];
+    }
+}
+
+// srow[j] = mul * <x, R_j> * q * Rn[j] for j < M, into the thread's own tile
+// row; the row maximum and its lowest index.
+template <int MB, class Rows>
+__device__ __forceinline__ void row_scores(const float x[MB], int M, const Rows &R, const float *Rn, float mul,
+                                           float q, float *srow, float &best, int &bi) {
+    best = -INFINITY;
+    bi = 0;
+#pragma unroll 2
+    for (int j = 0; j < M; ++j) {
+        float rr[MB];
+        R.row(j, rr);
+        float d = 0.f;
+#pragma unroll
+        for (int k = 0; k < MB; ++k) d += x[k] * rr[k];
+        const float sj = mul * d * q * Rn[j];
+        srow[j] = sj;
+        if (sj > best) { best = sj; bi = j; }
+    }
+}
+
+// In-place softmax of f * srow[0..M), given max_j f * srow[j] = mx.
+__device__ __forceinline__ void row_softmax(float *srow, int M, float f, float mx) {
+    float z = 0.f;
+    for (int j = 0; j < M; ++j) {
+        const float e = __expf(f * srow[j] - mx);
+        srow[j] = e;
+        z += e;
+    }
+    const float iz = 1.f / z;
+    for (int j = 0; j < M; ++j) srow[j] *= iz;
+}
+
+template <int MB>
+__device__ __forceinline__ void regs_to_tile(const float v[MB], int w, float *tile) {
+#pragma unroll
+    for (int k = 0; k < MB; ++k)
+        if (k < w) tile[threadIdx.x * w + k] = v[k];
+}
+
+template <int MB>
+__device__ __forceinline__ void tile_to_regs(const float *tile, int w, float v[MB]) {
+#pragma unroll
+    for (int k = 0; k < MB; ++k) v[k] = (k < w) ? tile[threadIdx.x * w + k] : 0.f;
+}
+
+// ------------------------------------------------------- separate calls
+
+template <typename TI, typename TO, int MODE, int MB, class Rows>
+__device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, const float *Rn, float *tile) {
     const int t = threadIdx.x;
     const int64_t b0 = (int64_t)blockIdx.x * ROWS;
     const int M = (int)a.M, r = (int)a.r;
-    const TI *R = static_cast<const TI *>(a.R);
-    const TI *In = static_cast<const TI *>(a.In);
-
-    for (int e = t; e < M * r; e += ROWS) Rs[e] = ld_f32<TI>(R, (int64_t)(e / r) * a.ldr + e % r);
-    // input tile: P rows (width M) or T rows (width r)
-    const int win = (MODE == MODE_P2V) ? M : r;
-    const int sin = odd_stride(win);
-    const int64_t nrow = (a.B - b0 < ROWS) ? (a.B - b0) : ROWS;
-    for (int e = t; e < nrow * win; e += ROWS) {
-        const int row = e / win, col = e % win;
-        tile_in[row * sin + col] = ld_f32<TI>(In, (b0 + row) * a.ldin + col);
-    }
-    __syncthreads();
-    if (MODE != MODE_P2V && t < M) {
-        float c = 1.f;
-        if (a.cosine) {
-            float n;
-            if (a.cnorm) n = a.cnorm[t];
-            else {
-                float s = 0.f;
-                for (int k = 0; k < r; ++k) s += Rs[t * r + k] * Rs[t * r + k];
-                n = sqrtf(s);
-            }
-            c = (n > 0.f) ? 1.f / n : 0.f;
-        }
-        Rn[t] = c;
-    }
-    __syncthreads();
-
-    const int64_t row = b0 + t;
-    const float *x = tile_in + t * sin;
+    const int nrow = (int)((a.B - b0 < ROWS) ? (a.B - b0) : ROWS);
+    float x[MB];
     if (MODE == MODE_P2V) {
-        const int sout = odd_stride(r);
-        if (t < nrow) {
-            float acc[MAXK];
-#pragma unroll
-            for (int k = 0; k < MAXK; ++k) acc[k] = 0.f;
-            for (int j = 0; j < M; ++j) {
-                const float p = x[j];
-#pragma unroll
-                for (int k = 0; k < MAXK; ++k)
-                    if (k < r) acc[k] += p * Rs[j * r + k];
-            }
-#pragma unroll
-            for (int k = 0; k < MAXK; ++k)
-                if (k < r) tile_out[t * sout + k] = acc[k];
-        }
+        row_prob2vec<MB>(tile + t * M, M, R, x);
+        __syncthreads();   // the tile is reused for the outputs
+        regs_to_tile<MB>(x, r, tile);
         __syncthreads();
-        TO *T = static_cast<TO *>(a.Out);
-        for (int e = t; e < nrow * r; e += ROWS) {
-            const int rr = e / r, k = e % r;
-            st_f32<TO>(T, (b0 + rr) * a.ldout + k, tile_out[rr * sout + k]);
-        }
+        tile_store<TO, ROWS>(static_cast<TO *>(a.Out), a.ldout, b0, nrow, r, tile);
         return;
     }
+    tile_to_regs<MB>(tile, r, x);
+    __syncthreads();   // the tile is reused for the outputs
+    float n2 = 0.f;
+#pragma unroll
+    for (int k = 0; k < MB; ++k) n2 += x[k] * x[k];
+    float q = 1.f;
+    if (a.cosine) {
+        if (a.qnorm2 && t < nrow) n2 = a.qnorm2[b0 + t];
+        q = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+    }
+    const float mul = (MODE == MODE_ATT) ? a.scale * a.beta : a.scale;
+    float *srow = tile + t * M;
+    float best;
+    int bi;
+    row_scores<MB>(x, M, R, Rn, mul, q, srow, best, bi);
+    if (MODE == MODE_SIM) {
+        if (a.argmax && t < nrow) a.argmax[b0 + t] = bi;
+        if (!a.Out) return;
+        __syncthreads();
+        tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
+        return;
+    }
+    row_softmax(srow, M, 1.f, best);
+    __syncthreads();
+    tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
+    if (!a.O) return;
+    float o[MB];
+    row_prob2vec<MB>(srow, M, R, o);
+    __syncthreads();
+    regs_to_tile<MB>(o, r, tile);
+    __syncthreads();
+    tile_store<TO, ROWS>(static_cast<TO *>(a.O), a.ldo, b0, nrow, r, tile);
+}
 
-    // similarity / attention: scores of this thread's row against all M codes
-    const int ss = odd_stride(M);
-    if (t < nrow) {
-        float xr[MAXK];
+template <typename TI, typename TO, int MODE, int MB>
+__global__ void __launch_bounds__(ROWS) small_kernel(SmallArgs a) {
+    __shared__ __attribute__((aligned(16))) float tile[ROWS * MAXK];
+    __shared__ __attribute__((aligned(16))) float Rs[MB * MB];
+    __shared__ float Rn[MB];
+    const int64_t b0 = (int64_t)blockIdx.x * ROWS;
+    const int M = (int)a.M, r = (int)a.r;
+    const int nrow = (int)((a.B - b0 < ROWS) ? (a.B - b0) : ROWS);
+    const TI *R = static_cast<const TI *>(a.R);
+    tile_load<TI, ROWS>(static_cast<const TI *>(a.In), a.ldin, b0, nrow, (MODE == MODE_P2V) ? M : r, tile);
+    if (MODE != MODE_P2V) stage_norms<TI, ROWS>(R, a.ldr, M, r, a.cnorm, a.cosine != 0, MB, Rn);
+    stage_padded<TI, MB, ROWS>(R, a.ldr, M, r, Rs);
+    __syncthreads();
+    small_body<TI, TO, MODE, MB>(a, LdsRows<MB>{Rs}, Rn, tile);
+}
+
+// ---------------------------------------------------------------------------
+// Fused soft selection.  A work-group of SROWS threads owns SROWS * RPT
+// consecutive rows of one codebook group; thread t owns rows t, t + SROWS, ...
+// so that every codebook value it reads serves RPT rows.  The probability
+// tile is requested first (vector loads into registers), the codebook block
+// and norms are staged in LDS while those loads are in flight, then the tile
+// goes through LDS to the threads' rows.  Outputs leave through the same LDS
+// tile with coalesced stores.
+
+constexpr int SROWS = 256;               // threads per work-group
+constexpr int RPT = SOFT_RPT;            // rows per thread
+constexpr int SBLK = SROWS * RPT;        // rows per work-group
+
+__device__ __forceinline__ int soft_group(const SoftArgs &a, int64_t blk) {
+    int gi = 0;
+    while (gi + 1 < a.ngroups && blk >= a.tile_start[gi + 1]) ++gi;
+    return gi;
+}
+
+// Row ops over RPT rows at once (row u of thread t lives at tile row
+// t + u * SROWS, row stride M).
+template <int MB, class Rows>
+__device__ __forceinline__ void rows_prob2vec(const float *tile, int M, int r, const Rows &R, float out[RPT][MB]) {
+#pragma unroll
+    for (int q = 0; q < RPT; ++q)
+#pragma unroll
+        for (int k = 0; k < MB; ++k) out[q][k] = 0.f;
+#pragma unroll 2
+    for (int j = 0; j < M; ++j) {
+        float p[RPT];
+#pragma unroll
+        for (int q = 0; q < RPT; ++q) p[q] = tile[(threadIdx.x + q * SROWS) * M + j];
+        float rr[MB];
+        R.row(j, rr);
+#pragma unroll
+        for (int k = 0; k < MB; ++k)
+#pragma unroll
+            for (int q = 0; q < RPT; ++q) out[q][k] += p[q] * rr[k];
+    }
+#pragma unroll
+    for (int q = 0; q < RPT; ++q)
+#pragma unroll
+        for (int k = 0; k < MB; ++k)
+            if (k >= r) out[q][k] = 0.f;
+}
+
+template <int MB, class Rows>
+__device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const Rows &R, const float *Rn,
+                                            float mul, const float q[RPT], float *tile, float best[RPT],
+                                            int bi[RPT]) {
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) { best[u] = -INFINITY; bi[u] = 0; }
+#pragma unroll 2
+    for (int j = 0; j < M; ++j) {
+        float rr[MB];
+        R.row(j, rr);
+        float d[RPT];
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) d[u] = 0.f;
+#pragma unroll
+        for (int k = 0; k < MB; ++k)
+#pragma unroll
+            for (int u = 0; u < RPT; ++u) d[u] += x[u][k] * rr[k];
+        const float rn = Rn[j];
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
+            const float sj = mul * d[u] * q[u] * rn;
+            tile[(threadIdx.x + u * SROWS) * M + j] = sj;
+            if (sj > best[u]) { best[u] = sj; bi[u] = j; }
+        }
+    }
+}
+
+template <typename TI, typename TT, int MB, class Rows>
+__device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow,
+                                           const Rows &Rsrc, const float *Rn, float *tile) {
+    const int t = threadIdx.x;
+    const int M = (int)G.M, r = (int)G.r;
+    float x[RPT][MB];
+    rows_prob2vec<MB>(tile, M, r, Rsrc, x);      // Gram-loc of the superposed vectors
+    float q[RPT];
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
         float n2 = 0.f;
 #pragma unroll
-        for (int k = 0; k < MAXK; ++k) {
-            xr[k] = (k < r) ? x[k] : 0.f;
-            n2 += xr[k] * xr[k];
-        }
-        float q = 1.f;
-        if (a.cosine) {
-            if (a.qnorm2) n2 = a.qnorm2[row];
-            q = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
-        }
-        const float mul = (MODE == MODE_ATT) ? a.scale * a.beta : a.scale;
-        float best = -INFINITY;
-        int bi = 0;
-        for (int j = 0; j < M; ++j) {
-            float d = 0.f;
+        for (int k = 0; k < MB; ++k) n2 += x[u][k] * x[u][k];   // in span: ||v|| = ||t||
+        q[u] = a.cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;
+    }
+    __syncthreads();   // the tile is reused for the outputs
+    if (G.T) {
 #pragma unroll
-            for (int k = 0; k < MAXK; ++k)
-                if (k < r) d += xr[k] * Rs[j * r + k];
-            const float s = mul * d * q * Rn[j];
-            tile_out[t * ss + j] = s;
-            if (s > best) { best = s; bi = j; }
+        for (int u = 0; u < RPT; ++u)
+#pragma unroll
+            for (int k = 0; k < MB; ++k)
+                if (k < r) tile[(t + u * SROWS) * r + k] = x[u][k];
+        __syncthreads();
+        tile_store<TT, SROWS>(static_cast<TT *>(G.T), G.ldt, b0, nrow, r, tile);
+        __syncthreads();
+    }
+    float best[RPT];
+    int bi[RPT];
+    rows_scores<MB>(x, M, Rsrc, Rn, a.scale, q, tile, best, bi);
+    if (G.argmax) {
+#pragma unroll
+        for (int u = 0; u < RPT; ++u)
+            if (t + u * SROWS < nrow) G.argmax[b0 + t + u * SROWS] = bi[u];
+    }
+    if (G.S) {
+        __syncthreads();
+        tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
+    }
+    if (G.A) {
+        // attention weights: softmax of beta times the same scores; the
+        // maximum of beta * s is taken after scaling (beta may be negative)
+        if (G.S) __syncthreads();   // S has left the tile before it is overwritten
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
+            float *srow = tile + (t + u * SROWS) * M;
+            float mx = -INFINITY;
+            for (int j = 0; j < M; ++j) mx = fmaxf(mx, a.beta * srow[j]);
+            row_softmax(srow, M, a.beta, mx);
         }
-        if (MODE == MODE_SIM) {
-            if (a.argmax) a.argmax[row] = bi;
-        } else {
-            float z = 0.f;
-            for (int j = 0; j < M; ++j) {
-                const float e = __expf(tile_out[t * ss + j] - best);
-                tile_out[t * ss + j] = e;
-                z += e;
-            }
-            const float iz = 1.f / z;
-            for (int j = 0; j < M; ++j) tile_out[t * ss + j] *= iz;
-            if (a.O) {
-                const int so = odd_stride(r);
-                float o[MAXK];
+        __syncthreads();
+        tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
+    }
+}
+
+template <typename TI, typename TT>
+__global__ void __launch_bounds__(SROWS) soft_select_kernel(SoftArgs a) {
+    __shared__ __attribute__((aligned(16))) float tile[SBLK * MAXK];
+    __shared__ __attribute__((aligned(16))) float Rs[MAXK * MAXK];
+    __shared__ float Rn[MAXK];
+    const int64_t blk = blockIdx.x;
+    const int gi = soft_group(a, blk);
+    const SoftGroup &G = a.g[gi];
+    const int64_t b0 = (blk - a.tile_start[gi]) * SBLK;
+    const int M = (int)G.M, r = (int)G.r;
+    const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
+    const int MB = a.mb[gi];
+    const TI *P = static_cast<const TI *>(G.P);
+    const TI *R = static_cast<const TI *>(G.R);
+
+    // 1. request the probability tile
+    const TI *base = P + b0 * G.ldp;
+    const bool contig = G.ldp == G.M && aligned16(base);
+    const int n = nrow * M, n4 = n >> 2;
+    constexpr int V = SBLK * MAXK / 4 / SROWS;
+    f4v v[V];
+    if (contig) {
 #pragma unroll
-                for (int k = 0; k < MAXK; ++k) o[k] = 0.f;
-                for (int j = 0; j < M; ++j) {
-                    const float p = tile_out[t * ss + j];
-#pragma unroll
-                    for (int k = 0; k < MAXK; ++k)
-                        if (k < r) o[k] += p * Rs[j * r + k];
-                }
-#pragma unroll
-                for (int k = 0; k < MAXK; ++k)
-                    if (k < r) tile_o[t * so + k] = o[k];
-            }
+        for (int i = 0; i < V; ++i) {
+            const int e4 = threadIdx.x + i * SROWS;
+            if (e4 < n4) v[i] = ld4(base + 4 * e4);
         }
+    }
+    // 2. stage the norms and the padded codebook block while the tile is in
+    // flight
+    stage_norms<TI, SROWS>(R, G.ldr, M, r, G.cnorm, a.cosine != 0, MB, Rn);
+    for (int e = threadIdx.x; e < MB * MB; e += SROWS) {
+        const int j = e / MB, k = e - (e / MB) * MB;
+        Rs[e] = (j < M && k < r) ? ld_f32<TI>(R, (int64_t)j * G.ldr + k) : 0.f;
+    }
+    // 3. tile to LDS
+    if (contig) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e4 = threadIdx.x + i * SROWS;
+            if (e4 < n4) st4(tile + 4 * e4, v[i]);
+        }
+        const int e = 4 * n4 + threadIdx.x;
+        if (e < n) tile[e] = ld_f32<TI>(base, e);
+    } else {
+        tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
     }
     __syncthreads();
-    float *S = static_cast<float *>(a.Out);
-    if (S) {
-        for (int e = t; e < nrow * M; e += ROWS) {
-            const int rr = e / M, j = e % M;
-            S[(b0 + rr) * a.ldout + j] = tile_out[rr * ss + j];
-        }
-    }
-    if (MODE == MODE_ATT && a.O) {
-        const int so = odd_stride(r);
-        TO *O = static_cast<TO *>(a.O);
-        for (int e = t; e < nrow * r; e += ROWS) {
-            const int rr = e / r, k = e % r;
-            st_f32<TO>(O, (b0 + rr) * a.ldo + k, tile_o[rr * so + k]);
-        }
+    switch (MB) {
+        case 8: soft_block<TI, TT, 8>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
+        case 16: soft_block<TI, TT, 16>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
+        case 24: soft_block<TI, TT, 24>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
+        default: soft_block<TI, TT, 32>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
     }
 }
 
 template <typename TI, typename TO, int MODE>
 hipError_t launch(const SmallArgs &a, hipStream_t s) {
     if (a.B == 0) return hipSuccess;
-    const int64_t grid = (a.B + ROWS - 1) / ROWS;
-    hipLaunchKernelGGL((small_kernel<TI, TO, MODE>), dim3(grid), dim3(ROWS), 0, s, a);
+    const dim3 grid((unsigned)((a.B + ROWS - 1) / ROWS)), block(ROWS);
+    switch (pad_of(a.M)) {
+        case 8: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 8>), grid, block, 0, s, a); break;
+        case 16: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 16>), grid, block, 0, s, a); break;
+        case 24: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 24>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 32>), grid, block, 0, s, a); break;
+    }
     return hipGetLastError();
 }
 
@@ -194,5 +524,20 @@ hipError_t launch_small_attention(gs_dtype tin, gs_dtype to, const SmallArgs &a,
     if (tin == GS_BF16 && to == GS_BF16) return launch<bf16_t, bf16_t, MODE_ATT>(a, s);
     return hipErrorInvalidValue;
 }
+
+hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s) {
+    if (a.ntiles == 0) return hipSuccess;
+    const dim3 grid((unsigned)a.ntiles), block(SROWS);
+    if (tin == GS_F32 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<float, float>), grid, block, 0, s, a);
+    else if (tin == GS_F32 && tt == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<float, bf16_t>), grid, block, 0, s, a);
+    else if (tin == GS_BF16 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<bf16_t, float>), grid, block, 0, s, a);
+    else if (tin == GS_BF16 && tt == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<bf16_t, bf16_t>), grid, block, 0, s, a);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+int64_t soft_select_tiles(int64_t B) { return (B + SBLK - 1) / SBLK; }
+
+int soft_select_pad(int64_t M) { return pad_of(M); }
 
 }  // namespace gs

@@ -65,6 +65,17 @@ _SIGS = {
 }
 
 
+class SoftGroup(ctypes.Structure):
+    """Mirror of gs_soft_group."""
+    _fields_ = [("P", _vp), ("ldp", _i64), ("R", _vp), ("ldr", _i64), ("cnorm", _vp),
+                ("B", _i64), ("M", _i64), ("r", _i64), ("T", _vp), ("ldt", _i64),
+                ("S", _vp), ("lds", _i64), ("argmax", _vp), ("A", _vp), ("lda", _i64)]
+
+
+_SIGS["gs_soft_select"] = ([ctypes.POINTER(SoftGroup), ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                            ctypes.c_int, ctypes.c_float, ctypes.c_float, _vp], ctypes.c_int)
+
+
 def lib():
     """The loaded libgramspace.so (raises GramSpaceError if it is not built)."""
     global _lib
@@ -233,3 +244,43 @@ def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = N
     _check(lib().gs_reconstruct(_ptr(T), tt, B, r, ldt, _ptr(T2), ldt2, b, _ptr(Q), qt, D, ldq,
                                 _ptr(out), xt, ldx, _stream()))
     return out
+
+
+def soft_groups(groups):
+    """Build the gs_soft_group array for gs_soft_select from dicts with keys
+    P, R and optionally cnorm, T, S, argmax, A (torch tensors).  Returns the
+    ctypes array and the element types (pt, tt)."""
+    arr = (SoftGroup * len(groups))()
+    pt = tt = None
+    for i, g in enumerate(groups):
+        P, R = g["P"], g["R"]
+        p_t, ldp = _mat(P, "P")
+        _, ldr = _mat(R, "R")
+        pt = p_t
+        d = arr[i]
+        d.P, d.ldp, d.R, d.ldr = P.data_ptr(), ldp, R.data_ptr(), ldr
+        d.cnorm = g["cnorm"].data_ptr() if g.get("cnorm") is not None else None
+        d.B, d.M, d.r = P.shape[0], P.shape[1], R.shape[1]
+        if g.get("T") is not None:
+            t_t, d.ldt = _mat(g["T"], "T")
+            d.T, tt = g["T"].data_ptr(), t_t
+        else:
+            d.T, d.ldt = None, R.shape[1]
+        for key, ld in (("S", "lds"), ("A", "lda")):
+            if g.get(key) is not None:
+                _, l = _mat(g[key], key)
+                setattr(d, key, g[key].data_ptr())
+                setattr(d, ld, l)
+            else:
+                setattr(d, key, None)
+                setattr(d, ld, P.shape[1])
+        d.argmax = g["argmax"].data_ptr() if g.get("argmax") is not None else None
+    return arr, pt, (tt if tt is not None else GS_F32)
+
+
+def gs_soft_select(groups, mode="cosine", scale: float = 1.0, beta: float = 1.0, prepared=None):
+    """Fused prob2vec -> similarity/argmax -> attention over several small
+    codebooks in one launch.  `groups` is a list of dicts (see soft_groups);
+    outputs named in the dicts are written in place."""
+    arr, pt, tt = prepared if prepared is not None else soft_groups(groups)
+    _check(lib().gs_soft_select(arr, len(arr), pt, tt, _mode(mode), float(scale), float(beta), _stream()))

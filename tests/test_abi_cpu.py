@@ -182,3 +182,50 @@ def test_no_device_is_reported(L):
 def test_python_wrapper_raises_with_status():
     e = gsm.GramSpaceError(gsm.GS_ERR_SHAPE, "boom")
     assert e.status == gsm.GS_ERR_SHAPE and "GS_ERR_SHAPE" in str(e)
+
+
+def test_empty_batch_accepts_null_buffers(L):
+    # B == 0: batch-sized buffers may be null (torch gives empty tensors no storage)
+    assert L.gs_similarity(NULL, gsm.GS_F32, 0, 4, 4, A2, gsm.GS_F32, 4, 4, NULL, NULL, gsm.GS_SIM_COSINE,
+                           1.0, NULL, 4, NULL, NULL) == gsm.GS_OK
+    assert L.gs_prob2vec(NULL, gsm.GS_F32, 0, 4, 4, A2, gsm.GS_F32, 4, 4, NULL, gsm.GS_F32, 4, NULL) == gsm.GS_OK
+    assert L.gs_attention(NULL, gsm.GS_F32, 0, 4, 4, A2, gsm.GS_F32, 4, 4, NULL, NULL, gsm.GS_SIM_DOT, 1.0, 1.0,
+                          NULL, 4, NULL, gsm.GS_F32, 4, NULL) == gsm.GS_OK
+    assert L.gs_reconstruct(NULL, gsm.GS_F32, 0, 4, 4, NULL, 4, gsm.GS_BIND_NONE, A2, gsm.GS_F32, 8, 8, NULL,
+                            gsm.GS_F32, 8, NULL) == gsm.GS_OK
+    assert L.gs_project(NULL, gsm.GS_F32, 0, 8, 8, A2, gsm.GS_F32, 2, 8, NULL, gsm.GS_F32, 2, NULL, NULL) == gsm.GS_OK
+    # ... but not the codebook
+    assert L.gs_prob2vec(NULL, gsm.GS_F32, 0, 4, 4, NULL, gsm.GS_F32, 4, 4, NULL, gsm.GS_F32, 4, NULL) == gsm.GS_ERR_ARG
+
+
+def soft(L, groups, ngroups=None, pt=gsm.GS_F32, tt=gsm.GS_F32, mode=gsm.GS_SIM_COSINE):
+    arr = (gsm.SoftGroup * max(1, len(groups)))()
+    for i, g in enumerate(groups):
+        for k, v in g.items():
+            setattr(arr[i], k, v)
+    n = len(groups) if ngroups is None else ngroups
+    return L.gs_soft_select(arr, n, pt, tt, mode, 1.0, 1.0, None)
+
+
+def group(**kw):
+    g = dict(P=0x10000, ldp=10, R=0x200000, ldr=10, cnorm=None, B=5, M=10, r=10, T=None, ldt=10,
+             S=0x400000, lds=10, argmax=None, A=None, lda=10)
+    g.update(kw)
+    return g
+
+
+def test_soft_select_validation(L):
+    assert L.gs_soft_select(None, 1, gsm.GS_F32, gsm.GS_F32, 1, 1.0, 1.0, None) == gsm.GS_ERR_ARG
+    assert soft(L, [group()], ngroups=0) == gsm.GS_ERR_ARG
+    assert soft(L, [group()] * 9) == gsm.GS_ERR_ARG                      # more than 8 groups
+    assert soft(L, [group()], pt=gsm.GS_F64) == gsm.GS_ERR_DTYPE
+    assert soft(L, [group()], mode=5) == gsm.GS_ERR_ARG
+    assert soft(L, [group(M=33, ldp=33, r=33, ldr=33, lds=33)]) == gsm.GS_ERR_SHAPE  # beyond small codebooks
+    assert soft(L, [group(r=11, ldr=11)]) == gsm.GS_ERR_SHAPE            # r > M
+    assert soft(L, [group(ldp=9)]) == gsm.GS_ERR_SHAPE
+    assert soft(L, [group(P=None)]) == gsm.GS_ERR_ARG
+    assert soft(L, [group(A=0x400000 + 16)]) == gsm.GS_ERR_ARG           # A overlaps S
+    assert soft(L, [group(), group(S=0x10000 + 40)]) == gsm.GS_ERR_ARG   # S of group 1 inside P of group 0
+    assert soft(L, [group(argmax=0x600002)]) == gsm.GS_ERR_ALIGN
+    assert soft(L, [group(B=0, P=None, S=None)]) == gsm.GS_OK            # empty: nothing to do
+    assert "gs_" in err(L) or err(L) == ""

@@ -363,3 +363,119 @@ def test_deterministic():
     torch.cuda.synchronize()
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
     assert torch.equal(t1, t2)
+
+
+# ------------------------------------------------- fused soft selection
+
+def soft_case(Ms, Bs, D, seed, dtype=torch.float32):
+    books = []
+    for i, (M, B) in enumerate(zip(Ms, Bs)):
+        C = rq_codebook("bipolar", M, D, seed + i)
+        Qo, Ro, kept, r = oracle.compress(C)
+        P = wl.softmax_probs(B, M, math.sqrt(2), seed + i)
+        Pin, Rin = (P, Ro.astype(np.float32)) if dtype == torch.float32 else \
+            (wl.round_bf16(P), wl.round_bf16(Ro.astype(np.float32)))
+        books.append(dict(C=C, Qo=Qo, Ro=Ro, P=P, Pd=dev(Pin, dtype), Rd=dev(Rin, dtype), M=M, B=B, r=r))
+    return books
+
+
+def soft_outputs(books, want=("T", "S", "argmax", "A")):
+    groups = []
+    for b in books:
+        g = {"P": b["Pd"], "R": b["Rd"]}
+        if "T" in want:
+            g["T"] = torch.full((b["B"], b["r"]), np.nan, device="cuda")
+        if "S" in want:
+            g["S"] = torch.full((b["B"], b["M"]), np.nan, device="cuda")
+        if "argmax" in want:
+            g["argmax"] = torch.full((b["B"],), -1, dtype=torch.int32, device="cuda")
+        if "A" in want:
+            g["A"] = torch.full((b["B"], b["M"]), np.nan, device="cuda")
+        groups.append(g)
+    return groups
+
+
+@pytest.mark.parametrize("mode,scale,beta", [("cosine", 1.0, 16.0), ("dot", 0.03, 1.0), ("cosine", 2.0, -3.0)])
+def test_soft_select(mode, scale, beta):
+    books = soft_case([5, 6, 10, 22, 32], [1000, 257, 1, 513, 300], 1024, 40)
+    groups = soft_outputs(books)
+    gsm.gs_soft_select(groups, mode=mode, scale=scale, beta=beta)
+    torch.cuda.synchronize()
+    m = oracle.COSINE if mode == "cosine" else oracle.DOT
+    for b, g in zip(books, groups):
+        V = oracle.prob2vec(b["P"], b["C"])
+        So = oracle.similarity(V, b["C"], m, scale)
+        assert rowrel(host(g["T"]), oracle.project(V, b["Qo"])) <= TOL_F32
+        assert rowrel(host(g["S"]), So) <= TOL_F32
+        assert rowrel(host(g["A"]), oracle.softmax(So, beta)) <= TOL_F32
+        check_argmax(host(g["argmax"]), So)
+
+
+def test_soft_select_bf16_and_partial_outputs():
+    books = soft_case([10, 22], [700, 450], 1024, 50, dtype=torch.bfloat16)
+    groups = soft_outputs(books, want=("argmax", "A"))
+    gsm.gs_soft_select(groups, mode="cosine", beta=4.0)
+    torch.cuda.synchronize()
+    for b, g in zip(books, groups):
+        V = oracle.prob2vec(b["P"], b["C"])
+        So = oracle.similarity(V, b["C"], oracle.COSINE)
+        assert rowrel(host(g["A"]), oracle.softmax(So, 4.0)) <= TOL_BF16
+        # argmax against the oracle on the bf16-rounded inputs
+        Pb = wl.round_bf16(b["P"]).astype(np.float64)
+        Rb = wl.round_bf16(b["Ro"].astype(np.float32)).astype(np.float64)
+        Tb = Pb @ Rb
+        Sb = (Tb @ Rb.T) / np.linalg.norm(Tb, axis=1)[:, None] / np.linalg.norm(Rb, axis=1)[None, :]
+        check_argmax(host(g["argmax"]), Sb)
+
+
+def test_soft_select_matches_separate_calls():
+    books = soft_case([6, 22], [900, 333], 1024, 60)
+    groups = soft_outputs(books)
+    gsm.gs_soft_select(groups, mode="cosine", beta=16.0)
+    for b, g in zip(books, groups):
+        T = gsm.gs_prob2vec(b["Pd"], b["Rd"])
+        S, idx = gsm.gs_similarity(T, b["Rd"], mode="cosine")
+        A, _ = gsm.gs_attention(T, b["Rd"], mode="cosine", beta=16.0)
+        torch.cuda.synchronize()
+        assert torch.equal(idx, g["argmax"])
+        assert rowrel(host(g["S"]), host(S)) <= 1e-6
+        assert rowrel(host(g["A"]), host(A)) <= 1e-6
+
+
+def test_soft_select_full_vsa_workload():
+    # the benchmark's workload at full size and launch configuration: GPU
+    # compress, then one fused launch over the four attribute codebooks
+    w = wl.WORKLOADS["vsa"]
+    groups, ref = [], []
+    for i, M in enumerate(w.Ms):
+        C = wl.codebook(w, i)
+        P = wl.probabilities(w, i)
+        Q, R, r, kept, cnorm = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+        assert r == M
+        groups.append({"P": dev(P), "R": R.contiguous(), "cnorm": cnorm,
+                       "T": torch.empty((w.B, r), device="cuda"), "S": torch.empty((w.B, M), device="cuda"),
+                       "argmax": torch.empty(w.B, dtype=torch.int32, device="cuda"),
+                       "A": torch.empty((w.B, M), device="cuda")})
+        ref.append((C, P))
+    gsm.gs_soft_select(groups, mode="cosine", beta=16.0)
+    torch.cuda.synchronize()
+    near = 0
+    for (C, P), g in zip(ref, groups):
+        V = oracle.prob2vec(P, C)
+        So = oracle.similarity(V, C, oracle.COSINE)
+        assert rowrel(host(g["S"]), So) <= TOL_F32
+        assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
+        near += check_argmax(host(g["argmax"]), So)
+    print("near-ties:", near)
+
+
+def test_soft_select_rejects_bad_groups():
+    R = dev(np.eye(4, dtype=np.float32))
+    P = dev(np.full((10, 4), 0.25, np.float32))
+    with pytest.raises(gsm.GramSpaceError) as e:
+        gsm.gs_soft_select([{"P": dev(np.zeros((10, 40), np.float32)), "R": dev(np.zeros((40, 40), np.float32))}])
+    assert e.value.status == gsm.GS_ERR_SHAPE
+    out = torch.empty((10, 4), device="cuda")
+    with pytest.raises(gsm.GramSpaceError) as e:
+        gsm.gs_soft_select([{"P": P, "R": R, "S": out, "A": out}])
+    assert e.value.status == gsm.GS_ERR_ARG
