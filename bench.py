@@ -46,6 +46,9 @@ wl = None
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress"],
+                    help="vsa (default, the headline): fused soft selection; large / binary / stress: "
+                         "the matrix-core rows (project, reconstruct + bind, large similarity)")
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--sets", type=int, default=0, help="batch copies to cycle through (0: >= 1 GiB)")
@@ -216,6 +219,109 @@ def pmc_summary(args):
     print(json.dumps(out))
 
 
+MFMA_PEAK = {"f32": 157.3, "bf16": 2516.6}
+
+
+def mfma_workload(args, torch, gsm):
+    """One step of a large workload through the separate calls; per-call HIP
+    events on the launch stream give each kernel's time and the dominant one
+    goes into the roofline entry (matrix-core bound)."""
+    w = wl.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    C = torch.from_numpy(wl.codebook(w)).to(dev)
+    bf = w.bf16
+    dt = torch.bfloat16 if bf else torch.float32
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
+    torch.cuda.synchronize()
+    compress_ms = (time.perf_counter() - t0) * 1e3
+    R = R.contiguous()
+    B, D, M = w.B, w.D, w.Ms[0]
+    calls = []
+    if args.workload in ("large", "stress"):
+        P = wl.device_dirichlet_half(B, M, w.seed, torch, dev, dtype=dt)
+        X = wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch, dtype=dt)
+        T = torch.empty((B, r), dtype=dt, device=dev)
+        xn = torch.empty(B, dtype=torch.float32, device=dev)
+        S = torch.empty((B, M), dtype=torch.float32, device=dev)
+        A = torch.empty((B, M), dtype=torch.float32, device=dev)
+        idx = torch.empty(B, dtype=torch.int32, device=dev)
+        calls.append(("project", lambda: gsm.gs_project(X, Q, out=T, xnorm2=True, xnorm2_out=xn), 2.0 * B * D * r))
+        if args.workload == "stress":
+            T2 = torch.empty((B, r), dtype=dt, device=dev)
+            calls.append(("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2), 2.0 * B * M * r))
+        calls.append(("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx),
+                      2.0 * B * M * r))
+        calls.append(("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=args.beta, out=A),
+                      2.0 * B * M * r))
+        if args.workload == "stress":
+            Xr = torch.empty((B, D), dtype=dt, device=dev)
+            calls.append(("reconstruct", lambda: gsm.gs_reconstruct(T2, Q, out=Xr), 2.0 * B * r * D))
+    else:   # binary: bind pairs
+        Pa = torch.from_numpy(wl.probabilities(w, 0)).to(dev)
+        Pb = torch.from_numpy(wl.probabilities(w, 0, stream=wl.STREAM_PROBS_B)).to(dev)
+        Ta = torch.empty((B, r), device=dev)
+        Tb = torch.empty((B, r), device=dev)
+        S = torch.empty((B, M), device=dev)
+        idx = torch.empty(B, dtype=torch.int32, device=dev)
+        Y = torch.empty((B, D), device=dev)
+        Ty = torch.empty((B, r), device=dev)
+        calls.append(("prob2vec", lambda: (gsm.gs_prob2vec(Pa, R, out=Ta), gsm.gs_prob2vec(Pb, R, out=Tb)),
+                      2 * 2.0 * B * M * r))
+        calls.append(("similarity", lambda: gsm.gs_similarity(Ta, R, cnorm=cnorm, out=S, argmax_out=idx),
+                      2.0 * B * M * r))
+        calls.append(("reconstruct_bind", lambda: gsm.gs_reconstruct(Ta, Q, T2=Tb, bind="mul", out=Y),
+                      4.0 * B * r * D))
+        calls.append(("reproject", lambda: gsm.gs_project(Y, Q, out=Ty), 2.0 * B * D * r))
+    stream = torch.cuda.current_stream()
+    for _ in range(max(1, args.warmup)):
+        for _, f, _ in calls:
+            f()
+    torch.cuda.synchronize()
+    per = {n: [] for n, _, _ in calls}
+    evs = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for n, f, _ in calls:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            f()
+            e1.record(stream)
+            evs.append((n, e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for n, e0, e1 in evs:
+        per[n].append(e0.elapsed_time(e1))
+    flops = {n: fl for n, _, fl in calls}
+    dom = max(per, key=lambda n: sum(per[n]))
+    dom_ms = float(np.mean(per[dom]))
+    peak = MFMA_PEAK["bf16" if bf else "f32"]
+    achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
+    kernel = {"project": "gemm_store_kernel (X Q^T)", "reproject": "gemm_store_kernel (Y Q^T)",
+              "reconstruct": "gemm_store_kernel (T Q)", "reconstruct_bind": "gemm_store_kernel (T Q .* T2 Q)",
+              "prob2vec": "gemm_store_kernel (P R)", "similarity": "gemm_rowsweep_kernel (similarity)",
+              "attention": "gemm_rowsweep_kernel (softmax)"}[dom]
+    out = {
+        "metric": METRIC, "value": B * args.steps / wall, "unit": "queries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32", "data": "synthetic",
+        "config": {"workload": "%s: codebook M=%d, D=%d (r=%d), batch %d; calls %s"
+                               % (w.name, M, D, r, B, ", ".join(n for n, _, _ in calls))},
+        "roofline": {"bound": "mfma", "kernel": kernel, "call": dom, "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "flops_per_launch": flops[dom], "avg_launch_ms": dom_ms},
+        "cpu_baseline": None,
+        "extra": {"per_call_ms": {n: float(np.mean(v)) for n, v in per.items()},
+                  "per_call_TFLOPs": {n: flops[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in per},
+                  "compress_ms": compress_ms, "rank": r, "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -246,6 +352,9 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 5}))
         return
 
+    if args.workload != "vsa":
+        mfma_workload(args, torch, gsm)
+        return
     w = wl.WORKLOADS["vsa"]
     per_set = sum(w.B * (16 * M + 4) for M in w.Ms)
     nsets = args.sets or max(1, int(np.ceil((1 << 30) / per_set)))

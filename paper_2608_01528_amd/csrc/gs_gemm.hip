@@ -245,6 +245,192 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
     }
 }
 
+// ------------------------------------------------------- bf16 main loop
+//
+// Both operands bf16: v_mfma_f32_32x32x16_bf16 on the same 128 x 128 block
+// with K-steps of 64.  Operands stay bf16 in LDS, k-contiguous per row
+// ([m][k] and [n][k], row stride BSTR), so every MFMA operand is one 16-byte
+// LDS read (8 consecutive k) per lane.  A K x N operand (b_nn) is transposed
+// while it is written to LDS.  Same accumulator layout as the fp32 loop.
+
+constexpr int BK16 = 64;                       // K-step of the bf16 loop
+constexpr int BSTR = BK16 + 8;                 // bf16 per staged row (16-byte pad)
+constexpr int BTILE = 128 * BSTR;              // bf16 per staged operand tile
+
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+// LDS floats used by the staging buffers of either loop.
+template <typename TA, typename TB, bool TWO>
+constexpr size_t mma_lds_floats() {
+    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2) return (size_t)2 * (TWO ? 3 : 2) * BTILE / 2;
+    else return (size_t)2 * (TWO ? 3 : 2) * TILE_FLOATS;
+}
+
+// 8 consecutive bf16 (raw bits) starting at p, zeros at or beyond `lim`
+// elements from p (lim <= 0: all zero); vector load when allowed.
+__device__ __forceinline__ uint4 load8_bf16(const bf16_t *p, int64_t lim, bool vec) {
+    if (lim >= 8 && vec) return *reinterpret_cast<const uint4 *>(p);
+    uint16_t h[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = (i < lim) ? p[i].bits : (uint16_t)0;
+    return uint4{(uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16),
+                 (uint32_t)h[4] | ((uint32_t)h[5] << 16), (uint32_t)h[6] | ((uint32_t)h[7] << 16)};
+}
+
+// Row operand (128 rows x 64 k): thread t moves rows t / 8 + 32 i (i < 4),
+// k-chunk 8 (t % 8).  The chunk's validity is all-or-nothing in vector mode
+// (K a multiple of 8), element-wise otherwise.
+__device__ __forceinline__ void fetch_rows_bf16(const bf16_t *base, int64_t ld, int64_t row0, int64_t nrows,
+                                                int64_t k0, int64_t K, bool vec, uint4 v[4]) {
+    const int t = threadIdx.x;
+    const int64_t kc = k0 + 8 * (t & 7);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = row0 + (t >> 3) + 32 * i;
+        v[i] = (row < nrows && kc < K) ? load8_bf16(base + row * ld + kc, K - kc, vec) : uint4{0, 0, 0, 0};
+    }
+}
+
+__device__ __forceinline__ void stash_rows_bf16(uint16_t *tile, const uint4 v[4]) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<uint4 *>(tile + ((t >> 3) + 32 * i) * BSTR + 8 * (t & 7)) = v[i];
+}
+
+// K x N operand (64 k x 128 n): thread t moves k-rows t / 16 + 16 i (i < 4),
+// n-chunk 8 (t % 16); written transposed ([n][k]) into LDS.
+__device__ __forceinline__ void fetch_kmajor_bf16(const bf16_t *base, int64_t ld, int64_t k0, int64_t K,
+                                                  int64_t n0, int64_t N, bool vec, uint4 v[4]) {
+    const int t = threadIdx.x;
+    const int64_t nc = n0 + 8 * (t & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t k = k0 + (t >> 4) + 16 * i;
+        v[i] = (k < K && nc < N) ? load8_bf16(base + k * ld + nc, N - nc, vec) : uint4{0, 0, 0, 0};
+    }
+}
+
+__device__ __forceinline__ void stash_kmajor_bf16(uint16_t *tile, const uint4 v[4]) {
+    const int t = threadIdx.x;
+    const int nb = 8 * (t & 15);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int k = (t >> 4) + 16 * i;
+        const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            tile[(nb + 2 * e) * BSTR + k] = (uint16_t)(w[e] & 0xffffu);
+            tile[(nb + 2 * e + 1) * BSTR + k] = (uint16_t)(w[e] >> 16);
+        }
+    }
+}
+
+__device__ __forceinline__ bf8v lds_frag(const uint16_t *tile, int row, int kofs) {
+    return *reinterpret_cast<const bf8v *>(tile + row * BSTR + kofs);
+}
+
+// Sum of squares of the 64 staged k-values of row t (t < 128).
+__device__ __forceinline__ float row_sq_bf16(const uint16_t *tile, int row) {
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < BK16 / 8; ++q) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(tile + row * BSTR + 8 * q);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(w[e] << 16), hi = __uint_as_float(w[e] & 0xffff0000u);
+            s += lo * lo + hi * hi;
+        }
+    }
+    return s;
+}
+
+template <bool BNN, bool TWO>
+__device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, int64_t n0, bool veca, bool vecb,
+                                               float *lds_f, f16v acc[2][2], f16v acc2[2][2], bool sqa,
+                                               float *sqa_out, bool sqb, float *sqb_out) {
+    const bf16_t *A = static_cast<const bf16_t *>(g.A);
+    const bf16_t *A2 = static_cast<const bf16_t *>(g.A2);
+    const bf16_t *B = static_cast<const bf16_t *>(g.B);
+    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+    const int nstage = TWO ? 3 : 2;
+    uint16_t *buf[2] = {lds, lds + nstage * BTILE};
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            acc[i][j] = f16v{};
+            if (TWO) acc2[i][j] = f16v{};
+        }
+    float sa = 0.f, sb = 0.f;
+    uint4 va[4], vb[4], va2[4];
+    const int64_t nk = (g.K + BK16 - 1) / BK16;
+    auto fetch = [&](int64_t kt) {
+        fetch_rows_bf16(A, g.lda, m0, g.M, kt * BK16, g.K, veca, va);
+        if (TWO) fetch_rows_bf16(A2, g.lda2, m0, g.M, kt * BK16, g.K, veca, va2);
+        if (BNN) fetch_kmajor_bf16(B, g.ldb, kt * BK16, g.K, n0, g.N, vecb, vb);
+        else fetch_rows_bf16(B, g.ldb, n0, g.N, kt * BK16, g.K, vecb, vb);
+    };
+    auto stash = [&](uint16_t *b) {
+        stash_rows_bf16(b, va);
+        if (BNN) stash_kmajor_bf16(b + BTILE, vb);
+        else stash_rows_bf16(b + BTILE, vb);
+        if (TWO) stash_rows_bf16(b + 2 * BTILE, va2);
+    };
+
+    fetch(0);
+    stash(buf[0]);
+    __syncthreads();
+    for (int64_t kt = 0; kt < nk; ++kt) {
+        uint16_t *cur = buf[kt & 1];
+        if (kt + 1 < nk) fetch(kt + 1);
+        const uint16_t *As = cur, *Bs = cur + BTILE, *As2 = cur + 2 * BTILE;
+#pragma unroll
+        for (int kk = 0; kk < BK16; kk += 16) {
+            const int ko = kk + 8 * (l >> 5);
+            const bf8v a0 = lds_frag(As, wm + (l & 31), ko), a1 = lds_frag(As, wm + 32 + (l & 31), ko);
+            const bf8v b0 = lds_frag(Bs, wn + (l & 31), ko), b1 = lds_frag(Bs, wn + 32 + (l & 31), ko);
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+            if (TWO) {
+                const bf8v c0 = lds_frag(As2, wm + (l & 31), ko), c1 = lds_frag(As2, wm + 32 + (l & 31), ko);
+                acc2[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c0, b0, acc2[0][0], 0, 0, 0);
+                acc2[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c0, b1, acc2[0][1], 0, 0, 0);
+                acc2[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c1, b0, acc2[1][0], 0, 0, 0);
+                acc2[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c1, b1, acc2[1][1], 0, 0, 0);
+            }
+        }
+        if (threadIdx.x < 128) {
+            if (sqa) sa += row_sq_bf16(As, threadIdx.x);
+            if (sqb) sb += row_sq_bf16(Bs, threadIdx.x);
+        }
+        if (kt + 1 < nk) stash(buf[(kt + 1) & 1]);
+        __syncthreads();
+    }
+    if (threadIdx.x < 128) {
+        if (sqa) *sqa_out = sa;
+        if (sqb) *sqb_out = sb;
+    }
+}
+
+// Dispatch on the operand types: both bf16 -> bf16 matrix cores, otherwise
+// fp32 matrix cores on widened operands.
+template <typename TA, typename TB, bool BNN, bool TWO>
+__device__ __forceinline__ void block_mma_any(const GemmArgs &g, int64_t m0, int64_t n0, bool veca, bool vecb,
+                                              float *lds, f16v acc[2][2], f16v acc2[2][2], bool sqa,
+                                              float *sqa_out, bool sqb, float *sqb_out) {
+    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2)
+        block_mma_bf16<BNN, TWO>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
+    else
+        block_mma<TA, TB, BNN, TWO>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
+}
+
 // XCD-aware tile order: work-group ids are dealt to the 8 XCDs round-robin,
 // so logical tile L is given to ids that share an XCD for consecutive L.
 // Consecutive logical tiles share their A row block (n varies fastest), which
@@ -267,7 +453,7 @@ __global__ void __launch_bounds__(NTHR) gemm_store_kernel(GemmArgs g, int veca, 
     f16v acc[2][2], acc2[2][2];
     const bool sqa = (g.rownorm2 != nullptr) && (n0 == 0);
     float sa = 0.f, sb = 0.f;
-    block_mma<TA, TB, BNN, BIND>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
+    block_mma_any<TA, TB, BNN, BIND>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
     if (sqa && threadIdx.x < 128 && m0 + threadIdx.x < g.M) g.rownorm2[m0 + threadIdx.x] = sa;
 
     TO *C = static_cast<TO *>(g.C);
@@ -305,7 +491,7 @@ constexpr int SS_STRIDE = BN + 1;
 template <typename TA, typename TB, bool SOFTMAX>
 __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int veca, int vecb) {
     extern __shared__ float lds[];
-    float *ss = lds + 2 * 2 * TILE_FLOATS;         // scores [BM][SS_STRIDE]
+    float *ss = lds + mma_lds_floats<TA, TB, false>();   // scores [BM][SS_STRIDE]
     float *rq = ss + BM * SS_STRIDE;               // 1 / ||x|| per row (or 1)
     float *cn = rq + BM;                           // 1 / ||c|| per column (or 1)
     const int64_t nM = (g.M + BM - 1) / BM;
@@ -329,7 +515,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
         const bool sqa = g.cosine && g.qnorm2 == nullptr && nt == 0;
         const bool sqb = g.cosine && g.cnorm == nullptr;
         float sa = 0.f, sb = 0.f;
-        block_mma<TA, TB, false, false>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, sqb, &sb);
+        block_mma_any<TA, TB, false, false>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, sqb, &sb);
         if (t < 128) {
             if (nt == 0) {
                 float q = 1.f;
@@ -444,7 +630,7 @@ hipError_t dispatch_store(bool b_nn, bool bind, const GemmArgs &a, bool veca, bo
     const int64_t nM = (a.M + BM - 1) / BM, nN = (a.N + BN - 1) / BN;
     const int64_t total = nM * nN;
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const size_t lds = (size_t)2 * (bind ? 3 : 2) * TILE_FLOATS * sizeof(float);
+    const size_t lds = (bind ? mma_lds_floats<TA, TB, true>() : mma_lds_floats<TA, TB, false>()) * sizeof(float);
     if (b_nn) {
         if (bind) return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, true>, grid, lds, s, a, veca, vecb);
         return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, false>, grid, lds, s, a, veca, vecb);
@@ -457,7 +643,7 @@ template <typename TA, typename TB>
 hipError_t dispatch_rowsweep(bool softmax, const GemmArgs &a, bool veca, bool vecb, hipStream_t s) {
     const int64_t nM = (a.M + BM - 1) / BM;
     const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
-    const size_t lds = ((size_t)4 * TILE_FLOATS + BM * SS_STRIDE + 2 * BM) * sizeof(float);
+    const size_t lds = (mma_lds_floats<TA, TB, false>() + BM * SS_STRIDE + 2 * BM) * sizeof(float);
     if (softmax) return launch_with_lds(gemm_rowsweep_kernel<TA, TB, true>, grid, lds, s, a, veca, vecb);
     return launch_with_lds(gemm_rowsweep_kernel<TA, TB, false>, grid, lds, s, a, veca, vecb);
 }

@@ -207,3 +207,34 @@ def probabilities(w: Workload, i: int = 0, B: int | None = None, stream: int = S
     if w.probs == "softmax":
         return softmax_probs(B, M, w.prob_param, w.seed, s, chunks)
     return dirichlet_probs(B, M, w.prob_param, w.seed, s, chunks)
+
+
+# ------------------------------------------------- device-side large batches
+
+def device_dirichlet_half(B: int, M: int, seed: int, torch, device, dtype=None):
+    """B x M rows of Dirichlet(1/2 * 1_M), generated on the device: Gamma(1/2)
+    equals Z^2 / 2 for a standard normal Z, so normalising Z^2 gives the
+    Dirichlet(1/2) law exactly.  Seeded torch generator on the device."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed * 1000003 + 11)
+    Z = torch.randn((B, M), generator=g, device=device, dtype=torch.float32)
+    Z = Z * Z
+    P = Z / Z.sum(dim=1, keepdim=True)
+    return P if dtype is None else P.to(dtype)
+
+
+def device_noisy_queries(P, C, var: float, seed: int, torch, dtype=None, chunk: int = 16384):
+    """Hard-selection queries on the device: rows p C + N(0, var) noise, built
+    in row chunks (fp32 arithmetic, optional cast of the result)."""
+    B, D = P.shape[0], C.shape[1]
+    out = torch.empty((B, D), dtype=dtype or torch.float32, device=P.device)
+    g = torch.Generator(device=P.device)
+    g.manual_seed(seed * 1000003 + 29)
+    Cf = C.float()
+    sd = float(np.sqrt(var))
+    for a in range(0, B, chunk):
+        b = min(B, a + chunk)
+        x = P[a:b].float() @ Cf
+        x += sd * torch.randn((b - a, D), generator=g, device=P.device, dtype=torch.float32)
+        out[a:b] = x.to(out.dtype)
+    return out

@@ -1,0 +1,156 @@
+"""Parity at the configured full sizes, in the shapes the benchmark and the
+stress workload use.
+
+The GPU processes every row of each batch; the fp64 oracle recomputes a
+sample of rows (the first and last rows, chunk boundaries and random rows) one
+by one from the same inputs, read back from the device.  Properties that hold
+at any size (softmax rows sum to one, argmax agrees with the returned scores,
+cosines lie in [-1, 1]) are checked on every row.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_01528_amd import gramspace as gsm
+from paper_2608_01528_amd import workloads as wl
+from tests.gpu_util import TOL_BF16, TOL_F32, check_argmax, dev, host, rowrel
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gsm.lib()
+
+
+def sample_rows(B, n_random, seed):
+    fixed = [0, 1, B // 2, B - 2, B - 1] + [c for c in (4095, 4096, 16383, 16384) if c < B]
+    rnd = np.random.default_rng(seed).choice(B, size=n_random, replace=False)
+    return np.array(sorted(set(fixed) | set(int(x) for x in rnd)))
+
+
+def whole_batch_properties(S, idx, A=None, cosine=True):
+    Sg = S.float()
+    am = torch.argmax(Sg, dim=1).to(torch.int32)
+    # the returned argmax points at a maximal score of its row
+    picked = Sg.gather(1, idx.long()[:, None])[:, 0]
+    assert torch.all(picked >= Sg.max(dim=1).values).item()
+    assert (am == idx).float().mean().item() > 0.999
+    if cosine:
+        assert Sg.abs().max().item() <= 1.0 + 1e-4
+    if A is not None:
+        assert torch.allclose(A.sum(dim=1), torch.ones(A.shape[0], device=A.device), atol=1e-4)
+
+
+def test_large_workload_full_size():
+    w = wl.WORKLOADS["large"]
+    C = wl.codebook(w)
+    print("large: compress", C.shape, flush=True)
+    Cd = dev(C)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    Q64, R64, r64, kept64, _ = gsm.gs_compress(Cd)
+    Q, R, r, kept, cnorm = gsm.gs_compress(Cd, q_dtype=torch.float32, r_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert r == r64 == ro == 256
+    assert np.abs(host(Q64) - Qo).max() <= 1e-12
+    assert np.abs(host(R64) - Ro).max() <= 1e-12 * np.abs(Ro).max()
+    print("large: batch", flush=True)
+    P = wl.device_dirichlet_half(w.B, 256, w.seed, torch, "cuda")
+    X = wl.device_noisy_queries(P, Cd, w.noise_var, w.seed, torch)
+    T, xn = gsm.gs_project(X, Q, xnorm2=True)
+    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine")
+    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0)
+    torch.cuda.synchronize()
+    whole_batch_properties(S, idx, A)
+    rows = sample_rows(w.B, 48, 3)
+    Xs = host(X[rows])
+    assert rowrel(host(T[rows]), oracle.project(Xs, Qo)) <= TOL_F32
+    np.testing.assert_allclose(host(xn[rows]), oracle.row_norms(Xs) ** 2, rtol=TOL_F32)
+    So = oracle.similarity(Xs, C, oracle.COSINE)
+    assert rowrel(host(S[rows]), So) <= TOL_F32
+    assert rowrel(host(A[rows]), oracle.softmax(So, 16.0)) <= TOL_F32
+    print("large: near-ties", check_argmax(host(idx[rows]), So), flush=True)
+
+
+def test_binary_workload_full_size():
+    w = wl.WORKLOADS["binary"]
+    C = wl.codebook(w)
+    print("binary: compress", C.shape, flush=True)
+    Cd = dev(C)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    Q64, R64, r64, _, _ = gsm.gs_compress(Cd)
+    Q, R, r, kept, cnorm = gsm.gs_compress(Cd, q_dtype=torch.float32, r_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert r == r64 == ro == 1000
+    assert np.abs(host(Q64) - Qo).max() <= 1e-12
+    assert np.abs(host(R64) - Ro).max() <= 1e-12 * np.abs(Ro).max()
+    rows = sample_rows(w.B, 40, 4)
+    print("binary: batch", flush=True)
+    Pa = wl.probabilities(w, 0)
+    Pb = wl.probabilities(w, 0, stream=wl.STREAM_PROBS_B)
+    Ta = gsm.gs_prob2vec(dev(Pa), R)
+    Tb = gsm.gs_prob2vec(dev(Pb), R)
+    S, idx = gsm.gs_similarity(Ta, R, cnorm=cnorm, mode="cosine")
+    Y = gsm.gs_reconstruct(Ta, Q, T2=Tb, bind="mul")
+    Ty = gsm.gs_project(Y, Q)
+    torch.cuda.synchronize()
+    whole_batch_properties(S, idx)
+    Va = oracle.prob2vec(Pa[rows], C)
+    Vb = oracle.prob2vec(Pb[rows], C)
+    assert rowrel(host(Ta[rows]), oracle.project(Va, Qo)) <= TOL_F32
+    So = oracle.similarity(Va, C, oracle.COSINE)
+    assert rowrel(host(S[rows]), So) <= TOL_F32
+    print("binary: near-ties", check_argmax(host(idx[rows]), So), flush=True)
+    Yo = oracle.bind(Va, Vb)
+    assert rowrel(host(Y[rows]), Yo) <= TOL_F32
+    assert rowrel(host(Ty[rows]), oracle.project(Yo, Qo)) <= TOL_F32
+
+
+@pytest.mark.timeout(400)
+def test_stress_workload_full_size():
+    w = wl.WORKLOADS["stress"]
+    C = wl.codebook(w)
+    print("stress: oracle compress", C.shape, flush=True)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    assert ro == 2048 - 205
+    Cd = dev(C)
+    print("stress: gpu compress", flush=True)
+    Q64, R64, r64, kept64, _ = gsm.gs_compress(Cd)
+    torch.cuda.synchronize()
+    assert r64 == ro
+    assert list(host(kept64).astype(int)) == list(kept_o)
+    assert np.abs(host(Q64) - Qo).max() <= 1e-12
+    assert np.abs(host(R64) - Ro).max() <= 1e-12 * np.abs(Ro).max()
+    del Q64, R64
+    Q, R, r, kept, cnorm = gsm.gs_compress(Cd, q_dtype=torch.bfloat16, r_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert r == ro
+    print("stress: batch", flush=True)
+    P = wl.device_dirichlet_half(w.B, 2048, w.seed, torch, "cuda", dtype=torch.bfloat16)
+    X = wl.device_noisy_queries(P, Cd, w.noise_var, w.seed, torch, dtype=torch.bfloat16)
+    print("stress: project", flush=True)
+    T, xn = gsm.gs_project(X, Q, out_dtype=torch.bfloat16, xnorm2=True)
+    T2 = gsm.gs_prob2vec(P, R, out_dtype=torch.bfloat16)
+    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine")
+    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0)
+    Xr = gsm.gs_reconstruct(T2, Q, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    whole_batch_properties(S, idx, A)
+    rows = sample_rows(w.B, 24, 5)
+    Xs = host(X[rows])
+    Ps = host(P[rows])
+    assert rowrel(host(T[rows]), oracle.project(Xs, Qo)) <= TOL_BF16
+    np.testing.assert_allclose(host(xn[rows]), oracle.row_norms(Xs) ** 2, rtol=1e-4)
+    Vs = oracle.prob2vec(Ps, C)
+    assert rowrel(host(T2[rows]), oracle.project(Vs, Qo)) <= TOL_BF16
+    assert rowrel(host(Xr[rows]), Vs) <= TOL_BF16
+    So = oracle.similarity(Xs, C, oracle.COSINE)
+    assert rowrel(host(S[rows]), So) <= TOL_BF16
+    assert rowrel(host(A[rows]), oracle.softmax(So, 16.0)) <= TOL_BF16
+    # bf16 coordinates and codebook: near-tie band of the bf16 rounding
+    print("stress: near-ties", check_argmax(host(idx[rows]), So, band_rel=1e-2), flush=True)
