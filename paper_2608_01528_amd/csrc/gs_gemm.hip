@@ -298,31 +298,34 @@ __device__ __forceinline__ void stash_rows_bf16(uint16_t *tile, const uint4 v[4]
         *reinterpret_cast<uint4 *>(tile + ((t >> 3) + 32 * i) * BSTR + 8 * (t & 7)) = v[i];
 }
 
-// K x N operand (64 k x 128 n): thread t moves k-rows t / 16 + 16 i (i < 4),
-// n-chunk 8 (t % 16); written transposed ([n][k]) into LDS.
+// K x N operand (64 k x 128 n), written transposed ([n][k]) into LDS.
+// Thread t owns the 4 x 8 block k = 4 (t % 16) + 0..3, n = 8 (t / 16) + 0..7:
+// four 16-byte loads (one per k), a register transpose with v_perm_b32, and
+// eight 8-byte LDS writes (four k-values of one n each).  Lanes vary along k
+// first, so every 16 lanes fill one contiguous 128-byte LDS row segment.
 __device__ __forceinline__ void fetch_kmajor_bf16(const bf16_t *base, int64_t ld, int64_t k0, int64_t K,
                                                   int64_t n0, int64_t N, bool vec, uint4 v[4]) {
     const int t = threadIdx.x;
-    const int64_t nc = n0 + 8 * (t & 15);
+    const int64_t nc = n0 + 8 * (t >> 4);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int64_t k = k0 + (t >> 4) + 16 * i;
+        const int64_t k = k0 + 4 * (t & 15) + i;
         v[i] = (k < K && nc < N) ? load8_bf16(base + k * ld + nc, N - nc, vec) : uint4{0, 0, 0, 0};
     }
 }
 
 __device__ __forceinline__ void stash_kmajor_bf16(uint16_t *tile, const uint4 v[4]) {
     const int t = threadIdx.x;
-    const int nb = 8 * (t & 15);
+    const int kb = 4 * (t & 15), nb = 8 * (t >> 4);
+    const uint32_t w0[4] = {v[0].x, v[0].y, v[0].z, v[0].w}, w1[4] = {v[1].x, v[1].y, v[1].z, v[1].w};
+    const uint32_t w2[4] = {v[2].x, v[2].y, v[2].z, v[2].w}, w3[4] = {v[3].x, v[3].y, v[3].z, v[3].w};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int k = (t >> 4) + 16 * i;
-        const uint32_t w[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            tile[(nb + 2 * e) * BSTR + k] = (uint16_t)(w[e] & 0xffffu);
-            tile[(nb + 2 * e + 1) * BSTR + k] = (uint16_t)(w[e] >> 16);
-        }
+    for (int m = 0; m < 4; ++m) {
+        // low halves: column n = nb + 2m; high halves: n = nb + 2m + 1
+        const uint2 lo = {__builtin_amdgcn_perm(w1[m], w0[m], 0x05040100u), __builtin_amdgcn_perm(w3[m], w2[m], 0x05040100u)};
+        const uint2 hi = {__builtin_amdgcn_perm(w1[m], w0[m], 0x07060302u), __builtin_amdgcn_perm(w3[m], w2[m], 0x07060302u)};
+        *reinterpret_cast<uint2 *>(tile + (nb + 2 * m) * BSTR + kb) = lo;
+        *reinterpret_cast<uint2 *>(tile + (nb + 2 * m + 1) * BSTR + kb) = hi;
     }
 }
 
@@ -419,17 +422,249 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
     }
 }
 
-// Dispatch on the operand types: both bf16 -> bf16 matrix cores, otherwise
-// fp32 matrix cores on widened operands.
-template <typename TA, typename TB, bool BNN, bool TWO>
+// --------------------------------------------- bf16 pipelined main loop
+//
+// The same 128 x 128 block and K-steps of 64, with operand tiles brought
+// into LDS by asynchronous global->LDS loads (global_load_lds_dwordx4), NS
+// stages deep: the loads for K-step kt + NS - 1 are in flight while step kt
+// is multiplied, with one barrier per step and no register staging.  Each
+// load instruction fills 1 KB of LDS in lane order, so the layout is chosen
+// through which 16-byte chunk each lane fetches:
+//   row tile   [128][64]: chunk c of row r sits at position c ^ (r & 7);
+//   k-row tile [64][128]: chunk c of k-row k sits at position c ^ (k & 15);
+// (XOR swizzles that make the MFMA fragment reads conflict-free without
+// padding).  Fragments of a k-row tile (b_nn) come from transpose reads
+// (ds_read_b64_tr_b16), which hand each lane 4 consecutive k of one column.
+// Rows beyond the matrix reuse its last row (their results are discarded);
+// k beyond K is zeroed in LDS in the last step.  Requires 16-byte aligned
+// rows (ld a multiple of 8): rows are read in 16-byte units up to column
+// ceil(cols / 8) * 8 <= ld.
+
+constexpr int DTILE = 128 * 64;                 // bf16 per operand tile (16 KB)
+
+#define GS_G1 __attribute__((address_space(1)))
+#define GS_L3 __attribute__((address_space(3)))
+typedef short s4v __attribute__((ext_vector_type(4)));
+
+template <bool TWO, int NS>
+constexpr size_t dma_lds_floats() { return (size_t)NS * (TWO ? 3 : 2) * DTILE / 2; }
+
+// s_waitcnt with vmcnt <= n (expcnt and lgkmcnt unconstrained), gfx9 encoding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void dma16(const void *g, uint16_t *lds_wave_base) {
+    __builtin_amdgcn_global_load_lds((const GS_G1 void *)g, (GS_L3 void *)lds_wave_base, 16, 0, 0);
+}
+
+// 16 load instructions of 1 KB per row tile: wave w issues blocks 4w .. 4w+3
+// (8 rows each).  Lane L of block b fetches row 8b + L/8, chunk (L%8) ^ (L/8).
+__device__ __forceinline__ void dma_rows(const bf16_t *base, int64_t ld, int64_t row0, int64_t nrows,
+                                         int64_t k0, int64_t K, uint16_t *tile) {
+    const int L = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int rl = L >> 3, c = (L & 7) ^ rl;
+    int64_t kc = k0 + 8 * c;
+    const int64_t klast = ((K - 1) >> 3) << 3;
+    if (kc > klast) kc = klast;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int b = 4 * w + q;
+        int64_t row = row0 + 8 * b + rl;
+        if (row > nrows - 1) row = nrows - 1;
+        dma16(base + row * ld + kc, tile + b * 512);
+    }
+}
+
+// 16 load instructions of 1 KB per k-row tile: wave w issues blocks 4w .. 4w+3
+// (4 k-rows each).  Lane L of block b fetches k-row 4b + L/16, chunk
+// (L%16) ^ (k-row % 16).
+__device__ __forceinline__ void dma_krows(const bf16_t *base, int64_t ld, int64_t k0, int64_t K, int64_t n0,
+                                          int64_t N, uint16_t *tile) {
+    const int L = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nlast = ((N - 1) >> 3) << 3;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int b = 4 * w + q;
+        const int kl = 4 * b + (L >> 4);
+        const int c = (L & 15) ^ (kl & 15);
+        int64_t nc = n0 + 8 * c;
+        if (nc > nlast) nc = nlast;
+        int64_t k = k0 + kl;
+        if (k > K - 1) k = K - 1;
+        dma16(base + k * ld + nc, tile + b * 512);
+    }
+}
+
+// Zero the k >= kvalid part of a staged row tile / k-row tile.
+__device__ __forceinline__ void zero_rows_tail(uint16_t *tile, int kvalid) {
+    for (int e = threadIdx.x; e < 128 * 64; e += NTHR) {
+        const int r = e >> 6, kl = e & 63;
+        if (kl >= kvalid) tile[r * 64 + ((((kl >> 3) ^ (r & 7))) << 3) + (kl & 7)] = 0;
+    }
+}
+__device__ __forceinline__ void zero_krows_tail(uint16_t *tile, int kvalid) {
+    for (int e = threadIdx.x; e < 64 * 128; e += NTHR)
+        if ((e >> 7) >= kvalid) tile[e] = 0;
+}
+
+__device__ __forceinline__ bf8v frag_rows(const uint16_t *tile, int r, int c) {
+    return *reinterpret_cast<const bf8v *>(tile + r * 64 + ((c ^ (r & 7)) << 3));
+}
+
+// B fragment (8 consecutive k at kk + 8 (lane / 32), column n0w + lane % 32)
+// from a k-row tile, by two transpose reads of 4 k each.
+__device__ __forceinline__ bf8v frag_krows(const uint16_t *tile, int kk, int n0w) {
+    const int l = threadIdx.x & 63;
+    const int g = l >> 4, a = l & 15;
+    const int n = n0w + 16 * (g & 1) + 4 * (a & 3);
+    const int k = kk + 8 * (g >> 1) + (a >> 2);
+    const int c = n >> 3;
+    const uint16_t *p0 = tile + k * 128 + ((c ^ (k & 15)) << 3) + (n & 7);
+    const uint16_t *p1 = tile + (k + 4) * 128 + ((c ^ ((k + 4) & 15)) << 3) + (n & 7);
+    const s4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((GS_L3 s4v *)(p0));
+    const s4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((GS_L3 s4v *)(p1));
+    const s4v both[2] = {lo, hi};
+    return *reinterpret_cast<const bf8v *>(both);
+}
+
+__device__ __forceinline__ float row_sq_dma(const uint16_t *tile, int r) {
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(tile + r * 64 + 8 * q);
+        const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float lo = __uint_as_float(wv[e] << 16), hi = __uint_as_float(wv[e] & 0xffff0000u);
+            s += lo * lo + hi * hi;
+        }
+    }
+    return s;
+}
+
+template <bool BNN, bool TWO, int DMA_STAGES>
+__device__ __forceinline__ void block_mma_bf16_dma(const GemmArgs &g, int64_t m0, int64_t n0, float *lds_f,
+                                                   f16v acc[2][2], f16v acc2[2][2], bool sqa, float *sqa_out,
+                                                   bool sqb, float *sqb_out) {
+    const bf16_t *A = static_cast<const bf16_t *>(g.A);
+    const bf16_t *A2 = static_cast<const bf16_t *>(g.A2);
+    const bf16_t *B = static_cast<const bf16_t *>(g.B);
+    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
+    constexpr int NT_ = TWO ? 3 : 2;                 // tiles per stage
+    constexpr int OPS = 4 * NT_;                     // load instructions per stage per wave
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            acc[i][j] = f16v{};
+            if (TWO) acc2[i][j] = f16v{};
+        }
+    float sa = 0.f, sb = 0.f;
+    const int64_t nk = (g.K + BK16 - 1) / BK16;
+    auto stage = [&](int s) { return lds + s * NT_ * DTILE; };
+    auto issue = [&](int64_t kt) {
+        uint16_t *st = stage((int)(kt % DMA_STAGES));
+        dma_rows(A, g.lda, m0, g.M, kt * BK16, g.K, st);
+        if (BNN) dma_krows(B, g.ldb, kt * BK16, g.K, n0, g.N, st + DTILE);
+        else dma_rows(B, g.ldb, n0, g.N, kt * BK16, g.K, st + DTILE);
+        if (TWO) dma_rows(A2, g.lda2, m0, g.M, kt * BK16, g.K, st + 2 * DTILE);
+    };
+
+    for (int s = 0; s < DMA_STAGES - 1; ++s)
+        if (s < nk) issue(s);
+    for (int64_t kt = 0; kt < nk; ++kt) {
+        // the loads of step kt are complete once at most the later stages'
+        // loads remain outstanding
+        if (kt + 1 < nk) wait_vm<OPS * (DMA_STAGES - 2)>();
+        else wait_vm<0>();
+        __builtin_amdgcn_s_barrier();
+        if (kt + DMA_STAGES - 1 < nk) issue(kt + DMA_STAGES - 1);
+        uint16_t *cur = stage((int)(kt % DMA_STAGES));
+        const uint16_t *As = cur, *Bs = cur + DTILE, *As2 = cur + 2 * DTILE;
+        const int64_t kvalid = g.K - kt * BK16;
+        if (kvalid < BK16) {
+            zero_rows_tail(cur, (int)kvalid);
+            if (BNN) zero_krows_tail(cur + DTILE, (int)kvalid);
+            else zero_rows_tail(cur + DTILE, (int)kvalid);
+            if (TWO) zero_rows_tail(cur + 2 * DTILE, (int)kvalid);
+            __builtin_amdgcn_s_waitcnt(0xc07f);    // lgkmcnt(0): the zeros are in LDS
+            __builtin_amdgcn_s_barrier();
+        }
+#pragma unroll
+        for (int kk = 0; kk < BK16; kk += 16) {
+            const int c = (kk >> 3) + (l >> 5);
+            const bf8v a0 = frag_rows(As, wm + (l & 31), c), a1 = frag_rows(As, wm + 32 + (l & 31), c);
+            bf8v b0, b1;
+            if (BNN) {
+                b0 = frag_krows(Bs, kk, wn);
+                b1 = frag_krows(Bs, kk, wn + 32);
+            } else {
+                b0 = frag_rows(Bs, wn + (l & 31), c);
+                b1 = frag_rows(Bs, wn + 32 + (l & 31), c);
+            }
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, acc[1][1], 0, 0, 0);
+            if (TWO) {
+                const bf8v c0 = frag_rows(As2, wm + (l & 31), c), c1 = frag_rows(As2, wm + 32 + (l & 31), c);
+                acc2[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c0, b0, acc2[0][0], 0, 0, 0);
+                acc2[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c0, b1, acc2[0][1], 0, 0, 0);
+                acc2[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c1, b0, acc2[1][0], 0, 0, 0);
+                acc2[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(c1, b1, acc2[1][1], 0, 0, 0);
+            }
+        }
+        if (threadIdx.x < 128) {
+            if (sqa) sa += row_sq_dma(As, threadIdx.x);
+            if (sqb && !BNN) sb += row_sq_dma(Bs, threadIdx.x);
+        }
+    }
+    // every wave is done reading LDS before the caller reuses it
+    __syncthreads();
+    if (threadIdx.x < 128) {
+        if (sqa) *sqa_out = sa;
+        if (sqb) *sqb_out = sb;
+    }
+}
+
+// Dispatch on the operand types: both bf16 -> bf16 matrix cores (pipelined
+// asynchronous loads when every operand has 16-byte aligned rows, register
+// staging otherwise), else fp32 matrix cores on widened operands.
+template <typename TA, typename TB, bool BNN, bool TWO, int NS>
 __device__ __forceinline__ void block_mma_any(const GemmArgs &g, int64_t m0, int64_t n0, bool veca, bool vecb,
                                               float *lds, f16v acc[2][2], f16v acc2[2][2], bool sqa,
                                               float *sqa_out, bool sqb, float *sqb_out) {
-    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2)
-        block_mma_bf16<BNN, TWO>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
-    else
+    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2) {
+        if (g.dma)
+            block_mma_bf16_dma<BNN, TWO, NS>(g, m0, n0, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
+        else
+            block_mma_bf16<BNN, TWO>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
+    } else {
         block_mma<TA, TB, BNN, TWO>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, sqa_out, sqb, sqb_out);
+    }
 }
+
+// LDS floats for the staging of a kernel: the larger of the two bf16 loops.
+template <typename TA, typename TB, bool TWO, int NS>
+constexpr size_t stage_lds_floats() {
+    constexpr size_t a = mma_lds_floats<TA, TB, TWO>();
+    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2) {
+        constexpr size_t b = dma_lds_floats<TWO, NS>();
+        return a > b ? a : b;
+    }
+    return a;
+}
+
+constexpr int STORE_STAGES = 3;
+constexpr int SWEEP_STAGES = 2;
 
 // XCD-aware tile order: work-group ids are dealt to the 8 XCDs round-robin,
 // so logical tile L is given to ids that share an XCD for consecutive L.
@@ -453,7 +688,7 @@ __global__ void __launch_bounds__(NTHR) gemm_store_kernel(GemmArgs g, int veca, 
     f16v acc[2][2], acc2[2][2];
     const bool sqa = (g.rownorm2 != nullptr) && (n0 == 0);
     float sa = 0.f, sb = 0.f;
-    block_mma_any<TA, TB, BNN, BIND>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
+    block_mma_any<TA, TB, BNN, BIND, STORE_STAGES>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
     if (sqa && threadIdx.x < 128 && m0 + threadIdx.x < g.M) g.rownorm2[m0 + threadIdx.x] = sa;
 
     TO *C = static_cast<TO *>(g.C);
@@ -491,7 +726,7 @@ constexpr int SS_STRIDE = BN + 1;
 template <typename TA, typename TB, bool SOFTMAX>
 __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int veca, int vecb) {
     extern __shared__ float lds[];
-    float *ss = lds + mma_lds_floats<TA, TB, false>();   // scores [BM][SS_STRIDE]
+    float *ss = lds + stage_lds_floats<TA, TB, false, SWEEP_STAGES>();   // scores [BM][SS_STRIDE]
     float *rq = ss + BM * SS_STRIDE;               // 1 / ||x|| per row (or 1)
     float *cn = rq + BM;                           // 1 / ||c|| per column (or 1)
     const int64_t nM = (g.M + BM - 1) / BM;
@@ -515,7 +750,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
         const bool sqa = g.cosine && g.qnorm2 == nullptr && nt == 0;
         const bool sqb = g.cosine && g.cnorm == nullptr;
         float sa = 0.f, sb = 0.f;
-        block_mma_any<TA, TB, false, false>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, sqb, &sb);
+        block_mma_any<TA, TB, false, false, SWEEP_STAGES>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, sqb, &sb);
         if (t < 128) {
             if (nt == 0) {
                 float q = 1.f;
@@ -630,7 +865,7 @@ hipError_t dispatch_store(bool b_nn, bool bind, const GemmArgs &a, bool veca, bo
     const int64_t nM = (a.M + BM - 1) / BM, nN = (a.N + BN - 1) / BN;
     const int64_t total = nM * nN;
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const size_t lds = (bind ? mma_lds_floats<TA, TB, true>() : mma_lds_floats<TA, TB, false>()) * sizeof(float);
+    const size_t lds = (bind ? stage_lds_floats<TA, TB, true, STORE_STAGES>() : stage_lds_floats<TA, TB, false, STORE_STAGES>()) * sizeof(float);
     if (b_nn) {
         if (bind) return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, true>, grid, lds, s, a, veca, vecb);
         return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, false>, grid, lds, s, a, veca, vecb);
@@ -643,7 +878,7 @@ template <typename TA, typename TB>
 hipError_t dispatch_rowsweep(bool softmax, const GemmArgs &a, bool veca, bool vecb, hipStream_t s) {
     const int64_t nM = (a.M + BM - 1) / BM;
     const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
-    const size_t lds = (mma_lds_floats<TA, TB, false>() + BM * SS_STRIDE + 2 * BM) * sizeof(float);
+    const size_t lds = (stage_lds_floats<TA, TB, false, SWEEP_STAGES>() + BM * SS_STRIDE + 2 * BM) * sizeof(float);
     if (softmax) return launch_with_lds(gemm_rowsweep_kernel<TA, TB, true>, grid, lds, s, a, veca, vecb);
     return launch_with_lds(gemm_rowsweep_kernel<TA, TB, false>, grid, lds, s, a, veca, vecb);
 }
@@ -661,8 +896,13 @@ bool vec_ok(const void *p, gs_dtype t, int64_t ld, int64_t extent) {
 }  // namespace
 
 hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,
-                       const GemmArgs &a, hipStream_t s) {
-    if (a.M == 0 || a.N == 0) return hipSuccess;
+                       const GemmArgs &a_in, hipStream_t s) {
+    if (a_in.M == 0 || a_in.N == 0) return hipSuccess;
+    GemmArgs a = a_in;
+    // asynchronous-load bf16 loop: every operand with 16-byte aligned rows
+    auto rows16 = [](const void *p, int64_t ld) { return aligned16(p) && ld % 8 == 0; };
+    a.dma = ta == GS_BF16 && tb == GS_BF16 && rows16(a.A, a.lda) && rows16(a.B, a.ldb) &&
+            (epi != EPI_BIND || rows16(a.A2, a.lda2));
     bool veca = vec_ok(a.A, ta, a.lda, a.K);
     if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
     const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);

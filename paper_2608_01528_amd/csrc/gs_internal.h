@@ -69,6 +69,7 @@ struct GemmArgs {
     float beta;
     int32_t *argmax;                   // EPI_SIM, nullable
     int write_out;                     // EPI_SIM: write scores to C
+    int dma;                           // set by launch_gemm: bf16 pipelined loop
 };
 
 hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,

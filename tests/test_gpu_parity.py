@@ -479,3 +479,70 @@ def test_soft_select_rejects_bad_groups():
     with pytest.raises(gsm.GramSpaceError) as e:
         gsm.gs_soft_select([{"P": P, "R": R, "S": out, "A": out}])
     assert e.value.status == gsm.GS_ERR_ARG
+
+
+# ------------------------- bf16 pipelined path (16-byte aligned leading dims)
+
+def nan_padded_bf16(a, ld):
+    """bf16 device matrix with leading dimension ld whose padding columns hold
+    NaN: the kernels may read them in 16-byte units but must not use them."""
+    a = np.asarray(a, np.float32)
+    full = np.full((a.shape[0], ld), np.nan, np.float32)
+    full[:, : a.shape[1]] = a
+    return dev(full, torch.bfloat16)[:, : a.shape[1]]
+
+
+@pytest.mark.parametrize("B,D,r", [(300, 1000, 130), (257, 1001, 45), (64, 200, 136)])
+def test_bf16_pipelined_project_reconstruct(B, D, r):
+    print("bf16 pipelined", B, D, r, flush=True)
+    C = rq_codebook("bipolar", r, D, 77)
+    Qo, Ro, kept, rr = oracle.compress(C)
+    assert rr == r
+    ld_d = (D + 7) // 8 * 8 + 8
+    ld_r = (r + 7) // 8 * 8
+    X = np.random.default_rng(B).standard_normal((B, D)).astype(np.float32)
+    Xb, Qb = wl.round_bf16(X), wl.round_bf16(Qo.astype(np.float32))
+    T, xn = gsm.gs_project(nan_padded_bf16(Xb, ld_d), nan_padded_bf16(Qb, ld_d), out_dtype=torch.float32,
+                           xnorm2=True)
+    torch.cuda.synchronize()
+    assert np.isfinite(host(T)).all()
+    assert rowrel(host(T), oracle.project(X, Qo)) <= TOL_BF16
+    np.testing.assert_allclose(host(xn), oracle.row_norms(Xb) ** 2, rtol=1e-4)
+    # reconstruct and bind (K x N operand) from in-span coordinates
+    P = wl.dirichlet_probs(B, r, 0.3, 9)
+    P2 = wl.dirichlet_probs(B, r, 0.3, 10)
+    To, To2 = (P.astype(np.float64) @ Ro), (P2.astype(np.float64) @ Ro)
+    Tb, Tb2 = wl.round_bf16(To.astype(np.float32)), wl.round_bf16(To2.astype(np.float32))
+    Xr = gsm.gs_reconstruct(nan_padded_bf16(Tb, ld_r), nan_padded_bf16(Qb, ld_d), out_dtype=torch.float32)
+    Y = gsm.gs_reconstruct(nan_padded_bf16(Tb, ld_r), nan_padded_bf16(Qb, ld_d),
+                           T2=nan_padded_bf16(Tb2, ld_r), bind="mul", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert np.isfinite(host(Xr)).all() and np.isfinite(host(Y)).all()
+    V, V2 = oracle.prob2vec(P, C), oracle.prob2vec(P2, C)
+    assert rowrel(host(Xr), V) <= TOL_BF16
+    assert rowrel(host(Y), oracle.bind(V, V2)) <= TOL_BF16
+
+
+@pytest.mark.parametrize("B,M,D", [(300, 150, 700), (200, 300, 640)])
+def test_bf16_pipelined_prob2vec_similarity(B, M, D):
+    C = rq_codebook("bipolar", M, D, 88, dup=0.1)
+    Qo, Ro, kept, r = oracle.compress(C)
+    ld_m, ld_r = (M + 7) // 8 * 8 + 8, (r + 7) // 8 * 8
+    P = wl.dirichlet_probs(B, M, 0.5, 3)
+    Pb, Rb = wl.round_bf16(P), wl.round_bf16(Ro.astype(np.float32))
+    T = gsm.gs_prob2vec(nan_padded_bf16(Pb, ld_m), nan_padded_bf16(Rb, ld_r), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert np.isfinite(host(T)).all()
+    V = oracle.prob2vec(P, C)
+    assert rowrel(host(T), oracle.project(V, Qo)) <= TOL_BF16
+    X = V + np.sqrt(0.1) * np.random.default_rng(1).standard_normal(V.shape)
+    Tx = wl.round_bf16(oracle.project(X, Qo).astype(np.float32))
+    qn = dev(oracle.row_norms(X) ** 2)
+    S, idx = gsm.gs_similarity(nan_padded_bf16(Tx, ld_r), nan_padded_bf16(Rb, ld_r), qnorm2=qn, mode="cosine")
+    A, _ = gsm.gs_attention(nan_padded_bf16(Tx, ld_r), nan_padded_bf16(Rb, ld_r), qnorm2=qn, beta=8.0)
+    torch.cuda.synchronize()
+    So = oracle.similarity(X, C, oracle.COSINE)
+    assert np.isfinite(host(S)).all() and np.isfinite(host(A)).all()
+    assert rowrel(host(S), So) <= TOL_BF16
+    assert rowrel(host(A), oracle.softmax(So, 8.0)) <= TOL_BF16
+    check_argmax(host(idx), So, band_rel=1e-2)
