@@ -175,8 +175,11 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
     const TB *B = static_cast<const TB *>(g.B);
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
-    const int nstage = TWO ? 3 : 2;   // operand tiles per buffer
-    float *buf[2] = {lds, lds + nstage * TILE_FLOATS};
+    // operand tiles per buffer; buffers are addressed as offsets from the
+    // LDS base (a pointer select would make the compiler fall back to flat
+    // addressing, whose waits also cover the in-flight global prefetch)
+    constexpr int nstage = TWO ? 3 : 2;
+    auto buf = [&](int64_t i) { return lds + (int)(i & 1) * (nstage * TILE_FLOATS); };
 
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -203,10 +206,10 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
     };
 
     fetch(0);
-    stash(buf[0]);
+    stash(buf(0));
     __syncthreads();
     for (int64_t kt = 0; kt < nk; ++kt) {
-        float *cur = buf[kt & 1];
+        float *cur = buf(kt);
         if (kt + 1 < nk) fetch(kt + 1);
         const float *As = cur, *Bs = cur + TILE_FLOATS, *As2 = cur + 2 * TILE_FLOATS;
 #pragma unroll
@@ -236,7 +239,7 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
                 for (int k = 0; k < BK; ++k) { float x = Bs[k * LDS_STRIDE + threadIdx.x]; sb += x * x; }
             }
         }
-        if (kt + 1 < nk) stash(buf[(kt + 1) & 1]);
+        if (kt + 1 < nk) stash(buf(kt + 1));
         __syncthreads();
     }
     if (threadIdx.x < 128) {
@@ -359,8 +362,8 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
     uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
-    const int nstage = TWO ? 3 : 2;
-    uint16_t *buf[2] = {lds, lds + nstage * BTILE};
+    constexpr int nstage = TWO ? 3 : 2;
+    auto buf = [&](int64_t i) { return lds + (int)(i & 1) * (nstage * BTILE); };
 
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -386,10 +389,10 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
     };
 
     fetch(0);
-    stash(buf[0]);
+    stash(buf(0));
     __syncthreads();
     for (int64_t kt = 0; kt < nk; ++kt) {
-        uint16_t *cur = buf[kt & 1];
+        uint16_t *cur = buf(kt);
         if (kt + 1 < nk) fetch(kt + 1);
         const uint16_t *As = cur, *Bs = cur + BTILE, *As2 = cur + 2 * BTILE;
 #pragma unroll
@@ -413,7 +416,7 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
             if (sqa) sa += row_sq_bf16(As, threadIdx.x);
             if (sqb) sb += row_sq_bf16(Bs, threadIdx.x);
         }
-        if (kt + 1 < nk) stash(buf[(kt + 1) & 1]);
+        if (kt + 1 < nk) stash(buf(kt + 1));
         __syncthreads();
     }
     if (threadIdx.x < 128) {
@@ -430,10 +433,13 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
 // is multiplied, with one barrier per step and no register staging.  Each
 // load instruction fills 1 KB of LDS in lane order, so the layout is chosen
 // through which 16-byte chunk each lane fetches:
-//   row tile   [128][64]: chunk c of row r sits at position c ^ (r & 7);
-//   k-row tile [64][128]: chunk c of k-row k sits at position c ^ (k & 15);
-// (XOR swizzles that make the MFMA fragment reads conflict-free without
-// padding).  Fragments of a k-row tile (b_nn) come from transpose reads
+//   row tile   [128][64]: chunk c of row r sits at position c ^ ((r >> 1) & 7);
+//   k-row tile [64][128]: chunk c of k-row k sits at position c ^ (4 (k & 3)).
+// A 128-byte row covers half of the 64 LDS banks, so 16 consecutive rows (one
+// 256-byte read phase of ds_read_b128) reach all 16 bank groups only if the
+// swizzle changes with r >> 1; a transpose read takes 4 chunks from each of 4
+// consecutive k-rows per 32 lanes, which the k-row swizzle spreads over all 64
+// banks.  Both make the fragment reads conflict-free without padding.  Fragments of a k-row tile (b_nn) come from transpose reads
 // (ds_read_b64_tr_b16), which hand each lane 4 consecutive k of one column.
 // Rows beyond the matrix reuse its last row (their results are discarded);
 // k beyond K is zeroed in LDS in the last step.  Requires 16-byte aligned
@@ -456,23 +462,37 @@ __device__ __forceinline__ void wait_vm() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Wait until at most `later` stages of OPS loads each (this wave's) are still
+// in flight; later is clamped to MAXS.
+template <int OPS, int MAXS>
+__device__ __forceinline__ void wait_stages(int64_t later) {
+    if constexpr (MAXS <= 0) {
+        wait_vm<0>();
+    } else {
+        if (later >= MAXS) wait_vm<OPS * MAXS>();
+        else wait_stages<OPS, MAXS - 1>(later);
+    }
+}
+
 __device__ __forceinline__ void dma16(const void *g, uint16_t *lds_wave_base) {
     __builtin_amdgcn_global_load_lds((const GS_G1 void *)g, (GS_L3 void *)lds_wave_base, 16, 0, 0);
 }
 
 // 16 load instructions of 1 KB per row tile: wave w issues blocks 4w .. 4w+3
-// (8 rows each).  Lane L of block b fetches row 8b + L/8, chunk (L%8) ^ (L/8).
+// (8 rows each).  Lane L of block b lands at row r = 8b + L/8, position L%8,
+// so it fetches chunk (L%8) ^ ((r >> 1) & 7) = (L%8) ^ (4 (b & 1) + L/16).
 __device__ __forceinline__ void dma_rows(const bf16_t *base, int64_t ld, int64_t row0, int64_t nrows,
                                          int64_t k0, int64_t K, uint16_t *tile) {
     const int L = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int rl = L >> 3, c = (L & 7) ^ rl;
-    int64_t kc = k0 + 8 * c;
+    const int rl = L >> 3;
     const int64_t klast = ((K - 1) >> 3) << 3;
-    if (kc > klast) kc = klast;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const int b = 4 * w + q;
+        const int c = (L & 7) ^ (4 * (q & 1) + (rl >> 1));
+        int64_t kc = k0 + 8 * c;
+        if (kc > klast) kc = klast;
         int64_t row = row0 + 8 * b + rl;
         if (row > nrows - 1) row = nrows - 1;
         dma16(base + row * ld + kc, tile + b * 512);
@@ -481,7 +501,7 @@ __device__ __forceinline__ void dma_rows(const bf16_t *base, int64_t ld, int64_t
 
 // 16 load instructions of 1 KB per k-row tile: wave w issues blocks 4w .. 4w+3
 // (4 k-rows each).  Lane L of block b fetches k-row 4b + L/16, chunk
-// (L%16) ^ (k-row % 16).
+// (L%16) ^ (4 (k-row % 4)).
 __device__ __forceinline__ void dma_krows(const bf16_t *base, int64_t ld, int64_t k0, int64_t K, int64_t n0,
                                           int64_t N, uint16_t *tile) {
     const int L = threadIdx.x & 63;
@@ -491,7 +511,7 @@ __device__ __forceinline__ void dma_krows(const bf16_t *base, int64_t ld, int64_
     for (int q = 0; q < 4; ++q) {
         const int b = 4 * w + q;
         const int kl = 4 * b + (L >> 4);
-        const int c = (L & 15) ^ (kl & 15);
+        const int c = (L & 15) ^ (4 * (kl & 3));
         int64_t nc = n0 + 8 * c;
         if (nc > nlast) nc = nlast;
         int64_t k = k0 + kl;
@@ -504,7 +524,7 @@ __device__ __forceinline__ void dma_krows(const bf16_t *base, int64_t ld, int64_
 __device__ __forceinline__ void zero_rows_tail(uint16_t *tile, int kvalid) {
     for (int e = threadIdx.x; e < 128 * 64; e += NTHR) {
         const int r = e >> 6, kl = e & 63;
-        if (kl >= kvalid) tile[r * 64 + ((((kl >> 3) ^ (r & 7))) << 3) + (kl & 7)] = 0;
+        if (kl >= kvalid) tile[r * 64 + ((((kl >> 3) ^ ((r >> 1) & 7))) << 3) + (kl & 7)] = 0;
     }
 }
 __device__ __forceinline__ void zero_krows_tail(uint16_t *tile, int kvalid) {
@@ -513,7 +533,7 @@ __device__ __forceinline__ void zero_krows_tail(uint16_t *tile, int kvalid) {
 }
 
 __device__ __forceinline__ bf8v frag_rows(const uint16_t *tile, int r, int c) {
-    return *reinterpret_cast<const bf8v *>(tile + r * 64 + ((c ^ (r & 7)) << 3));
+    return *reinterpret_cast<const bf8v *>(tile + r * 64 + ((c ^ ((r >> 1) & 7)) << 3));
 }
 
 // B fragment (8 consecutive k at kk + 8 (lane / 32), column n0w + lane % 32)
@@ -524,19 +544,22 @@ __device__ __forceinline__ bf8v frag_krows(const uint16_t *tile, int kk, int n0w
     const int n = n0w + 16 * (g & 1) + 4 * (a & 3);
     const int k = kk + 8 * (g >> 1) + (a >> 2);
     const int c = n >> 3;
-    const uint16_t *p0 = tile + k * 128 + ((c ^ (k & 15)) << 3) + (n & 7);
-    const uint16_t *p1 = tile + (k + 4) * 128 + ((c ^ ((k + 4) & 15)) << 3) + (n & 7);
+    const uint16_t *p0 = tile + k * 128 + ((c ^ (4 * (k & 3))) << 3) + (n & 7);
+    const uint16_t *p1 = tile + (k + 4) * 128 + ((c ^ (4 * (k & 3))) << 3) + (n & 7);
     const s4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((GS_L3 s4v *)(p0));
     const s4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((GS_L3 s4v *)(p1));
     const s4v both[2] = {lo, hi};
     return *reinterpret_cast<const bf8v *>(both);
 }
 
+// Sum of squares of row r of a row tile (all 8 chunks, started at a position
+// that differs between neighbouring row pairs so the 16-lane phases of the
+// reads do not collide on banks).
 __device__ __forceinline__ float row_sq_dma(const uint16_t *tile, int r) {
     float s = 0.f;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-        const uint4 u = *reinterpret_cast<const uint4 *>(tile + r * 64 + 8 * q);
+        const uint4 u = *reinterpret_cast<const uint4 *>(tile + r * 64 + 8 * ((q + (r >> 1)) & 7));
         const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -581,10 +604,9 @@ __device__ __forceinline__ void block_mma_bf16_dma(const GemmArgs &g, int64_t m0
     for (int s = 0; s < DMA_STAGES - 1; ++s)
         if (s < nk) issue(s);
     for (int64_t kt = 0; kt < nk; ++kt) {
-        // the loads of step kt are complete once at most the later stages'
-        // loads remain outstanding
-        if (kt + 1 < nk) wait_vm<OPS * (DMA_STAGES - 2)>();
-        else wait_vm<0>();
+        // the loads of step kt are complete once at most those of the later
+        // stages already issued (kt + 1 .. min(kt + NS - 2, nk - 1)) remain
+        wait_stages<OPS, DMA_STAGES - 2>(nk - 1 - kt);
         __builtin_amdgcn_s_barrier();
         if (kt + DMA_STAGES - 1 < nk) issue(kt + DMA_STAGES - 1);
         uint16_t *cur = stage((int)(kt % DMA_STAGES));
@@ -652,18 +674,19 @@ __device__ __forceinline__ void block_mma_any(const GemmArgs &g, int64_t m0, int
     }
 }
 
-// LDS floats for the staging of a kernel: the larger of the two bf16 loops.
+// LDS floats for the operand staging of a launch: the pipelined bf16 loop's
+// stages when it runs (dma), the register-staged loop's buffers otherwise.
 template <typename TA, typename TB, bool TWO, int NS>
-constexpr size_t stage_lds_floats() {
-    constexpr size_t a = mma_lds_floats<TA, TB, TWO>();
-    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2) {
-        constexpr size_t b = dma_lds_floats<TWO, NS>();
-        return a > b ? a : b;
-    }
-    return a;
+__host__ __device__ size_t stage_lds_floats(bool dma) {
+    if constexpr (sizeof(TA) == 2 && sizeof(TB) == 2)
+        if (dma) return dma_lds_floats<TWO, NS>();
+    return mma_lds_floats<TA, TB, TWO>();
 }
 
-constexpr int STORE_STAGES = 3;
+// Pipeline depth of the asynchronous loop: 4 stages (128 KiB) for a single
+// product, 3 (144 KiB) when a second A operand is staged.
+template <bool TWO>
+constexpr int store_stages() { return TWO ? 3 : 4; }
 constexpr int SWEEP_STAGES = 2;
 
 // XCD-aware tile order: work-group ids are dealt to the 8 XCDs round-robin,
@@ -688,7 +711,8 @@ __global__ void __launch_bounds__(NTHR) gemm_store_kernel(GemmArgs g, int veca, 
     f16v acc[2][2], acc2[2][2];
     const bool sqa = (g.rownorm2 != nullptr) && (n0 == 0);
     float sa = 0.f, sb = 0.f;
-    block_mma_any<TA, TB, BNN, BIND, STORE_STAGES>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false, &sb);
+    block_mma_any<TA, TB, BNN, BIND, store_stages<BIND>()>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa, false,
+                                                          &sb);
     if (sqa && threadIdx.x < 128 && m0 + threadIdx.x < g.M) g.rownorm2[m0 + threadIdx.x] = sa;
 
     TO *C = static_cast<TO *>(g.C);
@@ -726,7 +750,7 @@ constexpr int SS_STRIDE = BN + 1;
 template <typename TA, typename TB, bool SOFTMAX>
 __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int veca, int vecb) {
     extern __shared__ float lds[];
-    float *ss = lds + stage_lds_floats<TA, TB, false, SWEEP_STAGES>();   // scores [BM][SS_STRIDE]
+    float *ss = lds + stage_lds_floats<TA, TB, false, SWEEP_STAGES>(g.dma);   // scores [BM][SS_STRIDE]
     float *rq = ss + BM * SS_STRIDE;               // 1 / ||x|| per row (or 1)
     float *cn = rq + BM;                           // 1 / ||c|| per column (or 1)
     const int64_t nM = (g.M + BM - 1) / BM;
@@ -836,23 +860,11 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
     }
 }
 
-// Kernels whose dynamic LDS exceeds the default 64 KiB limit raise it once,
-// before their first launch (never inside a stream capture of a later call).
-hipError_t allow_lds(const void *kernel, size_t lds) {
-    static std::mutex mu;
-    static std::unordered_set<const void *> done;
-    std::lock_guard<std::mutex> lock(mu);
-    if (done.count(kernel)) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e == hipSuccess) done.insert(kernel);
-    return e;
-}
-
 template <typename K>
 hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const GemmArgs &a, int veca,
                            int vecb) {
     if (lds > 65536) {
-        hipError_t e = allow_lds(reinterpret_cast<const void *>(kernel), lds);
+        hipError_t e = raise_lds_limit(reinterpret_cast<const void *>(kernel), lds);
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(kernel, grid, dim3(NTHR), lds, s, a, veca, vecb);
@@ -865,7 +877,8 @@ hipError_t dispatch_store(bool b_nn, bool bind, const GemmArgs &a, bool veca, bo
     const int64_t nM = (a.M + BM - 1) / BM, nN = (a.N + BN - 1) / BN;
     const int64_t total = nM * nN;
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const size_t lds = (bind ? stage_lds_floats<TA, TB, true, STORE_STAGES>() : stage_lds_floats<TA, TB, false, STORE_STAGES>()) * sizeof(float);
+    const size_t lds = (bind ? stage_lds_floats<TA, TB, true, store_stages<true>()>(a.dma)
+                             : stage_lds_floats<TA, TB, false, store_stages<false>()>(a.dma)) * sizeof(float);
     if (b_nn) {
         if (bind) return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, true>, grid, lds, s, a, veca, vecb);
         return launch_with_lds(gemm_store_kernel<TA, TB, TO, true, false>, grid, lds, s, a, veca, vecb);
@@ -878,7 +891,7 @@ template <typename TA, typename TB>
 hipError_t dispatch_rowsweep(bool softmax, const GemmArgs &a, bool veca, bool vecb, hipStream_t s) {
     const int64_t nM = (a.M + BM - 1) / BM;
     const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
-    const size_t lds = (stage_lds_floats<TA, TB, false, SWEEP_STAGES>() + BM * SS_STRIDE + 2 * BM) * sizeof(float);
+    const size_t lds = (stage_lds_floats<TA, TB, false, SWEEP_STAGES>(a.dma) + BM * SS_STRIDE + 2 * BM) * sizeof(float);
     if (softmax) return launch_with_lds(gemm_rowsweep_kernel<TA, TB, true>, grid, lds, s, a, veca, vecb);
     return launch_with_lds(gemm_rowsweep_kernel<TA, TB, false>, grid, lds, s, a, veca, vecb);
 }
@@ -895,6 +908,22 @@ bool vec_ok(const void *p, gs_dtype t, int64_t ld, int64_t extent) {
 
 }  // namespace
 
+// Kernels whose dynamic LDS exceeds the default 64 KiB limit raise it once,
+// before their first launch, to the whole 160 KiB of a CU: a kernel's
+// launches differ in size (pipelined or register-staged operands), and the
+// attribute only permits; occupancy follows each launch's own size.
+hipError_t raise_lds_limit(const void *kernel, size_t lds) {
+    constexpr size_t LDS_MAX = 160 * 1024;
+    static std::mutex mu;
+    static std::unordered_set<const void *> done;
+    if (lds > LDS_MAX) return hipErrorInvalidValue;
+    std::lock_guard<std::mutex> lock(mu);
+    if (done.count(kernel)) return hipSuccess;
+    hipError_t e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)LDS_MAX);
+    if (e == hipSuccess) done.insert(kernel);
+    return e;
+}
+
 hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,
                        const GemmArgs &a_in, hipStream_t s) {
     if (a_in.M == 0 || a_in.N == 0) return hipSuccess;
@@ -903,6 +932,7 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
     auto rows16 = [](const void *p, int64_t ld) { return aligned16(p) && ld % 8 == 0; };
     a.dma = ta == GS_BF16 && tb == GS_BF16 && rows16(a.A, a.lda) && rows16(a.B, a.ldb) &&
             (epi != EPI_BIND || rows16(a.A2, a.lda2));
+    if (epi == EPI_STORE && a.dma && gemm256_fits(a)) return launch_gemm256(tout, b_nn, a, s);
     bool veca = vec_ok(a.A, ta, a.lda, a.K);
     if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
     const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);

@@ -111,6 +111,15 @@ def _mat(t: torch.Tensor, name: str):
     return _DT[t.dtype], max(t.stride(0), t.size(1))
 
 
+def alloc_rows(rows: int, cols: int, dtype, device) -> torch.Tensor:
+    """rows x cols matrix whose rows start on 16-byte boundaries (leading
+    dimension rounded up to a multiple of 16 bytes).  bf16 operands laid out
+    this way take the kernels' direct global-to-LDS load path."""
+    per = 16 // torch.empty((), dtype=dtype).element_size()
+    ld = max(1, (cols + per - 1) // per * per)
+    return torch.empty((rows, ld), dtype=dtype, device=device)[:, :cols]
+
+
 def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -135,8 +144,8 @@ def gs_compress(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dt
     ct, ldc = _mat(C, "C")
     M, D = C.shape
     dev = C.device
-    Q = torch.empty((M, D), dtype=q_dtype, device=dev)
-    R = torch.empty((M, M), dtype=r_dtype, device=dev)
+    Q = alloc_rows(M, D, q_dtype, dev)
+    R = alloc_rows(M, M, r_dtype, dev)
     kept = torch.empty(M, dtype=torch.int32, device=dev)
     cnorm = torch.empty(M, dtype=torch.float32, device=dev)
     need = compress_workspace_bytes(M, D)
@@ -145,8 +154,8 @@ def gs_compress(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dt
     base = workspace.data_ptr()
     off = (-base) % 256
     rank = ctypes.c_int32(0)
-    _check(lib().gs_compress(_ptr(C), ct, M, D, ldc, float(tol), _ptr(Q), _DT[q_dtype], D,
-                             _ptr(R), _DT[r_dtype], M, _ptr(kept), _ptr(cnorm), ctypes.byref(rank),
+    _check(lib().gs_compress(_ptr(C), ct, M, D, ldc, float(tol), _ptr(Q), _DT[q_dtype], Q.stride(0),
+                             _ptr(R), _DT[r_dtype], R.stride(0), _ptr(kept), _ptr(cnorm), ctypes.byref(rank),
                              ctypes.c_void_p(base + off), workspace.numel() - off, _stream()))
     r = rank.value
     return Q[:r], R[:, :r], r, kept[:r], cnorm
@@ -160,7 +169,7 @@ def gs_project(X: torch.Tensor, Q: torch.Tensor, out_dtype=None, xnorm2: bool = 
     B, D = X.shape
     r = Q.shape[0]
     if out is None:
-        out = torch.empty((B, r), dtype=out_dtype or X.dtype, device=X.device)
+        out = alloc_rows(B, r, out_dtype or X.dtype, X.device)
     tt, ldt = _mat(out, "T")
     xn = None
     if xnorm2:
@@ -177,7 +186,7 @@ def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Ten
     B, M = P.shape
     r = R.shape[1]
     if out is None:
-        out = torch.empty((B, r), dtype=out_dtype or P.dtype, device=P.device)
+        out = alloc_rows(B, r, out_dtype or P.dtype, P.device)
     tt, ldt = _mat(out, "T")
     _check(lib().gs_prob2vec(_ptr(P), pt, B, M, ldp, _ptr(R), rt, r, ldr, _ptr(out), tt, ldt, _stream()))
     return out
@@ -216,7 +225,7 @@ def gs_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode
     _, lda = _mat(A, "A")
     O, ot, ldo = None, GS_F32, r
     if weighted_sum:
-        O = o_out if o_out is not None else torch.empty((B, r), dtype=out_dtype or T.dtype, device=T.device)
+        O = o_out if o_out is not None else alloc_rows(B, r, out_dtype or T.dtype, T.device)
         ot, ldo = _mat(O, "O")
     _check(lib().gs_attention(_ptr(T), tt, B, r, ldt, _ptr(R), rt, M, ldr, _ptr(qnorm2), _ptr(cnorm),
                               _mode(mode), float(scale), float(beta), _ptr(A), lda, _ptr(O), ot, ldo,
@@ -239,7 +248,7 @@ def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = N
     elif bind not in (None, "none", GS_BIND_NONE):
         raise ValueError("bind must be None or 'mul'")
     if out is None:
-        out = torch.empty((B, D), dtype=out_dtype or T.dtype, device=T.device)
+        out = alloc_rows(B, D, out_dtype or T.dtype, T.device)
     xt, ldx = _mat(out, "X")
     _check(lib().gs_reconstruct(_ptr(T), tt, B, r, ldt, _ptr(T2), ldt2, b, _ptr(Q), qt, D, ldq,
                                 _ptr(out), xt, ldx, _stream()))

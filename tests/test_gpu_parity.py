@@ -546,3 +546,69 @@ def test_bf16_pipelined_prob2vec_similarity(B, M, D):
     assert rowrel(host(S), So) <= TOL_BF16
     assert rowrel(host(A), oracle.softmax(So, 8.0)) <= TOL_BF16
     check_argmax(host(idx), So, band_rel=1e-2)
+
+
+# ------------------------ bf16 large-tile path (>= 256 tiles of 256 x 256)
+#
+# Products large enough for the 256 x 256 tiles, with ragged M and N, K tails
+# that are neither multiples of the K-step (32) nor of 8, NaN-filled row
+# padding, and both output types.  Q and R are arbitrary here: project,
+# prob2vec and reconstruct are plain products of their operands.  Rows are
+# sampled: the first and last, the tile boundaries and random rows.
+
+def _tile_rows(B, seed):
+    fixed = [0, 1, 255, 256, 511, 512, B // 2, B - 2, B - 1]
+    rnd = np.random.default_rng(seed).choice(B, size=24, replace=False)
+    return np.array(sorted(set(f for f in fixed if f < B) | set(int(x) for x in rnd)))
+
+
+def _bf16_mat(rows, cols, seed, scale=1.0):
+    return wl.round_bf16((scale * np.random.default_rng(seed).standard_normal((rows, cols))).astype(np.float32))
+
+
+@pytest.mark.parametrize("D", [300, 4100])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_bf16_large_tile_project(D, out_dtype):
+    B, r = 8200, 2000
+    print("large-tile project", B, D, r, out_dtype, flush=True)
+    X, Q = _bf16_mat(B, D, 1), _bf16_mat(r, D, 2, 1 / np.sqrt(D))
+    ld = (D + 7) // 8 * 8
+    T, xn = gsm.gs_project(nan_padded_bf16(X, ld), nan_padded_bf16(Q, ld), out_dtype=out_dtype, xnorm2=True)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 3)
+    Tr = host(T[rows])
+    assert np.isfinite(Tr).all()
+    tol = TOL_BF16 if out_dtype == torch.bfloat16 else TOL_F32
+    assert rowrel(Tr, oracle.project(X[rows], Q)) <= tol
+    np.testing.assert_allclose(host(xn), oracle.row_norms(X) ** 2, rtol=1e-4)
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_bf16_large_tile_reconstruct(out_dtype):
+    B, r, D = 2100, 45, 7700
+    print("large-tile reconstruct", B, r, D, out_dtype, flush=True)
+    T, Q = _bf16_mat(B, r, 4), _bf16_mat(r, D, 5)
+    X = gsm.gs_reconstruct(nan_padded_bf16(T, (r + 7) // 8 * 8), nan_padded_bf16(Q, (D + 7) // 8 * 8 + 8),
+                           out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 6)
+    Xr = host(X[rows])
+    assert np.isfinite(Xr).all()
+    tol = TOL_BF16 if out_dtype == torch.bfloat16 else TOL_F32
+    assert rowrel(Xr, oracle.reconstruct(T[rows], Q)) <= tol
+    # every column block, including the ragged last one, on a full row
+    assert rowrel(host(X[B - 1:B]), oracle.reconstruct(T[B - 1:B], Q)) <= tol
+
+
+def test_bf16_large_tile_prob2vec():
+    B, M, r = 8200, 2050, 2000
+    print("large-tile prob2vec", B, M, r, flush=True)
+    P = wl.round_bf16(wl.dirichlet_probs(B, M, 0.5, 7))
+    R = _bf16_mat(M, r, 8)
+    T = gsm.gs_prob2vec(nan_padded_bf16(P, (M + 7) // 8 * 8), nan_padded_bf16(R, (r + 7) // 8 * 8),
+                        out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 9)
+    Tr = host(T[rows])
+    assert np.isfinite(Tr).all()
+    assert rowrel(Tr, oracle.prob2vec(P[rows], R)) <= TOL_F32
