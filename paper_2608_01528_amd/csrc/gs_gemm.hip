@@ -932,7 +932,7 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
     auto rows16 = [](const void *p, int64_t ld) { return aligned16(p) && ld % 8 == 0; };
     a.dma = ta == GS_BF16 && tb == GS_BF16 && rows16(a.A, a.lda) && rows16(a.B, a.ldb) &&
             (epi != EPI_BIND || rows16(a.A2, a.lda2));
-    if (epi == EPI_STORE && a.dma && gemm256_fits(a)) return launch_gemm256(tout, b_nn, a, s);
+    if (epi == EPI_STORE && a.dma && gemm256_fits(a, b_nn)) return launch_gemm256(tout, b_nn, a, s);
     bool veca = vec_ok(a.A, ta, a.lda, a.K);
     if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
     const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);

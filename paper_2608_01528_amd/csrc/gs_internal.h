@@ -78,7 +78,7 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
 // 256 x 256-tile bf16 x bf16 product with a plain store (and optional row
 // norms of A); needs 16-byte aligned operand rows.  gemm256_fits tells whether
 // the product is large enough to fill the chip with such tiles.
-bool gemm256_fits(const GemmArgs &a);
+bool gemm256_fits(const GemmArgs &a, bool b_nn);
 hipError_t launch_gemm256(gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s);
 
 // Raise a kernel's dynamic LDS limit (once per kernel, to a whole CU's LDS);
