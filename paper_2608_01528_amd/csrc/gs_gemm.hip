@@ -207,7 +207,7 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
 
     fetch(0);
     stash(buf(0));
-    __syncthreads();
+    lds_barrier();
     for (int64_t kt = 0; kt < nk; ++kt) {
         float *cur = buf(kt);
         if (kt + 1 < nk) fetch(kt + 1);
@@ -240,7 +240,7 @@ __device__ __forceinline__ void block_mma(const GemmArgs &g, int64_t m0, int64_t
             }
         }
         if (kt + 1 < nk) stash(buf(kt + 1));
-        __syncthreads();
+        lds_barrier();
     }
     if (threadIdx.x < 128) {
         if (sqa) *sqa_out = sa;
@@ -390,7 +390,7 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
 
     fetch(0);
     stash(buf(0));
-    __syncthreads();
+    lds_barrier();
     for (int64_t kt = 0; kt < nk; ++kt) {
         uint16_t *cur = buf(kt);
         if (kt + 1 < nk) fetch(kt + 1);
@@ -417,7 +417,7 @@ __device__ __forceinline__ void block_mma_bf16(const GemmArgs &g, int64_t m0, in
             if (sqb) sb += row_sq_bf16(Bs, threadIdx.x);
         }
         if (kt + 1 < nk) stash(buf(kt + 1));
-        __syncthreads();
+        lds_barrier();
     }
     if (threadIdx.x < 128) {
         if (sqa) *sqa_out = sa;
@@ -650,7 +650,7 @@ __device__ __forceinline__ void block_mma_bf16_dma(const GemmArgs &g, int64_t m0
         }
     }
     // every wave is done reading LDS before the caller reuses it
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x < 128) {
         if (sqa) *sqa_out = sa;
         if (sqb) *sqb_out = sb;
@@ -762,6 +762,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
     const int l = t & 63, w = t >> 6;
     const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
     float *out = static_cast<float *>(g.C);
+    const bool vec_out = (reinterpret_cast<uintptr_t>(out) & 15) == 0 && g.ldc % 4 == 0;
 
     // running row state, identical in both threads of a pair
     const int prow = t >> 1, half = t & 1;
@@ -791,7 +792,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
             }
             cn[t] = c;
         }
-        __syncthreads();
+        lds_barrier();
         // scores -> LDS and (optionally) global
         const float mul = SOFTMAX ? g.scale * g.beta : g.scale;
 #pragma unroll
@@ -803,14 +804,29 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int rl = wm + 32 * i + acc_row(r, l);
-                    const int64_t row = m0 + rl;
-                    float v = mul * acc[i][j][r] * rq[rl] * cn[cl];
+                    const float v = mul * acc[i][j][r] * rq[rl] * cn[cl];
                     ss[rl * SS_STRIDE + cl] = (col < g.N) ? v : -INFINITY;
-                    if ((SOFTMAX || g.write_out) && row < g.M && col < g.N)
-                        out[row * g.ldc + col] = v;
                 }
             }
-        __syncthreads();
+        lds_barrier();
+        if (SOFTMAX || g.write_out) {
+            // the block's scores leave from the LDS tile, four columns per
+            // thread: rows t / 32 + 8 q, columns 4 (t % 32) .. + 3
+            const int c4 = 4 * (t & 31);
+            const int64_t col = n0 + c4;
+            for (int q = 0; q < 16; ++q) {
+                const int rl = (t >> 5) + 8 * q;
+                const int64_t row = m0 + rl;
+                if (row >= g.M || col >= g.N) continue;
+                const float *src = ss + rl * SS_STRIDE + c4;
+                float *dst = out + row * g.ldc + col;
+                if (vec_out && col + 4 <= g.N) {
+                    *reinterpret_cast<f4v *>(dst) = f4v{src[0], src[1], src[2], src[3]};
+                } else {
+                    for (int e = 0; e < 4 && col + e < g.N; ++e) dst[e] = src[e];
+                }
+            }
+        }
         // fold this column block into the running row state
         const int ncols = (int)((g.N - n0 < BN) ? (g.N - n0) : BN);
         float bm = -INFINITY, bs = 0.f;
@@ -837,7 +853,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
             if (om > bm || (om == bm && oi < bi)) { bm = om; bi = oi; }
             if (bm > run_max) { run_max = bm; run_idx = (int)(n0 + bi); }
         }
-        __syncthreads();   // ss and the staged tiles are reused by the next block
+        lds_barrier();   // ss and the staged tiles are reused by the next block
     }
 
     if (!SOFTMAX) {
@@ -850,7 +866,8 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
         rmax[prow] = run_max;
         rinv[prow] = 1.f / run_sum;
     }
-    __threadfence_block();
+    // the second sweep reads scores that other threads stored to global
+    // memory: a full barrier (their stores complete and visible)
     __syncthreads();
     const int64_t rows = (g.M - m0 < BM) ? (g.M - m0) : BM;
     for (int64_t r = 0; r < rows; ++r) {

@@ -36,6 +36,16 @@ __device__ __forceinline__ uint16_t f64_to_bf16(double d) {
     return f32_to_bf16(f);
 }
 
+// Work-group barrier for hand-offs through LDS: every thread's LDS accesses
+// before it are complete and visible after it.  Global stores still in flight
+// are not waited for (__syncthreads would wait for them to complete, which
+// serialises the store phases of a work-group on memory latency).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <typename T> __device__ __forceinline__ float ld_f32(const T *p, int64_t i);
 template <> __device__ __forceinline__ float ld_f32<float>(const float *p, int64_t i) { return p[i]; }
 template <> __device__ __forceinline__ float ld_f32<bf16_t>(const bf16_t *p, int64_t i) {

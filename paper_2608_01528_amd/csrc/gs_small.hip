@@ -18,6 +18,7 @@
 namespace gs {
 namespace {
 
+
 constexpr int ROWS = 256;                 // batch rows per work-group (separate calls)
 #ifndef SOFT_RPT
 #define SOFT_RPT 1
@@ -249,14 +250,14 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
     float x[MB];
     if (MODE == MODE_P2V) {
         row_prob2vec<MB>(tile + t * M, M, R, x);
-        __syncthreads();   // the tile is reused for the outputs
+        lds_barrier();   // the tile is reused for the outputs
         regs_to_tile<MB>(x, r, tile);
-        __syncthreads();
+        lds_barrier();
         tile_store<TO, ROWS>(static_cast<TO *>(a.Out), a.ldout, b0, nrow, r, tile);
         return;
     }
     tile_to_regs<MB>(tile, r, x);
-    __syncthreads();   // the tile is reused for the outputs
+    lds_barrier();   // the tile is reused for the outputs
     float n2 = 0.f;
 #pragma unroll
     for (int k = 0; k < MB; ++k) n2 += x[k] * x[k];
@@ -273,19 +274,19 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
     if (MODE == MODE_SIM) {
         if (a.argmax && t < nrow) a.argmax[b0 + t] = bi;
         if (!a.Out) return;
-        __syncthreads();
+        lds_barrier();
         tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
         return;
     }
     row_softmax(srow, M, 1.f, best);
-    __syncthreads();
+    lds_barrier();
     tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
     if (!a.O) return;
     float o[MB];
     row_prob2vec<MB>(srow, M, R, o);
-    __syncthreads();
+    lds_barrier();
     regs_to_tile<MB>(o, r, tile);
-    __syncthreads();
+    lds_barrier();
     tile_store<TO, ROWS>(static_cast<TO *>(a.O), a.ldo, b0, nrow, r, tile);
 }
 
@@ -301,7 +302,7 @@ __global__ void __launch_bounds__(ROWS) small_kernel(SmallArgs a) {
     tile_load<TI, ROWS>(static_cast<const TI *>(a.In), a.ldin, b0, nrow, (MODE == MODE_P2V) ? M : r, tile);
     if (MODE != MODE_P2V) stage_norms<TI, ROWS>(R, a.ldr, M, r, a.cnorm, a.cosine != 0, MB, Rn);
     stage_padded<TI, MB, ROWS>(R, a.ldr, M, r, Rs);
-    __syncthreads();
+    lds_barrier();
     small_body<TI, TO, MODE, MB>(a, LdsRows<MB>{Rs}, Rn, tile);
 }
 
@@ -393,16 +394,16 @@ __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G
         for (int k = 0; k < MB; ++k) n2 += x[u][k] * x[u][k];   // in span: ||v|| = ||t||
         q[u] = a.cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;
     }
-    __syncthreads();   // the tile is reused for the outputs
+    lds_barrier();   // the tile is reused for the outputs
     if (G.T) {
 #pragma unroll
         for (int u = 0; u < RPT; ++u)
 #pragma unroll
             for (int k = 0; k < MB; ++k)
                 if (k < r) tile[(t + u * SROWS) * r + k] = x[u][k];
-        __syncthreads();
+        lds_barrier();
         tile_store<TT, SROWS>(static_cast<TT *>(G.T), G.ldt, b0, nrow, r, tile);
-        __syncthreads();
+        lds_barrier();
     }
     float best[RPT];
     int bi[RPT];
@@ -413,13 +414,13 @@ __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G
             if (t + u * SROWS < nrow) G.argmax[b0 + t + u * SROWS] = bi[u];
     }
     if (G.S) {
-        __syncthreads();
+        lds_barrier();
         tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
     }
     if (G.A) {
         // attention weights: softmax of beta times the same scores; the
         // maximum of beta * s is taken after scaling (beta may be negative)
-        if (G.S) __syncthreads();   // S has left the tile before it is overwritten
+        if (G.S) lds_barrier();   // S has left the tile before it is overwritten
 #pragma unroll
         for (int u = 0; u < RPT; ++u) {
             float *srow = tile + (t + u * SROWS) * M;
@@ -427,7 +428,7 @@ __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G
             for (int j = 0; j < M; ++j) mx = fmaxf(mx, a.beta * srow[j]);
             row_softmax(srow, M, a.beta, mx);
         }
-        __syncthreads();
+        lds_barrier();
         tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
     }
 }
@@ -479,7 +480,7 @@ __global__ void __launch_bounds__(SROWS) soft_select_kernel(SoftArgs a) {
     } else {
         tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
     }
-    __syncthreads();
+    lds_barrier();
     switch (MB) {
         case 8: soft_block<TI, TT, 8>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
         case 16: soft_block<TI, TT, 16>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
