@@ -18,6 +18,13 @@
  * r is the algebraic rank of C (Sec. 3.2).  All matrices are row-major with a
  * leading dimension (elements between consecutive rows) ld >= columns.
  *
+ * Row padding.  When both bf16 operands of a contraction have 16-byte aligned
+ * rows (base address 16-byte aligned and ld a multiple of 8), rows are read
+ * in 16-byte units, up to column ceil(columns / 8) * 8 - 1 <= ld - 1: the
+ * row's padding may be read but never contributes (it may hold anything,
+ * NaN included).  Such operands take the asynchronous-load paths; any other
+ * layout is accepted as well.
+ *
  * Memory and ownership.  Every matrix argument is a device pointer (HIP
  * device memory of the current device) unless marked HOST.  The caller
  * allocates every buffer, including workspace; the library allocates no
