@@ -869,12 +869,7 @@ __global__ void __launch_bounds__(NTHR) gemm_rowsweep_kernel(GemmArgs g, int vec
     // the second sweep reads scores that other threads stored to global
     // memory: a full barrier (their stores complete and visible)
     __syncthreads();
-    const int64_t rows = (g.M - m0 < BM) ? (g.M - m0) : BM;
-    for (int64_t r = 0; r < rows; ++r) {
-        float *orow = out + (m0 + r) * g.ldc;
-        const float mx = rmax[r], iv = rinv[r];
-        for (int64_t c = t; c < g.N; c += NTHR) orow[c] = __expf(orow[c] - mx) * iv;
-    }
+    softmax_rows(out, g.ldc, m0, (g.M - m0 < BM) ? (g.M - m0) : BM, g.N, rmax, rinv, vec_out, NTHR);
 }
 
 template <typename K>
@@ -965,6 +960,8 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
         return hipErrorInvalidValue;
     }
     const bool sm = epi == EPI_SOFTMAX;
+    if (a.dma && !b_nn && (sm || a.write_out) && gemm256_fits(a, false)) return launch_scores256(a, sm, s);
+    if (a.dma && !b_nn && sweep256_fits(a)) return launch_sweep256(sm, a, s);
     if (!bf_a && !bf_b) return dispatch_rowsweep<float, float>(sm, a, veca, vecb, s);
     if (bf_a && bf_b) return dispatch_rowsweep<bf16_t, bf16_t>(sm, a, veca, vecb, s);
     return hipErrorInvalidValue;

@@ -47,6 +47,7 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
 typedef short s4v __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f4v __attribute__((ext_vector_type(4)));
 #define AS_L __attribute__((address_space(3)))
 
 // s_waitcnt with vmcnt <= n (expcnt and lgkmcnt unconstrained), gfx9 encoding.
@@ -92,9 +93,9 @@ __device__ __forceinline__ void dma16(const rsrc_t &r, int64_t byte_off, const u
 // starts at the tile's first row; rows past the last one (nrows rows from
 // there) reuse it.
 __device__ __forceinline__ void dma_rows(const rsrc_t &r, int64_t ld, int64_t nrows, int64_t k0, int64_t K,
-                                         uint16_t *tile) {
-    const int L = threadIdx.x & 63;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+                                         uint16_t *tile, int tid) {
+    const int L = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t klast = ((K - 1) >> 3) << 3;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -113,9 +114,9 @@ __device__ __forceinline__ void dma_rows(const rsrc_t &r, int64_t ld, int64_t nr
 // fetches chunk (L%32) ^ (4 (k-row % 4)).  `r` starts at the tile's first
 // column; ncols columns exist from there.
 __device__ __forceinline__ void dma_krows(const rsrc_t &r, int64_t ld, int64_t k0, int64_t K, int64_t ncols,
-                                          uint16_t *tile) {
-    const int L = threadIdx.x & 63;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+                                          uint16_t *tile, int tid) {
+    const int L = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t nlast = ((ncols - 1) >> 3) << 3;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -137,8 +138,8 @@ __device__ __forceinline__ bf8v frag_rows(const uint16_t *tile, int r, int c) {
 
 // K x N B fragment (8 consecutive k at kk + 8 (lane / 32), column
 // n0w + lane % 32) by two transpose reads of 4 k each.
-__device__ __forceinline__ bf8v frag_krows(const uint16_t *tile, int kk, int n0w) {
-    const int l = threadIdx.x & 63;
+__device__ __forceinline__ bf8v frag_krows(const uint16_t *tile, int kk, int n0w, int tid) {
+    const int l = tid & 63;
     const int g = l >> 4, a = l & 15;
     const int n = n0w + 16 * (g & 1) + 4 * (a & 3);
     const int k = kk + 8 * (g >> 1) + (a >> 2);
@@ -169,31 +170,25 @@ template <> __device__ __forceinline__ bf16_t to_out<bf16_t>(float v) {
 // Row of the output held by accumulator register g of a 32x32 block, for lane l.
 __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 * (l >> 5) + (g & 3); }
 
-template <typename TO, bool BNN>
-__global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
-gemm256_kernel(GemmArgs g) {
-    extern __shared__ float lds_f[];
-    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
-    const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
-    const int64_t total = nM * nN;
-    // Work-group ids are dealt to the 8 XCDs round robin: XCD x runs the
-    // logical tiles [x per, (x + 1) per) in order.
-    const int64_t per = (total + 7) / 8;
-    const int64_t lt = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
-    if (lt >= total) return;
-    // Logical order: groups of GROUP_M m-tiles take each n-tile in turn, so the
-    // tiles one XCD runs together share A row blocks and B column blocks in L2.
-    const int64_t grp = lt / (GROUP_M * nN);
-    const int64_t first_m = grp * GROUP_M;
-    const int64_t gm = (nM - first_m < GROUP_M) ? (nM - first_m) : GROUP_M;
-    const int64_t within = lt - grp * GROUP_M * nN;
-    const int64_t m0 = (first_m + within % gm) * TM;
-    const int64_t n0 = (within / gm) * TN;
-
+// The 256 x 256 block (m0, n0) of A * Bop, accumulated into acc (zeroed
+// here).  Wave w owns rows wm = 128 (w / 2) .. + 127 and columns
+// wn = 128 (w % 2) .. + 127 of the block.  When SQA && sqa, sq[i] gathers this
+// lane's share of sum_k A[row, k]^2 for row wm + 32 i + lane % 32 (lanes l
+// and l + 32 hold the two k-halves of a row); when SQB && sqb, sb[j] does the same
+// for row wn + 32 j + lane % 32 of an N x K operand.  Returns once the last
+// MFMA is issued; the stages stay in use until the caller's next barrier.
+template <bool BNN, bool SQA, bool SQB>
+__device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n0, uint16_t *lds,
+                                        f16v acc[4][4], bool sqa, float sq[4], bool sqb, float sb[4],
+                                        int tid) {
+    const int l = tid & 63, w = tid >> 6;
+    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f16v{};
     const bf16_t *A = static_cast<const bf16_t *>(g.A);
     const bf16_t *B = static_cast<const bf16_t *>(g.B);
-    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
     // buffer resources over exactly what this tile reads (row slices end at
     // column ceil(K / 8) * 8, k-row slices at column ceil(N / 8) * 8)
     const int64_t k8 = (g.K + 7) / 8 * 8, n8 = (g.N + 7) / 8 * 8;
@@ -212,23 +207,14 @@ gemm256_kernel(GemmArgs g) {
         cols_b = 0;
     }
 
-    f16v acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f16v{};
-    // row norms of A from the fragments already in registers: the waves of
-    // the left column (wn == 0) of the tiles with n0 == 0
-    const bool sqa = g.rownorm2 != nullptr && n0 == 0 && (w & 1) == 0;
-    float sq[4] = {0.f, 0.f, 0.f, 0.f};
 
     const int64_t nk = (g.K + TK - 1) / TK;
     auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
     auto issue = [&](int64_t kt) {
         uint16_t *st = stage(kt);
-        dma_rows(ra, g.lda, rows_a, kt * TK, g.K, st);
-        if (BNN) dma_krows(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT);
-        else dma_rows(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT);
+        dma_rows(ra, g.lda, rows_a, kt * TK, g.K, st, tid);
+        if (BNN) dma_krows(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid);
+        else dma_rows(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid);
     };
     struct Frags { bf8v a[4], b[4]; };
     auto load_frags = [&](const uint16_t *st, int kk, Frags &f) {
@@ -237,7 +223,7 @@ gemm256_kernel(GemmArgs g) {
         for (int i = 0; i < 4; ++i) f.a[i] = frag_rows(st, wm + 32 * i + (l & 31), c);
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            f.b[j] = BNN ? frag_krows(st + OPT, kk, wn + 32 * j) : frag_rows(st + OPT, wn + 32 * j + (l & 31), c);
+            f.b[j] = BNN ? frag_krows(st + OPT, kk, wn + 32 * j, tid) : frag_rows(st + OPT, wn + 32 * j + (l & 31), c);
     };
     // In the last K-step, zero the fragment elements at k >= K (both operands:
     // what lies there in LDS is row padding or a re-read chunk, possibly NaN).
@@ -260,9 +246,13 @@ gemm256_kernel(GemmArgs g) {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
-        if (sqa) {
+        if (SQA && sqa) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) sq[i] += sum_sq(f.a[i]);
+        }
+        if (SQB && sqb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sb[j] += sum_sq(f.b[j]);
         }
     };
 
@@ -322,7 +312,77 @@ gemm256_kernel(GemmArgs g) {
         mma(f1);
     }
 
-    if (sqa) {
+}
+
+// SCALED: similarity scores instead of the plain product (fp32 output, B
+// stored N x K): out = scale * acc / (||x_row|| ||c_col||) for cosine (row
+// norms from qnorm2 or from the A fragments, column norms from cnorm or from
+// the B fragments), scale * acc for dot.
+template <typename TO, bool BNN, bool SCALED>
+__global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
+gemm256_kernel(GemmArgs g) {
+    extern __shared__ float lds_f[];
+    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
+    const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
+    const int64_t total = nM * nN;
+    // Work-group ids are dealt to the 8 XCDs round robin: XCD x runs the
+    // logical tiles [x per, (x + 1) per) in order.
+    const int64_t per = (total + 7) / 8;
+    const int64_t lt = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (lt >= total) return;
+    // Logical order: groups of GROUP_M m-tiles take each n-tile in turn, so the
+    // tiles one XCD runs together share A row blocks and B column blocks in L2.
+    const int64_t grp = lt / (GROUP_M * nN);
+    const int64_t first_m = grp * GROUP_M;
+    const int64_t gm = (nM - first_m < GROUP_M) ? (nM - first_m) : GROUP_M;
+    const int64_t within = lt - grp * GROUP_M * nN;
+    const int64_t m0 = (first_m + within % gm) * TM;
+    const int64_t n0 = (within / gm) * TN;
+
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
+    f16v acc[4][4];
+    // row norms of A from the fragments already in registers (the waves of
+    // the left column, wn == 0): for the rownorm2 side output of the tiles
+    // with n0 == 0, or for cosine scores without qnorm2; column norms of B
+    // likewise (the waves of the top row, wm == 0) for cosine without cnorm
+    const bool sqa = SCALED ? (g.cosine && g.qnorm2 == nullptr && (w & 1) == 0)
+                            : (g.rownorm2 != nullptr && n0 == 0 && (w & 1) == 0);
+    const bool sqb = SCALED && g.cosine && g.cnorm == nullptr && (w >> 1) == 0;
+    float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[4] = {0.f, 0.f, 0.f, 0.f};
+    mma_256<BNN, true, SCALED>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
+
+    float *rq = lds_f + LDS_BYTES / sizeof(float);   // SCALED: scale / ||x|| per row of the tile
+    float *cn = rq + TM;                             // SCALED: 1 / ||c|| per column of the tile
+    if (SCALED) {
+        const int t = threadIdx.x;
+        if (!g.cosine) {
+            rq[t] = g.scale;
+            cn[t] = 1.f;
+        } else {
+            if (g.qnorm2) {
+                const float n2 = (m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f;
+                rq[t] = (n2 > 0.f) ? g.scale / sqrtf(n2) : 0.f;
+            } else if (sqa) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float n2 = sq[i] + __shfl_xor(sq[i], 32);
+                    if (l < 32) rq[wm + 32 * i + l] = (n2 > 0.f) ? g.scale / sqrtf(n2) : 0.f;
+                }
+            }
+            if (g.cnorm) {
+                const float c = (n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f;
+                cn[t] = (c > 0.f) ? 1.f / c : 0.f;
+            } else if (sqb) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float n2 = sb[j] + __shfl_xor(sb[j], 32);
+                    if (l < 32) cn[wn + 32 * j + l] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+                }
+            }
+        }
+    }
+    if (!SCALED && sqa) {
         // lanes l and l + 32 hold the two k-halves of row wm + 32 i + l % 32
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -361,7 +421,12 @@ gemm256_kernel(GemmArgs g) {
 #pragma unroll 4
             for (int id = l; id < 64 * CPR; id += 64) {
                 const int rr = id / CPR, cc = id % CPR;
-                const u32x4 v = *reinterpret_cast<const u32x4 *>(region + rr * STRIDE + cc * 16);
+                u32x4 v = *reinterpret_cast<const u32x4 *>(region + rr * STRIDE + cc * 16);
+                if (SCALED) {
+                    const f4v x = __builtin_bit_cast(f4v, v) * rq[wm + 64 * h + rr] *
+                                  *reinterpret_cast<const f4v *>(cn + wn + cc * EPC);
+                    v = __builtin_bit_cast(u32x4, x);
+                }
                 TO *dst = C + (m0 + wm + 64 * h + rr) * g.ldc + (n0 + wn + cc * EPC);
                 // streaming store: the output is not re-read by this kernel and
                 // should not displace the operand slices other tiles share in L2
@@ -372,27 +437,339 @@ gemm256_kernel(GemmArgs g) {
             for (int id = l; id < 64 * 128; id += 64) {
                 const int rr = id >> 7, cc = id & 127;
                 const int64_t grow = m0 + wm + 64 * h + rr, gcol = n0 + wn + cc;
-                if (grow < g.M && gcol < g.N)
-                    C[grow * g.ldc + gcol] = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
+                if (grow < g.M && gcol < g.N) {
+                    TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
+                    if constexpr (SCALED) x = x * rq[wm + 64 * h + rr] * cn[wn + cc];
+                    C[grow * g.ldc + gcol] = x;
+                }
             }
         }
     }
+}
+
+// ------------------------------------------------ similarity / softmax sweep
+//
+// One work-group owns 256 query rows and sweeps the codebook in column blocks
+// of 256 with the same product loop (B = R stored N x K).  After each block,
+// the scaled scores of one half of the rows at a time (rows wm + 64 h ..
+// + 63 of each wave) are staged in LDS: from there they are stored (scores
+// requested, or raw softmax scores for the second pass) with 16-byte row
+// chunks, and two threads per row fold them into the row's running state:
+// (max, lowest index of the max) for similarity, (max, sum of exp) for
+// softmax.  Softmax rows are finished by a second pass over the row block's
+// stored scores.
+
+// a, b: (value, index) pairs; the larger value wins, the lower index on ties
+__device__ __forceinline__ void fold_max(float &v, int &i, float v2, int i2) {
+    if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
+}
+// (max, sum of exp(x - max)) pairs
+__device__ __forceinline__ void fold_sum(float &m, float &z, float m2, float z2) {
+    const float mx = fmaxf(m, m2);
+    const float a = (m == -INFINITY) ? 0.f : z * __expf(m - mx);
+    const float b = (m2 == -INFINITY) ? 0.f : z2 * __expf(m2 - mx);
+    m = mx;
+    z = a + b;
+}
+
+constexpr size_t SWEEP_LDS_BYTES = LDS_BYTES + 4 * TM * sizeof(float);   // + rq, cn, rmax, rinv
+
+// ROWN: row norms of T from its fragments (cosine without qnorm2); COLN:
+// column norms of R from its fragments (cosine without cnorm).
+template <bool SOFTMAX, bool ROWN, bool COLN>
+__global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
+sweep256_kernel(GemmArgs g) {
+    extern __shared__ float lds_f[];
+    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
+    float *rq = lds_f + LDS_BYTES / sizeof(float);   // 1 / ||x|| per row (or 1)
+    float *cn = rq + TM;                             // 1 / ||c|| per column of the block (or 1)
+    float *rmax = cn + TN, *rinv = rmax + TM;        // softmax row results
+    const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
+    // row blocks dealt to the XCDs in contiguous ranges: the blocks one XCD
+    // runs together sweep the same codebook block at about the same time
+    const int64_t per = (nM + 7) / 8;
+    const int64_t lt = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (lt >= nM) return;
+    const int64_t m0 = lt * TM;
+    const int t = threadIdx.x, l = t & 63, w = t >> 6;
+    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
+    float *out = static_cast<float *>(g.C);
+    const bool write = SOFTMAX || g.write_out;
+    const bool interior_rows = m0 + TM <= g.M;
+    const bool vec_out = (reinterpret_cast<uintptr_t>(out) & 15) == 0 && g.ldc % 4 == 0;
+    const float mul = SOFTMAX ? g.scale * g.beta : g.scale;
+    // the staged half h holds rows wm + 64 h + (0 .. 63) of every wave; thread
+    // pair (t, t ^ 1) folds staged row t / 2 of that half: wave region
+    // 2 (t / 128) + (t & 1), local row (t / 2) % 64
+    const int srow = (t >> 1) & 63, sreg = 2 * (t >> 7) + (t & 1);
+    float run_m[2] = {-INFINITY, -INFINITY}, run_z[2] = {0.f, 0.f};
+    int run_i[2] = {0, 0};
+
+    constexpr int STRIDE = 128 * 4 + 32;             // staged fp32 row: 128 values + pad
+    for (int64_t nt = 0; nt < nN; ++nt) {
+        const int64_t n0 = nt * TN;
+        f16v acc[4][4];
+        const bool sqa = ROWN && (w & 1) == 0;
+        const bool sqb = COLN && (w >> 1) == 0;
+        float sa[4] = {0.f, 0.f, 0.f, 0.f}, sb[4] = {0.f, 0.f, 0.f, 0.f};
+        // the thread id passes through an empty asm per block, so the
+        // product loop's lane-dependent addresses are recomputed here rather
+        // than kept live (and spilled) across the whole sweep
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        if (ROWN && nt == 0) mma_256<false, ROWN, COLN>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
+        else mma_256<false, false, COLN>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
+
+        // cosine factors of the rows (first block) and of this block's columns
+        if (nt == 0) {
+            if (!g.cosine) {
+                rq[t] = 1.f;
+            } else if (!ROWN) {
+                const float n2 = (m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f;
+                rq[t] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+            } else if (sqa) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float n2 = sa[i] + __shfl_xor(sa[i], 32);
+                    if (l < 32) rq[wm + 32 * i + l] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+                }
+            }
+        }
+        if (!g.cosine) {
+            cn[t] = 1.f;
+        } else if (!COLN) {
+            const float c = (n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f;
+            cn[t] = (c > 0.f) ? 1.f / c : 0.f;
+        } else if (sqb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float n2 = sb[j] + __shfl_xor(sb[j], 32);
+                if (l < 32) cn[wn + 32 * j + l] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
+            }
+        }
+        // every wave is done with the stages (reused for staging) and the
+        // factors are in place
+        lds_barrier();
+
+        const int64_t ncols = (g.N - n0 < TN) ? (g.N - n0) : TN;
+        unsigned char *region = reinterpret_cast<unsigned char *>(lds) + w * (64 * STRIDE);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // stage the raw accumulators of rows wm + 64 h .. + 63 of this wave
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = 32 * ii + acc_row(r, l), col = 32 * j + (l & 31);
+                        *reinterpret_cast<float *>(region + row * STRIDE + col * 4) = acc[2 * h + ii][j][r];
+                    }
+            lds_barrier();
+            // score of staged (row, 4 columns): raw * (mul / (||x|| ||c||)), one
+            // expression for the stored scores and the fold
+            if (write) {
+                const bool full = vec_out && interior_rows && n0 + wn + 128 <= g.N;
+#pragma unroll 4
+                for (int id = l; id < 64 * 32; id += 64) {
+                    const int rr = id >> 5, cc = id & 31;
+                    const int64_t grow = m0 + wm + 64 * h + rr, gcol = n0 + wn + 4 * cc;
+                    const f4v raw = *reinterpret_cast<const f4v *>(region + rr * STRIDE + cc * 16);
+                    const f4v cf = *reinterpret_cast<const f4v *>(cn + wn + 4 * cc);
+                    const f4v v = raw * (mul * rq[wm + 64 * h + rr]) * cf;
+                    float *dst = out + grow * g.ldc + gcol;
+                    if (full) {
+                        *reinterpret_cast<f4v *>(dst) = v;
+                    } else if (grow < g.M) {
+                        for (int e = 0; e < 4; ++e)
+                            if (gcol + e < g.N) dst[e] = v[e];
+                    }
+                }
+            }
+            // fold: thread t scans the 128 staged columns of its row, then pairs up
+            {
+                const float *src = reinterpret_cast<const float *>(
+                    reinterpret_cast<const unsigned char *>(lds) + sreg * (64 * STRIDE) + srow * STRIDE);
+                const int half = 128 * (t & 1);
+                const float f = mul * rq[128 * (t >> 7) + 64 * h + srow];
+                float m = -INFINITY, z = 0.f;
+                int mi = 0;
+#pragma unroll 2
+                for (int c4 = 0; c4 < 32; ++c4) {
+                    const f4v v = *reinterpret_cast<const f4v *>(src + 4 * c4) * f *
+                                  *reinterpret_cast<const f4v *>(cn + half + 4 * c4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int c = half + 4 * c4 + e;
+                        if (c < ncols && v[e] > m) { m = v[e]; mi = (int)n0 + c; }
+                    }
+                }
+                if (SOFTMAX && m != -INFINITY) {
+#pragma unroll 2
+                    for (int c4 = 0; c4 < 32; ++c4) {
+                        const f4v v = *reinterpret_cast<const f4v *>(src + 4 * c4) * f *
+                                      *reinterpret_cast<const f4v *>(cn + half + 4 * c4);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (half + 4 * c4 + e < ncols) z += __expf(v[e] - m);
+                    }
+                }
+                // the partner thread holds the other 128 columns of the row
+                const float m2 = __shfl_xor(m, 1), z2 = __shfl_xor(z, 1);
+                const int i2 = __shfl_xor(mi, 1);
+                if (SOFTMAX) {
+                    fold_sum(m, z, m2, z2);
+                    fold_sum(run_m[h], run_z[h], m, z);
+                } else {
+                    fold_max(m, mi, m2, i2);
+                    fold_max(run_m[h], run_i[h], m, mi);
+                }
+            }
+            lds_barrier();    // the staging region is rewritten next
+        }
+    }
+
+    // rows owned by thread pair (t, t ^ 1) in half h: wm + 64 h + srow of wave
+    // region sreg, i.e. 128 (t / 128) + 64 h + srow
+    if (!SOFTMAX) {
+        if (g.argmax && (t & 1) == 0) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int64_t row = m0 + 128 * (t >> 7) + 64 * h + srow;
+                if (row < g.M) g.argmax[row] = run_i[h];
+            }
+        }
+        return;
+    }
+    if ((t & 1) == 0) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int rl = 128 * (t >> 7) + 64 * h + srow;
+            rmax[rl] = run_m[h];
+            rinv[rl] = 1.f / run_z[h];
+        }
+    }
+    // the second pass reads scores other threads stored to global memory
+    __syncthreads();
+    softmax_rows(out, g.ldc, m0, (g.M - m0 < TM) ? (g.M - m0) : TM, g.N, rmax, rinv, vec_out, NTH);
 }
 
 template <typename TO>
 hipError_t launch_to(bool b_nn, const GemmArgs &a, hipStream_t s) {
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_kernel<TO, true>)
-                         : reinterpret_cast<const void *>(gemm256_kernel<TO, false>);
+    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_kernel<TO, true, false>)
+                         : reinterpret_cast<const void *>(gemm256_kernel<TO, false, false>);
     hipError_t e = raise_lds_limit(k, LDS_BYTES);
     if (e != hipSuccess) return e;
-    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<TO, true>), grid, dim3(NTH), LDS_BYTES, s, a);
-    else hipLaunchKernelGGL((gemm256_kernel<TO, false>), grid, dim3(NTH), LDS_BYTES, s, a);
+    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<TO, true, false>), grid, dim3(NTH), LDS_BYTES, s, a);
+    else hipLaunchKernelGGL((gemm256_kernel<TO, false, false>), grid, dim3(NTH), LDS_BYTES, s, a);
     return hipGetLastError();
 }
 
+constexpr size_t SCORES_LDS_BYTES = LDS_BYTES + 2 * TM * sizeof(float);   // + row and column factors
+
+// One wave per row: the maximum of the row and its lowest column index.
+__global__ void __launch_bounds__(256) rows_argmax_kernel(const float *S, int64_t lds, int64_t B, int64_t M,
+                                                          int32_t *idx) {
+    const int l = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= B) return;
+    const float *s = S + row * lds;
+    float m = -INFINITY;
+    int mi = 0;
+#pragma unroll 8
+    for (int64_t c = l; c < M; c += 64) {
+        const float v = s[c];
+        if (v > m) { m = v; mi = (int)c; }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float m2 = __shfl_xor(m, o);
+        const int i2 = __shfl_xor(mi, o);
+        fold_max(m, mi, m2, i2);
+    }
+    if (l == 0) idx[row] = mi;
+}
+
+// One wave per row, in place: softmax of the row (max-subtracted).
+__global__ void __launch_bounds__(256) rows_softmax_kernel(float *A, int64_t lda, int64_t B, int64_t M) {
+    const int l = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= B) return;
+    float *a = A + row * lda;
+    float m = -INFINITY;
+#pragma unroll 8
+    for (int64_t c = l; c < M; c += 64) m = fmaxf(m, a[c]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float z = 0.f;
+#pragma unroll 8
+    for (int64_t c = l; c < M; c += 64) z += __expf(a[c] - m);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    const float iz = 1.f / z;
+#pragma unroll 8
+    for (int64_t c = l; c < M; c += 64) a[c] = __expf(a[c] - m) * iz;
+}
+
+template <bool SOFTMAX, bool ROWN, bool COLN>
+hipError_t launch_sweep(const GemmArgs &a, hipStream_t s) {
+    const int64_t nM = (a.M + TM - 1) / TM;
+    const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
+    const void *k = reinterpret_cast<const void *>(sweep256_kernel<SOFTMAX, ROWN, COLN>);
+    hipError_t e = raise_lds_limit(k, SWEEP_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((sweep256_kernel<SOFTMAX, ROWN, COLN>), grid, dim3(NTH), SWEEP_LDS_BYTES, s, a);
+    return hipGetLastError();
+}
+
+template <bool SOFTMAX>
+hipError_t launch_sweep_norms(const GemmArgs &a, hipStream_t s) {
+    const bool rown = a.cosine && a.qnorm2 == nullptr, coln = a.cosine && a.cnorm == nullptr;
+    if (rown) return coln ? launch_sweep<SOFTMAX, true, true>(a, s) : launch_sweep<SOFTMAX, true, false>(a, s);
+    return coln ? launch_sweep<SOFTMAX, false, true>(a, s) : launch_sweep<SOFTMAX, false, false>(a, s);
+}
+
 }  // namespace
+
+hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s) {
+    if (a.M == 0 || a.N == 0) return hipSuccess;
+    const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
+    const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
+    GemmArgs b = a;
+    if (softmax) b.scale = a.scale * a.beta;      // the softmax acts on beta * score
+    const void *k = reinterpret_cast<const void *>(gemm256_kernel<float, false, true>);
+    hipError_t e = raise_lds_limit(k, SCORES_LDS_BYTES);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm256_kernel<float, false, true>), grid, dim3(NTH), SCORES_LDS_BYTES, s, b);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 rgrid((unsigned)((a.M + 3) / 4));
+    float *out = static_cast<float *>(a.C);
+    if (softmax) {
+        hipLaunchKernelGGL(rows_softmax_kernel, rgrid, dim3(256), 0, s, out, a.ldc, a.M, a.N);
+        return hipGetLastError();
+    }
+    if (a.argmax) {
+        hipLaunchKernelGGL(rows_argmax_kernel, rgrid, dim3(256), 0, s, out, a.ldc, a.M, a.N, a.argmax);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+bool sweep256_fits(const GemmArgs &a) {
+    // at least one 256-row block per CU; offsets within the buffer resources
+    // below 2^31
+    if ((a.M + TM - 1) / TM < 256) return false;
+    const int64_t lim = (int64_t)1 << 31;
+    return 2 * (TM * a.lda + a.K + 8) < lim && 2 * (TN * a.ldb + a.K + 8) < lim;
+}
+
+hipError_t launch_sweep256(bool softmax, const GemmArgs &a, hipStream_t s) {
+    if (a.M == 0 || a.N == 0) return hipSuccess;
+    return softmax ? launch_sweep_norms<true>(a, s) : launch_sweep_norms<false>(a, s);
+}
 
 bool gemm256_fits(const GemmArgs &a, bool b_nn) {
     // at least one full round of 256 x 256 tiles over the 256 CUs; smaller

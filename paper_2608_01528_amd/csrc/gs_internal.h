@@ -46,6 +46,45 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Second pass of the attention sweeps: row r of the block (rows m0 ..
+// m0 + rows - 1 of out, leading dimension ldc, N columns) becomes
+// exp(s - rmax[r]) * rinv[r].  Eight rows are in flight per thread (their
+// loads are issued before any is used), in 16-byte chunks when vec (out
+// 16-byte aligned, ldc a multiple of 4).  nthr threads take part.
+__device__ __forceinline__ void softmax_rows(float *out, int64_t ldc, int64_t m0, int64_t rows, int64_t N,
+                                             const float *rmax, const float *rinv, bool vec, int nthr) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const int t = threadIdx.x;
+    const int64_t n4 = vec ? N / 4 : 0;
+    for (int64_t r0 = 0; r0 < rows; r0 += 8) {
+        const int nr = (int)((rows - r0 < 8) ? (rows - r0) : 8);
+        for (int64_t c = t; c < n4; c += nthr) {
+            f4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (u < nr) v[u] = *reinterpret_cast<const f4 *>(out + (m0 + r0 + u) * ldc + 4 * c);
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (u < nr) {
+                    const float mx = rmax[r0 + u], iv = rinv[r0 + u];
+                    f4 e;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) e[q] = __expf(v[u][q] - mx) * iv;
+                    *reinterpret_cast<f4 *>(out + (m0 + r0 + u) * ldc + 4 * c) = e;
+                }
+        }
+        for (int64_t c = 4 * n4 + t; c < N; c += nthr) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (u < nr) v[u] = out[(m0 + r0 + u) * ldc + c];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (u < nr) out[(m0 + r0 + u) * ldc + c] = __expf(v[u] - rmax[r0 + u]) * rinv[r0 + u];
+        }
+    }
+}
+
 template <typename T> __device__ __forceinline__ float ld_f32(const T *p, int64_t i);
 template <> __device__ __forceinline__ float ld_f32<float>(const float *p, int64_t i) { return p[i]; }
 template <> __device__ __forceinline__ float ld_f32<bf16_t>(const bf16_t *p, int64_t i) {
@@ -90,6 +129,14 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
 // the product is large enough to fill the chip with such tiles.
 bool gemm256_fits(const GemmArgs &a, bool b_nn);
 hipError_t launch_gemm256(gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s);
+// Row sweep of similarity (softmax = false) or attention scores over 256 x
+// 256 blocks, bf16 x bf16 with 16-byte aligned rows (B stored N x K).
+bool sweep256_fits(const GemmArgs &a);
+hipError_t launch_sweep256(bool softmax, const GemmArgs &a, hipStream_t s);
+// Scores written to memory (similarity with S, or attention): the 256 x 256
+// product kernel with a scaled-score epilogue, then a row pass (argmax, or
+// softmax in place).  Same operand conditions as launch_gemm256 (B N x K).
+hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s);
 
 // Raise a kernel's dynamic LDS limit (once per kernel, to a whole CU's LDS);
 // fails for requests beyond that.

@@ -612,3 +612,77 @@ def test_bf16_large_tile_prob2vec():
     Tr = host(T[rows])
     assert np.isfinite(Tr).all()
     assert rowrel(Tr, oracle.prob2vec(P[rows], R)) <= TOL_F32
+
+
+# ------------------- bf16 row sweep (>= 256 row blocks of 256, 256-column blocks)
+#
+# With Q the identity, coordinates and codebook coordinates are themselves the
+# D-space vectors, so the oracle's dense cosine / dot similarity and softmax
+# apply directly to T and R.  Ragged row count, a codebook size that leaves a
+# partial column block, r not a multiple of the K-step or of 8, NaN row padding.
+
+SWEEP_B, SWEEP_M, SWEEP_R = 65573, 600, 300
+
+
+@pytest.fixture(scope="module")
+def sweep_case():
+    T = _bf16_mat(SWEEP_B, SWEEP_R, 21)
+    R = _bf16_mat(SWEEP_M, SWEEP_R, 22)
+    ld = (SWEEP_R + 7) // 8 * 8
+    Td, Rd = nan_padded_bf16(T, ld), nan_padded_bf16(R, ld)
+    rows = _tile_rows(SWEEP_B, 23)
+    return T, R, Td, Rd, rows
+
+
+@pytest.mark.parametrize("norms", ["computed", "given"])
+def test_bf16_sweep_similarity_cosine(sweep_case, norms):
+    T, R, Td, Rd, rows = sweep_case
+    print("sweep similarity cosine", norms, flush=True)
+    qn = cn = None
+    if norms == "given":
+        qn = dev(oracle.row_norms(T) ** 2)
+        cn = dev(oracle.row_norms(R))
+    S, idx = gsm.gs_similarity(Td, Rd, qnorm2=qn, cnorm=cn, mode="cosine")
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.COSINE)
+    Sg = host(S[rows])
+    assert np.isfinite(Sg).all()
+    assert rowrel(Sg, So) <= TOL_F32
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    # whole batch: the returned index points at a maximal score of its row
+    Sf = S.float()
+    assert torch.all(Sf.gather(1, idx.long()[:, None])[:, 0] >= Sf.max(dim=1).values).item()
+
+
+def test_bf16_sweep_similarity_dot_argmax_only(sweep_case):
+    T, R, Td, Rd, rows = sweep_case
+    _, idx = gsm.gs_similarity(Td, Rd, mode="dot", scale=0.5, scores=False)
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.DOT, 0.5)
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+
+
+@pytest.mark.parametrize("norms", ["computed", "given"])
+def test_bf16_sweep_attention(sweep_case, norms):
+    T, R, Td, Rd, rows = sweep_case
+    print("sweep attention", norms, flush=True)
+    qn = cn = None
+    if norms == "given":
+        qn = dev(oracle.row_norms(T) ** 2)
+        cn = dev(oracle.row_norms(R))
+    A, _ = gsm.gs_attention(Td, Rd, qnorm2=qn, cnorm=cn, mode="cosine", beta=8.0)
+    torch.cuda.synchronize()
+    Ao = oracle.softmax(oracle.similarity(T[rows], R, oracle.COSINE), 8.0)
+    Ag = host(A[rows])
+    assert np.isfinite(Ag).all()
+    assert rowrel(Ag, Ao) <= TOL_F32
+    assert torch.allclose(A.sum(dim=1), torch.ones(A.shape[0], device=A.device), atol=1e-4)
+
+
+def test_bf16_sweep_cosine_argmax_only(sweep_case):
+    # no scores requested: the fused row sweep, norms taken from T and R
+    T, R, Td, Rd, rows = sweep_case
+    _, idx = gsm.gs_similarity(Td, Rd, mode="cosine", scores=False)
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.COSINE)
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
