@@ -736,6 +736,65 @@ __global__ void __launch_bounds__(NTHR) gemm_store_kernel(GemmArgs g, int veca, 
         }
 }
 
+// ------------------------------------------------- epilogue: scores
+//
+// Similarity / attention when the scores (or weights) are written anyway:
+// out = scale * acc / (||x|| ||c||) for cosine, scale * acc for dot (scale
+// includes beta for attention); the row pass (argmax, or softmax in place)
+// follows as its own launch.  Row norms come from qnorm2 or from the A tile,
+// column norms from cnorm or from the B tile, both accumulated by the main
+// loop.
+
+template <typename TA, typename TB>
+__global__ void __launch_bounds__(NTHR) gemm_scores_kernel(GemmArgs g, int veca, int vecb) {
+    extern __shared__ float lds[];
+    const int64_t nM = (g.M + BM - 1) / BM, nN = (g.N + BN - 1) / BN;
+    const int64_t L = logical_tile(nM * nN);
+    if (L >= nM * nN) return;
+    const int64_t m0 = (L / nN) * BM, n0 = (L % nN) * BN;
+    f16v acc[2][2], acc2[2][2];
+    const bool sqa = g.cosine && g.qnorm2 == nullptr, sqb = g.cosine && g.cnorm == nullptr;
+    float sa = 0.f, sb = 0.f;
+    block_mma_any<TA, TB, false, false, store_stages<false>()>(g, m0, n0, veca, vecb, lds, acc, acc2, sqa, &sa,
+                                                               sqb, &sb);
+    // the main loop has passed a barrier after its last LDS read
+    float *rq = lds, *cn = lds + BM;
+    const int t = threadIdx.x;
+    if (t < 128) {
+        float q = g.scale;
+        if (g.cosine) {
+            const float n2 = g.qnorm2 ? ((m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f) : sa;
+            q = (n2 > 0.f) ? g.scale / sqrtf(n2) : 0.f;
+        }
+        rq[t] = q;
+        float c = 1.f;
+        if (g.cosine) {
+            const float cc = g.cnorm ? ((n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f) : sqrtf(sb);
+            c = (cc > 0.f) ? 1.f / cc : 0.f;
+        }
+        cn[t] = c;
+    }
+    lds_barrier();
+    float *C = static_cast<float *>(g.C);
+    const int l = t & 63, w = t >> 6;
+    const int wm = (w >> 1) * 64, wn = (w & 1) * 64;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int cl = wn + 32 * j + (l & 31);
+            const int64_t col = n0 + cl;
+            if (col >= g.N) continue;
+            const float cf = cn[cl];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rl = wm + 32 * i + acc_row(r, l);
+                const int64_t row = m0 + rl;
+                if (row < g.M) C[row * g.ldc + col] = acc[i][j][r] * rq[rl] * cf;
+            }
+        }
+}
+
 // ---------------------------------------- epilogue: similarity / softmax
 //
 // One work-group owns a 128-row block and sweeps every 128-column block of
@@ -900,6 +959,18 @@ hipError_t dispatch_store(bool b_nn, bool bind, const GemmArgs &a, bool veca, bo
 }
 
 template <typename TA, typename TB>
+hipError_t dispatch_scores(bool softmax, const GemmArgs &a_in, bool veca, bool vecb, hipStream_t s) {
+    GemmArgs a = a_in;
+    if (softmax) a.scale = a_in.scale * a_in.beta;   // the softmax acts on beta * score
+    const int64_t nM = (a.M + BM - 1) / BM, nN = (a.N + BN - 1) / BN;
+    const dim3 grid((unsigned)(8 * ((nM * nN + 7) / 8)));
+    const size_t lds = stage_lds_floats<TA, TB, false, store_stages<false>()>(a.dma) * sizeof(float);
+    hipError_t e = launch_with_lds(gemm_scores_kernel<TA, TB>, grid, lds, s, a, veca, vecb);
+    if (e != hipSuccess) return e;
+    return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
+}
+
+template <typename TA, typename TB>
 hipError_t dispatch_rowsweep(bool softmax, const GemmArgs &a, bool veca, bool vecb, hipStream_t s) {
     const int64_t nM = (a.M + BM - 1) / BM;
     const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
@@ -962,6 +1033,12 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
     const bool sm = epi == EPI_SOFTMAX;
     if (a.dma && !b_nn && (sm || a.write_out) && gemm256_fits(a, false)) return launch_scores256(a, sm, s);
     if (a.dma && !b_nn && sweep256_fits(a)) return launch_sweep256(sm, a, s);
+    // scores or weights written anyway: product with a scaled epilogue, then
+    // the row pass; argmax alone: the row sweep (no score matrix in memory)
+    if ((sm || a.write_out) && !b_nn) {
+        if (!bf_a && !bf_b) return dispatch_scores<float, float>(sm, a, veca, vecb, s);
+        if (bf_a && bf_b) return dispatch_scores<bf16_t, bf16_t>(sm, a, veca, vecb, s);
+    }
     if (!bf_a && !bf_b) return dispatch_rowsweep<float, float>(sm, a, veca, vecb, s);
     if (bf_a && bf_b) return dispatch_rowsweep<bf16_t, bf16_t>(sm, a, veca, vecb, s);
     return hipErrorInvalidValue;

@@ -745,14 +745,19 @@ hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s) {
     hipLaunchKernelGGL((gemm256_kernel<float, false, true>), grid, dim3(NTH), SCORES_LDS_BYTES, s, b);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const dim3 rgrid((unsigned)((a.M + 3) / 4));
-    float *out = static_cast<float *>(a.C);
+    return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
+}
+
+hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int64_t M, int32_t *argmax,
+                            hipStream_t s) {
+    if (B == 0 || M == 0) return hipSuccess;
+    const dim3 rgrid((unsigned)((B + 3) / 4));
     if (softmax) {
-        hipLaunchKernelGGL(rows_softmax_kernel, rgrid, dim3(256), 0, s, out, a.ldc, a.M, a.N);
+        hipLaunchKernelGGL(rows_softmax_kernel, rgrid, dim3(256), 0, s, out, ld, B, M);
         return hipGetLastError();
     }
-    if (a.argmax) {
-        hipLaunchKernelGGL(rows_argmax_kernel, rgrid, dim3(256), 0, s, out, a.ldc, a.M, a.N, a.argmax);
+    if (argmax) {
+        hipLaunchKernelGGL(rows_argmax_kernel, rgrid, dim3(256), 0, s, out, ld, B, M, argmax);
         return hipGetLastError();
     }
     return hipSuccess;

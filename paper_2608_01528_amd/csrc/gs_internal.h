@@ -137,6 +137,10 @@ hipError_t launch_sweep256(bool softmax, const GemmArgs &a, hipStream_t s);
 // product kernel with a scaled-score epilogue, then a row pass (argmax, or
 // softmax in place).  Same operand conditions as launch_gemm256 (B N x K).
 hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s);
+// Row pass over a B x M fp32 score matrix (leading dimension ld): softmax in
+// place, or the row argmax (lowest index on ties) into argmax when non-null.
+hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int64_t M, int32_t *argmax,
+                            hipStream_t s);
 
 // Raise a kernel's dynamic LDS limit (once per kernel, to a whole CU's LDS);
 // fails for requests beyond that.
