@@ -379,35 +379,116 @@ __device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const
     }
 }
 
-template <typename TI, typename TT, int MB, class Rows>
+// Scores of the thread's rows from the Gram matrix of the codebook block,
+// G[j][k] = <c_j, c_k> (staged in place of R): s_j = <p, G_j> equals
+// <sum_k p_k c_k, c_j>, and ||v||^2 = <p, s>.  The probabilities are the
+// thread's tile rows; raw scores replace them there, then the scaled scores
+// (and the row maximum with its lowest index).
+template <int MB, class Rows>
+__device__ __forceinline__ void rows_gram_scores(int M, const Rows &Gs, const float *Rn, float mul, bool cosine,
+                                                 float *tile, float best[RPT], int bi[RPT]) {
+    float p[RPT][MB];
+#pragma unroll
+    for (int u = 0; u < RPT; ++u)
+#pragma unroll
+        for (int k = 0; k < MB; ++k) p[u][k] = (k < M) ? tile[(threadIdx.x + u * SROWS) * M + k] : 0.f;
+    float n2[RPT];
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) n2[u] = 0.f;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+        if (j < M) {
+            float gr[MB];
+            Gs.row(j, gr);
+#pragma unroll
+            for (int u = 0; u < RPT; ++u) {
+                float d = 0.f;
+#pragma unroll
+                for (int k = 0; k < MB; ++k) d += p[u][k] * gr[k];
+                tile[(threadIdx.x + u * SROWS) * M + j] = d;
+                n2[u] += p[u][j] * d;
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < RPT; ++u) {
+        const float q = cosine ? ((n2[u] > 0.f) ? 1.f / sqrtf(n2[u]) : 0.f) : 1.f;
+        float *srow = tile + (threadIdx.x + u * SROWS) * M;
+        best[u] = -INFINITY;
+        bi[u] = 0;
+        for (int j = 0; j < M; ++j) {
+            const float sj = mul * srow[j] * q * Rn[j];
+            srow[j] = sj;
+            if (sj > best[u]) { best[u] = sj; bi[u] = j; }
+        }
+    }
+}
+
+typedef float gs16v __attribute__((ext_vector_type(16)));
+
+// Replace the padded codebook block Rs (MB x MB) by its Gram matrix,
+// G[j][k] = <R_j, R_k> (= <c_j, c_k>: Q has orthonormal rows).  Wave 0 forms
+// it on the matrix cores as one 32 x 32 block of v_mfma_f32_32x32x2f32
+// (A = R and B = R^T take the same register: lane l holds R[l % 32][k]);
+// the other waves wait at the barrier.
+
+template <int MB>
+__device__ __forceinline__ void stage_gram(float *Rs) {
+    if (threadIdx.x < 64) {
+        const int l = threadIdx.x;
+        const int row = l & 31;
+        gs16v acc = {};
+#pragma unroll
+        for (int kk = 0; kk < MB / 2; ++kk) {
+            const int k = 2 * kk + (l >> 5);
+            const float v = (row < MB) ? Rs[row * MB + k] : 0.f;
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(v, v, acc, 0, 0, 0);
+        }
+        // every read of R has returned before any lane overwrites it: the
+        // MFMAs above consumed them, and this wave alone writes
+#pragma unroll
+        for (int g = 0; g < 16; ++g) {
+            const int j = 8 * (g >> 2) + 4 * (l >> 5) + (g & 3);
+            if (j < MB && row < MB) Rs[j * MB + row] = acc[g];
+        }
+    }
+    lds_barrier();
+}
+
+template <typename TI, typename TT, int MB, bool GRAM, class Rows>
 __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow,
                                            const Rows &Rsrc, const float *Rn, float *tile) {
     const int t = threadIdx.x;
     const int M = (int)G.M, r = (int)G.r;
-    float x[RPT][MB];
-    rows_prob2vec<MB>(tile, M, r, Rsrc, x);      // Gram-loc of the superposed vectors
-    float q[RPT];
-#pragma unroll
-    for (int u = 0; u < RPT; ++u) {
-        float n2 = 0.f;
-#pragma unroll
-        for (int k = 0; k < MB; ++k) n2 += x[u][k] * x[u][k];   // in span: ||v|| = ||t||
-        q[u] = a.cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;
-    }
-    lds_barrier();   // the tile is reused for the outputs
-    if (G.T) {
-#pragma unroll
-        for (int u = 0; u < RPT; ++u)
-#pragma unroll
-            for (int k = 0; k < MB; ++k)
-                if (k < r) tile[(t + u * SROWS) * r + k] = x[u][k];
-        lds_barrier();
-        tile_store<TT, SROWS>(static_cast<TT *>(G.T), G.ldt, b0, nrow, r, tile);
-        lds_barrier();
-    }
     float best[RPT];
     int bi[RPT];
-    rows_scores<MB>(x, M, Rsrc, Rn, a.scale, q, tile, best, bi);
+    if constexpr (GRAM) {
+        // no coordinates requested: scores straight from the Gram matrix
+        rows_gram_scores<MB>(M, Rsrc, Rn, a.scale, a.cosine != 0, tile, best, bi);
+    } else {
+        float x[RPT][MB];
+        rows_prob2vec<MB>(tile, M, r, Rsrc, x);      // Gram-loc of the superposed vectors
+        float q[RPT];
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
+            float n2 = 0.f;
+#pragma unroll
+            for (int k = 0; k < MB; ++k) n2 += x[u][k] * x[u][k];   // in span: ||v|| = ||t||
+            q[u] = a.cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;
+        }
+        lds_barrier();   // the tile is reused for the outputs
+        if (G.T) {
+#pragma unroll
+            for (int u = 0; u < RPT; ++u)
+#pragma unroll
+                for (int k = 0; k < MB; ++k)
+                    if (k < r) tile[(t + u * SROWS) * r + k] = x[u][k];
+            lds_barrier();
+            tile_store<TT, SROWS>(static_cast<TT *>(G.T), G.ldt, b0, nrow, r, tile);
+            lds_barrier();
+        }
+        rows_scores<MB>(x, M, Rsrc, Rn, a.scale, q, tile, best, bi);
+    }
     if (G.argmax) {
 #pragma unroll
         for (int u = 0; u < RPT; ++u)
@@ -433,8 +514,10 @@ __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G
     }
 }
 
+// At least four work-groups per CU (every work-group of the vsa launch in one
+// round): at most 128 registers per lane.
 template <typename TI, typename TT>
-__global__ void __launch_bounds__(SROWS) soft_select_kernel(SoftArgs a) {
+__global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     __shared__ __attribute__((aligned(16))) float tile[SBLK * MAXK];
     __shared__ __attribute__((aligned(16))) float Rs[MAXK * MAXK];
     __shared__ float Rn[MAXK];
@@ -481,11 +564,20 @@ __global__ void __launch_bounds__(SROWS) soft_select_kernel(SoftArgs a) {
         tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
     }
     lds_barrier();
+    if (G.T == nullptr) {
+        switch (MB) {
+            case 8: stage_gram<8>(Rs); soft_block<TI, TT, 8, true>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
+            case 16: stage_gram<16>(Rs); soft_block<TI, TT, 16, true>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
+            case 24: stage_gram<24>(Rs); soft_block<TI, TT, 24, true>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
+            default: stage_gram<32>(Rs); soft_block<TI, TT, 32, true>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
+        }
+        return;
+    }
     switch (MB) {
-        case 8: soft_block<TI, TT, 8>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
-        case 16: soft_block<TI, TT, 16>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
-        case 24: soft_block<TI, TT, 24>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
-        default: soft_block<TI, TT, 32>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
+        case 8: soft_block<TI, TT, 8, false>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
+        case 16: soft_block<TI, TT, 16, false>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
+        case 24: soft_block<TI, TT, 24, false>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
+        default: soft_block<TI, TT, 32, false>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
     }
 }
 
