@@ -232,6 +232,10 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
  *   A[b, j] = softmax over j of beta * S[b, j]
  * It computes what gs_prob2vec, gs_similarity and gs_attention compute on the
  * same inputs, without storing and re-reading the coordinates in between.
+ * When T is null the coordinates are not formed at all: the scores are taken
+ * through the Gram matrix G = R_g R_g^T (= C C^T, Sec. 3.2) of the codebook,
+ * <t, R_g[j]> = sum_k p_k G[k][j] and ||t||^2 = sum_j p_j <t, R_g[j]>, which
+ * equal the definitions above up to rounding order.
  *
  *   groups     HOST array of ngroups descriptors, 1 <= ngroups <= 8; in each,
  *              1 <= r <= M <= 32, B >= 0, and
