@@ -46,6 +46,15 @@ __device__ __forceinline__ void st4(bf16_t *p, f4v v) {
     *reinterpret_cast<uint2 *>(p) = u;
 }
 
+// Output stores: fp32 outputs are written with streaming (non-temporal)
+// stores, which leave the cache for data the kernel never reads back.
+__device__ __forceinline__ void st4_out(float *p, f4v v) { __builtin_nontemporal_store(v, reinterpret_cast<f4v *>(p)); }
+__device__ __forceinline__ void st4_out(bf16_t *p, f4v v) { st4(p, v); }
+template <typename T> __device__ __forceinline__ void st1_out(T *p, int64_t i, float v) { st_f32<T>(p, i, v); }
+template <> __device__ __forceinline__ void st1_out<float>(float *p, int64_t i, float v) {
+    __builtin_nontemporal_store(v, p + i);
+}
+
 // Smallest supported padded size for a codebook of M entries.
 __host__ __device__ __forceinline__ int pad_of(int64_t M) { return M <= 8 ? 8 : M <= 16 ? 16 : M <= 24 ? 24 : 32; }
 
@@ -109,15 +118,15 @@ __device__ __forceinline__ void tile_store(T *__restrict__ g, int64_t ld, int64_
     T *base = g + b0 * ld;
     if (ld == w && aligned16(base)) {
         const int n4 = n >> 2;
-        for (int e4 = t; e4 < n4; e4 += NT) st4(base + 4 * e4, *reinterpret_cast<const f4v *>(tile + 4 * e4));
+        for (int e4 = t; e4 < n4; e4 += NT) st4_out(base + 4 * e4, *reinterpret_cast<const f4v *>(tile + 4 * e4));
         const int e = 4 * n4 + t;
-        if (e < n) st_f32<T>(base, e, tile[e]);
+        if (e < n) st1_out<T>(base, e, tile[e]);
         return;
     }
     int row = t / w, col = t - (t / w) * w;
     const int dq = NT / w, dc = NT - (NT / w) * w;
     for (int e = t; e < n; e += NT) {
-        st_f32<T>(base, (int64_t)row * ld + col, tile[e]);
+        st1_out<T>(base, (int64_t)row * ld + col, tile[e]);
         row += dq;
         col += dc;
         if (col >= w) { col -= w; ++row; }
@@ -272,7 +281,7 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
     int bi;
     row_scores<MB>(x, M, R, Rn, mul, q, srow, best, bi);
     if (MODE == MODE_SIM) {
-        if (a.argmax && t < nrow) a.argmax[b0 + t] = bi;
+        if (a.argmax && t < nrow) __builtin_nontemporal_store(bi, a.argmax + b0 + t);
         if (!a.Out) return;
         lds_barrier();
         tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
@@ -379,93 +388,214 @@ __device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const
     }
 }
 
-// Scores of the thread's rows from the Gram matrix of the codebook block,
-// G[j][k] = <c_j, c_k> (staged in place of R): s_j = <p, G_j> equals
-// <sum_k p_k c_k, c_j>, and ||v||^2 = <p, s>.  The probabilities are the
-// thread's tile rows; raw scores replace them there, then the scaled scores
-// (and the row maximum with its lowest index).
-template <int MB, class Rows>
-__device__ __forceinline__ void rows_gram_scores(int M, const Rows &Gs, const float *Rn, float mul, bool cosine,
-                                                 float *tile, float best[RPT], int bi[RPT]) {
-    float p[RPT][MB];
-#pragma unroll
-    for (int u = 0; u < RPT; ++u)
-#pragma unroll
-        for (int k = 0; k < MB; ++k) p[u][k] = (k < M) ? tile[(threadIdx.x + u * SROWS) * M + k] : 0.f;
-    float n2[RPT];
-#pragma unroll
-    for (int u = 0; u < RPT; ++u) n2[u] = 0.f;
-#pragma unroll
-    for (int j = 0; j < MB; ++j) {
-        if (j < M) {
-            float gr[MB];
-            Gs.row(j, gr);
-#pragma unroll
-            for (int u = 0; u < RPT; ++u) {
-                float d = 0.f;
-#pragma unroll
-                for (int k = 0; k < MB; ++k) d += p[u][k] * gr[k];
-                tile[(threadIdx.x + u * SROWS) * M + j] = d;
-                n2[u] += p[u][j] * d;
-            }
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < RPT; ++u) {
-        const float q = cosine ? ((n2[u] > 0.f) ? 1.f / sqrtf(n2[u]) : 0.f) : 1.f;
-        float *srow = tile + (threadIdx.x + u * SROWS) * M;
-        best[u] = -INFINITY;
-        bi[u] = 0;
-        for (int j = 0; j < M; ++j) {
-            const float sj = mul * srow[j] * q * Rn[j];
-            srow[j] = sj;
-            if (sj > best[u]) { best[u] = sj; bi[u] = j; }
-        }
-    }
-}
-
 typedef float gs16v __attribute__((ext_vector_type(16)));
 
-// Replace the padded codebook block Rs (MB x MB) by its Gram matrix,
-// G[j][k] = <R_j, R_k> (= <c_j, c_k>: Q has orthonormal rows).  Wave 0 forms
-// it on the matrix cores as one 32 x 32 block of v_mfma_f32_32x32x2f32
-// (A = R and B = R^T take the same register: lane l holds R[l % 32][k]);
-// the other waves wait at the barrier.
+// --------------------------------------------- soft selection, Gram form
+//
+// Without a coordinate output the coordinates t = p R are never formed: with
+// the Gram matrix G = R R^T of the codebook block (G[j][k] = <c_j, c_k>, Q
+// having orthonormal rows), <t, R_j> = sum_k p_k G[k][j] and
+// ||t||^2 = sum_j p_j <t, R_j>.  Per row this is M^2 multiply-adds in place
+// of 2 M r, all in registers.
 
-template <int MB>
-__device__ __forceinline__ void stage_gram(float *Rs) {
-    if (threadIdx.x < 64) {
-        const int l = threadIdx.x;
-        const int row = l & 31;
-        gs16v acc = {};
+// Probability tile request: 16-byte pieces into registers.  fp32 rows use
+// buffer loads whose range is the tile itself, so every thread issues the same
+// number of loads whatever the row count (the pieces beyond the range read as
+// zero and are not used) and the codebook loads issued before them can be
+// waited for alone.
+template <typename TI> struct TileReq;
+template <> struct TileReq<float> {
+    static constexpr int V = SBLK * MAXK / 4 / SROWS;   // 16-byte pieces per thread
+    f4v v[V];
+    __device__ __forceinline__ void issue(const float *base, int n) {
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, n * 4, 0x00020000);
 #pragma unroll
-        for (int kk = 0; kk < MB / 2; ++kk) {
-            const int k = 2 * kk + (l >> 5);
-            const float v = (row < MB) ? Rs[row * MB + k] : 0.f;
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(v, v, acc, 0, 0, 0);
-        }
-        // every read of R has returned before any lane overwrites it: the
-        // MFMAs above consumed them, and this wave alone writes
+        for (int i = 0; i < V; ++i)
+            v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(
+                                                rs, (int)(threadIdx.x + i * SROWS) * 16, 0, 0));
+    }
+};
+template <> struct TileReq<bf16_t> {
+    static constexpr int V = SBLK * MAXK / 4 / SROWS;   // 4-element pieces per thread
+    f4v v[V];
+    __device__ __forceinline__ void issue(const bf16_t *base, int n) {
+        const int n4 = n >> 2;
 #pragma unroll
-        for (int g = 0; g < 16; ++g) {
-            const int j = 8 * (g >> 2) + 4 * (l >> 5) + (g & 3);
-            if (j < MB && row < MB) Rs[j * MB + row] = acc[g];
+        for (int i = 0; i < V; ++i) {
+            const int e4 = threadIdx.x + i * SROWS;
+            if (e4 < n4) v[i] = ld4(base + 4 * e4);
         }
     }
-    lds_barrier();
+};
+
+// Wave 0 replaces the padded codebook block Rs (MB x MB, zero beyond M rows
+// and r columns) by its Gram matrix, formed on the matrix cores as one
+// 32 x 32 block of v_mfma_f32_32x32x2f32 (A = R and B = R^T take the same
+// register: lane l holds R[l % 32][k]), and writes the per-entry factors Rn
+// (1 / ||c_j|| for cosine, from the given norms or from the diagonal of G;
+// 1 for dot; 0 beyond M).  Lanes of rows past MB read row MB - 1 and use zero.
+template <int MB>
+__device__ __forceinline__ void stage_gram(float *Rs, float *Rn, int M, bool cosine, const float *cnorm, float cn) {
+    if (threadIdx.x >= 64) return;
+    const int l = threadIdx.x;
+    const int row = l & 31;
+    const int rrow = (row < MB) ? row : MB - 1;
+    float v[MB / 2];
+#pragma unroll
+    for (int kk = 0; kk < MB / 2; ++kk) {
+        const float x = Rs[rrow * MB + 2 * kk + (l >> 5)];
+        v[kk] = (row < MB) ? x : 0.f;
+    }
+    gs16v acc = {};
+    float s2 = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < MB / 2; ++kk) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(v[kk], v[kk], acc, 0, 0, 0);
+        s2 += v[kk] * v[kk];
+    }
+    s2 += __shfl_xor(s2, 32);   // ||R_row||^2: even and odd columns
+    // every read of R has returned before any lane overwrites it: the MFMAs
+    // above consumed them, and this wave alone writes
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+        const int j = 8 * (g >> 2) + 4 * (l >> 5) + (g & 3);
+        if (j < MB && row < MB) Rs[j * MB + row] = acc[g];
+    }
+    if (l < MB) {
+        float c = 0.f;
+        if (l < M) {
+            c = 1.f;
+            if (cosine) {
+                const float n = cnorm ? cn : sqrtf(s2);
+                c = (n > 0.f) ? 1.f / n : 0.f;
+            }
+        }
+        Rn[l] = c;
+    }
 }
 
-template <typename TI, typename TT, int MB, bool GRAM, class Rows>
+template <typename TI, int MB>
+__device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow, float *tile,
+                                          float *Rs, float *Rn) {
+    const int t = threadIdx.x;
+    const int M = (int)G.M, r = (int)G.r;
+    const bool cosine = a.cosine != 0;
+    const TI *R = static_cast<const TI *>(G.R);
+
+    // 1. the codebook block and norms, requested first so that they return first
+    constexpr int RE = (MB * MB + SROWS - 1) / SROWS;
+    float rv[RE];
+#pragma unroll
+    for (int i = 0; i < RE; ++i) {
+        const int e = t + i * SROWS, j = e / MB, k = e - (e / MB) * MB;
+        rv[i] = (e < MB * MB && j < M && k < r) ? ld_f32<TI>(R, (int64_t)j * G.ldr + k) : 0.f;
+    }
+    const float cn = (cosine && G.cnorm && t < M) ? G.cnorm[t] : 0.f;
+
+    // 2. the probability tile
+    const TI *base = static_cast<const TI *>(G.P) + b0 * G.ldp;
+    const bool contig = G.ldp == G.M && aligned16(base);
+    const int n = nrow * M, n4 = n >> 2;
+    TileReq<TI> req;
+    req.issue(base, contig ? n : 0);   // an empty range issues nothing useful
+
+    // 3. Gram matrix and factors while the tile is in flight
+#pragma unroll
+    for (int i = 0; i < RE; ++i)
+        if (t + i * SROWS < MB * MB) Rs[t + i * SROWS] = rv[i];
+    lds_barrier();
+    stage_gram<MB>(Rs, Rn, M, cosine, G.cnorm, cn);
+
+    // 4. tile to LDS
+    if (contig) {
+#pragma unroll
+        for (int i = 0; i < TileReq<TI>::V; ++i) {
+            const int e4 = t + i * SROWS;
+            if (e4 < n4) st4(tile + 4 * e4, req.v[i]);
+        }
+        const int e = 4 * n4 + t;
+        if (e < n) tile[e] = ld_f32<TI>(base, e);
+    } else {
+        tile_load<TI, SROWS>(static_cast<const TI *>(G.P), G.ldp, b0, nrow, M, tile);
+    }
+    lds_barrier();
+
+    // 5. scores of the thread's row, all in registers
+    float *srow = tile + t * M;
+    float p[MB];
+#pragma unroll
+    for (int k = 0; k < MB; ++k) {
+        const float x = srow[(k < M) ? k : M - 1];
+        p[k] = (k < M) ? x : 0.f;
+    }
+    // d_j = sum_k p_k G[k][j], one G row at a time into MB independent sums
+    float d[MB];
+#pragma unroll
+    for (int j = 0; j < MB; ++j) d[j] = 0.f;
+#pragma unroll
+    for (int k = 0; k < MB; ++k) {
+        const f4v *gq = reinterpret_cast<const f4v *>(Rs + k * MB);
+#pragma unroll
+        for (int c = 0; c < MB / 4; ++c) {
+            const f4v g = gq[c];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) d[4 * c + i] += p[k] * g[i];
+        }
+    }
+    float n2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) n2 += p[j] * d[j];
+    const float q = cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;   // in span: ||v|| = ||t||
+    const float mq = a.scale * q;
+    float best = -INFINITY;
+    int bi = 0;
+#pragma unroll
+    for (int j = 0; j < MB; ++j) {
+        d[j] = mq * d[j] * Rn[j];
+        if (j < M && d[j] > best) { best = d[j]; bi = j; }
+    }
+    if (G.argmax && t < nrow) __builtin_nontemporal_store(bi, G.argmax + b0 + t);
+
+    // 6. outputs through the tile (each thread overwrites only its own row)
+    if (G.S) {
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+            if (j < M) srow[j] = d[j];
+        lds_barrier();
+        tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
+    }
+    if (G.A) {
+        // softmax of beta times the scores; the maximum is taken after
+        // scaling (beta may be negative)
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+            if (j < M) mx = fmaxf(mx, a.beta * d[j]);
+        float z = 0.f;
+#pragma unroll
+        for (int j = 0; j < MB; ++j) {
+            d[j] = (j < M) ? __expf(a.beta * d[j] - mx) : 0.f;
+            z += d[j];
+        }
+        const float iz = 1.f / z;
+        if (G.S) lds_barrier();   // S has left the tile before it is overwritten
+#pragma unroll
+        for (int j = 0; j < MB; ++j)
+            if (j < M) srow[j] = d[j] * iz;
+        lds_barrier();
+        tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
+    }
+}
+
+template <typename TI, typename TT, int MB, class Rows>
 __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow,
                                            const Rows &Rsrc, const float *Rn, float *tile) {
     const int t = threadIdx.x;
     const int M = (int)G.M, r = (int)G.r;
     float best[RPT];
     int bi[RPT];
-    if constexpr (GRAM) {
-        // no coordinates requested: scores straight from the Gram matrix
-        rows_gram_scores<MB>(M, Rsrc, Rn, a.scale, a.cosine != 0, tile, best, bi);
-    } else {
+    {
         float x[RPT][MB];
         rows_prob2vec<MB>(tile, M, r, Rsrc, x);      // Gram-loc of the superposed vectors
         float q[RPT];
@@ -492,7 +622,7 @@ __device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G
     if (G.argmax) {
 #pragma unroll
         for (int u = 0; u < RPT; ++u)
-            if (t + u * SROWS < nrow) G.argmax[b0 + t + u * SROWS] = bi[u];
+            if (t + u * SROWS < nrow) __builtin_nontemporal_store(bi[u], G.argmax + b0 + t + u * SROWS);
     }
     if (G.S) {
         lds_barrier();
@@ -528,6 +658,15 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     const int M = (int)G.M, r = (int)G.r;
     const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
     const int MB = a.mb[gi];
+    if (G.T == nullptr) {   // no coordinate output: Gram form
+        switch (MB) {
+            case 8: soft_gram<TI, 8>(a, G, b0, nrow, tile, Rs, Rn); break;
+            case 16: soft_gram<TI, 16>(a, G, b0, nrow, tile, Rs, Rn); break;
+            case 24: soft_gram<TI, 24>(a, G, b0, nrow, tile, Rs, Rn); break;
+            default: soft_gram<TI, 32>(a, G, b0, nrow, tile, Rs, Rn); break;
+        }
+        return;
+    }
     const TI *P = static_cast<const TI *>(G.P);
     const TI *R = static_cast<const TI *>(G.R);
 
@@ -564,20 +703,11 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
         tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
     }
     lds_barrier();
-    if (G.T == nullptr) {
-        switch (MB) {
-            case 8: stage_gram<8>(Rs); soft_block<TI, TT, 8, true>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
-            case 16: stage_gram<16>(Rs); soft_block<TI, TT, 16, true>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
-            case 24: stage_gram<24>(Rs); soft_block<TI, TT, 24, true>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
-            default: stage_gram<32>(Rs); soft_block<TI, TT, 32, true>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
-        }
-        return;
-    }
     switch (MB) {
-        case 8: soft_block<TI, TT, 8, false>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
-        case 16: soft_block<TI, TT, 16, false>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
-        case 24: soft_block<TI, TT, 24, false>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
-        default: soft_block<TI, TT, 32, false>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
+        case 8: soft_block<TI, TT, 8>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
+        case 16: soft_block<TI, TT, 16>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
+        case 24: soft_block<TI, TT, 24>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
+        default: soft_block<TI, TT, 32>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
     }
 }
 
