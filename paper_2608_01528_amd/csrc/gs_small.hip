@@ -529,18 +529,63 @@ __device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G,
         const float x = srow[(k < M) ? k : M - 1];
         p[k] = (k < M) ? x : 0.f;
     }
-    // d_j = sum_k p_k G[k][j], one G row at a time into MB independent sums
     float d[MB];
+    if constexpr (MB >= 24) {
+        // Matrix cores: the wave's 64 rows as two 32 x MB blocks times G
+        // (v_mfma_f32_32x32x2f32; step kk pairs k = kk and kk + MB/2 over the
+        // two half-waves).  Lane l supplies A = P[row l % 32][k] from the
+        // tile and B = G[k][l % 32] from registers; the result block (lane l,
+        // register g: row 8(g/4) + 4(l/32) + g % 4, column l % 32) replaces the
+        // block's probabilities in the tile, from where each thread takes its
+        // own row.  Entries past M are zero on both sides.
+        constexpr int KH = MB / 2;
+        const int l = t & 63, c = l & 31, h = l >> 5;
+        float bf[KH];
 #pragma unroll
-    for (int j = 0; j < MB; ++j) d[j] = 0.f;
+        for (int kk = 0; kk < KH; ++kk) {
+            const float x = Rs[(kk + KH * h) * MB + ((c < MB) ? c : 0)];
+            bf[kk] = (c < MB) ? x : 0.f;
+        }
 #pragma unroll
-    for (int k = 0; k < MB; ++k) {
-        const f4v *gq = reinterpret_cast<const f4v *>(Rs + k * MB);
+        for (int b = 0; b < 2; ++b) {
+            const int r0 = (t & ~63) + 32 * b;
+            const float *arow = tile + (r0 + c) * M;
+            gs16v acc = {};
 #pragma unroll
-        for (int c = 0; c < MB / 4; ++c) {
-            const f4v g = gq[c];
+            for (int kk = 0; kk < KH; ++kk) {
+                const int k = kk + KH * h;
+                const float x = arow[(k < M) ? k : M - 1];
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((k < M) ? x : 0.f, bf[kk], acc, 0, 0, 0);
+            }
+            // the block's reads have returned (the products consumed them) and
+            // only this wave touches its rows
+            if (c < M) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) d[4 * c + i] += p[k] * g[i];
+                for (int g = 0; g < 16; ++g) tile[(r0 + 8 * (g >> 2) + 4 * h + (g & 3)) * M + c] = acc[g];
+            }
+        }
+        // LDS operations of one wave complete in order: the row written by
+        // the other lanes is read back after these fences
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+#pragma unroll
+        for (int j = 0; j < MB; ++j) {
+            const float x = srow[(j < M) ? j : M - 1];
+            d[j] = (j < M) ? x : 0.f;
+        }
+    } else {
+        // d_j = sum_k p_k G[k][j], one G row at a time into MB independent sums
+#pragma unroll
+        for (int j = 0; j < MB; ++j) d[j] = 0.f;
+#pragma unroll
+        for (int k = 0; k < MB; ++k) {
+            const f4v *gq = reinterpret_cast<const f4v *>(Rs + k * MB);
+#pragma unroll
+            for (int c = 0; c < MB / 4; ++c) {
+                const f4v g = gq[c];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) d[4 * c + i] += p[k] * g[i];
+            }
         }
     }
     float n2 = 0.f;

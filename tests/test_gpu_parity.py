@@ -414,6 +414,32 @@ def test_soft_select(mode, scale, beta, with_t):
         check_argmax(host(g["argmax"]), So)
 
 
+def test_soft_select_strided_rows():
+    # probabilities and outputs as column slices of wider matrices (row
+    # strides above M): element-wise tile moves instead of 16-byte pieces
+    books = soft_case([6, 22, 32], [300, 777, 40], 1024, 45)
+    groups = []
+    for b in books:
+        Pw = torch.full((b["B"], b["M"] + 3), np.nan, device="cuda")
+        Pw[:, : b["M"]] = b["Pd"]
+        Sw = torch.full((b["B"], b["M"] + 5), np.nan, device="cuda")
+        Aw = torch.full((b["B"], b["M"] + 1), np.nan, device="cuda")
+        groups.append({"P": Pw[:, : b["M"]], "R": b["Rd"], "S": Sw[:, : b["M"]],
+                       "argmax": torch.full((b["B"],), -1, dtype=torch.int32, device="cuda"),
+                       "A": Aw[:, : b["M"]], "_S": Sw, "_A": Aw})
+    gsm.gs_soft_select([{k: v for k, v in g.items() if not k.startswith("_")} for g in groups],
+                       mode="cosine", beta=16.0)
+    torch.cuda.synchronize()
+    for b, g in zip(books, groups):
+        V = oracle.prob2vec(b["P"], b["C"])
+        So = oracle.similarity(V, b["C"], oracle.COSINE)
+        assert rowrel(host(g["S"]), So) <= TOL_F32
+        assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
+        check_argmax(host(g["argmax"]), So)
+        # the padding columns of the output rows are untouched
+        assert torch.isnan(g["_S"][:, b["M"]:]).all() and torch.isnan(g["_A"][:, b["M"]:]).all()
+
+
 def test_soft_select_bf16_and_partial_outputs():
     books = soft_case([10, 22], [700, 450], 1024, 50, dtype=torch.bfloat16)
     groups = soft_outputs(books, want=("argmax", "A"))
