@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <string>
+#include <algorithm>
 #include <vector>
 
 #include "gs_internal.h"
@@ -351,13 +352,22 @@ gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, 
         out.push_back(span(g.S, g.B, g.M, g.lds, 4, "S"));
         out.push_back(span(g.argmax, 1, g.B, g.B, 4, "argmax"));
         out.push_back(span(g.A, g.B, g.M, g.lda, 4, "A"));
-        SoftGroup &d = a.g[i];
+    }
+    // Work-groups are dispatched in index order and the first ones get their
+    // tiles first: the groups with the most work per row (the largest
+    // codebooks) go first, so the longest work-groups start earliest.
+    int order[SOFT_MAX_GROUPS];
+    for (int i = 0; i < ngroups; ++i) order[i] = i;
+    std::stable_sort(order, order + ngroups, [&](int x, int y) { return groups[x].M > groups[y].M; });
+    for (int k = 0; k < ngroups; ++k) {
+        const gs_soft_group &g = groups[order[k]];
+        SoftGroup &d = a.g[k];
         d.P = g.P; d.ldp = g.ldp; d.R = g.R; d.ldr = g.ldr; d.cnorm = g.cnorm;
         d.B = g.B; d.M = g.M; d.r = g.r; d.T = g.T; d.ldt = g.ldt; d.S = g.S; d.lds = g.lds;
         d.argmax = g.argmax; d.A = g.A; d.lda = g.lda;
-        a.tile_start[i] = tiles;
+        a.tile_start[k] = tiles;
         tiles += soft_select_tiles(g.B);
-        a.mb[i] = soft_select_pad(g.M);
+        a.mb[k] = soft_select_pad(g.M);
     }
     a.tile_start[ngroups] = tiles;
     a.ntiles = tiles;
