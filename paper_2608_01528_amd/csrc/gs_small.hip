@@ -429,83 +429,75 @@ template <> struct TileReq<bf16_t> {
     }
 };
 
-// Wave 0 replaces the padded codebook block Rs (MB x MB, zero beyond M rows
-// and r columns) by its Gram matrix, formed on the matrix cores as one
-// 32 x 32 block of v_mfma_f32_32x32x2f32 (A = R and B = R^T take the same
-// register: lane l holds R[l % 32][k]), and writes the per-entry factors Rn
-// (1 / ||c_j|| for cosine, from the given norms or from the diagonal of G;
-// 1 for dot; 0 beyond M).  Lanes of rows past MB read row MB - 1 and use zero.
-template <int MB>
-__device__ __forceinline__ void stage_gram(float *Rs, float *Rn, int M, bool cosine, const float *cnorm, float cn) {
-    if (threadIdx.x >= 64) return;
+// Gram matrix of the codebook, formed by wave 0 on the matrix cores as one
+// 32 x 32 block of v_mfma_f32_32x32x2f32 with A = R and B = R^T in the same
+// register: lane l holds R[l % 32][2 kk + l / 32] in rk[kk] (zero past M
+// rows and r columns).  G[j][i] goes to Gs[j * GS + i] for i, j < M, and the
+// per-entry factors to Rn (1 / ||c_j|| for cosine, from the given norms or
+// from the codebook rows; 1 for dot).
+template <int M, int GS>
+__device__ __forceinline__ void gram_stage(const float (&rk)[(M + 1) / 2], float *Gs, float *Rn, bool cosine,
+                                           bool given, float cn) {
     const int l = threadIdx.x;
-    const int row = l & 31;
-    const int rrow = (row < MB) ? row : MB - 1;
-    float v[MB / 2];
-#pragma unroll
-    for (int kk = 0; kk < MB / 2; ++kk) {
-        const float x = Rs[rrow * MB + 2 * kk + (l >> 5)];
-        v[kk] = (row < MB) ? x : 0.f;
-    }
+    const int row = l & 31, h = l >> 5;
     gs16v acc = {};
     float s2 = 0.f;
 #pragma unroll
-    for (int kk = 0; kk < MB / 2; ++kk) {
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(v[kk], v[kk], acc, 0, 0, 0);
-        s2 += v[kk] * v[kk];
+    for (int kk = 0; kk < (M + 1) / 2; ++kk) {
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(rk[kk], rk[kk], acc, 0, 0, 0);
+        s2 += rk[kk] * rk[kk];
     }
     s2 += __shfl_xor(s2, 32);   // ||R_row||^2: even and odd columns
-    // every read of R has returned before any lane overwrites it: the MFMAs
-    // above consumed them, and this wave alone writes
+    if (row < M) {
 #pragma unroll
-    for (int g = 0; g < 16; ++g) {
-        const int j = 8 * (g >> 2) + 4 * (l >> 5) + (g & 3);
-        if (j < MB && row < MB) Rs[j * MB + row] = acc[g];
+        for (int g = 0; g < 16; ++g) {
+            const int j = 8 * (g >> 2) + 4 * h + (g & 3);
+            if (j < M) Gs[j * GS + row] = acc[g];
+        }
     }
-    if (l < MB) {
-        float c = 0.f;
-        if (l < M) {
-            c = 1.f;
-            if (cosine) {
-                const float n = cnorm ? cn : sqrtf(s2);
-                c = (n > 0.f) ? 1.f / n : 0.f;
-            }
+    if (l < M) {
+        float c = 1.f;
+        if (cosine) {
+            const float n = given ? cn : sqrtf(s2);
+            c = (n > 0.f) ? 1.f / n : 0.f;
         }
         Rn[l] = c;
     }
 }
 
-template <typename TI, int MB>
-__device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow, float *tile,
-                                          float *Rs, float *Rn) {
+// One row block of one group, for a codebook of exactly M entries.
+template <typename TI, int M>
+__device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float scale, float beta, int64_t b0,
+                                          int nrow, float *tile, float *Gs, float *Rn) {
+    constexpr int GS = (M + 3) & ~3;   // row stride of G in LDS (16-byte rows)
+    constexpr int KG = (M + 1) / 2;    // steps of the Gram product
     const int t = threadIdx.x;
-    const int M = (int)G.M, r = (int)G.r;
-    const bool cosine = a.cosine != 0;
-    const TI *R = static_cast<const TI *>(G.R);
+    const int r = (int)G.r;
 
-    // 1. the codebook block and norms, requested first so that they return first
-    constexpr int RE = (MB * MB + SROWS - 1) / SROWS;
-    float rv[RE];
+    // 1. wave 0: the codebook rows in the Gram product's operand layout and
+    // the given norms, requested before the tile so that they return first
+    float rk[KG];
+    float cn = 0.f;
+    if (t < 64) {
+        const int row = t & 31, h = t >> 5;
+        const TI *Rrow = static_cast<const TI *>(G.R) + (int64_t)((row < M) ? row : 0) * G.ldr;
 #pragma unroll
-    for (int i = 0; i < RE; ++i) {
-        const int e = t + i * SROWS, j = e / MB, k = e - (e / MB) * MB;
-        rv[i] = (e < MB * MB && j < M && k < r) ? ld_f32<TI>(R, (int64_t)j * G.ldr + k) : 0.f;
+        for (int kk = 0; kk < KG; ++kk) {
+            const int k = 2 * kk + h;
+            rk[kk] = (row < M && k < r) ? ld_f32<TI>(Rrow, k) : 0.f;
+        }
+        if (cosine && G.cnorm && t < M) cn = G.cnorm[t];
     }
-    const float cn = (cosine && G.cnorm && t < M) ? G.cnorm[t] : 0.f;
 
     // 2. the probability tile
     const TI *base = static_cast<const TI *>(G.P) + b0 * G.ldp;
-    const bool contig = G.ldp == G.M && aligned16(base);
+    const bool contig = G.ldp == M && aligned16(base);
     const int n = nrow * M, n4 = n >> 2;
     TileReq<TI> req;
     req.issue(base, contig ? n : 0);   // an empty range issues nothing useful
 
     // 3. Gram matrix and factors while the tile is in flight
-#pragma unroll
-    for (int i = 0; i < RE; ++i)
-        if (t + i * SROWS < MB * MB) Rs[t + i * SROWS] = rv[i];
-    lds_barrier();
-    stage_gram<MB>(Rs, Rn, M, cosine, G.cnorm, cn);
+    if (t < 64) gram_stage<M, GS>(rk, Gs, Rn, cosine, G.cnorm != nullptr, cn);
 
     // 4. tile to LDS
     if (contig) {
@@ -521,47 +513,50 @@ __device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G,
     }
     lds_barrier();
 
-    // 5. scores of the thread's row, all in registers
+    // 5. scores of the thread's row, in registers
     float *srow = tile + t * M;
-    float p[MB];
+    float p[M];
 #pragma unroll
-    for (int k = 0; k < MB; ++k) {
-        const float x = srow[(k < M) ? k : M - 1];
-        p[k] = (k < M) ? x : 0.f;
-    }
-    float d[MB];
-    if constexpr (MB >= 24) {
-        // Matrix cores: the wave's 64 rows as two 32 x MB blocks times G
-        // (v_mfma_f32_32x32x2f32; step kk pairs k = kk and kk + MB/2 over the
+    for (int k = 0; k < M; ++k) p[k] = srow[k];
+    float d[M];
+    if constexpr (M > 16) {
+        // Matrix cores: the wave's 64 rows as two 32 x M blocks times G
+        // (v_mfma_f32_32x32x2f32; step kk pairs k = kk and kk + KH over the
         // two half-waves).  Lane l supplies A = P[row l % 32][k] from the
         // tile and B = G[k][l % 32] from registers; the result block (lane l,
         // register g: row 8(g/4) + 4(l/32) + g % 4, column l % 32) replaces the
         // block's probabilities in the tile, from where each thread takes its
-        // own row.  Entries past M are zero on both sides.
-        constexpr int KH = MB / 2;
+        // own row.  Columns past M are never stored; a k past M (odd M) is
+        // zero on both sides.
+        constexpr int KH = (M + 1) / 2;
         const int l = t & 63, c = l & 31, h = l >> 5;
         float bf[KH];
 #pragma unroll
         for (int kk = 0; kk < KH; ++kk) {
-            const float x = Rs[(kk + KH * h) * MB + ((c < MB) ? c : 0)];
-            bf[kk] = (c < MB) ? x : 0.f;
+            if (M % 2 == 1 && kk == KH - 1) {
+                const float x = Gs[kk * GS + c];
+                bf[kk] = (h == 0) ? x : 0.f;
+            } else {
+                bf[kk] = Gs[(kk + KH * h) * GS + c];
+            }
         }
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
             const int r0 = (t & ~63) + 32 * b;
-            const float *arow = tile + (r0 + c) * M;
+            const float *arow = tile + (r0 + c) * M + KH * h;
             gs16v acc = {};
 #pragma unroll
             for (int kk = 0; kk < KH; ++kk) {
-                const int k = kk + KH * h;
-                const float x = arow[(k < M) ? k : M - 1];
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((k < M) ? x : 0.f, bf[kk], acc, 0, 0, 0);
+                float x = arow[kk];
+                if (M % 2 == 1 && kk == KH - 1) x = (h == 0) ? x : 0.f;
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x, bf[kk], acc, 0, 0, 0);
             }
             // the block's reads have returned (the products consumed them) and
             // only this wave touches its rows
             if (c < M) {
+                float *drow = tile + (r0 + 4 * h) * M + c;
 #pragma unroll
-                for (int g = 0; g < 16; ++g) tile[(r0 + 8 * (g >> 2) + 4 * h + (g & 3)) * M + c] = acc[g];
+                for (int g = 0; g < 16; ++g) drow[(8 * (g >> 2) + (g & 3)) * M] = acc[g];
             }
         }
         // LDS operations of one wave complete in order: the row written by
@@ -569,44 +564,41 @@ __device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G,
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 #pragma unroll
-        for (int j = 0; j < MB; ++j) {
-            const float x = srow[(j < M) ? j : M - 1];
-            d[j] = (j < M) ? x : 0.f;
-        }
+        for (int j = 0; j < M; ++j) d[j] = srow[j];
     } else {
-        // d_j = sum_k p_k G[k][j], one G row at a time into MB independent sums
+        // d_j = sum_k p_k G[k][j], one G row at a time into M independent sums
 #pragma unroll
-        for (int j = 0; j < MB; ++j) d[j] = 0.f;
+        for (int j = 0; j < M; ++j) d[j] = 0.f;
 #pragma unroll
-        for (int k = 0; k < MB; ++k) {
-            const f4v *gq = reinterpret_cast<const f4v *>(Rs + k * MB);
+        for (int k = 0; k < M; ++k) {
+            const f4v *gq = reinterpret_cast<const f4v *>(Gs + k * GS);
 #pragma unroll
-            for (int c = 0; c < MB / 4; ++c) {
-                const f4v g = gq[c];
+            for (int q = 0; q < GS / 4; ++q) {
+                const f4v g = gq[q];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) d[4 * c + i] += p[k] * g[i];
+                for (int i = 0; i < 4; ++i)
+                    if (4 * q + i < M) d[4 * q + i] += p[k] * g[i];
             }
         }
     }
     float n2 = 0.f;
 #pragma unroll
-    for (int j = 0; j < MB; ++j) n2 += p[j] * d[j];
+    for (int j = 0; j < M; ++j) n2 += p[j] * d[j];
     const float q = cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;   // in span: ||v|| = ||t||
-    const float mq = a.scale * q;
+    const float mq = scale * q;
     float best = -INFINITY;
     int bi = 0;
 #pragma unroll
-    for (int j = 0; j < MB; ++j) {
+    for (int j = 0; j < M; ++j) {
         d[j] = mq * d[j] * Rn[j];
-        if (j < M && d[j] > best) { best = d[j]; bi = j; }
+        if (d[j] > best) { best = d[j]; bi = j; }
     }
     if (G.argmax && t < nrow) __builtin_nontemporal_store(bi, G.argmax + b0 + t);
 
     // 6. outputs through the tile (each thread overwrites only its own row)
     if (G.S) {
 #pragma unroll
-        for (int j = 0; j < MB; ++j)
-            if (j < M) srow[j] = d[j];
+        for (int j = 0; j < M; ++j) srow[j] = d[j];
         lds_barrier();
         tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
     }
@@ -615,22 +607,48 @@ __device__ __forceinline__ void soft_gram(const SoftArgs &a, const SoftGroup &G,
         // scaling (beta may be negative)
         float mx = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < MB; ++j)
-            if (j < M) mx = fmaxf(mx, a.beta * d[j]);
+        for (int j = 0; j < M; ++j) mx = fmaxf(mx, beta * d[j]);
         float z = 0.f;
 #pragma unroll
-        for (int j = 0; j < MB; ++j) {
-            d[j] = (j < M) ? __expf(a.beta * d[j] - mx) : 0.f;
+        for (int j = 0; j < M; ++j) {
+            d[j] = __expf(beta * d[j] - mx);
             z += d[j];
         }
         const float iz = 1.f / z;
         if (G.S) lds_barrier();   // S has left the tile before it is overwritten
 #pragma unroll
-        for (int j = 0; j < MB; ++j)
-            if (j < M) srow[j] = d[j] * iz;
+        for (int j = 0; j < M; ++j) srow[j] = d[j] * iz;
         lds_barrier();
         tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
     }
+}
+
+template <typename TI, int M>
+__device__ __forceinline__ void soft_gram_m(int m, const SoftGroup &G, bool cosine, float scale, float beta,
+                                            int64_t b0, int nrow, float *tile, float *Gs, float *Rn) {
+    if constexpr (M <= MAXK) {
+        if (m == M) soft_gram<TI, M>(G, cosine, scale, beta, b0, nrow, tile, Gs, Rn);
+        else soft_gram_m<TI, M + 1>(m, G, cosine, scale, beta, b0, nrow, tile, Gs, Rn);
+    }
+}
+
+// Fused soft selection without a coordinate output: scores through the
+// codebook's Gram matrix (G = R R^T = C C^T, Sec. 3.2): with t = p R,
+// <t, R_j> = sum_k p_k G[k][j] and ||t||^2 = sum_j p_j <t, R_j>, so the
+// coordinates are never formed; per row this is M^2 multiply-adds in place
+// of 2 M r.  One work-group per 256-row block of a group; at least four
+// work-groups per CU (at most 128 registers per lane).
+template <typename TI>
+__global__ void __launch_bounds__(SROWS, 4) soft_gram_kernel(SoftArgs a) {
+    __shared__ __attribute__((aligned(16))) float tile[SBLK * MAXK];
+    __shared__ __attribute__((aligned(16))) float Gs[MAXK * MAXK];
+    __shared__ float Rn[MAXK];
+    const int64_t blk = blockIdx.x;
+    const int gi = soft_group(a, blk);
+    const SoftGroup G = a.g[gi];   // by value: the group's descriptor in scalar registers
+    const int64_t b0 = (blk - a.tile_start[gi]) * SBLK;
+    const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
+    soft_gram_m<TI, 1>((int)G.M, G, a.cosine != 0, a.scale, a.beta, b0, nrow, tile, Gs, Rn);
 }
 
 template <typename TI, typename TT, int MB, class Rows>
@@ -703,15 +721,6 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     const int M = (int)G.M, r = (int)G.r;
     const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
     const int MB = a.mb[gi];
-    if (G.T == nullptr) {   // no coordinate output: Gram form
-        switch (MB) {
-            case 8: soft_gram<TI, 8>(a, G, b0, nrow, tile, Rs, Rn); break;
-            case 16: soft_gram<TI, 16>(a, G, b0, nrow, tile, Rs, Rn); break;
-            case 24: soft_gram<TI, 24>(a, G, b0, nrow, tile, Rs, Rn); break;
-            default: soft_gram<TI, 32>(a, G, b0, nrow, tile, Rs, Rn); break;
-        }
-        return;
-    }
     const TI *P = static_cast<const TI *>(G.P);
     const TI *R = static_cast<const TI *>(G.R);
 
@@ -796,6 +805,14 @@ hipError_t launch_small_attention(gs_dtype tin, gs_dtype to, const SmallArgs &a,
 hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s) {
     if (a.ntiles == 0) return hipSuccess;
     const dim3 grid((unsigned)a.ntiles), block(SROWS);
+    bool coords = false;
+    for (int i = 0; i < a.ngroups; ++i) coords = coords || a.g[i].T != nullptr;
+    if (!coords) {
+        if (tin == GS_F32) hipLaunchKernelGGL((soft_gram_kernel<float>), grid, block, 0, s, a);
+        else if (tin == GS_BF16) hipLaunchKernelGGL((soft_gram_kernel<bf16_t>), grid, block, 0, s, a);
+        else return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     if (tin == GS_F32 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<float, float>), grid, block, 0, s, a);
     else if (tin == GS_F32 && tt == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<float, bf16_t>), grid, block, 0, s, a);
     else if (tin == GS_BF16 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<bf16_t, float>), grid, block, 0, s, a);
