@@ -586,12 +586,13 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     for (int j = 0; j < M; ++j) n2 += p[j] * d[j];
     const float q = cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;   // in span: ||v|| = ||t||
     const float mq = scale * q;
-    float best = -INFINITY;
+    float best = -INFINITY, worst = INFINITY;
     int bi = 0;
 #pragma unroll
     for (int j = 0; j < M; ++j) {
         d[j] = mq * d[j] * Rn[j];
         if (d[j] > best) { best = d[j]; bi = j; }
+        worst = fminf(worst, d[j]);
     }
     if (G.argmax && t < nrow) __builtin_nontemporal_store(bi, G.argmax + b0 + t);
 
@@ -603,15 +604,15 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
         tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
     }
     if (G.A) {
-        // softmax of beta times the scores; the maximum is taken after
-        // scaling (beta may be negative)
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < M; ++j) mx = fmaxf(mx, beta * d[j]);
+        // softmax of beta times the scores in base 2: exp(beta s) =
+        // 2^(beta log2(e) s); the largest exponent is beta log2(e) times the
+        // largest score, or the smallest one when beta is negative
+        const float bl = beta * 1.44269504088896341f;
+        const float m2 = (bl >= 0.f) ? bl * best : bl * worst;
         float z = 0.f;
 #pragma unroll
         for (int j = 0; j < M; ++j) {
-            d[j] = __expf(beta * d[j] - mx);
+            d[j] = __builtin_amdgcn_exp2f(fmaf(bl, d[j], -m2));
             z += d[j];
         }
         const float iz = 1.f / z;
