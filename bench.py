@@ -61,7 +61,7 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE counter CSVs (kernel run, copy calibration) "
                          "into profiles/traffic_<kernel>_<workload>.json and exit")
-    ap.add_argument("--pmc-kernel", default="soft_select_kernel")
+    ap.add_argument("--pmc-kernel", default="soft_gram_kernel")
     ap.add_argument("--pmc-copy-mib", type=int, default=512)
     return ap.parse_args()
 
@@ -466,9 +466,9 @@ def main():
             "codebooks_M": w.Ms, "D": w.D, "rows_per_codebook": w.B, "queries_per_step": work.queries,
         },
         "roofline": {
-            "bound": "hbm", "kernel": "soft_select_kernel", "call": "gs_soft_select",
+            "bound": "hbm", "kernel": "soft_gram_kernel", "call": "gs_soft_select",
             "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-            "traffic": load_traffic("soft_select_kernel", "vsa"),
+            "traffic": load_traffic("soft_gram_kernel", "vsa"),
             "bytes_per_launch": bpl, "avg_launch_us": launch_ms * 1e3,
         },
         "cpu_baseline": cpu,
