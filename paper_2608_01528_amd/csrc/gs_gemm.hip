@@ -1011,11 +1011,14 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
                        const GemmArgs &a_in, hipStream_t s) {
     if (a_in.M == 0 || a_in.N == 0) return hipSuccess;
     GemmArgs a = a_in;
-    // asynchronous-load bf16 loop: every operand with 16-byte aligned rows
-    auto rows16 = [](const void *p, int64_t ld) { return aligned16(p) && ld % 8 == 0; };
-    a.dma = ta == GS_BF16 && tb == GS_BF16 && rows16(a.A, a.lda) && rows16(a.B, a.ldb) &&
-            (epi != EPI_BIND || rows16(a.A2, a.lda2));
-    if (epi == EPI_STORE && a.dma && gemm256_fits(a, b_nn)) return launch_gemm256(tout, b_nn, a, s);
+    // asynchronous-load loops: operands of one type, every row 16-byte aligned
+    const bool same = (ta == GS_BF16 && tb == GS_BF16) || (ta == GS_F32 && tb == GS_F32);
+    const int64_t per = (ta == GS_BF16) ? 8 : 4;
+    auto rows16 = [&](const void *p, int64_t ld) { return aligned16(p) && ld % per == 0; };
+    const bool rows_ok = same && rows16(a.A, a.lda) && rows16(a.B, a.ldb) &&
+                         (epi != EPI_BIND || rows16(a.A2, a.lda2));
+    a.dma = rows_ok && ta == GS_BF16;   // the 128 x 128 pipelined loop is bf16 only
+    if (epi == EPI_STORE && rows_ok && gemm256_fits(ta, a, b_nn)) return launch_gemm256(ta, tout, b_nn, a, s);
     bool veca = vec_ok(a.A, ta, a.lda, a.K);
     if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
     const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);
@@ -1031,8 +1034,8 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
         return hipErrorInvalidValue;
     }
     const bool sm = epi == EPI_SOFTMAX;
-    if (a.dma && !b_nn && (sm || a.write_out) && gemm256_fits(a, false)) return launch_scores256(a, sm, s);
-    if (a.dma && !b_nn && sweep256_fits(a)) return launch_sweep256(sm, a, s);
+    if (rows_ok && !b_nn && (sm || a.write_out) && gemm256_fits(ta, a, false)) return launch_scores256(ta, a, sm, s);
+    if (rows_ok && !b_nn && sweep256_fits(ta, a)) return launch_sweep256(ta, sm, a, s);
     // scores or weights written anyway: product with a scaled epilogue, then
     // the row pass; argmax alone: the row sweep (no score matrix in memory)
     if ((sm || a.write_out) && !b_nn) {

@@ -32,10 +32,10 @@
 namespace gs {
 namespace {
 
-constexpr int TM = 256, TN = 256, TK = 64;
+constexpr int TM = 256, TN = 256;
 constexpr int NTH = 256;
 constexpr int NSTAGE = 2;
-constexpr int OPT = TM * TK;        // bf16 per staged operand tile (32 KiB)
+constexpr int OPT = TM * 64;        // 16-bit units per staged operand tile (32 KiB)
 constexpr int OPS = 16;             // load instructions per stage and wave
 constexpr int GROUP_M = 4;          // m-tiles that take each n-tile in turn
 constexpr int EP_STRIDE_MAX = 128 * 4 + 32;   // staged fp32 output row: 128 values + 32-byte pad
@@ -49,6 +49,20 @@ typedef short s4v __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f4v __attribute__((ext_vector_type(4)));
 #define AS_L __attribute__((address_space(3)))
+
+// Operand element type: a staged row slice is always 128 bytes (TK elements)
+// and a fragment one 16-byte chunk (PER elements) per lane.
+template <typename T> struct Op;
+template <> struct Op<bf16_t> {
+    typedef bf8v V;
+    typedef __bf16 E;
+    static constexpr int TK = 64, PER = 8;
+};
+template <> struct Op<float> {
+    typedef f4v V;
+    typedef float E;
+    static constexpr int TK = 32, PER = 4;
+};
 
 // s_waitcnt with vmcnt <= n (expcnt and lgkmcnt unconstrained), gfx9 encoding.
 template <int N>
@@ -87,53 +101,79 @@ __device__ __forceinline__ void dma16(const rsrc_t &r, int64_t byte_off, const u
                  : "memory", "m0");
 }
 
-// Row tile: 32 load instructions of 8 rows x 128 bytes; wave w issues blocks
-// 8w .. 8w+7.  Lane L lands at row 8b + L/8, position L%8, so it fetches
-// chunk (L%8) ^ (((8b + L/8) >> 1) % 8) = (L%8) ^ (4 (b % 2) + L/16).  `r`
+// Row tile: 32 load instructions of 8 rows x 128 bytes; wave w issues
+// blocks 8w .. 8w+7.  Lane L lands at row 8b + L/8, position L%8, so it
+// fetches chunk (L%8) ^ (((8b + L/8) >> 1) % 8) = (L%8) ^ (4 (b % 2) + L/16).  `r`
 // starts at the tile's first row; rows past the last one (nrows rows from
 // there) reuse it.
+template <typename T>
 __device__ __forceinline__ void dma_rows(const rsrc_t &r, int64_t ld, int64_t nrows, int64_t k0, int64_t K,
                                          uint16_t *tile, int tid) {
+    constexpr int P = Op<T>::PER;
     const int L = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t klast = ((K - 1) >> 3) << 3;
+    const int64_t klast = ((K - 1) / P) * P;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int b = 8 * w + q;
         const int c = (L & 7) ^ (4 * (q & 1) + (L >> 4));
-        int64_t kc = k0 + 8 * c;
+        int64_t kc = k0 + P * c;
         if (kc > klast) kc = klast;
         int64_t row = 8 * b + (L >> 3);
         if (row > nrows - 1) row = nrows - 1;
-        dma16(r, 2 * (row * ld + kc), tile + b * 512);
+        dma16(r, (int64_t)sizeof(T) * (row * ld + kc), tile + b * 512);
     }
 }
 
-// k-row tile: 32 load instructions of 2 k-rows x 512 bytes; wave w issues
-// blocks 8w .. 8w+7.  Lane L lands at k-row 2b + L/32, position L%32, so it
-// fetches chunk (L%32) ^ (4 (k-row % 4)).  `r` starts at the tile's first
-// column; ncols columns exist from there.
+// k-row tile (bf16): 32 load instructions of 2 k-rows x 512 bytes; wave w
+// issues blocks 8w .. 8w+7.  Lane L lands at k-row 2b + L/32, position L%32,
+// so it fetches chunk (L%32) ^ (4 (k-row % 4)).  `r` starts at the tile's
+// first column; ncols columns exist from there.
+// k-row tile (fp32): 32 load instructions of one k-row x 1 KiB; lane L lands
+// at position L of k-row b and fetches chunk L ^ (8 ((b / 16) % 2)), so the
+// two half-waves of a column read (k-rows k and k + 16) use opposite halves
+// of the banks.
+template <typename T>
 __device__ __forceinline__ void dma_krows(const rsrc_t &r, int64_t ld, int64_t k0, int64_t K, int64_t ncols,
                                           uint16_t *tile, int tid) {
     const int L = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t nlast = ((ncols - 1) >> 3) << 3;
+    constexpr int P = Op<T>::PER;
+    const int64_t nlast = ((ncols - 1) / P) * P;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         const int b = 8 * w + q;
-        const int kl = 2 * b + (L >> 5);
-        const int c = (L & 31) ^ (4 * (kl & 3));
-        int64_t nc = 8 * c;
+        int kl, c;
+        if constexpr (sizeof(T) == 2) {
+            kl = 2 * b + (L >> 5);
+            c = (L & 31) ^ (4 * (kl & 3));
+        } else {
+            kl = b;
+            c = L ^ (8 * ((b >> 4) & 1));
+        }
+        int64_t nc = P * c;
         if (nc > nlast) nc = nlast;
         int64_t k = k0 + kl;
         if (k > K - 1) k = K - 1;
-        dma16(r, 2 * (k * ld + nc), tile + b * 512);
+        dma16(r, (int64_t)sizeof(T) * (k * ld + nc), tile + b * 512);
     }
 }
 
-// A (or N x K B) fragment: 8 consecutive k of chunk c of row r.
-__device__ __forceinline__ bf8v frag_rows(const uint16_t *tile, int r, int c) {
-    return *reinterpret_cast<const bf8v *>(tile + r * TK + ((c ^ ((r >> 1) & 7)) << 3));
+// A (or N x K B) fragment: the 16-byte chunk c of row r (8 bf16 or 4 fp32
+// consecutive k).
+template <typename T>
+__device__ __forceinline__ typename Op<T>::V frag_rows(const uint16_t *tile, int r, int c) {
+    return *reinterpret_cast<const typename Op<T>::V *>(tile + r * 64 + ((c ^ ((r >> 1) & 7)) << 3));
+}
+
+// K x N fp32 fragment: the 4 consecutive k from 16 (lane / 32) + 4 q of
+// column n0w + lane % 32, one read per k-row.
+__device__ __forceinline__ f4v frag_krows_f32(const uint16_t *tile, int q, int n0w, int tid) {
+    const int l = tid & 63, h = l >> 5;
+    const int n = n0w + (l & 31);
+    const float *base = reinterpret_cast<const float *>(tile) + (16 * h + 4 * q) * 256 +
+                        ((((n >> 2) ^ (8 * h)) << 2) | (n & 3));
+    return f4v{base[0], base[256], base[512], base[768]};
 }
 
 // K x N B fragment (8 consecutive k at kk + 8 (lane / 32), column
@@ -150,15 +190,18 @@ __device__ __forceinline__ bf8v frag_krows(const uint16_t *tile, int kk, int n0w
     return *reinterpret_cast<const bf8v *>(both);
 }
 
-__device__ __forceinline__ float sum_sq(const bf8v v) {
+template <typename V>
+__device__ __forceinline__ float sum_sq(const V v) {
     float s = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < (int)(sizeof(V) / sizeof(v[0])); ++e) {
         const float x = (float)v[e];
         s += x * x;
     }
     return s;
 }
+
+inline int64_t elt_bytes(gs_dtype t) { return t == GS_BF16 ? 2 : 4; }
 
 template <typename TO> __device__ __forceinline__ TO to_out(float v);
 template <> __device__ __forceinline__ float to_out<float>(float v) { return v; }
@@ -177,75 +220,93 @@ __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 *
 // and l + 32 hold the two k-halves of a row); when SQB && sqb, sb[j] does the same
 // for row wn + 32 j + lane % 32 of an N x K operand.  Returns once the last
 // MFMA is issued; the stages stay in use until the caller's next barrier.
-template <bool BNN, bool SQA, bool SQB>
+template <typename T, bool BNN, bool SQA, bool SQB>
 __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n0, uint16_t *lds,
                                         f16v acc[4][4], bool sqa, float sq[4], bool sqb, float sb[4],
                                         int tid) {
-    const int l = tid & 63, w = tid >> 6;
+    constexpr int TK = Op<T>::TK, P = Op<T>::PER;
+    constexpr int64_t ES = sizeof(T);
+    typedef typename Op<T>::V V;
+    const int l = tid & 63, w = tid >> 6, h = l >> 5;
     const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f16v{};
-    const bf16_t *A = static_cast<const bf16_t *>(g.A);
-    const bf16_t *B = static_cast<const bf16_t *>(g.B);
+    const T *A = static_cast<const T *>(g.A);
+    const T *B = static_cast<const T *>(g.B);
     // buffer resources over exactly what this tile reads (row slices end at
-    // column ceil(K / 8) * 8, k-row slices at column ceil(N / 8) * 8)
-    const int64_t k8 = (g.K + 7) / 8 * 8, n8 = (g.N + 7) / 8 * 8;
+    // column ceil(K / P) * P, k-row slices at column ceil(N / P) * P)
+    const int64_t kp = (g.K + P - 1) / P * P, np = (g.N + P - 1) / P * P;
     const int64_t rows_a = (g.M - m0 < TM) ? (g.M - m0) : TM;
-    const rsrc_t ra = make_rsrc(A + m0 * g.lda, 2 * ((rows_a - 1) * g.lda + k8));
+    const rsrc_t ra = make_rsrc(A + m0 * g.lda, ES * ((rows_a - 1) * g.lda + kp));
     int64_t rows_b, cols_b;
     rsrc_t rb;
     if (BNN) {
         cols_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
-        const int64_t span = (n8 - n0 < TN) ? (n8 - n0) : TN;
-        rb = make_rsrc(B + n0, 2 * ((g.K - 1) * g.ldb + span));
+        const int64_t span = (np - n0 < TN) ? (np - n0) : TN;
+        rb = make_rsrc(B + n0, ES * ((g.K - 1) * g.ldb + span));
         rows_b = 0;
     } else {
         rows_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
-        rb = make_rsrc(B + n0 * g.ldb, 2 * ((rows_b - 1) * g.ldb + k8));
+        rb = make_rsrc(B + n0 * g.ldb, ES * ((rows_b - 1) * g.ldb + kp));
         cols_b = 0;
     }
-
 
     const int64_t nk = (g.K + TK - 1) / TK;
     auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
     auto issue = [&](int64_t kt) {
         uint16_t *st = stage(kt);
-        dma_rows(ra, g.lda, rows_a, kt * TK, g.K, st, tid);
-        if (BNN) dma_krows(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid);
-        else dma_rows(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid);
+        dma_rows<T>(ra, g.lda, rows_a, kt * TK, g.K, st, tid);
+        if (BNN) dma_krows<T>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid);
+        else dma_rows<T>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid);
     };
-    struct Frags { bf8v a[4], b[4]; };
-    auto load_frags = [&](const uint16_t *st, int kk, Frags &f) {
-        const int c = (kk >> 3) + (l >> 5);
+    // Substep q (0..3) of a K-step: bf16 lanes take chunk 2q + lane / 32 (k
+    // from 16 q + 8 (lane / 32)); fp32 lanes take chunk 4 (lane / 32) + q (k
+    // from 16 (lane / 32) + 4 q), A and B alike, so each MFMA pairs the same k.
+    struct Frags { V a[4], b[4]; };
+    auto load_frags = [&](const uint16_t *st, int q, Frags &f) {
+        const int c = (sizeof(T) == 2) ? 2 * q + h : 4 * h + q;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) f.a[i] = frag_rows(st, wm + 32 * i + (l & 31), c);
+        for (int i = 0; i < 4; ++i) f.a[i] = frag_rows<T>(st, wm + 32 * i + (l & 31), c);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-            f.b[j] = BNN ? frag_krows(st + OPT, kk, wn + 32 * j, tid) : frag_rows(st + OPT, wn + 32 * j + (l & 31), c);
+        for (int j = 0; j < 4; ++j) {
+            if constexpr (!BNN) f.b[j] = frag_rows<T>(st + OPT, wn + 32 * j + (l & 31), c);
+            else if constexpr (sizeof(T) == 2) f.b[j] = frag_krows(st + OPT, 16 * q, wn + 32 * j, tid);
+            else f.b[j] = frag_krows_f32(st + OPT, q, wn + 32 * j, tid);
+        }
     };
     // In the last K-step, zero the fragment elements at k >= K (both operands:
     // what lies there in LDS is row padding or a re-read chunk, possibly NaN).
     Frags f0, f1;
-    auto mask_tail = [&](Frags &f, int64_t kt, int kk) {
+    auto mask_tail = [&](Frags &f, int64_t kt, int q) {
         if (kt * TK + TK <= g.K) return;                 // a full step
-        const int64_t kb = kt * TK + kk + 8 * (l >> 5);  // first k of this lane's fragments
+        const int64_t kb = kt * TK + ((sizeof(T) == 2) ? 16 * q + 8 * h : 16 * h + 4 * q);
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
+        for (int e = 0; e < P; ++e)
             if (kb + e >= g.K) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) f.a[i][e] = (__bf16)0.f;
+                for (int i = 0; i < 4; ++i) f.a[i][e] = (typename Op<T>::E)0.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) f.b[j][e] = (__bf16)0.f;
+                for (int j = 0; j < 4; ++j) f.b[j][e] = (typename Op<T>::E)0.f;
             }
     };
     auto mma = [&](const Frags &f) {
+        if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][e], f.b[j][e], acc[i][j], 0, 0, 0);
+        }
         if (SQA && sqa) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) sq[i] += sum_sq(f.a[i]);
@@ -256,22 +317,22 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         }
     };
 
-    // Software pipeline over the four k-substeps of 16 of a step: the
-    // fragments of the next substep are read while the MFMAs of the current
-    // one run.  Before the last substep's MFMAs each wave has its reads of
-    // the current slot back and the next stage landed; one barrier then
-    // hands the current slot to the load of step kt + 2.
+    // Software pipeline over the four substeps of a step: the fragments of
+    // the next substep are read while the MFMAs of the current one run.
+    // Before the last substep's MFMAs each wave has its reads of the current
+    // slot back and the next stage landed; one barrier then hands the
+    // current slot to the load of step kt + 2.
     auto step = [&](int64_t kt, bool next_is_last) {
         const uint16_t *cur = stage(kt);
-        load_frags(cur, 16, f1);
+        load_frags(cur, 1, f1);
         __builtin_amdgcn_sched_barrier(0);
         mma(f0);
         __builtin_amdgcn_sched_barrier(0);
-        load_frags(cur, 32, f0);
+        load_frags(cur, 2, f0);
         __builtin_amdgcn_sched_barrier(0);
         mma(f1);
         __builtin_amdgcn_sched_barrier(0);
-        load_frags(cur, 48, f1);
+        load_frags(cur, 3, f1);
         __builtin_amdgcn_sched_barrier(0);
         mma(f0);
         __builtin_amdgcn_sched_barrier(0);
@@ -300,25 +361,24 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
     {
         const int64_t kt = nk - 1;
         const uint16_t *cur = stage(kt);
-        load_frags(cur, 16, f1);
-        mask_tail(f1, kt, 16);
+        load_frags(cur, 1, f1);
+        mask_tail(f1, kt, 1);
         mma(f0);
-        load_frags(cur, 32, f0);
-        mask_tail(f0, kt, 32);
+        load_frags(cur, 2, f0);
+        mask_tail(f0, kt, 2);
         mma(f1);
-        load_frags(cur, 48, f1);
-        mask_tail(f1, kt, 48);
+        load_frags(cur, 3, f1);
+        mask_tail(f1, kt, 3);
         mma(f0);
         mma(f1);
     }
-
 }
 
 // SCALED: similarity scores instead of the plain product (fp32 output, B
 // stored N x K): out = scale * acc / (||x_row|| ||c_col||) for cosine (row
 // norms from qnorm2 or from the A fragments, column norms from cnorm or from
 // the B fragments), scale * acc for dot.
-template <typename TO, bool BNN, bool SCALED>
+template <typename T, typename TO, bool BNN, bool SCALED>
 __global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm256_kernel(GemmArgs g) {
     extern __shared__ float lds_f[];
@@ -350,7 +410,7 @@ gemm256_kernel(GemmArgs g) {
                             : (g.rownorm2 != nullptr && n0 == 0 && (w & 1) == 0);
     const bool sqb = SCALED && g.cosine && g.cnorm == nullptr && (w >> 1) == 0;
     float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[4] = {0.f, 0.f, 0.f, 0.f};
-    mma_256<BNN, true, SCALED>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
+    mma_256<T, BNN, true, SCALED>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
 
     float *rq = lds_f + LDS_BYTES / sizeof(float);   // SCALED: scale / ||x|| per row of the tile
     float *cn = rq + TM;                             // SCALED: 1 / ||c|| per column of the tile
@@ -476,7 +536,7 @@ constexpr size_t SWEEP_LDS_BYTES = LDS_BYTES + 4 * TM * sizeof(float);   // + rq
 
 // ROWN: row norms of T from its fragments (cosine without qnorm2); COLN:
 // column norms of R from its fragments (cosine without cnorm).
-template <bool SOFTMAX, bool ROWN, bool COLN>
+template <typename T, bool SOFTMAX, bool ROWN, bool COLN>
 __global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
 sweep256_kernel(GemmArgs g) {
     extern __shared__ float lds_f[];
@@ -517,8 +577,8 @@ sweep256_kernel(GemmArgs g) {
         // than kept live (and spilled) across the whole sweep
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
-        if (ROWN && nt == 0) mma_256<false, ROWN, COLN>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
-        else mma_256<false, false, COLN>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
+        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
+        else mma_256<T, false, false, COLN>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
 
         // cosine factors of the rows (first block) and of this block's columns
         if (nt == 0) {
@@ -654,16 +714,16 @@ sweep256_kernel(GemmArgs g) {
     softmax_rows(out, g.ldc, m0, (g.M - m0 < TM) ? (g.M - m0) : TM, g.N, rmax, rinv, vec_out, NTH);
 }
 
-template <typename TO>
+template <typename T, typename TO>
 hipError_t launch_to(bool b_nn, const GemmArgs &a, hipStream_t s) {
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_kernel<TO, true, false>)
-                         : reinterpret_cast<const void *>(gemm256_kernel<TO, false, false>);
+    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_kernel<T, TO, true, false>)
+                         : reinterpret_cast<const void *>(gemm256_kernel<T, TO, false, false>);
     hipError_t e = raise_lds_limit(k, LDS_BYTES);
     if (e != hipSuccess) return e;
-    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<TO, true, false>), grid, dim3(NTH), LDS_BYTES, s, a);
-    else hipLaunchKernelGGL((gemm256_kernel<TO, false, false>), grid, dim3(NTH), LDS_BYTES, s, a);
+    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<T, TO, true, false>), grid, dim3(NTH), LDS_BYTES, s, a);
+    else hipLaunchKernelGGL((gemm256_kernel<T, TO, false, false>), grid, dim3(NTH), LDS_BYTES, s, a);
     return hipGetLastError();
 }
 
@@ -713,37 +773,42 @@ __global__ void __launch_bounds__(256) rows_softmax_kernel(float *A, int64_t lda
     for (int64_t c = l; c < M; c += 64) a[c] = __expf(a[c] - m) * iz;
 }
 
-template <bool SOFTMAX, bool ROWN, bool COLN>
+template <typename T, bool SOFTMAX, bool ROWN, bool COLN>
 hipError_t launch_sweep(const GemmArgs &a, hipStream_t s) {
     const int64_t nM = (a.M + TM - 1) / TM;
     const dim3 grid((unsigned)(8 * ((nM + 7) / 8)));
-    const void *k = reinterpret_cast<const void *>(sweep256_kernel<SOFTMAX, ROWN, COLN>);
+    const void *k = reinterpret_cast<const void *>(sweep256_kernel<T, SOFTMAX, ROWN, COLN>);
     hipError_t e = raise_lds_limit(k, SWEEP_LDS_BYTES);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((sweep256_kernel<SOFTMAX, ROWN, COLN>), grid, dim3(NTH), SWEEP_LDS_BYTES, s, a);
+    hipLaunchKernelGGL((sweep256_kernel<T, SOFTMAX, ROWN, COLN>), grid, dim3(NTH), SWEEP_LDS_BYTES, s, a);
     return hipGetLastError();
 }
 
-template <bool SOFTMAX>
+template <typename T, bool SOFTMAX>
 hipError_t launch_sweep_norms(const GemmArgs &a, hipStream_t s) {
     const bool rown = a.cosine && a.qnorm2 == nullptr, coln = a.cosine && a.cnorm == nullptr;
-    if (rown) return coln ? launch_sweep<SOFTMAX, true, true>(a, s) : launch_sweep<SOFTMAX, true, false>(a, s);
-    return coln ? launch_sweep<SOFTMAX, false, true>(a, s) : launch_sweep<SOFTMAX, false, false>(a, s);
+    if (rown) return coln ? launch_sweep<T, SOFTMAX, true, true>(a, s) : launch_sweep<T, SOFTMAX, true, false>(a, s);
+    return coln ? launch_sweep<T, SOFTMAX, false, true>(a, s) : launch_sweep<T, SOFTMAX, false, false>(a, s);
 }
 
-}  // namespace
-
-hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s) {
-    if (a.M == 0 || a.N == 0) return hipSuccess;
+template <typename T>
+hipError_t launch_scores(const GemmArgs &a, bool softmax, hipStream_t s) {
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
     GemmArgs b = a;
     if (softmax) b.scale = a.scale * a.beta;      // the softmax acts on beta * score
-    const void *k = reinterpret_cast<const void *>(gemm256_kernel<float, false, true>);
+    const void *k = reinterpret_cast<const void *>(gemm256_kernel<T, float, false, true>);
     hipError_t e = raise_lds_limit(k, SCORES_LDS_BYTES);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm256_kernel<float, false, true>), grid, dim3(NTH), SCORES_LDS_BYTES, s, b);
-    e = hipGetLastError();
+    hipLaunchKernelGGL((gemm256_kernel<T, float, false, true>), grid, dim3(NTH), SCORES_LDS_BYTES, s, b);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_scores256(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s) {
+    if (a.M == 0 || a.N == 0) return hipSuccess;
+    hipError_t e = (t == GS_BF16) ? launch_scores<bf16_t>(a, softmax, s) : launch_scores<float>(a, softmax, s);
     if (e != hipSuccess) return e;
     return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
 }
@@ -763,35 +828,36 @@ hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int
     return hipSuccess;
 }
 
-bool sweep256_fits(const GemmArgs &a) {
+bool sweep256_fits(gs_dtype t, const GemmArgs &a) {
     // at least one 256-row block per CU; offsets within the buffer resources
     // below 2^31
     if ((a.M + TM - 1) / TM < 256) return false;
-    const int64_t lim = (int64_t)1 << 31;
-    return 2 * (TM * a.lda + a.K + 8) < lim && 2 * (TN * a.ldb + a.K + 8) < lim;
+    const int64_t es = elt_bytes(t), lim = (int64_t)1 << 31;
+    return es * (TM * a.lda + a.K + 8) < lim && es * (TN * a.ldb + a.K + 8) < lim;
 }
 
-hipError_t launch_sweep256(bool softmax, const GemmArgs &a, hipStream_t s) {
+hipError_t launch_sweep256(gs_dtype t, bool softmax, const GemmArgs &a, hipStream_t s) {
     if (a.M == 0 || a.N == 0) return hipSuccess;
-    return softmax ? launch_sweep_norms<true>(a, s) : launch_sweep_norms<false>(a, s);
+    if (t == GS_BF16) return softmax ? launch_sweep_norms<bf16_t, true>(a, s) : launch_sweep_norms<bf16_t, false>(a, s);
+    return softmax ? launch_sweep_norms<float, true>(a, s) : launch_sweep_norms<float, false>(a, s);
 }
 
-bool gemm256_fits(const GemmArgs &a, bool b_nn) {
+bool gemm256_fits(gs_dtype t, const GemmArgs &a, bool b_nn) {
     // at least one full round of 256 x 256 tiles over the 256 CUs; smaller
     // products keep the 128 x 128 tiles, which spread over more CUs
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
     if (total < 256) return false;
     // byte offsets within a tile's buffer resources stay below 2^31
-    const int64_t lim = (int64_t)1 << 31;
-    if (2 * (TM * a.lda + a.K + 8) >= lim) return false;
-    if (b_nn) return 2 * (a.K * a.ldb + TN) < lim;
-    return 2 * (TN * a.ldb + a.K + 8) < lim;
+    const int64_t es = elt_bytes(t), lim = (int64_t)1 << 31;
+    if (es * (TM * a.lda + a.K + 8) >= lim) return false;
+    if (b_nn) return es * (a.K * a.ldb + TN) < lim;
+    return es * (TN * a.ldb + a.K + 8) < lim;
 }
 
-hipError_t launch_gemm256(gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s) {
+hipError_t launch_gemm256(gs_dtype t, gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s) {
     if (a.M == 0 || a.N == 0) return hipSuccess;
-    if (tout == GS_BF16) return launch_to<bf16_t>(b_nn, a, s);
-    return launch_to<float>(b_nn, a, s);
+    if (t == GS_BF16) return (tout == GS_BF16) ? launch_to<bf16_t, bf16_t>(b_nn, a, s) : launch_to<bf16_t, float>(b_nn, a, s);
+    return (tout == GS_BF16) ? launch_to<float, bf16_t>(b_nn, a, s) : launch_to<float, float>(b_nn, a, s);
 }
 
 }  // namespace gs

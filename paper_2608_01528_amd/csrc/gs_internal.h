@@ -124,19 +124,20 @@ struct GemmArgs {
 hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,
                        const GemmArgs &a, hipStream_t s);
 
-// 256 x 256-tile bf16 x bf16 product with a plain store (and optional row
-// norms of A); needs 16-byte aligned operand rows.  gemm256_fits tells whether
-// the product is large enough to fill the chip with such tiles.
-bool gemm256_fits(const GemmArgs &a, bool b_nn);
-hipError_t launch_gemm256(gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s);
+// 256 x 256-tile product with a plain store (and optional row norms of A),
+// both operands of type t (bf16 or fp32) with 16-byte aligned rows.
+// gemm256_fits tells whether the product is large enough to fill the chip
+// with such tiles.
+bool gemm256_fits(gs_dtype t, const GemmArgs &a, bool b_nn);
+hipError_t launch_gemm256(gs_dtype t, gs_dtype tout, bool b_nn, const GemmArgs &a, hipStream_t s);
 // Row sweep of similarity (softmax = false) or attention scores over 256 x
-// 256 blocks, bf16 x bf16 with 16-byte aligned rows (B stored N x K).
-bool sweep256_fits(const GemmArgs &a);
-hipError_t launch_sweep256(bool softmax, const GemmArgs &a, hipStream_t s);
+// 256 blocks, same operand conditions (B stored N x K).
+bool sweep256_fits(gs_dtype t, const GemmArgs &a);
+hipError_t launch_sweep256(gs_dtype t, bool softmax, const GemmArgs &a, hipStream_t s);
 // Scores written to memory (similarity with S, or attention): the 256 x 256
 // product kernel with a scaled-score epilogue, then a row pass (argmax, or
 // softmax in place).  Same operand conditions as launch_gemm256 (B N x K).
-hipError_t launch_scores256(const GemmArgs &a, bool softmax, hipStream_t s);
+hipError_t launch_scores256(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s);
 // Row pass over a B x M fp32 score matrix (leading dimension ld): softmax in
 // place, or the row argmax (lowest index on ties) into argmax when non-null.
 hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int64_t M, int32_t *argmax,

@@ -580,13 +580,17 @@ def test_bf16_pipelined_prob2vec_similarity(B, M, D):
     check_argmax(host(idx), So, band_rel=1e-2)
 
 
-# ------------------------ bf16 large-tile path (>= 256 tiles of 256 x 256)
+# --------------------- large-tile path (>= 256 tiles of 256 x 256), bf16 and fp32
 #
 # Products large enough for the 256 x 256 tiles, with ragged M and N, K tails
-# that are neither multiples of the K-step (32) nor of 8, NaN-filled row
-# padding, and both output types.  Q and R are arbitrary here: project,
-# prob2vec and reconstruct are plain products of their operands.  Rows are
-# sampled: the first and last, the tile boundaries and random rows.
+# that are neither multiples of the K-step (64 bf16, 32 fp32) nor of a
+# 16-byte chunk, NaN-filled row padding, and both output types.  Q and R are
+# arbitrary here: project, prob2vec and reconstruct are plain products of
+# their operands.  Rows are sampled: the first and last, the tile boundaries
+# and random rows.
+
+OP_DTYPES = [torch.bfloat16, torch.float32]
+
 
 def _tile_rows(B, seed):
     fixed = [0, 1, 255, 256, 511, 512, B // 2, B - 2, B - 1]
@@ -594,18 +598,39 @@ def _tile_rows(B, seed):
     return np.array(sorted(set(f for f in fixed if f < B) | set(int(x) for x in rnd)))
 
 
-def _bf16_mat(rows, cols, seed, scale=1.0):
-    return wl.round_bf16((scale * np.random.default_rng(seed).standard_normal((rows, cols))).astype(np.float32))
+def _mat(rows, cols, seed, dtype, scale=1.0):
+    """Seeded matrix, exactly representable in `dtype`."""
+    x = (scale * np.random.default_rng(seed).standard_normal((rows, cols))).astype(np.float32)
+    return wl.round_bf16(x) if dtype == torch.bfloat16 else x
 
 
+def _ld(cols, dtype, extra=0):
+    per = 8 if dtype == torch.bfloat16 else 4          # elements per 16 bytes
+    return (cols + per - 1) // per * per + extra
+
+
+def nan_padded(a, ld, dtype):
+    """Device matrix with leading dimension ld whose padding columns hold NaN."""
+    a = np.asarray(a, np.float32)
+    full = np.full((a.shape[0], ld), np.nan, np.float32)
+    full[:, : a.shape[1]] = a
+    return dev(full, dtype)[:, : a.shape[1]]
+
+
+def _name(dt):
+    return "bf16" if dt == torch.bfloat16 else "f32"
+
+
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
 @pytest.mark.parametrize("D", [300, 4100])
-@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
-def test_bf16_large_tile_project(D, out_dtype):
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=_name)
+def test_large_tile_project(op_dtype, D, out_dtype):
     B, r = 8200, 2000
-    print("large-tile project", B, D, r, out_dtype, flush=True)
-    X, Q = _bf16_mat(B, D, 1), _bf16_mat(r, D, 2, 1 / np.sqrt(D))
-    ld = (D + 7) // 8 * 8
-    T, xn = gsm.gs_project(nan_padded_bf16(X, ld), nan_padded_bf16(Q, ld), out_dtype=out_dtype, xnorm2=True)
+    print("large-tile project", _name(op_dtype), B, D, r, _name(out_dtype), flush=True)
+    X, Q = _mat(B, D, 1, op_dtype), _mat(r, D, 2, op_dtype, 1 / np.sqrt(D))
+    ld = _ld(D, op_dtype)
+    T, xn = gsm.gs_project(nan_padded(X, ld, op_dtype), nan_padded(Q, ld, op_dtype), out_dtype=out_dtype,
+                           xnorm2=True)
     torch.cuda.synchronize()
     rows = _tile_rows(B, 3)
     Tr = host(T[rows])
@@ -615,12 +640,13 @@ def test_bf16_large_tile_project(D, out_dtype):
     np.testing.assert_allclose(host(xn), oracle.row_norms(X) ** 2, rtol=1e-4)
 
 
-@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
-def test_bf16_large_tile_reconstruct(out_dtype):
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=_name)
+def test_large_tile_reconstruct(op_dtype, out_dtype):
     B, r, D = 2100, 45, 7700
-    print("large-tile reconstruct", B, r, D, out_dtype, flush=True)
-    T, Q = _bf16_mat(B, r, 4), _bf16_mat(r, D, 5)
-    X = gsm.gs_reconstruct(nan_padded_bf16(T, (r + 7) // 8 * 8), nan_padded_bf16(Q, (D + 7) // 8 * 8 + 8),
+    print("large-tile reconstruct", _name(op_dtype), B, r, D, _name(out_dtype), flush=True)
+    T, Q = _mat(B, r, 4, op_dtype), _mat(r, D, 5, op_dtype)
+    X = gsm.gs_reconstruct(nan_padded(T, _ld(r, op_dtype), op_dtype), nan_padded(Q, _ld(D, op_dtype, 8), op_dtype),
                            out_dtype=out_dtype)
     torch.cuda.synchronize()
     rows = _tile_rows(B, 6)
@@ -632,12 +658,15 @@ def test_bf16_large_tile_reconstruct(out_dtype):
     assert rowrel(host(X[B - 1:B]), oracle.reconstruct(T[B - 1:B], Q)) <= tol
 
 
-def test_bf16_large_tile_prob2vec():
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+def test_large_tile_prob2vec(op_dtype):
     B, M, r = 8200, 2050, 2000
-    print("large-tile prob2vec", B, M, r, flush=True)
-    P = wl.round_bf16(wl.dirichlet_probs(B, M, 0.5, 7))
-    R = _bf16_mat(M, r, 8)
-    T = gsm.gs_prob2vec(nan_padded_bf16(P, (M + 7) // 8 * 8), nan_padded_bf16(R, (r + 7) // 8 * 8),
+    print("large-tile prob2vec", _name(op_dtype), B, M, r, flush=True)
+    P = wl.dirichlet_probs(B, M, 0.5, 7)
+    if op_dtype == torch.bfloat16:
+        P = wl.round_bf16(P)
+    R = _mat(M, r, 8, op_dtype)
+    T = gsm.gs_prob2vec(nan_padded(P, _ld(M, op_dtype), op_dtype), nan_padded(R, _ld(r, op_dtype), op_dtype),
                         out_dtype=torch.float32)
     torch.cuda.synchronize()
     rows = _tile_rows(B, 9)
@@ -646,30 +675,32 @@ def test_bf16_large_tile_prob2vec():
     assert rowrel(Tr, oracle.prob2vec(P[rows], R)) <= TOL_F32
 
 
-# ------------------- bf16 row sweep (>= 256 row blocks of 256, 256-column blocks)
+# ------------- row sweep / scored products (>= 256 row blocks of 256, 256-column blocks)
 #
 # With Q the identity, coordinates and codebook coordinates are themselves the
 # D-space vectors, so the oracle's dense cosine / dot similarity and softmax
 # apply directly to T and R.  Ragged row count, a codebook size that leaves a
-# partial column block, r not a multiple of the K-step or of 8, NaN row padding.
+# partial column block, r not a multiple of the K-step or of a 16-byte chunk,
+# NaN row padding; bf16 and fp32 operands.
 
 SWEEP_B, SWEEP_M, SWEEP_R = 65573, 600, 300
 
 
-@pytest.fixture(scope="module")
-def sweep_case():
-    T = _bf16_mat(SWEEP_B, SWEEP_R, 21)
-    R = _bf16_mat(SWEEP_M, SWEEP_R, 22)
-    ld = (SWEEP_R + 7) // 8 * 8
-    Td, Rd = nan_padded_bf16(T, ld), nan_padded_bf16(R, ld)
+@pytest.fixture(scope="module", params=OP_DTYPES, ids=_name)
+def sweep_case(request):
+    dt = request.param
+    T = _mat(SWEEP_B, SWEEP_R, 21, dt)
+    R = _mat(SWEEP_M, SWEEP_R, 22, dt)
+    ld = _ld(SWEEP_R, dt)
+    Td, Rd = nan_padded(T, ld, dt), nan_padded(R, ld, dt)
     rows = _tile_rows(SWEEP_B, 23)
     return T, R, Td, Rd, rows
 
 
 @pytest.mark.parametrize("norms", ["computed", "given"])
-def test_bf16_sweep_similarity_cosine(sweep_case, norms):
+def test_sweep_similarity_cosine(sweep_case, norms):
     T, R, Td, Rd, rows = sweep_case
-    print("sweep similarity cosine", norms, flush=True)
+    print("sweep similarity cosine", Td.dtype, norms, flush=True)
     qn = cn = None
     if norms == "given":
         qn = dev(oracle.row_norms(T) ** 2)
@@ -686,8 +717,9 @@ def test_bf16_sweep_similarity_cosine(sweep_case, norms):
     assert torch.all(Sf.gather(1, idx.long()[:, None])[:, 0] >= Sf.max(dim=1).values).item()
 
 
-def test_bf16_sweep_similarity_dot_argmax_only(sweep_case):
+def test_sweep_similarity_dot_argmax_only(sweep_case):
     T, R, Td, Rd, rows = sweep_case
+    print("sweep similarity dot argmax", Td.dtype, flush=True)
     _, idx = gsm.gs_similarity(Td, Rd, mode="dot", scale=0.5, scores=False)
     torch.cuda.synchronize()
     So = oracle.similarity(T[rows], R, oracle.DOT, 0.5)
@@ -695,9 +727,9 @@ def test_bf16_sweep_similarity_dot_argmax_only(sweep_case):
 
 
 @pytest.mark.parametrize("norms", ["computed", "given"])
-def test_bf16_sweep_attention(sweep_case, norms):
+def test_sweep_attention(sweep_case, norms):
     T, R, Td, Rd, rows = sweep_case
-    print("sweep attention", norms, flush=True)
+    print("sweep attention", Td.dtype, norms, flush=True)
     qn = cn = None
     if norms == "given":
         qn = dev(oracle.row_norms(T) ** 2)
@@ -711,9 +743,10 @@ def test_bf16_sweep_attention(sweep_case, norms):
     assert torch.allclose(A.sum(dim=1), torch.ones(A.shape[0], device=A.device), atol=1e-4)
 
 
-def test_bf16_sweep_cosine_argmax_only(sweep_case):
+def test_sweep_cosine_argmax_only(sweep_case):
     # no scores requested: the fused row sweep, norms taken from T and R
     T, R, Td, Rd, rows = sweep_case
+    print("sweep cosine argmax", Td.dtype, flush=True)
     _, idx = gsm.gs_similarity(Td, Rd, mode="cosine", scores=False)
     torch.cuda.synchronize()
     So = oracle.similarity(T[rows], R, oracle.COSINE)
