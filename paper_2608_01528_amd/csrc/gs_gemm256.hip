@@ -36,7 +36,6 @@ constexpr int TM = 256, TN = 256;
 constexpr int NTH = 256;
 constexpr int NSTAGE = 2;
 constexpr int OPT = TM * 64;        // 16-bit units per staged operand tile (32 KiB)
-constexpr int OPS = 16;             // load instructions per stage and wave
 constexpr int GROUP_M = 4;          // m-tiles that take each n-tile in turn
 constexpr int EP_STRIDE_MAX = 128 * 4 + 32;   // staged fp32 output row: 128 values + 32-byte pad
 constexpr size_t STAGE_BYTES = (size_t)NSTAGE * 2 * OPT * sizeof(uint16_t);
@@ -75,9 +74,12 @@ __device__ __forceinline__ void wait_vm() {
 typedef int rsrc_t __attribute__((ext_vector_type(4)));
 constexpr int RSRC_WORD3 = 0x00020000;
 
-// Resource over `bytes` bytes from base (at most 2^31 - 1); wave-uniform.
+// Resource over the `bytes` bytes from base, starting DMA_BIAS bytes before
+// it (only offsets of at least DMA_BIAS are used); wave-uniform.
+constexpr int DMA_BIAS = 4096;
 __device__ __forceinline__ rsrc_t make_rsrc(const void *base, int64_t bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint64_t a = reinterpret_cast<uint64_t>(base) - DMA_BIAS;
+    bytes += DMA_BIAS;
     const int n = bytes > 0x7fffffff ? 0x7fffffff : (int)bytes;
     rsrc_t r;
     r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
@@ -87,42 +89,55 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, int64_t bytes) {
     return r;
 }
 
-// One buffer->LDS load of 16 bytes per lane: lane l's bytes land at
-// lds + 16 l.  Written as assembly so that the compiler neither waits for
-// these loads before unrelated LDS reads (it cannot tell the stages apart)
-// nor keeps the resource in vector registers; the loop's own vmcnt waits
-// order them.  M0 holds the LDS base; one wait state separates its write
-// from the load.
-__device__ __forceinline__ void dma16(const rsrc_t &r, int64_t byte_off, const uint16_t *lds) {
+// Four buffer->LDS loads of 16 bytes per lane into four consecutive 1 KiB
+// LDS blocks (lane l's bytes of load j land at lds + j KiB + 16 l), from one
+// M0 value: the instruction offset (j KiB) moves both the LDS destination and
+// the memory address, so the lane offset of load j is off[j] + DMA_BIAS -
+// j KiB, which stays positive because the resource starts DMA_BIAS bytes
+// before the operand.  Written as assembly so that the compiler neither
+// waits for these loads before unrelated LDS reads (it cannot tell the
+// stages apart) nor keeps the resource in vector registers; the loop's own
+// vmcnt waits order them.  One wait state separates the M0 write from the
+// first load.
+__device__ __forceinline__ void dma16x4(const rsrc_t &r, const int off[4], const uint16_t *lds) {
     const int m0v = __builtin_amdgcn_readfirstlane((int)(size_t)(const AS_L void *)lds);
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"((int)byte_off), "s"(r), "s"(m0v)
-                 : "memory", "m0");
+    asm volatile(
+        "s_mov_b32 m0, %4\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %0, %5, 0 offen lds\n\t"
+        "buffer_load_dwordx4 %1, %5, 0 offen offset:1024 lds\n\t"
+        "buffer_load_dwordx4 %2, %5, 0 offen offset:2048 lds\n\t"
+        "buffer_load_dwordx4 %3, %5, 0 offen offset:3072 lds"
+        :
+        : "v"(off[0] + DMA_BIAS), "v"(off[1] + DMA_BIAS - 1024), "v"(off[2] + DMA_BIAS - 2048),
+          "v"(off[3] + DMA_BIAS - 3072), "s"(m0v), "s"(r)
+        : "memory", "m0");
 }
 
-// Row tile: 32 load instructions of 8 rows x 128 bytes; wave w issues
-// blocks 8w .. 8w+7.  Lane L lands at row 8b + L/8, position L%8, so it
-// fetches chunk (L%8) ^ (((8b + L/8) >> 1) % 8) = (L%8) ^ (4 (b % 2) + L/16).  `r`
-// starts at the tile's first row; rows past the last one (nrows rows from
-// there) reuse it.
+// Lane byte offset of instruction q (0..7) of this wave's share of a row tile.
 template <typename T>
-__device__ __forceinline__ void dma_rows(const rsrc_t &r, int64_t ld, int64_t nrows, int64_t k0, int64_t K,
-                                         uint16_t *tile, int tid) {
+__device__ __forceinline__ int rows_off(int64_t ld, int64_t nrows, int64_t k0, int64_t K, int tid, int q) {
     constexpr int P = Op<T>::PER;
     const int L = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int w = tid >> 6;
     const int64_t klast = ((K - 1) / P) * P;
+    const int b = 8 * w + q;
+    const int c = (L & 7) ^ (4 * (q & 1) + (L >> 4));
+    int64_t kc = k0 + P * c;
+    if (kc > klast) kc = klast;
+    int64_t row = 8 * b + (L >> 3);
+    if (row > nrows - 1) row = nrows - 1;
+    return (int)((int64_t)sizeof(T) * (row * ld + kc));
+}
+
+// Instructions 4 h .. 4 h + 3 of this wave's share of a row tile.
+template <typename T>
+__device__ __forceinline__ void dma_rows4(const rsrc_t &r, int64_t ld, int64_t nrows, int64_t k0, int64_t K,
+                                          uint16_t *tile, int tid, int h) {
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int off[4];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int b = 8 * w + q;
-        const int c = (L & 7) ^ (4 * (q & 1) + (L >> 4));
-        int64_t kc = k0 + P * c;
-        if (kc > klast) kc = klast;
-        int64_t row = 8 * b + (L >> 3);
-        if (row > nrows - 1) row = nrows - 1;
-        dma16(r, (int64_t)sizeof(T) * (row * ld + kc), tile + b * 512);
-    }
+    for (int j = 0; j < 4; ++j) off[j] = rows_off<T>(ld, nrows, k0, K, tid, 4 * h + j);
+    dma16x4(r, off, tile + (8 * w + 4 * h) * 512);
 }
 
 // k-row tile (bf16): 32 load instructions of 2 k-rows x 512 bytes; wave w
@@ -134,29 +149,35 @@ __device__ __forceinline__ void dma_rows(const rsrc_t &r, int64_t ld, int64_t nr
 // two half-waves of a column read (k-rows k and k + 16) use opposite halves
 // of the banks.
 template <typename T>
-__device__ __forceinline__ void dma_krows(const rsrc_t &r, int64_t ld, int64_t k0, int64_t K, int64_t ncols,
-                                          uint16_t *tile, int tid) {
+__device__ __forceinline__ int krows_off(int64_t ld, int64_t k0, int64_t K, int64_t ncols, int tid, int q) {
     const int L = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int w = tid >> 6;
     constexpr int P = Op<T>::PER;
     const int64_t nlast = ((ncols - 1) / P) * P;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        const int b = 8 * w + q;
-        int kl, c;
-        if constexpr (sizeof(T) == 2) {
-            kl = 2 * b + (L >> 5);
-            c = (L & 31) ^ (4 * (kl & 3));
-        } else {
-            kl = b;
-            c = L ^ (8 * ((b >> 4) & 1));
-        }
-        int64_t nc = P * c;
-        if (nc > nlast) nc = nlast;
-        int64_t k = k0 + kl;
-        if (k > K - 1) k = K - 1;
-        dma16(r, (int64_t)sizeof(T) * (k * ld + nc), tile + b * 512);
+    const int b = 8 * w + q;
+    int kl, c;
+    if constexpr (sizeof(T) == 2) {
+        kl = 2 * b + (L >> 5);
+        c = (L & 31) ^ (4 * (kl & 3));
+    } else {
+        kl = b;
+        c = L ^ (8 * ((b >> 4) & 1));
     }
+    int64_t nc = P * c;
+    if (nc > nlast) nc = nlast;
+    int64_t k = k0 + kl;
+    if (k > K - 1) k = K - 1;
+    return (int)((int64_t)sizeof(T) * (k * ld + nc));
+}
+
+template <typename T>
+__device__ __forceinline__ void dma_krows4(const rsrc_t &r, int64_t ld, int64_t k0, int64_t K, int64_t ncols,
+                                           uint16_t *tile, int tid, int h) {
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int off[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) off[j] = krows_off<T>(ld, k0, K, ncols, tid, 4 * h + j);
+    dma16x4(r, off, tile + (8 * w + 4 * h) * 512);
 }
 
 // A (or N x K B) fragment: the 16-byte chunk c of row r (8 bf16 or 4 fp32
@@ -255,11 +276,13 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 
     const int64_t nk = (g.K + TK - 1) / TK;
     auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
-    auto issue = [&](int64_t kt) {
+    // part p (0..1) of this wave's loads of stage kt: instructions 4p ..
+    // 4p + 3 (of 8) of each operand
+    auto issue_part = [&](int64_t kt, int p) {
         uint16_t *st = stage(kt);
-        dma_rows<T>(ra, g.lda, rows_a, kt * TK, g.K, st, tid);
-        if (BNN) dma_krows<T>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid);
-        else dma_rows<T>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid);
+        dma_rows4<T>(ra, g.lda, rows_a, kt * TK, g.K, st, tid, p);
+        if (BNN) dma_krows4<T>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid, p);
+        else dma_rows4<T>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid, p);
     };
     // Substep q (0..3) of a K-step: bf16 lanes take chunk 2q + lane / 32 (k
     // from 16 q + 8 (lane / 32)); fp32 lanes take chunk 4 (lane / 32) + q (k
@@ -318,16 +341,20 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
     };
 
     // Software pipeline over the four substeps of a step: the fragments of
-    // the next substep are read while the MFMAs of the current one run.
-    // Before the last substep's MFMAs each wave has its reads of the current
-    // slot back and the next stage landed; one barrier then hands the
-    // current slot to the load of step kt + 2.
+    // the next substep are read while the MFMAs of the current one run, and
+    // the loads of the next stage (into the slot the previous step read) go
+    // out in two parts before the first two substeps, so they never queue
+    // up in front of the MFMAs.  Before the last substep's MFMAs each
+    // wave has its loads landed and its reads of the current slot back; one
+    // barrier then makes the next stage visible and frees the current slot.
     auto step = [&](int64_t kt, bool next_is_last) {
         const uint16_t *cur = stage(kt);
+        issue_part(kt + 1, 0);
         load_frags(cur, 1, f1);
         __builtin_amdgcn_sched_barrier(0);
         mma(f0);
         __builtin_amdgcn_sched_barrier(0);
+        issue_part(kt + 1, 1);
         load_frags(cur, 2, f0);
         __builtin_amdgcn_sched_barrier(0);
         mma(f1);
@@ -336,22 +363,17 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         __builtin_amdgcn_sched_barrier(0);
         mma(f0);
         __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(0);       // this wave's reads and loads have returned
+        __builtin_amdgcn_s_waitcnt(0);       // this wave's loads and reads have returned
         __builtin_amdgcn_s_barrier();        // ... and every other wave's
-        if (kt + 2 < nk) issue(kt + 2);      // into the slot just read
         load_frags(stage(kt + 1), 0, f0);
         if (next_is_last) mask_tail(f0, kt + 1, 0);
         __builtin_amdgcn_sched_barrier(0);
         mma(f1);
     };
 
-    issue(0);
-    if (nk > 1) {
-        issue(1);
-        wait_vm<OPS>();                      // stage 0 has landed (stage 1 may be in flight)
-    } else {
-        wait_vm<0>();
-    }
+    issue_part(0, 0);
+    issue_part(0, 1);
+    wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     load_frags(stage(0), 0, f0);
     if (nk == 1) mask_tail(f0, 0, 0);
@@ -832,7 +854,7 @@ bool sweep256_fits(gs_dtype t, const GemmArgs &a) {
     // at least one 256-row block per CU; offsets within the buffer resources
     // below 2^31
     if ((a.M + TM - 1) / TM < 256) return false;
-    const int64_t es = elt_bytes(t), lim = (int64_t)1 << 31;
+    const int64_t es = elt_bytes(t), lim = ((int64_t)1 << 31) - 8192;
     return es * (TM * a.lda + a.K + 8) < lim && es * (TN * a.ldb + a.K + 8) < lim;
 }
 
@@ -848,7 +870,7 @@ bool gemm256_fits(gs_dtype t, const GemmArgs &a, bool b_nn) {
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
     if (total < 256) return false;
     // byte offsets within a tile's buffer resources stay below 2^31
-    const int64_t es = elt_bytes(t), lim = (int64_t)1 << 31;
+    const int64_t es = elt_bytes(t), lim = ((int64_t)1 << 31) - 8192;
     if (es * (TM * a.lda + a.K + 8) >= lim) return false;
     if (b_nn) return es * (a.K * a.ldb + TN) < lim;
     return es * (TN * a.ldb + a.K + 8) < lim;
