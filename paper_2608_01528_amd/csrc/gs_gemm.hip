@@ -1019,6 +1019,19 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
                          (epi != EPI_BIND || rows16(a.A2, a.lda2));
     a.dma = rows_ok && ta == GS_BF16;   // the 128 x 128 pipelined loop is bf16 only
     if (epi == EPI_STORE && rows_ok && gemm256_fits(ta, a, b_nn)) return launch_gemm256(ta, tout, b_nn, a, s);
+    if (epi == EPI_BIND && rows_ok && tout == GS_F32 && gemm256_fits(ta, a, b_nn)) {
+        // bound product on the large tiles: X = T Q, then X = X .* (T2 Q) in
+        // the second product's epilogue (fp32 X holds the first factor exactly)
+        GemmArgs first = a, second = a;
+        first.A2 = nullptr;
+        second.A = a.A2;
+        second.lda = a.lda2;
+        second.A2 = nullptr;
+        second.mul_out = 1;
+        hipError_t e = launch_gemm256(ta, tout, b_nn, first, s);
+        if (e != hipSuccess) return e;
+        return launch_gemm256(ta, tout, b_nn, second, s);
+    }
     bool veca = vec_ok(a.A, ta, a.lda, a.K);
     if (epi == EPI_BIND) veca = veca && vec_ok(a.A2, ta, a.lda2, a.K);
     const bool vecb = b_nn ? vec_ok(a.B, tb, a.ldb, a.N) : vec_ok(a.B, tb, a.ldb, a.K);

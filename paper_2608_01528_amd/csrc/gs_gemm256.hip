@@ -510,6 +510,13 @@ gemm256_kernel(GemmArgs g) {
                     v = __builtin_bit_cast(u32x4, x);
                 }
                 TO *dst = C + (m0 + wm + 64 * h + rr) * g.ldc + (n0 + wn + cc * EPC);
+                if constexpr (sizeof(TO) == 4 && !SCALED) {
+                    if (g.mul_out) {   // second factor of a bound product
+                        const f4v x = __builtin_bit_cast(f4v, v) *
+                                      __builtin_nontemporal_load(reinterpret_cast<const f4v *>(dst));
+                        v = __builtin_bit_cast(u32x4, x);
+                    }
+                }
                 // streaming store: the output is not re-read by this kernel and
                 // should not displace the operand slices other tiles share in L2
                 __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dst));
@@ -522,6 +529,9 @@ gemm256_kernel(GemmArgs g) {
                 if (grow < g.M && gcol < g.N) {
                     TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
                     if constexpr (SCALED) x = x * rq[wm + 64 * h + rr] * cn[wn + cc];
+                    if constexpr (sizeof(TO) == 4 && !SCALED) {
+                        if (g.mul_out) x = x * C[grow * g.ldc + gcol];
+                    }
                     C[grow * g.ldc + gcol] = x;
                 }
             }

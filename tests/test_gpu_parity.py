@@ -659,6 +659,28 @@ def test_large_tile_reconstruct(op_dtype, out_dtype):
 
 
 @pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=_name)
+def test_large_tile_bind(op_dtype, out_dtype):
+    # X = (T Q) .* (T2 Q): with an fp32 output the large-tile path forms the
+    # two products one after the other, the second multiplied into the first
+    B, r, D = 2100, 45, 7700
+    print("large-tile bind", _name(op_dtype), B, r, D, _name(out_dtype), flush=True)
+    T, T2, Q = _mat(B, r, 31, op_dtype), _mat(B, r, 32, op_dtype), _mat(r, D, 33, op_dtype)
+    ldr, ldd = _ld(r, op_dtype), _ld(D, op_dtype, 8)
+    X = gsm.gs_reconstruct(nan_padded(T, ldr, op_dtype), nan_padded(Q, ldd, op_dtype),
+                           T2=nan_padded(T2, ldr, op_dtype), bind="mul", out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 34)
+    Xr = host(X[rows])
+    assert np.isfinite(Xr).all()
+    tol = TOL_BF16 if out_dtype == torch.bfloat16 else TOL_F32
+    Xo = oracle.bind(oracle.reconstruct(T[rows], Q), oracle.reconstruct(T2[rows], Q))
+    assert rowrel(Xr, Xo) <= tol
+    last = oracle.bind(oracle.reconstruct(T[B - 1:B], Q), oracle.reconstruct(T2[B - 1:B], Q))
+    assert rowrel(host(X[B - 1:B]), last) <= tol
+
+
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
 def test_large_tile_prob2vec(op_dtype):
     B, M, r = 8200, 2050, 2000
     print("large-tile prob2vec", _name(op_dtype), B, M, r, flush=True)
