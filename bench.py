@@ -317,18 +317,19 @@ def mfma_workload(args, torch, gsm):
     dom_ms = float(np.mean(per[dom]))
     peak = MFMA_PEAK["bf16" if bf else "f32"]
     achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
-    # bf16 plain products with at least 256 tiles of 256 x 256 run on the
-    # large-tile kernel, everything else on the 128 x 128 kernels
+    # products with at least 256 tiles of 256 x 256 (bf16 or fp32 operands,
+    # 16-byte aligned rows) run on the large-tile kernel, the fp32 bound
+    # product as two of its launches; the rest on the 128 x 128 kernels
     def big(m, n):
-        return bf and ((m + 255) // 256) * ((n + 255) // 256) >= 256
+        return ((m + 255) // 256) * ((n + 255) // 256) >= 256
     store = {"project": (B, r, "X Q^T"), "reproject": (B, r, "Y Q^T"), "reconstruct": (B, D, "T Q"),
              "reconstruct_bind": (B, D, "T Q .* T2 Q"), "prob2vec": (B, r, "P R")}
     if dom in store:
         m_, n_, what = store[dom]
-        kernel = "%s (%s)" % ("gemm256_kernel" if big(m_, n_) and dom != "reconstruct_bind" else "gemm_store_kernel",
-                              what)
+        on_big = big(m_, n_) and (dom != "reconstruct_bind" or not bf)
+        kernel = "%s (%s)" % ("gemm256_kernel" if on_big else "gemm_store_kernel", what)
     else:
-        kernel = {"similarity": "gemm_rowsweep_kernel (similarity)", "attention": "gemm_rowsweep_kernel (softmax)"}[dom]
+        kernel = {"similarity": "similarity scores", "attention": "attention weights"}[dom]
     out = {
         "metric": METRIC, "value": B * args.steps / wall, "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
