@@ -46,9 +46,10 @@ wl = None
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress"],
+    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress", "dimsweep"],
                     help="vsa (default, the headline): fused soft selection; large / binary / stress: "
-                         "the matrix-core rows (project, reconstruct + bind, large similarity)")
+                         "the matrix-core rows (project, reconstruct + bind, large similarity); dimsweep: "
+                         "similarity latency against the vector dimension, dense vs Gram-Space")
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--sets", type=int, default=0, help="batch copies to cycle through (0: >= 1 GiB)")
@@ -348,6 +349,72 @@ def mfma_workload(args, torch, gsm):
     print(json.dumps(out), flush=True)
 
 
+def dimsweep_workload(args, torch, gsm):
+    """Similarity query latency against the original vector dimension D (the
+    setting of the paper's codebook-latency table, Sec. 4): a global codebook
+    of M = 40 bipolar entries (4 attributes x 10 values), D = 256 .. 8192.
+    Dense: cosine similarity of D-space queries X against the codebook C (a
+    K = D contraction on the same kernels); Gram-Space: the same scores from
+    the coordinates T = X Q^T against R (K = rank = 40).  Queries are
+    superposed vectors p C, p = softmax(N(0, 2)) over the 40 entries; a single
+    lookup (B = 1) and a batch of 65536 (4096 problems x 16 panels).  Also the
+    storage of each form: M D values dense, r D + M r compressed."""
+    M, Ds, Bs = 40, [256, 512, 1024, 2048, 4096, 8192], [1, 65536]
+    reps = max(20, args.steps)
+    stream = torch.cuda.current_stream()
+
+    def timed(f):
+        for _ in range(5):
+            f()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            f()
+            e1.record(stream)
+            ts.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ts])) * 1e3     # us
+
+    rows = []
+    for D in Ds:
+        C = torch.from_numpy(wl.bipolar_codebook(M, D, 6, D)).cuda()
+        Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=torch.float32, r_dtype=torch.float32)
+        Cd = gsm.alloc_rows(M, D, torch.float32, "cuda")
+        Cd.copy_(C)
+        Rc = R.contiguous()
+        row = {"D": D, "rank": r, "storage_bytes_dense": 4 * M * D, "storage_bytes_gram": 4 * (r * D + M * r),
+               "per_vector_ratio": D / r}
+        for B in Bs:
+            P = torch.from_numpy(wl.softmax_probs(B, M, float(np.sqrt(2.0)), 6, 100 + D)).cuda()
+            X = gsm.alloc_rows(B, D, torch.float32, "cuda")
+            X.copy_(P @ C)
+            T = gsm.gs_project(X, Q)
+            S = torch.empty((B, M), device="cuda")
+            idx = torch.empty(B, dtype=torch.int32, device="cuda")
+            dense = timed(lambda: gsm.gs_similarity(X, Cd, cnorm=cnorm, out=S, argmax_out=idx))
+            gram = timed(lambda: gsm.gs_similarity(T, Rc, cnorm=cnorm, out=S, argmax_out=idx))
+            row["B%d" % B] = {"dense_us": dense, "gram_us": gram, "speedup": dense / gram}
+            del X, T, S, idx, P
+        rows.append(row)
+        del C, Cd, Q, R, Rc
+        torch.cuda.empty_cache()
+    big = rows[-1]["B65536"]
+    out = {
+        "metric": "similarity query latency vs vector dimension (dense D-space vs Gram-Space)",
+        "value": big["gram_us"], "unit": "us", "n_gpus": 1, "steps": reps, "warmup": 5,
+        "ms_per_step": big["gram_us"] * 1e-3, "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "dimsweep: global codebook M=40 bipolar, D=256..8192, cosine similarity + "
+                               "argmax, batches of 1 and 65536 queries; value: Gram-Space batch latency at D=8192"},
+        "roofline": None, "cpu_baseline": None,
+        "extra": {"rows": rows, "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -378,6 +445,9 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": 4 * n, "copy_probe_bytes_written": 4 * n, "launches": 5}))
         return
 
+    if args.workload == "dimsweep":
+        dimsweep_workload(args, torch, gsm)
+        return
     if args.workload != "vsa":
         mfma_workload(args, torch, gsm)
         return

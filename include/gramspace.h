@@ -173,6 +173,8 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
  *
  *   T      in   B x r, tt in {F32, BF16}, ldt >= r
  *   R      in   M x r, rt == tt, ldr >= r
+ *               (r >= 1 and may exceed M: the same call on D-space vectors
+ *               and the uncompressed codebook, r = D, is the dense lookup)
  *   qnorm2 in   float[B], nullable;  cnorm in float[M], nullable
  *   S      out  float B x M, nullable, lds >= M
  *   argmax out  int32[B], nullable: index of the largest S[b, :], the lowest

@@ -228,7 +228,7 @@ static gs_status check_sim_common(const char *fn, const void *T, gs_dtype tt, in
     if (!is_batch_type(tt) || rt != tt)
         return fail(GS_ERR_DTYPE, "%s: T/R must be both f32 or both bf16", fn);
     if (mode != GS_SIM_DOT && mode != GS_SIM_COSINE) return fail(GS_ERR_ARG, "%s: unknown similarity mode", fn);
-    if (B < 0 || M < 1 || r < 1 || r > M) return fail(GS_ERR_SHAPE, "%s: need B >= 0 and 1 <= r <= M", fn);
+    if (B < 0 || M < 1 || r < 1) return fail(GS_ERR_SHAPE, "%s: need B >= 0, M >= 1 and r >= 1", fn);
     GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
     GS_CHECK(check_matrix(R, "R", M, r, ldr, rt, false));
     GS_CHECK(check_aligned(qnorm2, 4, "qnorm2"));
@@ -249,7 +249,7 @@ gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_
                             {span(S, B, M, lds, 4, "S"), span(argmax, 1, B, B, 4, "argmax")}));
     if (B == 0) return ok();
     GS_CHECK(check_device());
-    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+    if (M <= SMALL_MAX && r <= M) {   // small-codebook kernels (rows of r <= M <= 32)
         SmallArgs a{};
         a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = S; a.ldout = lds;
         a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale; a.argmax = argmax;
@@ -277,7 +277,7 @@ gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t
     if (B == 0) return ok();
     GS_CHECK(check_device());
     hipStream_t s = (hipStream_t)stream;
-    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+    if (M <= SMALL_MAX && r <= M) {   // small-codebook kernels (rows of r <= M <= 32)
         SmallArgs a{};
         a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = A; a.ldout = lda;
         a.O = O; a.ldo = ldo; a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE;

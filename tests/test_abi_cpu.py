@@ -133,8 +133,11 @@ def test_similarity_validation(L):
     assert call(am=P(0x60000001)) == gsm.GS_ERR_ALIGN
     assert call(am=P(0x40000004)) == gsm.GS_ERR_ARG          # argmax inside S
     assert call(S=A1) == gsm.GS_ERR_ARG                      # S aliases T
-    assert call(r=6) == gsm.GS_ERR_SHAPE
+    assert call(r=6) == gsm.GS_ERR_SHAPE                     # ldt < r
+    assert call(r=0) == gsm.GS_ERR_SHAPE
     assert call(B=0) == gsm.GS_OK
+    # r above M is the dense form of the lookup (D-space rows, uncompressed codebook)
+    assert call(B=0, r=6, ldt=6, ldr=6) == gsm.GS_OK
 
 
 def test_attention_and_reconstruct_validation(L):

@@ -365,6 +365,29 @@ def test_deterministic():
     assert torch.equal(t1, t2)
 
 
+# ------------------------------------ dense vs Gram-Space similarity (M = 40)
+
+@pytest.mark.parametrize("D", [256, 2048])
+def test_dense_and_gram_similarity_agree(D):
+    # the dimension sweep's two forms of one lookup: cosine scores of D-space
+    # queries against the codebook, and of their coordinates against R
+    M, B = 40, 300
+    C = wl.bipolar_codebook(M, D, 6, D)
+    P = wl.softmax_probs(B, M, np.sqrt(2.0), 6, 100 + D)
+    Q, R, r, kept, cn = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    assert r == M
+    X = dev(oracle.prob2vec(P, C).astype(np.float32))
+    Sd, idd = gsm.gs_similarity(X, dev(C), cnorm=cn)
+    T = gsm.gs_project(X, Q)
+    Sg, idg = gsm.gs_similarity(T, R.contiguous(), cnorm=cn)
+    torch.cuda.synchronize()
+    So = oracle.similarity(oracle.prob2vec(P, C), C, oracle.COSINE)
+    assert rowrel(host(Sd), So) <= TOL_F32
+    assert rowrel(host(Sg), So) <= TOL_F32
+    check_argmax(host(idd), So)
+    check_argmax(host(idg), So)
+
+
 # ------------------------------------------------- fused soft selection
 
 def soft_case(Ms, Bs, D, seed, dtype=torch.float32):
