@@ -249,7 +249,9 @@ gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_
                             {span(S, B, M, lds, 4, "S"), span(argmax, 1, B, B, 4, "argmax")}));
     if (B == 0) return ok();
     GS_CHECK(check_device());
-    if (M <= SMALL_MAX && r <= M) {   // small-codebook kernels (rows of r <= M <= 32)
+    // small-codebook kernels (one thread per row of r <= M <= 64), unless a
+    // few rows write their scores: those split the K reduction over work-groups
+    if (M <= SMALL_MAX && r <= M && !(B <= FEW_ROWS && S)) {
         SmallArgs a{};
         a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = S; a.ldout = lds;
         a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale; a.argmax = argmax;
@@ -277,7 +279,7 @@ gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t
     if (B == 0) return ok();
     GS_CHECK(check_device());
     hipStream_t s = (hipStream_t)stream;
-    if (M <= SMALL_MAX && r <= M) {   // small-codebook kernels (rows of r <= M <= 32)
+    if (M <= SMALL_MAX && r <= M && B > FEW_ROWS) {   // small-codebook kernels, as in gs_similarity
         SmallArgs a{};
         a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = A; a.ldout = lda;
         a.O = O; a.ldo = ldo; a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE;
@@ -336,8 +338,8 @@ gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, 
     int64_t tiles = 0;
     for (int i = 0; i < ngroups; ++i) {
         const gs_soft_group &g = groups[i];
-        if (g.B < 0 || g.M < 1 || g.M > SMALL_MAX || g.r < 1 || g.r > g.M)
-            return fail(GS_ERR_SHAPE, "gs_soft_select: group %d needs B >= 0 and 1 <= r <= M <= %d", i, SMALL_MAX);
+        if (g.B < 0 || g.M < 1 || g.M > SOFT_MAX_M || g.r < 1 || g.r > g.M)
+            return fail(GS_ERR_SHAPE, "gs_soft_select: group %d needs B >= 0 and 1 <= r <= M <= %d", i, SOFT_MAX_M);
         GS_CHECK(check_matrix(g.P, "P", g.B, g.M, g.ldp, pt, false));
         GS_CHECK(check_matrix(g.R, "R", g.M, g.r, g.ldr, pt, false));
         GS_CHECK(check_aligned(g.cnorm, 4, "cnorm"));

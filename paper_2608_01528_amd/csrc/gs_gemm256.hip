@@ -805,6 +805,58 @@ __global__ void __launch_bounds__(256) rows_softmax_kernel(float *A, int64_t lda
     for (int64_t c = l; c < M; c += 64) a[c] = __expf(a[c] - m) * iz;
 }
 
+// Scores of a few query rows (A, g.M rows) against every codebook row (B
+// stored N x K): one work-group per (query row, J codebook rows), the K range
+// split over its 256 threads, which also sum the squares for cosine norms
+// not given.  out[b, j] = scale * <a_b, b_j> (/ (||a_b|| ||b_j||) for cosine,
+// 0 if a norm is 0).
+template <typename T, int J>
+__global__ void __launch_bounds__(256) few_rows_kernel(GemmArgs g) {
+    constexpr int NV = 2 * J + 1;   // J products, J codebook squares, the query square
+    const int64_t b = blockIdx.y;
+    const int64_t j0 = (int64_t)blockIdx.x * J;
+    const int nj = (g.N - j0 < J) ? (int)(g.N - j0) : J;
+    const T *x = static_cast<const T *>(g.A) + b * g.lda;
+    const T *Bm = static_cast<const T *>(g.B) + j0 * g.ldb;
+    float v[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = 0.f;
+    for (int64_t k = threadIdx.x; k < g.K; k += 256) {
+        const float xv = ld_f32<T>(x, k);
+        v[2 * J] += xv * xv;
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+            if (j < nj) {
+                const float c = ld_f32<T>(Bm, (int64_t)j * g.ldb + k);
+                v[j] += xv * c;
+                v[J + j] += c * c;
+            }
+    }
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) v[i] += __shfl_xor(v[i], o);
+    __shared__ float part[4][NV];
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    if (l == 0) {
+#pragma unroll
+        for (int i = 0; i < NV; ++i) part[w][i] = v[i];
+    }
+    __syncthreads();
+    if (threadIdx.x < nj) {
+        const int j = threadIdx.x;
+        const float dot = part[0][j] + part[1][j] + part[2][j] + part[3][j];
+        float f = g.scale;
+        if (g.cosine) {
+            const float n2 = g.qnorm2 ? g.qnorm2[b] : part[0][2 * J] + part[1][2 * J] + part[2][2 * J] + part[3][2 * J];
+            const float c = g.cnorm ? g.cnorm[j0 + j]
+                                    : sqrtf(part[0][J + j] + part[1][J + j] + part[2][J + j] + part[3][J + j]);
+            f = (n2 > 0.f && c > 0.f) ? g.scale / (sqrtf(n2) * c) : 0.f;
+        }
+        static_cast<float *>(g.C)[b * g.ldc + j0 + j] = dot * f;
+    }
+}
+
 template <typename T, bool SOFTMAX, bool ROWN, bool COLN>
 hipError_t launch_sweep(const GemmArgs &a, hipStream_t s) {
     const int64_t nM = (a.M + TM - 1) / TM;
@@ -841,6 +893,26 @@ hipError_t launch_scores(const GemmArgs &a, bool softmax, hipStream_t s) {
 hipError_t launch_scores256(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s) {
     if (a.M == 0 || a.N == 0) return hipSuccess;
     hipError_t e = (t == GS_BF16) ? launch_scores<bf16_t>(a, softmax, s) : launch_scores<float>(a, softmax, s);
+    if (e != hipSuccess) return e;
+    return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
+}
+
+hipError_t launch_few_rows(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s) {
+    if (a.M == 0 || a.N == 0) return hipSuccess;
+    GemmArgs b = a;
+    if (softmax) b.scale = a.scale * a.beta;      // the softmax acts on beta * score
+    // 8 codebook rows per work-group while that still gives a round of 256
+    // work-groups, else one (more work-groups, each reading its query again)
+    if (a.M * ((a.N + 7) / 8) >= 256) {
+        const dim3 grid((unsigned)((a.N + 7) / 8), (unsigned)a.M);
+        if (t == GS_BF16) hipLaunchKernelGGL((few_rows_kernel<bf16_t, 8>), grid, dim3(256), 0, s, b);
+        else hipLaunchKernelGGL((few_rows_kernel<float, 8>), grid, dim3(256), 0, s, b);
+    } else {
+        const dim3 grid((unsigned)a.N, (unsigned)a.M);
+        if (t == GS_BF16) hipLaunchKernelGGL((few_rows_kernel<bf16_t, 1>), grid, dim3(256), 0, s, b);
+        else hipLaunchKernelGGL((few_rows_kernel<float, 1>), grid, dim3(256), 0, s, b);
+    }
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
 }

@@ -139,6 +139,10 @@ hipError_t launch_sweep256(gs_dtype t, bool softmax, const GemmArgs &a, hipStrea
 // product kernel with a scaled-score epilogue, then a row pass (argmax, or
 // softmax in place).  Same operand conditions as launch_gemm256 (B N x K).
 hipError_t launch_scores256(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s);
+// Scores of a few query rows (a.M <= FEW_ROWS) written to a.C, then the row
+// pass (argmax, or softmax in place); any K, B stored N x K.
+constexpr int64_t FEW_ROWS = 32;
+hipError_t launch_few_rows(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s);
 // Row pass over a B x M fp32 score matrix (leading dimension ld): softmax in
 // place, or the row argmax (lowest index on ties) into argmax when non-null.
 hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int64_t M, int32_t *argmax,
@@ -148,8 +152,10 @@ hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int
 // fails for requests beyond that.
 hipError_t raise_lds_limit(const void *kernel, size_t lds);
 
-// Small-codebook streaming kernels (M <= SMALL_MAX and r <= SMALL_MAX).
-constexpr int SMALL_MAX = 32;
+// Small-codebook streaming kernels of the separate calls (r <= M <= SMALL_MAX)
+// and of the fused soft selection (r <= M <= SOFT_MAX_M).
+constexpr int SMALL_MAX = 64;
+constexpr int SOFT_MAX_M = 32;
 
 struct SmallArgs {
     const void *In; int64_t ldin;      // P (prob2vec) or T (similarity / attention)

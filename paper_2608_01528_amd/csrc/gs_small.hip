@@ -19,11 +19,14 @@ namespace gs {
 namespace {
 
 
-constexpr int ROWS = 256;                 // batch rows per work-group (separate calls)
+// Batch rows (and threads) per work-group of the separate calls: 256, or 128
+// for the widest codebooks (keeps the row tile and codebook block within
+// 64 KiB of LDS).
+template <int MB> constexpr int rows_of() { return MB <= 48 ? 256 : 128; }
 #ifndef SOFT_RPT
 #define SOFT_RPT 1
 #endif
-constexpr int MAXK = SMALL_MAX;           // 32
+constexpr int MAXK = SOFT_MAX_M;          // widest row of the fused soft selection (32)
 
 enum Mode { MODE_P2V = 0, MODE_SIM = 1, MODE_ATT = 2 };
 
@@ -57,6 +60,8 @@ template <> __device__ __forceinline__ void st1_out<float>(float *p, int64_t i, 
 
 // Smallest supported padded size for a codebook of M entries.
 __host__ __device__ __forceinline__ int pad_of(int64_t M) { return M <= 8 ? 8 : M <= 16 ? 16 : M <= 24 ? 24 : 32; }
+// ... for the separate calls, up to 64 entries.
+__host__ __device__ __forceinline__ int pad_small(int64_t M) { return M <= 32 ? pad_of(M) : M <= 48 ? 48 : 64; }
 
 // ------------------------------------------------------------- tile moves
 //
@@ -66,7 +71,7 @@ __host__ __device__ __forceinline__ int pad_of(int64_t M) { return M <= 8 ? 8 : 
 // as 4-element vectors; otherwise element by element with the row and column
 // advanced incrementally.  NT is the number of threads taking part.
 
-template <typename T, int NT>
+template <typename T, int NT, int WMAX = MAXK>
 __device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, int64_t b0, int nrow, int w,
                                           float *tile) {
     const int t = threadIdx.x;
@@ -74,7 +79,7 @@ __device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, i
     const T *base = g + b0 * ld;
     if (ld == w && aligned16(base)) {
         const int n4 = n >> 2;
-        constexpr int V = (NT * MAXK / 4 + NT - 1) / NT;
+        constexpr int V = (NT * WMAX / 4 + NT - 1) / NT;
         f4v v[V];
 #pragma unroll
         for (int i = 0; i < V; ++i) {
@@ -252,17 +257,18 @@ __device__ __forceinline__ void tile_to_regs(const float *tile, int w, float v[M
 
 template <typename TI, typename TO, int MODE, int MB, class Rows>
 __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, const float *Rn, float *tile) {
+    constexpr int NR = rows_of<MB>();
     const int t = threadIdx.x;
-    const int64_t b0 = (int64_t)blockIdx.x * ROWS;
+    const int64_t b0 = (int64_t)blockIdx.x * NR;
     const int M = (int)a.M, r = (int)a.r;
-    const int nrow = (int)((a.B - b0 < ROWS) ? (a.B - b0) : ROWS);
+    const int nrow = (int)((a.B - b0 < NR) ? (a.B - b0) : NR);
     float x[MB];
     if (MODE == MODE_P2V) {
         row_prob2vec<MB>(tile + t * M, M, R, x);
         lds_barrier();   // the tile is reused for the outputs
         regs_to_tile<MB>(x, r, tile);
         lds_barrier();
-        tile_store<TO, ROWS>(static_cast<TO *>(a.Out), a.ldout, b0, nrow, r, tile);
+        tile_store<TO, NR>(static_cast<TO *>(a.Out), a.ldout, b0, nrow, r, tile);
         return;
     }
     tile_to_regs<MB>(tile, r, x);
@@ -284,33 +290,34 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
         if (a.argmax && t < nrow) __builtin_nontemporal_store(bi, a.argmax + b0 + t);
         if (!a.Out) return;
         lds_barrier();
-        tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
+        tile_store<float, NR>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
         return;
     }
     row_softmax(srow, M, 1.f, best);
     lds_barrier();
-    tile_store<float, ROWS>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
+    tile_store<float, NR>(static_cast<float *>(a.Out), a.ldout, b0, nrow, M, tile);
     if (!a.O) return;
     float o[MB];
     row_prob2vec<MB>(srow, M, R, o);
     lds_barrier();
     regs_to_tile<MB>(o, r, tile);
     lds_barrier();
-    tile_store<TO, ROWS>(static_cast<TO *>(a.O), a.ldo, b0, nrow, r, tile);
+    tile_store<TO, NR>(static_cast<TO *>(a.O), a.ldo, b0, nrow, r, tile);
 }
 
 template <typename TI, typename TO, int MODE, int MB>
-__global__ void __launch_bounds__(ROWS) small_kernel(SmallArgs a) {
-    __shared__ __attribute__((aligned(16))) float tile[ROWS * MAXK];
+__global__ void __launch_bounds__(rows_of<MB>()) small_kernel(SmallArgs a) {
+    constexpr int NR = rows_of<MB>();
+    __shared__ __attribute__((aligned(16))) float tile[NR * MB];
     __shared__ __attribute__((aligned(16))) float Rs[MB * MB];
     __shared__ float Rn[MB];
-    const int64_t b0 = (int64_t)blockIdx.x * ROWS;
+    const int64_t b0 = (int64_t)blockIdx.x * NR;
     const int M = (int)a.M, r = (int)a.r;
-    const int nrow = (int)((a.B - b0 < ROWS) ? (a.B - b0) : ROWS);
+    const int nrow = (int)((a.B - b0 < NR) ? (a.B - b0) : NR);
     const TI *R = static_cast<const TI *>(a.R);
-    tile_load<TI, ROWS>(static_cast<const TI *>(a.In), a.ldin, b0, nrow, (MODE == MODE_P2V) ? M : r, tile);
-    if (MODE != MODE_P2V) stage_norms<TI, ROWS>(R, a.ldr, M, r, a.cnorm, a.cosine != 0, MB, Rn);
-    stage_padded<TI, MB, ROWS>(R, a.ldr, M, r, Rs);
+    tile_load<TI, NR, MB>(static_cast<const TI *>(a.In), a.ldin, b0, nrow, (MODE == MODE_P2V) ? M : r, tile);
+    if (MODE != MODE_P2V) stage_norms<TI, NR>(R, a.ldr, M, r, a.cnorm, a.cosine != 0, MB, Rn);
+    stage_padded<TI, MB, NR>(R, a.ldr, M, r, Rs);
     lds_barrier();
     small_body<TI, TO, MODE, MB>(a, LdsRows<MB>{Rs}, Rn, tile);
 }
@@ -769,12 +776,15 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
 template <typename TI, typename TO, int MODE>
 hipError_t launch(const SmallArgs &a, hipStream_t s) {
     if (a.B == 0) return hipSuccess;
-    const dim3 grid((unsigned)((a.B + ROWS - 1) / ROWS)), block(ROWS);
-    switch (pad_of(a.M)) {
+    const int nr = pad_small(a.M) <= 48 ? 256 : 128;   // rows_of
+    const dim3 grid((unsigned)((a.B + nr - 1) / nr)), block(nr);
+    switch (pad_small(a.M)) {
         case 8: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 8>), grid, block, 0, s, a); break;
         case 16: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 16>), grid, block, 0, s, a); break;
         case 24: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 24>), grid, block, 0, s, a); break;
-        default: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 32>), grid, block, 0, s, a); break;
+        case 32: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 32>), grid, block, 0, s, a); break;
+        case 48: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 48>), grid, block, 0, s, a); break;
+        default: hipLaunchKernelGGL((small_kernel<TI, TO, MODE, 64>), grid, block, 0, s, a); break;
     }
     return hipGetLastError();
 }

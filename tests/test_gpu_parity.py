@@ -168,6 +168,9 @@ def test_project_bf16_output():
 @pytest.mark.parametrize("B,M,D,dup,dtype", [
     (1000, 22, 1024, 0.0, torch.float32),    # small-codebook kernel
     (129, 5, 1024, 0.0, torch.float32),
+    (700, 40, 1024, 0.0, torch.float32),     # small-codebook kernel, padded to 48
+    (257, 64, 800, 0.1, torch.float32),      # padded to 64, rank-deficient
+    (300, 47, 512, 0.0, torch.bfloat16),
     (333, 100, 512, 0.0, torch.float32),     # matrix-core path
     (300, 160, 900, 0.1, torch.float32),     # rank-deficient, r < M
     (250, 150, 800, 0.0, torch.bfloat16),
@@ -190,6 +193,8 @@ def test_prob2vec(B, M, D, dup, dtype):
 SIM_CASES = [  # (B, M, D, dup, in_span)
     (700, 10, 1024, 0.0, True),
     (513, 22, 1024, 0.0, False),
+    (600, 40, 1024, 0.0, True),     # small-codebook kernels up to 64 entries
+    (300, 64, 700, 0.1, False),     # r < M
     (300, 100, 1000, 0.0, True),
     (260, 300, 700, 0.1, False),    # r < M, three column blocks, ragged
 ]
@@ -386,6 +391,36 @@ def test_dense_and_gram_similarity_agree(D):
     assert rowrel(host(Sg), So) <= TOL_F32
     check_argmax(host(idd), So)
     check_argmax(host(idg), So)
+
+
+@pytest.mark.parametrize("B,M,K,dtype", [(1, 40, 8192, torch.float32), (17, 1000, 300, torch.float32),
+                                         (32, 40, 1000, torch.bfloat16), (5, 70, 45, torch.float32)])
+@pytest.mark.parametrize("norms", ["computed", "given"])
+def test_few_rows_scores(B, M, K, dtype, norms):
+    # at most 32 query rows: the reduction over K is split over work-groups
+    print("few rows", B, M, K, dtype, norms, flush=True)
+    rng = np.random.default_rng(B * 1000 + M)
+    T = rng.standard_normal((B, K)).astype(np.float32)
+    R = rng.standard_normal((M, K)).astype(np.float32)
+    if dtype == torch.bfloat16:
+        T, R = wl.round_bf16(T), wl.round_bf16(R)
+    qn = dev(oracle.row_norms(T) ** 2) if norms == "given" else None
+    cn = dev(oracle.row_norms(R)) if norms == "given" else None
+    S, idx = gsm.gs_similarity(dev(T, dtype), dev(R, dtype), qnorm2=qn, cnorm=cn, mode="cosine")
+    Sd, idd = gsm.gs_similarity(dev(T, dtype), dev(R, dtype), mode="dot", scale=0.25)
+    A, O = gsm.gs_attention(dev(T, dtype), dev(R, dtype), qnorm2=qn, cnorm=cn, mode="cosine", beta=12.0,
+                            weighted_sum=True, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    So = oracle.similarity(T, R, oracle.COSINE)
+    assert rowrel(host(S), So) <= TOL_F32
+    check_argmax(host(idx), So)
+    Sdo = oracle.similarity(T, R, oracle.DOT, 0.25)
+    assert rowrel(host(Sd), Sdo) <= TOL_F32
+    check_argmax(host(idd), Sdo)
+    Ao = oracle.softmax(So, 12.0)
+    assert rowrel(host(A), Ao) <= TOL_F32
+    # weighted sum of the codebook rows, O = A R
+    assert rowrel(host(O), Ao @ R.astype(np.float64)) <= (TOL_F32 if dtype == torch.float32 else TOL_BF16)
 
 
 # ------------------------------------------------- fused soft selection
