@@ -20,6 +20,10 @@ paper's W transposed: row j is codebook vector c_j; Q = U^T; R = T^T):
 * project      -- Sec. 3.1: t = U^T x.
 * reconstruct  -- Sec. 3.1 and 3.3: x = U t ("decompose").
 * bind         -- Sec. 2.2 / Table 1: element-wise product in D-space.
+* circular     -- Sec. 2.2, Sec. 3.3: blockwise circular convolution (bind)
+                  and circular correlation (unbind) of restored vectors, the
+                  modulo-style component-wise operators, by their sums.
+* xor          -- exclusive-or binding of binary vectors (bits value >= 0.5).
 * memory_model -- Sec. 3.1: storage O(MD) against O(Dk + Mk), ratio D/k.
 
 The C part (gs_oracle.c) is compiled with gcc -O2 for the baseline x86-64
@@ -76,6 +80,8 @@ def _load():
     lib.gso_project.argtypes = [dp, L, L, dp, L, dp]
     lib.gso_reconstruct.argtypes = [dp, L, L, dp, L, dp]
     lib.gso_bind.argtypes = [dp, dp, L, dp]
+    lib.gso_circular.argtypes = [dp, dp, L, L, L, ctypes.c_int, dp]
+    lib.gso_xor.argtypes = [dp, dp, L, dp]
     _lib = lib
     return lib
 
@@ -194,6 +200,27 @@ def bind(X, Y) -> np.ndarray:
     assert X.shape == Y.shape
     Z = np.empty_like(X)
     _load().gso_bind(_dp(X), _dp(Y), X.size, _dp(Z))
+    return Z
+
+
+def circular(X, Y, L: int, corr: bool = False) -> np.ndarray:
+    """Blockwise circular convolution (corr=False) or correlation (corr=True)
+    of the rows of X and Y over consecutive blocks of length L."""
+    X, Y = _f64(X), _f64(Y)
+    assert X.shape == Y.shape and X.ndim == 2
+    B, D = X.shape
+    assert L >= 1 and D % L == 0
+    Z = np.empty_like(X)
+    _load().gso_circular(_dp(X), _dp(Y), B, D, int(L), int(bool(corr)), _dp(Z))
+    return Z
+
+
+def xor(X, Y) -> np.ndarray:
+    """Exclusive or of the bits (value >= 0.5) of X and Y, as 0.0 / 1.0."""
+    X, Y = _f64(X), _f64(Y)
+    assert X.shape == Y.shape
+    Z = np.empty_like(X)
+    _load().gso_xor(_dp(X), _dp(Y), X.size, _dp(Z))
     return Z
 
 

@@ -223,3 +223,37 @@ void gso_bind(const double *X, const double *Y, long n, double *Z)
     #pragma omp parallel for schedule(static)
     for (long i = 0; i < n; ++i) Z[i] = X[i] * Y[i];
 }
+
+/* Blockwise circular convolution (binding) and circular correlation
+   (unbinding) of restored vectors, the component-wise "modulo-style"
+   operators that follow a restore (Sec. 2.2, Sec. 3.3).  Each row of D
+   values splits into D / L consecutive blocks of length L; within a block,
+     conv: Z[i] = sum_j X[j] Y[(i - j) mod L]
+     corr: Z[i] = sum_j X[j] Y[(j - i) mod L]
+   summed in index order j = 0 .. L - 1.  X, Y, Z are B x D. */
+void gso_circular(const double *X, const double *Y, long B, long D, long L, int corr, double *Z)
+{
+    #pragma omp parallel for schedule(static)
+    for (long b = 0; b < B; ++b)
+        for (long s0 = 0; s0 < D; s0 += L) {
+            const double *x = X + b * D + s0, *y = Y + b * D + s0;
+            for (long i = 0; i < L; ++i) {
+                double acc = 0.0;
+                for (long j = 0; j < L; ++j) {
+                    long k = corr ? (j - i) : (i - j);
+                    k %= L;
+                    if (k < 0) k += L;
+                    acc += x[j] * y[k];
+                }
+                Z[b * D + s0 + i] = acc;
+            }
+        }
+}
+
+/* Exclusive-or binding of binary vectors: each restored value is read as the
+   bit (value >= 0.5), Z = 1 where the two bits differ, else 0. */
+void gso_xor(const double *X, const double *Y, long n, double *Z)
+{
+    #pragma omp parallel for schedule(static)
+    for (long i = 0; i < n; ++i) Z[i] = ((X[i] >= 0.5) != (Y[i] >= 0.5)) ? 1.0 : 0.0;
+}

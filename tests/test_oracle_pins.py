@@ -406,3 +406,71 @@ def test_rank_threshold_is_relative_residual(D):
     assert r == 2
     # the residual is a difference of vectors of norm |c1|: error ~ eps |c1|
     assert abs(R[1, 1] - delta * math.sqrt(1 - 1 / D)) <= 1e-12 * np.linalg.norm(c1)
+
+
+# ------------------------------------------- circular binding and unbinding
+
+def test_circular_hand_worked_example():
+    # L = 4, by hand: x (*) e_1 shifts x right by one, correlation with e_1
+    # shifts it left; x (*) (1, 1, 0, 0) adds x to its right shift
+    x = np.array([[1.0, 2.0, 3.0, 4.0]])
+    assert np.array_equal(oracle.circular(x, np.array([[0.0, 1, 0, 0]]), 4), [[4.0, 1, 2, 3]])
+    assert np.array_equal(oracle.circular(x, np.array([[0.0, 1, 0, 0]]), 4, corr=True), [[2.0, 3, 4, 1]])
+    assert np.array_equal(oracle.circular(x, np.array([[1.0, 1, 0, 0]]), 4), [[5.0, 3, 5, 7]])
+
+
+@pytest.mark.parametrize("L", [1, 2, 8, 64])
+def test_circular_identity_and_shifts(L):
+    rng = np.random.default_rng(L)
+    X = rng.standard_normal((3, 4 * L))
+    for s in range(0, L, max(1, L // 4)):
+        E = np.zeros_like(X)
+        E[:, s::L] = 1.0                          # e_s in every block
+        shifted = np.concatenate([np.roll(X[:, a:a + L], s, axis=1) for a in range(0, 4 * L, L)], axis=1)
+        back = np.concatenate([np.roll(X[:, a:a + L], -s, axis=1) for a in range(0, 4 * L, L)], axis=1)
+        np.testing.assert_array_equal(oracle.circular(X, E, L), shifted)
+        np.testing.assert_array_equal(oracle.circular(X, E, L, corr=True), back)
+
+
+@pytest.mark.parametrize("L", [16, 128])
+def test_circular_convolution_theorem(L):
+    # numpy's FFT as an independent route: conv <-> product of spectra,
+    # corr <-> product with the conjugate spectrum
+    rng = np.random.default_rng(100 + L)
+    X, Y = rng.standard_normal((5, 3 * L)), rng.standard_normal((5, 3 * L))
+    Xb, Yb = X.reshape(5, 3, L), Y.reshape(5, 3, L)
+    conv = np.fft.ifft(np.fft.fft(Xb) * np.fft.fft(Yb)).real.reshape(5, 3 * L)
+    corr = np.fft.ifft(np.fft.fft(Xb) * np.conj(np.fft.fft(Yb))).real.reshape(5, 3 * L)
+    np.testing.assert_allclose(oracle.circular(X, Y, L), conv, atol=1e-10)
+    np.testing.assert_allclose(oracle.circular(X, Y, L, corr=True), corr, atol=1e-10)
+    # binding is commutative; blocks are independent
+    np.testing.assert_allclose(oracle.circular(X, Y, L), oracle.circular(Y, X, L), atol=1e-12)
+    np.testing.assert_allclose(oracle.circular(X, Y, L)[:, L:2 * L], oracle.circular(X[:, L:2 * L], Y[:, L:2 * L], L),
+                               atol=0)
+
+
+def test_circular_unbinding_with_unitary_key_is_exact():
+    # a key whose spectrum has unit modulus everywhere: correlating the bound
+    # vector with the key returns the original exactly (up to rounding)
+    L = 64
+    rng = np.random.default_rng(7)
+    phase = rng.uniform(-np.pi, np.pi, L // 2 + 1)
+    phase[0] = 0.0
+    phase[-1] = 0.0
+    key = np.fft.irfft(np.exp(1j * phase), n=L)[None, :]
+    X = rng.standard_normal((4, L))
+    K = np.repeat(key, 4, axis=0)
+    np.testing.assert_allclose(oracle.circular(oracle.circular(X, K, L), K, L, corr=True), X, atol=1e-12)
+
+
+def test_xor_binding_of_binary_vectors():
+    # bits of 0/1 vectors (and of values near them); x XOR x = 0, x XOR 0 = x
+    rng = np.random.default_rng(3)
+    a = rng.integers(0, 2, (6, 50)).astype(np.float64)
+    b = rng.integers(0, 2, (6, 50)).astype(np.float64)
+    np.testing.assert_array_equal(oracle.xor(a, b), np.logical_xor(a > 0, b > 0).astype(np.float64))
+    np.testing.assert_array_equal(oracle.xor(a, a), np.zeros_like(a))
+    np.testing.assert_array_equal(oracle.xor(a, np.zeros_like(a)), a)
+    noisy = a + rng.uniform(-0.3, 0.3, a.shape)
+    np.testing.assert_array_equal(oracle.xor(noisy, b), oracle.xor(a, b))
+    assert oracle.xor(np.array([0.5]), np.array([0.4999999]))[0] == 1.0
