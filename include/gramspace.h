@@ -82,6 +82,9 @@ typedef enum { GS_SIM_DOT = 0, GS_SIM_COSINE = 1 } gs_sim_mode;
 /* Component-wise operator applied after restoring two vectors. */
 typedef enum { GS_BIND_NONE = 0, GS_BIND_MUL = 1 } gs_bind;
 
+/* Component-wise binding operator of gs_bind_restored. */
+typedef enum { GS_BINDOP_MUL = 0, GS_BINDOP_XOR = 1, GS_BINDOP_CONV = 2, GS_BINDOP_CORR = 3 } gs_bind_op;
+
 /* ABI version of the loaded library (GS_ABI_VERSION of its build). */
 int gs_abi_version(void);
 
@@ -220,6 +223,29 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
                          const void *T2, int64_t ldt2, gs_bind bind,
                          const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
                          void *X, gs_dtype xt, int64_t ldx, void *stream);
+
+/*
+ * gs_bind_restored -- binding and unbinding of restored vectors, row by row (Sec. 2.2:
+ * the modulo-style component-wise operators run in the original domain,
+ * after gs_reconstruct; Sec. 3.3: circular convolution).  For each row b:
+ *   GS_BINDOP_MUL   Z = X .* Y                        element-wise product
+ *   GS_BINDOP_XOR   Z = (X >= 0.5) xor (Y >= 0.5)     binary vectors, 0 / 1
+ *   GS_BINDOP_CONV  blockwise circular convolution over consecutive blocks
+ *                   of L values: Z[i] = sum_j X[j] Y[(i - j) mod L]  (bind)
+ *   GS_BINDOP_CORR  blockwise circular correlation:
+ *                   Z[i] = sum_j X[j] Y[(j - i) mod L]  (unbind by Y)
+ *
+ *   X, Y   in   B x D, type xt in {F32, BF16}, ldx, ldy >= D
+ *   L           CONV / CORR block length: a power of two with 2 <= L <= 8192
+ *               that divides D (L = D: the whole row); ignored otherwise
+ *   Z      out  B x D, type zt in {F32, BF16}, ldz >= D; overlaps neither X
+ *               nor Y
+ * CONV and CORR go through an fp32 FFT of each block, so each result carries
+ * an error of a few fp32 units of log2(L) ||x_block|| ||y_block||.
+ */
+gs_status gs_bind_restored(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,
+                           const void *Y, int64_t ldy, gs_bind_op op, int64_t L,
+                           void *Z, gs_dtype zt, int64_t ldz, void *stream);
 
 /*
  * gs_soft_select -- the soft-selection pass (Sec. 3.1: probabilities are

@@ -321,6 +321,29 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
                                 (hipStream_t)stream), "gs_reconstruct");
 }
 
+gs_status gs_bind_restored(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,
+                           const void *Y, int64_t ldy, gs_bind_op op, int64_t L,
+                           void *Z, gs_dtype zt, int64_t ldz, void *stream) {
+    if (!is_batch_type(xt) || !is_batch_type(zt)) return fail(GS_ERR_DTYPE, "gs_bind_restored: X/Y and Z must be f32 or bf16");
+    if (op != GS_BINDOP_MUL && op != GS_BINDOP_XOR && op != GS_BINDOP_CONV && op != GS_BINDOP_CORR)
+        return fail(GS_ERR_ARG, "gs_bind_restored: unknown operator");
+    if (B < 0 || D < 1) return fail(GS_ERR_SHAPE, "gs_bind_restored: need B >= 0 and D >= 1");
+    if (op == GS_BINDOP_CONV || op == GS_BINDOP_CORR) {
+        if (L < 2 || L > 8192 || (L & (L - 1)) != 0 || D % L != 0)
+            return fail(GS_ERR_SHAPE, "gs_bind_restored: L must be a power of two in [2, 8192] dividing D");
+    }
+    GS_CHECK(check_matrix(X, "X", B, D, ldx, xt, false));
+    GS_CHECK(check_matrix(Y, "Y", B, D, ldy, xt, false));
+    GS_CHECK(check_matrix(Z, "Z", B, D, ldz, zt, false));
+    GS_CHECK(check_overlaps({span(X, B, D, ldx, esize(xt), "X"), span(Y, B, D, ldy, esize(xt), "Y")},
+                            {span(Z, B, D, ldz, esize(zt), "Z")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    BindArgs a{};
+    a.X = X; a.ldx = ldx; a.Y = Y; a.ldy = ldy; a.Z = Z; a.ldz = ldz; a.B = B; a.D = D; a.L = L;
+    return launched(launch_bind(xt, zt, (int)op, a, (hipStream_t)stream), "gs_bind_restored");
+}
+
 gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, gs_dtype tt,
                          gs_sim_mode mode, float scale, float beta, void *stream) {
     if (!groups) return fail(GS_ERR_ARG, "gs_soft_select: groups is null");

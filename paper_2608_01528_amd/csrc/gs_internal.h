@@ -152,6 +152,19 @@ hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int
 // fails for requests beyond that.
 hipError_t raise_lds_limit(const void *kernel, size_t lds);
 
+// Component-wise binding of restored vectors (gs_bind).
+struct BindArgs {
+    const void *X; int64_t ldx;
+    const void *Y; int64_t ldy;
+    void *Z; int64_t ldz;
+    int64_t B, D;
+    int64_t L;          // block length of the circular operators
+    int lg;             // log2 L (set by launch_bind)
+    int nb;             // blocks per work-group (set by launch_bind)
+    int64_t nblocks;    // D / L (set by launch_bind)
+};
+hipError_t launch_bind(gs_dtype tin, gs_dtype tout, int op, const BindArgs &a, hipStream_t s);
+
 // Small-codebook streaming kernels of the separate calls (r <= M <= SMALL_MAX)
 // and of the fused soft selection (r <= M <= SOFT_MAX_M).
 constexpr int SMALL_MAX = 64;

@@ -30,6 +30,7 @@ STATUS_NAMES = ["GS_OK", "GS_ERR_ARG", "GS_ERR_SHAPE", "GS_ERR_DTYPE", "GS_ERR_A
 GS_F32, GS_BF16, GS_F64 = 0, 1, 2
 GS_SIM_DOT, GS_SIM_COSINE = 0, 1
 GS_BIND_NONE, GS_BIND_MUL = 0, 1
+GS_BINDOP_MUL, GS_BINDOP_XOR, GS_BINDOP_CONV, GS_BINDOP_CORR = 0, 1, 2, 3
 
 _DT = {torch.float32: GS_F32, torch.bfloat16: GS_BF16, torch.float64: GS_F64}
 
@@ -71,6 +72,9 @@ class SoftGroup(ctypes.Structure):
                 ("B", _i64), ("M", _i64), ("r", _i64), ("T", _vp), ("ldt", _i64),
                 ("S", _vp), ("lds", _i64), ("argmax", _vp), ("A", _vp), ("lda", _i64)]
 
+
+_SIGS["gs_bind_restored"] = ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ctypes.c_int, _i64,
+                     _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
 
 _SIGS["gs_soft_select"] = ([ctypes.POINTER(SoftGroup), ctypes.c_int, ctypes.c_int, ctypes.c_int,
                             ctypes.c_int, ctypes.c_float, ctypes.c_float, _vp], ctypes.c_int)
@@ -252,6 +256,25 @@ def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = N
     xt, ldx = _mat(out, "X")
     _check(lib().gs_reconstruct(_ptr(T), tt, B, r, ldt, _ptr(T2), ldt2, b, _ptr(Q), qt, D, ldq,
                                 _ptr(out), xt, ldx, _stream()))
+    return out
+
+
+_BINDOPS = {"mul": GS_BINDOP_MUL, "xor": GS_BINDOP_XOR, "conv": GS_BINDOP_CONV, "corr": GS_BINDOP_CORR}
+
+
+def gs_bind_restored(X: torch.Tensor, Y: torch.Tensor, op: str = "conv", L: int | None = None, out_dtype=None,
+            out: torch.Tensor | None = None):
+    """Binding of restored vectors row by row: 'mul' (element-wise product),
+    'xor' (binary vectors), 'conv' / 'corr' (blockwise circular convolution /
+    correlation over blocks of L values, L = D by default)."""
+    xt, ldx = _mat(X, "X")
+    _, ldy = _mat(Y, "Y")
+    B, D = X.shape
+    if out is None:
+        out = alloc_rows(B, D, out_dtype or X.dtype, X.device)
+    zt, ldz = _mat(out, "Z")
+    _check(lib().gs_bind_restored(_ptr(X), xt, B, D, ldx, _ptr(Y), ldy, _BINDOPS[op], int(L or D), _ptr(out), zt, ldz,
+                         _stream()))
     return out
 
 

@@ -232,3 +232,27 @@ def test_soft_select_validation(L):
     assert soft(L, [group(argmax=0x600002)]) == gsm.GS_ERR_ALIGN
     assert soft(L, [group(B=0, P=None, S=None)]) == gsm.GS_OK            # empty: nothing to do
     assert "gs_" in err(L) or err(L) == ""
+
+
+def test_bind_restored_validation(L):
+    f = L.gs_bind_restored
+    ok = dict(X=A1, xt=gsm.GS_F32, B=4, D=16, ldx=16, Y=A2, ldy=16, op=gsm.GS_BINDOP_CONV, Lb=8, Z=A3,
+              zt=gsm.GS_F32, ldz=16)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["X"], a["xt"], a["B"], a["D"], a["ldx"], a["Y"], a["ldy"], a["op"], a["Lb"], a["Z"], a["zt"],
+                 a["ldz"], NULL)
+
+    assert call(op=7) == gsm.GS_ERR_ARG
+    assert call(xt=gsm.GS_F64) == gsm.GS_ERR_DTYPE
+    assert call(Lb=6) == gsm.GS_ERR_SHAPE                     # not a power of two
+    assert call(Lb=32) == gsm.GS_ERR_SHAPE                    # does not divide D
+    assert call(Lb=1) == gsm.GS_ERR_SHAPE
+    assert call(D=16384, ldx=16384, ldy=16384, ldz=16384, Lb=16384) == gsm.GS_ERR_SHAPE   # above 8192
+    assert call(ldz=15) == gsm.GS_ERR_SHAPE
+    assert call(Z=A1) == gsm.GS_ERR_ARG                       # Z aliases X
+    assert call(B=0) == gsm.GS_OK
+    assert call(B=0, op=gsm.GS_BINDOP_XOR, Lb=6) == gsm.GS_OK    # L is ignored by the element-wise operators
+    assert err(L) == ""

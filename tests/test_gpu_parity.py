@@ -831,3 +831,62 @@ def test_sweep_cosine_argmax_only(sweep_case):
     torch.cuda.synchronize()
     So = oracle.similarity(T[rows], R, oracle.COSINE)
     check_argmax(host(idx[rows]), So, band_rel=1e-4)
+
+
+# ------------------------------------------- binding of restored vectors
+
+@pytest.mark.parametrize("B,D,L", [(37, 4096, 4096), (33, 1024, 128), (5, 8192, 8192), (9, 64, 2), (300, 512, 512)])
+@pytest.mark.parametrize("op", ["conv", "corr"])
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+def test_bind_circular(B, D, L, op, dt):
+    print("bind", op, B, D, L, dt, flush=True)
+    rng = np.random.default_rng(D + L + B)
+    X = rng.standard_normal((B, D)).astype(np.float32)
+    Y = rng.standard_normal((B, D)).astype(np.float32)
+    if dt == torch.bfloat16:
+        X, Y = wl.round_bf16(X), wl.round_bf16(Y)
+    Z = gsm.gs_bind_restored(dev(X, dt), dev(Y, dt), op=op, L=L, out_dtype=torch.float32)
+    Zb = gsm.gs_bind_restored(dev(X, dt), dev(Y, dt), op=op, L=L, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    Zo = oracle.circular(X, Y, L, corr=(op == "corr"))
+    assert rowrel(host(Z), Zo) <= TOL_F32
+    assert rowrel(host(Zb), Zo) <= TOL_BF16
+
+
+def test_bind_restored_codebook_vectors():
+    # restored bipolar codebook vectors (reconstruct of their coordinates):
+    # bind two of them, unbind with the second, and compare each step with the
+    # oracle's sums; also the element-wise product against gs_reconstruct's
+    # fused bind
+    D, M = 1024, 12
+    C = rq_codebook("bipolar", M, D, 91)
+    Q, R, r, kept, cn = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    idx_a, idx_b = np.arange(M), np.roll(np.arange(M), 3)
+    Xa = gsm.gs_reconstruct(R[idx_a].contiguous(), Q)
+    Xb = gsm.gs_reconstruct(R[idx_b].contiguous(), Q)
+    Zc = gsm.gs_bind_restored(Xa, Xb, op="conv")
+    Zu = gsm.gs_bind_restored(Zc, Xb, op="corr")
+    Zm = gsm.gs_bind_restored(Xa, Xb, op="mul")
+    Zf = gsm.gs_reconstruct(R[idx_a].contiguous(), Q, T2=R[idx_b].contiguous(), bind="mul")
+    torch.cuda.synchronize()
+    Ca, Cb = C[idx_a], C[idx_b]
+    Zco = oracle.circular(Ca, Cb, D)
+    assert rowrel(host(Zc), Zco) <= TOL_F32
+    assert rowrel(host(Zu), oracle.circular(Zco, Cb, D, corr=True)) <= TOL_F32
+    assert rowrel(host(Zm), oracle.bind(Ca, Cb)) <= TOL_F32
+    assert rowrel(host(Zm), host(Zf)) <= 1e-6
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+def test_bind_xor_binary(dt):
+    # restored binary vectors carry rounding noise around 0 and 1; the bits
+    # (value >= 0.5) decide, bit-exact against the oracle on the same inputs
+    rng = np.random.default_rng(5)
+    B, D = 300, 4100
+    Xb = rng.integers(0, 2, (B, D)).astype(np.float32) + rng.uniform(-0.2, 0.2, (B, D)).astype(np.float32)
+    Yb = rng.integers(0, 2, (B, D)).astype(np.float32) + rng.uniform(-0.2, 0.2, (B, D)).astype(np.float32)
+    if dt == torch.bfloat16:
+        Xb, Yb = wl.round_bf16(Xb), wl.round_bf16(Yb)
+    Z = gsm.gs_bind_restored(dev(Xb, dt), dev(Yb, dt), op="xor", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(Z), oracle.xor(Xb, Yb))
