@@ -46,10 +46,11 @@ wl = None
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress", "dimsweep"],
+    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress", "dimsweep", "bind"],
                     help="vsa (default, the headline): fused soft selection; large / binary / stress: "
                          "the matrix-core rows (project, reconstruct + bind, large similarity); dimsweep: "
-                         "similarity latency against the vector dimension, dense vs Gram-Space")
+                         "similarity latency against the vector dimension, dense vs Gram-Space; bind: binding of restored "
+                         "vectors (circular convolution / correlation, xor, product)")
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--sets", type=int, default=0, help="batch copies to cycle through (0: >= 1 GiB)")
@@ -424,6 +425,63 @@ def dimsweep_workload(args, torch, gsm):
     print(json.dumps(out), flush=True)
 
 
+def bind_workload(args, torch, gsm):
+    """Binding of restored vectors at the binary workload's shape (16384 rows
+    of D = 4096, fp32): blockwise circular convolution and correlation over the
+    whole row and over 256-value blocks, xor of binary vectors, element-wise
+    product.  Per call: HBM bytes read (two operands) and written (one result)
+    over the mean time of a HIP graph of 20 calls."""
+    B, D = 16384, 4096
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    X = gsm.alloc_rows(B, D, torch.float32, "cuda")
+    Y = gsm.alloc_rows(B, D, torch.float32, "cuda")
+    X.copy_(torch.randn((B, D), generator=g, device="cuda"))
+    Y.copy_(torch.randn((B, D), generator=g, device="cuda"))
+    Z = gsm.alloc_rows(B, D, torch.float32, "cuda")
+    stream = torch.cuda.current_stream()
+    reps = max(10, min(args.steps, 50))
+    calls = [("conv L=4096", "conv", D), ("corr L=4096", "corr", D), ("conv L=256", "conv", 256),
+             ("xor", "xor", None), ("mul", "mul", None)]
+    nbytes = 3 * B * D * 4
+    per = {}
+    for name, op, L in calls:
+        f = lambda: gsm.gs_bind_restored(X, Y, op=op, L=L, out=Z)
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(20):
+                f()
+        graph.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (reps * 20)
+        per[name] = {"us": us, "GBps": nbytes / us * 1e-3, "frac": nbytes / us * 1e-3 / HBM_PEAK_GBS}
+    dom = "conv L=4096"
+    out = {
+        "metric": "binding of restored vectors: HBM GB/s vs peak", "value": per[dom]["GBps"], "unit": "GB/s",
+        "n_gpus": 1, "steps": reps * 20, "warmup": 3, "ms_per_step": per[dom]["us"] * 1e-3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "bind: 16384 restored rows of D=4096 (fp32), operators conv / corr (blocks of 4096 "
+                               "and 256), xor, mul; value: circular convolution over whole rows"},
+        "roofline": {"bound": "hbm", "kernel": "circular_kernel", "call": "gs_bind_restored (conv, L=4096)",
+                     "achieved": per[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": per[dom]["frac"], "traffic": None, "bytes_per_launch": nbytes,
+                     "avg_launch_us": per[dom]["us"]},
+        "cpu_baseline": None,
+        "extra": {"per_call": per, "kernel_source_hash": kernel_source_hash()},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -456,6 +514,9 @@ def main():
 
     if args.workload == "dimsweep":
         dimsweep_workload(args, torch, gsm)
+        return
+    if args.workload == "bind":
+        bind_workload(args, torch, gsm)
         return
     if args.workload != "vsa":
         mfma_workload(args, torch, gsm)
