@@ -33,13 +33,28 @@ namespace gs {
 namespace {
 
 constexpr int TM = 256, TN = 256;
-constexpr int NTH = 256;
+constexpr int NTH = 256;                // threads of the sweep (4 waves)
+// Waves of the product kernel: 8 (two per SIMD, 128 x 64 each, so one wave's
+// waits overlap the other's matrix work) or 4 (one per SIMD, 128 x 128).
+constexpr int GEMM_NW = 8;
+template <int NW> struct Waves {
+    static constexpr int WTN = NW == 4 ? 128 : 64;   // columns of a wave's sub-tile
+    static constexpr int NJ = WTN / 32;             // 32-column MFMA blocks per wave
+    static constexpr int IPW = 32 / NW;             // 1 KiB load instructions per wave per operand tile
+    static constexpr int NTHR = 64 * NW;
+    // rows wm = 128 (w / (NW / 2)) .. + 127, columns wn = WTN (w % (NW / 2)) .. + WTN - 1
+    static __device__ __forceinline__ int wm(int w) { return (w / (NW / 2)) * 128; }
+    static __device__ __forceinline__ int wn(int w) { return (w % (NW / 2)) * WTN; }
+};
 constexpr int NSTAGE = 2;
 constexpr int OPT = TM * 64;        // 16-bit units per staged operand tile (32 KiB)
 constexpr int GROUP_M = 4;          // m-tiles that take each n-tile in turn
 constexpr int EP_STRIDE_MAX = 128 * 4 + 32;   // staged fp32 output row: 128 values + 32-byte pad
+// bytes per staged output row of a wave's sub-tile (WTN values + 8 values of pad)
+template <typename TO, int NW>
+constexpr int ep_stride() { return Waves<NW>::WTN * (int)sizeof(TO) + 16 * (int)sizeof(TO) / 2; }
 constexpr size_t STAGE_BYTES = (size_t)NSTAGE * 2 * OPT * sizeof(uint16_t);
-constexpr size_t EPI_BYTES = (size_t)4 * 64 * EP_STRIDE_MAX;
+constexpr size_t EPI_BYTES = (size_t)GEMM_NW * 64 * (Waves<GEMM_NW>::WTN * 4 + 32);   // fp32 staging of the product kernel
 constexpr size_t LDS_BYTES = STAGE_BYTES > EPI_BYTES ? STAGE_BYTES : EPI_BYTES;
 
 typedef float f16v __attribute__((ext_vector_type(16)));
@@ -114,13 +129,13 @@ __device__ __forceinline__ void dma16x4(const rsrc_t &r, const int off[4], const
 }
 
 // Lane byte offset of instruction q (0..7) of this wave's share of a row tile.
-template <typename T>
+template <typename T, int IPW>
 __device__ __forceinline__ int rows_off(int64_t ld, int64_t nrows, int64_t k0, int64_t K, int tid, int q) {
     constexpr int P = Op<T>::PER;
     const int L = tid & 63;
     const int w = tid >> 6;
     const int64_t klast = ((K - 1) / P) * P;
-    const int b = 8 * w + q;
+    const int b = IPW * w + q;
     const int c = (L & 7) ^ (4 * (q & 1) + (L >> 4));
     int64_t kc = k0 + P * c;
     if (kc > klast) kc = klast;
@@ -130,31 +145,31 @@ __device__ __forceinline__ int rows_off(int64_t ld, int64_t nrows, int64_t k0, i
 }
 
 // Instructions 4 h .. 4 h + 3 of this wave's share of a row tile.
-template <typename T>
+template <typename T, int IPW>
 __device__ __forceinline__ void dma_rows4(const rsrc_t &r, int64_t ld, int64_t nrows, int64_t k0, int64_t K,
                                           uint16_t *tile, int tid, int h) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     int off[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) off[j] = rows_off<T>(ld, nrows, k0, K, tid, 4 * h + j);
-    dma16x4(r, off, tile + (8 * w + 4 * h) * 512);
+    for (int j = 0; j < 4; ++j) off[j] = rows_off<T, IPW>(ld, nrows, k0, K, tid, 4 * h + j);
+    dma16x4(r, off, tile + (IPW * w + 4 * h) * 512);
 }
 
 // k-row tile (bf16): 32 load instructions of 2 k-rows x 512 bytes; wave w
-// issues blocks 8w .. 8w+7.  Lane L lands at k-row 2b + L/32, position L%32,
+// issues blocks IPW w .. IPW w + IPW - 1 (IPW instructions per wave).  Lane L lands at k-row 2b + L/32, position L%32,
 // so it fetches chunk (L%32) ^ (4 (k-row % 4)).  `r` starts at the tile's
 // first column; ncols columns exist from there.
 // k-row tile (fp32): 32 load instructions of one k-row x 1 KiB; lane L lands
 // at position L of k-row b and fetches chunk L ^ (8 ((b / 16) % 2)), so the
 // two half-waves of a column read (k-rows k and k + 16) use opposite halves
 // of the banks.
-template <typename T>
+template <typename T, int IPW>
 __device__ __forceinline__ int krows_off(int64_t ld, int64_t k0, int64_t K, int64_t ncols, int tid, int q) {
     const int L = tid & 63;
     const int w = tid >> 6;
     constexpr int P = Op<T>::PER;
     const int64_t nlast = ((ncols - 1) / P) * P;
-    const int b = 8 * w + q;
+    const int b = IPW * w + q;
     int kl, c;
     if constexpr (sizeof(T) == 2) {
         kl = 2 * b + (L >> 5);
@@ -170,14 +185,14 @@ __device__ __forceinline__ int krows_off(int64_t ld, int64_t k0, int64_t K, int6
     return (int)((int64_t)sizeof(T) * (k * ld + nc));
 }
 
-template <typename T>
+template <typename T, int IPW>
 __device__ __forceinline__ void dma_krows4(const rsrc_t &r, int64_t ld, int64_t k0, int64_t K, int64_t ncols,
                                            uint16_t *tile, int tid, int h) {
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     int off[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) off[j] = krows_off<T>(ld, k0, K, ncols, tid, 4 * h + j);
-    dma16x4(r, off, tile + (8 * w + 4 * h) * 512);
+    for (int j = 0; j < 4; ++j) off[j] = krows_off<T, IPW>(ld, k0, K, ncols, tid, 4 * h + j);
+    dma16x4(r, off, tile + (IPW * w + 4 * h) * 512);
 }
 
 // A (or N x K B) fragment: the 16-byte chunk c of row r (8 bf16 or 4 fp32
@@ -235,25 +250,26 @@ template <> __device__ __forceinline__ bf16_t to_out<bf16_t>(float v) {
 __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 * (l >> 5) + (g & 3); }
 
 // The 256 x 256 block (m0, n0) of A * Bop, accumulated into acc (zeroed
-// here).  Wave w owns rows wm = 128 (w / 2) .. + 127 and columns
-// wn = 128 (w % 2) .. + 127 of the block.  When SQA && sqa, sq[i] gathers this
+// here), by NW waves: wave w owns the rows and columns Waves<NW>::wm / wn
+// give (128 x 128 with four waves, 128 x 64 with eight).  When SQA && sqa, sq[i] gathers this
 // lane's share of sum_k A[row, k]^2 for row wm + 32 i + lane % 32 (lanes l
 // and l + 32 hold the two k-halves of a row); when SQB && sqb, sb[j] does the same
 // for row wn + 32 j + lane % 32 of an N x K operand.  Returns once the last
 // MFMA is issued; the stages stay in use until the caller's next barrier.
-template <typename T, bool BNN, bool SQA, bool SQB>
+template <typename T, bool BNN, bool SQA, bool SQB, int NW>
 __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n0, uint16_t *lds,
-                                        f16v acc[4][4], bool sqa, float sq[4], bool sqb, float sb[4],
-                                        int tid) {
+                                        f16v acc[4][Waves<NW>::NJ], bool sqa, float sq[4], bool sqb,
+                                        float sb[Waves<NW>::NJ], int tid) {
     constexpr int TK = Op<T>::TK, P = Op<T>::PER;
+    constexpr int NJ = Waves<NW>::NJ, IPW = Waves<NW>::IPW;
     constexpr int64_t ES = sizeof(T);
     typedef typename Op<T>::V V;
     const int l = tid & 63, w = tid >> 6, h = l >> 5;
-    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
+    const int wm = Waves<NW>::wm(w), wn = Waves<NW>::wn(w);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f16v{};
+        for (int j = 0; j < NJ; ++j) acc[i][j] = f16v{};
     const T *A = static_cast<const T *>(g.A);
     const T *B = static_cast<const T *>(g.B);
     // buffer resources over exactly what this tile reads (row slices end at
@@ -276,24 +292,28 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 
     const int64_t nk = (g.K + TK - 1) / TK;
     auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
-    // part p (0..1) of this wave's loads of stage kt: instructions 4p ..
-    // 4p + 3 (of 8) of each operand
+    // part p (0..1) of this wave's loads of stage kt: with four waves,
+    // instructions 4p .. 4p + 3 (of 8) of each operand; with eight, the four
+    // of operand A (p = 0) or of operand B (p = 1)
     auto issue_part = [&](int64_t kt, int p) {
         uint16_t *st = stage(kt);
-        dma_rows4<T>(ra, g.lda, rows_a, kt * TK, g.K, st, tid, p);
-        if (BNN) dma_krows4<T>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid, p);
-        else dma_rows4<T>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid, p);
+        const int hp = (IPW == 8) ? p : 0;
+        if (IPW == 8 || p == 0) dma_rows4<T, IPW>(ra, g.lda, rows_a, kt * TK, g.K, st, tid, hp);
+        if (IPW == 8 || p == 1) {
+            if (BNN) dma_krows4<T, IPW>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid, hp);
+            else dma_rows4<T, IPW>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid, hp);
+        }
     };
     // Substep q (0..3) of a K-step: bf16 lanes take chunk 2q + lane / 32 (k
     // from 16 q + 8 (lane / 32)); fp32 lanes take chunk 4 (lane / 32) + q (k
     // from 16 (lane / 32) + 4 q), A and B alike, so each MFMA pairs the same k.
-    struct Frags { V a[4], b[4]; };
+    struct Frags { V a[4], b[NJ]; };
     auto load_frags = [&](const uint16_t *st, int q, Frags &f) {
         const int c = (sizeof(T) == 2) ? 2 * q + h : 4 * h + q;
 #pragma unroll
         for (int i = 0; i < 4; ++i) f.a[i] = frag_rows<T>(st, wm + 32 * i + (l & 31), c);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < NJ; ++j) {
             if constexpr (!BNN) f.b[j] = frag_rows<T>(st + OPT, wn + 32 * j + (l & 31), c);
             else if constexpr (sizeof(T) == 2) f.b[j] = frag_krows(st + OPT, 16 * q, wn + 32 * j, tid);
             else f.b[j] = frag_krows_f32(st + OPT, q, wn + 32 * j, tid);
@@ -311,7 +331,7 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 #pragma unroll
                 for (int i = 0; i < 4; ++i) f.a[i][e] = (typename Op<T>::E)0.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) f.b[j][e] = (typename Op<T>::E)0.f;
+                for (int j = 0; j < NJ; ++j) f.b[j][e] = (typename Op<T>::E)0.f;
             }
     };
     auto mma = [&](const Frags &f) {
@@ -319,7 +339,7 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+                for (int j = 0; j < NJ; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
         } else {
 #pragma unroll
@@ -327,7 +347,7 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
+                    for (int j = 0; j < NJ; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][e], f.b[j][e], acc[i][j], 0, 0, 0);
         }
         if (SQA && sqa) {
@@ -336,7 +356,7 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         }
         if (SQB && sqb) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) sb[j] += sum_sq(f.b[j]);
+            for (int j = 0; j < NJ; ++j) sb[j] += sum_sq(f.b[j]);
         }
     };
 
@@ -401,8 +421,10 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
 // norms from qnorm2 or from the A fragments, column norms from cnorm or from
 // the B fragments), scale * acc for dot.
 template <typename T, typename TO, bool BNN, bool SCALED>
-__global__ void __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ void __launch_bounds__(Waves<GEMM_NW>::NTHR) __attribute__((amdgpu_waves_per_eu(GEMM_NW / 4, GEMM_NW / 4)))
 gemm256_kernel(GemmArgs g) {
+    typedef Waves<GEMM_NW> W;
+    constexpr int NJ = W::NJ, WTN = W::WTN;
     extern __shared__ float lds_f[];
     uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
     const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
@@ -422,29 +444,33 @@ gemm256_kernel(GemmArgs g) {
     const int64_t n0 = (within / gm) * TN;
 
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int wm = (w >> 1) * 128, wn = (w & 1) * 128;
-    f16v acc[4][4];
+    const int wm = W::wm(w), wn = W::wn(w);
+    f16v acc[4][NJ];
     // row norms of A from the fragments already in registers (the waves of
     // the left column, wn == 0): for the rownorm2 side output of the tiles
     // with n0 == 0, or for cosine scores without qnorm2; column norms of B
     // likewise (the waves of the top row, wm == 0) for cosine without cnorm
-    const bool sqa = SCALED ? (g.cosine && g.qnorm2 == nullptr && (w & 1) == 0)
-                            : (g.rownorm2 != nullptr && n0 == 0 && (w & 1) == 0);
-    const bool sqb = SCALED && g.cosine && g.cnorm == nullptr && (w >> 1) == 0;
-    float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[4] = {0.f, 0.f, 0.f, 0.f};
-    mma_256<T, BNN, true, SCALED>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
+    const bool sqa = SCALED ? (g.cosine && g.qnorm2 == nullptr && wn == 0)
+                            : (g.rownorm2 != nullptr && n0 == 0 && wn == 0);
+    const bool sqb = SCALED && g.cosine && g.cnorm == nullptr && wm == 0;
+    float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) sb[j] = 0.f;
+    mma_256<T, BNN, true, SCALED, GEMM_NW>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
 
     float *rq = lds_f + LDS_BYTES / sizeof(float);   // SCALED: scale / ||x|| per row of the tile
     float *cn = rq + TM;                             // SCALED: 1 / ||c|| per column of the tile
     if (SCALED) {
         const int t = threadIdx.x;
         if (!g.cosine) {
-            rq[t] = g.scale;
-            cn[t] = 1.f;
+            if (t < TM) {
+                rq[t] = g.scale;
+                cn[t] = 1.f;
+            }
         } else {
             if (g.qnorm2) {
-                const float n2 = (m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f;
-                rq[t] = (n2 > 0.f) ? g.scale / sqrtf(n2) : 0.f;
+                const float n2 = (t < TM && m0 + t < g.M) ? g.qnorm2[m0 + t] : 1.f;
+                if (t < TM) rq[t] = (n2 > 0.f) ? g.scale / sqrtf(n2) : 0.f;
             } else if (sqa) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -453,11 +479,11 @@ gemm256_kernel(GemmArgs g) {
                 }
             }
             if (g.cnorm) {
-                const float c = (n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f;
-                cn[t] = (c > 0.f) ? 1.f / c : 0.f;
+                const float c = (t < TN && n0 + t < g.N) ? g.cnorm[n0 + t] : 1.f;
+                if (t < TN) cn[t] = (c > 0.f) ? 1.f / c : 0.f;
             } else if (sqb) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
+                for (int j = 0; j < NJ; ++j) {
                     const float n2 = sb[j] + __shfl_xor(sb[j], 32);
                     if (l < 32) cn[wn + 32 * j + l] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
                 }
@@ -481,9 +507,9 @@ gemm256_kernel(GemmArgs g) {
     __syncthreads();                      // every wave is done with the operand stages
     TO *C = static_cast<TO *>(g.C);
     constexpr int EPC = 16 / (int)sizeof(TO);                 // elements per 16-byte chunk
-    constexpr int CPR = 128 / EPC;                            // chunks per sub-tile row
-    constexpr int STRIDE = 128 * (int)sizeof(TO) + 16 * (int)sizeof(TO) / 2;   // bytes per staged row
-    unsigned char *region = reinterpret_cast<unsigned char *>(lds) + w * (64 * EP_STRIDE_MAX);
+    constexpr int CPR = WTN / EPC;                            // chunks per sub-tile row
+    constexpr int STRIDE = ep_stride<TO, GEMM_NW>();          // bytes per staged row
+    unsigned char *region = reinterpret_cast<unsigned char *>(lds) + w * (64 * ep_stride<float, GEMM_NW>());
     // whole tile inside the output, rows 16-byte aligned: plain 16-byte stores
     const bool interior = ((reinterpret_cast<uintptr_t>(C) & 15) == 0) && (g.ldc % EPC == 0) &&
                           m0 + TM <= g.M && n0 + TN <= g.N;
@@ -492,7 +518,7 @@ gemm256_kernel(GemmArgs g) {
 #pragma unroll
         for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int row = 32 * ii + acc_row(r, l), col = 32 * j + (l & 31);
@@ -523,8 +549,8 @@ gemm256_kernel(GemmArgs g) {
             }
         } else {
             // edge tiles and unaligned outputs: element stores within bounds
-            for (int id = l; id < 64 * 128; id += 64) {
-                const int rr = id >> 7, cc = id & 127;
+            for (int id = l; id < 64 * WTN; id += 64) {
+                const int rr = id / WTN, cc = id % WTN;
                 const int64_t grow = m0 + wm + 64 * h + rr, gcol = n0 + wn + cc;
                 if (grow < g.M && gcol < g.N) {
                     TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
@@ -609,8 +635,8 @@ sweep256_kernel(GemmArgs g) {
         // than kept live (and spilled) across the whole sweep
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
-        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
-        else mma_256<T, false, false, COLN>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
+        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN, 4>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
+        else mma_256<T, false, false, COLN, 4>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
 
         // cosine factors of the rows (first block) and of this block's columns
         if (nt == 0) {
@@ -754,8 +780,9 @@ hipError_t launch_to(bool b_nn, const GemmArgs &a, hipStream_t s) {
                          : reinterpret_cast<const void *>(gemm256_kernel<T, TO, false, false>);
     hipError_t e = raise_lds_limit(k, LDS_BYTES);
     if (e != hipSuccess) return e;
-    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<T, TO, true, false>), grid, dim3(NTH), LDS_BYTES, s, a);
-    else hipLaunchKernelGGL((gemm256_kernel<T, TO, false, false>), grid, dim3(NTH), LDS_BYTES, s, a);
+    const dim3 block(Waves<GEMM_NW>::NTHR);
+    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<T, TO, true, false>), grid, block, LDS_BYTES, s, a);
+    else hipLaunchKernelGGL((gemm256_kernel<T, TO, false, false>), grid, block, LDS_BYTES, s, a);
     return hipGetLastError();
 }
 
@@ -884,7 +911,8 @@ hipError_t launch_scores(const GemmArgs &a, bool softmax, hipStream_t s) {
     const void *k = reinterpret_cast<const void *>(gemm256_kernel<T, float, false, true>);
     hipError_t e = raise_lds_limit(k, SCORES_LDS_BYTES);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm256_kernel<T, float, false, true>), grid, dim3(NTH), SCORES_LDS_BYTES, s, b);
+    hipLaunchKernelGGL((gemm256_kernel<T, float, false, true>), grid, dim3(Waves<GEMM_NW>::NTHR), SCORES_LDS_BYTES, s,
+                       b);
     return hipGetLastError();
 }
 
