@@ -269,11 +269,11 @@ def mfma_workload(args, torch, gsm):
         calls.append(("project", lambda: gsm.gs_project(X, Q, out=T, xnorm2=True, xnorm2_out=xn), 2.0 * B * D * r))
         if args.workload == "stress":
             T2 = rows(B, r, dt)
-            calls.append(("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2), 2.0 * B * M * r))
-        calls.append(("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx),
-                      2.0 * B * M * r))
-        calls.append(("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=args.beta, out=A),
-                      2.0 * B * M * r))
+            calls.append(("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2, echelon=True), 2.0 * B * M * r))
+        calls.append(("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx,
+                                                              echelon=True), 2.0 * B * M * r))
+        calls.append(("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=args.beta, out=A,
+                                                            echelon=True), 2.0 * B * M * r))
         if args.workload == "stress":
             Xr = rows(B, D, dt)
             calls.append(("reconstruct", lambda: gsm.gs_reconstruct(T2, Q, out=Xr), 2.0 * B * r * D))
@@ -286,10 +286,10 @@ def mfma_workload(args, torch, gsm):
         idx = torch.empty(B, dtype=torch.int32, device=dev)
         Y = rows(B, D, torch.float32)
         Ty = rows(B, r, torch.float32)
-        calls.append(("prob2vec", lambda: (gsm.gs_prob2vec(Pa, R, out=Ta), gsm.gs_prob2vec(Pb, R, out=Tb)),
-                      2 * 2.0 * B * M * r))
-        calls.append(("similarity", lambda: gsm.gs_similarity(Ta, R, cnorm=cnorm, out=S, argmax_out=idx),
-                      2.0 * B * M * r))
+        calls.append(("prob2vec", lambda: (gsm.gs_prob2vec(Pa, R, out=Ta, echelon=True),
+                                           gsm.gs_prob2vec(Pb, R, out=Tb, echelon=True)), 2 * 2.0 * B * M * r))
+        calls.append(("similarity", lambda: gsm.gs_similarity(Ta, R, cnorm=cnorm, out=S, argmax_out=idx,
+                                                              echelon=True), 2.0 * B * M * r))
         calls.append(("reconstruct_bind", lambda: gsm.gs_reconstruct(Ta, Q, T2=Tb, bind="mul", out=Y),
                       4.0 * B * r * D))
         calls.append(("reproject", lambda: gsm.gs_project(Y, Q, out=Ty), 2.0 * B * D * r))
@@ -315,6 +315,10 @@ def mfma_workload(args, torch, gsm):
     for n, e0, e1 in evs:
         per[n].append(e0.elapsed_time(e1))
     flops = {n: fl for n, _, fl in calls}
+    # products with the lower-echelon R: flops on its nonzero entries only
+    # (2 B nnz(R) per product; R's zero blocks are skipped by the kernels)
+    nnz = int((R != 0).sum().item())
+    useful = {n: flops[n] * nnz / (M * r) for n in flops if n in ("prob2vec", "similarity", "attention")}
     dom = max(per, key=lambda n: sum(per[n]))
     dom_ms = float(np.mean(per[dom]))
     peak = MFMA_PEAK["bf16" if bf else "f32"]
@@ -345,6 +349,8 @@ def mfma_workload(args, torch, gsm):
         "cpu_baseline": None,
         "extra": {"per_call_ms": {n: float(np.mean(v)) for n, v in per.items()},
                   "per_call_TFLOPs": {n: flops[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in per},
+                  "per_call_useful_TFLOPs": {n: useful[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in useful},
+                  "nnz_R": nnz,
                   "compress_ms": compress_ms, "rank": r, "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(out), flush=True)

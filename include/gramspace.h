@@ -79,6 +79,20 @@ typedef enum { GS_F32 = 0, GS_BF16 = 1, GS_F64 = 2 } gs_dtype;
    of the normalised vectors (cosine). */
 typedef enum { GS_SIM_DOT = 0, GS_SIM_COSINE = 1 } gs_sim_mode;
 
+/*
+ * Structure flag for the codebook coordinates R of gs_prob2vec, gs_similarity
+ * and gs_attention: OR it into rt when R is lower echelon, R[j][k] == 0 for
+ * every k > j.  gs_compress returns R in this form: its basis is built from
+ * the codebook vectors in index order, so c_j lies in the span of the first
+ * j + 1 basis vectors (Eq. 1).  The large products then skip the blocks of R
+ * above its diagonal (at r = M about half the work of P R, T R^T and A R);
+ * for finite P, T and A the results are those of the same call without the
+ * flag.  Entries of R above the diagonal may then go unread: if they are not
+ * zero, the results are undefined.  Cosine scores whose ||x_b|| comes from T
+ * (qnorm2 == NULL) keep the full range.
+ */
+#define GS_ECHELON 0x100
+
 /* Component-wise operator applied after restoring two vectors. */
 typedef enum { GS_BIND_NONE = 0, GS_BIND_MUL = 1 } gs_bind;
 
@@ -157,7 +171,7 @@ gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t l
  * T = P R.
  *
  *   P      in   B x M, pt in {F32, BF16}, ldp >= M
- *   R      in   M x r, rt == pt, ldr >= r
+ *   R      in   M x r, rt == pt (| GS_ECHELON), ldr >= r
  *   T      out  B x r, tt in {F32, BF16}, ldt >= r
  * fp32 accumulation.
  */
@@ -175,7 +189,7 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
  * ||c_j|| = cnorm[j] when given, else ||R_j||.
  *
  *   T      in   B x r, tt in {F32, BF16}, ldt >= r
- *   R      in   M x r, rt == tt, ldr >= r
+ *   R      in   M x r, rt == tt (| GS_ECHELON), ldr >= r
  *               (r >= 1 and may exceed M: the same call on D-space vectors
  *               and the uncompressed codebook, r = D, is the dense lookup)
  *   qnorm2 in   float[B], nullable;  cnorm in float[M], nullable

@@ -199,9 +199,17 @@ gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t l
     return launched(launch_gemm(xt, qt, tt, false, EPI_STORE, a, (hipStream_t)stream), "gs_project");
 }
 
+// Element type of a codebook-coordinate argument without the GS_ECHELON flag.
+static gs_dtype coord_type(gs_dtype rt, bool *echelon) {
+    *echelon = ((int)rt & GS_ECHELON) != 0;
+    return (gs_dtype)((int)rt & ~GS_ECHELON);
+}
+
 gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t ldp,
-                      const void *R, gs_dtype rt, int64_t r, int64_t ldr,
+                      const void *R, gs_dtype rt_in, int64_t r, int64_t ldr,
                       void *T, gs_dtype tt, int64_t ldt, void *stream) {
+    bool ech;
+    const gs_dtype rt = coord_type(rt_in, &ech);
     if (!is_batch_type(pt) || rt != pt || !is_batch_type(tt))
         return fail(GS_ERR_DTYPE, "gs_prob2vec: P/R must be both f32 or both bf16 and T f32 or bf16");
     if (B < 0 || M < 1 || r < 1 || r > M) return fail(GS_ERR_SHAPE, "gs_prob2vec: need B >= 0 and 1 <= r <= M");
@@ -219,6 +227,7 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
     }
     GemmArgs a{};
     a.A = P; a.lda = ldp; a.B = R; a.ldb = ldr; a.C = T; a.ldc = ldt; a.M = B; a.N = r; a.K = M;
+    a.echelon = ech;
     return launched(launch_gemm(pt, rt, tt, true, EPI_STORE, a, (hipStream_t)stream), "gs_prob2vec");
 }
 
@@ -237,9 +246,11 @@ static gs_status check_sim_common(const char *fn, const void *T, gs_dtype tt, in
 }
 
 gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
-                        const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                        const void *R, gs_dtype rt_in, int64_t M, int64_t ldr,
                         const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
                         float *S, int64_t lds, int32_t *argmax, void *stream) {
+    bool ech;
+    const gs_dtype rt = coord_type(rt_in, &ech);
     GS_CHECK(check_sim_common("gs_similarity", T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
     if (!S && !argmax && B > 0) return fail(GS_ERR_ARG, "gs_similarity: S and argmax are both null");
     GS_CHECK(check_matrix(S, "S", B, M, lds, GS_F32, true));
@@ -260,15 +271,17 @@ gs_status gs_similarity(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_
     GemmArgs a{};
     a.A = T; a.lda = ldt; a.B = R; a.ldb = ldr; a.C = S; a.ldc = lds; a.M = B; a.N = M; a.K = r;
     a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale;
-    a.argmax = argmax; a.write_out = S != nullptr;
+    a.argmax = argmax; a.write_out = S != nullptr; a.echelon = ech;
     return launched(launch_gemm(tt, rt, GS_F32, false, EPI_SIM, a, (hipStream_t)stream), "gs_similarity");
 }
 
 gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
-                       const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                       const void *R, gs_dtype rt_in, int64_t M, int64_t ldr,
                        const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
                        float beta, float *A, int64_t lda, void *O, gs_dtype ot, int64_t ldo,
                        void *stream) {
+    bool ech;
+    const gs_dtype rt = coord_type(rt_in, &ech);
     GS_CHECK(check_sim_common("gs_attention", T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
     GS_CHECK(check_matrix(A, "A", B, M, lda, GS_F32, false));
     if (O && !is_batch_type(ot)) return fail(GS_ERR_DTYPE, "gs_attention: O must be f32 or bf16");
@@ -289,10 +302,12 @@ gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t
     GemmArgs a{};
     a.A = T; a.lda = ldt; a.B = R; a.ldb = ldr; a.C = A; a.ldc = lda; a.M = B; a.N = M; a.K = r;
     a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale; a.beta = beta;
+    a.echelon = ech;
     gs_status st = launched(launch_gemm(tt, rt, GS_F32, false, EPI_SOFTMAX, a, s), "gs_attention");
     if (st != GS_OK || !O) return st;
     GemmArgs o{};
     o.A = A; o.lda = lda; o.B = R; o.ldb = ldr; o.C = O; o.ldc = ldo; o.M = B; o.N = r; o.K = M;
+    o.echelon = ech;
     return launched(launch_gemm(GS_F32, rt, ot, true, EPI_STORE, o, s), "gs_attention (weighted sum)");
 }
 

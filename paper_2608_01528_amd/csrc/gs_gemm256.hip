@@ -254,12 +254,13 @@ __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 *
 // give (128 x 128 with four waves, 128 x 64 with eight).  When SQA && sqa, sq[i] gathers this
 // lane's share of sum_k A[row, k]^2 for row wm + 32 i + lane % 32 (lanes l
 // and l + 32 hold the two k-halves of a row); when SQB && sqb, sb[j] does the same
-// for row wn + 32 j + lane % 32 of an N x K operand.  Returns once the last
+// for row wn + 32 j + lane % 32 of an N x K operand.  Only k in [k_lo, k_hi)
+// is accumulated (k_lo a multiple of the K-step).  Returns once the last
 // MFMA is issued; the stages stay in use until the caller's next barrier.
 template <typename T, bool BNN, bool SQA, bool SQB, int NW>
 __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n0, uint16_t *lds,
                                         f16v acc[4][Waves<NW>::NJ], bool sqa, float sq[4], bool sqb,
-                                        float sb[Waves<NW>::NJ], int tid) {
+                                        float sb[Waves<NW>::NJ], int64_t k_lo, int64_t k_hi, int tid) {
     constexpr int TK = Op<T>::TK, P = Op<T>::PER;
     constexpr int NJ = Waves<NW>::NJ, IPW = Waves<NW>::IPW;
     constexpr int64_t ES = sizeof(T);
@@ -290,7 +291,7 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         cols_b = 0;
     }
 
-    const int64_t nk = (g.K + TK - 1) / TK;
+    const int64_t kt0 = k_lo / TK, kt1 = (k_hi + TK - 1) / TK;
     auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
     // part p (0..1) of this wave's loads of stage kt: with four waves,
     // instructions 4p .. 4p + 3 (of 8) of each operand; with eight, the four
@@ -319,15 +320,16 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
             else f.b[j] = frag_krows_f32(st + OPT, q, wn + 32 * j, tid);
         }
     };
-    // In the last K-step, zero the fragment elements at k >= K (both operands:
-    // what lies there in LDS is row padding or a re-read chunk, possibly NaN).
+    // In the last K-step, zero the fragment elements at k >= k_hi (both
+    // operands: what lies there in LDS is row padding, a re-read chunk or
+    // data past the range, possibly NaN).
     Frags f0, f1;
     auto mask_tail = [&](Frags &f, int64_t kt, int q) {
-        if (kt * TK + TK <= g.K) return;                 // a full step
+        if (kt * TK + TK <= k_hi) return;                // a full step
         const int64_t kb = kt * TK + ((sizeof(T) == 2) ? 16 * q + 8 * h : 16 * h + 4 * q);
 #pragma unroll
         for (int e = 0; e < P; ++e)
-            if (kb + e >= g.K) {
+            if (kb + e >= k_hi) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) f.a[i][e] = (typename Op<T>::E)0.f;
 #pragma unroll
@@ -391,17 +393,17 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         mma(f1);
     };
 
-    issue_part(0, 0);
-    issue_part(0, 1);
+    issue_part(kt0, 0);
+    issue_part(kt0, 1);
     wait_vm<0>();
     __builtin_amdgcn_s_barrier();
-    load_frags(stage(0), 0, f0);
-    if (nk == 1) mask_tail(f0, 0, 0);
+    load_frags(stage(kt0), 0, f0);
+    if (kt1 - kt0 == 1) mask_tail(f0, kt0, 0);
     // the steady state has no tail handling: the last two steps are peeled
-    for (int64_t kt = 0; kt + 2 < nk; ++kt) step(kt, false);
-    if (nk >= 2) step(nk - 2, true);
+    for (int64_t kt = kt0; kt + 2 < kt1; ++kt) step(kt, false);
+    if (kt1 - kt0 >= 2) step(kt1 - 2, true);
     {
-        const int64_t kt = nk - 1;
+        const int64_t kt = kt1 - 1;
         const uint16_t *cur = stage(kt);
         load_frags(cur, 1, f1);
         mask_tail(f1, kt, 1);
@@ -456,7 +458,20 @@ gemm256_kernel(GemmArgs g) {
     float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) sb[j] = 0.f;
-    mma_256<T, BNN, true, SCALED, GEMM_NW>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, threadIdx.x);
+    // Lower-echelon R (R[j][k] == 0 for k > j): as the K x N operand (P R,
+    // A R), its rows j < n0 are zero in this tile's columns; as the N x K
+    // operand (T R^T), its columns k >= n0 + TN are zero in this tile's rows.
+    // Row norms of A summed from the fragments need the whole K range.
+    int64_t k_lo = 0, k_hi = g.K;
+    const bool a_norms = SCALED ? (g.cosine && g.qnorm2 == nullptr) : (g.rownorm2 != nullptr);
+    if (g.echelon && !a_norms) {
+        if (BNN) {
+            if (n0 < g.K) k_lo = (n0 / Op<T>::TK) * Op<T>::TK;   // (else R is zero there: keep one range)
+        } else {
+            k_hi = (n0 + TN < g.K) ? n0 + TN : g.K;
+        }
+    }
+    mma_256<T, BNN, true, SCALED, GEMM_NW>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, k_lo, k_hi, threadIdx.x);
 
     float *rq = lds_f + LDS_BYTES / sizeof(float);   // SCALED: scale / ||x|| per row of the tile
     float *cn = rq + TM;                             // SCALED: 1 / ||c|| per column of the tile
@@ -635,8 +650,8 @@ sweep256_kernel(GemmArgs g) {
         // than kept live (and spilled) across the whole sweep
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
-        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN, 4>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, tid);
-        else mma_256<T, false, false, COLN, 4>(g, m0, n0, lds, acc, false, sa, sqb, sb, tid);
+        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN, 4>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, 0, g.K, tid);
+        else mma_256<T, false, false, COLN, 4>(g, m0, n0, lds, acc, false, sa, sqb, sb, 0, g.K, tid);
 
         // cosine factors of the rows (first block) and of this block's columns
         if (nt == 0) {

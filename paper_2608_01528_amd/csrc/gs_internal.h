@@ -120,6 +120,7 @@ struct GemmArgs {
     int write_out;                     // EPI_SIM: write scores to C
     int dma;                           // set by launch_gemm: bf16 pipelined loop
     int mul_out;                       // 256 x 256 store: C = C .* product (fp32 C)
+    int echelon;                       // B is a lower-echelon R (R[j][k] == 0 for k > j)
 };
 
 hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi epi,

@@ -31,6 +31,7 @@ GS_F32, GS_BF16, GS_F64 = 0, 1, 2
 GS_SIM_DOT, GS_SIM_COSINE = 0, 1
 GS_BIND_NONE, GS_BIND_MUL = 0, 1
 GS_BINDOP_MUL, GS_BINDOP_XOR, GS_BINDOP_CONV, GS_BINDOP_CORR = 0, 1, 2, 3
+GS_ECHELON = 0x100   # OR'ed into R's type: R[j, k] == 0 for k > j (as gs_compress returns it)
 
 _DT = {torch.float32: GS_F32, torch.bfloat16: GS_BF16, torch.float64: GS_F64}
 
@@ -183,10 +184,13 @@ def gs_project(X: torch.Tensor, Q: torch.Tensor, out_dtype=None, xnorm2: bool = 
     return (out, xn) if xnorm2 else out
 
 
-def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Tensor | None = None):
-    """T = P R: Gram-loc of sum_j P[b, j] c_j."""
+def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Tensor | None = None,
+                echelon: bool = False):
+    """T = P R: Gram-loc of sum_j P[b, j] c_j.  echelon: R is lower echelon
+    (as gs_compress returns it), so its zero blocks may be skipped."""
     pt, ldp = _mat(P, "P")
     rt, ldr = _mat(R, "R")
+    rt |= GS_ECHELON if echelon else 0
     B, M = P.shape
     r = R.shape[1]
     if out is None:
@@ -198,10 +202,13 @@ def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Ten
 
 def gs_similarity(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode="cosine",
                   scale: float = 1.0, scores: bool = True, argmax: bool = True,
-                  out: torch.Tensor | None = None, argmax_out: torch.Tensor | None = None):
-    """Scores S (B x M, fp32) and row argmax (int32) of T against R."""
+                  out: torch.Tensor | None = None, argmax_out: torch.Tensor | None = None,
+                  echelon: bool = False):
+    """Scores S (B x M, fp32) and row argmax (int32) of T against R
+    (echelon: as in gs_prob2vec)."""
     tt, ldt = _mat(T, "T")
     rt, ldr = _mat(R, "R")
+    rt |= GS_ECHELON if echelon else 0
     B, r = T.shape
     M = R.shape[0]
     S = None
@@ -218,11 +225,13 @@ def gs_similarity(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mod
 
 def gs_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode="cosine",
                  scale: float = 1.0, beta: float = 1.0, weighted_sum: bool = False, out_dtype=None,
-                 out: torch.Tensor | None = None, o_out: torch.Tensor | None = None):
+                 out: torch.Tensor | None = None, o_out: torch.Tensor | None = None,
+                 echelon: bool = False):
     """Attention weights A = softmax(beta * S) (B x M, fp32) and optionally the
-    weighted sum O = A R (B x r)."""
+    weighted sum O = A R (B x r) (echelon: as in gs_prob2vec)."""
     tt, ldt = _mat(T, "T")
     rt, ldr = _mat(R, "R")
+    rt |= GS_ECHELON if echelon else 0
     B, r = T.shape
     M = R.shape[0]
     A = out if out is not None else torch.empty((B, M), dtype=torch.float32, device=T.device)

@@ -256,3 +256,28 @@ def test_bind_restored_validation(L):
     assert call(B=0) == gsm.GS_OK
     assert call(B=0, op=gsm.GS_BINDOP_XOR, Lb=6) == gsm.GS_OK    # L is ignored by the element-wise operators
     assert err(L) == ""
+
+
+def test_echelon_flag_validation(L):
+    # GS_ECHELON is accepted on R of prob2vec, similarity and attention and
+    # stripped before the type checks; other bits, or the flag elsewhere, are not
+    e32, e16 = gsm.GS_F32 | gsm.GS_ECHELON, gsm.GS_BF16 | gsm.GS_ECHELON
+    p = L.gs_prob2vec
+    assert p(A1, gsm.GS_F32, 0, 5, 5, A2, e32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_OK
+    assert p(A1, gsm.GS_BF16, 0, 5, 8, A2, e16, 5, 8, A3, gsm.GS_BF16, 8, NULL) == gsm.GS_OK
+    assert p(A1, gsm.GS_BF16, 4, 5, 5, A2, e32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE
+    assert p(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32 | 0x200, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE
+    assert p(A1, e32, 4, 5, 5, A2, e32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE   # flag on P
+    s = L.gs_similarity
+    assert s(A1, gsm.GS_F32, 0, 5, 5, A2, e32, 5, 5, NULL, NULL, gsm.GS_SIM_COSINE, 1.0, A3, 5, A4,
+             NULL) == gsm.GS_OK
+    assert s(A1, gsm.GS_BF16, 4, 5, 5, A2, e32, 5, 5, NULL, NULL, gsm.GS_SIM_COSINE, 1.0, A3, 5, A4,
+             NULL) == gsm.GS_ERR_DTYPE
+    a = L.gs_attention
+    assert a(A1, gsm.GS_F32, 0, 5, 5, A2, e32, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0, 2.0, A3, 5, A4,
+             gsm.GS_F32, 5, NULL) == gsm.GS_OK
+    assert a(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F64 | gsm.GS_ECHELON, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0,
+             2.0, A3, 5, A4, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE
+    # not a coordinate argument of these calls
+    assert L.gs_project(A1, gsm.GS_F32, 4, 8, 8, A2, e32, 2, 8, A3, gsm.GS_F32, 2, NULL,
+                        NULL) == gsm.GS_ERR_DTYPE

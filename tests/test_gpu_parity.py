@@ -833,6 +833,110 @@ def test_sweep_cosine_argmax_only(sweep_case):
     check_argmax(host(idx[rows]), So, band_rel=1e-4)
 
 
+# ------------------------------------- lower-echelon R (GS_ECHELON) on the large tiles
+#
+# R from compress is lower echelon, R[j, k] == 0 for k > j; with the flag the
+# large-tile products skip the K-steps whose part of R is zero.  On a clean
+# echelon R the flagged and unflagged calls agree exactly (the skipped terms
+# are exact zeros); NaN put where a flagged call never reads (R[j, k] with k
+# in a later 256-block than j) shows the skip is taken, and the results still
+# match the oracle on the clean R.
+
+
+def echelon_pair(M, r, dtype, seed):
+    """(clean lower-echelon R, the same with NaN in the blocks a flagged call skips)."""
+    R = np.tril(_mat(M, r, seed, dtype))
+    j, k = np.meshgrid(np.arange(M), np.arange(r), indexing="ij")
+    dirty = R.copy()
+    dirty[(k // 256) > (j // 256)] = np.nan
+    return R, dirty
+
+
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+def test_echelon_prob2vec(op_dtype):
+    B, M, r = 8200, 2050, 2000
+    print("echelon prob2vec", _name(op_dtype), B, M, r, flush=True)
+    P = wl.dirichlet_probs(B, M, 0.5, 41)
+    if op_dtype == torch.bfloat16:
+        P = wl.round_bf16(P)
+    R, Rnan = echelon_pair(M, r, op_dtype, 42)
+    ldp, ldr = _ld(M, op_dtype), _ld(r, op_dtype)
+    Pd = nan_padded(P, ldp, op_dtype)
+    full = gsm.gs_prob2vec(Pd, nan_padded(R, ldr, op_dtype), out_dtype=torch.float32)
+    flagged = gsm.gs_prob2vec(Pd, nan_padded(R, ldr, op_dtype), out_dtype=torch.float32, echelon=True)
+    skipped = gsm.gs_prob2vec(Pd, nan_padded(Rnan, ldr, op_dtype), out_dtype=torch.float32, echelon=True)
+    torch.cuda.synchronize()
+    assert torch.equal(full, flagged)
+    rows = _tile_rows(B, 43)
+    Tr = host(skipped[rows])
+    assert np.isfinite(Tr).all()
+    assert rowrel(Tr, oracle.prob2vec(P[rows], R)) <= TOL_F32
+
+
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+@pytest.mark.parametrize("mode", ["cosine", "dot"])
+def test_echelon_similarity(op_dtype, mode):
+    B, M, r = 65573, 600, 500
+    print("echelon similarity", _name(op_dtype), mode, B, M, r, flush=True)
+    T = _mat(B, r, 44, op_dtype)
+    R, Rnan = echelon_pair(M, r, op_dtype, 45)
+    ld = _ld(r, op_dtype)
+    Td = nan_padded(T, ld, op_dtype)
+    qn = dev(oracle.row_norms(T) ** 2)
+    m = oracle.COSINE if mode == "cosine" else oracle.DOT
+    S0, i0 = gsm.gs_similarity(Td, nan_padded(R, ld, op_dtype), qnorm2=qn, mode=mode, scale=0.5)
+    S1, i1 = gsm.gs_similarity(Td, nan_padded(R, ld, op_dtype), qnorm2=qn, mode=mode, scale=0.5, echelon=True)
+    S2, i2 = gsm.gs_similarity(Td, nan_padded(Rnan, ld, op_dtype), qnorm2=qn, mode=mode, scale=0.5, echelon=True)
+    torch.cuda.synchronize()
+    assert torch.equal(S0, S1) and torch.equal(i0, i1)
+    rows = _tile_rows(B, 46)
+    So = oracle.similarity(T[rows], R, m, 0.5)
+    Sg = host(S2[rows])
+    assert np.isfinite(Sg).all()
+    assert rowrel(Sg, So) <= TOL_F32
+    check_argmax(host(i2[rows]), So, band_rel=1e-4)
+
+
+def test_echelon_similarity_norms_from_t_keep_full_range():
+    # cosine with ||x|| taken from T: the flagged call walks the whole K range
+    # (so it reads the whole of R) and still agrees exactly
+    dt = torch.bfloat16
+    B, M, r = 65573, 600, 500
+    print("echelon similarity, norms from T", B, M, r, flush=True)
+    T = _mat(B, r, 47, dt)
+    R, _ = echelon_pair(M, r, dt, 48)
+    ld = _ld(r, dt)
+    Td, Rd = nan_padded(T, ld, dt), nan_padded(R, ld, dt)
+    S0, i0 = gsm.gs_similarity(Td, Rd, mode="cosine")
+    S1, i1 = gsm.gs_similarity(Td, Rd, mode="cosine", echelon=True)
+    torch.cuda.synchronize()
+    assert torch.equal(S0, S1) and torch.equal(i0, i1)
+    rows = _tile_rows(B, 49)
+    assert rowrel(host(S1[rows]), oracle.similarity(T[rows], R, oracle.COSINE)) <= TOL_F32
+
+
+def test_echelon_attention_weighted_sum():
+    dt = torch.float32
+    B, M, r = 65573, 600, 500
+    print("echelon attention + weighted sum", B, M, r, flush=True)
+    T = _mat(B, r, 50, dt)
+    R, Rnan = echelon_pair(M, r, dt, 51)
+    ld = _ld(r, dt)
+    Td = nan_padded(T, ld, dt)
+    qn = dev(oracle.row_norms(T) ** 2)
+    A0, O0 = gsm.gs_attention(Td, nan_padded(R, ld, dt), qnorm2=qn, beta=4.0, weighted_sum=True)
+    A1, O1 = gsm.gs_attention(Td, nan_padded(R, ld, dt), qnorm2=qn, beta=4.0, weighted_sum=True, echelon=True)
+    A2, O2 = gsm.gs_attention(Td, nan_padded(Rnan, ld, dt), qnorm2=qn, beta=4.0, weighted_sum=True, echelon=True)
+    torch.cuda.synchronize()
+    assert torch.equal(A0, A1) and torch.equal(O0, O1)
+    rows = _tile_rows(B, 52)
+    Ao = oracle.softmax(oracle.similarity(T[rows], R, oracle.COSINE), 4.0)
+    Ag, Og = host(A2[rows]), host(O2[rows])
+    assert np.isfinite(Ag).all() and np.isfinite(Og).all()
+    assert rowrel(Ag, Ao) <= TOL_F32
+    assert rowrel(Og, oracle.prob2vec(Ao, R)) <= TOL_F32
+
+
 # ------------------------------------------- binding of restored vectors
 
 @pytest.mark.parametrize("B,D,L", [(37, 4096, 4096), (33, 1024, 128), (5, 8192, 8192), (9, 64, 2), (300, 512, 512)])
