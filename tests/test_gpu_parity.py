@@ -937,6 +937,53 @@ def test_echelon_attention_weighted_sum():
     assert rowrel(Og, oracle.prob2vec(Ao, R)) <= TOL_F32
 
 
+# ---------------------------- more entries than dimensions (D < M): partitioned bases
+#
+# The paper's treatment of D < M: split the M entries into subsets of at most
+# D and give each its own orthonormal basis; after the restore, the subsets
+# are put side by side again.  The calls compose it without new entry points:
+# one compress per row range; similarity by projecting the queries into each
+# basis and writing each subset's scores into its column block of S; prob2vec
+# by each subset's coordinates side by side, restored against the stacked
+# bases (sum over subsets of T_s Q_s = P C).  Checked against the oracle's
+# dense definitions.
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=_name)
+def test_partitioned_codebook_d_below_m(dt):
+    M, D, B = 100, 32, 300
+    print("partitioned codebook", M, D, B, _name(dt), flush=True)
+    C = wl.bipolar_codebook(M, D, 61)
+    X = _mat(B, D, 62, dt)
+    P = wl.dirichlet_probs(B, M, 0.5, 63)
+    if dt == torch.bfloat16:
+        P = wl.round_bf16(P)
+    Cd, Xd, Pd = dev(C), dev(X, dt), dev(P, dt)
+    S = torch.full((B, M), float("nan"), dtype=torch.float32, device="cuda")
+    xn = None
+    Ts, Qs = [], []
+    for off in range(0, M, D):
+        n = min(D, M - off)
+        Q, R, r, kept, cn = gsm.gs_compress(Cd[off:off + n], q_dtype=dt, r_dtype=dt)
+        assert r == n                                  # bipolar subsets of <= D rows: full rank
+        if xn is None:
+            T, xn = gsm.gs_project(Xd, Q, xnorm2=True)
+        else:
+            T = gsm.gs_project(Xd, Q)
+        gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, out=S[:, off:off + n], argmax=False, echelon=True)
+        Ts.append(gsm.gs_prob2vec(Pd[:, off:off + n].contiguous(), R, out_dtype=torch.float32, echelon=True))
+        Qs.append(Q.float())
+    torch.cuda.synchronize()
+    tol = TOL_BF16 if dt == torch.bfloat16 else TOL_F32      # bf16: Q and R rounded from fp64
+    So = oracle.similarity(X, C, oracle.COSINE)
+    assert np.isfinite(host(S)).all()
+    assert rowrel(host(S), So) <= tol
+    # restore: the subsets' coordinates side by side against the stacked bases
+    V = gsm.gs_reconstruct(torch.cat(Ts, dim=1).contiguous(), torch.cat(Qs, dim=0).contiguous())
+    torch.cuda.synchronize()
+    assert rowrel(host(V), oracle.prob2vec(P, C)) <= tol
+
+
 # ------------------------------------------- binding of restored vectors
 
 @pytest.mark.parametrize("B,D,L", [(37, 4096, 4096), (33, 1024, 128), (5, 8192, 8192), (9, 64, 2), (300, 512, 512)])
