@@ -63,6 +63,10 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE counter CSVs (kernel run, copy calibration) "
                          "into profiles/traffic_<kernel>_<workload>.json and exit")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="vsa: also time the fused steps spread round robin over this many streams in one "
+                         "graph (independent batches in flight together, as a server would run them); reported "
+                         "under extra.concurrent, not as the headline")
     ap.add_argument("--pmc-kernel", default="soft_gram_kernel")
     ap.add_argument("--pmc-copy-mib", type=int, default=512)
     return ap.parse_args()
@@ -181,14 +185,33 @@ def cpu_baseline_vsa(w, beta, seconds):
                                                                                     total)}
 
 
-def timed_graph(torch, steps, launch_step, stream):
+def timed_graph(torch, steps, launch_step, stream, nstreams=1):
     """Capture `steps` steps into one HIP graph and replay it once, bracketed
     by device synchronisation (wall clock) and by HIP events recorded on the
-    replay stream (GPU time).  Returns (wall seconds, GPU ms per step)."""
+    replay stream (GPU time).  Returns (wall seconds, GPU ms per step).  With
+    nstreams > 1 the steps go round robin to that many streams forked from
+    and joined back into the capture stream (independent steps overlap)."""
     g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for k in range(steps):
-            launch_step(k)
+    if nstreams == 1:
+        with torch.cuda.graph(g):
+            for k in range(steps):
+                launch_step(k)
+    else:
+        main = torch.cuda.Stream()
+        aux = [torch.cuda.Stream() for _ in range(nstreams - 1)]
+        with torch.cuda.graph(g, stream=main):
+            fork = torch.cuda.Event()
+            fork.record(main)
+            for s_ in aux:
+                s_.wait_event(fork)
+            streams = [main] + aux
+            for k in range(steps):
+                with torch.cuda.stream(streams[k % nstreams]):
+                    launch_step(k)
+            for s_ in aux:
+                join = torch.cuda.Event()
+                join.record(s_)
+                main.wait_event(join)
     g.replay()                      # warm replay (uploads the graph)
     torch.cuda.synchronize()
     a = torch.cuda.Event(enable_timing=True)
@@ -573,6 +596,11 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
         "buffer_copies": nsets,
     }
+    if args.streams > 1:
+        cwall, _ = timed_graph(torch, args.steps, fused_step, stream, nstreams=args.streams)
+        extra["concurrent"] = {"streams": args.streams, "ms_per_step": cwall * 1e3 / args.steps,
+                               "queries_per_s": work.queries * args.steps / cwall,
+                               "GBps": bpl * args.steps / cwall / 1e9}
     if not args.no_unfused:
         uwall, _ = timed_graph(torch, args.steps, unfused_step, stream)
         extra["unfused_12_calls_ms_per_step"] = uwall * 1e3 / args.steps

@@ -63,8 +63,9 @@ def test_large_workload_full_size():
     P = wl.device_dirichlet_half(w.B, 256, w.seed, torch, "cuda")
     X = wl.device_noisy_queries(P, Cd, w.noise_var, w.seed, torch)
     T, xn = gsm.gs_project(X, Q, xnorm2=True)
-    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine")
-    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0)
+    # R from compress is lower echelon: flagged as the benchmark does
+    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", echelon=True)
+    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0, echelon=True)
     torch.cuda.synchronize()
     whole_batch_properties(S, idx, A)
     rows = sample_rows(w.B, 48, 3)
@@ -93,9 +94,9 @@ def test_binary_workload_full_size():
     print("binary: batch", flush=True)
     Pa = wl.probabilities(w, 0)
     Pb = wl.probabilities(w, 0, stream=wl.STREAM_PROBS_B)
-    Ta = gsm.gs_prob2vec(dev(Pa), R)
-    Tb = gsm.gs_prob2vec(dev(Pb), R)
-    S, idx = gsm.gs_similarity(Ta, R, cnorm=cnorm, mode="cosine")
+    Ta = gsm.gs_prob2vec(dev(Pa), R, echelon=True)
+    Tb = gsm.gs_prob2vec(dev(Pb), R, echelon=True)
+    S, idx = gsm.gs_similarity(Ta, R, cnorm=cnorm, mode="cosine", echelon=True)
     Y = gsm.gs_reconstruct(Ta, Q, T2=Tb, bind="mul")
     Ty = gsm.gs_project(Y, Q)
     torch.cuda.synchronize()
@@ -135,9 +136,9 @@ def test_stress_workload_full_size():
     X = wl.device_noisy_queries(P, Cd, w.noise_var, w.seed, torch, dtype=torch.bfloat16)
     print("stress: project", flush=True)
     T, xn = gsm.gs_project(X, Q, out_dtype=torch.bfloat16, xnorm2=True)
-    T2 = gsm.gs_prob2vec(P, R, out_dtype=torch.bfloat16)
-    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine")
-    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0)
+    T2 = gsm.gs_prob2vec(P, R, out_dtype=torch.bfloat16, echelon=True)
+    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", echelon=True)
+    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0, echelon=True)
     Xr = gsm.gs_reconstruct(T2, Q, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     whole_batch_properties(S, idx, A)
