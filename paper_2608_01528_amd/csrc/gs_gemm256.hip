@@ -826,6 +826,55 @@ __global__ void __launch_bounds__(256) rows_argmax_kernel(const float *S, int64_
     if (l == 0) idx[row] = mi;
 }
 
+// One wave per row, in place: softmax of the row (max-subtracted), the row
+// held in registers (16-byte pieces; M <= 4 * 64 * V4, rows 16-byte aligned),
+// so it is read once and written once.
+template <int V4>
+__global__ void __launch_bounds__(256) rows_softmax_reg_kernel(float *A, int64_t lda, int64_t B, int64_t M) {
+    const int l = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= B) return;
+    float *a = A + row * lda;
+    f4v v[V4];
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < V4; ++i) {
+        const int64_t c = 4 * (l + 64 * i);
+        if (c + 4 <= M) {
+            v[i] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(a + c));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[i][e] = (c + e < M) ? a[c + e] : -INFINITY;
+        }
+        m = fmaxf(m, fmaxf(fmaxf(v[i][0], v[i][1]), fmaxf(v[i][2], v[i][3])));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float z = 0.f;
+#pragma unroll
+    for (int i = 0; i < V4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[i][e] = __expf(v[i][e] - m);          // exp(-inf) = 0 past the row's end
+            z += v[i][e];
+        }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    const float iz = 1.f / z;
+#pragma unroll
+    for (int i = 0; i < V4; ++i) {
+        const int64_t c = 4 * (l + 64 * i);
+        const f4v w = v[i] * iz;
+        if (c + 4 <= M) {
+            __builtin_nontemporal_store(w, reinterpret_cast<f4v *>(a + c));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (c + e < M) a[c + e] = w[e];
+        }
+    }
+}
+
 // One wave per row, in place: softmax of the row (max-subtracted).
 __global__ void __launch_bounds__(256) rows_softmax_kernel(float *A, int64_t lda, int64_t B, int64_t M) {
     const int l = threadIdx.x & 63;
@@ -965,7 +1014,11 @@ hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int
     if (B == 0 || M == 0) return hipSuccess;
     const dim3 rgrid((unsigned)((B + 3) / 4));
     if (softmax) {
-        hipLaunchKernelGGL(rows_softmax_kernel, rgrid, dim3(256), 0, s, out, ld, B, M);
+        // rows in registers when they fit (16-byte aligned rows of up to 2048)
+        const bool aligned = (reinterpret_cast<uintptr_t>(out) & 15) == 0 && ld % 4 == 0;
+        if (aligned && M <= 512) hipLaunchKernelGGL((rows_softmax_reg_kernel<2>), rgrid, dim3(256), 0, s, out, ld, B, M);
+        else if (aligned && M <= 2048) hipLaunchKernelGGL((rows_softmax_reg_kernel<8>), rgrid, dim3(256), 0, s, out, ld, B, M);
+        else hipLaunchKernelGGL(rows_softmax_kernel, rgrid, dim3(256), 0, s, out, ld, B, M);
         return hipGetLastError();
     }
     if (argmax) {

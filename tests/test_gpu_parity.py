@@ -937,6 +937,41 @@ def test_echelon_attention_weighted_sum():
     assert rowrel(Og, oracle.prob2vec(Ao, R)) <= TOL_F32
 
 
+def test_echelon_on_compressed_rank_deficient_codebook():
+    # R as gs_compress returns it for a codebook with duplicated rows (rank
+    # below M, pivots shifted left): flagged and unflagged products agree
+    # exactly, and match the oracle's dense definitions
+    M, D, B = 1100, 2048, 16400
+    print("echelon, compressed rank-deficient codebook", M, D, B, flush=True)
+    C = wl.bipolar_codebook(M, D, 71)
+    rng = np.random.default_rng(72)
+    tgt = rng.choice(M, size=110, replace=False)
+    src = rng.choice(np.setdiff1d(np.arange(M), tgt), size=110)
+    C[tgt] = C[src]
+    Q, R, r, kept, cn = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert r == M - 110
+    Rh = host(R)
+    assert np.all(np.triu(Rh, 1) == 0)                    # R[j, k] == 0 for k > j
+    P = wl.dirichlet_probs(B, M, 0.5, 73)
+    Pd = dev(P)
+    T0 = gsm.gs_prob2vec(Pd, R)
+    T1 = gsm.gs_prob2vec(Pd, R, echelon=True)
+    X = _mat(B, D, 74, torch.float32)
+    Tx, xn = gsm.gs_project(dev(X), Q, xnorm2=True)
+    S0, i0 = gsm.gs_similarity(Tx, R, qnorm2=xn, cnorm=cn)
+    S1, i1 = gsm.gs_similarity(Tx, R, qnorm2=xn, cnorm=cn, echelon=True)
+    torch.cuda.synchronize()
+    assert torch.equal(T0, T1)
+    assert torch.equal(S0, S1) and torch.equal(i0, i1)
+    rows = _tile_rows(B, 75)
+    Qo = oracle.compress(C)[0]
+    assert rowrel(host(T1[rows]), oracle.project(oracle.prob2vec(P[rows], C), Qo)) <= TOL_F32
+    So = oracle.similarity(X[rows], C, oracle.COSINE)
+    assert rowrel(host(S1[rows]), So) <= TOL_F32
+    check_argmax(host(i1[rows]), So, band_rel=1e-4)
+
+
 # ---------------------------- more entries than dimensions (D < M): partitioned bases
 #
 # The paper's treatment of D < M: split the M entries into subsets of at most
