@@ -356,7 +356,7 @@ def mfma_workload(args, torch, gsm):
     if dom in store:
         m_, n_, what = store[dom]
         on_big = big(m_, n_) and (dom != "reconstruct_bind" or not bf)
-        kernel = "%s (%s)" % ("gemm256_kernel" if on_big else "gemm_store_kernel", what)
+        kernel = "%s (%s)" % ("gemm256_store_kernel" if on_big else "gemm_store_kernel", what)
     else:
         kernel = {"similarity": "similarity scores", "attention": "attention weights"}[dom]
     out = {

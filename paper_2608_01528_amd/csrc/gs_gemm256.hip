@@ -249,21 +249,68 @@ template <> __device__ __forceinline__ bf16_t to_out<bf16_t>(float v) {
 // Row of the output held by accumulator register g of a 32x32 block, for lane l.
 __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 * (l >> 5) + (g & 3); }
 
+// The loads of one 256 x 256 tile (m0, n0): buffer resources over exactly
+// what the tile reads (row slices end at column ceil(K / P) * P, k-row slices
+// at column ceil(N / P) * P) and the issue of part p (0..1) of this wave's
+// share of the operand tiles of K-step kt into a stage: with four waves,
+// instructions 4p .. 4p + 3 (of 8) of each operand; with eight, the four of
+// operand A (p = 0) or of operand B (p = 1).
+template <typename T, bool BNN, int NW>
+struct TileLoads {
+    rsrc_t ra, rb;
+    int64_t rows_a, rows_b, cols_b;
+    __device__ __forceinline__ void init(const GemmArgs &g, int64_t m0, int64_t n0) {
+        constexpr int P = Op<T>::PER;
+        constexpr int64_t ES = sizeof(T);
+        const T *A = static_cast<const T *>(g.A);
+        const T *B = static_cast<const T *>(g.B);
+        const int64_t kp = (g.K + P - 1) / P * P, np = (g.N + P - 1) / P * P;
+        rows_a = (g.M - m0 < TM) ? (g.M - m0) : TM;
+        ra = make_rsrc(A + m0 * g.lda, ES * ((rows_a - 1) * g.lda + kp));
+        if (BNN) {
+            cols_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
+            const int64_t span = (np - n0 < TN) ? (np - n0) : TN;
+            rb = make_rsrc(B + n0, ES * ((g.K - 1) * g.ldb + span));
+            rows_b = 0;
+        } else {
+            rows_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
+            rb = make_rsrc(B + n0 * g.ldb, ES * ((rows_b - 1) * g.ldb + kp));
+            cols_b = 0;
+        }
+    }
+    __device__ __forceinline__ void issue(const GemmArgs &g, int64_t kt, int p, uint16_t *st, int tid) const {
+        constexpr int TK = Op<T>::TK, IPW = Waves<NW>::IPW;
+        const int hp = (IPW == 8) ? p : 0;
+        if (IPW == 8 || p == 0) dma_rows4<T, IPW>(ra, g.lda, rows_a, kt * TK, g.K, st, tid, hp);
+        if (IPW == 8 || p == 1) {
+            if (BNN) dma_krows4<T, IPW>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid, hp);
+            else dma_rows4<T, IPW>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid, hp);
+        }
+    }
+};
+
+// LDS stage slot s (0 or 1): both operand tiles of one K-step.
+__device__ __forceinline__ uint16_t *stage_slot(uint16_t *lds, int s) { return lds + s * (2 * OPT); }
+
 // The 256 x 256 block (m0, n0) of A * Bop, accumulated into acc (zeroed
 // here), by NW waves: wave w owns the rows and columns Waves<NW>::wm / wn
 // give (128 x 128 with four waves, 128 x 64 with eight).  When SQA && sqa, sq[i] gathers this
 // lane's share of sum_k A[row, k]^2 for row wm + 32 i + lane % 32 (lanes l
 // and l + 32 hold the two k-halves of a row); when SQB && sqb, sb[j] does the same
 // for row wn + 32 j + lane % 32 of an N x K operand.  Only k in [k_lo, k_hi)
-// is accumulated (k_lo a multiple of the K-step).  Returns once the last
-// MFMA is issued; the stages stay in use until the caller's next barrier.
+// is accumulated (k_lo a multiple of the K-step).  K-step k_lo / TK + i uses
+// stage slot (slot0 + i) mod 2.  With preissued the first stage's loads were
+// issued by the caller, followed by `pending` (0, 16 or 32) other vector
+// memory instructions of this wave that need not be waited for.  Returns once
+// the last MFMA is issued; the stages stay in use until the caller's next
+// barrier.
 template <typename T, bool BNN, bool SQA, bool SQB, int NW>
-__device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n0, uint16_t *lds,
+__device__ __forceinline__ void mma_256(const GemmArgs &g, const TileLoads<T, BNN, NW> &tl, uint16_t *lds,
+                                        int slot0, bool preissued, int pending,
                                         f16v acc[4][Waves<NW>::NJ], bool sqa, float sq[4], bool sqb,
                                         float sb[Waves<NW>::NJ], int64_t k_lo, int64_t k_hi, int tid) {
     constexpr int TK = Op<T>::TK, P = Op<T>::PER;
-    constexpr int NJ = Waves<NW>::NJ, IPW = Waves<NW>::IPW;
-    constexpr int64_t ES = sizeof(T);
+    constexpr int NJ = Waves<NW>::NJ;
     typedef typename Op<T>::V V;
     const int l = tid & 63, w = tid >> 6, h = l >> 5;
     const int wm = Waves<NW>::wm(w), wn = Waves<NW>::wn(w);
@@ -271,40 +318,9 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = f16v{};
-    const T *A = static_cast<const T *>(g.A);
-    const T *B = static_cast<const T *>(g.B);
-    // buffer resources over exactly what this tile reads (row slices end at
-    // column ceil(K / P) * P, k-row slices at column ceil(N / P) * P)
-    const int64_t kp = (g.K + P - 1) / P * P, np = (g.N + P - 1) / P * P;
-    const int64_t rows_a = (g.M - m0 < TM) ? (g.M - m0) : TM;
-    const rsrc_t ra = make_rsrc(A + m0 * g.lda, ES * ((rows_a - 1) * g.lda + kp));
-    int64_t rows_b, cols_b;
-    rsrc_t rb;
-    if (BNN) {
-        cols_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
-        const int64_t span = (np - n0 < TN) ? (np - n0) : TN;
-        rb = make_rsrc(B + n0, ES * ((g.K - 1) * g.ldb + span));
-        rows_b = 0;
-    } else {
-        rows_b = (g.N - n0 < TN) ? (g.N - n0) : TN;
-        rb = make_rsrc(B + n0 * g.ldb, ES * ((rows_b - 1) * g.ldb + kp));
-        cols_b = 0;
-    }
-
     const int64_t kt0 = k_lo / TK, kt1 = (k_hi + TK - 1) / TK;
-    auto stage = [&](int64_t kt) { return lds + (int)(kt % NSTAGE) * (2 * OPT); };
-    // part p (0..1) of this wave's loads of stage kt: with four waves,
-    // instructions 4p .. 4p + 3 (of 8) of each operand; with eight, the four
-    // of operand A (p = 0) or of operand B (p = 1)
-    auto issue_part = [&](int64_t kt, int p) {
-        uint16_t *st = stage(kt);
-        const int hp = (IPW == 8) ? p : 0;
-        if (IPW == 8 || p == 0) dma_rows4<T, IPW>(ra, g.lda, rows_a, kt * TK, g.K, st, tid, hp);
-        if (IPW == 8 || p == 1) {
-            if (BNN) dma_krows4<T, IPW>(rb, g.ldb, kt * TK, g.K, cols_b, st + OPT, tid, hp);
-            else dma_rows4<T, IPW>(rb, g.ldb, rows_b, kt * TK, g.K, st + OPT, tid, hp);
-        }
-    };
+    auto stage = [&](int64_t kt) { return stage_slot(lds, (int)((kt - kt0 + slot0) & 1)); };
+    auto issue_part = [&](int64_t kt, int p) { tl.issue(g, kt, p, stage(kt), tid); };
     // Substep q (0..3) of a K-step: bf16 lanes take chunk 2q + lane / 32 (k
     // from 16 q + 8 (lane / 32)); fp32 lanes take chunk 4 (lane / 32) + q (k
     // from 16 (lane / 32) + 4 q), A and B alike, so each MFMA pairs the same k.
@@ -393,9 +409,13 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
         mma(f1);
     };
 
-    issue_part(kt0, 0);
-    issue_part(kt0, 1);
-    wait_vm<0>();
+    if (!preissued) {
+        issue_part(kt0, 0);
+        issue_part(kt0, 1);
+    }
+    if (preissued && pending == 32) wait_vm<32>();
+    else if (preissued && pending == 16) wait_vm<16>();
+    else wait_vm<0>();
     __builtin_amdgcn_s_barrier();
     load_frags(stage(kt0), 0, f0);
     if (kt1 - kt0 == 1) mask_tail(f0, kt0, 0);
@@ -418,14 +438,197 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, int64_t m0, int64_t n
     }
 }
 
-// SCALED: similarity scores instead of the plain product (fp32 output, B
-// stored N x K): out = scale * acc / (||x_row|| ||c_col||) for cosine (row
-// norms from qnorm2 or from the A fragments, column norms from cnorm or from
-// the B fragments), scale * acc for dot.
-template <typename T, typename TO, bool BNN, bool SCALED>
+// Tile order shared by the 256 x 256 kernels.  Work-group ids are dealt to
+// the 8 XCDs round robin, so XCD x runs logical tiles [x per, (x + 1) per);
+// in logical order, groups of GROUP_M m-tiles take each n-tile in turn, so
+// the tiles one XCD runs together share A row blocks and B column blocks in
+// L2.
+__device__ __forceinline__ void tile_of(int64_t lt, int64_t nM, int64_t nN, int64_t &m0, int64_t &n0) {
+    const int64_t grp = lt / (GROUP_M * nN);
+    const int64_t first_m = grp * GROUP_M;
+    const int64_t gm = (nM - first_m < GROUP_M) ? (nM - first_m) : GROUP_M;
+    const int64_t within = lt - grp * GROUP_M * nN;
+    m0 = (first_m + within % gm) * TM;
+    n0 = (within / gm) * TN;
+}
+
+// K range of tile column n0 when B is a lower-echelon R (R[j][k] == 0 for
+// k > j): as the K x N operand (P R, A R) its rows j < n0 are zero in this
+// tile's columns; as the N x K operand (T R^T) its columns k >= n0 + TN are
+// zero in this tile's rows.  Row norms of A summed from the fragments need
+// the whole K range.
+template <typename T, bool BNN>
+__device__ __forceinline__ void k_range(const GemmArgs &g, int64_t n0, bool a_norms, int64_t &k_lo, int64_t &k_hi) {
+    k_lo = 0;
+    k_hi = g.K;
+    if (!g.echelon || a_norms) return;
+    if (BNN) {
+        if (n0 < g.K) k_lo = (n0 / Op<T>::TK) * Op<T>::TK;   // (else R is zero there: keep one range)
+    } else {
+        k_hi = (n0 + TN < g.K) ? n0 + TN : g.K;
+    }
+}
+
+// Plain products on 256 x 256 tiles (project, prob2vec, reconstruct, the
+// second factor of a bound product).  Work-group b takes tile lt = x per + b / 8
+// of its XCD x's range, then every (grid / 8)-th after it in that range: with
+// one work-group per tile that is the tile alone; with a persistent grid (one
+// work-group per CU) it walks its share of the range.
+// When a tile's last MFMAs are issued, the next tile's first stage is loaded
+// into the stage slot the last K-step did not read, and the output is staged
+// through the other slot in passes of PR rows (32 bf16 or 16 fp32 rows of
+// every wave, 36 KiB in all), then written with streaming stores that are not
+// waited for: the next tile waits only for its own first stage (issued before
+// those stores), so the stores drain while it computes.
+template <typename T, typename TO, bool BNN>
 __global__ void __launch_bounds__(Waves<GEMM_NW>::NTHR) __attribute__((amdgpu_waves_per_eu(GEMM_NW / 4, GEMM_NW / 4)))
-gemm256_kernel(GemmArgs g) {
+gemm256_store_kernel(GemmArgs g) {
     typedef Waves<GEMM_NW> W;
+    constexpr int NJ = W::NJ, WTN = W::WTN, TK = Op<T>::TK;
+    constexpr int PR = sizeof(TO) == 2 ? 32 : 16;            // rows per staging pass
+    constexpr int RP = PR / 2;                               // accumulator registers per pass
+    constexpr int EPC = 16 / (int)sizeof(TO);                // elements per 16-byte chunk
+    constexpr int CPR = WTN / EPC;                           // chunks per sub-tile row
+    constexpr int STRIDE = ep_stride<TO, GEMM_NW>();         // bytes per staged row
+    constexpr int NSTORES = 4 * (32 / PR) * (PR * CPR / 64); // streaming stores per wave per interior tile
+    static_assert(NSTORES == 16 || NSTORES == 32, "waits of mma_256");
+    static_assert(GEMM_NW * PR * STRIDE <= 2 * OPT * 2, "staging fits one stage slot");
+    extern __shared__ float lds_f[];
+    uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
+    const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
+    const int64_t total = nM * nN;
+    const int64_t per = (total + 7) / 8;
+    const int64_t xcd = blockIdx.x & 7, nq = gridDim.x >> 3;
+    const int64_t lt_end = ((xcd + 1) * per < total) ? (xcd + 1) * per : total;
+    int64_t lt = xcd * per + (blockIdx.x >> 3);
+    if (lt >= lt_end) return;
+    TO *C = static_cast<TO *>(g.C);
+    const bool a_norms = g.rownorm2 != nullptr;
+
+    int64_t m0, n0, k_lo, k_hi;
+    tile_of(lt, nM, nN, m0, n0);
+    k_range<T, BNN>(g, n0, a_norms, k_lo, k_hi);
+    TileLoads<T, BNN, GEMM_NW> tl;
+    tl.init(g, m0, n0);
+    int slot0 = 0, pending = 0;
+    tl.issue(g, k_lo / TK, 0, stage_slot(lds, slot0), threadIdx.x);
+    tl.issue(g, k_lo / TK, 1, stage_slot(lds, slot0), threadIdx.x);
+    for (;;) {
+        // the thread id passes through an empty asm per tile, so the
+        // lane-dependent addresses are recomputed here rather than kept live
+        // (and spilled) across the product loop
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));
+        const int l = tid & 63, w = tid >> 6;
+        const int wm = W::wm(w), wn = W::wn(w);
+        f16v acc[4][NJ];
+        // row norms of A from the fragments (the waves of the left column):
+        // the rownorm2 side output of the tiles with n0 == 0
+        const bool sqa = a_norms && n0 == 0 && wn == 0;
+        float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[NJ];
+        mma_256<T, BNN, true, false, GEMM_NW>(g, tl, lds, slot0, true, pending, acc, sqa, sq, false, sb, k_lo,
+                                              k_hi, tid);
+        if (sqa) {
+            // lanes l and l + 32 hold the two k-halves of row wm + 32 i + l % 32
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float t = sq[i] + __shfl_xor(sq[i], 32);
+                const int64_t row = m0 + wm + 32 * i + l;
+                if (l < 32 && row < g.M) g.rownorm2[row] = t;
+            }
+        }
+        // the next tile's first stage, into the slot the last K-step did not read
+        const int next_slot = (int)((slot0 + (k_hi + TK - 1) / TK - k_lo / TK) & 1);
+        const int64_t nlt = lt + nq;
+        const bool has_next = nlt < lt_end;
+        int64_t m1 = 0, n1 = 0, k_lo1 = 0, k_hi1 = 0;
+        TileLoads<T, BNN, GEMM_NW> tl1;
+        if (has_next) {
+            tile_of(nlt, nM, nN, m1, n1);
+            k_range<T, BNN>(g, n1, a_norms, k_lo1, k_hi1);
+            tl1.init(g, m1, n1);
+            tl1.issue(g, k_lo1 / TK, 0, stage_slot(lds, next_slot), tid);
+            tl1.issue(g, k_lo1 / TK, 1, stage_slot(lds, next_slot), tid);
+        }
+        __syncthreads();                  // every wave is done reading this tile's stages
+
+        // Epilogue: each wave stages PR rows of its 128 x WTN sub-tile at a
+        // time in its own part of the other slot (rows padded so the
+        // column-wise writes of the accumulator layout do not collide on
+        // banks), then writes whole 16-byte row chunks.
+        unsigned char *region = reinterpret_cast<unsigned char *>(stage_slot(lds, next_slot ^ 1)) + w * (PR * STRIDE);
+        // whole tile inside the output, rows 16-byte aligned: 16-byte stores
+        const bool interior = ((reinterpret_cast<uintptr_t>(C) & 15) == 0) && (g.ldc % EPC == 0) &&
+                              m0 + TM <= g.M && n0 + TN <= g.N;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int hh = 0; hh < 32 / PR; ++hh) {
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int gg = 0; gg < RP; ++gg) {
+                        const int row = acc_row(RP * hh + gg, l) - PR * hh, col = 32 * j + (l & 31);
+                        *reinterpret_cast<TO *>(region + row * STRIDE + col * (int)sizeof(TO)) =
+                            to_out<TO>(acc[i][j][RP * hh + gg]);
+                    }
+                const int64_t rb = m0 + wm + 32 * i + PR * hh;   // first output row of this pass
+                if (interior) {
+#pragma unroll
+                    for (int id = l; id < PR * CPR; id += 64) {
+                        const int rr = id / CPR, cc = id % CPR;
+                        u32x4 v = *reinterpret_cast<const u32x4 *>(region + rr * STRIDE + cc * 16);
+                        TO *dst = C + (rb + rr) * g.ldc + (n0 + wn + cc * EPC);
+                        if constexpr (sizeof(TO) == 4) {
+                            if (g.mul_out) {   // second factor of a bound product
+                                const f4v x = __builtin_bit_cast(f4v, v) *
+                                              __builtin_nontemporal_load(reinterpret_cast<const f4v *>(dst));
+                                v = __builtin_bit_cast(u32x4, x);
+                            }
+                        }
+                        // streaming store: the output is not re-read by this kernel and
+                        // should not displace the operand slices other tiles share in L2
+                        __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dst));
+                    }
+                } else {
+                    // edge tiles and unaligned outputs: element stores within bounds
+                    for (int id = l; id < PR * WTN; id += 64) {
+                        const int rr = id / WTN, cc = id % WTN;
+                        const int64_t grow = rb + rr, gcol = n0 + wn + cc;
+                        if (grow < g.M && gcol < g.N) {
+                            TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
+                            if constexpr (sizeof(TO) == 4) {
+                                if (g.mul_out) x = x * C[grow * g.ldc + gcol];
+                            }
+                            C[grow * g.ldc + gcol] = x;
+                        }
+                    }
+                }
+            }
+        if (!has_next) break;
+        // the stores just issued (a fixed count on interior tiles without
+        // loads in the epilogue) need not land before the next tile starts
+        pending = (interior && !g.mul_out) ? NSTORES : 0;
+        lt = nlt;
+        m0 = m1;
+        n0 = n1;
+        k_lo = k_lo1;
+        k_hi = k_hi1;
+        tl = tl1;
+        slot0 = next_slot;
+    }
+}
+
+// Similarity scores on 256 x 256 tiles (fp32 output, B = R stored N x K):
+// out = scale * acc / (||x_row|| ||c_col||) for cosine (row norms from qnorm2
+// or from the A fragments, column norms from cnorm or from the B fragments),
+// scale * acc for dot; one tile per work-group.
+template <typename T>
+__global__ void __launch_bounds__(Waves<GEMM_NW>::NTHR) __attribute__((amdgpu_waves_per_eu(GEMM_NW / 4, GEMM_NW / 4)))
+scores256_kernel(GemmArgs g) {
+    typedef Waves<GEMM_NW> W;
+    typedef float TO;
+    constexpr bool BNN = false, SCALED = true;
     constexpr int NJ = W::NJ, WTN = W::WTN;
     extern __shared__ float lds_f[];
     uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
@@ -436,42 +639,25 @@ gemm256_kernel(GemmArgs g) {
     const int64_t per = (total + 7) / 8;
     const int64_t lt = (int64_t)(blockIdx.x & 7) * per + (blockIdx.x >> 3);
     if (lt >= total) return;
-    // Logical order: groups of GROUP_M m-tiles take each n-tile in turn, so the
-    // tiles one XCD runs together share A row blocks and B column blocks in L2.
-    const int64_t grp = lt / (GROUP_M * nN);
-    const int64_t first_m = grp * GROUP_M;
-    const int64_t gm = (nM - first_m < GROUP_M) ? (nM - first_m) : GROUP_M;
-    const int64_t within = lt - grp * GROUP_M * nN;
-    const int64_t m0 = (first_m + within % gm) * TM;
-    const int64_t n0 = (within / gm) * TN;
+    int64_t m0, n0;
+    tile_of(lt, nM, nN, m0, n0);
 
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int wm = W::wm(w), wn = W::wn(w);
     f16v acc[4][NJ];
     // row norms of A from the fragments already in registers (the waves of
-    // the left column, wn == 0): for the rownorm2 side output of the tiles
-    // with n0 == 0, or for cosine scores without qnorm2; column norms of B
-    // likewise (the waves of the top row, wm == 0) for cosine without cnorm
-    const bool sqa = SCALED ? (g.cosine && g.qnorm2 == nullptr && wn == 0)
-                            : (g.rownorm2 != nullptr && n0 == 0 && wn == 0);
-    const bool sqb = SCALED && g.cosine && g.cnorm == nullptr && wm == 0;
+    // the left column, wn == 0) for cosine scores without qnorm2; column
+    // norms of B likewise (the waves of the top row, wm == 0) without cnorm
+    const bool sqa = g.cosine && g.qnorm2 == nullptr && wn == 0;
+    const bool sqb = g.cosine && g.cnorm == nullptr && wm == 0;
     float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) sb[j] = 0.f;
-    // Lower-echelon R (R[j][k] == 0 for k > j): as the K x N operand (P R,
-    // A R), its rows j < n0 are zero in this tile's columns; as the N x K
-    // operand (T R^T), its columns k >= n0 + TN are zero in this tile's rows.
-    // Row norms of A summed from the fragments need the whole K range.
-    int64_t k_lo = 0, k_hi = g.K;
-    const bool a_norms = SCALED ? (g.cosine && g.qnorm2 == nullptr) : (g.rownorm2 != nullptr);
-    if (g.echelon && !a_norms) {
-        if (BNN) {
-            if (n0 < g.K) k_lo = (n0 / Op<T>::TK) * Op<T>::TK;   // (else R is zero there: keep one range)
-        } else {
-            k_hi = (n0 + TN < g.K) ? n0 + TN : g.K;
-        }
-    }
-    mma_256<T, BNN, true, SCALED, GEMM_NW>(g, m0, n0, lds, acc, sqa, sq, sqb, sb, k_lo, k_hi, threadIdx.x);
+    int64_t k_lo, k_hi;
+    k_range<T, BNN>(g, n0, g.cosine && g.qnorm2 == nullptr, k_lo, k_hi);
+    TileLoads<T, BNN, GEMM_NW> tl;
+    tl.init(g, m0, n0);
+    mma_256<T, BNN, true, SCALED, GEMM_NW>(g, tl, lds, 0, false, 0, acc, sqa, sq, sqb, sb, k_lo, k_hi, threadIdx.x);
 
     float *rq = lds_f + LDS_BYTES / sizeof(float);   // SCALED: scale / ||x|| per row of the tile
     float *cn = rq + TM;                             // SCALED: 1 / ||c|| per column of the tile
@@ -503,15 +689,6 @@ gemm256_kernel(GemmArgs g) {
                     if (l < 32) cn[wn + 32 * j + l] = (n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f;
                 }
             }
-        }
-    }
-    if (!SCALED && sqa) {
-        // lanes l and l + 32 hold the two k-halves of row wm + 32 i + l % 32
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float t = sq[i] + __shfl_xor(sq[i], 32);
-            const int64_t row = m0 + wm + 32 * i + l;
-            if (l < 32 && row < g.M) g.rownorm2[row] = t;
         }
     }
 
@@ -551,13 +728,6 @@ gemm256_kernel(GemmArgs g) {
                     v = __builtin_bit_cast(u32x4, x);
                 }
                 TO *dst = C + (m0 + wm + 64 * h + rr) * g.ldc + (n0 + wn + cc * EPC);
-                if constexpr (sizeof(TO) == 4 && !SCALED) {
-                    if (g.mul_out) {   // second factor of a bound product
-                        const f4v x = __builtin_bit_cast(f4v, v) *
-                                      __builtin_nontemporal_load(reinterpret_cast<const f4v *>(dst));
-                        v = __builtin_bit_cast(u32x4, x);
-                    }
-                }
                 // streaming store: the output is not re-read by this kernel and
                 // should not displace the operand slices other tiles share in L2
                 __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dst));
@@ -570,9 +740,6 @@ gemm256_kernel(GemmArgs g) {
                 if (grow < g.M && gcol < g.N) {
                     TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
                     if constexpr (SCALED) x = x * rq[wm + 64 * h + rr] * cn[wn + cc];
-                    if constexpr (sizeof(TO) == 4 && !SCALED) {
-                        if (g.mul_out) x = x * C[grow * g.ldc + gcol];
-                    }
                     C[grow * g.ldc + gcol] = x;
                 }
             }
@@ -650,8 +817,12 @@ sweep256_kernel(GemmArgs g) {
         // than kept live (and spilled) across the whole sweep
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
-        if (ROWN && nt == 0) mma_256<T, false, ROWN, COLN, 4>(g, m0, n0, lds, acc, sqa, sa, sqb, sb, 0, g.K, tid);
-        else mma_256<T, false, false, COLN, 4>(g, m0, n0, lds, acc, false, sa, sqb, sb, 0, g.K, tid);
+        TileLoads<T, false, 4> tl;
+        tl.init(g, m0, n0);
+        if (ROWN && nt == 0)
+            mma_256<T, false, ROWN, COLN, 4>(g, tl, lds, 0, false, 0, acc, sqa, sa, sqb, sb, 0, g.K, tid);
+        else
+            mma_256<T, false, false, COLN, 4>(g, tl, lds, 0, false, 0, acc, false, sa, sqb, sb, 0, g.K, tid);
 
         // cosine factors of the rows (first block) and of this block's columns
         if (nt == 0) {
@@ -789,15 +960,22 @@ sweep256_kernel(GemmArgs g) {
 
 template <typename T, typename TO>
 hipError_t launch_to(bool b_nn, const GemmArgs &a, hipStream_t s) {
+    // Tiles of equal work (all interior, the whole K range): one persistent
+    // work-group per CU (256 CUs, 32 per XCD; the tile count is at least 256,
+    // gemm256_fits).  Otherwise one work-group per tile, so the dispatcher
+    // balances tiles of unequal work (edge tiles, echelon K ranges), which a
+    // fixed stride would let drift apart and lose their shared L2 slices.
     const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
-    const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_kernel<T, TO, true, false>)
-                         : reinterpret_cast<const void *>(gemm256_kernel<T, TO, false, false>);
-    hipError_t e = raise_lds_limit(k, LDS_BYTES);
+    const bool uniform = !a.echelon && a.M % TM == 0 && a.N % TN == 0;
+    const dim3 grid(uniform ? 256u : (unsigned)(8 * ((total + 7) / 8)));
+    const size_t lds = 2 * 2 * OPT * sizeof(uint16_t);      // the two stage slots
+    const void *k = b_nn ? reinterpret_cast<const void *>(gemm256_store_kernel<T, TO, true>)
+                         : reinterpret_cast<const void *>(gemm256_store_kernel<T, TO, false>);
+    hipError_t e = raise_lds_limit(k, lds);
     if (e != hipSuccess) return e;
     const dim3 block(Waves<GEMM_NW>::NTHR);
-    if (b_nn) hipLaunchKernelGGL((gemm256_kernel<T, TO, true, false>), grid, block, LDS_BYTES, s, a);
-    else hipLaunchKernelGGL((gemm256_kernel<T, TO, false, false>), grid, block, LDS_BYTES, s, a);
+    if (b_nn) hipLaunchKernelGGL((gemm256_store_kernel<T, TO, true>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((gemm256_store_kernel<T, TO, false>), grid, block, lds, s, a);
     return hipGetLastError();
 }
 
@@ -972,11 +1150,10 @@ hipError_t launch_scores(const GemmArgs &a, bool softmax, hipStream_t s) {
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
     GemmArgs b = a;
     if (softmax) b.scale = a.scale * a.beta;      // the softmax acts on beta * score
-    const void *k = reinterpret_cast<const void *>(gemm256_kernel<T, float, false, true>);
+    const void *k = reinterpret_cast<const void *>(scores256_kernel<T>);
     hipError_t e = raise_lds_limit(k, SCORES_LDS_BYTES);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm256_kernel<T, float, false, true>), grid, dim3(Waves<GEMM_NW>::NTHR), SCORES_LDS_BYTES, s,
-                       b);
+    hipLaunchKernelGGL((scores256_kernel<T>), grid, dim3(Waves<GEMM_NW>::NTHR), SCORES_LDS_BYTES, s, b);
     return hipGetLastError();
 }
 
