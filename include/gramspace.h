@@ -28,9 +28,10 @@
  * Memory and ownership.  Every matrix argument is a device pointer (HIP
  * device memory of the current device) unless marked HOST.  The caller
  * allocates every buffer, including workspace; the library allocates no
- * device memory, keeps no state besides a thread-local error message, and
- * never frees caller memory.  Inputs are read-only.  Outputs must not overlap
- * inputs or each other (GS_ERR_ARG).
+ * device memory and never frees caller memory.  Besides a thread-local error
+ * message it keeps two process-wide caches: whether a HIP device exists, and
+ * which of its kernels have had their LDS limit raised.  Inputs are
+ * read-only.  Outputs must not overlap inputs or each other (GS_ERR_ARG).
  *
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
  * Every call except gs_compress only enqueues work on that stream and returns

@@ -100,22 +100,6 @@ gs_status check_device() {
     return GS_OK;
 }
 
-// Compute units of the current device (queried once per process).
-int cu_count() {
-    static std::atomic<int> n{0};
-    int v = n.load();
-    if (v == 0) {
-        int dev = 0, cus = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
-            v = cus;
-        else
-            v = 256;
-        n.store(v);
-    }
-    return v;
-}
-
 gs_status launched(hipError_t e, const char *what) {
     if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
     if (getenv("GS_DEBUG")) {

@@ -49,7 +49,6 @@ template <int NW> struct Waves {
 constexpr int NSTAGE = 2;
 constexpr int OPT = TM * 64;        // 16-bit units per staged operand tile (32 KiB)
 constexpr int GROUP_M = 4;          // m-tiles that take each n-tile in turn
-constexpr int EP_STRIDE_MAX = 128 * 4 + 32;   // staged fp32 output row: 128 values + 32-byte pad
 // bytes per staged output row of a wave's sub-tile (WTN values + 8 values of pad)
 template <typename TO, int NW>
 constexpr int ep_stride() { return Waves<NW>::WTN * (int)sizeof(TO) + 16 * (int)sizeof(TO) / 2; }
@@ -1112,7 +1111,7 @@ __global__ void __launch_bounds__(256) few_rows_kernel(GemmArgs g) {
         for (int i = 0; i < NV; ++i) part[w][i] = v[i];
     }
     __syncthreads();
-    if (threadIdx.x < nj) {
+    if ((int)threadIdx.x < nj) {
         const int j = threadIdx.x;
         const float dot = part[0][j] + part[1][j] + part[2][j] + part[3][j];
         float f = g.scale;
