@@ -755,6 +755,39 @@ def test_large_tile_prob2vec(op_dtype):
     assert rowrel(Tr, oracle.prob2vec(P[rows], R)) <= TOL_F32
 
 
+# Products whose tiles all do the same work (M and N multiples of 256, no
+# echelon range) run on a persistent grid that walks several tiles per
+# work-group, loading each next tile's first stage while the previous
+# output drains: 512 tiles here, so every work-group takes two, with a K tail
+# (K = 300) and NaN row padding; project with its row norms, restore, and the
+# fp32 bound product (whose second pass reads the output back).
+
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+def test_persistent_tile_walk(op_dtype):
+    B, K, N = 16384, 300, 2048
+    print("persistent tile walk", _name(op_dtype), B, K, N, flush=True)
+    X, Q = _mat(B, K, 81, op_dtype), _mat(N, K, 82, op_dtype, 1 / np.sqrt(K))
+    ldk = _ld(K, op_dtype)
+    T, xn = gsm.gs_project(nan_padded(X, ldk, op_dtype), nan_padded(Q, ldk, op_dtype), out_dtype=torch.float32,
+                           xnorm2=True)
+    Tc, Qr = _mat(B, K, 83, op_dtype), _mat(K, N, 84, op_dtype)
+    Td, Qd = nan_padded(Tc, ldk, op_dtype), nan_padded(Qr, _ld(N, op_dtype, 8), op_dtype)
+    Xr = gsm.gs_reconstruct(Td, Qd, out_dtype=torch.float32)
+    T2 = _mat(B, K, 85, op_dtype)
+    Y = gsm.gs_reconstruct(Td, Qd, T2=nan_padded(T2, ldk, op_dtype), bind="mul", out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 86)
+    for got in (T, Xr, Y):
+        assert np.isfinite(host(got[rows])).all()
+    assert rowrel(host(T[rows]), oracle.project(X[rows], Q)) <= TOL_F32
+    np.testing.assert_allclose(host(xn), oracle.row_norms(X) ** 2, rtol=1e-4)
+    Xo = oracle.reconstruct(Tc[rows], Qr)
+    assert rowrel(host(Xr[rows]), Xo) <= TOL_F32
+    assert rowrel(host(Y[rows]), oracle.bind(Xo, oracle.reconstruct(T2[rows], Qr))) <= TOL_F32
+    # every tile was written (the outputs start uninitialised)
+    assert torch.isfinite(Xr).all().item() and torch.isfinite(Y).all().item() and torch.isfinite(T).all().item()
+
+
 # ------------- row sweep / scored products (>= 256 row blocks of 256, 256-column blocks)
 #
 # With Q the identity, coordinates and codebook coordinates are themselves the
