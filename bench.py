@@ -17,12 +17,20 @@ Inputs stay resident in HBM.  Steps cycle through several independent copies
 of the batch (inputs and outputs) so that the working set exceeds the 256 MiB
 Infinity Cache: every step reads its inputs from HBM.  The K timed steps are
 captured in one HIP graph and replayed once, bracketed by device
-synchronisation; each kernel launch inside it is bracketed by HIP events on
-the same stream, which give the kernel's mean launch duration for the
-roofline entry.
+synchronisation (the wall clock of `value`) and by HIP events on the replay
+stream, whose interval over K is the mean time per launch (the kernel and the
+dispatch gap between graph nodes) used by the roofline entry.  --streams N
+also times the steps spread over N streams of one graph (extra.concurrent).
 
 The JSON line also carries the oracle's throughput on the host cores for a
 bounded sample of the same workload.
+
+Other workloads (--workload): large, binary and stress time one step of the
+separate calls of those configurations with HIP events per call (the
+products with the codebook coordinates R flag R as lower echelon, as
+gs_compress returns it); dimsweep measures the similarity lookup against the
+vector dimension, dense and Gram-Space; bind times the binding operators on
+restored vectors.
 """
 from __future__ import annotations
 
