@@ -5,7 +5,8 @@ Two layers with the C names:
 * `lib()` returns the loaded shared library; its `gs_*` functions take raw
   pointers exactly as declared in the header.
 * `gs_compress`, `gs_project`, `gs_prob2vec`, `gs_similarity`,
-  `gs_attention`, `gs_reconstruct` below take torch tensors on the current
+  `gs_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
+  below take torch tensors on the current
   GPU, allocate the outputs with torch, and pass pointers, sizes and the
   current stream to the library.  They only marshal arguments: every step of
   the computation runs in the library's HIP kernels.
