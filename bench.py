@@ -277,6 +277,7 @@ def mfma_workload(args, torch, gsm):
     goes into the roofline entry (matrix-core bound)."""
     w = wl.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
+    print("%s: codebook %d x %d, compress" % (w.name, w.Ms[0], w.D), file=sys.stderr, flush=True)
     C = torch.from_numpy(wl.codebook(w)).to(dev)
     bf = w.bf16
     dt = torch.bfloat16 if bf else torch.float32
@@ -325,10 +326,13 @@ def mfma_workload(args, torch, gsm):
                       4.0 * B * r * D))
         calls.append(("reproject", lambda: gsm.gs_project(Y, Q, out=Ty), 2.0 * B * D * r))
     stream = torch.cuda.current_stream()
+    print("%s: inputs ready (rank %d), %d warm-up step(s)" % (w.name, r, max(1, args.warmup)), file=sys.stderr,
+          flush=True)
     for _ in range(max(1, args.warmup)):
         for _, f, _ in calls:
             f()
     torch.cuda.synchronize()
+    print("%s: %d timed step(s)" % (w.name, args.steps), file=sys.stderr, flush=True)
     per = {n: [] for n, _, _ in calls}
     evs = []
     torch.cuda.synchronize()
