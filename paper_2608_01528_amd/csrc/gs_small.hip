@@ -69,12 +69,12 @@ __host__ __device__ __forceinline__ int pad_small(int64_t M) { return M <= 32 ? 
 // element e is matrix element (e / w, e % w).  With contiguous rows
 // (ld == w) and an aligned base, tile and matrix are one linear range moved
 // as 4-element vectors; otherwise element by element with the row and column
-// advanced incrementally.  NT is the number of threads taking part.
+// advanced incrementally.  NT threads take part, thread t of them (by
+// default the work-group's threads).
 
 template <typename T, int NT, int WMAX = MAXK>
 __device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, int64_t b0, int nrow, int w,
-                                          float *tile) {
-    const int t = threadIdx.x;
+                                          float *tile, int t = threadIdx.x) {
     const int n = nrow * w;
     const T *base = g + b0 * ld;
     if (ld == w && aligned16(base)) {
@@ -117,8 +117,7 @@ __device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, i
 
 template <typename T, int NT>
 __device__ __forceinline__ void tile_store(T *__restrict__ g, int64_t ld, int64_t b0, int nrow, int w,
-                                           const float *tile) {
-    const int t = threadIdx.x;
+                                           const float *tile, int t = threadIdx.x) {
     const int n = nrow * w;
     T *base = g + b0 * ld;
     if (ld == w && aligned16(base)) {
@@ -412,25 +411,24 @@ typedef float gs16v __attribute__((ext_vector_type(16)));
 // waited for alone.
 template <typename TI> struct TileReq;
 template <> struct TileReq<float> {
-    static constexpr int V = SBLK * MAXK / 4 / SROWS;   // 16-byte pieces per thread
+    static constexpr int V = 64 * MAXK / 4 / 64;   // 16-byte pieces per lane of a wave's 64 rows
     f4v v[V];
-    __device__ __forceinline__ void issue(const float *base, int n) {
+    __device__ __forceinline__ void issue(const float *base, int n, int lane) {
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, n * 4, 0x00020000);
 #pragma unroll
         for (int i = 0; i < V; ++i)
-            v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(
-                                                rs, (int)(threadIdx.x + i * SROWS) * 16, 0, 0));
+            v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rs, (lane + i * 64) * 16, 0, 0));
     }
 };
 template <> struct TileReq<bf16_t> {
-    static constexpr int V = SBLK * MAXK / 4 / SROWS;   // 4-element pieces per thread
+    static constexpr int V = 64 * MAXK / 4 / 64;   // 4-element pieces per lane
     f4v v[V];
-    __device__ __forceinline__ void issue(const bf16_t *base, int n) {
+    __device__ __forceinline__ void issue(const bf16_t *base, int n, int lane) {
         const int n4 = n >> 2;
 #pragma unroll
         for (int i = 0; i < V; ++i) {
-            const int e4 = threadIdx.x + i * SROWS;
+            const int e4 = lane + i * 64;
             if (e4 < n4) v[i] = ld4(base + 4 * e4);
         }
     }
@@ -472,13 +470,27 @@ __device__ __forceinline__ void gram_stage(const float (&rk)[(M + 1) / 2], float
     }
 }
 
-// One row block of one group, for a codebook of exactly M entries.
+// LDS accesses of one wave complete in order: fences that keep the compiler
+// from moving this wave's LDS reads and writes across each other.
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// One row block of one group, for a codebook of exactly M entries.  Each
+// wave loads, scores and stores its own 64 rows (rows 64 w .. 64 w + 63 of
+// the block, their own part of the tile), so after the one work-group
+// barrier that publishes the Gram matrix the waves go on independently: one
+// wave's arithmetic overlaps another's loads and stores.
 template <typename TI, int M>
 __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float scale, float beta, int64_t b0,
                                           int nrow, float *tile, float *Gs, float *Rn) {
     constexpr int GS = (M + 3) & ~3;   // row stride of G in LDS (16-byte rows)
     constexpr int KG = (M + 1) / 2;    // steps of the Gram product
     const int t = threadIdx.x;
+    const int lane = t & 63, wrow0 = t & ~63;
+    const int nroww = (nrow - wrow0 < 0) ? 0 : (nrow - wrow0 < 64) ? nrow - wrow0 : 64;   // this wave's rows
+    float *wtile = tile + wrow0 * M;
     const int r = (int)G.r;
 
     // 1. wave 0: the codebook rows in the Gram product's operand layout and
@@ -496,29 +508,33 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
         if (cosine && G.cnorm && t < M) cn = G.cnorm[t];
     }
 
-    // 2. the probability tile
-    const TI *base = static_cast<const TI *>(G.P) + b0 * G.ldp;
-    const bool contig = G.ldp == M && aligned16(base);
-    const int n = nrow * M, n4 = n >> 2;
+    // 2. this wave's probability rows (contiguous rows: one linear range; the
+    // wave's start stays 16-byte aligned when the block's does)
+    const TI *bbase = static_cast<const TI *>(G.P) + b0 * G.ldp;
+    const bool contig = G.ldp == M && aligned16(bbase);
+    const TI *base = bbase + (int64_t)wrow0 * M;
+    const int n = nroww * M, n4 = n >> 2;
     TileReq<TI> req;
-    req.issue(base, contig ? n : 0);   // an empty range issues nothing useful
+    req.issue(base, contig ? n : 0, lane);   // an empty range issues nothing useful
 
-    // 3. Gram matrix and factors while the tile is in flight
+    // 3. Gram matrix and factors while the tiles are in flight, published to
+    // every wave
     if (t < 64) gram_stage<M, GS>(rk, Gs, Rn, cosine, G.cnorm != nullptr, cn);
+    lds_barrier();
 
-    // 4. tile to LDS
+    // 4. this wave's rows to its part of the tile
     if (contig) {
 #pragma unroll
         for (int i = 0; i < TileReq<TI>::V; ++i) {
-            const int e4 = t + i * SROWS;
-            if (e4 < n4) st4(tile + 4 * e4, req.v[i]);
+            const int e4 = lane + i * 64;
+            if (e4 < n4) st4(wtile + 4 * e4, req.v[i]);
         }
-        const int e = 4 * n4 + t;
-        if (e < n) tile[e] = ld_f32<TI>(base, e);
+        const int e = 4 * n4 + lane;
+        if (e < n) wtile[e] = ld_f32<TI>(base, e);
     } else {
-        tile_load<TI, SROWS>(static_cast<const TI *>(G.P), G.ldp, b0, nrow, M, tile);
+        tile_load<TI, 64>(static_cast<const TI *>(G.P), G.ldp, b0 + wrow0, nroww, M, wtile, lane);
     }
-    lds_barrier();
+    wave_lds_fence();
 
     // 5. scores of the thread's row, in registers
     float *srow = tile + t * M;
@@ -566,10 +582,8 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
                 for (int g = 0; g < 16; ++g) drow[(8 * (g >> 2) + (g & 3)) * M] = acc[g];
             }
         }
-        // LDS operations of one wave complete in order: the row written by
-        // the other lanes is read back after these fences
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+        // the row written by the other lanes is read back after these fences
+        wave_lds_fence();
 #pragma unroll
         for (int j = 0; j < M; ++j) d[j] = srow[j];
     } else {
@@ -603,12 +617,13 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     }
     if (G.argmax && t < nrow) __builtin_nontemporal_store(bi, G.argmax + b0 + t);
 
-    // 6. outputs through the tile (each thread overwrites only its own row)
+    // 6. outputs through the wave's part of the tile (each thread overwrites
+    // only its own row)
     if (G.S) {
 #pragma unroll
         for (int j = 0; j < M; ++j) srow[j] = d[j];
-        lds_barrier();
-        tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
+        wave_lds_fence();
+        tile_store<float, 64>(G.S, G.lds, b0 + wrow0, nroww, M, wtile, lane);
     }
     if (G.A) {
         // softmax of beta times the scores in base 2: exp(beta s) =
@@ -623,11 +638,11 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
             z += d[j];
         }
         const float iz = 1.f / z;
-        if (G.S) lds_barrier();   // S has left the tile before it is overwritten
+        if (G.S) wave_lds_fence();   // S has left the tile before it is overwritten
 #pragma unroll
         for (int j = 0; j < M; ++j) srow[j] = d[j] * iz;
-        lds_barrier();
-        tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
+        wave_lds_fence();
+        tile_store<float, 64>(G.A, G.lda, b0 + wrow0, nroww, M, wtile, lane);
     }
 }
 
