@@ -1,14 +1,15 @@
-// Large-tile bf16 contraction for the long products of the Gram-Space path at
-// batch sizes that fill the chip: project T = X Q^T (B stored N x K),
-// reconstruct X = T Q and prob2vec T = P R (B stored K x N).
+// Large-tile bf16 and fp32 contractions for the long products of the
+// Gram-Space path at batch sizes that fill the chip: project T = X Q^T (B
+// stored N x K), reconstruct X = T Q and prob2vec T = P R (B stored K x N),
+// the bound product, and the similarity scores (with the row argmax or
+// softmax folded in when a tile holds whole rows).
 //
-// Work-group tile 256 x 256, K-step 64, 256 threads = 4 waves in a 2 x 2
-// arrangement; each wave owns a 128 x 128 sub-tile as 4 x 4 blocks of the
-// 32x32x16 bf16 MFMA, whose 256 accumulators sit in the accumulation
-// registers (one wave per SIMD).  Per flop this moves half the bytes of a
-// 128 x 128 tile through L2 and LDS, and each wave issues 16 MFMAs per 8
-// fragment reads.  A K-step of 64 bf16 makes every row slice a whole
-// 128-byte line, so L2 serves the operands in full-line requests.
+// Work-group tile 256 x 256, 512 threads = 8 waves in a 2 x 4 arrangement;
+// each wave owns a 128 x 64 sub-tile as 4 x 2 blocks of the 32 x 32 MFMA
+// (32x32x16 bf16 or 32x32x2 fp32), 128 accumulators, two waves per SIMD so
+// that one wave's waits overlap the other's matrix work.  A K-step of 64
+// bf16 or 32 fp32 makes every row slice a whole 128-byte line, so L2 serves
+// the operands in full-line requests.
 //
 // Operand tiles come into LDS by asynchronous buffer->LDS loads
 // (buffer_load_dwordx4 ... lds) into two stages of 64 KiB, ordered by
@@ -17,16 +18,18 @@
 // reads, so 32-bit offsets reach it and the hardware range check backs up
 // the index clamping.  Each load instruction fills 1 KiB of LDS in lane
 // order, so the layout is chosen through the 16-byte chunk each lane fetches:
-//   row tile   [256][64]: chunk c of row r sits at position c ^ ((r >> 1) & 7)
-//   k-row tile [64][256]: chunk c of k-row k sits at position c ^ (4 (k & 3))
+//   row tile   (256 rows x 128 bytes): chunk c of row r at c ^ ((r >> 1) & 7)
+//   k-row tile bf16 (64 x 256): chunk c of k-row k at c ^ (4 (k & 3))
+//   k-row tile fp32 (32 x 256): chunk c of k-row k at c ^ (8 ((k >> 4) & 1))
 // A 128-byte row covers half of the 64 banks, so the 16 rows of one read
 // phase of ds_read_b128 reach all 16 bank groups only if the swizzle changes
 // with r >> 1.  A transpose read (ds_read_b64_tr_b16) takes 4 chunks from each
 // of 4 consecutive k-rows per 32 lanes, which the k-row swizzle spreads over
 // all 64 banks.  Rows beyond the matrix reuse its last row (their results are
 // discarded); fragment elements at k >= K are zeroed in registers in the last
-// K-step.  Operands must have 16-byte aligned rows (ld a multiple of 8): rows
-// are read in 16-byte units up to column ceil(cols / 8) * 8 <= ld.
+// K-step.  Operands must have 16-byte aligned rows (ld a multiple of 8 bf16
+// or 4 fp32): rows are read in 16-byte units up to the end of the row's last
+// 16-byte chunk, which lies within ld.
 #include "gs_internal.h"
 
 namespace gs {
@@ -618,11 +621,20 @@ gemm256_store_kernel(GemmArgs g) {
     }
 }
 
+// a, b: (value, index) pairs; the larger value wins, the lower index on ties
+__device__ __forceinline__ void fold_max(float &v, int &i, float v2, int i2) {
+    if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
+}
+
+// Row results folded into the scores epilogue when a tile holds whole rows.
+constexpr int FUSE_NONE = 0, FUSE_ARGMAX = 1, FUSE_SOFTMAX = 2;
+
 // Similarity scores on 256 x 256 tiles (fp32 output, B = R stored N x K):
 // out = scale * acc / (||x_row|| ||c_col||) for cosine (row norms from qnorm2
 // or from the A fragments, column norms from cnorm or from the B fragments),
-// scale * acc for dot; one tile per work-group.
-template <typename T>
+// scale * acc for dot; one tile per work-group.  FUSE (only with N <= 256)
+// also writes the row argmax, or replaces the scores by the row softmax.
+template <typename T, int FUSE>
 __global__ void __launch_bounds__(Waves<GEMM_NW>::NTHR) __attribute__((amdgpu_waves_per_eu(GEMM_NW / 4, GEMM_NW / 4)))
 scores256_kernel(GemmArgs g) {
     typedef Waves<GEMM_NW> W;
@@ -691,10 +703,16 @@ scores256_kernel(GemmArgs g) {
         }
     }
 
-    // Epilogue: each wave stages its 128 x 128 sub-tile through its own LDS
+    // Epilogue: each wave stages its 128 x 64 sub-tile through its own LDS
     // region in two halves of 64 rows (rows padded so the column-wise writes
     // of the accumulator layout do not collide on banks), then writes whole
-    // 16-byte row chunks with streaming stores.
+    // 16-byte row chunks with streaming stores.  With FUSE the tile holds
+    // whole rows (N <= 256): lane l of each wave first scales row l of its
+    // region in place and folds it into a partial (maximum, lowest index of
+    // the maximum) or (maximum, sum of exponentials) for its 64 columns; the
+    // four waves that share the rows combine their partials through LDS in a
+    // fixed order, so the argmax is written here and the weights leave
+    // normalised, with no second pass over the stored matrix.
     __syncthreads();                      // every wave is done with the operand stages
     TO *C = static_cast<TO *>(g.C);
     constexpr int EPC = 16 / (int)sizeof(TO);                 // elements per 16-byte chunk
@@ -704,6 +722,11 @@ scores256_kernel(GemmArgs g) {
     // whole tile inside the output, rows 16-byte aligned: plain 16-byte stores
     const bool interior = ((reinterpret_cast<uintptr_t>(C) & 15) == 0) && (g.ldc % EPC == 0) &&
                           m0 + TM <= g.M && n0 + TN <= g.N;
+    float *pm = cn + TN;                  // FUSE: [column quarter][row] partial maxima
+    float *px = pm + (TN / WTN) * TM;     // FUSE: partial indices (int) or sums of exponentials
+    const int cq = wn / WTN;              // this wave's column quarter
+    const int64_t nv = g.N - n0 - wn;     // this wave's columns inside the output
+    const int ncol = nv < 0 ? 0 : (nv < WTN ? (int)nv : WTN);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
 #pragma unroll
@@ -716,15 +739,74 @@ scores256_kernel(GemmArgs g) {
                     *reinterpret_cast<TO *>(region + row * STRIDE + col * (int)sizeof(TO)) =
                         to_out<TO>(acc[2 * h + ii][j][r]);
                 }
+        if constexpr (FUSE != FUSE_NONE) {
+            const int trow = wm + 64 * h + l;                 // tile row folded by this lane
+            float *mrow = reinterpret_cast<float *>(region + l * STRIDE);
+            const float rql = rq[trow];
+            float m = -INFINITY;
+            int mi = 0;
+#pragma unroll 4
+            for (int q = 0; q < CPR; ++q) {
+                const int qq = (q + l) & (CPR - 1);           // rotated: lanes spread over the banks
+                f4v v = *reinterpret_cast<const f4v *>(mrow + 4 * qq);
+                v = v * rql * *reinterpret_cast<const f4v *>(cn + wn + 4 * qq);
+                *reinterpret_cast<f4v *>(mrow + 4 * qq) = v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int c = 4 * qq + e;
+                    if (c < ncol) {
+                        if constexpr (FUSE == FUSE_ARGMAX) fold_max(m, mi, v[e], wn + c);
+                        else m = fmaxf(m, v[e]);
+                    }
+                }
+            }
+            pm[cq * TM + trow] = m;
+            if constexpr (FUSE == FUSE_ARGMAX) reinterpret_cast<int *>(px)[cq * TM + trow] = mi;
+            __syncthreads();
+            float rm = pm[trow];
+            int ri = 0;
+            if constexpr (FUSE == FUSE_ARGMAX) {
+                ri = reinterpret_cast<const int *>(px)[trow];
+#pragma unroll
+                for (int c = 1; c < TN / WTN; ++c)
+                    fold_max(rm, ri, pm[c * TM + trow], reinterpret_cast<const int *>(px)[c * TM + trow]);
+                if (cq == 0 && m0 + trow < g.M) g.argmax[m0 + trow] = ri;
+            } else {
+#pragma unroll
+                for (int c = 1; c < TN / WTN; ++c) rm = fmaxf(rm, pm[c * TM + trow]);
+                float z = 0.f;
+#pragma unroll 4
+                for (int q = 0; q < CPR; ++q) {
+                    const int qq = (q + l) & (CPR - 1);
+                    f4v v = *reinterpret_cast<const f4v *>(mrow + 4 * qq);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[e] = __expf(v[e] - rm);
+                        if (4 * qq + e < ncol) z += v[e];
+                    }
+                    *reinterpret_cast<f4v *>(mrow + 4 * qq) = v;
+                }
+                px[cq * TM + trow] = z;
+                __syncthreads();
+                float rz = px[trow];
+#pragma unroll
+                for (int c = 1; c < TN / WTN; ++c) rz += px[c * TM + trow];
+                // the partial maxima of these rows have all been read: the
+                // slot of this wave's own rows now holds their factor
+                pm[cq * TM + trow] = 1.f / rz;
+            }
+        }
         if (interior) {
 #pragma unroll 4
             for (int id = l; id < 64 * CPR; id += 64) {
                 const int rr = id / CPR, cc = id % CPR;
                 u32x4 v = *reinterpret_cast<const u32x4 *>(region + rr * STRIDE + cc * 16);
-                if (SCALED) {
+                if constexpr (FUSE == FUSE_NONE) {
                     const f4v x = __builtin_bit_cast(f4v, v) * rq[wm + 64 * h + rr] *
                                   *reinterpret_cast<const f4v *>(cn + wn + cc * EPC);
                     v = __builtin_bit_cast(u32x4, x);
+                } else if constexpr (FUSE == FUSE_SOFTMAX) {
+                    v = __builtin_bit_cast(u32x4, __builtin_bit_cast(f4v, v) * pm[cq * TM + wm + 64 * h + rr]);
                 }
                 TO *dst = C + (m0 + wm + 64 * h + rr) * g.ldc + (n0 + wn + cc * EPC);
                 // streaming store: the output is not re-read by this kernel and
@@ -738,7 +820,8 @@ scores256_kernel(GemmArgs g) {
                 const int64_t grow = m0 + wm + 64 * h + rr, gcol = n0 + wn + cc;
                 if (grow < g.M && gcol < g.N) {
                     TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
-                    if constexpr (SCALED) x = x * rq[wm + 64 * h + rr] * cn[wn + cc];
+                    if constexpr (FUSE == FUSE_NONE) x = x * rq[wm + 64 * h + rr] * cn[wn + cc];
+                    else if constexpr (FUSE == FUSE_SOFTMAX) x = x * pm[cq * TM + wm + 64 * h + rr];
                     C[grow * g.ldc + gcol] = x;
                 }
             }
@@ -758,10 +841,6 @@ scores256_kernel(GemmArgs g) {
 // softmax.  Softmax rows are finished by a second pass over the row block's
 // stored scores.
 
-// a, b: (value, index) pairs; the larger value wins, the lower index on ties
-__device__ __forceinline__ void fold_max(float &v, int &i, float v2, int i2) {
-    if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
-}
 // (max, sum of exp(x - max)) pairs
 __device__ __forceinline__ void fold_sum(float &m, float &z, float m2, float z2) {
     const float mx = fmaxf(m, m2);
@@ -979,6 +1058,8 @@ hipError_t launch_to(bool b_nn, const GemmArgs &a, hipStream_t s) {
 }
 
 constexpr size_t SCORES_LDS_BYTES = LDS_BYTES + 2 * TM * sizeof(float);   // + row and column factors
+// + partial row results of the four column quarters (FUSE)
+constexpr size_t SCORES_FUSED_LDS_BYTES = SCORES_LDS_BYTES + 2 * (TN / Waves<GEMM_NW>::WTN) * TM * sizeof(float);
 
 // One wave per row: the maximum of the row and its lowest column index.
 __global__ void __launch_bounds__(256) rows_argmax_kernel(const float *S, int64_t lds, int64_t B, int64_t M,
@@ -1143,25 +1224,36 @@ hipError_t launch_sweep_norms(const GemmArgs &a, hipStream_t s) {
     return coln ? launch_sweep<T, SOFTMAX, false, true>(a, s) : launch_sweep<T, SOFTMAX, false, false>(a, s);
 }
 
-template <typename T>
-hipError_t launch_scores(const GemmArgs &a, bool softmax, hipStream_t s) {
-    const int64_t total = ((a.M + TM - 1) / TM) * ((a.N + TN - 1) / TN);
+template <typename T, int FUSE>
+hipError_t launch_scores_fuse(const GemmArgs &b, hipStream_t s) {
+    const int64_t total = ((b.M + TM - 1) / TM) * ((b.N + TN - 1) / TN);
     const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
+    const size_t lds = FUSE == FUSE_NONE ? SCORES_LDS_BYTES : SCORES_FUSED_LDS_BYTES;
+    const void *k = reinterpret_cast<const void *>(scores256_kernel<T, FUSE>);
+    hipError_t e = raise_lds_limit(k, lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((scores256_kernel<T, FUSE>), grid, dim3(Waves<GEMM_NW>::NTHR), lds, s, b);
+    return hipGetLastError();
+}
+
+// `fused`: the row pass was folded into the epilogue (whole rows per tile).
+template <typename T>
+hipError_t launch_scores(const GemmArgs &a, bool softmax, bool &fused, hipStream_t s) {
     GemmArgs b = a;
     if (softmax) b.scale = a.scale * a.beta;      // the softmax acts on beta * score
-    const void *k = reinterpret_cast<const void *>(scores256_kernel<T>);
-    hipError_t e = raise_lds_limit(k, SCORES_LDS_BYTES);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((scores256_kernel<T>), grid, dim3(Waves<GEMM_NW>::NTHR), SCORES_LDS_BYTES, s, b);
-    return hipGetLastError();
+    fused = a.N <= TN && (softmax || a.argmax);
+    if (!fused) return launch_scores_fuse<T, FUSE_NONE>(b, s);
+    return softmax ? launch_scores_fuse<T, FUSE_SOFTMAX>(b, s) : launch_scores_fuse<T, FUSE_ARGMAX>(b, s);
 }
 
 }  // namespace
 
 hipError_t launch_scores256(gs_dtype t, const GemmArgs &a, bool softmax, hipStream_t s) {
     if (a.M == 0 || a.N == 0) return hipSuccess;
-    hipError_t e = (t == GS_BF16) ? launch_scores<bf16_t>(a, softmax, s) : launch_scores<float>(a, softmax, s);
-    if (e != hipSuccess) return e;
+    bool fused = false;
+    hipError_t e = (t == GS_BF16) ? launch_scores<bf16_t>(a, softmax, fused, s)
+                                  : launch_scores<float>(a, softmax, fused, s);
+    if (e != hipSuccess || fused) return e;
     return launch_rows_pass(softmax, static_cast<float *>(a.C), a.ldc, a.M, a.N, softmax ? nullptr : a.argmax, s);
 }
 

@@ -866,6 +866,71 @@ def test_sweep_cosine_argmax_only(sweep_case):
     check_argmax(host(idx[rows]), So, band_rel=1e-4)
 
 
+# ---------- whole rows in one 256-column tile: row argmax / softmax in the epilogue
+#
+# With a codebook of at most 256 entries every tile of the scored product
+# holds whole rows, so the argmax and the softmax are taken in the product's
+# epilogue from the four column quarters of the tile.  M = 200 leaves one
+# quarter partly and one wholly outside the codebook; M = 256 fills the tile.
+
+ROWS_B, ROWS_R = 65573, 300
+
+
+@pytest.fixture(scope="module", params=[(dt, m) for dt in OP_DTYPES for m in (200, 256)],
+                ids=lambda p: "%s-M%d" % (_name(p[0]), p[1]))
+def rows_case(request):
+    dt, M = request.param
+    T = _mat(ROWS_B, ROWS_R, 31, dt)
+    R = _mat(M, ROWS_R, 32 + M, dt)
+    ld = _ld(ROWS_R, dt)
+    Td, Rd = nan_padded(T, ld, dt), nan_padded(R, ld, dt)
+    rows = _tile_rows(ROWS_B, 33)
+    return T, R, Td, Rd, rows
+
+
+@pytest.mark.parametrize("norms", ["computed", "given"])
+def test_whole_row_similarity_cosine(rows_case, norms):
+    T, R, Td, Rd, rows = rows_case
+    print("whole-row similarity cosine", Td.dtype, R.shape[0], norms, flush=True)
+    qn = cn = None
+    if norms == "given":
+        qn = dev(oracle.row_norms(T) ** 2)
+        cn = dev(oracle.row_norms(R))
+    S, idx = gsm.gs_similarity(Td, Rd, qnorm2=qn, cnorm=cn, mode="cosine")
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.COSINE)
+    Sg = host(S[rows])
+    assert np.isfinite(Sg).all()
+    assert rowrel(Sg, So) <= TOL_F32
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    # every row: the index is the first maximum of the stored scores
+    assert torch.equal(idx.long(), torch.argmax(S, dim=1))
+
+
+def test_whole_row_similarity_dot(rows_case):
+    T, R, Td, Rd, rows = rows_case
+    print("whole-row similarity dot", Td.dtype, R.shape[0], flush=True)
+    S, idx = gsm.gs_similarity(Td, Rd, mode="dot", scale=0.25)
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.DOT, 0.25)
+    assert rowrel(host(S[rows]), So) <= TOL_F32
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    assert torch.equal(idx.long(), torch.argmax(S, dim=1))
+
+
+@pytest.mark.parametrize("beta", [8.0, -3.0])
+def test_whole_row_attention(rows_case, beta):
+    T, R, Td, Rd, rows = rows_case
+    print("whole-row attention", Td.dtype, R.shape[0], beta, flush=True)
+    A, _ = gsm.gs_attention(Td, Rd, mode="cosine", beta=beta)
+    torch.cuda.synchronize()
+    Ao = oracle.softmax(oracle.similarity(T[rows], R, oracle.COSINE), beta)
+    Ag = host(A[rows])
+    assert np.isfinite(Ag).all()
+    assert rowrel(Ag, Ao) <= TOL_F32
+    assert torch.allclose(A.sum(dim=1), torch.ones(A.shape[0], device=A.device), atol=1e-4)
+
+
 # ------------------------------------- lower-echelon R (GS_ECHELON) on the large tiles
 #
 # R from compress is lower echelon, R[j, k] == 0 for k > j; with the flag the
