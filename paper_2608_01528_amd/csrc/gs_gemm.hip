@@ -1050,7 +1050,10 @@ hipError_t launch_gemm(gs_dtype ta, gs_dtype tb, gs_dtype tout, bool b_nn, Epi e
     // a few query rows: the K range is split over whole work-groups instead
     // of walked by one tile
     if (!b_nn && (sm || a.write_out) && a.M <= FEW_ROWS && ta == tb) return launch_few_rows(ta, a, sm, s);
-    if (rows_ok && !b_nn && (sm || a.write_out) && gemm256_fits(ta, a, false)) return launch_scores256(ta, a, sm, s);
+    // scores written, or whole rows in one tile (the row results come from
+    // the product's epilogue): the large tiles
+    if (rows_ok && !b_nn && (sm || a.write_out || a.N <= 256) && gemm256_fits(ta, a, false))
+        return launch_scores256(ta, a, sm, s);
     if (rows_ok && !b_nn && sweep256_fits(ta, a)) return launch_sweep256(ta, sm, a, s);
     // scores or weights written anyway: product with a scaled epilogue, then
     // the row pass; argmax alone: the row sweep (no score matrix in memory)

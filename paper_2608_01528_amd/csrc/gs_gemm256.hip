@@ -771,6 +771,7 @@ scores256_kernel(GemmArgs g) {
                 for (int c = 1; c < TN / WTN; ++c)
                     fold_max(rm, ri, pm[c * TM + trow], reinterpret_cast<const int *>(px)[c * TM + trow]);
                 if (cq == 0 && m0 + trow < g.M) g.argmax[m0 + trow] = ri;
+                if (!g.write_out) continue;                   // argmax only: no scores leave
             } else {
 #pragma unroll
                 for (int c = 1; c < TN / WTN; ++c) rm = fmaxf(rm, pm[c * TM + trow]);

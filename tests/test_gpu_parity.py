@@ -918,6 +918,20 @@ def test_whole_row_similarity_dot(rows_case):
     assert torch.equal(idx.long(), torch.argmax(S, dim=1))
 
 
+@pytest.mark.parametrize("mode", ["cosine", "dot"])
+def test_whole_row_argmax_only(rows_case, mode):
+    # no scores requested: the argmax comes from the epilogue and nothing else
+    # is written
+    T, R, Td, Rd, rows = rows_case
+    print("whole-row argmax only", Td.dtype, R.shape[0], mode, flush=True)
+    _, idx = gsm.gs_similarity(Td, Rd, mode=mode, scale=0.5, scores=False)
+    torch.cuda.synchronize()
+    So = oracle.similarity(T[rows], R, oracle.COSINE if mode == "cosine" else oracle.DOT, 0.5)
+    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    S, idx2 = gsm.gs_similarity(Td, Rd, mode=mode, scale=0.5)
+    assert torch.equal(idx, idx2)
+
+
 @pytest.mark.parametrize("beta", [8.0, -3.0])
 def test_whole_row_attention(rows_case, beta):
     T, R, Td, Rd, rows = rows_case
