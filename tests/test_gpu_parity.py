@@ -936,13 +936,15 @@ def test_whole_row_argmax_only(rows_case, mode):
 def test_whole_row_attention(rows_case, beta):
     T, R, Td, Rd, rows = rows_case
     print("whole-row attention", Td.dtype, R.shape[0], beta, flush=True)
-    A, _ = gsm.gs_attention(Td, Rd, mode="cosine", beta=beta)
+    A, O = gsm.gs_attention(Td, Rd, mode="cosine", beta=beta, weighted_sum=True, out_dtype=torch.float32)
     torch.cuda.synchronize()
     Ao = oracle.softmax(oracle.similarity(T[rows], R, oracle.COSINE), beta)
     Ag = host(A[rows])
     assert np.isfinite(Ag).all()
     assert rowrel(Ag, Ao) <= TOL_F32
     assert torch.allclose(A.sum(dim=1), torch.ones(A.shape[0], device=A.device), atol=1e-4)
+    # the weighted sum reads the normalised weights back
+    assert rowrel(host(O[rows]), oracle.prob2vec(Ao, R)) <= TOL_F32
 
 
 # ------------------------------------- lower-echelon R (GS_ECHELON) on the large tiles
