@@ -788,6 +788,24 @@ def test_persistent_tile_walk(op_dtype):
     assert torch.isfinite(Xr).all().item() and torch.isfinite(Y).all().item() and torch.isfinite(T).all().item()
 
 
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+def test_large_tiles_ragged_columns(op_dtype):
+    # whole row blocks with a ragged last column tile (N = 1000 = 3 x 256 +
+    # 232; 128 x 4 = 512 tiles, one work-group each), both output types
+    B, K, N = 32768, 300, 1000
+    print("large tiles, ragged columns", _name(op_dtype), B, K, N, flush=True)
+    X, Q = _mat(B, K, 87, op_dtype), _mat(N, K, 88, op_dtype, 1 / np.sqrt(K))
+    ldk = _ld(K, op_dtype)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        T = gsm.gs_project(nan_padded(X, ldk, op_dtype), nan_padded(Q, ldk, op_dtype), out_dtype=out_dtype)
+        torch.cuda.synchronize()
+        rows = _tile_rows(B, 89)
+        Tg = host(T[rows])
+        assert np.isfinite(Tg).all() and torch.isfinite(T.float()).all().item()
+        tol = TOL_F32 if out_dtype == torch.float32 else TOL_BF16
+        assert rowrel(Tg, oracle.project(X[rows], Q)) <= tol
+
+
 # ------------- row sweep / scored products (>= 256 row blocks of 256, 256-column blocks)
 #
 # With Q the identity, coordinates and codebook coordinates are themselves the
