@@ -153,15 +153,6 @@ struct LdsRows {
     }
 };
 
-// Widen the codebook into the padded LDS block.
-template <typename T, int MB, int NT>
-__device__ __forceinline__ void stage_padded(const T *R, int64_t ldr, int M, int r, float *Rs) {
-    for (int e = threadIdx.x; e < MB * MB; e += NT) {
-        const int j = e / MB, k = e - (e / MB) * MB;
-        Rs[e] = (j < M && k < r) ? ld_f32<T>(R, (int64_t)j * ldr + k) : 0.f;
-    }
-}
-
 // Reciprocal codebook norms for cosine scores (ones for dot), zeros beyond M.
 // Without given norms they are ||R_j||, summed in fp32 from the source rows.
 template <typename T, int NT>
@@ -304,20 +295,56 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
     tile_store<TO, NR>(static_cast<TO *>(a.O), a.ldo, b0, nrow, r, tile);
 }
 
+// The codebook block and the given norms are requested first, then the row
+// tile, so their global round trips overlap (the loads are all in flight
+// before the first wait); missing norms are then summed from the block in LDS.
 template <typename TI, typename TO, int MODE, int MB>
 __global__ void __launch_bounds__(rows_of<MB>()) small_kernel(SmallArgs a) {
     constexpr int NR = rows_of<MB>();
+    constexpr int RE = (MB * MB + NR - 1) / NR;   // codebook block elements per thread
     __shared__ __attribute__((aligned(16))) float tile[NR * MB];
     __shared__ __attribute__((aligned(16))) float Rs[MB * MB];
     __shared__ float Rn[MB];
+    const int t = threadIdx.x;
     const int64_t b0 = (int64_t)blockIdx.x * NR;
     const int M = (int)a.M, r = (int)a.r;
     const int nrow = (int)((a.B - b0 < NR) ? (a.B - b0) : NR);
     const TI *R = static_cast<const TI *>(a.R);
+    const bool cosine = a.cosine != 0;
+    float rv[RE];
+#pragma unroll
+    for (int i = 0; i < RE; ++i) {
+        const int e = t + i * NR, j = e / MB, k = e - (e / MB) * MB;
+        rv[i] = (e < MB * MB && j < M && k < r) ? ld_f32<TI>(R, (int64_t)j * a.ldr + k) : 0.f;
+    }
+    float cn = 0.f;
+    if (MODE != MODE_P2V && cosine && a.cnorm && t < M) cn = a.cnorm[t];
     tile_load<TI, NR, MB>(static_cast<const TI *>(a.In), a.ldin, b0, nrow, (MODE == MODE_P2V) ? M : r, tile);
-    if (MODE != MODE_P2V) stage_norms<TI, NR>(R, a.ldr, M, r, a.cnorm, a.cosine != 0, MB, Rn);
-    stage_padded<TI, MB, NR>(R, a.ldr, M, r, Rs);
+#pragma unroll
+    for (int i = 0; i < RE; ++i)
+        if (t + i * NR < MB * MB) Rs[t + i * NR] = rv[i];
     lds_barrier();
+    if (MODE != MODE_P2V) {
+        // reciprocal codebook norms for cosine scores (ones for dot), zeros
+        // beyond M; without given norms ||R_j||, summed in fp32 over k < r
+        if (t < MB) {
+            float c = 0.f;
+            if (t < M) {
+                c = 1.f;
+                if (cosine) {
+                    float n = cn;
+                    if (!a.cnorm) {
+                        float s2 = 0.f;
+                        for (int k = 0; k < r; ++k) s2 += Rs[t * MB + k] * Rs[t * MB + k];
+                        n = sqrtf(s2);
+                    }
+                    c = (n > 0.f) ? 1.f / n : 0.f;
+                }
+            }
+            Rn[t] = c;
+        }
+        lds_barrier();
+    }
     small_body<TI, TO, MODE, MB>(a, LdsRows<MB>{Rs}, Rn, tile);
 }
 
