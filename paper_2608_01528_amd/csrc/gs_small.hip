@@ -31,6 +31,7 @@ constexpr int MAXK = SOFT_MAX_M;          // widest row of the fused soft select
 enum Mode { MODE_P2V = 0, MODE_SIM = 1, MODE_ATT = 2 };
 
 typedef float f4v __attribute__((ext_vector_type(4)));
+typedef float gs16v __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -245,6 +246,42 @@ __device__ __forceinline__ void tile_to_regs(const float *tile, int w, float v[M
 
 // ------------------------------------------------------- separate calls
 
+// Matrix-core product of the wave's 64 tile rows (two blocks of 32, rows
+// 64 (t / 64) + 32 b + i, row stride W) with a K x 32 operand:
+// acc[b][g] = sum_k A[32 b + i][k] B[k][l % 32] for row i = 8 (g / 4) +
+// 4 (l / 32) + g % 4 (v_mfma_f32_32x32x2f32).  Step kk pairs k = kk (lanes
+// 0..31) and k = kk + KH (lanes 32..63); bk[kk] is this lane's B[k][l % 32]
+// (zero for k >= K), and A elements at k >= K are zeroed.  Rows past the
+// tile's valid rows give results that are never stored.
+template <int KH>
+__device__ __forceinline__ void wave_rows_mm(const float *tile, int W, int K, const float (&bk)[KH],
+                                             gs16v acc[2]) {
+    const int t = threadIdx.x, l = t & 63, c = l & 31, h = l >> 5;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const float *arow = tile + ((t & ~63) + 32 * b + c) * W;
+        acc[b] = gs16v{};
+#pragma unroll
+        for (int kk = 0; kk < KH; ++kk) {
+            const int k = kk + KH * h;
+            const float x = (k < K) ? arow[k] : 0.f;
+            acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(x, bk[kk], acc[b], 0, 0, 0);
+        }
+    }
+}
+
+// The results of wave_rows_mm to the tile at row stride W, columns < ncol.
+__device__ __forceinline__ void wave_rows_out(const gs16v acc[2], int W, int ncol, float *tile) {
+    const int t = threadIdx.x, l = t & 63, c = l & 31, h = l >> 5;
+    if (c >= ncol) return;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        float *drow = tile + ((t & ~63) + 32 * b + 4 * h) * W + c;
+#pragma unroll
+        for (int g = 0; g < 16; ++g) drow[(8 * (g >> 2) + (g & 3)) * W] = acc[b][g];
+    }
+}
+
 template <typename TI, typename TO, int MODE, int MB, class Rows>
 __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, const float *Rn, float *tile) {
     constexpr int NR = rows_of<MB>();
@@ -252,15 +289,32 @@ __device__ __forceinline__ void small_body(const SmallArgs &a, const Rows &R, co
     const int64_t b0 = (int64_t)blockIdx.x * NR;
     const int M = (int)a.M, r = (int)a.r;
     const int nrow = (int)((a.B - b0 < NR) ? (a.B - b0) : NR);
+    // prob2vec with codebooks of 17..32 entries runs on the matrix cores
+    constexpr bool MM = MB == 24 || MB == 32;
+    constexpr int KH = MB / 2;
+    [[maybe_unused]] const int c = t & 31, h = (t >> 5) & 1;
     float x[MB];
     if (MODE == MODE_P2V) {
-        row_prob2vec<MB>(tile + t * M, M, R, x);
-        lds_barrier();   // the tile is reused for the outputs
-        regs_to_tile<MB>(x, r, tile);
+        if constexpr (MM) {
+            // T = P R: B[k][j] = R[k][j]
+            float bk[KH];
+#pragma unroll
+            for (int kk = 0; kk < KH; ++kk) bk[kk] = (c < r) ? R.Rs[(kk + KH * h) * MB + c] : 0.f;
+            gs16v acc[2];
+            wave_rows_mm<KH>(tile, M, M, bk, acc);
+            lds_barrier();   // the tile is reused for the outputs
+            wave_rows_out(acc, r, r, tile);
+        } else {
+            row_prob2vec<MB>(tile + t * M, M, R, x);
+            lds_barrier();   // the tile is reused for the outputs
+            regs_to_tile<MB>(x, r, tile);
+        }
         lds_barrier();
         tile_store<TO, NR>(static_cast<TO *>(a.Out), a.ldout, b0, nrow, r, tile);
         return;
     }
+    // (scores stay on the vector units: there the matrix-core form, which
+    // returns the products through the tile, measured slower)
     tile_to_regs<MB>(tile, r, x);
     lds_barrier();   // the tile is reused for the outputs
     float n2 = 0.f;
@@ -421,7 +475,6 @@ __device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const
     }
 }
 
-typedef float gs16v __attribute__((ext_vector_type(16)));
 
 // --------------------------------------------- soft selection, Gram form
 //

@@ -526,7 +526,9 @@ def test_soft_select_matches_separate_calls():
         torch.cuda.synchronize()
         assert torch.equal(idx, g["argmax"])
         assert rowrel(host(g["S"]), host(S)) <= 1e-6
-        assert rowrel(host(g["A"]), host(A)) <= 1e-6
+        # the two paths sum in different orders; a softmax of beta * s moves
+        # each weight by at most 2 beta max|ds| relative to itself
+        assert rowrel(host(g["A"]), host(A)) <= 2 * 16.0 * 1e-6
 
 
 @pytest.mark.parametrize("with_t", [False, True])
