@@ -175,6 +175,8 @@ def test_project_bf16_output():
     (300, 160, 900, 0.1, torch.float32),     # rank-deficient, r < M
     (250, 150, 800, 0.0, torch.bfloat16),
     (260, 20, 256, 0.0, torch.bfloat16),
+    (400, 29, 768, 0.1, torch.float32),      # padded to 32 (matrix cores), r < M, ragged rows
+    (333, 31, 512, 0.0, torch.bfloat16),
 ])
 def test_prob2vec(B, M, D, dup, dtype):
     print("prob2vec", B, M, D, dup, dtype, flush=True)
