@@ -489,6 +489,12 @@ __device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const
 // number of loads whatever the row count (the pieces beyond the range read as
 // zero and are not used) and the codebook loads issued before them can be
 // waited for alone.
+// Cache-policy operand of the fp32 tile loads: non-temporal (nt), since the
+// tile is read once.  Measured on the vsa step: 9.5 -> 8.8 us with the batch
+// coming from HBM, unchanged (8.1 -> 8.0 us) with it cache resident.  Plain
+// loads marked non-temporal in the separate calls' tile moves were 10-25 %
+// slower when their inputs were cache resident, so those stay plain.
+constexpr int NT_LOAD = 2;
 template <typename TI> struct TileReq;
 template <> struct TileReq<float> {
     static constexpr int V = 64 * MAXK / 4 / 64;   // 16-byte pieces per lane of a wave's 64 rows
@@ -498,7 +504,7 @@ template <> struct TileReq<float> {
             __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, n * 4, 0x00020000);
 #pragma unroll
         for (int i = 0; i < V; ++i)
-            v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rs, (lane + i * 64) * 16, 0, 0));
+            v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rs, (lane + i * 64) * 16, 0, NT_LOAD));
     }
 };
 template <> struct TileReq<bf16_t> {
