@@ -506,17 +506,45 @@ template <> struct TileReq<float> {
         for (int i = 0; i < V; ++i)
             v[i] = __builtin_bit_cast(f4v, __builtin_amdgcn_raw_buffer_load_b128(rs, (lane + i * 64) * 16, 0, NT_LOAD));
     }
-};
-template <> struct TileReq<bf16_t> {
-    static constexpr int V = 64 * MAXK / 4 / 64;   // 4-element pieces per lane
-    f4v v[V];
-    __device__ __forceinline__ void issue(const bf16_t *base, int n, int lane) {
+    // the requested pieces, then the last n % 4 elements, to the wave's tile
+    __device__ __forceinline__ void store(float *wtile, const float *base, int n, int lane) const {
         const int n4 = n >> 2;
 #pragma unroll
         for (int i = 0; i < V; ++i) {
             const int e4 = lane + i * 64;
-            if (e4 < n4) v[i] = ld4(base + 4 * e4);
+            if (e4 < n4) st4(wtile + 4 * e4, v[i]);
         }
+        const int e = 4 * n4 + lane;
+        if (e < n) wtile[e] = base[e];
+    }
+};
+// bf16 rows: 16-byte pieces of 8 elements (the tile start is 16-byte aligned).
+template <> struct TileReq<bf16_t> {
+    typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+    static constexpr int V = 64 * MAXK / 8 / 64;   // 8-element pieces per lane
+    u4v v[V];
+    __device__ __forceinline__ void issue(const bf16_t *base, int n, int lane) {
+        const int n8 = n >> 3;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e8 = lane + i * 64;
+            if (e8 < n8) v[i] = *reinterpret_cast<const u4v *>(base + 8 * e8);
+        }
+    }
+    __device__ __forceinline__ void store(float *wtile, const bf16_t *base, int n, int lane) const {
+        const int n8 = n >> 3;
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e8 = lane + i * 64;
+            if (e8 < n8) {
+                const u4v u = v[i];
+                st4(wtile + 8 * e8, f4v{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)});
+                st4(wtile + 8 * e8 + 4, f4v{__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u),
+                                            __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xffff0000u)});
+            }
+        }
+        for (int e = 8 * n8 + lane; e < n; e += 64) wtile[e] = ld_f32<bf16_t>(base, e);
     }
 };
 
@@ -599,7 +627,7 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     const TI *bbase = static_cast<const TI *>(G.P) + b0 * G.ldp;
     const bool contig = G.ldp == M && aligned16(bbase);
     const TI *base = bbase + (int64_t)wrow0 * M;
-    const int n = nroww * M, n4 = n >> 2;
+    const int n = nroww * M;
     TileReq<TI> req;
     req.issue(base, contig ? n : 0, lane);   // an empty range issues nothing useful
 
@@ -610,13 +638,7 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
 
     // 4. this wave's rows to its part of the tile
     if (contig) {
-#pragma unroll
-        for (int i = 0; i < TileReq<TI>::V; ++i) {
-            const int e4 = lane + i * 64;
-            if (e4 < n4) st4(wtile + 4 * e4, req.v[i]);
-        }
-        const int e = 4 * n4 + lane;
-        if (e < n) wtile[e] = ld_f32<TI>(base, e);
+        req.store(wtile, base, n, lane);
     } else {
         tile_load<TI, 64>(static_cast<const TI *>(G.P), G.ldp, b0 + wrow0, nroww, M, wtile, lane);
     }
