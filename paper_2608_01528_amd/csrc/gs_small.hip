@@ -78,6 +78,31 @@ __device__ __forceinline__ void tile_load(const T *__restrict__ g, int64_t ld, i
                                           float *tile, int t = threadIdx.x) {
     const int n = nrow * w;
     const T *base = g + b0 * ld;
+    if constexpr (sizeof(T) == 2) if (ld == w && aligned16(base)) {
+        // bf16: 16-byte pieces of eight values
+        typedef unsigned int u4v __attribute__((ext_vector_type(4)));
+        const int n8 = n >> 3;
+        constexpr int V = (NT * WMAX / 8 + NT - 1) / NT;
+        u4v v[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e8 = t + i * NT;
+            if (e8 < n8) v[i] = *reinterpret_cast<const u4v *>(base + 8 * e8);
+        }
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            const int e8 = t + i * NT;
+            if (e8 < n8) {
+                const u4v u = v[i];
+                st4(tile + 8 * e8, f4v{__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u)});
+                st4(tile + 8 * e8 + 4, f4v{__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u),
+                                           __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xffff0000u)});
+            }
+        }
+        for (int e = 8 * n8 + t; e < n; e += NT) tile[e] = ld_f32<T>(base, e);
+        return;
+    }
     if (ld == w && aligned16(base)) {
         const int n4 = n >> 2;
         constexpr int V = (NT * WMAX / 4 + NT - 1) / NT;
