@@ -880,19 +880,16 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     const TI *P = static_cast<const TI *>(G.P);
     const TI *R = static_cast<const TI *>(G.R);
 
-    // 1. request the probability tile
+    // 1. request the probability tile: each wave its own 64 rows, as in the
+    // Gram form (one linear range per wave when rows are contiguous)
+    static_assert(SBLK == SROWS, "one row per thread");
     const TI *base = P + b0 * G.ldp;
     const bool contig = G.ldp == G.M && aligned16(base);
-    const int n = nrow * M, n4 = n >> 2;
-    constexpr int V = SBLK * MAXK / 4 / SROWS;
-    f4v v[V];
-    if (contig) {
-#pragma unroll
-        for (int i = 0; i < V; ++i) {
-            const int e4 = threadIdx.x + i * SROWS;
-            if (e4 < n4) v[i] = ld4(base + 4 * e4);
-        }
-    }
+    const int lane = threadIdx.x & 63, wrow0 = threadIdx.x & ~63;
+    const int nroww = (nrow - wrow0 < 0) ? 0 : (nrow - wrow0 < 64) ? nrow - wrow0 : 64;
+    const TI *wbase = base + (int64_t)wrow0 * M;
+    TileReq<TI> req;
+    req.issue(wbase, contig ? nroww * M : 0, lane);
     // 2. stage the norms and the padded codebook block while the tile is in
     // flight
     stage_norms<TI, SROWS>(R, G.ldr, M, r, G.cnorm, a.cosine != 0, MB, Rn);
@@ -902,13 +899,7 @@ __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     }
     // 3. tile to LDS
     if (contig) {
-#pragma unroll
-        for (int i = 0; i < V; ++i) {
-            const int e4 = threadIdx.x + i * SROWS;
-            if (e4 < n4) st4(tile + 4 * e4, v[i]);
-        }
-        const int e = 4 * n4 + threadIdx.x;
-        if (e < n) tile[e] = ld_f32<TI>(base, e);
+        req.store(tile + wrow0 * M, wbase, nroww * M, lane);
     } else {
         tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
     }
