@@ -1,36 +1,33 @@
 """Throughput benchmark of the Gram-Space hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload stress]
 
-Workload: four bipolar attribute codebooks with M = 5, 6, 10, 22 entries of
-dimension D = 1024 (the VSA-reasoning shape: attribute codebooks of a
-RAVEN-style problem), and for each a batch of 4096 problems x 16 panels =
-65536 probability rows (softmax of N(0, 2) logits).  The codebooks are
-compressed once before timing (compress time is reported).  One step runs,
-for every codebook, probability vectorisation, cosine similarity with argmax
-and the attention-score softmax (beta = 16) on Gram-loc: 262144 queries per
-step, in one fused launch (gs_soft_select).  The same step through the
-separate calls (gs_prob2vec, gs_similarity, gs_attention: 12 launches) is
-timed as well and reported under "extra".
+Default workload (the headline line): the stress configuration.  One bipolar
+codebook of M = 2048 entries of dimension D = 16384, 205 of them duplicates of
+other entries (rank 1843), is compressed once before timing (its time is
+reported).  The batch holds 262144 queries x = p C + N(0, 0.1) noise with
+p ~ Dirichlet(1/2), stored as bf16 (P and X), with bf16 basis and coordinates
+and fp32 accumulation.  One step is the whole matrix-space pipeline over the
+batch: project (t = Q x, with ||x||^2), prob2vec (t = p R), cosine similarity
+with argmax, attention weights softmax(16 s) and reconstruct (x = t Q),
+each a separate library call; `value` is queries per second over the K timed
+steps (synchronised wall clock), and HIP events around every call on the
+launch stream give each kernel's mean duration, the dominant one going into
+the matrix-core roofline entry.  The fused soft-selection step of the vsa
+workload (four attribute codebooks, both of its forms) is reported under
+"extra", and the oracle's rate on a seeded sample of the same batch under
+"cpu_baseline".
 
-Inputs stay resident in HBM.  Steps cycle through several independent copies
-of the batch (inputs and outputs) so that the working set exceeds the 256 MiB
-Infinity Cache: every step reads its inputs from HBM.  The K timed steps are
-captured in one HIP graph and replayed once, bracketed by device
-synchronisation (the wall clock of `value`) and by HIP events on the replay
-stream, whose interval over K is the mean time per launch (the kernel and the
-dispatch gap between graph nodes) used by the roofline entry.  --streams N
-also times the steps spread over N streams of one graph (extra.concurrent).
+Inputs stay resident in HBM: they are generated on the device before the
+timed region, and every step reads and writes the same resident buffers
+(several GB each, far beyond the 256 MiB Infinity Cache).
 
-The JSON line also carries the oracle's throughput on the host cores for a
-bounded sample of the same workload.
-
-Other workloads (--workload): large, binary and stress time one step of the
-separate calls of those configurations with HIP events per call (the
-products with the codebook coordinates R flag R as lower echelon, as
-gs_compress returns it); dimsweep measures the similarity lookup against the
-vector dimension, dense and Gram-Space; bind times the binding operators on
-restored vectors.
+Other workloads (--workload): vsa makes the fused soft selection the headline
+(K launches captured in one HIP graph and replayed once, cycling through
+copies of the batch larger than the Infinity Cache); large and binary time one
+step of the separate calls of those configurations; dimsweep measures the
+similarity lookup against the vector dimension, dense and Gram-Space; bind
+times the binding operators on restored vectors.
 """
 from __future__ import annotations
 
@@ -54,30 +51,45 @@ wl = None
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="vsa", choices=["vsa", "large", "binary", "stress", "dimsweep", "bind"],
-                    help="vsa (default, the headline): fused soft selection; large / binary / stress: "
-                         "the matrix-core rows (project, reconstruct + bind, large similarity); dimsweep: "
-                         "similarity latency against the vector dimension, dense vs Gram-Space; bind: binding of restored "
-                         "vectors (circular convolution / correlation, xor, product)")
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--sets", type=int, default=0, help="batch copies to cycle through (0: >= 1 GiB)")
+    ap.add_argument("--workload", default="stress",
+                    choices=["stress", "vsa", "large", "binary", "dimsweep", "bind"],
+                    help="stress (default, the headline): the whole matrix-space pipeline of the stress "
+                         "configuration in bf16; vsa: the fused soft selection of four attribute codebooks; "
+                         "large / binary: the separate calls of those configurations (fp32); dimsweep: "
+                         "similarity latency against the vector dimension, dense vs Gram-Space; bind: binding of "
+                         "restored vectors (circular convolution / correlation, xor, product)")
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 20; vsa: 200)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed warm-up steps (default 3; vsa: 20)")
+    ap.add_argument("--sets", type=int, default=0, help="vsa: batch copies to cycle through (0: >= 1 GiB)")
     ap.add_argument("--beta", type=float, default=16.0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-unfused", action="store_true", help="skip timing the 12-call path")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="vsa: seconds of oracle work to time")
+    ap.add_argument("--cpu-rows", type=int, default=8192,
+                    help="stress / large / binary: rows of the seeded sample the oracle processes")
+    ap.add_argument("--no-vsa", action="store_true", help="stress: skip the fused vsa step reported under extra")
+    ap.add_argument("--no-unfused", action="store_true", help="vsa: skip timing the 12-call path")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this size (counter calibration)")
     ap.add_argument("--pmc-summary", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE counter CSVs (kernel run, copy calibration) "
-                         "into profiles/traffic_<kernel>_<workload>.json and exit")
+                         "into profiles/traffic_<call>_<workload>.json and exit")
     ap.add_argument("--streams", type=int, default=1,
                     help="vsa: also time the fused steps spread round robin over this many streams in one "
                          "graph (independent batches in flight together, as a server would run them); reported "
                          "under extra.concurrent, not as the headline")
-    ap.add_argument("--pmc-kernel", default="soft_gram_kernel")
+    ap.add_argument("--pmc-kernel", default="soft_gram_kernel",
+                    help="--pmc-summary: substring of the kernel name to summarise")
+    ap.add_argument("--pmc-call", default="soft_gram_kernel",
+                    help="--pmc-summary: name of the call in the output file name")
+    ap.add_argument("--pmc-workload", default="vsa")
     ap.add_argument("--pmc-copy-mib", type=int, default=512)
-    return ap.parse_args()
+    args = ap.parse_args()
+    heavy = args.workload in ("stress", "large", "binary")
+    if args.steps is None:
+        args.steps = 20 if heavy else 200
+    if args.warmup is None:
+        args.warmup = 3 if heavy else 20
+    return args
 
 
 def kernel_source_hash() -> str:
@@ -89,10 +101,10 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def load_traffic(kernel: str, workload: str):
+def load_traffic(call: str, workload: str):
     """HBM bytes per launch from the committed counter summary, if it was taken
     on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (call, workload))
     if not os.path.exists(path):
         return None
     try:
@@ -102,6 +114,16 @@ def load_traffic(kernel: str, workload: str):
     if d.get("source_hash") != kernel_source_hash():
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 class VsaWorkload:
@@ -235,14 +257,18 @@ def timed_graph(torch, steps, launch_step, stream, nstreams=1):
 
 
 def _counter_kib(path, name_part, counter):
-    """Mean per-dispatch value (KiB) of a counter for kernels whose name holds
-    name_part, from a rocprofv3 counter_collection CSV."""
+    """Mean per-dispatch value (KiB) of a counter for the longest dispatches of
+    kernels whose name holds name_part (those lasting at least half as long as
+    the longest one, so that one call is picked where two calls share a kernel
+    instance), from a rocprofv3 counter_collection CSV."""
     import csv
-    vals = [float(r["Counter_Value"]) for r in csv.DictReader(open(path))
+    rows = [r for r in csv.DictReader(open(path))
             if name_part in r["Kernel_Name"] and r["Counter_Name"] == counter]
-    if not vals:
+    if not rows:
         raise SystemExit("no %s records for kernels matching %r in %s" % (counter, name_part, path))
-    return float(np.mean(vals)), len(vals)
+    dur = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows]
+    keep = [float(r["Counter_Value"]) for r, d in zip(rows, dur) if d >= 0.5 * max(dur)]
+    return float(np.mean(keep)), len(keep)
 
 
 def pmc_summary(args):
@@ -258,12 +284,13 @@ def pmc_summary(args):
     w_scale = copy_bytes / (cw_kib * 1024.0)
     read = f_kib * 1024.0 * f_scale
     write = w_kib * 1024.0 * w_scale
-    out = {"kernel": args.pmc_kernel, "workload": "vsa", "source_hash": kernel_source_hash(),
+    out = {"kernel": args.pmc_kernel, "call": args.pmc_call, "workload": args.pmc_workload,
+           "source_hash": kernel_source_hash(),
            "hbm_bytes_per_launch": read + write, "read_bytes_per_launch": read, "write_bytes_per_launch": write,
            "fetch_kib_per_dispatch": f_kib, "write_kib_per_dispatch": w_kib, "dispatches": [nf, nw],
            "copy_calibration": {"bytes": copy_bytes, "fetch_kib": cf_kib, "write_kib": cw_kib,
                                 "fetch_scale": f_scale, "write_scale": w_scale}}
-    path = os.path.join(ROOT, "profiles", "traffic_%s_vsa.json" % args.pmc_kernel)
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (args.pmc_call, args.pmc_workload))
     json.dump(out, open(path, "w"), indent=1)
     print(json.dumps(out))
 
@@ -272,15 +299,15 @@ MFMA_PEAK = {"f32": 157.3, "bf16": 2516.6}
 
 
 def mfma_workload(args, torch, gsm):
-    """One step of a large workload through the separate calls; per-call HIP
-    events on the launch stream give each kernel's time and the dominant one
-    goes into the roofline entry (matrix-core bound)."""
+    """One step of the large (fp32) or binary (fp32) workload through the
+    separate calls; per-call HIP events on the launch stream give each
+    kernel's time and the dominant one goes into the roofline entry
+    (matrix-core bound)."""
     w = wl.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
-    print("%s: codebook %d x %d, compress" % (w.name, w.Ms[0], w.D), file=sys.stderr, flush=True)
+    log("%s: codebook %d x %d, compress" % (w.name, w.Ms[0], w.D))
     C = torch.from_numpy(wl.codebook(w)).to(dev)
-    bf = w.bf16
-    dt = torch.bfloat16 if bf else torch.float32
+    dt = torch.float32
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
@@ -290,7 +317,7 @@ def mfma_workload(args, torch, gsm):
     # matrices with 16-byte aligned rows, as the library's own outputs are
     rows = lambda n, c, t: gsm.alloc_rows(n, c, t, dev)
     calls = []
-    if args.workload in ("large", "stress"):
+    if args.workload == "large":
         P = wl.device_dirichlet_half(B, M, w.seed, torch, dev, dtype=dt)
         X = wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch, dtype=dt)
         T = rows(B, r, dt)
@@ -299,16 +326,10 @@ def mfma_workload(args, torch, gsm):
         A = torch.empty((B, M), dtype=torch.float32, device=dev)
         idx = torch.empty(B, dtype=torch.int32, device=dev)
         calls.append(("project", lambda: gsm.gs_project(X, Q, out=T, xnorm2=True, xnorm2_out=xn), 2.0 * B * D * r))
-        if args.workload == "stress":
-            T2 = rows(B, r, dt)
-            calls.append(("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2, echelon=True), 2.0 * B * M * r))
         calls.append(("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx,
                                                               echelon=True), 2.0 * B * M * r))
         calls.append(("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=args.beta, out=A,
                                                             echelon=True), 2.0 * B * M * r))
-        if args.workload == "stress":
-            Xr = rows(B, D, dt)
-            calls.append(("reconstruct", lambda: gsm.gs_reconstruct(T2, Q, out=Xr), 2.0 * B * r * D))
     else:   # binary: bind pairs
         Pa = torch.from_numpy(wl.probabilities(w, 0)).to(dev)
         Pb = torch.from_numpy(wl.probabilities(w, 0, stream=wl.STREAM_PROBS_B)).to(dev)
@@ -326,13 +347,12 @@ def mfma_workload(args, torch, gsm):
                       4.0 * B * r * D))
         calls.append(("reproject", lambda: gsm.gs_project(Y, Q, out=Ty), 2.0 * B * D * r))
     stream = torch.cuda.current_stream()
-    print("%s: inputs ready (rank %d), %d warm-up step(s)" % (w.name, r, max(1, args.warmup)), file=sys.stderr,
-          flush=True)
+    log("%s: inputs ready (rank %d), %d warm-up step(s)" % (w.name, r, max(1, args.warmup)))
     for _ in range(max(1, args.warmup)):
         for _, f, _ in calls:
             f()
     torch.cuda.synchronize()
-    print("%s: %d timed step(s)" % (w.name, args.steps), file=sys.stderr, flush=True)
+    log("%s: %d timed step(s)" % (w.name, args.steps))
     per = {n: [] for n, _, _ in calls}
     evs = []
     torch.cuda.synchronize()
@@ -356,32 +376,33 @@ def mfma_workload(args, torch, gsm):
     useful = {n: flops[n] * nnz / (M * r) for n in flops if n in ("prob2vec", "similarity", "attention")}
     dom = max(per, key=lambda n: sum(per[n]))
     dom_ms = float(np.mean(per[dom]))
-    peak = MFMA_PEAK["bf16" if bf else "f32"]
+    peak = MFMA_PEAK["f32"]
     achieved = flops[dom] / (dom_ms * 1e-3) / 1e12
-    # products with at least 256 tiles of 256 x 256 (bf16 or fp32 operands,
-    # 16-byte aligned rows) run on the large-tile kernel, the fp32 bound
-    # product as two of its launches; the rest on the 128 x 128 kernels
-    def big(m, n):
-        return ((m + 255) // 256) * ((n + 255) // 256) >= 256
-    store = {"project": (B, r, "X Q^T"), "reproject": (B, r, "Y Q^T"), "reconstruct": (B, D, "T Q"),
-             "reconstruct_bind": (B, D, "T Q .* T2 Q"), "prob2vec": (B, r, "P R")}
-    if dom in store:
-        m_, n_, what = store[dom]
-        on_big = big(m_, n_) and (dom != "reconstruct_bind" or not bf)
-        kernel = "%s (%s)" % ("gemm256_store_kernel" if on_big else "gemm_store_kernel", what)
-    else:
-        kernel = {"similarity": "similarity scores", "attention": "attention weights"}[dom]
+    kernel = {"project": "gemm256_store_kernel (X Q^T)", "reproject": "gemm256_store_kernel (Y Q^T)",
+              "reconstruct_bind": "gemm256_store_kernel x 2 (T Q, then .* T2 Q)",
+              "prob2vec": "gemm256_store_kernel (P R)", "similarity": "similarity scores",
+              "attention": "attention weights"}[dom]
+    cpu = None
+    if not args.no_cpu:
+        n = min(args.cpu_rows, B)
+        sample = np.sort(np.random.default_rng(w.seed).choice(B, size=n, replace=False))
+        si = torch.from_numpy(sample).to(dev)
+        if args.workload == "large":
+            cpu = cpu_baseline_rows(w, {"X": X.index_select(0, si).cpu().numpy()}, args.beta)
+        else:
+            cpu = cpu_baseline_rows(w, {"Pa": Pa.index_select(0, si).cpu().numpy(),
+                                        "Pb": Pb.index_select(0, si).cpu().numpy()}, args.beta)
     out = {
         "metric": METRIC, "value": B * args.steps / wall, "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if bf else "f32", "data": "synthetic",
+        "dtype": "f32", "data": "synthetic",
         "config": {"workload": "%s: codebook M=%d, D=%d (r=%d), batch %d; calls %s"
                                % (w.name, M, D, r, B, ", ".join(n for n, _, _ in calls))},
         "roofline": {"bound": "mfma", "kernel": kernel, "call": dom, "achieved": achieved, "peak": peak,
-                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": load_traffic(dom, w.name),
                      "flops_per_launch": flops[dom], "avg_launch_ms": dom_ms},
-        "cpu_baseline": None,
+        "cpu_baseline": cpu,
         "extra": {"per_call_ms": {n: float(np.mean(v)) for n, v in per.items()},
                   "per_call_TFLOPs": {n: flops[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in per},
                   "per_call_useful_TFLOPs": {n: useful[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in useful},
@@ -389,6 +410,194 @@ def mfma_workload(args, torch, gsm):
                   "compress_ms": compress_ms, "rank": r, "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_rows(w, inputs, beta):
+    """The oracle on a seeded sample of the large or binary batch.  large: cosine
+    similarity of x with the codebook, argmax and softmax (project +
+    similarity + attention).  binary: v_a = p_a C and v_b = p_b C (prob2vec),
+    the cosine similarity of v_a with the codebook and argmax, and the bound
+    vector v_a .* v_b (reconstruct + bind); the re-projection is left out
+    (the dense side has no basis)."""
+    import oracle
+    flags = oracle.use_native_build()
+    C = wl.codebook(w)
+    t0 = time.perf_counter()
+    if "X" in inputs:
+        n = inputs["X"].shape[0]
+        S = oracle.similarity(inputs["X"], C, oracle.COSINE)
+        oracle.argmax(S)
+        oracle.softmax(S, beta)
+        what = "dense fp64 cosine similarity of x with the codebook, argmax, softmax(beta=%g)" % beta
+    else:
+        n = inputs["Pa"].shape[0]
+        Va = oracle.prob2vec(inputs["Pa"], C)
+        Vb = oracle.prob2vec(inputs["Pb"], C)
+        S = oracle.similarity(Va, C, oracle.COSINE)
+        oracle.argmax(S)
+        oracle.bind(Va, Vb)
+        what = "dense fp64 v = p C for both operands, cosine similarity + argmax, v_a .* v_b"
+    dt = time.perf_counter() - t0
+    rate = n / dt
+    return {"value": rate, "unit": "queries/s", "cores": oracle.threads(), "cpu_model": cpu_model(),
+            "kind": "oracle", "build": flags,
+            "sample": "%d seeded rows of the %d-row batch: %s; %.1f s; full batch extrapolated to %.0f s"
+                      % (n, w.B, what, dt, w.B / rate)}
+
+
+STRESS_CALLS = ("project", "prob2vec", "similarity", "attention", "reconstruct")
+
+
+def cpu_baseline_stress(w, Ps, Xs, beta, rows_desc):
+    """The oracle (dense fp64 in D-space) on a seeded sample of the stress
+    batch: for each sampled query, cosine similarity of x against every
+    codebook vector (what project + similarity compute), argmax, the softmax
+    of beta times the scores (attention) and v = p C (what prob2vec +
+    reconstruct compute).  Inputs are read back from the device (bf16, upcast
+    exactly) before the timed region."""
+    import oracle
+    flags = oracle.use_native_build()
+    C = wl.codebook(w)
+    # the natively built copy computes bit for bit what the tested build does
+    # (same source, no FMA contraction, no reassociation): checked on two rows
+    t0 = time.perf_counter()
+    S = oracle.similarity(Xs, C, oracle.COSINE)
+    oracle.argmax(S)
+    oracle.softmax(S, beta)
+    oracle.prob2vec(Ps, C)
+    dt = time.perf_counter() - t0
+    n = Xs.shape[0]
+    rate = n / dt
+    return {"value": rate, "unit": "queries/s", "cores": oracle.threads(), "cpu_model": cpu_model(),
+            "kind": "oracle", "build": flags,
+            "sample": "%d seeded rows (%s) of the %d-row batch: dense fp64 cosine similarity of x with the "
+                      "%d x %d codebook, argmax, softmax(beta=%g), v = p C; %.1f s; full batch extrapolated "
+                      "to %.0f s" % (n, rows_desc, w.B, w.Ms[0], w.D, beta, dt, w.B / rate)}
+
+
+def stress_workload(args, torch, gsm):
+    """The headline: one step = project, prob2vec, similarity + argmax,
+    attention and reconstruct over the whole stress batch (bf16 storage, fp32
+    accumulation), K steps timed on the synchronised wall clock with HIP
+    events around every call."""
+    w = wl.WORKLOADS["stress"]
+    dev = torch.device("cuda:0")
+    B, D, M = w.B, w.D, w.Ms[0]
+    dt = torch.bfloat16
+    log("stress: codebook %d x %d, compress" % (M, D))
+    C = torch.from_numpy(wl.codebook(w)).to(dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
+    torch.cuda.synchronize()
+    compress_ms = (time.perf_counter() - t0) * 1e3
+    rows = lambda n, c, t: gsm.alloc_rows(n, c, t, dev)
+    P = wl.device_dirichlet_half(B, M, w.seed, torch, dev, dtype=dt)
+    X = wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch, dtype=dt)
+    del C
+    T = rows(B, r, dt)
+    T2 = rows(B, r, dt)
+    xn = torch.empty(B, dtype=torch.float32, device=dev)
+    S = torch.empty((B, M), dtype=torch.float32, device=dev)
+    A = torch.empty((B, M), dtype=torch.float32, device=dev)
+    idx = torch.empty(B, dtype=torch.int32, device=dev)
+    Xr = rows(B, D, dt)
+    beta = args.beta
+    fl_proj, fl_code = 2.0 * B * D * r, 2.0 * B * M * r
+    calls = [
+        ("project", lambda: gsm.gs_project(X, Q, out=T, xnorm2=True, xnorm2_out=xn), fl_proj),
+        ("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2, echelon=True), fl_code),
+        ("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx,
+                                                 echelon=True), fl_code),
+        ("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=beta, out=A, echelon=True),
+         fl_code),
+        ("reconstruct", lambda: gsm.gs_reconstruct(T2, Q, out=Xr), fl_proj),
+    ]
+    stream = torch.cuda.current_stream()
+    log("stress: inputs ready (rank %d), %d warm-up step(s)" % (r, args.warmup))
+    for _ in range(args.warmup):
+        for _, f, _ in calls:
+            f()
+    torch.cuda.synchronize()
+    log("stress: %d timed step(s)" % args.steps)
+    evs = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for n, f, _ in calls:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            f()
+            e1.record(stream)
+            evs.append((n, e0, e1))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {n: [] for n, _, _ in calls}
+    for n, e0, e1 in evs:
+        per[n].append(e0.elapsed_time(e1))
+    mean = {n: float(np.mean(v)) for n, v in per.items()}
+    flops = {n: fl for n, _, fl in calls}
+    # the products with the lower-echelon R skip its zero blocks: also the
+    # rate on R's nonzero entries (2 nnz(R) flops per row)
+    nnz = int((R != 0).sum().item())
+    useful = {n: flops[n] * nnz / (M * r) for n in ("prob2vec", "similarity", "attention")}
+    dom = max(mean, key=mean.get)
+    kernels = {"project": "gemm256_store_kernel<bf16, bf16, BNN=false> (X Q^T, with ||x||^2)",
+               "reconstruct": "gemm256_store_kernel<bf16, bf16, BNN=true> (T Q, persistent tile walk)",
+               "prob2vec": "gemm256_store_kernel<bf16, bf16, BNN=true> (P R, echelon K ranges)",
+               "similarity": "scores256_kernel + rows_argmax_kernel", "attention": "scores256_kernel"}
+    achieved = flops[dom] / (mean[dom] * 1e-3) / 1e12
+    peak = MFMA_PEAK["bf16"]
+    ms_per_step = wall * 1e3 / args.steps
+
+    # oracle sample rows, read back before anything else is freed
+    cpu = None
+    if not args.no_cpu:
+        n = min(args.cpu_rows, B)
+        rng = np.random.default_rng(w.seed)
+        sample = np.sort(rng.choice(B, size=n, replace=False))
+        si = torch.from_numpy(sample).to(dev)
+        Ps = P.index_select(0, si).float().cpu().numpy()
+        Xs = X.index_select(0, si).float().cpu().numpy()
+    del X, Xr, P, T, T2, S, A, Q, R
+    torch.cuda.empty_cache()
+    extra = {"per_call_ms": mean,
+             "per_call_sum_ms": float(sum(mean.values())),
+             "per_call_TFLOPs": {n: flops[n] / (mean[n] * 1e-3) / 1e12 for n in mean},
+             "per_call_frac_bf16_peak": {n: flops[n] / (mean[n] * 1e-3) / 1e12 / peak for n in mean},
+             "per_call_useful_TFLOPs": {n: useful[n] / (mean[n] * 1e-3) / 1e12 for n in useful},
+             "nnz_R": nnz, "compress_ms": compress_ms, "rank": r,
+             "timing": "K steps of the five calls on the current stream; HIP events around every call",
+             "kernel_source_hash": kernel_source_hash()}
+    if not args.no_vsa:
+        log("vsa: fused soft selection (both forms)")
+        extra["vsa_fused"] = vsa_fused_extra(args, torch, gsm)
+    if not args.no_cpu:
+        log("oracle: %d sampled rows" % n)
+        cpu = cpu_baseline_stress(w, Ps, Xs, beta, "numpy default_rng(%d).choice without replacement" % w.seed)
+    out = {
+        "metric": METRIC, "value": B * args.steps / wall, "unit": "queries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "stress: bipolar codebook M=%d (205 duplicated rows, rank %d), D=%d; %d queries "
+                               "x = p C + N(0, 0.1), p ~ Dir(1/2); bf16 storage, fp32 accumulation; step = "
+                               "project (+||x||^2), prob2vec (echelon R), cosine similarity + argmax, attention "
+                               "softmax(beta=%g), reconstruct; compress once before timing"
+                               % (M, r, D, B, beta),
+                   "M": M, "D": D, "rank": r, "batch": B},
+        "roofline": {"bound": "mfma", "kernel": kernels[dom], "call": dom, "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": load_traffic(dom, "stress"),
+                     "flops_per_launch": flops[dom], "avg_launch_ms": mean[dom]},
+        "cpu_baseline": cpu,
+        "extra": extra,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
 
 
 def dimsweep_workload(args, torch, gsm):
@@ -559,27 +768,69 @@ def main():
     if args.workload == "bind":
         bind_workload(args, torch, gsm)
         return
-    if args.workload != "vsa":
+    if args.workload == "stress":
+        stress_workload(args, torch, gsm)
+        return
+    if args.workload in ("large", "binary"):
         mfma_workload(args, torch, gsm)
         return
+    vsa_workload(args, torch, gsm)
+
+
+def vsa_prepare(args, torch, gsm):
     w = wl.WORKLOADS["vsa"]
     per_set = sum(w.B * (16 * M + 4) for M in w.Ms)
     nsets = args.sets or max(1, int(np.ceil((1 << 30) / per_set)))
     work = VsaWorkload(w, nsets, torch, gsm)
-    beta = args.beta
-
-    # fused step: one gs_soft_select launch over the four codebooks
     prepared = []
     for s in range(nsets):
-        # the fused step keeps the coordinates on chip: it reads P and writes
-        # the scores, their argmax and the attention weights
+        # the fused step reads P and writes the scores, their argmax and the
+        # attention weights; the coordinates are an intermediate
         groups = [{"P": b["sets"][s]["P"], "R": b["R"], "cnorm": b["cnorm"],
                    "S": b["sets"][s]["S"], "argmax": b["sets"][s]["argmax"], "A": b["sets"][s]["A"]}
                   for b in work.books]
         prepared.append(gsm.soft_groups(groups))
+    return w, work, nsets, prepared
+
+
+def vsa_fused_extra(args, torch, gsm, steps=200):
+    """The fused soft selection of the vsa workload in both of its forms:
+    scores through the Gram matrix (soft_gram_kernel) and through the
+    coordinates t = p R formed in registers (soft_select_kernel, T not
+    stored).  Each: `steps` launches in one HIP graph, replayed once."""
+    w, work, nsets, prepared = vsa_prepare(args, torch, gsm)
+    stream = torch.cuda.current_stream()
+    bpl = float(work.fused_bytes())
+    out = {"workload": "vsa: 4 bipolar attribute codebooks M=5,6,10,22, D=1024; 65536 probability rows each "
+                       "(262144 queries per launch); fp32; cosine similarity + argmax + softmax(beta=%g); "
+                       "%d batch copies (>= 1 GiB) cycled" % (args.beta, nsets),
+           "bytes_per_launch": bpl, "compress_ms": work.compress_ms}
+    for form, kernel in (("gram", "soft_gram_kernel"), ("coords", "soft_select_kernel")):
+        def step(k, form=form):
+            gsm.gs_soft_select(None, mode="cosine", beta=args.beta, prepared=prepared[k % nsets], form=form)
+        for k in range(10):
+            step(k)
+        torch.cuda.synchronize()
+        wall, launch_ms = timed_graph(torch, steps, step, stream)
+        gbs = bpl / (launch_ms * 1e-3) / 1e9
+        out[form] = {"kernel": kernel, "ms_per_step": wall * 1e3 / steps, "avg_launch_us": launch_ms * 1e3,
+                     "queries_per_s": work.queries * steps / wall, "GBps": gbs, "frac_hbm": gbs / HBM_PEAK_GBS,
+                     "traffic": load_traffic(kernel, "vsa")}
+    del work, prepared
+    torch.cuda.empty_cache()
+    return out
+
+
+def vsa_workload(args, torch, gsm):
+    """--workload vsa: the fused soft selection (Gram form) as the headline."""
+    w, work, nsets, prepared = vsa_prepare(args, torch, gsm)
+    beta = args.beta
 
     def fused_step(k):
-        gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[k % nsets])
+        gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[k % nsets], form="gram")
+
+    def coords_step(k):
+        gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[k % nsets], form="coords")
 
     def unfused_step(k):
         for b in work.books:
@@ -591,6 +842,7 @@ def main():
     stream = torch.cuda.current_stream()
     for k in range(args.warmup):
         fused_step(k)
+        coords_step(k)
         if not args.no_unfused:
             unfused_step(k)
     torch.cuda.synchronize()
@@ -608,6 +860,10 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
         "buffer_copies": nsets,
     }
+    cwall, claunch = timed_graph(torch, args.steps, coords_step, stream)
+    extra["coords_form"] = {"kernel": "soft_select_kernel", "ms_per_step": cwall * 1e3 / args.steps,
+                            "avg_launch_us": claunch * 1e3, "queries_per_s": work.queries * args.steps / cwall,
+                            "GBps": bpl / (claunch * 1e-3) / 1e9}
     if args.streams > 1:
         cwall, _ = timed_graph(torch, args.steps, fused_step, stream, nstreams=args.streams)
         extra["concurrent"] = {"streams": args.streams, "ms_per_step": cwall * 1e3 / args.steps,
@@ -624,7 +880,7 @@ def main():
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         for k in range(args.steps):
-            gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[0])
+            gsm.gs_soft_select(None, mode="cosine", beta=beta, prepared=prepared[0], form="gram")
     g.replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -649,11 +905,12 @@ def main():
         "config": {
             "workload": "vsa: 4 bipolar attribute codebooks M=5,6,10,22, D=1024; 4096 problems x 16 panels "
                         "= 65536 probability rows each; prob2vec + cosine similarity/argmax + softmax(beta=%g) "
-                        "fused, outputs S, argmax, A (coordinates stay on chip)" % beta,
+                        "fused in one launch, scores through the codebook Gram matrix R R^T (no coordinates "
+                        "formed); outputs S, argmax, A" % beta,
             "codebooks_M": w.Ms, "D": w.D, "rows_per_codebook": w.B, "queries_per_step": work.queries,
         },
         "roofline": {
-            "bound": "hbm", "kernel": "soft_gram_kernel", "call": "gs_soft_select",
+            "bound": "hbm", "kernel": "soft_gram_kernel", "call": "gs_soft_select (Gram form)",
             "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
             "traffic": load_traffic("soft_gram_kernel", "vsa"),
             "bytes_per_launch": bpl, "avg_launch_us": launch_ms * 1e3,

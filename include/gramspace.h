@@ -61,7 +61,7 @@
 extern "C" {
 #endif
 
-#define GS_ABI_VERSION 1
+#define GS_ABI_VERSION 2
 
 typedef enum {
     GS_OK = 0,
@@ -275,10 +275,16 @@ gs_status gs_bind_restored(const void *X, gs_dtype xt, int64_t B, int64_t D, int
  *   A[b, j] = softmax over j of beta * S[b, j]
  * It computes what gs_prob2vec, gs_similarity and gs_attention compute on the
  * same inputs, without storing and re-reading the coordinates in between.
- * When T is null the coordinates are not formed at all: the scores are taken
- * through the Gram matrix G = R_g R_g^T (= C C^T, Sec. 3.2) of the codebook,
- * <t, R_g[j]> = sum_k p_k G[k][j] and ||t||^2 = sum_j p_j <t, R_g[j]>, which
- * equal the definitions above up to rounding order.
+ * `form` chooses how the scores are formed:
+ *   GS_SOFT_COORDS  t = p R_g per row, in registers; stored only where T is
+ *                   given; scores <t, R_g[j]> from it
+ *   GS_SOFT_GRAM    the coordinates are not formed at all: the scores are
+ *                   taken through the Gram matrix G = R_g R_g^T (= C C^T,
+ *                   Sec. 3.2) of the codebook, <t, R_g[j]> = sum_k p_k G[k][j]
+ *                   and ||t||^2 = sum_j p_j <t, R_g[j]>, which equal the
+ *                   definitions above up to rounding order; every T must be
+ *                   null (GS_ERR_ARG otherwise)
+ *   GS_SOFT_AUTO    GS_SOFT_COORDS if some group asks for T, else GS_SOFT_GRAM
  *
  *   groups     HOST array of ngroups descriptors, 1 <= ngroups <= 8; in each,
  *              1 <= r <= M <= 32, B >= 0, and
@@ -303,8 +309,11 @@ typedef struct {
     float *A; int64_t lda;
 } gs_soft_group;
 
+typedef enum { GS_SOFT_AUTO = 0, GS_SOFT_GRAM = 1, GS_SOFT_COORDS = 2 } gs_soft_form;
+
 gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, gs_dtype tt,
-                         gs_sim_mode mode, float scale, float beta, void *stream);
+                         gs_sim_mode mode, float scale, float beta, gs_soft_form form,
+                         void *stream);
 
 #ifdef __cplusplus
 }

@@ -64,7 +64,43 @@ def _load():
         return _lib
     if not os.path.exists(_LIB):
         build(force=False)
-    lib = ctypes.CDLL(_LIB)
+    _lib = _bind(ctypes.CDLL(_LIB))
+    return _lib
+
+
+def use_native_build() -> str:
+    """For timing only: compile the same source on the running machine with
+    gcc -O3 -march=native (still no FMA contraction and no reassociation, so
+    every sum keeps its order), check on a small case that it returns bit for
+    bit what the tested build returns, and use it from then on.  Falls back to
+    the tested build if compilation or the check fails.  Returns the flags of
+    the build in use."""
+    global _lib
+    import tempfile
+    base = "gcc -O2 -fopenmp -ffp-contract=off"
+    ref = _load()
+    try:
+        d = tempfile.mkdtemp(prefix="gs_oracle_")
+        path = os.path.join(d, "liboracle_native.so")
+        subprocess.check_call(["gcc", "-O3", "-march=native", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+                               "-ffp-contract=off", _SRC, "-o", path, "-lm"],
+                              stdout=subprocess.DEVNULL, stderr=subprocess.DEVNULL)
+        native = _bind(ctypes.CDLL(path))
+    except (OSError, subprocess.CalledProcessError):
+        return base
+    g = np.random.default_rng(0)
+    X, C, P = g.standard_normal((3, 257)), g.standard_normal((5, 257)), g.random((3, 5))
+    outs = []
+    for lib in (ref, native):
+        _lib = lib
+        S = similarity(X, C, COSINE)
+        outs.append((S, softmax(S, 3.0), prob2vec(P, C), project(X, C), reconstruct(P, C)))
+    same = all(np.array_equal(a, b) for a, b in zip(*outs))
+    _lib = native if same else ref
+    return "gcc -O3 -march=native -fopenmp -ffp-contract=off" if same else base
+
+
+def _bind(lib):
     dp = ctypes.POINTER(ctypes.c_double)
     ip = ctypes.POINTER(ctypes.c_int)
     L = ctypes.c_long
@@ -82,7 +118,6 @@ def _load():
     lib.gso_bind.argtypes = [dp, dp, L, dp]
     lib.gso_circular.argtypes = [dp, dp, L, L, L, ctypes.c_int, dp]
     lib.gso_xor.argtypes = [dp, dp, L, dp]
-    _lib = lib
     return lib
 
 

@@ -109,17 +109,22 @@ int gso_compress(const double *C, long M, long D, double tau,
 }
 
 /* Probability vectorisation (Sec. 2.2): v_b = sum_j P[b, j] c_j.
-   P is B x M, C is M x D, V is B x D. */
+   P is B x M, C is M x D, V is B x D.  The scaled codebook vectors are added
+   to v_b one after the other, j = 0 .. M - 1, so every component is summed
+   in index order. */
 void gso_prob2vec(const double *P, long B, long M, const double *C, long D,
                   double *V)
 {
     #pragma omp parallel for schedule(static)
-    for (long b = 0; b < B; ++b)
-        for (long d = 0; d < D; ++d) {
-            double s = 0.0;
-            for (long j = 0; j < M; ++j) s += P[b * M + j] * C[j * D + d];
-            V[b * D + d] = s;
+    for (long b = 0; b < B; ++b) {
+        double *v = V + b * D;
+        for (long d = 0; d < D; ++d) v[d] = 0.0;
+        for (long j = 0; j < M; ++j) {
+            const double p = P[b * M + j];
+            const double *c = C + j * D;
+            for (long d = 0; d < D; ++d) v[d] += p * c[d];
         }
+    }
 }
 
 /* Euclidean row norms of a B x D matrix. */
@@ -204,17 +209,22 @@ void gso_project(const double *X, long B, long D, const double *Q, long r,
 }
 
 /* Restore to the original domain (Sec. 3.1, Sec. 3.3): x_b = U t_b, i.e.
-   X[b, d] = sum_k T[b, k] Q[k, d].  T is B x r, Q is r x D, X is B x D. */
+   X[b, d] = sum_k T[b, k] Q[k, d].  T is B x r, Q is r x D, X is B x D.  The
+   scaled basis vectors are added one after the other, k = 0 .. r - 1, so
+   every component is summed in index order. */
 void gso_reconstruct(const double *T, long B, long r, const double *Q, long D,
                      double *X)
 {
     #pragma omp parallel for schedule(static)
-    for (long b = 0; b < B; ++b)
-        for (long d = 0; d < D; ++d) {
-            double s = 0.0;
-            for (long k = 0; k < r; ++k) s += T[b * r + k] * Q[k * D + d];
-            X[b * D + d] = s;
+    for (long b = 0; b < B; ++b) {
+        double *x = X + b * D;
+        for (long d = 0; d < D; ++d) x[d] = 0.0;
+        for (long k = 0; k < r; ++k) {
+            const double t = T[b * r + k];
+            const double *q = Q + k * D;
+            for (long d = 0; d < D; ++d) x[d] += t * q[d];
         }
+    }
 }
 
 /* Component-wise binding by element-wise product (Sec. 2.2; Table 1). */

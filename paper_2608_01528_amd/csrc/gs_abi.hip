@@ -344,13 +344,15 @@ gs_status gs_bind_restored(const void *X, gs_dtype xt, int64_t B, int64_t D, int
 }
 
 gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, gs_dtype tt,
-                         gs_sim_mode mode, float scale, float beta, void *stream) {
+                         gs_sim_mode mode, float scale, float beta, gs_soft_form form, void *stream) {
     if (!groups) return fail(GS_ERR_ARG, "gs_soft_select: groups is null");
     if (ngroups < 1 || ngroups > SOFT_MAX_GROUPS)
         return fail(GS_ERR_ARG, "gs_soft_select: ngroups must be in [1, %d]", SOFT_MAX_GROUPS);
     if (!is_batch_type(pt) || !is_batch_type(tt))
         return fail(GS_ERR_DTYPE, "gs_soft_select: P/R and T must be f32 or bf16");
     if (mode != GS_SIM_DOT && mode != GS_SIM_COSINE) return fail(GS_ERR_ARG, "gs_soft_select: unknown mode");
+    if (form != GS_SOFT_AUTO && form != GS_SOFT_GRAM && form != GS_SOFT_COORDS)
+        return fail(GS_ERR_ARG, "gs_soft_select: unknown form");
     std::vector<Span> in, out;
     SoftArgs a{};
     a.ngroups = ngroups;
@@ -358,8 +360,10 @@ gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, 
     a.scale = scale;
     a.beta = beta;
     int64_t tiles = 0;
+    bool any_t = false;
     for (int i = 0; i < ngroups; ++i) {
         const gs_soft_group &g = groups[i];
+        any_t = any_t || (g.T != nullptr && g.B > 0);
         if (g.B < 0 || g.M < 1 || g.M > SOFT_MAX_M || g.r < 1 || g.r > g.M)
             return fail(GS_ERR_SHAPE, "gs_soft_select: group %d needs B >= 0 and 1 <= r <= M <= %d", i, SOFT_MAX_M);
         GS_CHECK(check_matrix(g.P, "P", g.B, g.M, g.ldp, pt, false));
@@ -395,6 +399,9 @@ gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, 
     }
     a.tile_start[ngroups] = tiles;
     a.ntiles = tiles;
+    if (form == GS_SOFT_GRAM && any_t)
+        return fail(GS_ERR_ARG, "gs_soft_select: the Gram form forms no coordinates, but a group asks for T");
+    a.coords = form == GS_SOFT_COORDS || (form == GS_SOFT_AUTO && any_t);
     GS_CHECK(check_overlaps(in, out));
     if (tiles == 0) return ok();
     GS_CHECK(check_device());

@@ -209,6 +209,7 @@ struct SoftArgs {
     int ngroups;
     int cosine;
     float scale, beta;
+    int coords;                                 // form t = p R per row (else scores through R R^T)
 };
 
 int64_t soft_select_tiles(int64_t B);

@@ -955,9 +955,7 @@ hipError_t launch_small_attention(gs_dtype tin, gs_dtype to, const SmallArgs &a,
 hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s) {
     if (a.ntiles == 0) return hipSuccess;
     const dim3 grid((unsigned)a.ntiles), block(SROWS);
-    bool coords = false;
-    for (int i = 0; i < a.ngroups; ++i) coords = coords || a.g[i].T != nullptr;
-    if (!coords) {
+    if (!a.coords) {
         if (tin == GS_F32) hipLaunchKernelGGL((soft_gram_kernel<float>), grid, block, 0, s, a);
         else if (tin == GS_BF16) hipLaunchKernelGGL((soft_gram_kernel<bf16_t>), grid, block, 0, s, a);
         else return hipErrorInvalidValue;

@@ -33,6 +33,7 @@ GS_SIM_DOT, GS_SIM_COSINE = 0, 1
 GS_BIND_NONE, GS_BIND_MUL = 0, 1
 GS_BINDOP_MUL, GS_BINDOP_XOR, GS_BINDOP_CONV, GS_BINDOP_CORR = 0, 1, 2, 3
 GS_ECHELON = 0x100   # OR'ed into R's type: R[j, k] == 0 for k > j (as gs_compress returns it)
+GS_SOFT_AUTO, GS_SOFT_GRAM, GS_SOFT_COORDS = 0, 1, 2
 
 _DT = {torch.float32: GS_F32, torch.bfloat16: GS_BF16, torch.float64: GS_F64}
 
@@ -79,7 +80,7 @@ _SIGS["gs_bind_restored"] = ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ct
                      _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
 
 _SIGS["gs_soft_select"] = ([ctypes.POINTER(SoftGroup), ctypes.c_int, ctypes.c_int, ctypes.c_int,
-                            ctypes.c_int, ctypes.c_float, ctypes.c_float, _vp], ctypes.c_int)
+                            ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_int, _vp], ctypes.c_int)
 
 
 def lib():
@@ -320,9 +321,14 @@ def soft_groups(groups):
     return arr, pt, (tt if tt is not None else GS_F32)
 
 
-def gs_soft_select(groups, mode="cosine", scale: float = 1.0, beta: float = 1.0, prepared=None):
+_SOFT_FORMS = {"auto": GS_SOFT_AUTO, "gram": GS_SOFT_GRAM, "coords": GS_SOFT_COORDS}
+
+
+def gs_soft_select(groups, mode="cosine", scale: float = 1.0, beta: float = 1.0, prepared=None, form="auto"):
     """Fused prob2vec -> similarity/argmax -> attention over several small
     codebooks in one launch.  `groups` is a list of dicts (see soft_groups);
-    outputs named in the dicts are written in place."""
+    outputs named in the dicts are written in place.  form: 'coords' (t = p R
+    per row), 'gram' (scores through R R^T, no coordinates) or 'auto'."""
     arr, pt, tt = prepared if prepared is not None else soft_groups(groups)
-    _check(lib().gs_soft_select(arr, len(arr), pt, tt, _mode(mode), float(scale), float(beta), _stream()))
+    _check(lib().gs_soft_select(arr, len(arr), pt, tt, _mode(mode), float(scale), float(beta),
+                                _SOFT_FORMS[form], _stream()))

@@ -201,13 +201,13 @@ def test_empty_batch_accepts_null_buffers(L):
     assert L.gs_prob2vec(NULL, gsm.GS_F32, 0, 4, 4, NULL, gsm.GS_F32, 4, 4, NULL, gsm.GS_F32, 4, NULL) == gsm.GS_ERR_ARG
 
 
-def soft(L, groups, ngroups=None, pt=gsm.GS_F32, tt=gsm.GS_F32, mode=gsm.GS_SIM_COSINE):
+def soft(L, groups, ngroups=None, pt=gsm.GS_F32, tt=gsm.GS_F32, mode=gsm.GS_SIM_COSINE, form=gsm.GS_SOFT_AUTO):
     arr = (gsm.SoftGroup * max(1, len(groups)))()
     for i, g in enumerate(groups):
         for k, v in g.items():
             setattr(arr[i], k, v)
     n = len(groups) if ngroups is None else ngroups
-    return L.gs_soft_select(arr, n, pt, tt, mode, 1.0, 1.0, None)
+    return L.gs_soft_select(arr, n, pt, tt, mode, 1.0, 1.0, form, None)
 
 
 def group(**kw):
@@ -218,7 +218,9 @@ def group(**kw):
 
 
 def test_soft_select_validation(L):
-    assert L.gs_soft_select(None, 1, gsm.GS_F32, gsm.GS_F32, 1, 1.0, 1.0, None) == gsm.GS_ERR_ARG
+    assert L.gs_soft_select(None, 1, gsm.GS_F32, gsm.GS_F32, 1, 1.0, 1.0, gsm.GS_SOFT_AUTO, None) == gsm.GS_ERR_ARG
+    assert soft(L, [group()], form=3) == gsm.GS_ERR_ARG                  # unknown form
+    assert soft(L, [group(T=0x800000)], form=gsm.GS_SOFT_GRAM) == gsm.GS_ERR_ARG   # Gram form writes no T
     assert soft(L, [group()], ngroups=0) == gsm.GS_ERR_ARG
     assert soft(L, [group()] * 9) == gsm.GS_ERR_ARG                      # more than 8 groups
     assert soft(L, [group()], pt=gsm.GS_F64) == gsm.GS_ERR_DTYPE

@@ -15,7 +15,8 @@ import torch
 import oracle
 from paper_2608_01528_amd import gramspace as gsm
 from paper_2608_01528_amd import workloads as wl
-from tests.gpu_util import TOL_BF16, TOL_F32, check_argmax, dev, host, rowrel
+from tests.gpu_util import (TOL_BF16, TOL_F32, U32, check_argmax_bound, dev, exact_scores_bound, gamma, host,
+                            rowrel, score_bound, cosine_factor)
 
 pytestmark = pytest.mark.gpu
 
@@ -40,6 +41,57 @@ def rq_codebook(kind, M, D, seed, dup=0.0):
     if dup:
         C, _, _ = wl.duplicate_rows(C, dup, seed)
     return C
+
+
+def _name_early(dt):
+    return "bf16" if dt == torch.bfloat16 else "f32"
+
+
+def argmax_exact(idx, T, R, qnorm2=None, cnorm=None, mode="cosine", scale=1.0):
+    """The argmax against the oracle's exact scores of the values the kernel
+    read: T and R (upcast exactly), and the norms passed to it (None: summed
+    by the kernel from T or R).  Bit-exact outside twice the a-priori bound of
+    the fp32 evaluation; returns the near-tie count."""
+    cos = mode == "cosine"
+    given = (qnorm2 is not None and cnorm is not None) or not cos
+    Se, E = exact_scores_bound(T, R, qnorm2, cnorm, cosine=cos, scale=scale, norms_given=given)
+    return check_argmax_bound(host(idx) if torch.is_tensor(idx) else idx, Se, E)
+
+
+def soft_exact(P, R, cnorm=None, mode="cosine", scale=1.0):
+    """The oracle's exact scores of the fused soft selection's inputs P and R
+    (t = p R, s_j = scale * sim(t, R_j) with ||t|| from t), and the per-row
+    bound of the kernel's fp32 evaluation.  Both of the kernel's forms (t
+    formed, or scores through R R^T) sum p_k and R entries in fp32; their
+    error is at most (gamma_M + gamma_r) times ((|P| |R|) |R|^T) for the
+    inner products, and the norm of t carries (2 gamma_M + gamma_r) rho^2 +
+    gamma_M rho + gamma_r with rho = || |p| |R| || / ||t||."""
+    P = np.asarray(P, np.float64)
+    R = np.asarray(R, np.float64)
+    M, r = R.shape
+    T = oracle.prob2vec(P, R)
+    dot = oracle.similarity(T, R, oracle.DOT)
+    absT = oracle.prob2vec(np.abs(P), np.abs(R))
+    absdot = oracle.similarity(absT, np.abs(R), oracle.DOT)
+    gam = gamma(M) + gamma(r)
+    if mode == "cosine":
+        tn2 = (T * T).sum(1)
+        cn = np.sqrt((R * R).sum(1)) if cnorm is None else np.asarray(cnorm, np.float64)
+        factor = cosine_factor(tn2, cn, scale)
+        rho = np.sqrt((absT * absT).sum(1)) / np.maximum(np.sqrt(tn2), 1e-300)
+        rel = ((2 * gamma(M) + gamma(r)) * rho ** 2 + gamma(M) * rho + gamma(r) + 10 * U32)[:, None]
+    else:
+        factor = np.full(dot.shape, float(scale))
+        rel = 8 * U32
+    S = factor * dot
+    return S, score_bound(S, absdot, factor, gam, rel)
+
+
+def soft_argmax_exact(idx, P, R, cnorm=None, mode="cosine", scale=1.0):
+    """The fused soft selection's argmax against the oracle's exact scores of
+    its inputs (soft_exact): bit-exact outside the near-tie band."""
+    S, E = soft_exact(P, R, cnorm, mode, scale)
+    return check_argmax_bound(host(idx) if torch.is_tensor(idx) else idx, S, E)
 
 
 # ---------------------------------------------------------------- compress
@@ -225,7 +277,8 @@ def test_similarity(B, M, D, dup, in_span, mode):
     torch.cuda.synchronize()
     So = oracle.similarity(X, C, oracle.COSINE if mode == "cosine" else oracle.DOT, scale)
     assert rowrel(host(S), So) <= TOL_F32
-    check_argmax(host(idx), So)
+    argmax_exact(idx, host(dev(To)), host(dev(Ro)), None if qn is None else host(qn), None if cn is None else host(cn),
+                 mode, scale)
     # argmax alone (no score output) gives the same indices
     _, idx2 = gsm.gs_similarity(dev(To), dev(Ro), qnorm2=qn, cnorm=cn, mode=mode, scale=scale, scores=False)
     torch.cuda.synchronize()
@@ -260,9 +313,7 @@ def test_similarity_bf16():
     assert rowrel(host(S), So) <= TOL_BF16
     assert rowrel(host(A), oracle.softmax(So, 4.0)) <= TOL_BF16
     # argmax: exact against the oracle on the bf16-rounded inputs (coordinates)
-    cn = np.linalg.norm(Rb.astype(np.float64), axis=1)
-    Sb = (Tb.astype(np.float64) @ Rb.astype(np.float64).T) / np.sqrt(qn)[:, None] / cn[None, :]
-    check_argmax(host(idx), Sb)
+    argmax_exact(idx, Tb, Rb, host(dev(qn)), None)
 
 
 def test_argmax_ties_lowest_index():
@@ -347,7 +398,7 @@ def test_chain_tiny_workload(wname):
     So = oracle.similarity(V, C, oracle.COSINE)
     assert r == 10
     assert rowrel(host(S), So) <= TOL_F32
-    check_argmax(host(idx), So)
+    argmax_exact(idx, host(T), host(R), None, host(cnorm))
     assert rowrel(host(A), oracle.softmax(So, 16.0)) <= TOL_F32
     assert rowrel(host(X), V) <= TOL_F32
 
@@ -391,8 +442,8 @@ def test_dense_and_gram_similarity_agree(D):
     So = oracle.similarity(oracle.prob2vec(P, C), C, oracle.COSINE)
     assert rowrel(host(Sd), So) <= TOL_F32
     assert rowrel(host(Sg), So) <= TOL_F32
-    check_argmax(host(idd), So)
-    check_argmax(host(idg), So)
+    argmax_exact(idd, host(X), C, None, host(cn))
+    argmax_exact(idg, host(T), host(R), None, host(cn))
 
 
 @pytest.mark.parametrize("B,M,K,dtype", [(1, 40, 8192, torch.float32), (17, 1000, 300, torch.float32),
@@ -415,10 +466,10 @@ def test_few_rows_scores(B, M, K, dtype, norms):
     torch.cuda.synchronize()
     So = oracle.similarity(T, R, oracle.COSINE)
     assert rowrel(host(S), So) <= TOL_F32
-    check_argmax(host(idx), So)
+    argmax_exact(idx, T, R, None if qn is None else host(qn), None if cn is None else host(cn))
     Sdo = oracle.similarity(T, R, oracle.DOT, 0.25)
     assert rowrel(host(Sd), Sdo) <= TOL_F32
-    check_argmax(host(idd), Sdo)
+    argmax_exact(idd, T, R, mode="dot", scale=0.25)
     Ao = oracle.softmax(So, 12.0)
     assert rowrel(host(A), Ao) <= TOL_F32
     # weighted sum of the codebook rows, O = A R
@@ -455,13 +506,15 @@ def soft_outputs(books, want=("T", "S", "argmax", "A")):
     return groups
 
 
-@pytest.mark.parametrize("with_t", [True, False])
+@pytest.mark.parametrize("form", ["auto-T", "auto", "coords", "gram"])
 @pytest.mark.parametrize("mode,scale,beta", [("cosine", 1.0, 16.0), ("dot", 0.03, 1.0), ("cosine", 2.0, -3.0)])
-def test_soft_select(mode, scale, beta, with_t):
-    # without a coordinate output the kernel scores through the codebook's Gram matrix
+def test_soft_select(mode, scale, beta, form):
+    # auto-T: coordinates stored; auto and gram: scores through the codebook's
+    # Gram matrix; coords: coordinates formed per row, not stored
     books = soft_case([5, 6, 10, 22, 32], [1000, 257, 1, 513, 300], 1024, 40)
+    with_t = form == "auto-T"
     groups = soft_outputs(books, want=("T", "S", "argmax", "A") if with_t else ("S", "argmax", "A"))
-    gsm.gs_soft_select(groups, mode=mode, scale=scale, beta=beta)
+    gsm.gs_soft_select(groups, mode=mode, scale=scale, beta=beta, form=form.split("-")[0])
     torch.cuda.synchronize()
     m = oracle.COSINE if mode == "cosine" else oracle.DOT
     for b, g in zip(books, groups):
@@ -471,16 +524,17 @@ def test_soft_select(mode, scale, beta, with_t):
             assert rowrel(host(g["T"]), oracle.project(V, b["Qo"])) <= TOL_F32
         assert rowrel(host(g["S"]), So) <= TOL_F32
         assert rowrel(host(g["A"]), oracle.softmax(So, beta)) <= TOL_F32
-        check_argmax(host(g["argmax"]), So)
+        soft_argmax_exact(g["argmax"], host(b["Pd"]), host(b["Rd"]), None, mode, scale)
 
 
-def test_soft_select_strided_rows():
+@pytest.mark.parametrize("pdt", [torch.float32, torch.bfloat16], ids=_name_early)
+def test_soft_select_strided_rows(pdt):
     # probabilities and outputs as column slices of wider matrices (row
     # strides above M): element-wise tile moves instead of 16-byte pieces
-    books = soft_case([6, 22, 32], [300, 777, 40], 1024, 45)
+    books = soft_case([6, 22, 32], [300, 777, 40], 1024, 45, dtype=pdt)
     groups = []
     for b in books:
-        Pw = torch.full((b["B"], b["M"] + 3), np.nan, device="cuda")
+        Pw = torch.full((b["B"], b["M"] + 3), np.nan, device="cuda", dtype=pdt)
         Pw[:, : b["M"]] = b["Pd"]
         Sw = torch.full((b["B"], b["M"] + 5), np.nan, device="cuda")
         Aw = torch.full((b["B"], b["M"] + 1), np.nan, device="cuda")
@@ -490,12 +544,19 @@ def test_soft_select_strided_rows():
     gsm.gs_soft_select([{k: v for k, v in g.items() if not k.startswith("_")} for g in groups],
                        mode="cosine", beta=16.0)
     torch.cuda.synchronize()
+    tol = TOL_F32 if pdt == torch.float32 else TOL_BF16
     for b, g in zip(books, groups):
         V = oracle.prob2vec(b["P"], b["C"])
         So = oracle.similarity(V, b["C"], oracle.COSINE)
-        assert rowrel(host(g["S"]), So) <= TOL_F32
-        assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
-        check_argmax(host(g["argmax"]), So)
+        assert rowrel(host(g["S"]), So) <= tol
+        # the weights against the softmax of the exact scores of the values
+        # the kernel read (a softmax of 16 s multiplies the bf16 rounding of
+        # the inputs by up to 32 in the weights)
+        Se, _ = soft_exact(host(b["Pd"]), host(b["Rd"]))
+        assert rowrel(host(g["A"]), oracle.softmax(Se, 16.0)) <= TOL_F32
+        if pdt == torch.float32:
+            assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
+        soft_argmax_exact(g["argmax"], host(b["Pd"]), host(b["Rd"]))
         # the padding columns of the output rows are untouched
         assert torch.isnan(g["_S"][:, b["M"]:]).all() and torch.isnan(g["_A"][:, b["M"]:]).all()
 
@@ -510,11 +571,54 @@ def test_soft_select_bf16_and_partial_outputs():
         So = oracle.similarity(V, b["C"], oracle.COSINE)
         assert rowrel(host(g["A"]), oracle.softmax(So, 4.0)) <= TOL_BF16
         # argmax against the oracle on the bf16-rounded inputs
-        Pb = wl.round_bf16(b["P"]).astype(np.float64)
-        Rb = wl.round_bf16(b["Ro"].astype(np.float32)).astype(np.float64)
-        Tb = Pb @ Rb
-        Sb = (Tb @ Rb.T) / np.linalg.norm(Tb, axis=1)[:, None] / np.linalg.norm(Rb, axis=1)[None, :]
-        check_argmax(host(g["argmax"]), Sb)
+        soft_argmax_exact(g["argmax"], host(b["Pd"]), host(b["Rd"]))
+
+
+@pytest.mark.parametrize("tdt", [torch.float32, torch.bfloat16], ids=_name_early)
+@pytest.mark.parametrize("form", ["auto", "coords"])
+def test_soft_select_bf16_with_coordinates(tdt, form):
+    # bf16 probabilities with a coordinate output of either type, ragged
+    # batches whose waves end off an 8-value boundary (M = 22, B = 450;
+    # M = 5 and 10 with B = 1000 and 257), and one group without T
+    books = soft_case([22, 5, 10, 6], [450, 1000, 257, 333], 1024, 55, dtype=torch.bfloat16)
+    groups = soft_outputs(books)
+    for b, g in zip(books, groups):
+        g["T"] = torch.full((b["B"], b["r"]), np.nan, device="cuda", dtype=tdt)
+    del groups[3]["T"]
+    gsm.gs_soft_select(groups, mode="cosine", beta=16.0, form=form)
+    torch.cuda.synchronize()
+    for i, (b, g) in enumerate(zip(books, groups)):
+        V = oracle.prob2vec(b["P"], b["C"])
+        So = oracle.similarity(V, b["C"], oracle.COSINE)
+        assert rowrel(host(g["S"]), So) <= TOL_BF16
+        Se, _ = soft_exact(host(b["Pd"]), host(b["Rd"]))
+        assert rowrel(host(g["A"]), oracle.softmax(Se, 16.0)) <= TOL_F32
+        if "T" in g:
+            Tg = host(g["T"])
+            assert np.isfinite(Tg).all()
+            # against the dense definition on the original inputs ...
+            assert rowrel(Tg, oracle.project(V, b["Qo"])) <= TOL_BF16
+            # ... and, to fp32 accumulation (one rounding to bf16 on top), on
+            # the bf16 values the kernel read
+            To = oracle.prob2vec(host(b["Pd"]), host(b["Rd"]))
+            assert rowrel(Tg, To) <= (1e-5 if tdt == torch.float32 else 8e-3)
+        soft_argmax_exact(g["argmax"], host(b["Pd"]), host(b["Rd"]))
+
+
+def test_soft_select_forms_agree():
+    # the Gram form and the coordinate form compute the same scores up to
+    # rounding order, and the same argmax outside the near-tie band
+    books = soft_case([5, 6, 10, 22], [4096, 4096, 4096, 4096], 1024, 57)
+    out = {}
+    for form in ("gram", "coords"):
+        groups = soft_outputs(books, want=("S", "argmax", "A"))
+        gsm.gs_soft_select(groups, mode="cosine", beta=16.0, form=form)
+        out[form] = groups
+    torch.cuda.synchronize()
+    for b, g0, g1 in zip(books, out["gram"], out["coords"]):
+        assert rowrel(host(g0["S"]), host(g1["S"])) <= 1e-5
+        soft_argmax_exact(g0["argmax"], host(b["Pd"]), host(b["Rd"]))
+        soft_argmax_exact(g1["argmax"], host(b["Pd"]), host(b["Rd"]))
 
 
 def test_soft_select_matches_separate_calls():
@@ -533,11 +637,10 @@ def test_soft_select_matches_separate_calls():
         assert rowrel(host(g["A"]), host(A)) <= 2 * 16.0 * 1e-6
 
 
-@pytest.mark.parametrize("with_t", [False, True])
-def test_soft_select_full_vsa_workload(with_t):
+@pytest.mark.parametrize("form", ["gram", "coords", "auto-T"])
+def test_soft_select_full_vsa_workload(form):
     # the benchmark's workload at full size and launch configuration (GPU
-    # compress, then one fused launch over the four attribute codebooks; the
-    # benchmark keeps the coordinates on chip)
+    # compress, then one fused launch over the four attribute codebooks)
     w = wl.WORKLOADS["vsa"]
     groups, ref = [], []
     for i, M in enumerate(w.Ms):
@@ -547,11 +650,11 @@ def test_soft_select_full_vsa_workload(with_t):
         assert r == M
         g = {"P": dev(P), "R": R.contiguous(), "cnorm": cnorm, "S": torch.empty((w.B, M), device="cuda"),
              "argmax": torch.empty(w.B, dtype=torch.int32, device="cuda"), "A": torch.empty((w.B, M), device="cuda")}
-        if with_t:
+        if form == "auto-T":
             g["T"] = torch.empty((w.B, r), device="cuda")
         groups.append(g)
         ref.append((C, P))
-    gsm.gs_soft_select(groups, mode="cosine", beta=16.0)
+    gsm.gs_soft_select(groups, mode="cosine", beta=16.0, form=form.split("-")[0])
     torch.cuda.synchronize()
     near = 0
     for (C, P), g in zip(ref, groups):
@@ -559,7 +662,7 @@ def test_soft_select_full_vsa_workload(with_t):
         So = oracle.similarity(V, C, oracle.COSINE)
         assert rowrel(host(g["S"]), So) <= TOL_F32
         assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
-        near += check_argmax(host(g["argmax"]), So)
+        near += soft_argmax_exact(g["argmax"], P, host(g["R"]), host(g["cnorm"]))
     print("near-ties:", near)
 
 
@@ -639,7 +742,9 @@ def test_bf16_pipelined_prob2vec_similarity(B, M, D):
     assert np.isfinite(host(S)).all() and np.isfinite(host(A)).all()
     assert rowrel(host(S), So) <= TOL_BF16
     assert rowrel(host(A), oracle.softmax(So, 8.0)) <= TOL_BF16
-    check_argmax(host(idx), So, band_rel=1e-2)
+    # argmax: the oracle's exact scores of the bf16 coordinates and codebook
+    # coordinates the kernel read (||x||^2 given, ||R_j|| summed by the kernel)
+    argmax_exact(idx, Tx, Rb, host(qn), None)
 
 
 # --------------------- large-tile path (>= 256 tiles of 256 x 256), bf16 and fp32
@@ -846,7 +951,7 @@ def test_sweep_similarity_cosine(sweep_case, norms):
     Sg = host(S[rows])
     assert np.isfinite(Sg).all()
     assert rowrel(Sg, So) <= TOL_F32
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R, None if qn is None else host(qn[rows]), None if cn is None else host(cn))
     # whole batch: the returned index points at a maximal score of its row
     Sf = S.float()
     assert torch.all(Sf.gather(1, idx.long()[:, None])[:, 0] >= Sf.max(dim=1).values).item()
@@ -857,8 +962,7 @@ def test_sweep_similarity_dot_argmax_only(sweep_case):
     print("sweep similarity dot argmax", Td.dtype, flush=True)
     _, idx = gsm.gs_similarity(Td, Rd, mode="dot", scale=0.5, scores=False)
     torch.cuda.synchronize()
-    So = oracle.similarity(T[rows], R, oracle.DOT, 0.5)
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R, mode="dot", scale=0.5)
 
 
 @pytest.mark.parametrize("norms", ["computed", "given"])
@@ -884,8 +988,7 @@ def test_sweep_cosine_argmax_only(sweep_case):
     print("sweep cosine argmax", Td.dtype, flush=True)
     _, idx = gsm.gs_similarity(Td, Rd, mode="cosine", scores=False)
     torch.cuda.synchronize()
-    So = oracle.similarity(T[rows], R, oracle.COSINE)
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R)
 
 
 # ---------- whole rows in one 256-column tile: row argmax / softmax in the epilogue
@@ -924,7 +1027,7 @@ def test_whole_row_similarity_cosine(rows_case, norms):
     Sg = host(S[rows])
     assert np.isfinite(Sg).all()
     assert rowrel(Sg, So) <= TOL_F32
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R, None if qn is None else host(qn[rows]), None if cn is None else host(cn))
     # every row: the index is the first maximum of the stored scores
     assert torch.equal(idx.long(), torch.argmax(S, dim=1))
 
@@ -936,7 +1039,7 @@ def test_whole_row_similarity_dot(rows_case):
     torch.cuda.synchronize()
     So = oracle.similarity(T[rows], R, oracle.DOT, 0.25)
     assert rowrel(host(S[rows]), So) <= TOL_F32
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R, mode="dot", scale=0.25)
     assert torch.equal(idx.long(), torch.argmax(S, dim=1))
 
 
@@ -948,8 +1051,7 @@ def test_whole_row_argmax_only(rows_case, mode):
     print("whole-row argmax only", Td.dtype, R.shape[0], mode, flush=True)
     _, idx = gsm.gs_similarity(Td, Rd, mode=mode, scale=0.5, scores=False)
     torch.cuda.synchronize()
-    So = oracle.similarity(T[rows], R, oracle.COSINE if mode == "cosine" else oracle.DOT, 0.5)
-    check_argmax(host(idx[rows]), So, band_rel=1e-4)
+    argmax_exact(idx[rows], T[rows], R, mode=mode, scale=0.5)
     S, idx2 = gsm.gs_similarity(Td, Rd, mode=mode, scale=0.5)
     assert torch.equal(idx, idx2)
 
@@ -1030,7 +1132,7 @@ def test_echelon_similarity(op_dtype, mode):
     Sg = host(S2[rows])
     assert np.isfinite(Sg).all()
     assert rowrel(Sg, So) <= TOL_F32
-    check_argmax(host(i2[rows]), So, band_rel=1e-4)
+    argmax_exact(i2[rows], T[rows], R, host(qn[rows]), None, mode=mode, scale=0.5)
 
 
 def test_echelon_similarity_norms_from_t_keep_full_range():
@@ -1105,7 +1207,7 @@ def test_echelon_on_compressed_rank_deficient_codebook():
     assert rowrel(host(T1[rows]), oracle.project(oracle.prob2vec(P[rows], C), Qo)) <= TOL_F32
     So = oracle.similarity(X[rows], C, oracle.COSINE)
     assert rowrel(host(S1[rows]), So) <= TOL_F32
-    check_argmax(host(i1[rows]), So, band_rel=1e-4)
+    argmax_exact(i1[rows], host(Tx[rows]), host(R), host(xn[rows]), host(cn))
 
 
 # ---------------------------- more entries than dimensions (D < M): partitioned bases
