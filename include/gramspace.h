@@ -28,9 +28,11 @@
  * Memory and ownership.  Every matrix argument is a device pointer (HIP
  * device memory of the current device) unless marked HOST.  The caller
  * allocates every buffer, including workspace; the library allocates no
- * device memory and never frees caller memory.  Besides a thread-local error
- * message it keeps two process-wide caches: whether a HIP device exists, and
- * which of its kernels have had their LDS limit raised.  Inputs are
+ * device memory and never frees caller memory (the one exception is the
+ * static scratch array of gs_compress_noalloc, part of the loaded code
+ * object).  Besides a thread-local error message it keeps three process-wide
+ * caches: whether a HIP device exists, which of its kernels have had their
+ * LDS limit raised, and the device address of each GPU's scratch array.  Inputs are
  * read-only.  Outputs must not overlap inputs or each other (GS_ERR_ARG).
  *
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
@@ -149,6 +151,29 @@ gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t 
                       void *R, gs_dtype rt, int64_t ldr,
                       int32_t *kept, float *cnorm, int32_t *rank,
                       void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * gs_compress_noalloc -- gs_compress for callers that cannot allocate device
+ * memory (code under stream capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation and arguments without the
+ * workspace, which comes instead from a static array of
+ * GS_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * (from the first call on that device until the process ends).  The call
+ * allocates nothing.  Codebooks whose workspace, gs_compress_workspace(M, D),
+ * exceeds the array are rejected with GS_ERR_WORKSPACE (64 MiB: e.g. up to
+ * 1000 x 4096 or 256 x 8192 in fp64 working precision).  All calls on one GPU
+ * share its array: calls that overlap in time on the same GPU (other threads,
+ * other streams) race and give undefined results; each call initialises what
+ * it needs, so consecutive calls are independent.  The scratch memory is the
+ * current device's.
+ */
+#define GS_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+gs_status gs_compress_noalloc(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
+                              double tol,
+                              void *Q, gs_dtype qt, int64_t ldq,
+                              void *R, gs_dtype rt, int64_t ldr,
+                              int32_t *kept, float *cnorm, int32_t *rank, void *stream);
 
 /*
  * gs_project -- Gram-loc of a batch (Sec. 3.1: t = U^T x):  T = X Q^T.

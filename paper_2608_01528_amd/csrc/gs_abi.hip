@@ -2,6 +2,7 @@
 // reporting and dispatch to the kernels.  Every check runs on the host before
 // any HIP call, so a rejected call touches neither the device nor its outputs.
 #include <atomic>
+#include <mutex>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -124,42 +125,119 @@ size_t gs_compress_workspace(int64_t M, int64_t D) {
     return compress_workspace(M, D);
 }
 
-gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
-                      void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
-                      int32_t *kept, float *cnorm, int32_t *rank, void *ws, size_t ws_bytes,
-                      void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by gs_compress and gs_compress_noalloc (everything but the
+// workspace).
+gs_status check_compress(const char *fn, const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
+                         double tol, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
+                         int32_t *kept, float *cnorm, int32_t *rank, const Span &ws_span) {
     if (!valid_dtype(ct) || !valid_dtype(qt) || !valid_dtype(rt))
-        return fail(GS_ERR_DTYPE, "gs_compress: unknown element type");
-    if (!rank) return fail(GS_ERR_ARG, "gs_compress: rank (host) is null");
-    if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "gs_compress: M and D must be >= 1 (M=%lld, D=%lld)",
+        return fail(GS_ERR_DTYPE, "%s: unknown element type", fn);
+    if (!rank) return fail(GS_ERR_ARG, "%s: rank (host) is null", fn);
+    if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "%s: M and D must be >= 1 (M=%lld, D=%lld)", fn,
                                     (long long)M, (long long)D);
-    if (M > D) return fail(GS_ERR_SHAPE, "gs_compress: M=%lld > D=%lld needs partitioned bases, not supported",
-                           (long long)M, (long long)D);
-    if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "gs_compress: tol must be in [0, 1)");
+    if (M > D) return fail(GS_ERR_SHAPE, "%s: M=%lld > D=%lld needs partitioned bases, not supported",
+                           fn, (long long)M, (long long)D);
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "%s: tol must be in [0, 1)", fn);
     GS_CHECK(check_matrix(C, "C", M, D, ldc, ct, false));
     GS_CHECK(check_matrix(Q, "Q", M, D, ldq, qt, false));
     GS_CHECK(check_matrix(R, "R", M, M, ldr, rt, false));
     GS_CHECK(check_aligned(kept, 4, "kept"));
     GS_CHECK(check_aligned(cnorm, 4, "cnorm"));
+    const Span sC = span(C, M, D, ldc, esize(ct), "C");
+    GS_CHECK(check_overlaps({sC, ws_span}, {span(Q, M, D, ldq, esize(qt), "Q"), span(R, M, M, ldr, esize(rt), "R"),
+                                           span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    return GS_OK;
+}
+
+gs_status finish_compress(const char *fn, hipError_t e, int nonfinite, int32_t r, int32_t *rank) {
+    if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: %s", fn, hipGetErrorString(e));
+    if (nonfinite) return fail(GS_ERR_NUMERIC, "%s: codebook holds a NaN or infinity", fn);
+    *rank = r;
+    return ok();
+}
+
+// Scratch memory of gs_compress_noalloc: one array per GPU, held by the
+// loaded code object until the process ends.  Host code never uses the
+// array's name as an address: its device address is looked up once per
+// device (with that device current) and kept in scratch_ptr.
+constexpr size_t kScratchBytes = (size_t)GS_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+gs_status scratch_for_current_device(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(GS_ERR_DEVICE, "gs_compress_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(GS_ERR_DEVICE, "gs_compress_noalloc: device %d beyond the %d supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(GS_ERR_DEVICE, "gs_compress_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return GS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                      void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
+                      int32_t *kept, float *cnorm, int32_t *rank, void *ws, size_t ws_bytes,
+                      void *stream) {
+    GS_CHECK(check_compress("gs_compress", C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm, rank,
+                            Span{}));
     if (!ws) return fail(GS_ERR_WORKSPACE, "gs_compress: workspace is null");
     if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
         return fail(GS_ERR_ALIGN, "gs_compress: workspace must be 256-byte aligned");
     const size_t need = compress_workspace(M, D);
     if (ws_bytes < need)
         return fail(GS_ERR_WORKSPACE, "gs_compress: workspace of %zu bytes, %zu needed", ws_bytes, need);
-    const Span sC = span(C, M, D, ldc, esize(ct), "C");
-    const Span sW = span(ws, 1, (int64_t)need, (int64_t)need, 1, "workspace");
-    GS_CHECK(check_overlaps({sC, sW}, {span(Q, M, D, ldq, esize(qt), "Q"), span(R, M, M, ldr, esize(rt), "R"),
-                                       span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    {
+        // the workspace overlaps neither the codebook nor an output
+        const Span sW = span(ws, 1, (int64_t)need, (int64_t)need, 1, "workspace");
+        GS_CHECK(check_overlaps({sW}, {span(C, M, D, ldc, esize(ct), "C"), span(Q, M, D, ldq, esize(qt), "Q"),
+                                       span(R, M, M, ldr, esize(rt), "R"), span(kept, 1, M, M, 4, "kept"),
+                                       span(cnorm, 1, M, M, 4, "cnorm")}));
+    }
     GS_CHECK(check_device());
     int nonfinite = 0;
     int32_t r = 0;
     hipError_t e = run_compress(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
                                 &nonfinite, ws, (hipStream_t)stream);
-    if (e != hipSuccess) return fail(GS_ERR_DEVICE, "gs_compress: %s", hipGetErrorString(e));
-    if (nonfinite) return fail(GS_ERR_NUMERIC, "gs_compress: codebook holds a NaN or infinity");
-    *rank = r;
-    return ok();
+    return finish_compress("gs_compress", e, nonfinite, r, rank);
+}
+
+gs_status gs_compress_noalloc(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                              void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
+                              int32_t *kept, float *cnorm, int32_t *rank, void *stream) {
+    GS_CHECK(check_compress("gs_compress_noalloc", C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm,
+                            rank, Span{}));
+    const size_t need = compress_workspace(M, D);
+    if (need > kScratchBytes)
+        return fail(GS_ERR_WORKSPACE, "gs_compress_noalloc: a %lld x %lld codebook needs %zu bytes of scratch, "
+                    "beyond the %zu of the library's static array (use gs_compress with a workspace)",
+                    (long long)M, (long long)D, need, kScratchBytes);
+    GS_CHECK(check_device());
+    void *ws = nullptr;
+    GS_CHECK(scratch_for_current_device(&ws));
+    int nonfinite = 0;
+    int32_t r = 0;
+    hipError_t e = run_compress(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
+                                &nonfinite, ws, (hipStream_t)stream);
+    return finish_compress("gs_compress_noalloc", e, nonfinite, r, rank);
 }
 
 gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,

@@ -4,7 +4,7 @@ Two layers with the C names:
 
 * `lib()` returns the loaded shared library; its `gs_*` functions take raw
   pointers exactly as declared in the header.
-* `gs_compress`, `gs_project`, `gs_prob2vec`, `gs_similarity`,
+* `gs_compress`, `gs_compress_noalloc`, `gs_project`, `gs_prob2vec`, `gs_similarity`,
   `gs_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
   below take torch tensors on the current
   GPU, allocate the outputs with torch, and pass pointers, sizes and the
@@ -55,6 +55,9 @@ _SIGS = {
     "gs_compress": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double,
                      _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
                      _vp, _vp, _i32p, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "gs_compress_noalloc": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double,
+                             _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
+                             _vp, _vp, _i32p, _vp], ctypes.c_int),
     "gs_project": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
                     _vp, ctypes.c_int, _i64, _vp, _vp], ctypes.c_int),
     "gs_prob2vec": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
@@ -164,6 +167,28 @@ def gs_compress(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dt
     _check(lib().gs_compress(_ptr(C), ct, M, D, ldc, float(tol), _ptr(Q), _DT[q_dtype], Q.stride(0),
                              _ptr(R), _DT[r_dtype], R.stride(0), _ptr(kept), _ptr(cnorm), ctypes.byref(rank),
                              ctypes.c_void_p(base + off), workspace.numel() - off, _stream()))
+    r = rank.value
+    return Q[:r], R[:, :r], r, kept[:r], cnorm
+
+
+def gs_compress_noalloc(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dtype=torch.float64,
+                        out=None):
+    """gs_compress without a workspace (the library's static scratch array).
+    `out` = (Q, R, kept, cnorm) full-capacity buffers (Q M x D, R M x M) to
+    write into; allocated here when None.  Returns (Q, R, rank, kept, cnorm)
+    as gs_compress does."""
+    ct, ldc = _mat(C, "C")
+    M, D = C.shape
+    dev = C.device
+    if out is None:
+        out = (alloc_rows(M, D, q_dtype, dev), alloc_rows(M, M, r_dtype, dev),
+               torch.empty(M, dtype=torch.int32, device=dev), torch.empty(M, dtype=torch.float32, device=dev))
+    Q, R, kept, cnorm = out
+    qt, ldq = _mat(Q, "Q")
+    rt, ldr = _mat(R, "R")
+    rank = ctypes.c_int32(0)
+    _check(lib().gs_compress_noalloc(_ptr(C), ct, M, D, ldc, float(tol), _ptr(Q), qt, ldq, _ptr(R), rt, ldr,
+                                     _ptr(kept), _ptr(cnorm), ctypes.byref(rank), _stream()))
     r = rank.value
     return Q[:r], R[:, :r], r, kept[:r], cnorm
 

@@ -90,6 +90,30 @@ def test_compress_validation(L):
     assert compress(L, kept=P(0x20000000 + 8)) == gsm.GS_ERR_ARG            # kept inside Q
 
 
+def compress_noalloc(L, C=A1, ct=gsm.GS_F32, M=10, D=64, ldc=64, tol=1e-10, Q=A2, qt=gsm.GS_F64, ldq=64,
+                     R=A3, rt=gsm.GS_F64, ldr=10, kept=NULL, cnorm=NULL, rank=True):
+    rk = ctypes.c_int32(0)
+    return L.gs_compress_noalloc(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm,
+                                 ctypes.byref(rk) if rank else None, None)
+
+
+def test_compress_noalloc_validation(L):
+    # the same argument checks as gs_compress ...
+    assert compress_noalloc(L, ct=7) == gsm.GS_ERR_DTYPE
+    assert compress_noalloc(L, rank=False) == gsm.GS_ERR_ARG
+    assert compress_noalloc(L, M=65, ldr=65) == gsm.GS_ERR_SHAPE
+    assert compress_noalloc(L, ldc=63) == gsm.GS_ERR_SHAPE
+    assert compress_noalloc(L, Q=A1) == gsm.GS_ERR_ARG and "overlaps" in err(L)
+    # ... and codebooks whose workspace exceeds the static array are refused
+    # before any device work
+    big = L.gs_compress_workspace(2048, 16384)
+    assert big > (64 << 20)
+    assert compress_noalloc(L, M=2048, D=16384, ldc=16384, ldq=16384, ldr=2048, Q=P(0x100000000),
+                            R=P(0x200000000)) == gsm.GS_ERR_WORKSPACE
+    assert "scratch" in err(L)
+    assert L.gs_compress_workspace(1000, 4096) <= (64 << 20)        # the binary workload's codebook fits
+
+
 def test_project_validation(L):
     f = L.gs_project
     # dtype mismatch X f32 / Q bf16
