@@ -155,7 +155,8 @@ gs_status check_compress(const char *fn, const void *C, gs_dtype ct, int64_t M, 
 
 gs_status finish_compress(const char *fn, hipError_t e, int nonfinite, int32_t r, int32_t *rank) {
     if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: %s", fn, hipGetErrorString(e));
-    if (nonfinite) return fail(GS_ERR_NUMERIC, "%s: codebook holds a NaN or infinity", fn);
+    if (nonfinite & 1) return fail(GS_ERR_NUMERIC, "%s: codebook holds a NaN or infinity", fn);
+    if (nonfinite) return fail(GS_ERR_NUMERIC, "%s: the orthogonalisation broke down", fn);
     *rank = r;
     return ok();
 }

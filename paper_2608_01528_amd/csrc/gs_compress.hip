@@ -1,58 +1,119 @@
-// Gram-Space compression on the GPU: blocked modified Gram-Schmidt with one
-// re-orthogonalisation pass and a relative rank threshold, in fp64.
+// Gram-Space compression on the GPU: block Gram-Schmidt with
+// re-orthogonalisation and a relative rank threshold, in fp64.
 //
 // The paper builds the basis U and the Gram-loc codebook T = U^T W by
 // Gram-Schmidt at initialisation (Sec. 3.3), with k the algebraic rank of the
-// codebook (Sec. 3.2).  Here codebook rows are processed in panels of PB rows.
-// Each panel is first orthogonalised against every basis vector built from
-// earlier panels (two block passes: coefficients H = W_p Q^T, then
-// W_p -= H Q), then row by row against the basis vectors created inside the
-// panel (two passes each).  A row whose remaining norm is <= tol * ||c_i||
-// after both passes is dependent; otherwise it is normalised into the next
-// basis vector.  The coefficients of both passes are summed into R, which
-// gives R[i, k] = <c_i, q_k> and a positive pivot for kept rows.
+// codebook (Sec. 3.2).  Codebook rows are taken in panels of PB rows, in index
+// order.  For each panel W (pb x D):
 //
-// The running rank lives on the device (rank_after[i] = rank once row i is
+//  1. first pass against the basis Q built from earlier panels (r_old rows):
+//     H1 = W Q^T (its coefficients, into R), W -= H1 Q;
+//  2. the rows of the panel are orthogonalised among themselves in the small
+//     space of the panel's triangular factor: W^T = Q_t R_t by a tree of
+//     Householder factorisations (TSQR), so the columns a_i of R_t have the
+//     inner products of the rows w_i.  Gram-Schmidt with one
+//     re-orthogonalisation pass runs on those 32-entry columns in index order;
+//     row i is dependent when the norm of what is left of it is
+//     <= tol * ||c_i||, otherwise it adds a basis vector.  Each new basis
+//     vector is a combination of the panel's rows: V = X1 W;
+//  3. second pass on the new vectors: H2 = V Q^T, V -= H2 Q, then V is
+//     re-orthonormalised within itself (Cholesky of its Gram matrix, which is
+//     the identity up to rounding at this point): Q_new = L^-1 V;
+//  4. R of the panel's rows: R[i, old] = H1 + C1 H2 and R[i, new] = C1 L, with
+//     C1 the small-space coefficients of step 2 (C1[i][k] = <w_i, v_k>).
+//
+// The result is the unique factorisation of the row-wise rules (rows in index
+// order, first occurrence of a direction kept, positive pivots), so it is the
+// one a Householder factorisation with column skipping returns.  The products
+// with the basis run on fp64 matrix cores (v_mfma_f64_16x16x4f64).  The
+// running rank lives on the device (rank_after[i] = rank once row i is
 // done), so no launch waits on the host; grids are sized for the largest rank
 // possible at that point and surplus work-groups exit.  Every reduction has a
 // fixed order (no atomics), so results are bitwise reproducible.
+#include <utility>
+
 #include "gs_internal.h"
 
 namespace gs {
 namespace {
 
 constexpr int PB = 32;        // panel rows
-constexpr int DCH = 512;      // D-chunk of a panel coefficient work-group
-constexpr int ICH = 1024;     // D-chunk of the in-panel kernels (256 thr x 4)
-constexpr int NT = 256;
+constexpr int NT = 256;       // threads of the panel kernels
+constexpr int TCH = 256;      // rows of a TSQR node: panel columns of a leaf, or 8 stacked factors
+constexpr int TFAN = TCH / PB;
+constexpr int BK = 512;       // D-chunk of the split products W Q^T
+constexpr int KS = 64;        // K-step staged in LDS by the matrix-core products
+constexpr int BN = 64;        // basis vectors (dots) or columns (update) per work-group
+constexpr int LDK = KS + 1;   // LDS row stride (odd in doubles)
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+
+// Row-count sources of the panel kernels: the panel's rows, the basis rows
+// built before the panel, or the new basis vectors of the panel.
+enum Rows { ROWS_PANEL = 0, ROWS_OLD = 1, ROWS_NEW = 2, ROWS_OLD_PASS2 = 3 };
+
+// Second pass against the earlier basis: needed only where the first pass
+// can have left the new vectors measurably off orthogonal to it.  A new
+// vector v = sum_i X1[i] w_i inherits each w_i's rounding-level component
+// along the earlier basis (about eps ||c_i||) weighted by |X1[i]|, so the
+// pass runs when some sum_i |X1[i]| ||c_i|| exceeds PASS2_WEIGHT (a vector
+// made from rows that were each at least about 1/PASS2_WEIGHT of their norm
+// away from the earlier span needs none).
+constexpr double PASS2_WEIGHT = 8.0;
 
 struct WsLayout {
-    size_t qm, wp, hc, hb, part, part2, part3, cn, rank_after, kept, flag, total;
+    size_t qm, wp, w2, hc, h2, g2, part, gpart, tsq0, tsq1, x1, c1, lx, cn, rank_after, kept, flag, pass2, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+int64_t leaf_count(int64_t D) { return (D + TCH - 1) / TCH; }
+int64_t chunk_count(int64_t D) { return (D + BK - 1) / BK; }
+
 WsLayout layout(int64_t M, int64_t D) {
     WsLayout L;
-    const int64_t nch = (D + DCH - 1) / DCH, nch2 = (D + ICH - 1) / ICH;
+    const int64_t nch = chunk_count(D), nl = leaf_count(D);
     size_t o = 0;
     L.qm = o;    o = align256(o + sizeof(double) * M * D);
     L.wp = o;    o = align256(o + sizeof(double) * PB * D);
+    L.w2 = o;    o = align256(o + sizeof(double) * PB * D);
     L.hc = o;    o = align256(o + sizeof(double) * M * M);
-    L.hb = o;    o = align256(o + sizeof(double) * PB * M);
-    L.part = o;  o = align256(o + sizeof(double) * nch * PB * M);
-    L.part2 = o; o = align256(o + sizeof(double) * nch2 * PB);
-    L.part3 = o; o = align256(o + sizeof(double) * nch2);
+    L.h2 = o;    o = align256(o + sizeof(double) * PB * M);
+    L.g2 = o;    o = align256(o + sizeof(double) * PB * PB);
+    L.part = o;  o = align256(o + sizeof(double) * nch * PB * (M > PB ? M : PB));
+    L.gpart = o; o = align256(o + sizeof(double) * ((D + BN - 1) / BN) * PB * PB);
+    L.tsq0 = o;  o = align256(o + sizeof(double) * nl * PB * PB);
+    L.tsq1 = o;  o = align256(o + sizeof(double) * nl * PB * PB);
+    L.x1 = o;    o = align256(o + sizeof(double) * PB * PB);
+    L.c1 = o;    o = align256(o + sizeof(double) * PB * PB);
+    L.lx = o;    o = align256(o + sizeof(double) * 2 * PB * PB);
     L.cn = o;    o = align256(o + sizeof(double) * M);
     L.rank_after = o; o = align256(o + sizeof(int32_t) * M);
     L.kept = o;  o = align256(o + sizeof(int32_t) * M);
     L.flag = o;  o = align256(o + sizeof(int32_t));
+    L.pass2 = o; o = align256(o + sizeof(int32_t));
     L.total = o;
     return L;
 }
 
+// Device view of the panel being processed.
+struct Panel {
+    int64_t i0;                 // first codebook row of the panel
+    int pb;                     // rows in the panel
+    const int32_t *rank_after;  // running rank
+    const int32_t *pass2;       // set by the rank decisions: the second pass is needed
+};
+
 __device__ __forceinline__ int rank_before(const int32_t *rank_after, int64_t row) {
     return row == 0 ? 0 : rank_after[row - 1];
+}
+
+__device__ __forceinline__ int rows_of(const Panel &p, int which) {
+    const int r_old = rank_before(p.rank_after, p.i0);
+    if (which == ROWS_PANEL) return p.pb;
+    if (which == ROWS_OLD) return r_old;
+    if (which == ROWS_OLD_PASS2) return *p.pass2 ? r_old : 0;
+    return p.rank_after[p.i0 + p.pb - 1] - r_old;   // ROWS_NEW: valid after the panel's rank decisions
 }
 
 template <typename T> __device__ __forceinline__ double ld_f64(const T *p, int64_t i);
@@ -75,6 +136,26 @@ __device__ double block_sum(double v, double *red) {
     return s;
 }
 
+// Cross-lane moves of a double within a row of 16 lanes by DPP (no LDS
+// round trip): the two 32-bit halves move alike.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffLL), CTRL, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xf, 0xf, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// Sum over the 8 lanes of an aligned group; every lane gets the same value
+// (each pairing adds the same two operands on both lanes): quad_perm swaps
+// within quads (xor 1, xor 2), then row_half_mirror pairs lane i with 7 - i.
+__device__ __forceinline__ double group8_sum(double v) {
+    v += dpp_f64<0xB1>(v);     // quad_perm [1, 0, 3, 2]
+    v += dpp_f64<0x4E>(v);     // quad_perm [2, 3, 0, 1]
+    v += dpp_f64<0x141>(v);    // row_half_mirror
+    return v;
+}
+
 __global__ void k_init(double *hc, int64_t nhc, int32_t *kept, int32_t *rank_after, int64_t M,
                        int32_t *flag) {
     const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
@@ -84,211 +165,604 @@ __global__ void k_init(double *hc, int64_t nhc, int32_t *kept, int32_t *rank_aft
     if (i == 0) *flag = 0;
 }
 
-// Copy panel rows to fp64 and record their norms.  One work-group per row.
+// Norms of the codebook rows (the rank threshold is relative to them) and
+// the check for non-finite entries.  One work-group per row.
 template <typename T>
-__global__ void __launch_bounds__(NT) k_load_panel(const T *C, int64_t ldc, int64_t D, int64_t i0,
-                                                   double *wp, double *cn, int32_t *flag) {
+__global__ void __launch_bounds__(NT) k_norms(const T *C, int64_t ldc, int64_t D, double *cn, int32_t *flag) {
     __shared__ double red[NT / 64];
     const int64_t i = blockIdx.x;
     double s = 0.0;
     bool bad = false;
     for (int64_t d = threadIdx.x; d < D; d += NT) {
-        const double v = ld_f64<T>(C, (i0 + i) * ldc + d);
+        const double v = ld_f64<T>(C, i * ldc + d);
         bad |= !isfinite(v);
-        wp[i * D + d] = v;
         s += v * v;
     }
     if (bad) *flag = 1;
     s = block_sum(s, red);
-    if (threadIdx.x == 0) cn[i0 + i] = sqrt(s);
+    if (threadIdx.x == 0) cn[i] = sqrt(s);
 }
 
-// part[c][i][k] = sum over D-chunk c of W_p[i, d] * Q[k, d], for the basis
-// vectors k < rank at panel start.  Work-group (kb, c): 32 basis vectors x 32
-// panel rows; thread t owns row t / 8 and basis vectors 4 (t % 8) + 0..3.
-__global__ void __launch_bounds__(NT) k_panel_dots(const double *wp, const double *qm, int64_t D,
-                                                   int pb, int64_t i0, const int32_t *rank_after,
-                                                   double *part, int64_t M) {
-    constexpr int DT = 32;
-    __shared__ double ws[PB][DT + 1];
-    __shared__ double qs[32][DT + 1];
-    const int r = rank_before(rank_after, i0);
-    const int kb = blockIdx.x * 32;
-    if (kb >= r) return;
+// Copy the panel's rows to fp64.  Grid: (rows, column blocks of 8 NT).
+template <typename T>
+__global__ void __launch_bounds__(NT) k_load_panel(const T *C, int64_t ldc, int64_t D, int64_t i0, double *wp) {
+    const int64_t i = blockIdx.x;
+    const int64_t d0 = (int64_t)blockIdx.y * NT * 8 + threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int64_t d = d0 + u * NT;
+        if (d < D) wp[i * D + d] = ld_f64<T>(C, (i0 + i) * ldc + d);
+    }
+}
+
+// ---------------------------------------------------------------- products with the basis
+//
+// Matrix-core fp64 tiles: a work-group of four waves computes a 32 x 64
+// block; wave w owns columns 16w .. 16w + 15 as two 16 x 16 blocks (rows
+// 0..15 and 16..31).  For v_mfma_f64_16x16x4f64, lane l supplies A[l % 16][l / 16]
+// and B[l / 16][l % 16], and holds D[l / 16 + 4 j][l % 16] in element j.
+
+// part[c][i][kb + n] = sum over the c-th D-chunk of S[i][d] * Qb[kb + n][d]
+// (i < rows(sw), kb + n < rows(qw)).  Grid: (basis blocks of 64, D-chunks).
+__global__ void __launch_bounds__(NT) k_bdots(const double *S, int sw, const double *Qb, int qw, int64_t D,
+                                              Panel p, double *part, int64_t ldp) {
+    __shared__ double Ss[PB * LDK];
+    __shared__ double Qs[BN * LDK];
+    const int ns = rows_of(p, sw), nq = rows_of(p, qw);
+    const int kb = blockIdx.x * BN;
+    if (kb >= nq || ns == 0) return;
     const int64_t c = blockIdx.y;
-    const int64_t d_lo = c * DCH, d_hi = (d_lo + DCH < D) ? d_lo + DCH : D;
-    const int t = threadIdx.x;
-    const int i = t >> 3, kq = 4 * (t & 7);
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int64_t d0 = d_lo; d0 < d_hi; d0 += DT) {
-        for (int e = t; e < 32 * DT; e += NT) {
-            const int rr = e / DT, dd = e % DT;
-            const int64_t d = d0 + dd;
-            ws[rr][dd] = (rr < pb && d < d_hi) ? wp[rr * D + d] : 0.0;
-            qs[rr][dd] = (kb + rr < r && d < d_hi) ? qm[(int64_t)(kb + rr) * D + d] : 0.0;
-        }
-        __syncthreads();
-#pragma unroll 8
-        for (int dd = 0; dd < DT; ++dd) {
-            const double w = ws[i][dd];
+    const int64_t d_lo = c * BK, d_hi = (d_lo + BK < D) ? d_lo + BK : D;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    // staging: element u of a thread is row (t + 256 u) / 64, column t % 64,
+    // so the 64 lanes of a wave read 64 consecutive doubles of one row
+    const int col = t & 63, row0 = t >> 6;
+    double sreg[8], qreg[16];
+    auto fetch = [&](int64_t d0) {
+        const int64_t d = d0 + col;
+        const bool din = d < d_hi;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[q] += w * qs[kq + q][dd];
+        for (int u = 0; u < 8; ++u) {
+            const int r = row0 + 4 * u;
+            sreg[u] = (r < ns && din) ? S[(int64_t)r * D + d] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int r = row0 + 4 * u;
+            qreg[u] = (kb + r < nq && din) ? Qb[(int64_t)(kb + r) * D + d] : 0.0;
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) Ss[(row0 + 4 * u) * LDK + col] = sreg[u];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) Qs[(row0 + 4 * u) * LDK + col] = qreg[u];
+    };
+    d4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+    fetch(d_lo);
+    stash();
+    __syncthreads();
+    for (int64_t d0 = d_lo; d0 < d_hi; d0 += KS) {
+        const bool more = d0 + KS < d_hi;
+        if (more) fetch(d0 + KS);
+#pragma unroll
+        for (int s = 0; s < KS / 4; ++s) {
+            const int kk = 4 * s + (lane >> 4);
+            const double b = Qs[(16 * w + (lane & 15)) * LDK + kk];
+            const double a0 = Ss[(lane & 15) * LDK + kk];
+            const double a1 = Ss[(16 + (lane & 15)) * LDK + kk];
+            acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b, acc1, 0, 0, 0);
         }
         __syncthreads();
+        if (more) {
+            stash();
+            __syncthreads();
+        }
     }
-    if (i < pb)
+    const int n = 16 * w + (lane & 15);
+    if (kb + n < nq) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (kb + kq + q < r) part[(c * PB + i) * M + kb + kq + q] = acc[q];
+        for (int j = 0; j < 4; ++j) {
+            const int i = (lane >> 4) + 4 * j;
+            part[(c * PB + i) * ldp + kb + n] = acc0[j];
+            part[(c * PB + 16 + i) * ldp + kb + n] = acc1[j];
+        }
+    }
 }
 
-// h[i][k] = sum_c part[c][i][k] (chunk order); R[i0 + i, k] += h.
-__global__ void k_panel_reduce(const double *part, int64_t nch, int pb, int64_t i0,
-                               const int32_t *rank_after, double *hc, double *hb, int64_t M) {
-    const int r = rank_before(rank_after, i0);
+// out[i][k] (leading dimension ldo) = sum over the chunks c (in order) of
+// part[c][i][k], for i < rows(sw), k < rows(qw).
+__global__ void k_breduce(const double *part, int64_t nch, int64_t ldp, int sw, int qw, Panel p,
+                          double *out, int64_t ldo) {
+    const int ns = rows_of(p, sw), nq = rows_of(p, qw);
     const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
-    const int i = (int)(e / M), k = (int)(e % M);
-    if (i >= pb || k >= r) return;
-    double s = 0.0;
-    for (int64_t c = 0; c < nch; ++c) s += part[(c * PB + i) * M + k];
-    hb[(int64_t)i * M + k] = s;
-    hc[(i0 + i) * M + k] += s;
+    const int i = (int)(e / ldp), k = (int)(e % ldp);
+    if (i >= ns || k >= nq) return;
+    // four running sums (chunks c = 4 m + j), added in a fixed order
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int64_t c = 0;
+    for (; c + 4 <= nch; c += 4) {
+        s0 += part[((c + 0) * PB + i) * ldp + k];
+        s1 += part[((c + 1) * PB + i) * ldp + k];
+        s2 += part[((c + 2) * PB + i) * ldp + k];
+        s3 += part[((c + 3) * PB + i) * ldp + k];
+    }
+    for (; c < nch; ++c) s0 += part[(c * PB + i) * ldp + k];
+    out[(int64_t)i * ldo + k] = (s0 + s1) + (s2 + s3);
 }
 
-// W_p[i, d] -= sum_k h[i][k] Q[k, d] over k < rank at panel start.
-// Work-group: 64 columns x 32 rows; thread t owns row t / 8, columns
-// 8 (t % 8) + 0..7.
-__global__ void __launch_bounds__(NT) k_panel_update(double *wp, const double *qm, const double *hb,
-                                                     int64_t D, int pb, int64_t i0,
-                                                     const int32_t *rank_after, int64_t M) {
-    constexpr int KT = 32, DC = 64;
-    __shared__ double hs[PB][KT + 1];
-    __shared__ double qs[KT][DC + 1];
-    const int r = rank_before(rank_after, i0);
-    const int64_t d0 = (int64_t)blockIdx.x * DC;
-    const int t = threadIdx.x;
-    const int i = t >> 3, cb = 8 * (t & 7);
-    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int k0 = 0; k0 < r; k0 += KT) {
-        for (int e = t; e < PB * KT; e += NT) {
-            const int rr = e / KT, kk = e % KT;
-            hs[rr][kk] = (rr < pb && k0 + kk < r) ? hb[(int64_t)rr * M + k0 + kk] : 0.0;
+// G[i][j] = sum over the column blocks b (in a fixed order) of
+// gpart[b][i][j]: work-group of 256 threads for 64 entries, each quarter of
+// the threads summing a quarter of the blocks, quarters added in order.
+__global__ void __launch_bounds__(NT) k_gram_reduce(const double *gpart, int64_t nblk, double *G) {
+    __shared__ double red[4][64];
+    const int t = threadIdx.x, e = blockIdx.x * 64 + (t & 63), qt = t >> 6;
+    const int64_t b0 = nblk * qt / 4, b1 = nblk * (qt + 1) / 4;
+    double s0 = 0.0, s1 = 0.0;
+    int64_t b = b0;
+    for (; b + 2 <= b1; b += 2) {
+        s0 += gpart[b * PB * PB + e];
+        s1 += gpart[(b + 1) * PB * PB + e];
+    }
+    if (b < b1) s0 += gpart[b * PB * PB + e];
+    red[qt][t & 63] = s0 + s1;
+    __syncthreads();
+    if (qt == 0) G[e] = (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
+}
+
+// S[i][d] -= sum over k < rows(qw) of H[i][k] * Qb[k][d], for i < rows(sw).
+// Grid: column blocks of 64.  With gpart, also the block's share of the
+// Gram matrix of the updated rows: gpart[blk][i][j] = sum over the block's
+// columns of S[i][d] S[j][d] (rows(qw) may then be 0: only the Gram part).
+__global__ void __launch_bounds__(NT) k_bupdate(double *S, int sw, const double *H, int64_t ldh,
+                                                const double *Qb, int qw, int64_t D, Panel p, double *gpart) {
+    __shared__ double Hs[PB * LDK];
+    __shared__ double Qs[KS * LDK];
+    const int ns = rows_of(p, sw), nq = rows_of(p, qw);
+    if (ns == 0 || (nq == 0 && !gpart)) return;
+    const int64_t d0 = (int64_t)blockIdx.x * BN;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    // staging: element u of a thread is row (t + 256 u) / 64, column t % 64
+    // (H tile 32 x 64 over k; Q tile 64 (k) x 64 (d)): 64 consecutive
+    // doubles of one row per wave
+    const int scol = t & 63, row0 = t >> 6;
+    double hreg[8], qreg[16];
+    auto fetch = [&](int k0) {
+        const int k = k0 + scol;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int r = row0 + 4 * u;
+            hreg[u] = (r < ns && k < nq) ? H[(int64_t)r * ldh + k] : 0.0;
         }
-        for (int e = t; e < KT * DC; e += NT) {
-            const int kk = e / DC, dd = e % DC;
-            qs[kk][dd] = (k0 + kk < r && d0 + dd < D) ? qm[(int64_t)(k0 + kk) * D + d0 + dd] : 0.0;
+        const int64_t d = d0 + scol;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int r = row0 + 4 * u;
+            qreg[u] = (k0 + r < nq && d < D) ? Qb[(int64_t)(k0 + r) * D + d] : 0.0;
+        }
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) Hs[(row0 + 4 * u) * LDK + scol] = hreg[u];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) Qs[(row0 + 4 * u) * LDK + scol] = qreg[u];
+    };
+    d4 acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+    if (nq > 0) {
+        fetch(0);
+        stash();
+        __syncthreads();
+    }
+    for (int k0 = 0; k0 < nq; k0 += KS) {
+        const bool more = k0 + KS < nq;
+        if (more) fetch(k0 + KS);
+#pragma unroll
+        for (int s = 0; s < KS / 4; ++s) {
+            const int kk = 4 * s + (lane >> 4);
+            const double b = Qs[kk * LDK + 16 * w + (lane & 15)];
+            const double a0 = Hs[(lane & 15) * LDK + kk];
+            const double a1 = Hs[(16 + (lane & 15)) * LDK + kk];
+            acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b, acc1, 0, 0, 0);
         }
         __syncthreads();
-#pragma unroll 4
-        for (int kk = 0; kk < KT; ++kk) {
-            const double h = hs[i][kk];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) acc[j] += h * qs[kk][cb + j];
+        if (more) {
+            stash();
+            __syncthreads();
         }
+    }
+    const int col = 16 * w + (lane & 15);
+    const int64_t d = d0 + col;
+    double nv[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int i = (lane >> 4) + 4 * j;
+        nv[j] = (i < ns && d < D) ? S[(int64_t)i * D + d] - acc0[j] : 0.0;
+        nv[4 + j] = (16 + i < ns && d < D) ? S[(int64_t)(16 + i) * D + d] - acc1[j] : 0.0;
+        if (i < ns && d < D) S[(int64_t)i * D + d] = nv[j];
+        if (16 + i < ns && d < D) S[(int64_t)(16 + i) * D + d] = nv[4 + j];
+    }
+    if (!gpart) return;
+    // the updated 32 x 64 block through LDS, then its Gram share
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int i = (lane >> 4) + 4 * j;
+        Hs[i * LDK + col] = nv[j];
+        Hs[(16 + i) * LDK + col] = nv[4 + j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < (PB * PB) / NT; ++u) {
+        const int e = t + u * NT;
+        const int i = e / PB, j = e % PB;
+        double g0 = 0.0, g1 = 0.0;
+#pragma unroll 8
+        for (int c = 0; c < BN; c += 2) {
+            g0 += Hs[i * LDK + c] * Hs[j * LDK + c];
+            g1 += Hs[i * LDK + c + 1] * Hs[j * LDK + c + 1];
+        }
+        gpart[((int64_t)blockIdx.x * PB + i) * PB + j] = g0 + g1;
+    }
+}
+
+// ---------------------------------------------------------------- panel factor (TSQR)
+//
+// Triangular factor R (PB x PB, upper) of a tall matrix T (TCH x PB) by
+// Householder reflections, T = Q R.  Leaf: T[t][i] = S[i][TCH c + t], the
+// panel's rows (i < rows(sw)) over D-chunk c.  Node: T stacks up to TFAN
+// factors of the previous level.  Thread (k, g) = (t / 8, t % 8) holds column
+// k of T in registers, rows g + 8 q; only the current reflector goes through
+// LDS.  Signs of R's rows are whatever the reflections give: only the inner
+// products of R's columns (those of the panel's rows) are used.
+
+constexpr int TNQ = TCH / 8;   // rows of T held per thread
+
+// Reflection j: zero column j of T below row j and apply it to the columns
+// to its right.  J is a compile-time constant so that every register index
+// is one.
+template <int J>
+__device__ __forceinline__ void hh_step(double (&a)[TNQ], int t, int k, int g, double (*vbuf)[TCH],
+                                        double (*coefs)[2]) {
+    constexpr int buf = J & 1, qj = J / 8, gj = J % 8;
+    constexpr int q0 = J / 8;        // rows g + 8q below this block are all above row J
+    if (k == J) {
+        double s4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int q = q0; q < TNQ; ++q) {
+            const int row = g + 8 * q;
+            const double x = (row > J) ? a[q] : 0.0;
+            s4[q & 3] += x * x;
+        }
+        const double sg = group8_sum((s4[0] + s4[1]) + (s4[2] + s4[3]));
+        const double alpha = group8_sum((g == gj) ? a[qj] : 0.0);   // lane gj's entry, on all 8
+        double beta, tau, scale;
+        if (sg == 0.0) {
+            beta = alpha; tau = 0.0; scale = 0.0;
+        } else {
+            const double nrm = sqrt(alpha * alpha + sg);
+            beta = (alpha <= 0.0) ? nrm : -nrm;
+            tau = (beta - alpha) / beta;
+            scale = 1.0 / (alpha - beta);
+        }
+#pragma unroll
+        for (int q = q0; q < TNQ; ++q) {
+            const int row = g + 8 * q;
+            vbuf[buf][row] = (row > J) ? a[q] * scale : (row == J ? 1.0 : 0.0);
+        }
+        if (g == 0) coefs[buf][0] = tau;
+        if (g == gj) a[qj] = beta;      // R[J][J]
+    }
+    __syncthreads();
+    if (k > J) {
+        const double tau = coefs[buf][0];
+        double vr[TNQ];
+#pragma unroll
+        for (int q = q0; q < TNQ; ++q) {
+            const int row = g + 8 * q;
+            vr[q] = (row >= J) ? vbuf[buf][row] : 0.0;
+        }
+        double w4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int q = q0; q < TNQ; ++q) w4[q & 3] += vr[q] * a[q];
+        const double wsum = group8_sum((w4[0] + w4[1]) + (w4[2] + w4[3])) * tau;
+#pragma unroll
+        for (int q = q0; q < TNQ; ++q) a[q] -= wsum * vr[q];
+    }
+}
+
+template <int... J>
+__device__ __forceinline__ void hh_all(double (&a)[TNQ], int t, int k, int g, double (*vbuf)[TCH],
+                                       double (*coefs)[2], std::integer_sequence<int, J...>) {
+    (hh_step<J>(a, t, k, g, vbuf, coefs), ...);
+}
+
+__global__ void __launch_bounds__(NT) k_tsqr(const double *S, int sw, int64_t D, const double *Rin,
+                                             int64_t nin, double *Rout, Panel p) {
+    __shared__ double vbuf[2][TCH];
+    __shared__ double coefs[2][2];
+    const int t = threadIdx.x;
+    const int k = t >> 3, g = t & 7;
+    const int64_t c = blockIdx.x;
+    double a[TNQ];
+    if (S) {
+        const int ns = rows_of(p, sw);
+#pragma unroll
+        for (int q = 0; q < TNQ; ++q) {
+            const int64_t d = c * TCH + g + 8 * q;
+            a[q] = (k < ns && d < D) ? S[(int64_t)k * D + d] : 0.0;
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < TNQ; ++q) {
+            const int row = g + 8 * q;                 // row of the stack
+            const int64_t f = c * TFAN + row / PB;     // factor index
+            a[q] = (f < nin) ? Rin[(f * PB + (row % PB)) * PB + k] : 0.0;
+        }
+    }
+    hh_all(a, t, k, g, vbuf, coefs, std::make_integer_sequence<int, PB>{});
+    // upper triangle of the first PB rows: R[i][k] = T[i][k], i <= k
+#pragma unroll
+    for (int q = 0; q < PB / 8; ++q) {
+        const int i = g + 8 * q;
+        Rout[(c * PB + i) * PB + k] = (i <= k) ? a[q] : 0.0;
+    }
+}
+
+// ---------------------------------------------------------------- small-space steps (one wave)
+
+// v of lane `lane` (a compile-time constant in the unrolled loops), on every lane.
+__device__ __forceinline__ double lane_value(double v, int lane) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffffLL), lane);
+    const int hi = __builtin_amdgcn_readlane((int)(b >> 32), lane);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+// Rank decisions of the panel.  Columns a_i of the panel factor R_t are
+// orthogonalised in index order by two Gram-Schmidt passes against the
+// vectors kept so far; row i is dependent if the norm left is
+// <= tol * ||c_i||.  Outputs: X1[l][i] (new vector l = sum_i X1[l][i] w_i),
+// C1[i][l] = <w_i, v_l> summed over both passes (the pivot for the row that
+// made v_l), rank_after and kept for the panel's rows.  One wave; lanes
+// 0..31 index vector entries or kept vectors; unkept rows of Z and X are
+// zero, so every loop runs over all 32.
+__global__ void __launch_bounds__(64) k_small_rank(const double *Rt, const double *cn, double tol, Panel p,
+                                                   int32_t *rank_after, int32_t *kept, double *X1, double *C1,
+                                                   int32_t *pass2_out) {
+    __shared__ double A[PB][PB + 1];     // A[i][e] = R_t[e][i]: column i of the factor
+    __shared__ __attribute__((aligned(16))) double vb[PB];
+    __shared__ __attribute__((aligned(16))) double hb[PB];
+    __shared__ double thr[PB], thr_cn[PB];
+    const int l = threadIdx.x;
+    const bool act = l < PB;
+    const int r_old = rank_before(p.rank_after, p.i0);
+    if (l < p.pb) {
+        thr_cn[l] = cn[p.i0 + l];
+        thr[l] = tol * thr_cn[l];
+    }
+    // lane l: zr[e] = z_l[e] (kept vector l), zc[k] = z_k[l], xc[k] = X[k][l];
+    // rows of vectors not (yet) kept are zero.  Values of other lanes come
+    // through vb / hb in LDS (broadcast reads).
+    double zr[PB], zc[PB], xc[PB];
+#pragma unroll
+    for (int e = 0; e < PB; ++e) { zr[e] = 0.0; zc[e] = 0.0; xc[e] = 0.0; }
+    for (int e = l; e < PB * PB; e += 64) {
+        const int i = e / PB, f = e % PB;
+        A[i][f] = Rt[f * PB + i];
+        C1[e] = 0.0;
+        X1[e] = 0.0;
+    }
+    __syncthreads();
+    // sum_j b[j] * r[j] with four running sums (fixed order)
+    auto dot4 = [](const double *b, const double (&r)[PB]) {
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll
+        for (int j = 0; j < PB; j += 4) {
+            s0 += b[j] * r[j];
+            s1 += b[j + 1] * r[j + 1];
+            s2 += b[j + 2] * r[j + 2];
+            s3 += b[j + 3] * r[j + 3];
+        }
+        return (s0 + s1) + (s2 + s3);
+    };
+    int nk = 0;
+    for (int i = 0; i < p.pb; ++i) {
+        double v = act ? A[i][l] : 0.0;
+        double csum = 0.0;                   // lane k: coefficient on kept vector k
+        for (int pass = 0; pass < 2; ++pass) {
+            if (act) vb[l] = v;
+            __syncthreads();
+            const double h = act ? dot4(vb, zr) : 0.0;   // lane k: <v, z_k>
+            csum += h;
+            if (act) hb[l] = h;
+            __syncthreads();
+            if (act) v -= dot4(hb, zc);                  // lane e: sum_k h_k z_k[e]
+        }
+        if (act) vb[l] = v * v;
         __syncthreads();
-    }
-    if (i < pb)
+        double s2 = 0.0;                     // ||v||^2, the same sum on every lane
+        {
+            double q0 = 0.0, q1 = 0.0, q2 = 0.0, q3 = 0.0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (d0 + cb + j < D) wp[i * D + d0 + cb + j] -= acc[j];
-}
-
-// In-panel pass for row i: partial dots of W_p[i] with the basis vectors made
-// earlier in this panel (at most PB - 1 of them), per D-chunk of ICH.
-__global__ void __launch_bounds__(NT) k_intra_dots(const double *wp, const double *qm, int64_t D,
-                                                   int64_t i0, int i, const int32_t *rank_after,
-                                                   double *part2) {
-    __shared__ double red[NT / 64][PB];
-    const int rb = rank_before(rank_after, i0);
-    const int nb = rank_before(rank_after, i0 + i) - rb;
-    if (nb == 0) return;
-    const int64_t c = blockIdx.x;
-    const int t = threadIdx.x;
-    double s[PB];
-#pragma unroll
-    for (int j = 0; j < PB; ++j) s[j] = 0.0;
-    for (int q = 0; q < ICH / NT; ++q) {
-        const int64_t d = c * ICH + q * NT + t;
-        if (d < D) {
-            const double w = wp[(int64_t)i * D + d];
-#pragma unroll
-            for (int j = 0; j < PB; ++j)
-                if (j < nb) s[j] += w * qm[(int64_t)(rb + j) * D + d];
+            for (int e = 0; e < PB; e += 4) {
+                q0 += vb[e]; q1 += vb[e + 1]; q2 += vb[e + 2]; q3 += vb[e + 3];
+            }
+            s2 = (q0 + q1) + (q2 + q3);
         }
-    }
-#pragma unroll
-    for (int j = 0; j < PB; ++j) {
-        double v = s[j];
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off);
-        if ((t & 63) == 0) red[t >> 6][j] = v;
-    }
-    __syncthreads();
-    if (t < nb) {
-        double v = 0.0;
-        for (int w = 0; w < NT / 64; ++w) v += red[w][t];
-        part2[c * PB + t] = v;
-    }
-}
-
-// Finish the pass for row i: reduce the chunk partials to coefficients g_j,
-// W_p[i] -= sum_j g_j q_{rb+j}, accumulate g into R, and emit per-chunk
-// partial sums of the updated row's squares.
-__global__ void __launch_bounds__(NT) k_intra_update(double *wp, const double *qm, double *hc,
-                                                     int64_t D, int64_t i0, int i,
-                                                     const int32_t *rank_after, const double *part2,
-                                                     int64_t nch2, double *part3, int64_t M) {
-    __shared__ double g[PB];
-    __shared__ double red[NT / 64];
-    const int rb = rank_before(rank_after, i0);
-    const int nb = rank_before(rank_after, i0 + i) - rb;
-    const int t = threadIdx.x;
-    if (t < nb) {
-        double v = 0.0;
-        for (int64_t c = 0; c < nch2; ++c) v += part2[c * PB + t];
-        g[t] = v;
-        if (blockIdx.x == 0) hc[(i0 + i) * M + rb + t] += v;
-    }
-    __syncthreads();
-    const int64_t c = blockIdx.x;
-    double s = 0.0;
-    for (int q = 0; q < ICH / NT; ++q) {
-        const int64_t d = c * ICH + q * NT + t;
-        if (d < D) {
-            double w = wp[(int64_t)i * D + d];
-            for (int j = 0; j < nb; ++j) w -= g[j] * qm[(int64_t)(rb + j) * D + d];
-            wp[(int64_t)i * D + d] = w;
-            s += w * w;
-        }
-    }
-    s = block_sum(s, red);
-    if (t == 0) part3[c] = s;
-}
-
-// Rank decision for row i after both passes; normalise it into the next basis
-// vector if it is independent.
-__global__ void __launch_bounds__(NT) k_intra_finalize(const double *wp, double *qm, double *hc,
-                                                       int64_t D, int64_t i0, int i,
-                                                       int32_t *rank_after, const double *part3,
-                                                       int64_t nch2, const double *cn, double tol,
-                                                       int32_t *kept, int64_t M) {
-    const int r = rank_before(rank_after, i0 + i);
-    double s = 0.0;
-    for (int64_t c = 0; c < nch2; ++c) s += part3[c];
-    const double rho = sqrt(s);
-    const bool keep = rho > tol * cn[i0 + i];
-    const int64_t c = blockIdx.x;
-    if (keep) {
-        for (int q = 0; q < ICH / NT; ++q) {
-            const int64_t d = c * ICH + q * NT + threadIdx.x;
-            if (d < D) qm[(int64_t)r * D + d] = wp[(int64_t)i * D + d] / rho;
-        }
-    }
-    if (c == 0 && threadIdx.x == 0) {
-        rank_after[i0 + i] = r + (keep ? 1 : 0);
+        const double rho = sqrt(s2);
+        const bool keep = rho > thr[i];
+        if (act && l < nk) C1[i * PB + l] = csum;
+        __syncthreads();
         if (keep) {
-            hc[(i0 + i) * M + r] = rho;
-            kept[r] = (int32_t)(i0 + i);
+            // new vector z = v / rho, combination X = (e_i - sum_k c_k X_k) / rho
+            const double z = v / rho;
+            if (act) {
+                vb[l] = z;
+                hb[l] = (l < nk) ? csum : 0.0;
+            }
+            __syncthreads();
+            const double x = (((l == i) ? 1.0 : 0.0) - dot4(hb, xc)) / rho;
+#pragma unroll
+            for (int kq = 0; kq < PB; ++kq) {
+                if (kq == nk) { zc[kq] = z; xc[kq] = x; }
+            }
+            if (l == nk) {
+#pragma unroll
+                for (int e = 0; e < PB; ++e) zr[e] = vb[e];
+            }
+            if (l == 0) {
+                C1[i * PB + nk] = rho;
+                kept[r_old + nk] = (int32_t)(p.i0 + i);
+            }
+            ++nk;
+            __syncthreads();
         }
+        if (l == 0) rank_after[p.i0 + i] = r_old + nk;
+    }
+    if (act) {
+#pragma unroll
+        for (int kq = 0; kq < PB; ++kq)
+            if (kq < nk) X1[kq * PB + l] = xc[kq];
+    }
+    // largest combination weight sum_i |X1[k][i]| ||c_i|| over the new
+    // vectors (A is free now: A[k][i] = |X1[k][i]| ||c_i||)
+    __syncthreads();
+    if (act) {
+        const double ci = (l < p.pb) ? thr_cn[l] : 0.0;
+#pragma unroll
+        for (int kq = 0; kq < PB; ++kq) A[kq][l] = fabs(xc[kq]) * ci;
+    }
+    __syncthreads();
+    double wk = 0.0;
+    if (act) {
+#pragma unroll
+        for (int i = 0; i < PB; ++i) wk += A[l][i];
+    }
+    for (int off = 32; off > 0; off >>= 1) wk = fmax(wk, __shfl_xor(wk, off));
+    if (l == 0) *pass2_out = (wk > PASS2_WEIGHT) ? 1 : 0;
+}
+
+// Cholesky factor L of the Gram matrix G (n x n, n = new vectors; the
+// vectors are orthonormal up to rounding) and its inverse.  LX[0] = L (lower),
+// LX[1] = L^-1.  A pivot that is not positive sets flag 2.  One wave; entries
+// not yet computed are zero, so the sums run over all 32.
+template <int... I>
+__device__ __forceinline__ void inv_rows(double (&y)[PB], int c, const double (*L)[PB + 1],
+                                         std::integer_sequence<int, I...>) {
+    // y[i] = (delta_ic - sum_{k<i} L[i][k] y[k]) / L[i][i], rows in order
+    auto row = [&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        double s = (i == c) ? 1.0 : 0.0;
+#pragma unroll
+        for (int k = 0; k < i; ++k) s -= L[i][k] * y[k];
+        y[i] = (i >= c) ? s / L[i][i] : 0.0;
+    };
+    (row(std::integral_constant<int, I>{}), ...);
+}
+
+__global__ void __launch_bounds__(64) k_small_chol(const double *G, Panel p, double *LX, int32_t *flag) {
+    __shared__ double L[PB][PB + 1];
+    __shared__ double Gs[PB][PB + 1];
+    const int l = threadIdx.x;
+    const bool act = l < PB;
+    const int n = rows_of(p, ROWS_NEW);
+    for (int e = l; e < PB * PB; e += 64) {
+        L[e / PB][e % PB] = 0.0;
+        Gs[e / PB][e % PB] = G[e];
+    }
+    __syncthreads();
+    bool bad = false;
+    for (int j = 0; j < n; ++j) {
+        // lane i >= j: L[i][j] = (G[i][j] - sum_k L[i][k] L[j][k]) / L[j][j]
+        double s = (act && l < n && l >= j) ? Gs[l][j] : 0.0;
+        if (act) {
+            double t0 = 0.0, t1 = 0.0;
+#pragma unroll
+            for (int kq = 0; kq < PB; kq += 2) {
+                t0 += L[l][kq] * L[j][kq];
+                t1 += L[l][kq + 1] * L[j][kq + 1];
+            }
+            s -= t0 + t1;
+        }
+        const double djj = lane_value(s, j);
+        if (!(djj > 0.0)) bad = true;
+        const double ljj = sqrt(djj > 0.0 ? djj : 1.0);
+        __syncthreads();
+        if (act && l < n && l >= j) L[l][j] = (l == j) ? ljj : s / ljj;
+        __syncthreads();
+    }
+    // identity padding beyond n keeps the inverse finite
+    if (act && l >= n) L[l][l] = 1.0;
+    __syncthreads();
+    double y[PB];
+    if (act) inv_rows(y, l, L, std::make_integer_sequence<int, PB>{});
+#pragma unroll
+    for (int i = 0; i < PB; ++i)
+        if (act) LX[PB * PB + i * PB + l] = (l < n && i < n) ? y[i] : 0.0;
+    for (int e = l; e < PB * PB; e += 64) {
+        const int i = e / PB, k = e % PB;
+        LX[e] = (i < n && k < n) ? L[i][k] : 0.0;
+    }
+    if (bad && l == 0) *flag |= 2;
+}
+
+// dst[o][d] = sum over i < rows(sw) of X[o][i] * src[i][d], for o < rows(ow);
+// with at_new, dst starts at row r_old (the panel's new basis rows).  Grid:
+// column blocks of 64; thread (column t % 64, output group t / 64) forms the
+// outputs o = t / 64 + 4 m.
+__global__ void __launch_bounds__(NT) k_combine(const double *X, int ow, const double *src, int sw, double *dst,
+                                                bool at_new, int64_t D, Panel p) {
+    __shared__ double Xs[PB * PB];
+    const int no = rows_of(p, ow), ns = rows_of(p, sw);
+    if (no == 0) return;
+    if (at_new) dst += (int64_t)rank_before(p.rank_after, p.i0) * D;
+    for (int e = threadIdx.x; e < PB * PB; e += NT) Xs[e] = X[e];
+    __syncthreads();
+    const int64_t d = (int64_t)blockIdx.x * 64 + (threadIdx.x & 63);
+    const int og = threadIdx.x >> 6;
+    if (d >= D) return;
+    double sv[PB];
+#pragma unroll
+    for (int i = 0; i < PB; ++i) sv[i] = (i < ns) ? src[(int64_t)i * D + d] : 0.0;
+#pragma unroll
+    for (int m = 0; m < PB / 4; ++m) {
+        const int o = og + 4 * m;
+        if (o < no) {
+            double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+            for (int i = 0; i < PB; i += 2) {
+                a0 += Xs[o * PB + i] * sv[i];
+                a1 += Xs[o * PB + i + 1] * sv[i + 1];
+            }
+            dst[(int64_t)o * D + d] = a0 + a1;
+        }
+    }
+}
+
+// Coefficients of the panel's rows: R[i0 + i][k] += sum_l C1[i][l] H2[l][k]
+// (k < r_old, second pass) and R[i0 + i][r_old + l] = sum_m C1[i][m] L[m][l].
+// One thread per (row, column); grid: (column blocks of 256, panel rows).
+__global__ void __launch_bounds__(NT) k_coef(const double *C1, const double *H2, int64_t ldh, bool pass2,
+                                             const double *LX, double *hc, int64_t M, Panel p) {
+    __shared__ double c[PB];
+    const int r_old = rank_before(p.rank_after, p.i0);
+    const int nn = rows_of(p, ROWS_NEW);
+    const int i = blockIdx.y;
+    if (threadIdx.x < PB) c[threadIdx.x] = C1[i * PB + threadIdx.x];
+    __syncthreads();
+    const int64_t k = (int64_t)blockIdx.x * NT + threadIdx.x;
+    if (k < r_old && pass2 && *p.pass2) {
+        double s = 0.0;
+#pragma unroll 8
+        for (int l = 0; l < nn; ++l) s += c[l] * H2[(int64_t)l * ldh + k];
+        hc[(p.i0 + i) * M + k] += s;
+    } else if (k >= r_old && k < r_old + nn) {
+        const int l = (int)(k - r_old);
+        double s = 0.0;
+        for (int m = l; m < nn; ++m) s += c[m] * LX[m * PB + l];
+        hc[(p.i0 + i) * M + k] = s;
     }
 }
 
@@ -338,9 +812,57 @@ hipError_t outputs_r(gs_dtype rt, const WsLayout &L, char *ws, int64_t M, int64_
 }
 
 template <typename T>
-hipError_t launch_load(const void *C, int64_t ldc, int64_t D, int64_t i0, int pb, double *wp,
-                       double *cn, int32_t *flag, hipStream_t s) {
-    hipLaunchKernelGGL((k_load_panel<T>), dim3(pb), dim3(NT), 0, s, (const T *)C, ldc, D, i0, wp, cn, flag);
+hipError_t launch_load(const void *C, int64_t ldc, int64_t D, int64_t i0, int pb, double *wp, hipStream_t s) {
+    hipLaunchKernelGGL((k_load_panel<T>), dim3(pb, (unsigned)((D + NT * 8 - 1) / (NT * 8))), dim3(NT), 0, s,
+                       (const T *)C, ldc, D, i0, wp);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_norms(const void *C, int64_t ldc, int64_t M, int64_t D, double *cn, int32_t *flag,
+                        hipStream_t s) {
+    hipLaunchKernelGGL((k_norms<T>), dim3((unsigned)M), dim3(NT), 0, s, (const T *)C, ldc, D, cn, flag);
+    return hipGetLastError();
+}
+
+#define GS_TRY(x) do { hipError_t e_ = (x); if (e_ != hipSuccess) return e_; } while (0)
+
+// One pass of the block projection: H = S Qb^T (split over D-chunks, reduced
+// in order into out, leading dimension ldo), then S -= H Qb (with gpart, also
+// the column blocks' shares of the Gram matrix of the updated S).
+hipError_t block_pass(double *S, int sw, const double *Qb, int qw, int64_t max_q, int64_t D, const Panel &p,
+                      double *part, int64_t ldp, double *out, int64_t ldo, double *gpart, hipStream_t s) {
+    const int64_t nch = chunk_count(D);
+    const dim3 gd((unsigned)((max_q + BN - 1) / BN), (unsigned)nch);
+    hipLaunchKernelGGL(k_bdots, gd, dim3(NT), 0, s, (const double *)S, sw, Qb, qw, D, p, part, ldp);
+    const unsigned gr = (unsigned)((PB * ldp + NT - 1) / NT);
+    hipLaunchKernelGGL(k_breduce, dim3(gr), dim3(NT), 0, s, (const double *)part, nch, ldp, sw, qw, p, out, ldo);
+    if (!gpart) {
+        hipLaunchKernelGGL(k_bupdate, dim3((unsigned)((D + BN - 1) / BN)), dim3(NT), 0, s, S, sw,
+                           (const double *)out, ldo, Qb, qw, D, p, (double *)nullptr);
+    } else {
+        hipLaunchKernelGGL(k_bupdate, dim3((unsigned)((D + BN - 1) / BN)), dim3(NT), 0, s, S, sw,
+                           (const double *)out, ldo, Qb, qw, D, p, gpart);
+    }
+    return hipGetLastError();
+}
+
+// Triangular factor of the panel held in S (rows(sw) rows): leaves, then
+// nodes until one factor remains.  Returns the buffer holding it.
+hipError_t panel_factor(const double *S, int sw, int64_t D, const Panel &p, double *b0, double *b1,
+                        double **out, hipStream_t s) {
+    int64_t n = leaf_count(D);
+    hipLaunchKernelGGL(k_tsqr, dim3((unsigned)n), dim3(NT), 0, s, S, sw, D, (const double *)nullptr, (int64_t)0,
+                       b0, p);
+    double *cur = b0, *nxt = b1;
+    while (n > 1) {
+        const int64_t m = (n + TFAN - 1) / TFAN;
+        hipLaunchKernelGGL(k_tsqr, dim3((unsigned)m), dim3(NT), 0, s, (const double *)nullptr, 0, D,
+                           (const double *)cur, n, nxt, p);
+        double *tmp = cur; cur = nxt; nxt = tmp;
+        n = m;
+    }
+    *out = cur;
     return hipGetLastError();
 }
 
@@ -348,50 +870,66 @@ hipError_t launch_load(const void *C, int64_t ldc, int64_t D, int64_t i0, int pb
 
 size_t compress_workspace(int64_t M, int64_t D) { return layout(M, D).total; }
 
-#define GS_TRY(x) do { hipError_t e_ = (x); if (e_ != hipSuccess) return e_; } while (0)
-
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                         void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                         int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite, void *ws_,
                         hipStream_t s) {
     const WsLayout L = layout(M, D);
     char *ws = static_cast<char *>(ws_);
-    double *qm = (double *)(ws + L.qm), *wp = (double *)(ws + L.wp), *hc = (double *)(ws + L.hc);
-    double *hb = (double *)(ws + L.hb), *part = (double *)(ws + L.part);
-    double *part2 = (double *)(ws + L.part2), *part3 = (double *)(ws + L.part3);
+    double *qm = (double *)(ws + L.qm), *wp = (double *)(ws + L.wp), *w2 = (double *)(ws + L.w2);
+    double *hc = (double *)(ws + L.hc), *h2 = (double *)(ws + L.h2), *g2 = (double *)(ws + L.g2);
+    double *part = (double *)(ws + L.part), *tsq0 = (double *)(ws + L.tsq0), *tsq1 = (double *)(ws + L.tsq1);
+    double *gpart = (double *)(ws + L.gpart);
+    const int64_t nblk = (D + BN - 1) / BN;
+    double *x1 = (double *)(ws + L.x1), *c1 = (double *)(ws + L.c1), *lx = (double *)(ws + L.lx);
     double *cn = (double *)(ws + L.cn);
     int32_t *rank_after = (int32_t *)(ws + L.rank_after), *kept_ws = (int32_t *)(ws + L.kept);
-    int32_t *flag = (int32_t *)(ws + L.flag);
-    const int64_t nch = (D + DCH - 1) / DCH, nch2 = (D + ICH - 1) / ICH;
+    int32_t *flag = (int32_t *)(ws + L.flag), *pass2 = (int32_t *)(ws + L.pass2);
+    const int64_t ldp = M > PB ? M : PB;
 
     hipLaunchKernelGGL(k_init, dim3(1024), dim3(NT), 0, s, hc, M * M, kept_ws, rank_after, M, flag);
     GS_TRY(hipGetLastError());
+    if (ct == GS_F32) GS_TRY(launch_norms<float>(C, ldc, M, D, cn, flag, s));
+    else if (ct == GS_F64) GS_TRY(launch_norms<double>(C, ldc, M, D, cn, flag, s));
+    else GS_TRY(launch_norms<bf16_t>(C, ldc, M, D, cn, flag, s));
 
     for (int64_t i0 = 0; i0 < M; i0 += PB) {
         const int pb = (int)((M - i0 < PB) ? (M - i0) : PB);
-        if (ct == GS_F32) GS_TRY(launch_load<float>(C, ldc, D, i0, pb, wp, cn, flag, s));
-        else if (ct == GS_F64) GS_TRY(launch_load<double>(C, ldc, D, i0, pb, wp, cn, flag, s));
-        else GS_TRY(launch_load<bf16_t>(C, ldc, D, i0, pb, wp, cn, flag, s));
+        const Panel p{i0, pb, rank_after, pass2};
+        if (ct == GS_F32) GS_TRY(launch_load<float>(C, ldc, D, i0, pb, wp, s));
+        else if (ct == GS_F64) GS_TRY(launch_load<double>(C, ldc, D, i0, pb, wp, s));
+        else GS_TRY(launch_load<bf16_t>(C, ldc, D, i0, pb, wp, s));
+        // 1. first pass against the earlier basis; its coefficients go to R
+        if (i0 > 0)
+            GS_TRY(block_pass(wp, ROWS_PANEL, qm, ROWS_OLD, i0, D, p, part, ldp, hc + i0 * M, M, nullptr, s));
+        // 2. rank decisions in the panel's small space; first-round new vectors
+        double *rt_ = nullptr;
+        GS_TRY(panel_factor(wp, ROWS_PANEL, D, p, tsq0, tsq1, &rt_, s));
+        hipLaunchKernelGGL(k_small_rank, dim3(1), dim3(64), 0, s, (const double *)rt_, (const double *)cn, tol, p,
+                           rank_after, kept_ws, x1, c1, pass2);
+        hipLaunchKernelGGL(k_combine, dim3((unsigned)nblk), dim3(NT), 0, s, (const double *)x1,
+                           (int)ROWS_NEW, (const double *)wp, (int)ROWS_PANEL, w2, false, D, p);
+        GS_TRY(hipGetLastError());
+        // 3. second pass on the new vectors, with their Gram matrix, and its
+        // Cholesky factor
         if (i0 > 0) {
-            const dim3 gd((unsigned)((i0 + 31) / 32), (unsigned)nch);
-            const unsigned gr = (unsigned)((pb * M + NT - 1) / NT);
-            const unsigned gu = (unsigned)((D + 63) / 64);
-            for (int pass = 0; pass < 2; ++pass) {
-                hipLaunchKernelGGL(k_panel_dots, gd, dim3(NT), 0, s, wp, qm, D, pb, i0, rank_after, part, M);
-                hipLaunchKernelGGL(k_panel_reduce, dim3(gr), dim3(NT), 0, s, part, nch, pb, i0, rank_after, hc, hb, M);
-                hipLaunchKernelGGL(k_panel_update, dim3(gu), dim3(NT), 0, s, wp, qm, hb, D, pb, i0, rank_after, M);
-                GS_TRY(hipGetLastError());
-            }
+            GS_TRY(block_pass(w2, ROWS_NEW, qm, ROWS_OLD_PASS2, i0, D, p, part, ldp, h2, M, gpart, s));
+        } else {
+            hipLaunchKernelGGL(k_bupdate, dim3((unsigned)nblk), dim3(NT), 0, s, w2, (int)ROWS_NEW,
+                               (const double *)h2, M, (const double *)qm, (int)ROWS_OLD, D, p, gpart);
         }
-        for (int i = 0; i < pb; ++i) {
-            for (int pass = 0; pass < 2; ++pass) {
-                if (i > 0)
-                    hipLaunchKernelGGL(k_intra_dots, dim3((unsigned)nch2), dim3(NT), 0, s, wp, qm, D, i0, i, rank_after, part2);
-                hipLaunchKernelGGL(k_intra_update, dim3((unsigned)nch2), dim3(NT), 0, s, wp, qm, hc, D, i0, i, rank_after, part2, nch2, part3, M);
-            }
-            hipLaunchKernelGGL(k_intra_finalize, dim3((unsigned)nch2), dim3(NT), 0, s, wp, qm, hc, D, i0, i, rank_after, part3, nch2, cn, tol, kept_ws, M);
-            GS_TRY(hipGetLastError());
-        }
+        hipLaunchKernelGGL(k_gram_reduce, dim3(PB * PB / 64), dim3(NT), 0, s, (const double *)gpart, nblk, g2);
+        GS_TRY(hipGetLastError());
+        hipLaunchKernelGGL(k_small_chol, dim3(1), dim3(64), 0, s, (const double *)g2, p, lx, flag);
+        // final basis vectors Q_new = L^-1 V, and the panel's coefficients
+        hipLaunchKernelGGL(k_combine, dim3((unsigned)nblk), dim3(NT), 0, s,
+                           (const double *)(lx + PB * PB), (int)ROWS_NEW, (const double *)w2, (int)ROWS_NEW,
+                           qm, true, D, p);
+        GS_TRY(hipGetLastError());
+        hipLaunchKernelGGL(k_coef, dim3((unsigned)((i0 + PB + NT - 1) / NT), (unsigned)pb), dim3(NT), 0, s,
+                           (const double *)c1,
+                           (const double *)h2, M, i0 > 0, (const double *)lx, hc, M, p);
+        GS_TRY(hipGetLastError());
     }
 
     if (qt == GS_F64) GS_TRY(outputs_r<double>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s));

@@ -165,6 +165,42 @@ def test_compress_capacity_is_zero_filled():
     assert float(Rb[:, 19:].abs().max()) == 0.0
 
 
+def near_dependent_codebook():
+    """Rows 40 and 41 almost in the span of earlier rows (residuals about 1e-9
+    and 0 relative to the row), row 41 a combination in the same panel, a
+    duplicate and a negation across panels, D not a multiple of the chunk
+    sizes, several levels of the panel factor (D = 5000: 20 leaves)."""
+    g = np.random.default_rng(3)
+    C = g.standard_normal((100, 5000))
+    C[40] = C[3] + 1e-9 * g.standard_normal(5000)
+    C[41] = C[40] + C[7]
+    C[70] = C[33]
+    C[95] = -C[64]
+    return C
+
+
+@pytest.mark.parametrize("tol", [1e-12, 1e-10, 1e-8, 1e-3])
+def test_compress_rank_threshold(tol):
+    # the rank decisions follow the relative threshold as the oracle does:
+    # row 40 (residual ~1e-9) is kept below tol 1e-9 and dropped above
+    C = near_dependent_codebook()
+    Qo, Ro, kept_o, ro = oracle.compress(C, tol)
+    Q, R, r, kept, cnorm = gsm.gs_compress(dev(C, torch.float64), tol=tol)
+    torch.cuda.synchronize()
+    print("rank threshold", tol, r, ro, flush=True)
+    assert r == ro == (97 if tol < 1e-9 else 96)
+    assert list(host(kept).astype(int)) == list(kept_o)
+    Qg, Rg = host(Q), host(R)
+    assert np.abs(Qg @ Qg.T - np.eye(r)).max() <= 1e-12
+    # C = R Q where every row is kept or exactly dependent; a dropped
+    # near-dependent row keeps its own residual, as in the oracle
+    assert np.abs(Rg @ Qg - Ro @ Qo).max() <= 1e-11 * np.abs(C).max()
+    if tol > 1e-9:
+        # with the near-dependent row dropped every basis vector is well determined
+        assert np.abs(Qg - Qo).max() <= 1e-12
+        assert np.abs(Rg - Ro).max() <= 1e-12 * np.abs(Ro).max()
+
+
 def test_compress_rejects_nonfinite():
     C = rq_codebook("bipolar", 8, 64, 1)
     C[3, 7] = np.nan
