@@ -120,10 +120,12 @@ size_t gs_compress_workspace(int64_t M, int64_t D);
  * construction at initialisation Sec. 3.3).
  *
  * Builds an orthonormal basis Q of the row space of the codebook C and its
- * coordinates R with C = R Q, by blocked modified Gram-Schmidt with one
- * re-orthogonalisation pass, in fp64.  Codebook rows are taken in index
- * order; row i is dependent (adds no basis vector) when the norm of its part
- * outside the current span, after both passes, is <= tol * ||c_i||.  Kept rows
+ * coordinates R with C = R Q, by block Gram-Schmidt with re-orthogonalisation
+ * over panels of codebook rows, in fp64 (the rows of a panel are
+ * orthogonalised among themselves, twice, in the space of the panel's
+ * triangular factor).  Codebook rows are taken in index order; row i is
+ * dependent (adds no basis vector) when the norm of its part outside the
+ * current span, after both passes, is <= tol * ||c_i||.  Kept rows
  * are listed in `kept`, so basis vector k comes from codebook row kept[k].  R
  * is lower-echelon: R[i, k] = <c_i, q_k> for basis vectors created before row
  * i, R[kept[k], k] > 0, zero elsewhere.  With these rules Q and R are unique.
@@ -143,7 +145,9 @@ size_t gs_compress_workspace(int64_t M, int64_t D);
  *               256-byte aligned; contents on return are unspecified
  *   stream      synchronised before return
  * Errors: GS_ERR_NUMERIC if C holds a NaN or infinity (detected on the device;
- * outputs are then undefined).
+ * outputs are then undefined), or if the re-orthonormalisation of a panel
+ * meets a Gram matrix that is not positive definite (not expected for finite
+ * input).
  */
 gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
                       double tol,
