@@ -131,8 +131,7 @@ size_t gs_compress_workspace(int64_t M, int64_t D);
  * i, R[kept[k], k] > 0, zero elsewhere.  With these rules Q and R are unique.
  *
  *   C      in   M x D, ct in {F32, BF16, F64}, leading dimension ldc >= D
- *   M, D        1 <= M <= D (D < M needs the paper's partitioned bases, which
- *               this library does not build: GS_ERR_SHAPE)
+ *   M, D        1 <= M <= D (D < M: gs_compress_partitioned)
  *   tol         relative rank threshold, 0 <= tol < 1 (1e-10 recommended)
  *   Q      out  rank x D, qt in {F64, F32, BF16}, ldq >= D; rows rank..M-1
  *               are zero-filled (capacity M rows)
@@ -155,6 +154,78 @@ gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t 
                       void *R, gs_dtype rt, int64_t ldr,
                       int32_t *kept, float *cnorm, int32_t *rank,
                       void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * gs_compress_padded -- a basis of k > M vectors (Sec. 3.1: k may exceed M
+ * to preserve representation sparsity, the orthonormal basis being augmented
+ * by zero-padding and a linear transformation that spreads the signal over
+ * the added dimensions).  The basis of the codebook (as gs_compress builds
+ * it, rank r) is completed to k orthonormal vectors by the unit vectors
+ * e_0, e_1, ... taken in index order, each kept only if it leaves the span
+ * built so far by more than tol (the codebook's coordinates on the added
+ * vectors are zero: its coordinates are zero-padded).  With H given, an
+ * orthogonal k x k matrix (fp64, device, row-major, leading dimension ldh),
+ * the basis and the coordinates are transformed together:
+ *   Q = H Q_k    (k x D, orthonormal rows)       R = R_k H^T    (M x k)
+ * so C = R Q, every inner product and norm of coordinates is unchanged, and
+ * reconstruction x = t Q is exact; H = NULL means the identity (plain zero
+ * padding).  H must be orthogonal for these properties (not checked); a
+ * normalised Hadamard matrix spreads each coordinate vector's energy evenly
+ * over the k dimensions.
+ *   M, D, k     M <= k and M + k <= D
+ *   Q      out  k x D, qt in {F64, F32, BF16}, ldq >= D
+ *   R      out  M x k, rt in {F64, F32, BF16}, ldr >= k
+ *   kept   out  int32[M] device, nullable: the codebook rows that made the
+ *               first r basis vectors (before the transformation), -1 after
+ *   cnorm  out  float[M] device, nullable
+ *   rank   out  HOST int32: r, the codebook's rank
+ *   ws          device workspace of >= gs_compress_padded_workspace(M, D, k)
+ *               bytes, 256-byte aligned
+ * Errors as gs_compress.
+ */
+size_t gs_compress_padded_workspace(int64_t M, int64_t D, int64_t k);
+
+gs_status gs_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
+                             double tol, int64_t k, const double *H, int64_t ldh,
+                             void *Q, gs_dtype qt, int64_t ldq,
+                             void *R, gs_dtype rt, int64_t ldr,
+                             int32_t *kept, float *cnorm, int32_t *rank,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * gs_compress_partitioned -- compression of a codebook with more entries than
+ * dimensions (Sec. 3.1: when D < M the entries are split into subsets of at
+ * most D, each with its own orthonormal basis, the subsets put side by side
+ * again after reconstruction).  Rows are taken in consecutive subsets of
+ * `subset` rows (1 <= subset <= D; the last one may be shorter); each is
+ * compressed as by gs_compress.  With subset ranks r_g and offsets
+ * o_g = r_0 + ... + r_{g-1}:
+ *   Q      out  the subsets' bases stacked: rows o_g .. o_g + r_g - 1 are the
+ *               basis of subset g (orthonormal within a subset, not across
+ *               subsets); capacity M x D, rows past the total rank zero
+ *   R      out  block diagonal: the rows of subset g hold their coordinates
+ *               in columns o_g .. o_g + r_g - 1, zero elsewhere; capacity
+ *               M x M (ldr >= M); C = R Q, and R is lower echelon
+ *   kept   out  int32[M] device, nullable: codebook row of each basis vector,
+ *               -1 past the total rank
+ *   cnorm  out  float[M] device, nullable
+ *   ranks  out  HOST int32[ceil(M / subset)]: r_g
+ *   rank   out  HOST int32: the total, sum of r_g (the rows of Q in use)
+ *   ws          workspace of >= gs_compress_workspace(min(subset, M), D) bytes
+ * Any M >= 1 is accepted (subset = M <= D is gs_compress).  With these
+ * outputs: gs_project(X, Q) gives each subset's coordinates of x side by side,
+ * and gs_similarity of them against R (dot, or cosine with the dense ||x||^2
+ * from gs_project and cnorm) is exactly the similarity with every codebook
+ * entry; gs_prob2vec(P, R) gives coefficients whose gs_reconstruct against Q
+ * is p C.  Those coefficients are not the projection of p C (the stacked
+ * basis is not orthonormal), so they are restored, not compared directly.
+ */
+gs_status gs_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc,
+                                  double tol, int64_t subset,
+                                  void *Q, gs_dtype qt, int64_t ldq,
+                                  void *R, gs_dtype rt, int64_t ldr,
+                                  int32_t *kept, float *cnorm, int32_t *ranks, int32_t *rank,
+                                  void *ws, size_t ws_bytes, void *stream);
 
 /*
  * gs_compress_noalloc -- gs_compress for callers that cannot allocate device
@@ -201,13 +272,37 @@ gs_status gs_project(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t l
  * T = P R.
  *
  *   P      in   B x M, pt in {F32, BF16}, ldp >= M
- *   R      in   M x r, rt == pt (| GS_ECHELON), ldr >= r
+ *   R      in   M x r, rt == pt (| GS_ECHELON), ldr >= r (r may exceed M for
+ *               a padded basis, gs_compress_padded)
  *   T      out  B x r, tt in {F32, BF16}, ldt >= r
  * fp32 accumulation.
  */
 gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t ldp,
                       const void *R, gs_dtype rt, int64_t r, int64_t ldr,
                       void *T, gs_dtype tt, int64_t ldt, void *stream);
+
+/*
+ * gs_prob2vec_sparse -- probability vectorisation (Sec. 2.2, Sec. 3.1) of
+ * sparse probability rows: t_b = sum over the stored entries (j, p) of row b
+ * of p R_j, the Gram-loc of sum_j p_j c_j, reading only the rows of R the
+ * entries name.  Rows come in compressed sparse row form:
+ *
+ *   rowptr in   int64[B + 1] device: the entries of row b are
+ *               rowptr[b] .. rowptr[b + 1] - 1 (rowptr[0] = 0, nondecreasing,
+ *               rowptr[B] = nnz)
+ *   cols   in   int32[nnz] device: codebook index j of each entry, 0 <= j < M
+ *   vals   in   nnz probabilities p, type vt in {F32, BF16}
+ *   R      in   M x r, rt == vt (a GS_ECHELON flag is ignored), ldr >= r
+ *   T      out  B x r, tt in {F32, BF16}, ldt >= r
+ * A row's entries are summed in their stored order in fp32; a row without
+ * entries gives t = 0.  Entries whose index lies outside [0, M), and pointer
+ * ranges outside [0, nnz], are skipped on the device (never read out of
+ * bounds); the result is then that of the remaining entries.
+ */
+gs_status gs_prob2vec_sparse(const int64_t *rowptr, const int32_t *cols, const void *vals, gs_dtype vt,
+                             int64_t B, int64_t M, int64_t nnz,
+                             const void *R, gs_dtype rt, int64_t r, int64_t ldr,
+                             void *T, gs_dtype tt, int64_t ldt, void *stream);
 
 /*
  * gs_similarity -- similarity of each batch vector with every codebook vector,

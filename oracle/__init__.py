@@ -12,6 +12,9 @@ paper's W transposed: row j is codebook vector c_j; Q = U^T; R = T^T):
                   the codebook, rank = algebraic rank, built by Householder QR
                   (the paper's finite-precision construction) with column
                   skipping; C = R Q, R lower-echelon with positive pivots.
+* compress_padded -- Sec. 3.1 (k > M): the basis completed by unit vectors,
+                  coordinates zero-padded, then an optional orthogonal
+                  transformation H of both.
 * prob2vec     -- Sec. 2.2: v = sum_j p_j c_j, dense in D-space.
 * similarity   -- Sec. 2.2, Sec. 3.2 Eq. 2-3: scaled dot product or cosine of
                   a query with every codebook vector, dense in D-space.
@@ -159,6 +162,30 @@ def compress(C, tau: float = 1e-10):
         raise MemoryError("oracle compress: allocation failed")
     r = rank.value
     return Q[:r].copy(), R[:M, :r].copy(), kept[:r].copy(), r
+
+
+def compress_padded(C, k: int, H=None, tau: float = 1e-10):
+    """Basis of k vectors (Sec. 3.1, k > M): the codebook's basis completed by
+    the unit vectors e_0, e_1, ... in index order (each kept when it leaves the
+    span built so far), the codebook's coordinates zero-padded; then, with an
+    orthogonal k x k matrix H, Q' = H Q and R' = R H^T.  The completion is
+    the Householder compression of the codebook followed by the unit rows.
+    Returns (Q' k x D, R' M x k, kept, rank) with kept / rank those of the
+    codebook itself."""
+    C = _f64(C)
+    M, D = C.shape
+    aug = np.vstack([C, np.eye(D)[:k]])
+    Qa, Ra, kept_a, ra = compress(aug, tau)
+    if ra < k:
+        raise ValueError("the unit rows did not complete the basis to k vectors")
+    Qk = Qa[:k]
+    Rk = Ra[:M, :k]
+    r = int(np.sum(kept_a < M))
+    if H is not None:
+        H = _f64(H)
+        Qk = H @ Qk
+        Rk = Rk @ H.T
+    return Qk, Rk, kept_a[:r].copy(), r
 
 
 def prob2vec(P, C) -> np.ndarray:

@@ -139,7 +139,7 @@ gs_status check_compress(const char *fn, const void *C, gs_dtype ct, int64_t M, 
     if (!rank) return fail(GS_ERR_ARG, "%s: rank (host) is null", fn);
     if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "%s: M and D must be >= 1 (M=%lld, D=%lld)", fn,
                                     (long long)M, (long long)D);
-    if (M > D) return fail(GS_ERR_SHAPE, "%s: M=%lld > D=%lld needs partitioned bases, not supported",
+    if (M > D) return fail(GS_ERR_SHAPE, "%s: M=%lld > D=%lld needs partitioned bases (gs_compress_partitioned)",
                            fn, (long long)M, (long long)D);
     if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "%s: tol must be in [0, 1)", fn);
     GS_CHECK(check_matrix(C, "C", M, D, ldc, ct, false));
@@ -221,6 +221,93 @@ gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t 
     return finish_compress("gs_compress", e, nonfinite, r, rank);
 }
 
+gs_status gs_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                                  int64_t subset, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt,
+                                  int64_t ldr, int32_t *kept, float *cnorm, int32_t *ranks, int32_t *rank,
+                                  void *ws, size_t ws_bytes, void *stream) {
+    const char *fn = "gs_compress_partitioned";
+    if (!valid_dtype(ct) || !valid_dtype(qt) || !valid_dtype(rt))
+        return fail(GS_ERR_DTYPE, "%s: unknown element type", fn);
+    if (!rank || !ranks) return fail(GS_ERR_ARG, "%s: rank or ranks (host) is null", fn);
+    if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "%s: M and D must be >= 1", fn);
+    if (subset < 1 || subset > D)
+        return fail(GS_ERR_SHAPE, "%s: subset must be in [1, D] (subset=%lld, D=%lld)", fn, (long long)subset,
+                    (long long)D);
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "%s: tol must be in [0, 1)", fn);
+    GS_CHECK(check_matrix(C, "C", M, D, ldc, ct, false));
+    GS_CHECK(check_matrix(Q, "Q", M, D, ldq, qt, false));
+    GS_CHECK(check_matrix(R, "R", M, M, ldr, rt, false));
+    GS_CHECK(check_aligned(kept, 4, "kept"));
+    GS_CHECK(check_aligned(cnorm, 4, "cnorm"));
+    GS_CHECK(check_overlaps({span(C, M, D, ldc, esize(ct), "C")},
+                            {span(Q, M, D, ldq, esize(qt), "Q"), span(R, M, M, ldr, esize(rt), "R"),
+                             span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    const int64_t ms = subset < M ? subset : M;
+    if (!ws) return fail(GS_ERR_WORKSPACE, "%s: workspace is null", fn);
+    if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+        return fail(GS_ERR_ALIGN, "%s: workspace must be 256-byte aligned", fn);
+    const size_t need = compress_workspace(ms, D);
+    if (ws_bytes < need) return fail(GS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    {
+        const Span sW = span(ws, 1, (int64_t)need, (int64_t)need, 1, "workspace");
+        GS_CHECK(check_overlaps({sW}, {span(C, M, D, ldc, esize(ct), "C"), span(Q, M, D, ldq, esize(qt), "Q"),
+                                       span(R, M, M, ldr, esize(rt), "R"), span(kept, 1, M, M, 4, "kept"),
+                                       span(cnorm, 1, M, M, 4, "cnorm")}));
+    }
+    GS_CHECK(check_device());
+    int nonfinite = 0;
+    int32_t total = 0;
+    hipError_t e = run_compress_partitioned(C, ct, M, D, ldc, tol, subset, Q, qt, ldq, R, rt, ldr, kept, cnorm,
+                                            ranks, &total, &nonfinite, ws, (hipStream_t)stream);
+    return finish_compress(fn, e, nonfinite, total, rank);
+}
+
+size_t gs_compress_padded_workspace(int64_t M, int64_t D, int64_t k) {
+    if (M < 1 || D < 1 || k < M || M + k > D) return 0;
+    return compress_padded_workspace(M, D, k);
+}
+
+gs_status gs_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                             int64_t k, const double *H, int64_t ldh, void *Q, gs_dtype qt, int64_t ldq,
+                             void *R, gs_dtype rt, int64_t ldr, int32_t *kept, float *cnorm, int32_t *rank,
+                             void *ws, size_t ws_bytes, void *stream) {
+    const char *fn = "gs_compress_padded";
+    if (!valid_dtype(ct) || !valid_dtype(qt) || !valid_dtype(rt))
+        return fail(GS_ERR_DTYPE, "%s: unknown element type", fn);
+    if (!rank) return fail(GS_ERR_ARG, "%s: rank (host) is null", fn);
+    if (M < 1 || D < 1) return fail(GS_ERR_SHAPE, "%s: M and D must be >= 1", fn);
+    if (k < M || M + k > D)
+        return fail(GS_ERR_SHAPE, "%s: need M <= k and M + k <= D (M=%lld, k=%lld, D=%lld)", fn, (long long)M,
+                    (long long)k, (long long)D);
+    if (!(tol >= 0.0 && tol < 1.0)) return fail(GS_ERR_ARG, "%s: tol must be in [0, 1)", fn);
+    GS_CHECK(check_matrix(C, "C", M, D, ldc, ct, false));
+    GS_CHECK(check_matrix(H, "H", k, k, ldh, GS_F64, true));
+    GS_CHECK(check_matrix(Q, "Q", k, D, ldq, qt, false));
+    GS_CHECK(check_matrix(R, "R", M, k, ldr, rt, false));
+    GS_CHECK(check_aligned(kept, 4, "kept"));
+    GS_CHECK(check_aligned(cnorm, 4, "cnorm"));
+    GS_CHECK(check_overlaps({span(C, M, D, ldc, esize(ct), "C"), span(H, k, k, ldh, 8, "H")},
+                            {span(Q, k, D, ldq, esize(qt), "Q"), span(R, M, k, ldr, esize(rt), "R"),
+                             span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    if (!ws) return fail(GS_ERR_WORKSPACE, "%s: workspace is null", fn);
+    if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+        return fail(GS_ERR_ALIGN, "%s: workspace must be 256-byte aligned", fn);
+    const size_t need = compress_padded_workspace(M, D, k);
+    if (ws_bytes < need) return fail(GS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, ws_bytes, need);
+    {
+        const Span sW = span(ws, 1, (int64_t)need, (int64_t)need, 1, "workspace");
+        GS_CHECK(check_overlaps({sW}, {span(C, M, D, ldc, esize(ct), "C"), span(H, k, k, ldh, 8, "H"),
+                                       span(Q, k, D, ldq, esize(qt), "Q"), span(R, M, k, ldr, esize(rt), "R"),
+                                       span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
+    }
+    GS_CHECK(check_device());
+    int nonfinite = 0;
+    int32_t r = 0;
+    hipError_t e = run_compress_padded(C, ct, M, D, ldc, tol, k, H, ldh, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
+                                       &nonfinite, ws, (hipStream_t)stream);
+    return finish_compress(fn, e, nonfinite, r, rank);
+}
+
 gs_status gs_compress_noalloc(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                               void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                               int32_t *kept, float *cnorm, int32_t *rank, void *stream) {
@@ -275,7 +362,7 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
     const gs_dtype rt = coord_type(rt_in, &ech);
     if (!is_batch_type(pt) || rt != pt || !is_batch_type(tt))
         return fail(GS_ERR_DTYPE, "gs_prob2vec: P/R must be both f32 or both bf16 and T f32 or bf16");
-    if (B < 0 || M < 1 || r < 1 || r > M) return fail(GS_ERR_SHAPE, "gs_prob2vec: need B >= 0 and 1 <= r <= M");
+    if (B < 0 || M < 1 || r < 1) return fail(GS_ERR_SHAPE, "gs_prob2vec: need B >= 0, M >= 1 and r >= 1");
     GS_CHECK(check_matrix(P, "P", B, M, ldp, pt, false));
     GS_CHECK(check_matrix(R, "R", M, r, ldr, rt, false));
     GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
@@ -283,7 +370,10 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
                             {span(T, B, r, ldt, esize(tt), "T")}));
     if (B == 0) return ok();
     GS_CHECK(check_device());
-    if (M <= SMALL_MAX && r <= SMALL_MAX) {
+    // small-codebook kernel for r <= M <= 64 (the codebook block is padded
+    // to M's size); more coordinates than entries (a padded basis) and larger
+    // codebooks take the matrix-core product
+    if (M <= SMALL_MAX && r <= M) {
         SmallArgs a{};
         a.In = P; a.ldin = ldp; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = T; a.ldout = ldt;
         return launched(launch_small_prob2vec(pt, tt, a, (hipStream_t)stream), "gs_prob2vec");
@@ -292,6 +382,35 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
     a.A = P; a.lda = ldp; a.B = R; a.ldb = ldr; a.C = T; a.ldc = ldt; a.M = B; a.N = r; a.K = M;
     a.echelon = ech;
     return launched(launch_gemm(pt, rt, tt, true, EPI_STORE, a, (hipStream_t)stream), "gs_prob2vec");
+}
+
+gs_status gs_prob2vec_sparse(const int64_t *rowptr, const int32_t *cols, const void *vals, gs_dtype vt,
+                             int64_t B, int64_t M, int64_t nnz,
+                             const void *R, gs_dtype rt_in, int64_t r, int64_t ldr,
+                             void *T, gs_dtype tt, int64_t ldt, void *stream) {
+    bool ech;
+    const gs_dtype rt = coord_type(rt_in, &ech);
+    if (!is_batch_type(vt) || rt != vt || !is_batch_type(tt))
+        return fail(GS_ERR_DTYPE, "gs_prob2vec_sparse: values/R must be both f32 or both bf16 and T f32 or bf16");
+    if (B < 0 || M < 1 || r < 1 || r > M || nnz < 0)
+        return fail(GS_ERR_SHAPE, "gs_prob2vec_sparse: need B >= 0, nnz >= 0 and 1 <= r <= M");
+    if (B > 0 && !rowptr) return fail(GS_ERR_ARG, "gs_prob2vec_sparse: rowptr is null");
+    if (nnz > 0 && (!cols || !vals)) return fail(GS_ERR_ARG, "gs_prob2vec_sparse: cols or vals is null");
+    GS_CHECK(check_aligned(rowptr, 8, "rowptr"));
+    GS_CHECK(check_aligned(cols, 4, "cols"));
+    GS_CHECK(check_aligned(vals, esize(vt), "vals"));
+    GS_CHECK(check_matrix(R, "R", M, r, ldr, rt, false));
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    GS_CHECK(check_overlaps({span(rowptr, 1, B > 0 ? B + 1 : 0, B + 1, 8, "rowptr"),
+                             span(cols, 1, nnz, nnz, 4, "cols"), span(vals, 1, nnz, nnz, esize(vt), "vals"),
+                             span(R, M, r, ldr, esize(rt), "R")},
+                            {span(T, B, r, ldt, esize(tt), "T")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    SparseArgs a{};
+    a.rowptr = rowptr; a.cols = cols; a.vals = vals; a.B = B; a.M = M; a.nnz = nnz;
+    a.R = R; a.ldr = ldr; a.r = r; a.T = T; a.ldt = ldt;
+    return launched(launch_sparse_prob2vec(vt, tt, a, (hipStream_t)stream), "gs_prob2vec_sparse");
 }
 
 static gs_status check_sim_common(const char *fn, const void *T, gs_dtype tt, int64_t B, int64_t r,

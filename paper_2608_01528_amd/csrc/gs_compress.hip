@@ -769,7 +769,7 @@ __global__ void __launch_bounds__(NT) k_coef(const double *C1, const double *H2,
 template <typename TQ, typename TR>
 __global__ void k_outputs(const double *qm, const double *hc, const double *cnd,
                           const int32_t *rank_after, const int32_t *kept_ws, int64_t M, int64_t D,
-                          TQ *Q, int64_t ldq, TR *R, int64_t ldr, int32_t *kept, float *cnorm) {
+                          TQ *Q, int64_t ldq, TR *R, int64_t ldr, int32_t *kept, float *cnorm, int64_t row_base) {
     const int r = rank_after[M - 1];
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -788,27 +788,28 @@ __global__ void k_outputs(const double *qm, const double *hc, const double *cnd,
         else R[i * ldr + k].bits = f64_to_bf16(v);
     }
     for (int64_t e = i0; e < M; e += stride) {
-        if (kept) kept[e] = (e < r) ? kept_ws[e] : -1;
+        if (kept) kept[e] = (e < r) ? (int32_t)(kept_ws[e] + row_base) : -1;
         if (cnorm) cnorm[e] = (float)cnd[e];
     }
 }
 
 template <typename TQ, typename TR>
 hipError_t launch_outputs(const WsLayout &L, char *ws, int64_t M, int64_t D, void *Q, int64_t ldq,
-                          void *R, int64_t ldr, int32_t *kept, float *cnorm, hipStream_t s) {
+                          void *R, int64_t ldr, int32_t *kept, float *cnorm, int64_t row_base, hipStream_t s) {
     hipLaunchKernelGGL((k_outputs<TQ, TR>), dim3(1024), dim3(NT), 0, s,
                        (const double *)(ws + L.qm), (const double *)(ws + L.hc),
                        (const double *)(ws + L.cn), (const int32_t *)(ws + L.rank_after),
-                       (const int32_t *)(ws + L.kept), M, D, (TQ *)Q, ldq, (TR *)R, ldr, kept, cnorm);
+                       (const int32_t *)(ws + L.kept), M, D, (TQ *)Q, ldq, (TR *)R, ldr, kept, cnorm, row_base);
     return hipGetLastError();
 }
 
 template <typename TQ>
 hipError_t outputs_r(gs_dtype rt, const WsLayout &L, char *ws, int64_t M, int64_t D, void *Q,
-                     int64_t ldq, void *R, int64_t ldr, int32_t *kept, float *cnorm, hipStream_t s) {
-    if (rt == GS_F64) return launch_outputs<TQ, double>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s);
-    if (rt == GS_F32) return launch_outputs<TQ, float>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s);
-    return launch_outputs<TQ, bf16_t>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s);
+                     int64_t ldq, void *R, int64_t ldr, int32_t *kept, float *cnorm, int64_t row_base,
+                     hipStream_t s) {
+    if (rt == GS_F64) return launch_outputs<TQ, double>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s);
+    if (rt == GS_F32) return launch_outputs<TQ, float>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s);
+    return launch_outputs<TQ, bf16_t>(L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s);
 }
 
 template <typename T>
@@ -873,7 +874,7 @@ size_t compress_workspace(int64_t M, int64_t D) { return layout(M, D).total; }
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                         void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                         int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite, void *ws_,
-                        hipStream_t s) {
+                        hipStream_t s, int64_t row_base) {
     const WsLayout L = layout(M, D);
     char *ws = static_cast<char *>(ws_);
     double *qm = (double *)(ws + L.qm), *wp = (double *)(ws + L.wp), *w2 = (double *)(ws + L.w2);
@@ -932,9 +933,9 @@ hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_
         GS_TRY(hipGetLastError());
     }
 
-    if (qt == GS_F64) GS_TRY(outputs_r<double>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s));
-    else if (qt == GS_F32) GS_TRY(outputs_r<float>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s));
-    else GS_TRY(outputs_r<bf16_t>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, s));
+    if (qt == GS_F64) GS_TRY(outputs_r<double>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s));
+    else if (qt == GS_F32) GS_TRY(outputs_r<float>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s));
+    else GS_TRY(outputs_r<bf16_t>(rt, L, ws, M, D, Q, ldq, R, ldr, kept, cnorm, row_base, s));
 
     int32_t host[2] = {0, 0};
     GS_TRY(hipMemcpyAsync(&host[0], rank_after + (M - 1), sizeof(int32_t), hipMemcpyDeviceToHost, s));
@@ -942,6 +943,197 @@ hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_
     GS_TRY(hipStreamSynchronize(s));
     *rank = host[0];
     *nonfinite = host[1];
+    return hipSuccess;
+}
+
+namespace {
+
+// Fill a rows x cols matrix (leading dimension ld, element size es) with
+// zero bits, or int32 matrices with fill_i32.
+__global__ void k_fill(char *base, int64_t rows, int64_t cols, int64_t ld, int es, int32_t fill_i32) {
+    const int64_t n = rows * cols;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+        const int64_t i = e / cols, k = e % cols;
+        char *p = base + (i * ld + k) * es;
+        if (es == 8) *reinterpret_cast<double *>(p) = 0.0;
+        else if (es == 4) *reinterpret_cast<int32_t *>(p) = fill_i32;
+        else *reinterpret_cast<uint16_t *>(p) = 0;
+    }
+}
+
+size_t esz(gs_dtype t) { return t == GS_F64 ? 8 : (t == GS_F32 ? 4 : 2); }
+
+// The augmented codebook of the padded basis, fp64: rows 0 .. M-1 the
+// codebook, rows M .. M + k - 1 the unit vectors e_0 .. e_{k-1}.
+template <typename T>
+__global__ void k_augment(const T *C, int64_t ldc, int64_t M, int64_t D, int64_t k, double *A) {
+    const int64_t n = (M + k) * D;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+        const int64_t i = e / D, d = e % D;
+        A[e] = (i < M) ? ld_f64<T>(C, i * ldc + d) : ((d == i - M) ? 1.0 : 0.0);
+    }
+}
+
+// out = op(A) op(B) in fp64 for small sizes (m x n, inner dimension kk):
+// A is m x kk (lda); B is kk x n (ldb), or n x kk read transposed when
+// b_trans.  16 x 16 tiles through LDS, one output per thread.
+__global__ void __launch_bounds__(256) k_dgemm(const double *A, int64_t lda, const double *B, int64_t ldb,
+                                               bool b_trans, double *out, int64_t ldo, int64_t m, int64_t n,
+                                               int64_t kk) {
+    __shared__ double As[16][17], Bs[16][17];
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    const int64_t i = (int64_t)blockIdx.y * 16 + ty, j = (int64_t)blockIdx.x * 16 + tx;
+    double acc = 0.0;
+    for (int64_t t0 = 0; t0 < kk; t0 += 16) {
+        As[ty][tx] = (i < m && t0 + tx < kk) ? A[i * lda + t0 + tx] : 0.0;
+        const int64_t bt = t0 + ty;
+        double bv = 0.0;
+        if (bt < kk && j < n) bv = b_trans ? B[j * ldb + bt] : B[bt * ldb + j];
+        Bs[ty][tx] = bv;
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc += As[ty][q] * Bs[q][tx];
+        __syncthreads();
+    }
+    if (i < m && j < n) out[i * ldo + j] = acc;
+}
+
+// Store an fp64 matrix (rows x cols, leading dimension lds) as type T.
+template <typename T>
+__global__ void k_store(const double *src, int64_t lds, T *dst, int64_t ldd, int64_t rows, int64_t cols) {
+    const int64_t n = rows * cols;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += stride) {
+        const int64_t i = e / cols, c = e % cols;
+        const double v = src[i * lds + c];
+        if constexpr (sizeof(T) == 8) dst[i * ldd + c] = v;
+        else if constexpr (sizeof(T) == 4) dst[i * ldd + c] = (float)v;
+        else dst[i * ldd + c].bits = f64_to_bf16(v);
+    }
+}
+
+hipError_t store_as(gs_dtype t, const double *src, int64_t lds, void *dst, int64_t ldd, int64_t rows, int64_t cols,
+                    hipStream_t s) {
+    if (t == GS_F64) hipLaunchKernelGGL((k_store<double>), dim3(1024), dim3(NT), 0, s, src, lds, (double *)dst, ldd, rows, cols);
+    else if (t == GS_F32) hipLaunchKernelGGL((k_store<float>), dim3(1024), dim3(NT), 0, s, src, lds, (float *)dst, ldd, rows, cols);
+    else hipLaunchKernelGGL((k_store<bf16_t>), dim3(1024), dim3(NT), 0, s, src, lds, (bf16_t *)dst, ldd, rows, cols);
+    return hipGetLastError();
+}
+
+struct PadLayout { size_t aug, qa, ra, qh, rh, kept, cn, cws, total; };
+
+PadLayout pad_layout(int64_t M, int64_t D, int64_t k) {
+    PadLayout L;
+    const int64_t Ma = M + k;
+    size_t o = 0;
+    L.aug = o;  o = align256(o + sizeof(double) * Ma * D);
+    L.qa = o;   o = align256(o + sizeof(double) * Ma * D);
+    L.ra = o;   o = align256(o + sizeof(double) * Ma * Ma);
+    L.qh = o;   o = align256(o + sizeof(double) * k * D);
+    L.rh = o;   o = align256(o + sizeof(double) * M * k);
+    L.kept = o; o = align256(o + sizeof(int32_t) * Ma);
+    L.cn = o;   o = align256(o + sizeof(float) * Ma);
+    L.cws = o;  o = align256(o + compress_workspace(Ma, D));
+    L.total = o;
+    return L;
+}
+
+// Copy n int32 / float values (4-byte elements).
+__global__ void k_copy4(const int32_t *src, int32_t *dst, int64_t n, int64_t valid) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < n) dst[e] = (e < valid) ? src[e] : -1;
+}
+
+}  // namespace
+
+size_t compress_padded_workspace(int64_t M, int64_t D, int64_t k) { return pad_layout(M, D, k).total; }
+
+hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                               int64_t k, const double *H, int64_t ldh, void *Q, gs_dtype qt, int64_t ldq,
+                               void *R, gs_dtype rt, int64_t ldr, int32_t *kept, float *cnorm, int32_t *rank,
+                               int *nonfinite, void *ws_, hipStream_t s) {
+    const PadLayout L = pad_layout(M, D, k);
+    char *ws = static_cast<char *>(ws_);
+    double *aug = (double *)(ws + L.aug), *qa = (double *)(ws + L.qa), *ra = (double *)(ws + L.ra);
+    int32_t *kept_a = (int32_t *)(ws + L.kept);
+    float *cn_a = (float *)(ws + L.cn);
+    const int64_t Ma = M + k;
+    if (ct == GS_F32) hipLaunchKernelGGL((k_augment<float>), dim3(1024), dim3(NT), 0, s, (const float *)C, ldc, M, D, k, aug);
+    else if (ct == GS_F64) hipLaunchKernelGGL((k_augment<double>), dim3(1024), dim3(NT), 0, s, (const double *)C, ldc, M, D, k, aug);
+    else hipLaunchKernelGGL((k_augment<bf16_t>), dim3(1024), dim3(NT), 0, s, (const bf16_t *)C, ldc, M, D, k, aug);
+    GS_TRY(hipGetLastError());
+    // the augmented codebook, codebook rows first: its first basis vectors and
+    // the codebook's coordinates are those of the plain compression, and the
+    // unit rows then complete the basis (its rank is at least k)
+    int32_t ra_rank = 0;
+    GS_TRY(run_compress(aug, GS_F64, Ma, D, D, tol, qa, GS_F64, D, ra, GS_F64, Ma, kept_a, cn_a, &ra_rank,
+                        nonfinite, ws + L.cws, s));
+    // rank of the codebook itself: the kept rows below M (kept is in index order)
+    int32_t r = 0;
+    GS_TRY(hipMemcpyAsync(&r, ws + L.cws + layout(Ma, D).rank_after + sizeof(int32_t) * (M - 1), sizeof(int32_t),
+                          hipMemcpyDeviceToHost, s));
+    const double *qk = qa, *rk = ra;     // first k basis vectors; the codebook rows' coordinates on them
+    int64_t ldqk = D, ldrk = Ma;
+    if (H) {
+        double *qh = (double *)(ws + L.qh), *rh = (double *)(ws + L.rh);
+        hipLaunchKernelGGL(k_dgemm, dim3((unsigned)((D + 15) / 16), (unsigned)((k + 15) / 16)), dim3(256), 0, s,
+                           H, ldh, (const double *)qa, D, false, qh, D, k, D, k);
+        hipLaunchKernelGGL(k_dgemm, dim3((unsigned)((k + 15) / 16), (unsigned)((M + 15) / 16)), dim3(256), 0, s,
+                           (const double *)ra, Ma, H, ldh, true, rh, k, M, k, k);
+        GS_TRY(hipGetLastError());
+        qk = qh; rk = rh; ldrk = k;
+    }
+    GS_TRY(store_as(qt, qk, ldqk, Q, ldq, k, D, s));
+    GS_TRY(store_as(rt, rk, ldrk, R, ldr, M, k, s));
+    GS_TRY(hipStreamSynchronize(s));      // r is on the host now
+    if (kept)
+        hipLaunchKernelGGL(k_copy4, dim3((unsigned)((M + NT - 1) / NT)), dim3(NT), 0, s, (const int32_t *)kept_a,
+                           kept, M, (int64_t)r);
+    if (cnorm)
+        hipLaunchKernelGGL(k_copy4, dim3((unsigned)((M + NT - 1) / NT)), dim3(NT), 0, s, (const int32_t *)cn_a,
+                           (int32_t *)cnorm, M, M);
+    GS_TRY(hipGetLastError());
+    GS_TRY(hipStreamSynchronize(s));
+    *rank = r;
+    (void)ra_rank;
+    return hipSuccess;
+}
+
+hipError_t run_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                                    int64_t subset, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt,
+                                    int64_t ldr, int32_t *kept, float *cnorm, int32_t *ranks, int32_t *total,
+                                    int *nonfinite, void *ws, hipStream_t s) {
+    // R's capacity starts at zero: each subset writes its own block only
+    hipLaunchKernelGGL(k_fill, dim3(1024), dim3(NT), 0, s, (char *)R, M, M, ldr, (int)esz(rt), 0);
+    GS_TRY(hipGetLastError());
+    int64_t o = 0, end = 0;
+    *nonfinite = 0;
+    for (int64_t m0 = 0, g = 0; m0 < M; m0 += subset, ++g) {
+        const int64_t mg = (M - m0 < subset) ? M - m0 : subset;
+        int32_t rg = 0;
+        int nf = 0;
+        GS_TRY(run_compress(static_cast<const char *>(C) + m0 * ldc * (int64_t)esz(ct), ct, mg, D, ldc, tol,
+                            static_cast<char *>(Q) + o * ldq * (int64_t)esz(qt), qt, ldq,
+                            static_cast<char *>(R) + (m0 * ldr + o) * (int64_t)esz(rt), rt, ldr,
+                            kept ? kept + o : nullptr, cnorm ? cnorm + m0 : nullptr, &rg, &nf, ws, s, m0));
+        ranks[g] = rg;
+        *nonfinite |= nf;
+        end = o + mg;         // rows o .. o + mg - 1 of Q / entries of kept were written
+        o += rg;
+    }
+    // capacity past the last subset's frame: zero rows of Q, kept entries -1
+    if (end < M) {
+        hipLaunchKernelGGL(k_fill, dim3(1024), dim3(NT), 0, s, static_cast<char *>(Q) + end * ldq * (int64_t)esz(qt),
+                           M - end, D, ldq, (int)esz(qt), 0);
+        if (kept)
+            hipLaunchKernelGGL(k_fill, dim3(64), dim3(NT), 0, s, (char *)(kept + end), (int64_t)1, M - end, M - end,
+                               4, -1);
+        GS_TRY(hipGetLastError());
+        GS_TRY(hipStreamSynchronize(s));
+    }
+    *total = (int32_t)o;
     return hipSuccess;
 }
 

@@ -216,11 +216,37 @@ int64_t soft_select_tiles(int64_t B);
 int soft_select_pad(int64_t M);
 hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s);
 
+// Probability vectorisation of sparse (CSR) probability rows.
+struct SparseArgs {
+    const int64_t *rowptr;             // B + 1 entries
+    const int32_t *cols;               // nnz column indices
+    const void *vals;                  // nnz values (type of R)
+    int64_t B, M, nnz;
+    const void *R; int64_t ldr;        // M x r
+    int64_t r;
+    void *T; int64_t ldt;              // B x r
+};
+hipError_t launch_sparse_prob2vec(gs_dtype tv, gs_dtype tt, const SparseArgs &a, hipStream_t s);
+
 // Compression.
 size_t compress_workspace(int64_t M, int64_t D);
+// row_base is added to the kept row indices (a subset's first codebook row).
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                         void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                         int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite,
-                        void *ws, hipStream_t s);
+                        void *ws, hipStream_t s, int64_t row_base = 0);
+// Basis completed to k vectors by unit vectors (coordinates zero-padded),
+// optionally transformed by an orthogonal k x k matrix H.
+size_t compress_padded_workspace(int64_t M, int64_t D, int64_t k);
+hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                               int64_t k, const double *H, int64_t ldh, void *Q, gs_dtype qt, int64_t ldq,
+                               void *R, gs_dtype rt, int64_t ldr, int32_t *kept, float *cnorm, int32_t *rank,
+                               int *nonfinite, void *ws, hipStream_t s);
+// Consecutive subsets of `subset` codebook rows, each compressed on its own;
+// bases stacked in Q, coordinate blocks on R's block diagonal.
+hipError_t run_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
+                                    int64_t subset, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt,
+                                    int64_t ldr, int32_t *kept, float *cnorm, int32_t *ranks, int32_t *total,
+                                    int *nonfinite, void *ws, hipStream_t s);
 
 }  // namespace gs

@@ -4,7 +4,8 @@ Two layers with the C names:
 
 * `lib()` returns the loaded shared library; its `gs_*` functions take raw
   pointers exactly as declared in the header.
-* `gs_compress`, `gs_compress_noalloc`, `gs_project`, `gs_prob2vec`, `gs_similarity`,
+* `gs_compress`, `gs_compress_padded`, `gs_compress_partitioned`, `gs_compress_noalloc`, `gs_project`, `gs_prob2vec`, `gs_prob2vec_sparse`,
+  `gs_similarity`,
   `gs_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
   below take torch tensors on the current
   GPU, allocate the outputs with torch, and pass pointers, sizes and the
@@ -55,6 +56,13 @@ _SIGS = {
     "gs_compress": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double,
                      _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
                      _vp, _vp, _i32p, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "gs_compress_padded_workspace": ([_i64, _i64, _i64], ctypes.c_size_t),
+    "gs_compress_padded": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double, _i64, _vp, _i64,
+                            _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
+                            _vp, _vp, _i32p, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "gs_compress_partitioned": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double, _i64,
+                                 _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
+                                 _vp, _vp, _i32p, _i32p, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
     "gs_compress_noalloc": ([_vp, ctypes.c_int, _i64, _i64, _i64, ctypes.c_double,
                              _vp, ctypes.c_int, _i64, _vp, ctypes.c_int, _i64,
                              _vp, _vp, _i32p, _vp], ctypes.c_int),
@@ -78,6 +86,9 @@ class SoftGroup(ctypes.Structure):
                 ("B", _i64), ("M", _i64), ("r", _i64), ("T", _vp), ("ldt", _i64),
                 ("S", _vp), ("lds", _i64), ("argmax", _vp), ("A", _vp), ("lda", _i64)]
 
+
+_SIGS["gs_prob2vec_sparse"] = ([_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                                _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
 
 _SIGS["gs_bind_restored"] = ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ctypes.c_int, _i64,
                      _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
@@ -171,6 +182,65 @@ def gs_compress(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dt
     return Q[:r], R[:, :r], r, kept[:r], cnorm
 
 
+def gs_compress_partitioned(C: torch.Tensor, subset: int | None = None, tol: float = 1e-10,
+                            q_dtype=torch.float64, r_dtype=torch.float64, workspace: torch.Tensor | None = None):
+    """Compress codebook C (M x D, any M) in consecutive subsets of `subset`
+    rows (default D).  Returns (Q, R, rank, ranks, kept, cnorm): Q the stacked
+    bases (rank x D), R (M x rank) block diagonal, ranks the subsets' ranks."""
+    ct, ldc = _mat(C, "C")
+    M, D = C.shape
+    subset = D if subset is None else int(subset)
+    dev = C.device
+    Q = alloc_rows(M, D, q_dtype, dev)
+    R = alloc_rows(M, M, r_dtype, dev)
+    kept = torch.empty(M, dtype=torch.int32, device=dev)
+    cnorm = torch.empty(M, dtype=torch.float32, device=dev)
+    need = compress_workspace_bytes(min(subset, M), D)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1) + 256, dtype=torch.uint8, device=dev)
+    base = workspace.data_ptr()
+    off = (-base) % 256
+    nsub = (M + subset - 1) // subset
+    ranks = (ctypes.c_int32 * nsub)()
+    rank = ctypes.c_int32(0)
+    _check(lib().gs_compress_partitioned(_ptr(C), ct, M, D, ldc, float(tol), subset, _ptr(Q), _DT[q_dtype],
+                                         Q.stride(0), _ptr(R), _DT[r_dtype], R.stride(0), _ptr(kept), _ptr(cnorm),
+                                         ranks, ctypes.byref(rank), ctypes.c_void_p(base + off),
+                                         workspace.numel() - off, _stream()))
+    r = rank.value
+    return Q[:r], R[:, :r], r, list(ranks), kept[:r], cnorm
+
+
+def gs_compress_padded(C: torch.Tensor, k: int, H: torch.Tensor | None = None, tol: float = 1e-10,
+                       q_dtype=torch.float64, r_dtype=torch.float64, workspace: torch.Tensor | None = None):
+    """Basis of k >= M vectors (the codebook's, completed by unit vectors),
+    optionally transformed by an orthogonal k x k fp64 matrix H.  Returns
+    (Q k x D, R M x k, rank, kept, cnorm)."""
+    ct, ldc = _mat(C, "C")
+    M, D = C.shape
+    dev = C.device
+    Q = alloc_rows(k, D, q_dtype, dev)
+    R = alloc_rows(M, k, r_dtype, dev)
+    kept = torch.empty(M, dtype=torch.int32, device=dev)
+    cnorm = torch.empty(M, dtype=torch.float32, device=dev)
+    ldh = k
+    if H is not None:
+        if H.dtype != torch.float64:
+            raise ValueError("H must be float64")
+        _, ldh = _mat(H, "H")
+    need = int(lib().gs_compress_padded_workspace(M, D, k))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1) + 256, dtype=torch.uint8, device=dev)
+    base = workspace.data_ptr()
+    off = (-base) % 256
+    rank = ctypes.c_int32(0)
+    _check(lib().gs_compress_padded(_ptr(C), ct, M, D, ldc, float(tol), int(k), _ptr(H), ldh, _ptr(Q), _DT[q_dtype],
+                                    Q.stride(0), _ptr(R), _DT[r_dtype], R.stride(0), _ptr(kept), _ptr(cnorm),
+                                    ctypes.byref(rank), ctypes.c_void_p(base + off), workspace.numel() - off,
+                                    _stream()))
+    return Q, R, rank.value, kept, cnorm
+
+
 def gs_compress_noalloc(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float64, r_dtype=torch.float64,
                         out=None):
     """gs_compress without a workspace (the library's static scratch array).
@@ -224,6 +294,23 @@ def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Ten
         out = alloc_rows(B, r, out_dtype or P.dtype, P.device)
     tt, ldt = _mat(out, "T")
     _check(lib().gs_prob2vec(_ptr(P), pt, B, M, ldp, _ptr(R), rt, r, ldr, _ptr(out), tt, ldt, _stream()))
+    return out
+
+
+def gs_prob2vec_sparse(rowptr: torch.Tensor, cols: torch.Tensor, vals: torch.Tensor, R: torch.Tensor,
+                       out_dtype=None, out: torch.Tensor | None = None):
+    """T = P R for P in compressed sparse row form: rowptr (int64, B + 1),
+    cols (int32, nnz), vals (nnz, the type of R)."""
+    if rowptr.dtype != torch.int64 or cols.dtype != torch.int32:
+        raise ValueError("rowptr must be int64 and cols int32")
+    rt, ldr = _mat(R, "R")
+    M, r = R.shape
+    B = rowptr.numel() - 1
+    if out is None:
+        out = alloc_rows(B, r, out_dtype or R.dtype, R.device)
+    tt, ldt = _mat(out, "T")
+    _check(lib().gs_prob2vec_sparse(_ptr(rowptr), _ptr(cols), _ptr(vals), _DT[vals.dtype], B, M, cols.numel(),
+                                    _ptr(R), rt, r, ldr, _ptr(out), tt, ldt, _stream()))
     return out
 
 

@@ -76,7 +76,7 @@ def test_compress_validation(L):
     assert compress(L, ct=7) == gsm.GS_ERR_DTYPE
     assert compress(L, rank=False) == gsm.GS_ERR_ARG
     assert compress(L, M=0) == gsm.GS_ERR_SHAPE
-    assert compress(L, M=65, ldr=65) == gsm.GS_ERR_SHAPE and "partitioned" in err(L)
+    assert compress(L, M=65, ldr=65) == gsm.GS_ERR_SHAPE and "gs_compress_partitioned" in err(L)
     assert compress(L, tol=1.5) == gsm.GS_ERR_ARG
     assert compress(L, tol=float("nan")) == gsm.GS_ERR_ARG
     assert compress(L, C=NULL) == gsm.GS_ERR_ARG and "C" in err(L)
@@ -88,6 +88,45 @@ def test_compress_validation(L):
     assert compress(L, wsb=100) == gsm.GS_ERR_WORKSPACE and "needed" in err(L)
     assert compress(L, Q=A1) == gsm.GS_ERR_ARG and "overlaps" in err(L)   # output aliases input
     assert compress(L, kept=P(0x20000000 + 8)) == gsm.GS_ERR_ARG            # kept inside Q
+
+
+def test_compress_partitioned_validation(L):
+    ranks = (ctypes.c_int32 * 8)()
+    rk = ctypes.c_int32(0)
+
+    def call(M=100, D=32, subset=32, ct=gsm.GS_F32, ldc=32, Q=A2, ldq=32, R=A3, ldr=100, ws=WS, wsb=1 << 30,
+             rank=True, rks=True):
+        return L.gs_compress_partitioned(A1, ct, M, D, ldc, 1e-10, subset, Q, gsm.GS_F64, ldq, R, gsm.GS_F64, ldr,
+                                         NULL, NULL, ranks if rks else None, ctypes.byref(rk) if rank else None,
+                                         ws, wsb, None)
+    assert call(ct=9) == gsm.GS_ERR_DTYPE
+    assert call(rank=False) == gsm.GS_ERR_ARG and call(rks=False) == gsm.GS_ERR_ARG
+    assert call(subset=0) == gsm.GS_ERR_SHAPE and call(subset=33) == gsm.GS_ERR_SHAPE
+    assert call(ldr=99) == gsm.GS_ERR_SHAPE                              # R holds M x M
+    assert call(ws=NULL) == gsm.GS_ERR_WORKSPACE
+    assert call(wsb=16) == gsm.GS_ERR_WORKSPACE and "needed" in err(L)
+    assert call(Q=A1) == gsm.GS_ERR_ARG                                   # Q over C
+    # the workspace is sized by one subset, not by the whole codebook
+    assert L.gs_compress_workspace(32, 32) < L.gs_compress_workspace(32, 32) * 2
+    assert call(wsb=L.gs_compress_workspace(32, 32)) == gsm.GS_ERR_DEVICE  # valid: only the device is missing
+
+
+def test_compress_padded_validation(L):
+    rk = ctypes.c_int32(0)
+
+    def call(M=10, D=64, k=20, ct=gsm.GS_F32, H=NULL, ldh=20, ldq=64, ldr=20, ws=WS, wsb=1 << 30, Q=A2, R=A3):
+        return L.gs_compress_padded(A1, ct, M, D, 64, 1e-10, k, H, ldh, Q, gsm.GS_F64, ldq, R, gsm.GS_F64, ldr,
+                                    NULL, NULL, ctypes.byref(rk), ws, wsb, None)
+    assert call(ct=7) == gsm.GS_ERR_DTYPE
+    assert call(k=9) == gsm.GS_ERR_SHAPE                     # k < M
+    assert call(k=55) == gsm.GS_ERR_SHAPE                    # M + k > D
+    assert call(ldr=19) == gsm.GS_ERR_SHAPE                  # R is M x k
+    assert call(H=P(0x60000004)) == gsm.GS_ERR_ALIGN         # fp64 H
+    assert call(ldh=19, H=A4) == gsm.GS_ERR_SHAPE
+    assert call(wsb=100) == gsm.GS_ERR_WORKSPACE
+    assert call(Q=A1) == gsm.GS_ERR_ARG
+    assert L.gs_compress_padded_workspace(10, 64, 9) == 0 and L.gs_compress_padded_workspace(10, 64, 20) > 0
+    assert call() == gsm.GS_ERR_DEVICE                       # valid: only the device is missing
 
 
 def compress_noalloc(L, C=A1, ct=gsm.GS_F32, M=10, D=64, ldc=64, tol=1e-10, Q=A2, qt=gsm.GS_F64, ldq=64,
@@ -114,6 +153,31 @@ def test_compress_noalloc_validation(L):
     assert L.gs_compress_workspace(1000, 4096) <= (64 << 20)        # the binary workload's codebook fits
 
 
+def test_prob2vec_sparse_validation(L):
+    f = L.gs_prob2vec_sparse
+    # rowptr, cols, vals, vt, B, M, nnz, R, rt, r, ldr, T, tt, ldt, stream
+    ok = [A1, A2, A3, gsm.GS_F32, 4, 10, 6, A4, gsm.GS_F32, 10, 10, WS, gsm.GS_F32, 10, NULL]
+
+    def call(**kw):
+        a = list(ok)
+        names = ["rowptr", "cols", "vals", "vt", "B", "M", "nnz", "R", "rt", "r", "ldr", "T", "tt", "ldt", "s"]
+        for k, v in kw.items():
+            a[names.index(k)] = v
+        return f(*a)
+
+    assert call(vt=gsm.GS_F64, rt=gsm.GS_F64) == gsm.GS_ERR_DTYPE
+    assert call(rt=gsm.GS_BF16) == gsm.GS_ERR_DTYPE
+    assert call(r=11, ldr=11, ldt=11) == gsm.GS_ERR_SHAPE               # r > M
+    assert call(nnz=-1) == gsm.GS_ERR_SHAPE
+    assert call(rowptr=NULL) == gsm.GS_ERR_ARG
+    assert call(cols=NULL) == gsm.GS_ERR_ARG
+    assert call(rowptr=P(0x10004)) == gsm.GS_ERR_ALIGN                  # int64 pointers
+    assert call(ldt=9) == gsm.GS_ERR_SHAPE
+    assert call(T=P(0x20000000 + 8)) == gsm.GS_ERR_ARG and "overlaps" in err(L)   # T on cols
+    assert call(B=0, rowptr=NULL, T=NULL) == gsm.GS_OK                  # empty batch
+    assert call(nnz=0, cols=NULL, vals=NULL, B=0) == gsm.GS_OK
+
+
 def test_project_validation(L):
     f = L.gs_project
     # dtype mismatch X f32 / Q bf16
@@ -133,7 +197,9 @@ def test_project_validation(L):
 
 def test_prob2vec_validation(L):
     f = L.gs_prob2vec
-    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 6, 6, A3, gsm.GS_F32, 6, NULL) == gsm.GS_ERR_SHAPE  # r > M
+    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 0, 6, A3, gsm.GS_F32, 6, NULL) == gsm.GS_ERR_SHAPE  # r = 0
+    # r > M is a padded basis: valid (only the device is missing here)
+    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 6, 6, A3, gsm.GS_F32, 6, NULL) == gsm.GS_ERR_DEVICE
     assert f(A1, gsm.GS_BF16, 4, 5, 5, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_DTYPE
     assert f(A1, gsm.GS_F32, 4, 5, 4, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_SHAPE
     assert f(A1, gsm.GS_F32, -1, 5, 5, A2, gsm.GS_F32, 5, 5, A3, gsm.GS_F32, 5, NULL) == gsm.GS_ERR_SHAPE

@@ -1250,47 +1250,73 @@ def test_echelon_on_compressed_rank_deficient_codebook():
 #
 # The paper's treatment of D < M: split the M entries into subsets of at most
 # D and give each its own orthonormal basis; after the restore, the subsets
-# are put side by side again.  The calls compose it without new entry points:
-# one compress per row range; similarity by projecting the queries into each
-# basis and writing each subset's scores into its column block of S; prob2vec
-# by each subset's coordinates side by side, restored against the stacked
-# bases (sum over subsets of T_s Q_s = P C).  Checked against the oracle's
-# dense definitions.
+# are put side by side again.  gs_compress_partitioned stacks the subsets'
+# bases in Q and puts their coordinates on R's block diagonal; each block is
+# checked against the oracle's compression of that subset, and the calls on
+# the stacked form against the oracle's dense definitions.
+
+
+def partitioned_codebook():
+    """100 x 32 bipolar codebook with a duplicate inside a subset, one across
+    subsets and a negation: subsets of 32 have ranks 31, 31, 32, 4."""
+    C = wl.bipolar_codebook(100, 32, 61)
+    C[20] = C[5]          # inside subset 0
+    C[40] = -C[3]         # subset 1 repeats a direction of subset 0: independent within subset 1
+    C[50] = C[41]         # inside subset 1
+    return C
 
 
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=_name)
 def test_partitioned_codebook_d_below_m(dt):
     M, D, B = 100, 32, 300
     print("partitioned codebook", M, D, B, _name(dt), flush=True)
-    C = wl.bipolar_codebook(M, D, 61)
+    C = partitioned_codebook()
+    Q64, R64, r64, ranks, kept, cn = gsm.gs_compress_partitioned(dev(C), subset=32)
+    torch.cuda.synchronize()
+    # each block is the oracle's compression of its subset
+    off = 0
+    Qh, Rh = host(Q64), host(R64)
+    for g, m0 in enumerate(range(0, M, 32)):
+        Cg = C[m0:m0 + 32]
+        Qo, Ro, ko, ro = oracle.compress(Cg)
+        assert ranks[g] == ro
+        assert np.abs(Qh[off:off + ro] - Qo).max() <= 1e-12
+        assert np.abs(Rh[m0:m0 + len(Cg), off:off + ro] - Ro).max() <= 1e-12 * np.abs(Ro).max()
+        assert list(host(kept[off:off + ro]).astype(int)) == list(ko + m0)
+        Rz = Rh[m0:m0 + len(Cg)].copy()
+        Rz[:, off:off + ro] = 0
+        assert np.all(Rz == 0)                        # block diagonal
+        off += ro
+    assert r64 == off == sum(ranks) == 31 + 31 + 32 + 4
+    assert np.abs(Rh @ Qh - C).max() <= 1e-12 * np.abs(C).max()
+    assert np.all(np.triu(Rh, 1) == 0)                # lower echelon
+    # calls on the stacked form (the benchmark's element types)
+    Q, R, r, ranks2, kept2, cn = gsm.gs_compress_partitioned(dev(C), subset=32, q_dtype=dt, r_dtype=dt)
     X = _mat(B, D, 62, dt)
     P = wl.dirichlet_probs(B, M, 0.5, 63)
     if dt == torch.bfloat16:
         P = wl.round_bf16(P)
-    Cd, Xd, Pd = dev(C), dev(X, dt), dev(P, dt)
-    S = torch.full((B, M), float("nan"), dtype=torch.float32, device="cuda")
-    xn = None
-    Ts, Qs = [], []
-    for off in range(0, M, D):
-        n = min(D, M - off)
-        Q, R, r, kept, cn = gsm.gs_compress(Cd[off:off + n], q_dtype=dt, r_dtype=dt)
-        assert r == n                                  # bipolar subsets of <= D rows: full rank
-        if xn is None:
-            T, xn = gsm.gs_project(Xd, Q, xnorm2=True)
-        else:
-            T = gsm.gs_project(Xd, Q)
-        gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, out=S[:, off:off + n], argmax=False, echelon=True)
-        Ts.append(gsm.gs_prob2vec(Pd[:, off:off + n].contiguous(), R, out_dtype=torch.float32, echelon=True))
-        Qs.append(Q.float())
+    T, xn = gsm.gs_project(dev(X, dt), Q, xnorm2=True)
+    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, mode="cosine", echelon=True)
+    Sd, _ = gsm.gs_similarity(T, R, mode="dot", scale=0.5, echelon=True)
+    V = gsm.gs_reconstruct(gsm.gs_prob2vec(dev(P, dt), R, out_dtype=dt, echelon=True), Q, out_dtype=torch.float32)
     torch.cuda.synchronize()
     tol = TOL_BF16 if dt == torch.bfloat16 else TOL_F32      # bf16: Q and R rounded from fp64
     So = oracle.similarity(X, C, oracle.COSINE)
-    assert np.isfinite(host(S)).all()
     assert rowrel(host(S), So) <= tol
-    # restore: the subsets' coordinates side by side against the stacked bases
-    V = gsm.gs_reconstruct(torch.cat(Ts, dim=1).contiguous(), torch.cat(Qs, dim=0).contiguous())
-    torch.cuda.synchronize()
+    assert rowrel(host(Sd), oracle.similarity(X, C, oracle.DOT, 0.5)) <= tol
+    argmax_exact(idx, host(T), host(R), host(xn), host(cn))
     assert rowrel(host(V), oracle.prob2vec(P, C)) <= tol
+
+
+def test_partitioned_equals_plain_compress_when_m_fits():
+    C = rq_codebook("binary", 60, 500, 64)
+    a = gsm.gs_compress(dev(C))
+    b = gsm.gs_compress_partitioned(dev(C), subset=60)
+    c = gsm.gs_compress_partitioned(dev(C))                  # default subset D >= M
+    torch.cuda.synchronize()
+    for x in (b, c):
+        assert x[2] == a[2] and torch.equal(x[0], a[0]) and torch.equal(x[1], a[1]) and torch.equal(x[4], a[3])
 
 
 # ------------------------------------------- binding of restored vectors
@@ -1350,3 +1376,128 @@ def test_bind_xor_binary(dt):
     Z = gsm.gs_bind_restored(dev(Xb, dt), dev(Yb, dt), op="xor", out_dtype=torch.float32)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(host(Z), oracle.xor(Xb, Yb))
+
+
+# ------------------------------------------------ sparse probability rows (CSR)
+#
+# prob2vec of rows given by their stored entries: the oracle sums the dense
+# rows (zeros elsewhere); rows without entries, column indices in any order,
+# r not a multiple of the 256-coordinate chunk, both value and output types.
+
+
+def csr_rows(B, M, per_row, seed, sort=True):
+    """Seeded CSR rows with 0 .. per_row entries (Dirichlet values on the
+    chosen columns) and the dense matrix they stand for."""
+    g = np.random.default_rng(seed)
+    counts = g.integers(0, per_row + 1, size=B)
+    counts[::7] = 0                                   # some empty rows
+    rowptr = np.zeros(B + 1, np.int64)
+    rowptr[1:] = np.cumsum(counts)
+    cols = np.empty(rowptr[-1], np.int32)
+    vals = np.empty(rowptr[-1], np.float32)
+    dense = np.zeros((B, M), np.float32)
+    for b in range(B):
+        c = g.choice(M, size=counts[b], replace=False)
+        if sort:
+            c = np.sort(c)
+        v = g.dirichlet(np.full(max(counts[b], 1), 0.5))[: counts[b]].astype(np.float32)
+        cols[rowptr[b]:rowptr[b + 1]] = c
+        vals[rowptr[b]:rowptr[b + 1]] = v
+        dense[b, c] = v
+    return rowptr, cols, vals, dense
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=_name_early)
+@pytest.mark.parametrize("M,D,per_row,sort", [(1000, 1500, 24, True), (300, 800, 300, False), (40, 256, 5, True)])
+def test_prob2vec_sparse(dt, M, D, per_row, sort):
+    B = 777
+    print("sparse prob2vec", M, D, per_row, sort, _name_early(dt), flush=True)
+    C = rq_codebook("binary", M, D, 90 + M)
+    Qo, Ro, kept, r = oracle.compress(C)
+    rowptr, cols, vals, dense = csr_rows(B, M, per_row, M, sort)
+    if dt == torch.bfloat16:
+        vals = wl.round_bf16(vals)
+        dense = wl.round_bf16(dense)
+    Rin = Ro.astype(np.float32) if dt == torch.float32 else wl.round_bf16(Ro.astype(np.float32))
+    rp, cd = torch.from_numpy(rowptr).cuda(), torch.from_numpy(cols).cuda()
+    vd, Rd = dev(vals, dt), dev(Rin, dt)
+    for out_dtype in (torch.float32, torch.bfloat16):
+        T = gsm.gs_prob2vec_sparse(rp, cd, vd, Rd, out_dtype=out_dtype)
+        Tdense = gsm.gs_prob2vec(dev(dense, dt), Rd, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        Tg = host(T)
+        assert np.isfinite(Tg).all()
+        tol = TOL_F32 if (dt == torch.float32 and out_dtype == torch.float32) else TOL_BF16
+        # the dense definition on the stored entries (in span: t = Q v)
+        assert rowrel(Tg, oracle.project(oracle.prob2vec(dense, C), Qo)) <= tol
+        # and the dense call on the same values, to fp32 accumulation
+        if out_dtype == torch.float32:
+            assert rowrel(Tg, host(Tdense)) <= 1e-5
+        empty = np.nonzero(np.diff(rowptr) == 0)[0]
+        assert np.all(Tg[empty] == 0.0)
+
+
+def test_prob2vec_sparse_skips_out_of_range_entries():
+    # stored indices outside [0, M) and entries past rowptr[B] contribute nothing
+    M, D, B = 50, 300, 40
+    C = rq_codebook("bipolar", M, D, 95)
+    Qo, Ro, kept, r = oracle.compress(C)
+    rowptr, cols, vals, dense = csr_rows(B, M, 6, 96)
+    bad = cols.copy()
+    bad[::5] = -1
+    bad[1::5] = M
+    keep = (bad >= 0) & (bad < M)
+    dense2 = np.zeros_like(dense)
+    for b in range(B):
+        for e in range(rowptr[b], rowptr[b + 1]):
+            if keep[e]:
+                dense2[b, bad[e]] += vals[e]
+    # stored arrays one entry longer than rowptr[B] says (never read)
+    cols_x = np.concatenate([bad, [3]]).astype(np.int32)
+    vals_x = np.concatenate([vals, [1.0]]).astype(np.float32)
+    T = gsm.gs_prob2vec_sparse(torch.from_numpy(rowptr).cuda(), torch.from_numpy(cols_x).cuda(), dev(vals_x),
+                               dev(Ro.astype(np.float32)))
+    torch.cuda.synchronize()
+    assert rowrel(host(T), oracle.project(oracle.prob2vec(dense2, C), Qo)) <= TOL_F32
+
+
+# ------------------------------------------------ padded bases (k > M)
+#
+# The basis completed to k vectors by unit vectors and, optionally, turned by
+# an orthogonal k x k matrix (a normalised Hadamard matrix here).  Compared
+# element by element with the oracle's padded compression, and the calls on
+# padded coordinates with the oracle's dense definitions.
+
+
+@pytest.mark.parametrize("transform", [False, True])
+@pytest.mark.parametrize("M,D,k,dup", [(22, 1024, 64, 0.0), (40, 700, 64, 0.1), (100, 2000, 256, 0.1)])
+def test_compress_padded(M, D, k, dup, transform):
+    print("padded", M, D, k, dup, transform, flush=True)
+    C = rq_codebook("bipolar", M, D, 120 + M, dup=dup)
+    H = (wl.hadamard_codebook(k).astype(np.float64) / math.sqrt(k)) if transform else None
+    Qo, Ro, kept_o, ro = oracle.compress_padded(C, k, H)
+    Hd = None if H is None else dev(H, torch.float64)
+    Q, R, r, kept, cn = gsm.gs_compress_padded(dev(C), k, Hd)
+    torch.cuda.synchronize()
+    assert r == ro == M - int(round(dup * M))
+    assert list(host(kept[:r]).astype(int)) == list(kept_o) and np.all(host(kept[r:]) == -1)
+    Qg, Rg = host(Q), host(R)
+    assert np.abs(Qg - Qo).max() <= 1e-12
+    assert np.abs(Rg - Ro).max() <= 1e-12 * np.abs(Ro).max()
+    assert np.abs(Qg @ Qg.T - np.eye(k)).max() <= 1e-12
+    np.testing.assert_allclose(host(cn), oracle.row_norms(C), rtol=1e-6)
+    # the operators on padded coordinates (fp32 copies)
+    Q32, R32, _, _, _ = gsm.gs_compress_padded(dev(C), k, Hd, q_dtype=torch.float32, r_dtype=torch.float32)
+    B = 300
+    P = wl.dirichlet_probs(B, M, 0.5, M)
+    X = oracle.prob2vec(P, C) + np.sqrt(0.1) * np.random.default_rng(M).standard_normal((B, D))
+    T, xn = gsm.gs_project(dev(X), Q32, xnorm2=True)
+    S, idx = gsm.gs_similarity(T, R32, qnorm2=xn, cnorm=cn, mode="cosine")
+    Tp = gsm.gs_prob2vec(dev(P), R32)
+    V = gsm.gs_reconstruct(Tp, Q32)
+    torch.cuda.synchronize()
+    So = oracle.similarity(X, C, oracle.COSINE)
+    assert rowrel(host(S), So) <= TOL_F32
+    argmax_exact(idx, host(T), host(R32), host(xn), host(cn))
+    assert rowrel(host(V), oracle.prob2vec(P, C)) <= TOL_F32
+    assert rowrel(host(Tp), oracle.project(oracle.prob2vec(P, C), Qo)) <= TOL_F32

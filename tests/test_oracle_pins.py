@@ -474,3 +474,61 @@ def test_xor_binding_of_binary_vectors():
     noisy = a + rng.uniform(-0.3, 0.3, a.shape)
     np.testing.assert_array_equal(oracle.xor(noisy, b), oracle.xor(a, b))
     assert oracle.xor(np.array([0.5]), np.array([0.4999999]))[0] == 1.0
+
+
+# ------------------------------------------------ padded bases (k > M, Sec. 3.1)
+
+def read_sections(path):
+    secs, cur = {}, None
+    for line in open(path):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        if line[0].isalpha():
+            cur = line
+            secs[cur] = []
+        else:
+            secs[cur].append([float(x) for x in line.split()])
+    return {k: np.array(v) for k, v in secs.items()}
+
+
+def test_padded_hand_worked_examples():
+    g = read_sections(os.path.join(GOLDEN, "worked_padded.txt"))
+    Q, R, kept, r = oracle.compress_padded(g["caseA_codebook"], 2, g["caseA_H"])
+    assert r == 1 and list(kept) == [0]
+    np.testing.assert_allclose(Q, g["caseA_Q"], atol=1e-15)
+    np.testing.assert_allclose(R, g["caseA_R"], atol=1e-15)
+    Q, R, kept, r = oracle.compress_padded(g["caseB_codebook"], 3)
+    assert r == 2 and list(kept) == [0, 1]
+    np.testing.assert_allclose(Q, g["caseB_Q"], atol=1e-15)
+    np.testing.assert_allclose(R, g["caseB_R"], atol=1e-15)
+
+
+def sylvester(n):
+    return wl.hadamard_codebook(n).astype(np.float64) / math.sqrt(n)
+
+
+@pytest.mark.parametrize("transform", [False, True])
+def test_padded_basis_invariants(transform):
+    # a bipolar codebook with a duplicate and a negation (rank 18 of 20),
+    # padded to k = 32, with or without a normalised Hadamard transformation
+    C = wl.bipolar_codebook(20, 128, 31).astype(np.float64)
+    C[7] = C[2]
+    C[15] = -C[4]
+    k = 32
+    H = sylvester(k) if transform else None
+    Q, R, kept, r = oracle.compress_padded(C, k, H)
+    assert r == exact_rank(C) == 18 and list(kept) == greedy_kept(C)
+    assert Q.shape == (k, 128) and R.shape == (20, k)
+    assert np.abs(Q @ Q.T - np.eye(k)).max() <= 1e-12            # orthonormal k-vector basis
+    assert np.abs(R @ Q - C).max() <= 1e-12 * np.abs(C).max()      # C = R Q
+    assert np.abs(R @ R.T - exact_gram(C)).max() <= 1e-12 * 128  # inner products: R R^T = C C^T
+    Q0, R0, _, _ = oracle.compress(C)
+    if not transform:
+        # plain zero padding: the codebook's basis first, zero coordinates after
+        assert np.array_equal(Q[:r], Q0) and np.array_equal(R[:, :r], R0)
+        assert np.all(R[:, r:] == 0)
+        assert np.abs(C @ Q[r:].T).max() <= 1e-12 * 128          # added vectors outside span(C)
+    else:
+        # the transformation spreads each coordinate vector over all k entries
+        assert np.count_nonzero(np.abs(R[kept]) > 1e-9) > 0.9 * len(kept) * k
