@@ -52,12 +52,13 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--workload", default="stress",
-                    choices=["stress", "vsa", "large", "binary", "dimsweep", "bind"],
+                    choices=["stress", "vsa", "large", "binary", "dimsweep", "bind", "memory"],
                     help="stress (default, the headline): the whole matrix-space pipeline of the stress "
                          "configuration in bf16; vsa: the fused soft selection of four attribute codebooks; "
                          "large / binary: the separate calls of those configurations (fp32); dimsweep: "
                          "similarity latency against the vector dimension, dense vs Gram-Space; bind: binding of "
-                         "restored vectors (circular convolution / correlation, xor, product)")
+                         "restored vectors (circular convolution / correlation, xor, product); memory: peak device "
+                         "memory of each workload's operators, dense against Gram-Space")
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default 20; vsa: 200)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed warm-up steps (default 3; vsa: 20)")
     ap.add_argument("--sets", type=int, default=0, help="vsa: batch copies to cycle through (0: >= 1 GiB)")
@@ -382,6 +383,9 @@ def mfma_workload(args, torch, gsm):
               "reconstruct_bind": "gemm256_store_kernel x 2 (T Q, then .* T2 Q)",
               "prob2vec": "gemm256_store_kernel (P R)", "similarity": "similarity scores",
               "attention": "attention weights"}[dom]
+    extra_binary = {}
+    if args.workload == "binary":
+        extra_binary = binary_extras(args, torch, gsm, Pa, R, Ta, Y, per, stream)
     cpu = None
     if not args.no_cpu:
         n = min(args.cpu_rows, B)
@@ -407,9 +411,69 @@ def mfma_workload(args, torch, gsm):
                   "per_call_TFLOPs": {n: flops[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in per},
                   "per_call_useful_TFLOPs": {n: useful[n] / (float(np.mean(per[n])) * 1e-3) / 1e12 for n in useful},
                   "nnz_R": nnz,
-                  "compress_ms": compress_ms, "rank": r, "kernel_source_hash": kernel_source_hash()},
+                  "compress_ms": compress_ms, "rank": r, "kernel_source_hash": kernel_source_hash(),
+                  **extra_binary},
     }
     print(json.dumps(out), flush=True)
+
+
+def event_ms(torch, f, reps=20):
+    """Mean device time of f over reps calls (HIP events on the current stream)."""
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        f()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        f()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def binary_extras(args, torch, gsm, Pa, R, Ta, Y, per, stream):
+    """Binary workload, two measured side questions.
+    1. Sparse probability rows: gs_prob2vec_sparse on the rows truncated to
+       the entries above 1e-9 (dropped mass at fp32 level) and to the 16
+       largest entries, against the dense product on the full rows.
+    2. Fusing restore -> bind -> re-project into one product would keep the
+       bound vectors Y on chip: the most it can save is Y's write and re-read,
+       timed here as a device copy of Y (read + write of the same bytes)."""
+    B, M = Pa.shape
+    out = {}
+    dense_ms = event_ms(torch, lambda: gsm.gs_prob2vec(Pa, R, out=Ta, echelon=True))
+    sp = {"dense_prob2vec_ms": dense_ms}
+    Tref = gsm.gs_prob2vec(Pa, R, echelon=True)
+    for name in ("above_1e-9", "top16"):
+        if name == "top16":
+            v, idx = torch.topk(Pa, 16, dim=1)
+            idx, order = torch.sort(idx, dim=1)
+            v = torch.gather(v, 1, order)
+            mask = torch.zeros_like(Pa, dtype=torch.bool).scatter_(1, idx, True)
+        else:
+            mask = Pa > 1e-9
+        counts = mask.sum(dim=1)
+        rowptr = torch.zeros(B + 1, dtype=torch.int64, device=Pa.device)
+        rowptr[1:] = torch.cumsum(counts, 0)
+        cols = torch.nonzero(mask)[:, 1].to(torch.int32).contiguous()
+        vals = Pa[mask].contiguous()
+        Ts = gsm.alloc_rows(B, R.shape[1], torch.float32, Pa.device)
+        ms = event_ms(torch, lambda: gsm.gs_prob2vec_sparse(rowptr, cols, vals, R, out=Ts))
+        dropped = (Pa * (~mask)).sum(dim=1)
+        err = ((Ts - Tref).abs().max(dim=1).values / Tref.abs().max(dim=1).values.clamp_min(1e-30)).max().item()
+        sp[name] = {"ms": ms, "speedup_vs_dense": dense_ms / ms, "nnz_per_row": float(counts.float().mean().item()),
+                    "dropped_mass_max": float(dropped.max().item()), "rowrel_diff_vs_full_rows": err}
+    out["sparse_prob2vec"] = sp
+    Y2 = torch.empty_like(Y)
+    copy_ms = event_ms(torch, lambda: Y2.copy_(Y))
+    chain = float(np.mean(per["reconstruct_bind"])) + float(np.mean(per["reproject"]))
+    out["fused_restore_bind_reproject"] = {
+        "y_bytes": Y.numel() * Y.element_size(), "y_round_trip_ms": copy_ms,
+        "chain_ms": chain, "max_saving_frac": copy_ms / chain}
+    del Y2
+    return out
 
 
 def cpu_baseline_rows(w, inputs, beta):
@@ -596,6 +660,157 @@ def stress_workload(args, torch, gsm):
     print(json.dumps(out), flush=True)
 
 
+def memory_workload(args, torch, gsm):
+    """Peak device memory of each workload's operators run in D-space on the
+    dense codebook against the same outputs through Gram-Space (the paper's
+    memory comparison, Sec. 4.2, measured in a run of its own, apart from
+    the timing).  Both paths use this library's kernels: the dense path calls
+    them with the codebook C itself in place of (Q, R) (r = D: t = p C is
+    then the dense vector).  The codebook (C, or Q and R) is built before
+    the peak counter is reset and counted separately; peaks are
+    torch.cuda.max_memory_allocated over the operators."""
+    dev = torch.device("cuda:0")
+    rows = lambda n, c, t: gsm.alloc_rows(n, c, t, dev)
+    nb = lambda *ts: int(sum(t.numel() * t.element_size() for t in ts if t is not None))
+    results = []
+
+    def measure(name, path, codebook, fn):
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        keep = fn()
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - base
+        results.append({"workload": name, "path": path, "codebook_bytes": nb(*codebook), "peak_bytes": int(peak),
+                        "outputs_bytes": nb(*keep)})
+        log("memory %s %s: codebook %.1f MB, operators peak %.1f MB" % (name, path, nb(*codebook) / 1e6,
+                                                                         peak / 1e6))
+        del keep
+
+    beta = args.beta
+    # vsa: four attribute codebooks, fused soft selection against dense vectors
+    w = wl.WORKLOADS["vsa"]
+    books = []
+    for i, M in enumerate(w.Ms):
+        C = torch.from_numpy(wl.codebook(w, i)).to(dev)
+        Q, R, r, kept, cn = gsm.gs_compress(C, q_dtype=torch.float32, r_dtype=torch.float32)
+        books.append((C, R.contiguous(), cn, torch.from_numpy(wl.probabilities(w, i)).to(dev)))
+
+    def vsa_dense():
+        out = []
+        for C, R, cn, P in books:
+            V = gsm.gs_prob2vec(P, C)                       # dense v = p C, B x D
+            S, idx = gsm.gs_similarity(V, C, mode="cosine")
+            A, _ = gsm.gs_attention(V, C, mode="cosine", beta=beta)
+            del V
+            out += [S, idx, A]
+        return out
+
+    def vsa_gram():
+        groups = [{"P": P, "R": R, "cnorm": cn, "S": torch.empty(P.shape, device=dev),
+                   "argmax": torch.empty(P.shape[0], dtype=torch.int32, device=dev),
+                   "A": torch.empty(P.shape, device=dev)} for C, R, cn, P in books]
+        gsm.gs_soft_select(groups, mode="cosine", beta=beta, form="gram")
+        return [t for g in groups for t in (g["S"], g["argmax"], g["A"])]
+
+    measure("vsa", "dense", [b[0] for b in books], vsa_dense)
+    measure("vsa", "gram", [b[1] for b in books] + [b[2] for b in books], vsa_gram)
+    del books
+
+    # large: hard-selection queries against the codebook
+    w = wl.WORKLOADS["large"]
+    C = torch.from_numpy(wl.codebook(w)).to(dev)
+    Q, R, r, kept, cn = gsm.gs_compress(C, q_dtype=torch.float32, r_dtype=torch.float32)
+    P = wl.device_dirichlet_half(w.B, w.Ms[0], w.seed, torch, dev)
+    X = rows(w.B, w.D, torch.float32)
+    X.copy_(wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch))
+    del P
+    Cd = rows(C.shape[0], C.shape[1], torch.float32)
+    Cd.copy_(C)
+
+    def large_dense():
+        S, idx = gsm.gs_similarity(X, Cd, mode="cosine")
+        A, _ = gsm.gs_attention(X, Cd, mode="cosine", beta=beta)
+        return [S, idx, A]
+
+    def large_gram():
+        T, xn = gsm.gs_project(X, Q, xnorm2=True)
+        S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, echelon=True)
+        A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cn, beta=beta, echelon=True)
+        return [S, idx, A]
+
+    measure("large", "dense", [Cd], large_dense)
+    measure("large", "gram", [Q, R], large_gram)
+    del X, C, Cd, Q, R
+
+    # binary: superposition, lookup, bind of restored pairs, re-projection
+    w = wl.WORKLOADS["binary"]
+    C = torch.from_numpy(wl.codebook(w)).to(dev)
+    Q, R, r, kept, cn = gsm.gs_compress(C, q_dtype=torch.float32, r_dtype=torch.float32)
+    Pa = torch.from_numpy(wl.probabilities(w, 0)).to(dev)
+    Pb = torch.from_numpy(wl.probabilities(w, 0, stream=wl.STREAM_PROBS_B)).to(dev)
+    Cd = rows(C.shape[0], C.shape[1], torch.float32)
+    Cd.copy_(C)
+
+    def binary_dense():
+        Va = gsm.gs_prob2vec(Pa, Cd)
+        Vb = gsm.gs_prob2vec(Pb, Cd)
+        S, idx = gsm.gs_similarity(Va, Cd, mode="cosine")
+        Y = gsm.gs_bind_restored(Va, Vb, op="mul")
+        return [S, idx, Y]
+
+    def binary_gram():
+        Ta = gsm.gs_prob2vec(Pa, R, echelon=True)
+        Tb = gsm.gs_prob2vec(Pb, R, echelon=True)
+        S, idx = gsm.gs_similarity(Ta, R, cnorm=cn, echelon=True)
+        Y = gsm.gs_reconstruct(Ta, Q, T2=Tb, bind="mul")
+        Ty = gsm.gs_project(Y, Q)
+        return [S, idx, Y, Ty]
+
+    measure("binary", "dense", [Cd], binary_dense)
+    measure("binary", "gram", [Q, R], binary_gram)
+    del C, Cd, Q, R, Pa, Pb
+
+    # stress: the full pipeline in bf16
+    w = wl.WORKLOADS["stress"]
+    dt = torch.bfloat16
+    C = torch.from_numpy(wl.codebook(w)).to(dev)
+    Q, R, r, kept, cn = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
+    P = wl.device_dirichlet_half(w.B, w.Ms[0], w.seed, torch, dev, dtype=dt)
+    X = wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch, dtype=dt)
+    Cd = rows(C.shape[0], C.shape[1], dt)
+    Cd.copy_(C)
+    del C
+
+    def stress_dense():
+        V = gsm.gs_prob2vec(P, Cd)                          # dense superposed vectors, B x D bf16
+        S, idx = gsm.gs_similarity(X, Cd, mode="cosine")
+        A, _ = gsm.gs_attention(X, Cd, mode="cosine", beta=beta)
+        return [V, S, idx, A]
+
+    def stress_gram():
+        T, xn = gsm.gs_project(X, Q, out_dtype=dt, xnorm2=True)
+        T2 = gsm.gs_prob2vec(P, R, out_dtype=dt, echelon=True)
+        S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, echelon=True)
+        A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cn, beta=beta, echelon=True)
+        Xr = gsm.gs_reconstruct(T2, Q, out_dtype=dt)         # restored superposed vectors
+        return [T2, S, idx, A, Xr]
+
+    measure("stress", "dense", [Cd], stress_dense)
+    measure("stress", "gram", [Q, R], stress_gram)
+    del X, P, Cd, Q, R
+    by = {}
+    for e in results:
+        by.setdefault(e["workload"], {})[e["path"]] = e
+    ratios = {k: {"peak_dense_over_gram": v["dense"]["peak_bytes"] / max(v["gram"]["peak_bytes"], 1),
+                  "codebook_dense_over_gram": v["dense"]["codebook_bytes"] / max(v["gram"]["codebook_bytes"], 1)}
+              for k, v in by.items()}
+    print(json.dumps({"metric": "peak device memory of the operators, dense vs Gram-Space", "unit": "bytes",
+                      "results": results, "ratios": ratios, "kernel_source_hash": kernel_source_hash()}),
+          flush=True)
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -767,6 +982,9 @@ def main():
         return
     if args.workload == "bind":
         bind_workload(args, torch, gsm)
+        return
+    if args.workload == "memory":
+        memory_workload(args, torch, gsm)
         return
     if args.workload == "stress":
         stress_workload(args, torch, gsm)
