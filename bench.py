@@ -9,8 +9,8 @@ reported).  The batch holds 262144 queries x = p C + N(0, 0.1) noise with
 p ~ Dirichlet(1/2), stored as bf16 (P and X), with bf16 basis and coordinates
 and fp32 accumulation.  One step is the whole matrix-space pipeline over the
 batch: project (t = Q x, with ||x||^2), prob2vec (t = p R), cosine similarity
-with argmax, attention weights softmax(16 s) and reconstruct (x = t Q),
-each a separate library call; `value` is queries per second over the K timed
+with argmax and attention weights softmax(16 s) from one score product
+(gs_similarity_attention), and reconstruct (x = t Q), four library calls; `value` is queries per second over the K timed
 steps (synchronised wall clock), and HIP events around every call on the
 launch stream give each kernel's mean duration, the dominant one going into
 the matrix-core roofline entry.  The fused soft-selection step of the vsa
@@ -509,9 +509,6 @@ def cpu_baseline_rows(w, inputs, beta):
                       % (n, w.B, what, dt, w.B / rate)}
 
 
-STRESS_CALLS = ("project", "prob2vec", "similarity", "attention", "reconstruct")
-
-
 def cpu_baseline_stress(w, Ps, Xs, beta, rows_desc):
     """The oracle (dense fp64 in D-space) on a seeded sample of the stress
     batch: for each sampled query, cosine similarity of x against every
@@ -540,9 +537,9 @@ def cpu_baseline_stress(w, Ps, Xs, beta, rows_desc):
 
 
 def stress_workload(args, torch, gsm):
-    """The headline: one step = project, prob2vec, similarity + argmax,
-    attention and reconstruct over the whole stress batch (bf16 storage, fp32
-    accumulation), K steps timed on the synchronised wall clock with HIP
+    """The headline: one step = project, prob2vec, similarity + argmax and
+    attention (one score product for both), and reconstruct over the whole
+    stress batch (bf16 storage, fp32 accumulation), K steps timed on the synchronised wall clock with HIP
     events around every call."""
     w = wl.WORKLOADS["stress"]
     dev = torch.device("cuda:0")
@@ -571,10 +568,10 @@ def stress_workload(args, torch, gsm):
     calls = [
         ("project", lambda: gsm.gs_project(X, Q, out=T, xnorm2=True, xnorm2_out=xn), fl_proj),
         ("prob2vec", lambda: gsm.gs_prob2vec(P, R, out=T2, echelon=True), fl_code),
-        ("similarity", lambda: gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, out=S, argmax_out=idx,
-                                                 echelon=True), fl_code),
-        ("attention", lambda: gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=beta, out=A, echelon=True),
-         fl_code),
+        # the scores once: S, their row argmax and A = softmax(beta S)
+        ("similarity_attention", lambda: gsm.gs_similarity_attention(T, R, qnorm2=xn, cnorm=cnorm, beta=beta,
+                                                                     out=S, argmax_out=idx, a_out=A,
+                                                                     echelon=True), fl_code),
         ("reconstruct", lambda: gsm.gs_reconstruct(T2, Q, out=Xr), fl_proj),
     ]
     stream = torch.cuda.current_stream()
@@ -605,12 +602,12 @@ def stress_workload(args, torch, gsm):
     # the products with the lower-echelon R skip its zero blocks: also the
     # rate on R's nonzero entries (2 nnz(R) flops per row)
     nnz = int((R != 0).sum().item())
-    useful = {n: flops[n] * nnz / (M * r) for n in ("prob2vec", "similarity", "attention")}
+    useful = {n: flops[n] * nnz / (M * r) for n in ("prob2vec", "similarity_attention")}
     dom = max(mean, key=mean.get)
     kernels = {"project": "gemm256_store_kernel<bf16, bf16, BNN=false> (X Q^T, with ||x||^2)",
                "reconstruct": "gemm256_store_kernel<bf16, bf16, BNN=true> (T Q, persistent tile walk)",
                "prob2vec": "gemm256_store_kernel<bf16, bf16, BNN=true> (P R, echelon K ranges)",
-               "similarity": "scores256_kernel + rows_argmax_kernel", "attention": "scores256_kernel"}
+               "similarity_attention": "scores256_kernel + rows_sim_attn_reg_kernel<8> (S, argmax, A)"}
     achieved = flops[dom] / (mean[dom] * 1e-3) / 1e12
     peak = MFMA_PEAK["bf16"]
     ms_per_step = wall * 1e3 / args.steps
@@ -632,7 +629,7 @@ def stress_workload(args, torch, gsm):
              "per_call_frac_bf16_peak": {n: flops[n] / (mean[n] * 1e-3) / 1e12 / peak for n in mean},
              "per_call_useful_TFLOPs": {n: useful[n] / (mean[n] * 1e-3) / 1e12 for n in useful},
              "nnz_R": nnz, "compress_ms": compress_ms, "rank": r,
-             "timing": "K steps of the five calls on the current stream; HIP events around every call",
+             "timing": "K steps of the four calls on the current stream; HIP events around every call",
              "kernel_source_hash": kernel_source_hash()}
     if not args.no_vsa:
         log("vsa: fused soft selection (both forms)")
@@ -647,8 +644,8 @@ def stress_workload(args, torch, gsm):
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "stress: bipolar codebook M=%d (205 duplicated rows, rank %d), D=%d; %d queries "
                                "x = p C + N(0, 0.1), p ~ Dir(1/2); bf16 storage, fp32 accumulation; step = "
-                               "project (+||x||^2), prob2vec (echelon R), cosine similarity + argmax, attention "
-                               "softmax(beta=%g), reconstruct; compress once before timing"
+                               "project (+||x||^2), prob2vec (echelon R), cosine similarity + argmax and attention "
+                               "softmax(beta=%g) from one score product, reconstruct; compress once before timing"
                                % (M, r, D, B, beta),
                    "M": M, "D": D, "rank": r, "batch": B},
         "roofline": {"bound": "mfma", "kernel": kernels[dom], "call": dom, "achieved": achieved, "peak": peak,

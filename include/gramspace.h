@@ -346,6 +346,31 @@ gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t
                        void *O, gs_dtype ot, int64_t ldo, void *stream);
 
 /*
+ * gs_similarity_attention -- the similarity lookup and the attention weights
+ * of one batch from a single evaluation of the scores (Sec. 2.2: the
+ * attention score is the softmax of beta times the similarity):
+ *   S[b, j]    as gs_similarity computes it (same T, R, qnorm2, cnorm, mode,
+ *              scale and conditions)
+ *   argmax[b]  the lowest index of the largest S[b, :]
+ *   A[b, j]    softmax over j of beta * S[b, j], taken from the fp32 scores
+ *              (max-subtracted; any sign of beta)
+ *
+ *   S      out  float B x M, nullable, lds >= M
+ *   argmax out  int32[B], nullable
+ *   A      out  float B x M, nullable, lda >= M; when S is NULL the scores
+ *               are formed in A and replaced there by the weights
+ * At least one of S, argmax and A must be given; the outputs must not
+ * overlap each other or the inputs.  Calling gs_similarity and gs_attention
+ * gives the same results up to rounding, at about twice the arithmetic.
+ */
+gs_status gs_similarity_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                                  const void *R, gs_dtype rt, int64_t M, int64_t ldr,
+                                  const float *qnorm2, const float *cnorm,
+                                  gs_sim_mode mode, float scale,
+                                  float *S, int64_t lds, int32_t *argmax,
+                                  float beta, float *A, int64_t lda, void *stream);
+
+/*
  * gs_reconstruct -- restore vectors to the original domain (Sec. 3.1 and
  * Sec. 3.3, the "decompose" step): X = T Q.  With bind == GS_BIND_MUL and a
  * second coordinate batch T2, the two restored vectors are bound

@@ -493,6 +493,48 @@ gs_status gs_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t
     return launched(launch_gemm(GS_F32, rt, ot, true, EPI_STORE, o, s), "gs_attention (weighted sum)");
 }
 
+gs_status gs_similarity_attention(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                                  const void *R, gs_dtype rt_in, int64_t M, int64_t ldr,
+                                  const float *qnorm2, const float *cnorm, gs_sim_mode mode, float scale,
+                                  float *S, int64_t lds, int32_t *argmax, float beta, float *A, int64_t lda,
+                                  void *stream) {
+    bool ech;
+    const gs_dtype rt = coord_type(rt_in, &ech);
+    const char *fn = "gs_similarity_attention";
+    GS_CHECK(check_sim_common(fn, T, tt, B, r, ldt, R, rt, M, ldr, qnorm2, cnorm, mode));
+    if (!S && !argmax && !A && B > 0) return fail(GS_ERR_ARG, "%s: S, argmax and A are all null", fn);
+    GS_CHECK(check_matrix(S, "S", B, M, lds, GS_F32, true));
+    GS_CHECK(check_matrix(A, "A", B, M, lda, GS_F32, true));
+    GS_CHECK(check_aligned(argmax, 4, "argmax"));
+    GS_CHECK(check_overlaps({span(T, B, r, ldt, esize(tt), "T"), span(R, M, r, ldr, esize(rt), "R"),
+                             span(qnorm2, 1, B, B, 4, "qnorm2"), span(cnorm, 1, M, M, 4, "cnorm")},
+                            {span(S, B, M, lds, 4, "S"), span(argmax, 1, B, B, 4, "argmax"),
+                             span(A, B, M, lda, 4, "A")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    hipStream_t s = (hipStream_t)stream;
+    // argmax alone needs no score matrix: the similarity kernels' own
+    if (!S && !A) return gs_similarity(T, tt, B, r, ldt, R, rt_in, M, ldr, qnorm2, cnorm, mode, scale,
+                                       nullptr, M, argmax, stream);
+    // the scores once, into S (or into A, replaced there by the weights)
+    float *W = S ? S : A;
+    const int64_t ldw = S ? lds : lda;
+    if (M <= SMALL_MAX && r <= M && B > FEW_ROWS) {
+        SmallArgs a{};
+        a.In = T; a.ldin = ldt; a.R = R; a.ldr = ldr; a.B = B; a.M = M; a.r = r; a.Out = W; a.ldout = ldw;
+        a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale;
+        GS_CHECK(launched(launch_small_similarity(tt, a, s), fn));
+    } else {
+        GemmArgs a{};
+        a.A = T; a.lda = ldt; a.B = R; a.ldb = ldr; a.C = W; a.ldc = ldw; a.M = B; a.N = M; a.K = r;
+        a.qnorm2 = qnorm2; a.cnorm = cnorm; a.cosine = mode == GS_SIM_COSINE; a.scale = scale;
+        a.write_out = true; a.echelon = ech;
+        GS_CHECK(launched(launch_gemm(tt, rt, GS_F32, false, EPI_SIM, a, s), fn));
+    }
+    // one pass over the scores: the row argmax and the weights
+    return launched(launch_sim_attn_pass(W, ldw, B, M, argmax, beta, A, lda, s), fn);
+}
+
 gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
                          const void *T2, int64_t ldt2, gs_bind bind,
                          const void *Q, gs_dtype qt, int64_t D, int64_t ldq,

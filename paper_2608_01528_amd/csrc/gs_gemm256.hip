@@ -1155,6 +1155,118 @@ __global__ void __launch_bounds__(256) rows_softmax_kernel(float *A, int64_t lda
     for (int64_t c = l; c < M; c += 64) a[c] = __expf(a[c] - m) * iz;
 }
 
+// One wave per row of the scores W: the lowest index of the row maximum into
+// argmax (when non-null), then A = softmax(beta * W) (when non-null; A may be
+// W itself: the row is in registers before anything is written).  Rows in
+// registers as 16-byte pieces (M <= 4 * 64 * V4, rows of W and A 16-byte
+// aligned), so W is read once and A written once.
+template <int V4>
+__global__ void __launch_bounds__(256) rows_sim_attn_reg_kernel(const float *W, int64_t ldw, int64_t B, int64_t M,
+                                                               int32_t *argmax, float beta, float *A, int64_t lda) {
+    const int l = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= B) return;
+    const float *w = W + row * ldw;
+    f4v v[V4];
+#pragma unroll
+    for (int i = 0; i < V4; ++i) {
+        const int64_t c = 4 * (l + 64 * i);
+        if (c + 4 <= M) {
+            v[i] = __builtin_nontemporal_load(reinterpret_cast<const f4v *>(w + c));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[i][e] = (c + e < M) ? w[c + e] : -INFINITY;
+        }
+    }
+    if (argmax) {
+        // each lane visits its columns in increasing order, so the strict
+        // comparison keeps its lowest maximal index; padding (-inf) never wins
+        float m = -INFINITY;
+        int mi = 0;
+#pragma unroll
+        for (int i = 0; i < V4; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (v[i][e] > m) { m = v[i][e]; mi = 4 * (l + 64 * i) + e; }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const float m2 = __shfl_xor(m, o);
+            const int i2 = __shfl_xor(mi, o);
+            fold_max(m, mi, m2, i2);
+        }
+        if (l == 0) argmax[row] = mi;
+    }
+    if (!A) return;
+    float mb = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < V4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[i][e] = (4 * (l + 64 * i) + e < M) ? beta * v[i][e] : -INFINITY;
+            mb = fmaxf(mb, v[i][e]);
+        }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mb = fmaxf(mb, __shfl_xor(mb, o));
+    float z = 0.f;
+#pragma unroll
+    for (int i = 0; i < V4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[i][e] = __expf(v[i][e] - mb);          // exp(-inf) = 0 past the row's end
+            z += v[i][e];
+        }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    const float iz = 1.f / z;
+    float *a = A + row * lda;
+#pragma unroll
+    for (int i = 0; i < V4; ++i) {
+        const int64_t c = 4 * (l + 64 * i);
+        const f4v q = v[i] * iz;
+        if (c + 4 <= M) {
+            __builtin_nontemporal_store(q, reinterpret_cast<f4v *>(a + c));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (c + e < M) a[c + e] = q[e];
+        }
+    }
+}
+
+// The same for any M and alignment: one wave per row, three sweeps (maximum
+// and its index, sum of exponentials, weights).  In place is safe: each
+// element is read and written by the same lane.
+__global__ void __launch_bounds__(256) rows_sim_attn_kernel(const float *W, int64_t ldw, int64_t B, int64_t M,
+                                                           int32_t *argmax, float beta, float *A, int64_t lda) {
+    const int l = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= B) return;
+    const float *w = W + row * ldw;
+    float m = -INFINITY, mb = -INFINITY;
+    int mi = 0;
+    for (int64_t c = l; c < M; c += 64) {
+        const float x = w[c];
+        if (x > m) { m = x; mi = (int)c; }
+        mb = fmaxf(mb, beta * x);
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const float m2 = __shfl_xor(m, o);
+        const int i2 = __shfl_xor(mi, o);
+        fold_max(m, mi, m2, i2);
+        mb = fmaxf(mb, __shfl_xor(mb, o));
+    }
+    if (argmax && l == 0) argmax[row] = mi;
+    if (!A) return;
+    float z = 0.f;
+    for (int64_t c = l; c < M; c += 64) z += __expf(beta * w[c] - mb);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    const float iz = 1.f / z;
+    float *a = A + row * lda;
+    for (int64_t c = l; c < M; c += 64) a[c] = __expf(beta * w[c] - mb) * iz;
+}
+
 // Scores of a few query rows (A, g.M rows) against every codebook row (B
 // stored N x K): one work-group per (query row, J codebook rows), the K range
 // split over its 256 threads, which also sum the squares for cosine norms
@@ -1295,6 +1407,21 @@ hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int
         return hipGetLastError();
     }
     return hipSuccess;
+}
+
+hipError_t launch_sim_attn_pass(const float *W, int64_t ldw, int64_t B, int64_t M, int32_t *argmax, float beta,
+                                float *A, int64_t lda, hipStream_t s) {
+    if (B == 0 || M == 0 || (!argmax && !A)) return hipSuccess;
+    const dim3 rgrid((unsigned)((B + 3) / 4));
+    const auto al = [](const float *p, int64_t ld) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 4 == 0; };
+    const bool aligned = al(W, ldw) && (!A || al(A, lda));
+    if (aligned && M <= 512)
+        hipLaunchKernelGGL((rows_sim_attn_reg_kernel<2>), rgrid, dim3(256), 0, s, W, ldw, B, M, argmax, beta, A, lda);
+    else if (aligned && M <= 2048)
+        hipLaunchKernelGGL((rows_sim_attn_reg_kernel<8>), rgrid, dim3(256), 0, s, W, ldw, B, M, argmax, beta, A, lda);
+    else
+        hipLaunchKernelGGL(rows_sim_attn_kernel, rgrid, dim3(256), 0, s, W, ldw, B, M, argmax, beta, A, lda);
+    return hipGetLastError();
 }
 
 bool sweep256_fits(gs_dtype t, const GemmArgs &a) {

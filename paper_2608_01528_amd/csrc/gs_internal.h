@@ -148,6 +148,11 @@ hipError_t launch_few_rows(gs_dtype t, const GemmArgs &a, bool softmax, hipStrea
 // place, or the row argmax (lowest index on ties) into argmax when non-null.
 hipError_t launch_rows_pass(bool softmax, float *out, int64_t ld, int64_t B, int64_t M, int32_t *argmax,
                             hipStream_t s);
+// One pass over a B x M fp32 score matrix W: the row argmax (lowest index on
+// ties) into argmax when non-null, and A = softmax(beta * W) row by row when
+// A is non-null (A may be W itself).
+hipError_t launch_sim_attn_pass(const float *W, int64_t ldw, int64_t B, int64_t M, int32_t *argmax, float beta,
+                                float *A, int64_t lda, hipStream_t s);
 
 // Raise a kernel's dynamic LDS limit (once per kernel, to a whole CU's LDS);
 // fails for requests beyond that.

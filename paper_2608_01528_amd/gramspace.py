@@ -6,7 +6,7 @@ Two layers with the C names:
   pointers exactly as declared in the header.
 * `gs_compress`, `gs_compress_padded`, `gs_compress_partitioned`, `gs_compress_noalloc`, `gs_project`, `gs_prob2vec`, `gs_prob2vec_sparse`,
   `gs_similarity`,
-  `gs_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
+  `gs_attention`, `gs_similarity_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
   below take torch tensors on the current
   GPU, allocate the outputs with torch, and pass pointers, sizes and the
   current stream to the library.  They only marshal arguments: every step of
@@ -75,6 +75,9 @@ _SIGS = {
     "gs_attention": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
                       _vp, _vp, ctypes.c_int, ctypes.c_float, ctypes.c_float, _vp, _i64,
                       _vp, ctypes.c_int, _i64, _vp], ctypes.c_int),
+    "gs_similarity_attention": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, ctypes.c_int, _i64, _i64,
+                                 _vp, _vp, ctypes.c_int, ctypes.c_float, _vp, _i64, _vp,
+                                 ctypes.c_float, _vp, _i64, _vp], ctypes.c_int),
     "gs_reconstruct": ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ctypes.c_int,
                         _vp, ctypes.c_int, _i64, _i64, _vp, ctypes.c_int, _i64, _vp], ctypes.c_int),
 }
@@ -358,6 +361,34 @@ def gs_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode
                               _mode(mode), float(scale), float(beta), _ptr(A), lda, _ptr(O), ot, ldo,
                               _stream()))
     return A, O
+
+
+def gs_similarity_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode="cosine",
+                            scale: float = 1.0, beta: float = 1.0, scores: bool = True, argmax: bool = True,
+                            attention: bool = True, out: torch.Tensor | None = None,
+                            argmax_out: torch.Tensor | None = None, a_out: torch.Tensor | None = None,
+                            echelon: bool = False):
+    """Scores S, row argmax and attention weights A = softmax(beta * S) from
+    one evaluation of the scores; each of the three may be switched off
+    (None is returned in its place)."""
+    tt, ldt = _mat(T, "T")
+    rt, ldr = _mat(R, "R")
+    rt |= GS_ECHELON if echelon else 0
+    B, r = T.shape
+    M = R.shape[0]
+    S = idx = A = None
+    if scores:
+        S = out if out is not None else torch.empty((B, M), dtype=torch.float32, device=T.device)
+    if argmax:
+        idx = argmax_out if argmax_out is not None else torch.empty(B, dtype=torch.int32, device=T.device)
+    if attention:
+        A = a_out if a_out is not None else torch.empty((B, M), dtype=torch.float32, device=T.device)
+    lds = _mat(S, "S")[1] if S is not None else M
+    lda = _mat(A, "A")[1] if A is not None else M
+    _check(lib().gs_similarity_attention(_ptr(T), tt, B, r, ldt, _ptr(R), rt, M, ldr, _ptr(qnorm2),
+                                         _ptr(cnorm), _mode(mode), float(scale), _ptr(S), lds, _ptr(idx),
+                                         float(beta), _ptr(A), lda, _stream()))
+    return S, idx, A
 
 
 def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = None, bind=None,

@@ -250,6 +250,24 @@ def test_attention_and_reconstruct_validation(L):
              NULL) == gsm.GS_ERR_SHAPE
 
 
+def test_similarity_attention_validation(L):
+    f = L.gs_similarity_attention
+    base = [A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0]
+    assert f(*base, NULL, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_ERR_ARG              # nothing asked for
+    assert "all null" in err(L)
+    assert f(*base, A3, 5, NULL, 2.0, A3, 5, NULL) == gsm.GS_ERR_ARG                  # A aliases S
+    assert f(*base, A1, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_ERR_ARG                # S aliases T
+    assert f(*base, NULL, 5, NULL, 2.0, A2, 5, NULL) == gsm.GS_ERR_ARG                # A aliases R
+    assert f(*base, A3, 4, NULL, 2.0, NULL, 5, NULL) == gsm.GS_ERR_SHAPE              # lds < M
+    assert f(*base, NULL, 5, NULL, 2.0, A3, 4, NULL) == gsm.GS_ERR_SHAPE              # lda < M
+    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_BF16, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0,
+             A3, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_ERR_DTYPE                     # T/R types differ
+    assert f(A1, gsm.GS_F32, 4, 5, 5, A2, gsm.GS_F32, 5, 5, NULL, NULL, 7, 1.0,
+             A3, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_ERR_ARG                       # unknown mode
+    assert f(NULL, gsm.GS_F32, 0, 5, 5, A2, gsm.GS_F32, 5, 5, NULL, NULL, gsm.GS_SIM_DOT, 1.0,
+             NULL, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_OK                          # empty batch
+
+
 def test_errors_are_per_thread(L):
     import threading
     assert compress(L, ct=7) == gsm.GS_ERR_DTYPE

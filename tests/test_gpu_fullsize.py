@@ -160,8 +160,8 @@ def test_stress_workload_full_size():
     # the benchmark's step: the same calls, flags and output types
     T, xn = gsm.gs_project(X, Q, out_dtype=torch.bfloat16, xnorm2=True)
     T2 = gsm.gs_prob2vec(P, R, out_dtype=torch.bfloat16, echelon=True)
-    S, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", echelon=True)
-    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0, echelon=True)
+    S, idx, A = gsm.gs_similarity_attention(T, R, qnorm2=xn, cnorm=cnorm, mode="cosine", beta=16.0,
+                                            echelon=True)
     Xr = gsm.gs_reconstruct(T2, Q, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     whole_batch_properties(S, idx, A)

@@ -366,6 +366,96 @@ def test_argmax_ties_lowest_index():
         assert int(host(idx).max()) == 0
 
 
+# ----------------------------------------- similarity and attention together
+
+SA_CASES = [
+    # B, M, D, storage, beta
+    (600, 40, 1024, torch.float32, 16.0),     # small-codebook scores
+    (300, 100, 1000, torch.float32, 4.0),     # product scores, one column tile
+    (520, 300, 700, torch.float32, -3.0),     # ragged column tiles, negative beta
+    (400, 600, 1200, torch.bfloat16, 16.0),   # bf16 storage
+]
+
+
+def softmax_of(S, beta):
+    """fp64 softmax of beta times the returned fp32 scores."""
+    z = beta * np.asarray(S, np.float64)
+    e = np.exp(z - z.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def first_max(S):
+    S = np.asarray(S)
+    return (S == S.max(axis=1, keepdims=True)).argmax(axis=1)
+
+
+@pytest.mark.parametrize("B,M,D,dt,beta", SA_CASES, ids=lambda v: _name_early(v) if isinstance(v, torch.dtype) else None)
+def test_similarity_attention(B, M, D, dt, beta):
+    print("similarity_attention", B, M, D, dt, beta, flush=True)
+    C, Qo, Ro, X, To = sim_inputs(B, M, D, 0.1 if M >= 300 else 0.0, False, seed=7)
+    qn = dev(oracle.row_norms(X) ** 2)
+    cn = dev(oracle.row_norms(C))
+    bf = dt == torch.bfloat16
+    Tin, Rin = (wl.round_bf16(To.astype(np.float32)), wl.round_bf16(Ro.astype(np.float32))) if bf else (To, Ro)
+    T, R = dev(Tin, dt), dev(Rin, dt)
+    kw = dict(qnorm2=qn, cnorm=cn, mode="cosine")
+    S, idx, A = gsm.gs_similarity_attention(T, R, beta=beta, **kw)
+    torch.cuda.synchronize()
+    tol = TOL_BF16 if bf else TOL_F32
+    So = oracle.similarity(X, C, oracle.COSINE)
+    assert rowrel(host(S), So) <= tol
+    assert rowrel(host(A), oracle.softmax(So, beta)) <= tol
+    # the three outputs derive from the one score matrix returned
+    Sh = host(S)
+    assert np.array_equal(host(idx), first_max(Sh))
+    assert rowrel(host(A), softmax_of(Sh, beta)) <= 1e-5
+    argmax_exact(idx, Tin, Rin, host(qn), host(cn))
+    # the scores and argmax are gs_similarity's, bit for bit
+    S1, idx1 = gsm.gs_similarity(T, R, **kw)
+    A1, _ = gsm.gs_attention(T, R, beta=beta, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(S, S1) and torch.equal(idx, idx1)
+    assert rowrel(host(A), host(A1)) <= 1e-5
+    # partial outputs: weights formed in place, argmax alone, weights alone
+    _, idx2, A2 = gsm.gs_similarity_attention(T, R, beta=beta, scores=False, **kw)
+    _, idx3, _ = gsm.gs_similarity_attention(T, R, beta=beta, scores=False, attention=False, **kw)
+    _, _, A4 = gsm.gs_similarity_attention(T, R, beta=beta, scores=False, argmax=False, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(A2, A) and torch.equal(A4, A)
+    assert torch.equal(idx2, idx) and torch.equal(idx3, idx)
+
+
+def test_similarity_attention_unaligned_and_long_rows():
+    # rows past 2048 entries and rows not 16-byte aligned take the three-sweep
+    # pass; the coordinates are arbitrary vectors (the dense form of the call)
+    rng = np.random.default_rng(11)
+    for B, M, r, ld_pad in [(300, 2500, 96, 0), (257, 700, 64, 1), (130, 5, 5, 2)]:
+        print("similarity_attention rows", B, M, r, ld_pad, flush=True)
+        T = rng.standard_normal((B, r)).astype(np.float32)
+        R = rng.standard_normal((M, r)).astype(np.float32)
+        S = torch.empty((B, M + ld_pad), device="cuda")[:, :M]
+        A = torch.empty((B, M + ld_pad), device="cuda")[:, :M]
+        for beta in (5.0, -2.0):
+            S_, idx, A_ = gsm.gs_similarity_attention(dev(T), dev(R), mode="cosine", beta=beta, out=S, a_out=A)
+            torch.cuda.synchronize()
+            So = oracle.similarity(T.astype(np.float64), R.astype(np.float64), oracle.COSINE)
+            assert rowrel(host(S), So) <= TOL_F32
+            assert rowrel(host(A), oracle.softmax(So, beta)) <= TOL_F32
+            assert np.array_equal(host(idx), first_max(host(S)))
+            assert rowrel(host(A), softmax_of(host(S), beta)) <= 1e-5
+            argmax_exact(idx, T, R)
+
+
+def test_similarity_attention_single_entry():
+    # one codebook entry: every weight is one and every argmax zero
+    T = np.random.default_rng(12).standard_normal((100, 1)).astype(np.float32)
+    S, idx, A = gsm.gs_similarity_attention(dev(T), dev(np.ones((1, 1), np.float32)), mode="dot", beta=3.0)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(S)[:, 0], T[:, 0])
+    assert not host(idx).any()
+    assert np.array_equal(host(A), np.ones((100, 1), np.float32))
+
+
 # -------------------------------------------------------------- reconstruct
 
 @pytest.mark.parametrize("B,M,D,dtype,pad", [
