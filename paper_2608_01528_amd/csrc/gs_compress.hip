@@ -146,16 +146,6 @@ __device__ __forceinline__ double dpp_f64(double v) {
     return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
-// Sum over the 8 lanes of an aligned group; every lane gets the same value
-// (each pairing adds the same two operands on both lanes): quad_perm swaps
-// within quads (xor 1, xor 2), then row_half_mirror pairs lane i with 7 - i.
-__device__ __forceinline__ double group8_sum(double v) {
-    v += dpp_f64<0xB1>(v);     // quad_perm [1, 0, 3, 2]
-    v += dpp_f64<0x4E>(v);     // quad_perm [2, 3, 0, 1]
-    v += dpp_f64<0x141>(v);    // row_half_mirror
-    return v;
-}
-
 __global__ void k_init(double *hc, int64_t nhc, int32_t *kept, int32_t *rank_after, int64_t M,
                        int32_t *flag) {
     const int64_t i = (int64_t)blockIdx.x * NT + threadIdx.x;
@@ -412,101 +402,105 @@ __global__ void __launch_bounds__(NT) k_bupdate(double *S, int sw, const double 
 // Triangular factor R (PB x PB, upper) of a tall matrix T (TCH x PB) by
 // Householder reflections, T = Q R.  Leaf: T[t][i] = S[i][TCH c + t], the
 // panel's rows (i < rows(sw)) over D-chunk c.  Node: T stacks up to TFAN
-// factors of the previous level.  Thread (k, g) = (t / 8, t % 8) holds column
-// k of T in registers, rows g + 8 q; only the current reflector goes through
-// LDS.  Signs of R's rows are whatever the reflections give: only the inner
+// factors of the previous level.  Thread (k, g) = (t / TG, t % TG) holds
+// column k of T in registers, rows g + TG q (q < TR), so the rows above a
+// reflection (j < PB = 2 TG) are the first two of every lane's rows and the
+// other rows need no masking; only the current reflector goes through LDS.
+// Signs of R's rows are whatever the reflections give: only the inner
 // products of R's columns (those of the panel's rows) are used.
+//
+// Reflection j: with x the part of column j from row j down, alpha = x_j,
+// beta = -sign(alpha) ||x|| and v = x - beta e_j, H = I - c v v^T with
+// c = 1 / (beta (beta - alpha)) maps x to beta e_j.  The loop over j is a
+// loop (not unrolled), so the kernel's code stays small.
 
-constexpr int TNQ = TCH / 8;   // rows of T held per thread
+constexpr int TG = 16;              // lanes per column (one DPP row)
+constexpr int TR = TCH / TG;        // rows of T held per lane
+constexpr int TSQR_NT = PB * TG;    // threads of the TSQR kernel
+// LDS stride of a lane's entries of the reflector: 16-byte reads of the 16
+// lanes of a column start at 36 g mod 64 banks, all distinct
+constexpr int VST = TR + 2;
+static_assert(PB == 2 * TG, "rows above a reflection: the first two of each lane");
 
-// Reflection j: zero column j of T below row j and apply it to the columns
-// to its right.  J is a compile-time constant so that every register index
-// is one.
-template <int J>
-__device__ __forceinline__ void hh_step(double (&a)[TNQ], int t, int k, int g, double (*vbuf)[TCH],
-                                        double (*coefs)[2]) {
-    constexpr int buf = J & 1, qj = J / 8, gj = J % 8;
-    constexpr int q0 = J / 8;        // rows g + 8q below this block are all above row J
-    if (k == J) {
-        double s4[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int q = q0; q < TNQ; ++q) {
-            const int row = g + 8 * q;
-            const double x = (row > J) ? a[q] : 0.0;
-            s4[q & 3] += x * x;
-        }
-        const double sg = group8_sum((s4[0] + s4[1]) + (s4[2] + s4[3]));
-        const double alpha = group8_sum((g == gj) ? a[qj] : 0.0);   // lane gj's entry, on all 8
-        double beta, tau, scale;
-        if (sg == 0.0) {
-            beta = alpha; tau = 0.0; scale = 0.0;
-        } else {
-            const double nrm = sqrt(alpha * alpha + sg);
-            beta = (alpha <= 0.0) ? nrm : -nrm;
-            tau = (beta - alpha) / beta;
-            scale = 1.0 / (alpha - beta);
-        }
-#pragma unroll
-        for (int q = q0; q < TNQ; ++q) {
-            const int row = g + 8 * q;
-            vbuf[buf][row] = (row > J) ? a[q] * scale : (row == J ? 1.0 : 0.0);
-        }
-        if (g == 0) coefs[buf][0] = tau;
-        if (g == gj) a[qj] = beta;      // R[J][J]
-    }
-    __syncthreads();
-    if (k > J) {
-        const double tau = coefs[buf][0];
-        double vr[TNQ];
-#pragma unroll
-        for (int q = q0; q < TNQ; ++q) {
-            const int row = g + 8 * q;
-            vr[q] = (row >= J) ? vbuf[buf][row] : 0.0;
-        }
-        double w4[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-        for (int q = q0; q < TNQ; ++q) w4[q & 3] += vr[q] * a[q];
-        const double wsum = group8_sum((w4[0] + w4[1]) + (w4[2] + w4[3])) * tau;
-#pragma unroll
-        for (int q = q0; q < TNQ; ++q) a[q] -= wsum * vr[q];
-    }
+// Sum over the 16 lanes of a DPP row; every lane gets the same value (each
+// pairing adds the same two operands on both lanes).
+__device__ __forceinline__ double group16_sum(double v) {
+    v += dpp_f64<0xB1>(v);     // quad_perm [1, 0, 3, 2]
+    v += dpp_f64<0x4E>(v);     // quad_perm [2, 3, 0, 1]
+    v += dpp_f64<0x141>(v);    // row_half_mirror
+    v += dpp_f64<0x140>(v);    // row_mirror
+    return v;
 }
 
-template <int... J>
-__device__ __forceinline__ void hh_all(double (&a)[TNQ], int t, int k, int g, double (*vbuf)[TCH],
-                                       double (*coefs)[2], std::integer_sequence<int, J...>) {
-    (hh_step<J>(a, t, k, g, vbuf, coefs), ...);
-}
-
-__global__ void __launch_bounds__(NT) k_tsqr(const double *S, int sw, int64_t D, const double *Rin,
-                                             int64_t nin, double *Rout, Panel p) {
-    __shared__ double vbuf[2][TCH];
-    __shared__ double coefs[2][2];
+__global__ void __launch_bounds__(TSQR_NT) k_tsqr(const double *S, int sw, int64_t D, const double *Rin,
+                                                  int64_t nin, double *Rout, Panel p) {
+    __shared__ __attribute__((aligned(16))) double vbuf[2][VST * TG];
+    __shared__ double coefs[2];
     const int t = threadIdx.x;
-    const int k = t >> 3, g = t & 7;
+    const int k = t / TG, g = t % TG;
     const int64_t c = blockIdx.x;
-    double a[TNQ];
+    double a[TR];
     if (S) {
         const int ns = rows_of(p, sw);
 #pragma unroll
-        for (int q = 0; q < TNQ; ++q) {
-            const int64_t d = c * TCH + g + 8 * q;
+        for (int q = 0; q < TR; ++q) {
+            const int64_t d = c * TCH + g + TG * q;
             a[q] = (k < ns && d < D) ? S[(int64_t)k * D + d] : 0.0;
         }
     } else {
 #pragma unroll
-        for (int q = 0; q < TNQ; ++q) {
-            const int row = g + 8 * q;                 // row of the stack
+        for (int q = 0; q < TR; ++q) {
+            const int row = g + TG * q;                // row of the stack
             const int64_t f = c * TFAN + row / PB;     // factor index
             a[q] = (f < nin) ? Rin[(f * PB + (row % PB)) * PB + k] : 0.0;
         }
     }
-    hh_all(a, t, k, g, vbuf, coefs, std::make_integer_sequence<int, PB>{});
-    // upper triangle of the first PB rows: R[i][k] = T[i][k], i <= k
+    double diag = 0.0;                  // R[k][k], set at reflection k
+#pragma unroll 1
+    for (int j = 0; j < PB; ++j) {
+        const int buf = j & 1;
+        if (k == j) {
+            // ||x below row j||^2 and alpha = T[j][j], on all 16 lanes
+            const double t0 = (g > j) ? a[0] : 0.0, t1 = (g + TG > j) ? a[1] : 0.0;
+            double s4[4] = {t0 * t0, t1 * t1, 0.0, 0.0};
 #pragma unroll
-    for (int q = 0; q < PB / 8; ++q) {
-        const int i = g + 8 * q;
-        Rout[(c * PB + i) * PB + k] = (i <= k) ? a[q] : 0.0;
+            for (int q = 2; q < TR; ++q) s4[q & 3] += a[q] * a[q];
+            const double al = (g == (j & (TG - 1))) ? (j < TG ? a[0] : a[1]) : 0.0;
+            const double sg = group16_sum((s4[0] + s4[1]) + (s4[2] + s4[3]));
+            const double alpha = group16_sum(al);
+            double beta = alpha, cf = 0.0;
+            if (sg != 0.0) {
+                const double nrm = sqrt(alpha * alpha + sg);
+                beta = (alpha <= 0.0) ? nrm : -nrm;
+                cf = 1.0 / (beta * (beta - alpha));
+            }
+            vbuf[buf][VST * g] = (g > j) ? a[0] : (g == j ? alpha - beta : 0.0);
+            vbuf[buf][VST * g + 1] = (g + TG > j) ? a[1] : (g + TG == j ? alpha - beta : 0.0);
+#pragma unroll
+            for (int q = 2; q < TR; ++q) vbuf[buf][VST * g + q] = a[q];
+            if (g == 0) coefs[buf] = cf;
+            diag = beta;
+        }
+        __syncthreads();
+        if (k > j) {
+            const double cf = coefs[buf];
+            double vr[TR];
+#pragma unroll
+            for (int q = 0; q < TR; ++q) vr[q] = vbuf[buf][VST * g + q];
+            double w4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+            for (int q = 0; q < TR; ++q) w4[q & 3] += vr[q] * a[q];
+            const double wsum = group16_sum((w4[0] + w4[1]) + (w4[2] + w4[3])) * cf;
+#pragma unroll
+            for (int q = 0; q < TR; ++q) a[q] -= wsum * vr[q];
+        }
+    }
+    // upper triangle of the first PB rows: R[i][k] for i < k from the
+    // registers, R[k][k] = beta of reflection k
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const int i = g + TG * q;
+        Rout[(c * PB + i) * PB + k] = (i < k) ? a[q] : (i == k ? diag : 0.0);
     }
 }
 
@@ -853,12 +847,12 @@ hipError_t block_pass(double *S, int sw, const double *Qb, int qw, int64_t max_q
 hipError_t panel_factor(const double *S, int sw, int64_t D, const Panel &p, double *b0, double *b1,
                         double **out, hipStream_t s) {
     int64_t n = leaf_count(D);
-    hipLaunchKernelGGL(k_tsqr, dim3((unsigned)n), dim3(NT), 0, s, S, sw, D, (const double *)nullptr, (int64_t)0,
+    hipLaunchKernelGGL(k_tsqr, dim3((unsigned)n), dim3(TSQR_NT), 0, s, S, sw, D, (const double *)nullptr, (int64_t)0,
                        b0, p);
     double *cur = b0, *nxt = b1;
     while (n > 1) {
         const int64_t m = (n + TFAN - 1) / TFAN;
-        hipLaunchKernelGGL(k_tsqr, dim3((unsigned)m), dim3(NT), 0, s, (const double *)nullptr, 0, D,
+        hipLaunchKernelGGL(k_tsqr, dim3((unsigned)m), dim3(TSQR_NT), 0, s, (const double *)nullptr, 0, D,
                            (const double *)cur, n, nxt, p);
         double *tmp = cur; cur = nxt; nxt = tmp;
         n = m;

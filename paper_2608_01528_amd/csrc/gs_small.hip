@@ -23,9 +23,6 @@ namespace {
 // for the widest codebooks (keeps the row tile and codebook block within
 // 64 KiB of LDS).
 template <int MB> constexpr int rows_of() { return MB <= 48 ? 256 : 128; }
-#ifndef SOFT_RPT
-#define SOFT_RPT 1
-#endif
 constexpr int MAXK = SOFT_MAX_M;          // widest row of the fused soft selection (32)
 
 enum Mode { MODE_P2V = 0, MODE_SIM = 1, MODE_ATT = 2 };
@@ -437,7 +434,7 @@ __global__ void __launch_bounds__(rows_of<MB>()) small_kernel(SmallArgs a) {
 // tile with coalesced stores.
 
 constexpr int SROWS = 256;               // threads per work-group
-constexpr int RPT = SOFT_RPT;            // rows per thread
+constexpr int RPT = 1;                   // rows per thread (the Gram form below assumes one)
 constexpr int SBLK = SROWS * RPT;        // rows per work-group
 
 __device__ __forceinline__ int soft_group(const SoftArgs &a, int64_t blk) {
