@@ -11,12 +11,13 @@
 //  2. the rows of the panel are orthogonalised among themselves in the small
 //     space of the panel's triangular factor: W^T = Q_t R_t by a tree of
 //     Householder factorisations (TSQR), so the columns a_i of R_t have the
-//     inner products of the rows w_i.  Gram-Schmidt with one
-//     re-orthogonalisation pass runs on those 32-entry columns in index order;
-//     row i is dependent when the norm of what is left of it is
-//     <= tol * ||c_i||, otherwise it adds a basis vector.  Each new basis
-//     vector is a combination of the panel's rows: V = X1 W;
-//  3. second pass on the new vectors: H2 = V Q^T, V -= H2 Q, then V is
+//     inner products of the rows w_i.  Modified Gram-Schmidt runs on those
+//     32-entry columns in index order, with a second projection for a column
+//     that lost most of its norm; row i is dependent when the norm of what
+//     is left of it is <= tol * ||c_i||, otherwise it adds a basis vector.
+//     Each new basis vector is a combination of the panel's rows: V = X1 W;
+//  3. second pass on the new vectors (where the first can have left them
+//     measurably off the earlier span): H2 = V Q^T, V -= H2 Q, then V is
 //     re-orthonormalised within itself (Cholesky of its Gram matrix, which is
 //     the identity up to rounding at this point): Q_new = L^-1 V;
 //  4. R of the panel's rows: R[i, old] = H1 + C1 H2 and R[i, new] = C1 L, with
@@ -514,184 +515,256 @@ __device__ __forceinline__ double lane_value(double v, int lane) {
     return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
-// Rank decisions of the panel.  Columns a_i of the panel factor R_t are
-// orthogonalised in index order by two Gram-Schmidt passes against the
-// vectors kept so far; row i is dependent if the norm left is
-// <= tol * ||c_i||.  Outputs: X1[l][i] (new vector l = sum_i X1[l][i] w_i),
-// C1[i][l] = <w_i, v_l> summed over both passes (the pivot for the row that
-// made v_l), rank_after and kept for the panel's rows.  One wave; lanes
-// 0..31 index vector entries or kept vectors; unkept rows of Z and X are
-// zero, so every loop runs over all 32.
+// Rank decisions of the panel, in the panel's small space: column a_i of the
+// factor R_t stands for row w_i (same inner products).  Rows are taken in
+// index order by modified Gram-Schmidt, right-looking: lane j holds a_j in
+// registers; when row i adds a vector z (its residual a_i / rho), the lanes
+// of the later rows project it out of their columns at once (local dot
+// products, one LDS broadcast of z per kept row).  Row i is dependent when the
+// norm rho left is <= tol * ||c_i||.  Where the projections took away most of
+// a_i (rho below REORTH of its norm), a_i is projected against all the kept
+// vectors once more (classical Gram-Schmidt) before the decision, so the kept
+// vectors stay orthogonal to working precision.  Outputs: X1[l][i] (new
+// vector l = sum_i X1[l][i] w_i), C1[i][l] = <w_i, v_l> summed over the
+// projections (the pivot for the row that made v_l), rank_after and kept for
+// the panel's rows, vectors in the order they were kept.  One wave; lanes
+// 0..31 are panel rows (columns of R_t) or vector entries.
+constexpr int LP = PB + 2;         // LDS row stride of the small-space matrices (16-byte aligned rows)
+constexpr double REORTH = 0.5;     // second projection when rho < REORTH * ||a_i||
+
+// Column c of the inverse of the lower-triangular matrix Ck (nk x nk) whose
+// row r is C[krow[r]][0 .. r] (the coefficients of the r-th kept row on the
+// vectors up to its own, the pivot last): y[r] for r < nk, zero above c and
+// past nk; rinv[r] = 1 / pivot r.  Rows are compile-time, so y stays in
+// registers.
+template <int... I>
+__device__ __forceinline__ void tri_inverse_column(double (&y)[PB], int c, int nk, const double (*C)[LP],
+                                                   const int *krow, const double *rinv,
+                                                   std::integer_sequence<int, I...>) {
+    auto row = [&](auto ic) {
+        constexpr int r = decltype(ic)::value;
+        const double *cr = C[krow[r]];
+        double s0 = (r == c) ? 1.0 : 0.0, s1 = 0.0;
+#pragma unroll
+        for (int q = 0; q + 1 < r; q += 2) {
+            s0 -= cr[q] * y[q];
+            s1 -= cr[q + 1] * y[q + 1];
+        }
+        if constexpr (r % 2 == 1) s0 -= cr[r - 1] * y[r - 1];
+        y[r] = (r >= c && r < nk) ? (s0 + s1) * rinv[r] : 0.0;
+    };
+    (row(std::integral_constant<int, I>{}), ...);
+}
+
 __global__ void __launch_bounds__(64) k_small_rank(const double *Rt, const double *cn, double tol, Panel p,
                                                    int32_t *rank_after, int32_t *kept, double *X1, double *C1,
                                                    int32_t *pass2_out) {
-    __shared__ double A[PB][PB + 1];     // A[i][e] = R_t[e][i]: column i of the factor
-    __shared__ __attribute__((aligned(16))) double vb[PB];
-    __shared__ __attribute__((aligned(16))) double hb[PB];
+    __shared__ __attribute__((aligned(16))) double C1s[PB][LP];  // C1s[i][k]: coefficient of row i on vector k
+    __shared__ __attribute__((aligned(16))) double XT[PB][LP];   // XT[i][k]: weight of row i in vector k
+    __shared__ __attribute__((aligned(16))) double P[PB][LP];    // second projection: h_k z_k[e]
+    __shared__ __attribute__((aligned(16))) double zb[PB];       // the vector broadcast
+    __shared__ __attribute__((aligned(16))) double tb[PB];
     __shared__ double thr[PB], thr_cn[PB];
+    __shared__ int kidx[PB];                                     // kept index of each row (-1: dependent)
+    __shared__ int krow[PB];                                     // row that made each kept vector
+    __shared__ double rinv[PB];                                  // 1 / pivot of each kept vector
     const int l = threadIdx.x;
     const bool act = l < PB;
+    const bool row_l = l < p.pb;       // lane l is a row of this panel
     const int r_old = rank_before(p.rank_after, p.i0);
-    if (l < p.pb) {
+    if (row_l) {
         thr_cn[l] = cn[p.i0 + l];
         thr[l] = tol * thr_cn[l];
     }
-    // lane l: zr[e] = z_l[e] (kept vector l), zc[k] = z_k[l], xc[k] = X[k][l];
-    // rows of vectors not (yet) kept are zero.  Values of other lanes come
-    // through vb / hb in LDS (broadcast reads).
-    double zr[PB], zc[PB], xc[PB];
-#pragma unroll
-    for (int e = 0; e < PB; ++e) { zr[e] = 0.0; zc[e] = 0.0; xc[e] = 0.0; }
-    for (int e = l; e < PB * PB; e += 64) {
-        const int i = e / PB, f = e % PB;
-        A[i][f] = Rt[f * PB + i];
-        C1[e] = 0.0;
-        X1[e] = 0.0;
+    if (act) {
+        kidx[l] = -1;
+        krow[l] = 0;
     }
-    __syncthreads();
-    // sum_j b[j] * r[j] with four running sums (fixed order)
-    auto dot4 = [](const double *b, const double (&r)[PB]) {
-        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    for (int e = l; e < PB * LP; e += 64) {
+        (&C1s[0][0])[e] = 0.0;
+        (&XT[0][0])[e] = 0.0;
+    }
+    // lane l: column l of R_t (zero for lanes past the panel)
+    double a[PB];
 #pragma unroll
-        for (int j = 0; j < PB; j += 4) {
-            s0 += b[j] * r[j];
-            s1 += b[j + 1] * r[j + 1];
-            s2 += b[j + 2] * r[j + 2];
-            s3 += b[j + 3] * r[j + 3];
+    for (int e = 0; e < PB; ++e) a[e] = row_l ? Rt[e * PB + l] : 0.0;
+    auto sumsq = [&]() {
+        double q0 = 0.0, q1 = 0.0, q2 = 0.0, q3 = 0.0;
+#pragma unroll
+        for (int e = 0; e < PB; e += 4) {
+            q0 += a[e] * a[e]; q1 += a[e + 1] * a[e + 1]; q2 += a[e + 2] * a[e + 2]; q3 += a[e + 3] * a[e + 3];
         }
-        return (s0 + s1) + (s2 + s3);
+        return (q0 + q1) + (q2 + q3);
     };
+    const double n0 = sqrt(sumsq());
+    __syncthreads();
     int nk = 0;
     for (int i = 0; i < p.pb; ++i) {
-        double v = act ? A[i][l] : 0.0;
-        double csum = 0.0;                   // lane k: coefficient on kept vector k
-        for (int pass = 0; pass < 2; ++pass) {
-            if (act) vb[l] = v;
-            __syncthreads();
-            const double h = act ? dot4(vb, zr) : 0.0;   // lane k: <v, z_k>
-            csum += h;
-            if (act) hb[l] = h;
-            __syncthreads();
-            if (act) v -= dot4(hb, zc);                  // lane e: sum_k h_k z_k[e]
-        }
-        if (act) vb[l] = v * v;
-        __syncthreads();
-        double s2 = 0.0;                     // ||v||^2, the same sum on every lane
-        {
-            double q0 = 0.0, q1 = 0.0, q2 = 0.0, q3 = 0.0;
+        double rho = sqrt(lane_value(sumsq(), i));
+        if (nk > 0 && rho < REORTH * lane_value(n0, i)) {
+            // a_i -= sum over kept k of <a_i, z_k> z_k; kept lanes k < i hold z_k
+            if (l == i) {
 #pragma unroll
-            for (int e = 0; e < PB; e += 4) {
-                q0 += vb[e]; q1 += vb[e + 1]; q2 += vb[e + 2]; q3 += vb[e + 3];
+                for (int e = 0; e < PB; ++e) zb[e] = a[e];
             }
-            s2 = (q0 + q1) + (q2 + q3);
-        }
-        const double rho = sqrt(s2);
-        const bool keep = rho > thr[i];
-        if (act && l < nk) C1[i * PB + l] = csum;
-        __syncthreads();
-        if (keep) {
-            // new vector z = v / rho, combination X = (e_i - sum_k c_k X_k) / rho
-            const double z = v / rho;
+            __syncthreads();
+            const bool holds_z = act && l < i && kidx[l] >= 0;
+            double h = 0.0;
+            if (holds_z) {
+                double h0 = 0.0, h1 = 0.0, h2 = 0.0, h3 = 0.0;
+#pragma unroll
+                for (int e = 0; e < PB; e += 4) {
+                    h0 += zb[e] * a[e]; h1 += zb[e + 1] * a[e + 1]; h2 += zb[e + 2] * a[e + 2]; h3 += zb[e + 3] * a[e + 3];
+                }
+                h = (h0 + h1) + (h2 + h3);
+                C1s[i][kidx[l]] += h;
+            }
             if (act) {
-                vb[l] = z;
-                hb[l] = (l < nk) ? csum : 0.0;
+#pragma unroll
+                for (int e = 0; e < PB; ++e) P[l][e] = holds_z ? h * a[e] : 0.0;
             }
             __syncthreads();
-            const double x = (((l == i) ? 1.0 : 0.0) - dot4(hb, xc)) / rho;
+            if (act) {
+                double t0 = 0.0, t1 = 0.0;           // entry l of sum_k h_k z_k, rows in order
 #pragma unroll
-            for (int kq = 0; kq < PB; ++kq) {
-                if (kq == nk) { zc[kq] = z; xc[kq] = x; }
+                for (int k = 0; k < PB; k += 2) { t0 += P[k][l]; t1 += P[k + 1][l]; }
+                tb[l] = t0 + t1;
             }
-            if (l == nk) {
+            __syncthreads();
+            if (l == i) {
 #pragma unroll
-                for (int e = 0; e < PB; ++e) zr[e] = vb[e];
+                for (int e = 0; e < PB; ++e) a[e] -= tb[e];
+            }
+            rho = sqrt(lane_value(sumsq(), i));
+        }
+        const bool keep = rho > thr[i];
+        if (keep) {
+            // lane i: z = a_i / rho; the later rows project it out
+            if (l == i) {
+                const double inv = 1.0 / rho;
+#pragma unroll
+                for (int e = 0; e < PB; ++e) {
+                    a[e] *= inv;
+                    zb[e] = a[e];
+                }
+                C1s[i][nk] = rho;
+                kidx[i] = nk;
+                rinv[nk] = inv;
+            }
+            __syncthreads();
+            if (row_l && l > i) {
+                double d0 = 0.0, d1 = 0.0, d2 = 0.0, d3 = 0.0;
+#pragma unroll
+                for (int e = 0; e < PB; e += 4) {
+                    d0 += zb[e] * a[e]; d1 += zb[e + 1] * a[e + 1]; d2 += zb[e + 2] * a[e + 2]; d3 += zb[e + 3] * a[e + 3];
+                }
+                const double d = (d0 + d1) + (d2 + d3);
+#pragma unroll
+                for (int e = 0; e < PB; ++e) a[e] -= d * zb[e];
+                C1s[l][nk] = d;
             }
             if (l == 0) {
-                C1[i * PB + nk] = rho;
                 kept[r_old + nk] = (int32_t)(p.i0 + i);
+                krow[nk] = i;
             }
             ++nk;
             __syncthreads();
         }
         if (l == 0) rank_after[p.i0 + i] = r_old + nk;
     }
-    if (act) {
-#pragma unroll
-        for (int kq = 0; kq < PB; ++kq)
-            if (kq < nk) X1[kq * PB + l] = xc[kq];
-    }
-    // largest combination weight sum_i |X1[k][i]| ||c_i|| over the new
-    // vectors (A is free now: A[k][i] = |X1[k][i]| ||c_i||)
     __syncthreads();
-    if (act) {
-        const double ci = (l < p.pb) ? thr_cn[l] : 0.0;
+    // weights of the new vectors: with Ck the coefficients of the kept rows on
+    // the new vectors (lower triangular, pivots on the diagonal), the kept
+    // rows are Ck times the new vectors, so X1 = Ck^-1 on the kept rows'
+    // columns.  Lane c: column c, written to XT[row of c][k]
+    if (act && l < nk) {
+        double y[PB];
+        tri_inverse_column(y, l, nk, C1s, krow, rinv, std::make_integer_sequence<int, PB>{});
+        const int ir = krow[l];
 #pragma unroll
-        for (int kq = 0; kq < PB; ++kq) A[kq][l] = fabs(xc[kq]) * ci;
+        for (int k = 0; k < PB; ++k)
+            if (k < nk) XT[ir][k] = y[k];
     }
     __syncthreads();
+    // outputs; and the largest combination weight sum_i |X1[k][i]| ||c_i||
+    // over the new vectors (lane k: vector k)
+    for (int e = l; e < PB * PB; e += 64) {
+        const int i = e / PB, k = e % PB;           // C1[i][k]
+        C1[e] = (i < p.pb && k < nk) ? C1s[i][k] : 0.0;
+        const int kx = e / PB, ix = e % PB;         // X1[kx][ix]
+        X1[e] = (kx < nk && ix < p.pb) ? XT[ix][kx] : 0.0;
+    }
     double wk = 0.0;
-    if (act) {
-#pragma unroll
-        for (int i = 0; i < PB; ++i) wk += A[l][i];
-    }
+    if (act && l < nk)
+        for (int i = 0; i < p.pb; ++i) wk += fabs(XT[i][l]) * thr_cn[i];
     for (int off = 32; off > 0; off >>= 1) wk = fmax(wk, __shfl_xor(wk, off));
     if (l == 0) *pass2_out = (wk > PASS2_WEIGHT) ? 1 : 0;
 }
 
 // Cholesky factor L of the Gram matrix G (n x n, n = new vectors; the
 // vectors are orthonormal up to rounding) and its inverse.  LX[0] = L (lower),
-// LX[1] = L^-1.  A pivot that is not positive sets flag 2.  One wave; entries
-// not yet computed are zero, so the sums run over all 32.
+// LX[1] = L^-1.  A pivot that is not positive sets flag 2.  One wave,
+// right-looking: lane l holds column l of the trailing matrix in registers;
+// step j broadcasts column j through LDS, and every later lane subtracts its
+// outer-product share (entries at or above j of a lane's column are no
+// longer read and are left as they come).
 template <int... I>
-__device__ __forceinline__ void inv_rows(double (&y)[PB], int c, const double (*L)[PB + 1],
+__device__ __forceinline__ void inv_rows(double (&y)[PB], int c, const double (*L)[PB + 1], const double *rd,
                                          std::integer_sequence<int, I...>) {
-    // y[i] = (delta_ic - sum_{k<i} L[i][k] y[k]) / L[i][i], rows in order
+    // y[i] = (delta_ic - sum_{k<i} L[i][k] y[k]) / L[i][i], rows in order, two running sums
     auto row = [&](auto ic) {
         constexpr int i = decltype(ic)::value;
-        double s = (i == c) ? 1.0 : 0.0;
+        double s0 = (i == c) ? 1.0 : 0.0, s1 = 0.0;
 #pragma unroll
-        for (int k = 0; k < i; ++k) s -= L[i][k] * y[k];
-        y[i] = (i >= c) ? s / L[i][i] : 0.0;
+        for (int k = 0; k + 1 < i; k += 2) {
+            s0 -= L[i][k] * y[k];
+            s1 -= L[i][k + 1] * y[k + 1];
+        }
+        if constexpr (i % 2 == 1) s0 -= L[i][i - 1] * y[i - 1];
+        y[i] = (i >= c) ? (s0 + s1) * rd[i] : 0.0;
     };
     (row(std::integral_constant<int, I>{}), ...);
 }
 
 __global__ void __launch_bounds__(64) k_small_chol(const double *G, Panel p, double *LX, int32_t *flag) {
     __shared__ double L[PB][PB + 1];
-    __shared__ double Gs[PB][PB + 1];
+    __shared__ __attribute__((aligned(16))) double zb[PB];
+    __shared__ double rd[PB];          // 1 / L[j][j]
     const int l = threadIdx.x;
     const bool act = l < PB;
     const int n = rows_of(p, ROWS_NEW);
-    for (int e = l; e < PB * PB; e += 64) {
-        L[e / PB][e % PB] = 0.0;
-        Gs[e / PB][e % PB] = G[e];
-    }
-    __syncthreads();
+    for (int e = l; e < PB * (PB + 1); e += 64) (&L[0][0])[e] = 0.0;
+    double a[PB];
+#pragma unroll
+    for (int e = 0; e < PB; ++e) a[e] = (act && l < n && e < n) ? G[e * PB + l] : 0.0;
     bool bad = false;
     for (int j = 0; j < n; ++j) {
-        // lane i >= j: L[i][j] = (G[i][j] - sum_k L[i][k] L[j][k]) / L[j][j]
-        double s = (act && l < n && l >= j) ? Gs[l][j] : 0.0;
-        if (act) {
-            double t0 = 0.0, t1 = 0.0;
+        if (l == j) {
 #pragma unroll
-            for (int kq = 0; kq < PB; kq += 2) {
-                t0 += L[l][kq] * L[j][kq];
-                t1 += L[l][kq + 1] * L[j][kq + 1];
-            }
-            s -= t0 + t1;
+            for (int e = 0; e < PB; ++e) zb[e] = a[e];
         }
-        const double djj = lane_value(s, j);
-        if (!(djj > 0.0)) bad = true;
-        const double ljj = sqrt(djj > 0.0 ? djj : 1.0);
         __syncthreads();
-        if (act && l < n && l >= j) L[l][j] = (l == j) ? ljj : s / ljj;
+        const double piv = zb[j];
+        if (!(piv > 0.0)) bad = true;
+        const double d = sqrt(piv > 0.0 ? piv : 1.0);
+        const double inv = 1.0 / d;
+        if (act && l >= j && l < n) L[l][j] = (l == j) ? d : zb[l] * inv;
+        if (l == j) rd[j] = inv;
+        if (act && l > j && l < n) {
+            const double f = zb[l] * inv * inv;    // L[l][j] / L[j][j]
+#pragma unroll
+            for (int e = 0; e < PB; ++e) a[e] -= f * zb[e];
+        }
         __syncthreads();
     }
     // identity padding beyond n keeps the inverse finite
-    if (act && l >= n) L[l][l] = 1.0;
+    if (act && l >= n) {
+        L[l][l] = 1.0;
+        rd[l] = 1.0;
+    }
     __syncthreads();
     double y[PB];
-    if (act) inv_rows(y, l, L, std::make_integer_sequence<int, PB>{});
+    if (act) inv_rows(y, l, L, rd, std::make_integer_sequence<int, PB>{});
 #pragma unroll
     for (int i = 0; i < PB; ++i)
         if (act) LX[PB * PB + i * PB + l] = (l < n && i < n) ? y[i] : 0.0;
