@@ -547,11 +547,16 @@ def stress_workload(args, torch, gsm):
     dt = torch.bfloat16
     log("stress: codebook %d x %d, compress" % (M, D))
     C = torch.from_numpy(wl.codebook(w)).to(dev)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
-    torch.cuda.synchronize()
-    compress_ms = (time.perf_counter() - t0) * 1e3
+    # the first call also loads the library's kernels; the second is the
+    # steady-state time
+    compress_runs = []
+    for _ in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        Q, R, r, kept, cnorm = gsm.gs_compress(C, q_dtype=dt, r_dtype=dt)
+        torch.cuda.synchronize()
+        compress_runs.append((time.perf_counter() - t0) * 1e3)
+    compress_ms = compress_runs[-1]
     rows = lambda n, c, t: gsm.alloc_rows(n, c, t, dev)
     P = wl.device_dirichlet_half(B, M, w.seed, torch, dev, dtype=dt)
     X = wl.device_noisy_queries(P, C, w.noise_var, w.seed, torch, dtype=dt)
@@ -628,7 +633,7 @@ def stress_workload(args, torch, gsm):
              "per_call_TFLOPs": {n: flops[n] / (mean[n] * 1e-3) / 1e12 for n in mean},
              "per_call_frac_bf16_peak": {n: flops[n] / (mean[n] * 1e-3) / 1e12 / peak for n in mean},
              "per_call_useful_TFLOPs": {n: useful[n] / (mean[n] * 1e-3) / 1e12 for n in useful},
-             "nnz_R": nnz, "compress_ms": compress_ms, "rank": r,
+             "nnz_R": nnz, "compress_ms": compress_ms, "compress_first_call_ms": compress_runs[0], "rank": r,
              "timing": "K steps of the four calls on the current stream; HIP events around every call",
              "kernel_source_hash": kernel_source_hash()}
     if not args.no_vsa:
