@@ -411,9 +411,13 @@ __global__ void __launch_bounds__(NT) k_bupdate(double *S, int sw, const double 
 // products of R's columns (those of the panel's rows) are used.
 //
 // Reflection j: with x the part of column j from row j down, alpha = x_j,
-// beta = -sign(alpha) ||x|| and v = x - beta e_j, H = I - c v v^T with
-// c = 1 / (beta (beta - alpha)) maps x to beta e_j.  The loop over j is a
-// loop (not unrolled), so the kernel's code stays small.
+// beta = -sign(alpha) ||x|| and v = x - beta e_j, H = I - v v^T / (beta
+// (beta - alpha)) maps x to beta e_j.  The two factors are applied one after
+// the other, (w / beta) / (beta - alpha) for w = <v, a>, each as a
+// reciprocal: their product underflows for columns of norm below about
+// 1e-154, the rounding residue that a rank-deficient panel leaves, and its
+// reciprocal would overflow.  The loop over j is a loop (not unrolled), so the
+// kernel's code stays small.
 
 constexpr int TG = 16;              // lanes per column (one DPP row)
 constexpr int TR = TCH / TG;        // rows of T held per lane
@@ -436,7 +440,7 @@ __device__ __forceinline__ double group16_sum(double v) {
 __global__ void __launch_bounds__(TSQR_NT) k_tsqr(const double *S, int sw, int64_t D, const double *Rin,
                                                   int64_t nin, double *Rout, Panel p) {
     __shared__ __attribute__((aligned(16))) double vbuf[2][VST * TG];
-    __shared__ double coefs[2];
+    __shared__ double coefs[2][2];
     const int t = threadIdx.x;
     const int k = t / TG, g = t % TG;
     const int64_t c = blockIdx.x;
@@ -469,29 +473,33 @@ __global__ void __launch_bounds__(TSQR_NT) k_tsqr(const double *S, int sw, int64
             const double al = (g == (j & (TG - 1))) ? (j < TG ? a[0] : a[1]) : 0.0;
             const double sg = group16_sum((s4[0] + s4[1]) + (s4[2] + s4[3]));
             const double alpha = group16_sum(al);
-            double beta = alpha, cf = 0.0;
+            double beta = alpha, c1 = 0.0, c2 = 0.0;
             if (sg != 0.0) {
                 const double nrm = sqrt(alpha * alpha + sg);
                 beta = (alpha <= 0.0) ? nrm : -nrm;
-                cf = 1.0 / (beta * (beta - alpha));
+                c1 = 1.0 / beta;
+                c2 = 1.0 / (beta - alpha);
             }
             vbuf[buf][VST * g] = (g > j) ? a[0] : (g == j ? alpha - beta : 0.0);
             vbuf[buf][VST * g + 1] = (g + TG > j) ? a[1] : (g + TG == j ? alpha - beta : 0.0);
 #pragma unroll
             for (int q = 2; q < TR; ++q) vbuf[buf][VST * g + q] = a[q];
-            if (g == 0) coefs[buf] = cf;
+            if (g == 0) {
+                coefs[buf][0] = c1;
+                coefs[buf][1] = c2;
+            }
             diag = beta;
         }
         __syncthreads();
         if (k > j) {
-            const double cf = coefs[buf];
+            const double c1 = coefs[buf][0], c2 = coefs[buf][1];
             double vr[TR];
 #pragma unroll
             for (int q = 0; q < TR; ++q) vr[q] = vbuf[buf][VST * g + q];
             double w4[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
             for (int q = 0; q < TR; ++q) w4[q & 3] += vr[q] * a[q];
-            const double wsum = group16_sum((w4[0] + w4[1]) + (w4[2] + w4[3])) * cf;
+            const double wsum = (group16_sum((w4[0] + w4[1]) + (w4[2] + w4[3])) * c1) * c2;
 #pragma unroll
             for (int q = 0; q < TR; ++q) a[q] -= wsum * vr[q];
         }

@@ -126,12 +126,15 @@ def _ptr(t):
 
 
 def _mat(t: torch.Tensor, name: str):
-    if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
+    # an empty matrix has no layout to check (its strides are arbitrary)
+    if t.dim() != 2 or (t.numel() > 0 and t.size(1) > 1 and t.stride(1) != 1):
         raise ValueError("%s must be a 2-D row-major tensor (unit column stride)" % name)
     if not t.is_cuda:
         raise ValueError("%s must be on the GPU" % name)
     if t.dtype not in _DT:
         raise ValueError("%s: unsupported dtype %s" % (name, t.dtype))
+    if t.numel() == 0:
+        return _DT[t.dtype], max(t.size(1), 1)
     return _DT[t.dtype], max(t.stride(0), t.size(1))
 
 

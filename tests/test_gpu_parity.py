@@ -201,6 +201,23 @@ def test_compress_rank_threshold(tol):
         assert np.abs(Rg - Ro).max() <= 1e-12 * np.abs(Ro).max()
 
 
+def test_compress_rank_one_codebook():
+    # every row a multiple of one bipolar vector: the panels' triangular
+    # factors hold only rounding residue past the first column, decaying by
+    # about 1e-16 per reflection towards the underflow range
+    rng = np.random.default_rng(21)
+    base = rng.choice([-1.0, 1.0], 700)
+    coef = rng.integers(1, 4, 45) * rng.choice([-1.0, 1.0], 45)
+    C = np.outer(coef, base).astype(np.float32)
+    Qo, Ro, kept_o, ro = oracle.compress(C)
+    Q, R, r, kept, _ = gsm.gs_compress(dev(C))
+    torch.cuda.synchronize()
+    assert r == ro == 1 and list(host(kept).astype(int)) == list(kept_o) == [0]
+    assert np.isfinite(host(R)).all() and np.isfinite(host(Q)).all()
+    assert np.abs(host(Q) - Qo).max() <= 1e-12
+    assert np.abs(host(R) - Ro).max() <= 1e-12 * np.abs(Ro).max()
+
+
 def test_compress_rejects_nonfinite():
     C = rq_codebook("bipolar", 8, 64, 1)
     C[3, 7] = np.nan

@@ -1,0 +1,227 @@
+"""Property tests of the GPU path on random small problems (hypothesis), and
+determinism / out-of-bounds checks.
+
+Properties, each drawn over random codebooks (bipolar, binary, Gaussian, with
+duplicated rows or of rank one), sizes with ragged tails (M, D, B not
+multiples of any tile; B = 0 and 1 included) and queries in or out of the
+codebook's span:
+
+* the factorisation (Sec. 3.1 Eq. 1, Sec. 3.2): Q Q^T = I, C = R Q, the rank
+  and kept rows of the oracle's Householder factorisation;
+* Sec. 3.2 Eq. 2-3: inner products and cosines of a query with the codebook
+  entries computed from the coordinates equal the dense ones (the oracle's
+  D-space definitions);
+* prob2vec and restore: the restore of p R is p C (Sec. 2.2, Sec. 3.1), and
+  projecting a restored vector returns its coordinates;
+* softmax invariants: rows sum to one, the weights are the softmax of beta
+  times the returned scores, beta = 0 gives 1/M; the returned argmax
+  is the first maximum of the returned scores.
+
+Determinism and bounds: every call twice gives bitwise identical outputs, and
+output buffers larger than the result (canary-filled rows before and after,
+padding after every row) keep the canary everywhere outside the result.
+
+Examples are derandomised (a fixed seed per test), so a failure reproduces.
+"""
+import numpy as np
+import pytest
+import torch
+from hypothesis import HealthCheck, given, settings, strategies as st
+
+import oracle
+from paper_2608_01528_amd import gramspace as gsm
+from tests.gpu_util import TOL_F32, dev, host, rowrel
+
+pytestmark = pytest.mark.gpu
+
+SETTINGS = settings(max_examples=30, deadline=None, derandomize=True, database=None,
+                    suppress_health_check=list(HealthCheck))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gsm.lib()
+
+
+def make_codebook(rng, kind, M, D, dup, rank_one):
+    if rank_one:
+        base = rng.choice([-1.0, 1.0], D)
+        C = np.outer(rng.integers(1, 4, M) * rng.choice([-1.0, 1.0], M), base)
+    elif kind == "bipolar":
+        C = rng.choice([-1.0, 1.0], (M, D))
+    elif kind == "binary":
+        C = rng.integers(0, 2, (M, D)).astype(np.float64)
+    else:
+        C = rng.standard_normal((M, D))
+    if dup and M > 2:
+        for i in rng.choice(np.arange(1, M), size=max(1, M // 8), replace=False):
+            C[i] = C[rng.integers(0, i)]
+    return C.astype(np.float32)
+
+
+@st.composite
+def problems(draw):
+    M = draw(st.integers(1, 70))
+    D = draw(st.integers(M, 330))
+    B = draw(st.one_of(st.sampled_from([0, 1, 2, 33, 257]), st.integers(0, 300)))
+    kind = draw(st.sampled_from(["bipolar", "binary", "gauss"]))
+    dup = draw(st.booleans())
+    rank_one = draw(st.booleans()) if M > 1 else False
+    in_span = draw(st.booleans())
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return M, D, B, kind, dup, rank_one, in_span, seed
+
+
+def inputs(M, D, B, kind, dup, rank_one, in_span, seed):
+    rng = np.random.default_rng(seed)
+    C = make_codebook(rng, kind, M, D, dup, rank_one)
+    P = rng.dirichlet(np.full(M, 0.5), size=B) if B > 0 else np.zeros((0, M))
+    X = P @ C.astype(np.float64)
+    if not in_span:
+        X = X + np.sqrt(0.1) * rng.standard_normal(X.shape)
+    return C, P.astype(np.float32), X.astype(np.float32)
+
+
+@SETTINGS
+@given(problems())
+def test_factorisation_properties(pr):
+    M, D, B, kind, dup, rank_one, in_span, seed = pr
+    C, _, _ = inputs(*pr)
+    Q, R, r, kept, _ = gsm.gs_compress(dev(C))
+    torch.cuda.synchronize()
+    Qh, Rh = host(Q), host(R)
+    _, _, kept_o, r_o = oracle.compress(C)
+    assert r == r_o and list(host(kept).astype(int)) == list(kept_o)
+    if rank_one:
+        assert r == 1
+    assert np.abs(Qh @ Qh.T - np.eye(r)).max() <= 1e-12
+    assert np.abs(Rh @ Qh - C).max() <= 1e-12 * max(1.0, np.abs(C).max())
+
+
+@SETTINGS
+@given(problems(), st.sampled_from([0.0, 1.0, 16.0, -3.0]))
+def test_coordinate_space_operators(pr, beta):
+    M, D, B, kind, dup, rank_one, in_span, seed = pr
+    C, P, X = inputs(*pr)
+    Q, R, r, _, cn = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    T, xn = gsm.gs_project(dev(X), Q, xnorm2=True)
+    S_dot, idx_dot = gsm.gs_similarity(T, R, mode="dot")
+    S_cos, idx = gsm.gs_similarity(T, R, qnorm2=xn, cnorm=cn, mode="cosine")
+    A, _ = gsm.gs_attention(T, R, qnorm2=xn, cnorm=cn, mode="cosine", beta=beta)
+    S2, idx2, A2 = gsm.gs_similarity_attention(T, R, qnorm2=xn, cnorm=cn, mode="cosine", beta=beta)
+    torch.cuda.synchronize()
+    assert S_dot.shape == (B, M) and A.shape == (B, M)
+    if B == 0:
+        return
+    # Eq. 2-3: the dense D-space definitions
+    assert rowrel(host(S_dot), oracle.similarity(X, C, oracle.DOT)) <= TOL_F32
+    assert rowrel(host(S_cos), oracle.similarity(X, C, oracle.COSINE)) <= TOL_F32
+    # argmax: the first maximum of the returned scores
+    for S_, i_ in ((S_dot, idx_dot), (S_cos, idx)):
+        Sh = host(S_)
+        assert np.array_equal(host(i_), (Sh == Sh.max(axis=1, keepdims=True)).argmax(axis=1))
+    # softmax invariants
+    Ah = host(A).astype(np.float64)
+    assert np.abs(Ah.sum(axis=1) - 1.0).max() <= 1e-5
+    z = beta * host(S_cos).astype(np.float64)
+    ref = np.exp(z - z.max(axis=1, keepdims=True))
+    ref /= ref.sum(axis=1, keepdims=True)
+    assert rowrel(Ah, ref) <= 1e-5
+    if beta == 0.0:
+        assert np.abs(Ah - 1.0 / M).max() <= 1e-7
+    # one score product: the scores and argmax are gs_similarity's
+    assert torch.equal(S2, S_cos) and torch.equal(idx2, idx)
+    assert rowrel(host(A2), ref) <= 1e-5
+
+
+@SETTINGS
+@given(problems())
+def test_prob2vec_restore_reproject(pr):
+    M, D, B, kind, dup, rank_one, in_span, seed = pr
+    C, P, _ = inputs(*pr)
+    Q, R, r, _, _ = gsm.gs_compress(dev(C), q_dtype=torch.float32, r_dtype=torch.float32)
+    T = gsm.gs_prob2vec(dev(P), R, echelon=True)
+    X = gsm.gs_reconstruct(T, Q)
+    T2 = gsm.gs_project(X, Q)
+    torch.cuda.synchronize()
+    if B == 0:
+        return
+    assert rowrel(host(X), oracle.prob2vec(P, C)) <= TOL_F32
+    assert rowrel(host(T2), host(T)) <= TOL_F32
+
+
+# ------------------------------------------------ determinism and bounds
+
+def canary_view(rows, cols, dtype, fill):
+    """A rows x cols view into a larger buffer: one canary row before, one
+    after, and 8 to 15 canary elements after every row (ld a multiple of 8)."""
+    ld = (cols + 8 + 7) // 8 * 8
+    buf = torch.full((rows + 2, ld), fill, dtype=dtype, device="cuda")
+    return buf, buf[1:1 + rows, :cols]
+
+
+def outside_untouched(buf, rows, cols, fill):
+    mask = torch.ones_like(buf, dtype=torch.bool)
+    mask[1:1 + rows, :cols] = False
+    outside = buf[mask]
+    if buf.dtype.is_floating_point:
+        return bool(torch.all(outside == torch.tensor(fill, dtype=buf.dtype, device=buf.device)))
+    return bool(torch.all(outside == fill))
+
+
+# shapes that reach the small kernels, the 128-row tiles and the 256 x 256
+# tiles with ragged edges
+SHAPES = [(257, 45, 40, 333), (600, 301, 150, 1000), (4099, 4101, 131, 4103)]
+
+
+def run_all(B, M, r, D, dt, seed=0):
+    """Every call of the path on random operands (T, R, Q need not come from
+    compress: the operators are defined for any coordinates), each output in
+    a canary-padded buffer; returns {name: (buffer, rows, cols, fill)}."""
+    g = torch.Generator(device="cuda").manual_seed(seed)
+
+    def rnd(a, b):            # 16-byte aligned rows, as the binding allocates them
+        t = gsm.alloc_rows(a, b, dt, "cuda")
+        t.copy_(torch.randn(a, b, generator=g, device="cuda"))
+        return t
+
+    T, R, Q, X = rnd(B, r), rnd(M, r), rnd(r, D), rnd(B, D)
+    P = gsm.alloc_rows(B, M, dt, "cuda")
+    P.copy_(torch.rand(B, M, generator=g, device="cuda"))
+    out = {}
+    fill_f, fill_i = 12345.0, -7
+
+    def fbuf(name, rows, cols, dtype):
+        b, v = canary_view(rows, cols, dtype, fill_f if dtype.is_floating_point else fill_i)
+        out[name] = (b, rows, cols, fill_f if dtype.is_floating_point else fill_i)
+        return v
+
+    gsm.gs_project(X, Q, out=fbuf("project", B, r, dt), xnorm2=True,
+                   xnorm2_out=fbuf("xnorm2", 1, B, torch.float32)[0])
+    gsm.gs_prob2vec(P, R, out=fbuf("prob2vec", B, r, dt))
+    gsm.gs_similarity(T, R, mode="cosine", out=fbuf("S", B, M, torch.float32),
+                      argmax_out=fbuf("argmax", 1, B, torch.int32)[0])
+    gsm.gs_attention(T, R, mode="cosine", beta=4.0, out=fbuf("A", B, M, torch.float32), weighted_sum=True,
+                     o_out=fbuf("O", B, r, dt))
+    gsm.gs_similarity_attention(T, R, mode="cosine", beta=4.0, out=fbuf("S2", B, M, torch.float32),
+                                argmax_out=fbuf("argmax2", 1, B, torch.int32)[0],
+                                a_out=fbuf("A2", B, M, torch.float32))
+    gsm.gs_reconstruct(T, Q, out=fbuf("reconstruct", B, D, dt))
+    gsm.gs_reconstruct(T, Q, T2=rnd(B, r), bind="mul", out=fbuf("bind", B, D, torch.float32))
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("B,M,r,D", SHAPES)
+def test_outputs_stay_inside_and_repeat_bitwise(B, M, r, D, dt):
+    print("canaries", B, M, r, D, dt, flush=True)
+    if M <= 64 and r > M:
+        r = M
+    a = run_all(B, M, r, D, dt)
+    b = run_all(B, M, r, D, dt)
+    for name, (buf, rows, cols, fill) in a.items():
+        assert outside_untouched(buf, rows, cols, fill), name
+        assert torch.equal(buf, b[name][0]), name
