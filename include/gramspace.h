@@ -122,10 +122,11 @@ size_t gs_compress_workspace(int64_t M, int64_t D);
  * Builds an orthonormal basis Q of the row space of the codebook C and its
  * coordinates R with C = R Q, by block Gram-Schmidt with re-orthogonalisation
  * over panels of codebook rows, in fp64 (the rows of a panel are
- * orthogonalised among themselves, twice, in the space of the panel's
- * triangular factor).  Codebook rows are taken in index order; row i is
- * dependent (adds no basis vector) when the norm of its part outside the
- * current span, after both passes, is <= tol * ||c_i||.  Kept rows
+ * orthogonalised among themselves in the space of the panel's triangular
+ * factor, by modified Gram-Schmidt with a second projection wherever the
+ * first took away most of a row's norm).  Codebook rows are taken in index
+ * order; row i is dependent (adds no basis vector) when the norm of its part
+ * outside the current span is <= tol * ||c_i||.  Kept rows
  * are listed in `kept`, so basis vector k comes from codebook row kept[k].  R
  * is lower-echelon: R[i, k] = <c_i, q_k> for basis vectors created before row
  * i, R[kept[k], k] > 0, zero elsewhere.  With these rules Q and R are unique.
@@ -293,6 +294,7 @@ gs_status gs_prob2vec(const void *P, gs_dtype pt, int64_t B, int64_t M, int64_t 
  *   cols   in   int32[nnz] device: codebook index j of each entry, 0 <= j < M
  *   vals   in   nnz probabilities p, type vt in {F32, BF16}
  *   R      in   M x r, rt == vt (a GS_ECHELON flag is ignored), ldr >= r
+ *               (r may exceed M, as for gs_prob2vec with a padded basis)
  *   T      out  B x r, tt in {F32, BF16}, ldt >= r
  * A row's entries are summed in their stored order in fp32; a row without
  * entries gives t = 0.  Entries whose index lies outside [0, M), and pointer

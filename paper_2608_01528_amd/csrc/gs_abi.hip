@@ -392,8 +392,8 @@ gs_status gs_prob2vec_sparse(const int64_t *rowptr, const int32_t *cols, const v
     const gs_dtype rt = coord_type(rt_in, &ech);
     if (!is_batch_type(vt) || rt != vt || !is_batch_type(tt))
         return fail(GS_ERR_DTYPE, "gs_prob2vec_sparse: values/R must be both f32 or both bf16 and T f32 or bf16");
-    if (B < 0 || M < 1 || r < 1 || r > M || nnz < 0)
-        return fail(GS_ERR_SHAPE, "gs_prob2vec_sparse: need B >= 0, nnz >= 0 and 1 <= r <= M");
+    if (B < 0 || M < 1 || r < 1 || nnz < 0)
+        return fail(GS_ERR_SHAPE, "gs_prob2vec_sparse: need B >= 0, M >= 1, r >= 1 and nnz >= 0");
     if (B > 0 && !rowptr) return fail(GS_ERR_ARG, "gs_prob2vec_sparse: rowptr is null");
     if (nnz > 0 && (!cols || !vals)) return fail(GS_ERR_ARG, "gs_prob2vec_sparse: cols or vals is null");
     GS_CHECK(check_aligned(rowptr, 8, "rowptr"));

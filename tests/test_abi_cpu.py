@@ -167,7 +167,8 @@ def test_prob2vec_sparse_validation(L):
 
     assert call(vt=gsm.GS_F64, rt=gsm.GS_F64) == gsm.GS_ERR_DTYPE
     assert call(rt=gsm.GS_BF16) == gsm.GS_ERR_DTYPE
-    assert call(r=11, ldr=11, ldt=11) == gsm.GS_ERR_SHAPE               # r > M
+    assert call(r=0) == gsm.GS_ERR_SHAPE
+    assert call(M=0) == gsm.GS_ERR_SHAPE
     assert call(nnz=-1) == gsm.GS_ERR_SHAPE
     assert call(rowptr=NULL) == gsm.GS_ERR_ARG
     assert call(cols=NULL) == gsm.GS_ERR_ARG

@@ -267,3 +267,123 @@ def test_outputs_stay_inside_and_repeat_bitwise(B, M, r, D, dt):
     for name, (buf, rows, cols, fill) in a.items():
         assert outside_untouched(buf, rows, cols, fill), name
         assert torch.equal(buf, b[name][0]), name
+
+
+# ------------------------------------------------ codebook variants
+
+@st.composite
+def partitioned_problems(draw):
+    M = draw(st.integers(1, 150))
+    D = draw(st.integers(max(1, M // 4), 260))
+    subset = draw(st.integers(1, D))
+    kind = draw(st.sampled_from(["bipolar", "binary", "gauss", "lowrank"]))
+    dup = draw(st.booleans())
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return M, D, subset, kind, dup, seed
+
+
+@SETTINGS
+@given(partitioned_problems())
+def test_partitioned_properties(pr):
+    # D < M allowed: one basis per consecutive subset of at most `subset` rows
+    M, D, subset, kind, dup, seed = pr
+    rng = np.random.default_rng(seed)
+    C = make_codebook(rng, kind, M, D, dup, False)
+    Q, R, r, ranks, kept, _ = gsm.gs_compress_partitioned(dev(C), subset=subset)
+    torch.cuda.synchronize()
+    Qh, Rh = host(Q), host(R)
+    starts = list(range(0, M, subset))
+    assert len(ranks) == len(starts) and sum(ranks) == r
+    assert np.abs(Rh @ Qh - C).max() <= 1e-12 * max(1.0, np.abs(C).max())
+    k0 = 0
+    for s0, rk in zip(starts, ranks):
+        rows = slice(s0, min(M, s0 + subset))
+        _, _, kept_o, r_o = oracle.compress(C[rows])
+        assert rk == r_o
+        Qs = Qh[k0:k0 + rk]
+        if rk:
+            assert np.abs(Qs @ Qs.T - np.eye(rk)).max() <= 1e-12
+        # block diagonal: the subset's rows use only its own basis rows
+        outside = np.ones(r, bool)
+        outside[k0:k0 + rk] = False
+        assert not np.any(Rh[rows][:, outside])
+        assert list(host(kept)[k0:k0 + rk].astype(int)) == [s0 + i for i in kept_o]
+        k0 += rk
+
+
+@st.composite
+def padded_problems(draw):
+    M = draw(st.integers(1, 40))
+    k = draw(st.integers(M, 80))
+    D = draw(st.integers(M + k, 300))
+    kind = draw(st.sampled_from(["bipolar", "binary", "gauss", "lowrank"]))
+    transform = draw(st.booleans())
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return M, k, D, kind, transform, seed
+
+
+@SETTINGS
+@given(padded_problems())
+def test_padded_properties(pr):
+    M, k, D, kind, transform, seed = pr
+    rng = np.random.default_rng(seed)
+    C = make_codebook(rng, kind, M, D, False, False)
+    H = None
+    if transform:                                   # a random orthogonal k x k
+        H, _ = np.linalg.qr(rng.standard_normal((k, k)))
+        H = torch.from_numpy(np.ascontiguousarray(H)).cuda()
+    Q, R, r, kept, _ = gsm.gs_compress_padded(dev(C), k, H=H)
+    Q0, R0, r0, kept0, _ = gsm.gs_compress(dev(C))
+    torch.cuda.synchronize()
+    Qh, Rh = host(Q), host(R)
+    assert Qh.shape == (k, D) and Rh.shape == (M, k) and r == r0
+    assert np.abs(Qh @ Qh.T - np.eye(k)).max() <= 1e-12
+    assert np.abs(Rh @ Qh - C).max() <= 1e-12 * max(1.0, np.abs(C).max())
+    if not transform and r > 0:
+        # the codebook's own basis first, coordinates zero past it
+        assert np.abs(Qh[:r] - host(Q0)).max() <= 1e-12
+        assert np.abs(Rh[:, :r] - host(R0)).max() <= 1e-12 * max(1.0, np.abs(host(R0)).max())
+        assert not np.any(Rh[:, r:])
+
+
+@st.composite
+def sparse_problems(draw):
+    B = draw(st.integers(0, 300))
+    M = draw(st.integers(1, 200))
+    r = draw(st.integers(1, 300))
+    density = draw(st.sampled_from([0.0, 0.01, 0.1, 0.5, 1.0]))
+    dt = draw(st.sampled_from(["f32", "bf16"]))
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return B, M, r, density, dt, seed
+
+
+@SETTINGS
+@given(sparse_problems())
+def test_sparse_prob2vec_properties(pr):
+    # t_b = sum over the stored entries of row b of p R_j, rows in CSR form
+    # (empty rows, repeated columns allowed), against the dense product
+    B, M, r, density, dts, seed = pr
+    rng = np.random.default_rng(seed)
+    dt = torch.float32 if dts == "f32" else torch.bfloat16
+    nnz_row = rng.binomial(M, density, size=B) if B else np.zeros(0, int)
+    cols = np.concatenate([rng.integers(0, M, n) for n in nnz_row]) if B else np.zeros(0, int)
+    vals = rng.random(cols.size).astype(np.float32)
+    R = rng.standard_normal((M, r)).astype(np.float32)
+    if dts == "bf16":
+        import paper_2608_01528_amd.workloads as wl
+        vals, R = wl.round_bf16(vals), wl.round_bf16(R)
+    rowptr = np.concatenate([[0], np.cumsum(nnz_row)]).astype(np.int64)
+    Rd = gsm.alloc_rows(M, r, dt, "cuda")
+    Rd.copy_(torch.from_numpy(R))
+    T = gsm.gs_prob2vec_sparse(torch.from_numpy(rowptr).cuda(), torch.from_numpy(cols.astype(np.int32)).cuda(),
+                               torch.from_numpy(vals).to(dt).cuda(), Rd, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = np.zeros((B, r))
+    absref = np.zeros((B, r))
+    for b in range(B):
+        for e in range(rowptr[b], rowptr[b + 1]):
+            ref[b] += float(vals[e]) * R[cols[e]].astype(np.float64)
+            absref[b] += abs(float(vals[e])) * np.abs(R[cols[e]].astype(np.float64))
+    u = 2.0 ** -24
+    n = np.maximum(nnz_row, 1)[:, None] if B else 1
+    assert np.all(np.abs(host(T) - ref) <= 1.5 * n * u * absref + 1e-30)
