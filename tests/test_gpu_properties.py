@@ -387,3 +387,67 @@ def test_sparse_prob2vec_properties(pr):
     u = 2.0 ** -24
     n = np.maximum(nnz_row, 1)[:, None] if B else 1
     assert np.all(np.abs(host(T) - ref) <= 1.5 * n * u * absref + 1e-30)
+
+
+# ------------------------------------------------ fused soft selection
+
+@st.composite
+def soft_problems(draw):
+    ngroups = draw(st.integers(1, 8))
+    Ms = draw(st.lists(st.integers(1, 32), min_size=ngroups, max_size=ngroups))
+    Bs = draw(st.lists(st.one_of(st.sampled_from([0, 1, 255, 256, 257]), st.integers(0, 700)),
+                       min_size=ngroups, max_size=ngroups))
+    D = draw(st.integers(32, 300))
+    form = draw(st.sampled_from(["auto", "coords", "gram", "auto-T"]))
+    mode = draw(st.sampled_from(["cosine", "dot"]))
+    beta = draw(st.sampled_from([1.0, 16.0, -3.0]))
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return Ms, Bs, D, form, mode, beta, seed
+
+
+@SETTINGS
+@given(soft_problems())
+def test_soft_select_properties(pr):
+    # several codebooks in one launch: the coordinates (when asked) are p R,
+    # the scores those of t = p R against R within the a-priori fp32 bound,
+    # the argmax bit-exact outside the near-tie band, the weights the softmax
+    # of beta times the returned scores
+    from tests.test_gpu_parity import soft_exact
+    from tests.gpu_util import check_argmax_bound
+    Ms, Bs, D, form, mode, beta, seed = pr
+    rng = np.random.default_rng(seed)
+    scale = 1.0 if mode == "cosine" else 0.05
+    groups, books = [], []
+    for M, B in zip(Ms, Bs):
+        C = make_codebook(rng, "bipolar", M, D, False, False)
+        _, Ro, _, r = oracle.compress(C)
+        P = rng.dirichlet(np.full(M, 0.5), size=B).astype(np.float32) if B else np.zeros((0, M), np.float32)
+        Rf = Ro.astype(np.float32)
+        g = {"P": dev(P), "R": dev(Rf),
+             "S": torch.full((B, M), np.nan, device="cuda"), "argmax": torch.full((B,), -1, dtype=torch.int32,
+                                                                                  device="cuda"),
+             "A": torch.full((B, M), np.nan, device="cuda")}
+        if form == "auto-T":
+            g["T"] = torch.full((B, r), np.nan, device="cuda")
+        groups.append(g)
+        books.append((P, Rf))
+    gsm.gs_soft_select(groups, mode=mode, scale=scale, beta=beta, form="auto" if form == "auto-T" else form)
+    torch.cuda.synchronize()
+    for g, (P, Rf) in zip(groups, books):
+        if P.shape[0] == 0:
+            continue
+        Se, E = soft_exact(P, Rf, None, mode, scale)
+        Sg = host(g["S"]).astype(np.float64)
+        assert np.all(np.abs(Sg - Se) <= E[:, None] + 1e-30)
+        check_argmax_bound(host(g["argmax"]), Se, E)
+        assert np.array_equal(host(g["argmax"]), (Sg == Sg.max(axis=1, keepdims=True)).argmax(axis=1))
+        z = beta * Sg
+        ref = np.exp(z - z.max(axis=1, keepdims=True))
+        ref /= ref.sum(axis=1, keepdims=True)
+        assert rowrel(host(g["A"]), ref) <= 1e-5
+        if "T" in g:
+            u = 2.0 ** -24
+            Tt = oracle.prob2vec(P, Rf)
+            absT = oracle.prob2vec(np.abs(P), np.abs(Rf))
+            M = Rf.shape[0]
+            assert np.all(np.abs(host(g["T"]) - Tt) <= 1.5 * M * u * absT + 1e-30)
