@@ -25,6 +25,10 @@ Determinism and bounds: every call twice gives bitwise identical outputs, and
 output buffers larger than the result (canary-filled rows before and after,
 padding after every row) keep the canary everywhere outside the result.
 
+The codebook variants (partitioned and padded bases, sparse probability
+rows), the fused soft selection and the binding of restored vectors get the
+same treatment against their definitions.
+
 Examples are derandomised (a fixed seed per test), so a failure reproduces.
 """
 import numpy as np
@@ -451,3 +455,55 @@ def test_soft_select_properties(pr):
             absT = oracle.prob2vec(np.abs(P), np.abs(Rf))
             M = Rf.shape[0]
             assert np.all(np.abs(host(g["T"]) - Tt) <= 1.5 * M * u * absT + 1e-30)
+
+
+# ------------------------------------------------ binding of restored vectors
+
+@st.composite
+def bind_problems(draw):
+    op = draw(st.sampled_from(["mul", "xor", "conv", "corr"]))
+    L = 2 ** draw(st.integers(1, 13))
+    blocks = draw(st.integers(1, max(1, 4096 // L)))
+    D = L * blocks if op in ("conv", "corr") else draw(st.integers(1, 3000))
+    B = draw(st.one_of(st.sampled_from([0, 1]), st.integers(2, 64)))
+    if op in ("conv", "corr"):
+        B = min(B, max(1, int(2e8 // (D * L))))    # the oracle's direct sums stay short
+    dt = draw(st.sampled_from(["f32", "bf16"]))
+    seed = draw(st.integers(0, 2 ** 31 - 1))
+    return op, L, D, B, dt, seed
+
+
+@SETTINGS
+@given(bind_problems())
+def test_bind_restored_properties(pr):
+    # each operator against the oracle's definition: products and xor exactly
+    # (after rounding to the output type), circular convolution / correlation
+    # within the fp32 FFT bound of a few units of log2(L) ||x|| ||y|| per block
+    op, L, D, B, dts, seed = pr
+    import paper_2608_01528_amd.workloads as wl
+    rng = np.random.default_rng(seed)
+    dt = torch.float32 if dts == "f32" else torch.bfloat16
+    if op == "xor":
+        X = rng.integers(0, 2, (B, D)).astype(np.float32)
+        Y = rng.integers(0, 2, (B, D)).astype(np.float32)
+    else:
+        X = rng.standard_normal((B, D)).astype(np.float32)
+        Y = rng.standard_normal((B, D)).astype(np.float32)
+    if dts == "bf16":
+        X, Y = wl.round_bf16(X), wl.round_bf16(Y)
+    Z = gsm.gs_bind_restored(dev(X, dt), dev(Y, dt), op=op, L=L, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    if B == 0:
+        return
+    Zh = host(Z).astype(np.float64)
+    if op == "mul":
+        assert np.array_equal(Zh, (X.astype(np.float64) * Y).astype(np.float32))
+    elif op == "xor":
+        assert np.array_equal(Zh, oracle.xor(X, Y))
+    else:
+        ref = oracle.circular(X, Y, L, corr=(op == "corr"))
+        xb = np.sqrt((X.astype(np.float64).reshape(B, -1, L) ** 2).sum(-1))
+        yb = np.sqrt((Y.astype(np.float64).reshape(B, -1, L) ** 2).sum(-1))
+        lim = 8 * np.log2(L) * 2.0 ** -24 * xb * yb                       # per block
+        err = np.abs(Zh - ref).reshape(B, -1, L).max(-1)
+        assert np.all(err <= lim + 1e-30)
