@@ -391,6 +391,7 @@ SA_CASES = [
     (300, 100, 1000, torch.float32, 4.0),     # product scores, one column tile
     (520, 300, 700, torch.float32, -3.0),     # ragged column tiles, negative beta
     (400, 600, 1200, torch.bfloat16, 16.0),   # bf16 storage
+    (500, 30, 700, torch.bfloat16, 8.0),      # bf16 storage, small-codebook scores
 ]
 
 
