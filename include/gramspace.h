@@ -52,6 +52,11 @@
  * written.  A zero batch (B == 0) is valid and does nothing; its batch-sized
  * buffers may then be NULL.  A failing launch
  * returns GS_ERR_DEVICE and leaves outputs undefined.
+ *
+ * Environment.  GS_DEBUG (any value): every call waits for the device after
+ * its launches and reports a failure found there as GS_ERR_DEVICE (slow; for
+ * locating a failing call).  GS_LOG (any value but "0"): one line on stderr
+ * per rejected call (status and message) and per launched call.
  */
 #ifndef GRAMSPACE_H
 #define GRAMSPACE_H

@@ -18,6 +18,16 @@ namespace {
 
 thread_local std::string g_err;
 
+// GS_LOG set (to anything but "0"): one line on stderr per rejected call
+// (its status and message) and per launched call (its name).
+bool logging() {
+    static const bool on = [] {
+        const char *v = getenv("GS_LOG");
+        return v && *v && !(v[0] == '0' && v[1] == 0);
+    }();
+    return on;
+}
+
 gs_status fail(gs_status st, const char *fmt, ...) {
     char buf[512];
     va_list ap;
@@ -25,6 +35,7 @@ gs_status fail(gs_status st, const char *fmt, ...) {
     vsnprintf(buf, sizeof buf, fmt, ap);
     va_end(ap);
     g_err = buf;
+    if (logging()) fprintf(stderr, "[gramspace] status %d: %s\n", (int)st, buf);
     return st;
 }
 
@@ -103,6 +114,7 @@ gs_status check_device() {
 
 gs_status launched(hipError_t e, const char *what) {
     if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+    if (logging()) fprintf(stderr, "[gramspace] %s: launched\n", what);
     if (getenv("GS_DEBUG")) {
         hipError_t e2 = hipDeviceSynchronize();
         if (e2 != hipSuccess) return fail(GS_ERR_DEVICE, "%s (GS_DEBUG sync): %s", what, hipGetErrorString(e2));

@@ -392,3 +392,20 @@ def test_echelon_flag_validation(L):
     # not a coordinate argument of these calls
     assert L.gs_project(A1, gsm.GS_F32, 4, 8, 8, A2, e32, 2, 8, A3, gsm.GS_F32, 2, NULL,
                         NULL) == gsm.GS_ERR_DTYPE
+
+
+def test_log_lines_for_rejected_calls():
+    # GS_LOG is read once per process: run a rejected call in a child process
+    import subprocess
+    import sys
+    code = ("import ctypes\nfrom paper_2608_01528_amd import gramspace as gsm\n"
+            "L = gsm.lib()\n"
+            "print(L.gs_prob2vec(None, gsm.GS_F32, 4, 4, 4, None, gsm.GS_F32, 4, 4, None, gsm.GS_F32, 4, None))\n")
+    env = dict(os.environ, GS_LOG="1")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, cwd=ROOT, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip() == str(gsm.GS_ERR_ARG)
+    assert "[gramspace] status %d:" % gsm.GS_ERR_ARG in r.stderr
+    env["GS_LOG"] = "0"
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, cwd=ROOT, timeout=120)
+    assert "[gramspace]" not in r.stderr
