@@ -523,9 +523,9 @@ def cpu_baseline_stress(w, Ps, Xs, beta, rows_desc):
     # (same source, no FMA contraction, no reassociation): checked on two rows
     t0 = time.perf_counter()
     S = oracle.similarity(Xs, C, oracle.COSINE)
-    oracle.argmax(S)
-    oracle.softmax(S, beta)
-    oracle.prob2vec(Ps, C)
+    idx = oracle.argmax(S)
+    A = oracle.softmax(S, beta)
+    V = oracle.prob2vec(Ps, C)
     dt = time.perf_counter() - t0
     n = Xs.shape[0]
     rate = n / dt
@@ -533,7 +533,34 @@ def cpu_baseline_stress(w, Ps, Xs, beta, rows_desc):
             "kind": "oracle", "build": flags,
             "sample": "%d seeded rows (%s) of the %d-row batch: dense fp64 cosine similarity of x with the "
                       "%d x %d codebook, argmax, softmax(beta=%g), v = p C; %.1f s; full batch extrapolated "
-                      "to %.0f s" % (n, rows_desc, w.B, w.Ms[0], w.D, beta, dt, w.B / rate)}
+                      "to %.0f s" % (n, rows_desc, w.B, w.Ms[0], w.D, beta, dt, w.B / rate)}, (S, idx, A, V)
+
+
+def rowrel(g, o):
+    """Row-scaled maximum relative difference: max over rows of
+    max_j |g - o| / max_j |o|."""
+    g = np.asarray(g, np.float64)
+    o = np.asarray(o, np.float64)
+    den = np.maximum(np.abs(o).max(axis=1), 1e-30)
+    return float((np.abs(g - o).max(axis=1) / den).max())
+
+
+def oracle_check(gpu, ref, tol=2e-2):
+    """The step's outputs on the oracle's sample rows against the oracle's
+    dense results (taken outside the timed region): row-scaled relative
+    differences of S, A and the restored v, and the argmax agreement; an
+    argmax differing where the oracle's top two scores are more than twice
+    the bf16 tolerance apart would be a fault."""
+    Sg, ig, Ag, Vg = gpu
+    So, io, Ao, Vo = ref
+    srt = np.sort(So, axis=1)
+    gap = srt[:, -1] - srt[:, -2]
+    band = 2 * tol * np.abs(So).max(axis=1)
+    diff = np.asarray(ig) != np.asarray(io)
+    return {"rows": int(len(So)), "max_rowrel_S": rowrel(Sg, So), "max_rowrel_A": rowrel(Ag, Ao),
+            "max_rowrel_restore": rowrel(Vg, Vo), "tolerance": tol,
+            "argmax_differ": int(diff.sum()), "argmax_differ_outside_band": int((diff & (gap > band)).sum()),
+            "against": "dense fp64 D-space definitions on the fp32 codebook and the queries' bf16 values"}
 
 
 def stress_workload(args, torch, gsm):
@@ -626,6 +653,8 @@ def stress_workload(args, torch, gsm):
         si = torch.from_numpy(sample).to(dev)
         Ps = P.index_select(0, si).float().cpu().numpy()
         Xs = X.index_select(0, si).float().cpu().numpy()
+        gpu_rows = (S.index_select(0, si).cpu().numpy(), idx.index_select(0, si).cpu().numpy(),
+                    A.index_select(0, si).cpu().numpy(), Xr.index_select(0, si).float().cpu().numpy())
     del X, Xr, P, T, T2, S, A, Q, R
     torch.cuda.empty_cache()
     extra = {"per_call_ms": mean,
@@ -641,7 +670,8 @@ def stress_workload(args, torch, gsm):
         extra["vsa_fused"] = vsa_fused_extra(args, torch, gsm)
     if not args.no_cpu:
         log("oracle: %d sampled rows" % n)
-        cpu = cpu_baseline_stress(w, Ps, Xs, beta, "numpy default_rng(%d).choice without replacement" % w.seed)
+        cpu, ref = cpu_baseline_stress(w, Ps, Xs, beta, "numpy default_rng(%d).choice without replacement" % w.seed)
+        extra["oracle_check"] = oracle_check(gpu_rows, ref)
     out = {
         "metric": METRIC, "value": B * args.steps / wall, "unit": "queries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
