@@ -93,18 +93,29 @@ def parse():
     return args
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(files=None) -> str:
+    """Hash of the library sources (all of csrc/, or the listed file names)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_01528_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    names = sorted(files) if files else sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    for f in names:
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
+
+
+def traffic_sources(kernel: str):
+    """Source files that build a profiled kernel and its launch path (a counter
+    record stays valid while these are unchanged)."""
+    if "gemm256" in kernel or "scores256" in kernel:
+        return ["gs_abi.hip", "gs_gemm.hip", "gs_gemm256.hip", "gs_internal.h"]
+    if "soft_" in kernel:
+        return ["gs_abi.hip", "gs_internal.h", "gs_small.hip"]
+    return None
 
 
 def load_traffic(call: str, workload: str):
     """HBM bytes per launch from the committed counter summary, if it was taken
-    on the current kernel sources (else None)."""
+    on the current sources of its kernel (else None)."""
     path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (call, workload))
     if not os.path.exists(path):
         return None
@@ -112,7 +123,7 @@ def load_traffic(call: str, workload: str):
         d = json.load(open(path))
     except ValueError:
         return None
-    if d.get("source_hash") != kernel_source_hash():
+    if d.get("source_hash") != kernel_source_hash(d.get("sources")):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -285,8 +296,9 @@ def pmc_summary(args):
     w_scale = copy_bytes / (cw_kib * 1024.0)
     read = f_kib * 1024.0 * f_scale
     write = w_kib * 1024.0 * w_scale
+    srcs = traffic_sources(args.pmc_kernel)
     out = {"kernel": args.pmc_kernel, "call": args.pmc_call, "workload": args.pmc_workload,
-           "source_hash": kernel_source_hash(),
+           "sources": srcs, "source_hash": kernel_source_hash(srcs),
            "hbm_bytes_per_launch": read + write, "read_bytes_per_launch": read, "write_bytes_per_launch": write,
            "fetch_kib_per_dispatch": f_kib, "write_kib_per_dispatch": w_kib, "dispatches": [nf, nw],
            "copy_calibration": {"bytes": copy_bytes, "fetch_kib": cf_kib, "write_kib": cw_kib,
