@@ -104,25 +104,99 @@ template <typename TI, typename TO> struct BlockIo {
     __device__ __forceinline__ void store(int e, f2v v) const { st_f32<TO>(out, e, v.x * inv); }
 };
 
-// One Stockham pass of radix R over the S values in LDS (blocks of L = 2^lg
-// values), the sub-transforms done so far having length Ns: butterfly q of
-// block blk (j = q mod L/R) takes values j + r L/R and writes its outputs to
-// (j / Ns) Ns R + (j mod Ns) + r Ns.  Each thread holds VPT values.  GIN:
-// gather from io.load instead of LDS; GOUT: scatter to io.store instead.
-template <int R, int VPT, bool GIN, bool GOUT, class Io>
-__device__ __forceinline__ void stockham_pass(f2v *z, int S, int lg, int Ns, int t, const Io &io) {
+// Pass P of a transform of L = 2^LG values: radix-16 passes, then one pass of
+// the remaining radix; the sub-transforms before it have length NS.
+template <int LG, int P> struct PassShape {
+    static constexpr int N16 = LG / 4, REM = LG % 4, NPASS = N16 + (REM != 0);
+    static constexpr int R = P < N16 ? 16 : (REM == 3 ? 8 : REM == 2 ? 4 : 2);
+    static constexpr int LOGR = R == 16 ? 4 : R == 8 ? 3 : R == 4 ? 2 : 1;
+    static constexpr int NS = 1 << (4 * P);
+    static constexpr int LR = 1 << (LG - LOGR);
+};
+
+// The pass twiddles exp(-2 pi i (j mod NS) r / (NS R)), r = 1 .. R - 1, of
+// this thread's butterflies in passes P, P + 1, ... (pass 0 has none): the
+// forward and the inverse transform take the same passes with the same
+// butterflies, so they are computed once per work-group and kept in
+// registers (with 16 values per thread; with 32, L = 8192, they would not
+// fit and each pass computes its own).  Powers by repeated products of
+// exp(-2 pi i (j mod NS) / (NS R)).
+template <int LG, int P, int VPT> __device__ __forceinline__ void pass_twiddles(f2v *w, int q) {
+    typedef PassShape<LG, P> Sh;
+    const int jm = (q & (Sh::LR - 1)) & (Sh::NS - 1);
+    float sn, cs;
+    // -2 jm / (NS R) exactly: the divisor is a power of two
+    sincospif((-2.0f / (float)(Sh::NS * Sh::R)) * (float)jm, &sn, &cs);
+    const f2v w1 = f2v{cs, sn};
+    f2v wr = w1;
+#pragma unroll
+    for (int r = 0; r < Sh::R - 1; ++r) {
+        w[r] = wr;
+        wr = cmul(wr, w1);
+    }
+}
+template <int LG, int P, int VPT, bool END = (P >= PassShape<LG, P>::NPASS || VPT > 16)> struct Twiddles {
+    static constexpr bool CACHED = true;
+    typedef PassShape<LG, P> Sh;
+    static constexpr int G = VPT / Sh::R;
+    f2v w[G][Sh::R - 1];
+    Twiddles<LG, P + 1, VPT> next;
+    __device__ __forceinline__ void init(int S, int t) {
+        const int nq = S >> Sh::LOGR;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int q = t + g * BT;
+            if (q < nq) pass_twiddles<LG, P, VPT>(w[g], q);
+        }
+        next.init(S, t);
+    }
+};
+template <int LG, int P, int VPT> struct Twiddles<LG, P, VPT, true> {
+    static constexpr bool CACHED = false;
+    __device__ __forceinline__ void init(int, int) {}
+};
+// The twiddles from pass 1 on (pass 0 has none).
+template <int LG, int VPT> struct TwiddlesAll {
+    static constexpr bool CACHED = true;
+    Twiddles<LG, 1, VPT> next;
+};
+// The twiddles of the passes after the one tw serves.
+template <class Tw> __device__ __forceinline__ const auto &next_twiddles(const Tw &tw) {
+    if constexpr (Tw::CACHED) return tw.next;
+    else return tw;
+}
+
+// One Stockham pass of radix R over the S values in LDS (blocks of L = 2^LG
+// values), the sub-transforms done so far having length NS: butterfly q of
+// block blk (j = q mod L/R) takes values j + r L/R, multiplies value r by the
+// pass twiddle r, and writes its outputs to (j / NS) NS R + (j mod NS) + r NS.
+// Each thread holds VPT values.  GIN: gather from io.load instead of LDS;
+// GOUT: scatter to io.store instead.  With L, R and NS known at compile time
+// the element offsets of a gather or scatter are constants added to one
+// padded base slot wherever a whole number of 16-value groups separates
+// consecutive elements.
+template <int LG, int P, int VPT, bool GIN, bool GOUT, class Io, class Tw>
+__device__ __forceinline__ void stockham_pass(f2v *z, int S, int t, const Io &io, const Tw &tw) {
+    typedef PassShape<LG, P> Sh;
+    constexpr int R = Sh::R, NS = Sh::NS, LR = Sh::LR, LOGR = Sh::LOGR;
     constexpr int G = VPT / R;
-    constexpr int LOGR = R == 16 ? 4 : R == 8 ? 3 : R == 4 ? 2 : 1;
-    const int lr = lg - LOGR, LR = 1 << lr, nq = S >> LOGR;
+    // consecutive gather elements LR apart; scatter elements NS apart (or the
+    // 16 outputs of a first radix-16 pass filling one group)
+    constexpr bool GC = LR % 16 == 0, SC = NS % 16 == 0 || (NS == 1 && R == 16);
+    const int nq = S >> LOGR;
     f2v v[G][R];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const int q = t + g * BT;
         if (q < nq) {
-            const int blk = q >> lr, j = q & (LR - 1);
-            const int base = (blk << lg) + j;
+            const int blk = q >> (LG - LOGR), j = q & (LR - 1);
+            const int base = (blk << LG) + j;
+            const int pb = pad(base);
 #pragma unroll
-            for (int r = 0; r < R; ++r) v[g][r] = GIN ? io.load(base + r * LR) : z[pad(base + r * LR)];
+            for (int r = 0; r < R; ++r) {
+                if (GIN) v[g][r] = io.load(base + r * LR);
+                else v[g][r] = z[GC ? pb + r * (LR + LR / 16) : pad(base + r * LR)];
+            }
         }
     }
     if (!GIN && !GOUT) __syncthreads();   // every gather is done before LDS is overwritten
@@ -130,57 +204,49 @@ __device__ __forceinline__ void stockham_pass(f2v *z, int S, int lg, int Ns, int
     for (int g = 0; g < G; ++g) {
         const int q = t + g * BT;
         if (q < nq) {
-            const int blk = q >> lr, j = q & (LR - 1);
-            const int jm = j & (Ns - 1);
-            if (Ns > 1) {
-                float sn, cs;
-                sincospif(-2.0f * (float)jm / (float)(Ns * R), &sn, &cs);
-                const f2v w = f2v{cs, sn};
-                f2v wr = w;
+            const int blk = q >> (LG - LOGR), j = q & (LR - 1);
+            const int jm = j & (NS - 1);
+            if constexpr (NS > 1) {
+                if constexpr (Tw::CACHED) {
 #pragma unroll
-                for (int r = 1; r < R; ++r) {
-                    v[g][r] = cmul(v[g][r], wr);
-                    wr = cmul(wr, w);
+                    for (int r = 1; r < R; ++r) v[g][r] = cmul(v[g][r], tw.w[g][r - 1]);
+                } else {
+                    f2v w[R - 1];
+                    pass_twiddles<LG, P, VPT>(w, q);
+#pragma unroll
+                    for (int r = 1; r < R; ++r) v[g][r] = cmul(v[g][r], w[r - 1]);
                 }
             }
             dft<R>(v[g]);
-            const int out = (blk << lg) + (j - jm) * R + jm;
+            const int out = (blk << LG) + (j - jm) * R + jm;
+            const int po = pad(out);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                if (GOUT) io.store(out + r * Ns, v[g][r]);
-                else z[pad(out + r * Ns)] = v[g][r];
+                if (GOUT) io.store(out + r * NS, v[g][r]);
+                else z[SC ? po + r * (NS + NS / 16) : pad(out + r * NS)] = v[g][r];
             }
         }
     }
     if (!GOUT) __syncthreads();
 }
 
-template <int R, int VPT, bool GIN, bool GOUT, class Io>
-__device__ __forceinline__ void pass_io(f2v *z, int S, int lg, int Ns, int t, const Io &io, bool first, bool last) {
-    if (GIN && first && GOUT && last) stockham_pass<R, VPT, true, true>(z, S, lg, Ns, t, io);
-    else if (GIN && first) stockham_pass<R, VPT, true, false>(z, S, lg, Ns, t, io);
-    else if (GOUT && last) stockham_pass<R, VPT, false, true>(z, S, lg, Ns, t, io);
-    else stockham_pass<R, VPT, false, false>(z, S, lg, Ns, t, io);
+// Passes P .. of the forward transform of every block; GIN / GOUT as in
+// stockham_pass, for the first / last pass.
+template <int LG, int P, int VPT, bool GIN, bool GOUT, class Io, class Tw>
+__device__ __forceinline__ void fft_passes(f2v *z, int S, int t, const Io &io, const Tw &tw) {
+    typedef PassShape<LG, P> Sh;
+    if constexpr (P < Sh::NPASS) {
+        stockham_pass<LG, P, VPT, GIN && P == 0, GOUT && P == Sh::NPASS - 1>(z, S, t, io, tw);
+        fft_passes<LG, P + 1, VPT, GIN, GOUT>(z, S, t, io, next_twiddles(tw));
+    }
 }
 
-// Forward transform of every block: radix-16 passes, then one pass of the
-// remaining radix; GIN / GOUT as in stockham_pass, for the first / last pass.
-template <int VPT, bool GIN, bool GOUT, class Io>
-__device__ __forceinline__ void fft_blocks(f2v *z, int S, int lg, int t, const Io &io) {
-    const int n16 = lg >> 2, rem = lg & 3, npass = n16 + (rem != 0);
-    int Ns = 1;
-    for (int p = 0; p < n16; ++p, Ns <<= 4)
-        pass_io<16, VPT, GIN, GOUT>(z, S, lg, Ns, t, io, p == 0, p == npass - 1);
-    const bool first = n16 == 0;
-    if (rem == 3) pass_io<8, VPT, GIN, GOUT>(z, S, lg, Ns, t, io, first, true);
-    else if (rem == 2) pass_io<4, VPT, GIN, GOUT>(z, S, lg, Ns, t, io, first, true);
-    else if (rem == 1) pass_io<2, VPT, GIN, GOUT>(z, S, lg, Ns, t, io, first, true);
-}
-
-template <typename TI, typename TO, bool CORR, int VPT>
+// Blocks of L = 2^LG values; a work-group holds nb of them (S = nb L <= VPT BT).
+template <typename TI, typename TO, bool CORR, int LG>
 __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
+    constexpr int L = 1 << LG, VPT = L > 16 * BT ? L / BT : 16;
     extern __shared__ f2v smem[];
-    const int L = (int)a.L, lg = a.lg, nbmax = a.nb;
+    const int nbmax = a.nb;
     const int64_t wpr = (a.nblocks + nbmax - 1) / nbmax;          // work-groups per row
     const int64_t row = (int64_t)blockIdx.x / wpr;
     const int64_t blk0 = ((int64_t)blockIdx.x - row * wpr) * nbmax;
@@ -194,14 +260,16 @@ __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
     io.out = static_cast<TO *>(a.Z) + row * a.ldz + blk0 * L;
     io.inv = 1.0f / (float)L;
 
-    fft_blocks<VPT, true, false>(z, S, lg, t, io);
+    TwiddlesAll<LG, VPT> tw;
+    tw.next.init(S, t);
+    fft_passes<LG, 0, VPT, true, false>(z, S, t, io, tw);
 
     // product of the two spectra, stored conjugated for the inverse;
     // P_{L-k} = conj P_k (real signals)
     for (int q = t; q < nb * (L / 2 + 1); q += BT) {
         const int blk = q / (L / 2 + 1), k = q - blk * (L / 2 + 1);
         const int kk = (L - k) & (L - 1);
-        const int ik = pad((blk << lg) + k), ikk = pad((blk << lg) + kk);
+        const int ik = pad((blk << LG) + k), ikk = pad((blk << LG) + kk);
         const f2v zk = z[ik], zm = conjv(z[ikk]);
         const f2v X = (zk + zm) * 0.5f;
         const f2v Yk = mul_mi((zk - zm) * 0.5f);
@@ -210,7 +278,7 @@ __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
         if (kk != k) z[ikk] = P;
     }
     __syncthreads();
-    fft_blocks<VPT, false, true>(z, S, lg, t, io);
+    fft_passes<LG, 0, VPT, false, true>(z, S, t, io, tw);
 }
 
 // Element-wise product or exclusive or; one work-group per 2048 values of a row.
@@ -229,14 +297,14 @@ __global__ void __launch_bounds__(BT) elementwise_kernel(BindArgs a) {
     }
 }
 
-template <typename TI, typename TO, int VPT>
+template <typename TI, typename TO, int LG>
 hipError_t launch_circular(int op, dim3 grid, size_t lds, const BindArgs &a, hipStream_t s) {
-    const void *k = (op == GS_BINDOP_CORR) ? reinterpret_cast<const void *>(circular_kernel<TI, TO, true, VPT>)
-                                           : reinterpret_cast<const void *>(circular_kernel<TI, TO, false, VPT>);
+    const void *k = (op == GS_BINDOP_CORR) ? reinterpret_cast<const void *>(circular_kernel<TI, TO, true, LG>)
+                                           : reinterpret_cast<const void *>(circular_kernel<TI, TO, false, LG>);
     hipError_t e = raise_lds_limit(k, lds);
     if (e != hipSuccess) return e;
-    if (op == GS_BINDOP_CORR) hipLaunchKernelGGL((circular_kernel<TI, TO, true, VPT>), grid, dim3(BT), lds, s, a);
-    else hipLaunchKernelGGL((circular_kernel<TI, TO, false, VPT>), grid, dim3(BT), lds, s, a);
+    if (op == GS_BINDOP_CORR) hipLaunchKernelGGL((circular_kernel<TI, TO, true, LG>), grid, dim3(BT), lds, s, a);
+    else hipLaunchKernelGGL((circular_kernel<TI, TO, false, LG>), grid, dim3(BT), lds, s, a);
     return hipGetLastError();
 }
 
@@ -253,9 +321,23 @@ hipError_t launch_typed(int op, const BindArgs &a, hipStream_t s) {
     const dim3 grid((unsigned)(a.B * wpr));
     const int64_t S = a.nb * a.L;                         // values per work-group
     const size_t lds = (size_t)(S + S / 16) * sizeof(f2v);
-    if (S > 32 * BT) return hipErrorInvalidValue;
-    if (S <= 16 * BT) return launch_circular<TI, TO, 16>(op, grid, lds, a, s);
-    return launch_circular<TI, TO, 32>(op, grid, lds, a, s);
+    if (S > (a.lg == 13 ? 32 : 16) * BT) return hipErrorInvalidValue;
+    switch (a.lg) {
+    case 1: return launch_circular<TI, TO, 1>(op, grid, lds, a, s);
+    case 2: return launch_circular<TI, TO, 2>(op, grid, lds, a, s);
+    case 3: return launch_circular<TI, TO, 3>(op, grid, lds, a, s);
+    case 4: return launch_circular<TI, TO, 4>(op, grid, lds, a, s);
+    case 5: return launch_circular<TI, TO, 5>(op, grid, lds, a, s);
+    case 6: return launch_circular<TI, TO, 6>(op, grid, lds, a, s);
+    case 7: return launch_circular<TI, TO, 7>(op, grid, lds, a, s);
+    case 8: return launch_circular<TI, TO, 8>(op, grid, lds, a, s);
+    case 9: return launch_circular<TI, TO, 9>(op, grid, lds, a, s);
+    case 10: return launch_circular<TI, TO, 10>(op, grid, lds, a, s);
+    case 11: return launch_circular<TI, TO, 11>(op, grid, lds, a, s);
+    case 12: return launch_circular<TI, TO, 12>(op, grid, lds, a, s);
+    case 13: return launch_circular<TI, TO, 13>(op, grid, lds, a, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace
