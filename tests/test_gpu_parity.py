@@ -1447,6 +1447,28 @@ def test_bind_circular(B, D, L, op, dt):
     assert rowrel(host(Zb), Zo) <= TOL_BF16
 
 
+@pytest.mark.parametrize("L", [1 << k for k in range(1, 14)])
+@pytest.mark.parametrize("op", ["conv", "corr"])
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+def test_bind_circular_every_block_length(L, op, dt):
+    # the transform is compiled once per block length: every length from 2 to
+    # 8192, with a row split over two work-groups, the second holding fewer
+    # blocks (6144 values) where blocks are shorter than 4096
+    B, D = 3, (6144 if L <= 2048 else 8192)
+    print("bind all L", op, L, D, dt, flush=True)
+    rng = np.random.default_rng(1000 + L)
+    X = rng.standard_normal((B, D)).astype(np.float32)
+    Y = rng.standard_normal((B, D)).astype(np.float32)
+    if dt == torch.bfloat16:
+        X, Y = wl.round_bf16(X), wl.round_bf16(Y)
+    Z = gsm.gs_bind_restored(dev(X, dt), dev(Y, dt), op=op, L=L, out_dtype=torch.float32)
+    Zb = gsm.gs_bind_restored(dev(X, dt), dev(Y, dt), op=op, L=L, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    Zo = oracle.circular(X, Y, L, corr=(op == "corr"))
+    assert rowrel(host(Z), Zo) <= TOL_F32
+    assert rowrel(host(Zb), Zo) <= TOL_BF16
+
+
 def test_bind_restored_codebook_vectors():
     # restored bipolar codebook vectors (reconstruct of their coordinates):
     # bind two of them, unbind with the second, and compare each step with the
