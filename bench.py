@@ -670,12 +670,14 @@ def stress_workload(args, torch, gsm):
     del X, Xr, P, T, T2, S, A, Q, R
     torch.cuda.empty_cache()
     extra = {"per_call_ms": mean,
+             "per_call_median_ms": {n: float(np.median(v)) for n, v in per.items()},
+             "per_call_min_ms": {n: float(np.min(v)) for n, v in per.items()},
              "per_call_sum_ms": float(sum(mean.values())),
              "per_call_TFLOPs": {n: flops[n] / (mean[n] * 1e-3) / 1e12 for n in mean},
              "per_call_frac_bf16_peak": {n: flops[n] / (mean[n] * 1e-3) / 1e12 / peak for n in mean},
              "per_call_useful_TFLOPs": {n: useful[n] / (mean[n] * 1e-3) / 1e12 for n in useful},
              "nnz_R": nnz, "compress_ms": compress_ms, "compress_first_call_ms": compress_runs[0], "rank": r,
-             "timing": "K steps of the four calls on the current stream; HIP events around every call",
+             "timing": "K steps of the four calls on the current stream; HIP events around every call (mean, median and minimum per call)",
              "kernel_source_hash": kernel_source_hash()}
     if not args.no_vsa:
         log("vsa: fused soft selection (both forms)")
