@@ -117,11 +117,11 @@ template <int LG, int P> struct PassShape {
 // The pass twiddles exp(-2 pi i (j mod NS) r / (NS R)), r = 1 .. R - 1, of
 // this thread's butterflies in passes P, P + 1, ... (pass 0 has none): the
 // forward and the inverse transform take the same passes with the same
-// butterflies, so they are computed once per work-group and kept in
+// butterflies, so each thread computes its own once and keeps them in
 // registers (with 16 values per thread; with 32, L = 8192, they would not
 // fit and each pass computes its own).  Powers by repeated products of
 // exp(-2 pi i (j mod NS) / (NS R)).
-template <int LG, int P, int VPT> __device__ __forceinline__ void pass_twiddles(f2v *w, int q) {
+template <int LG, int P> __device__ __forceinline__ void pass_twiddles(f2v *w, int q) {
     typedef PassShape<LG, P> Sh;
     const int jm = (q & (Sh::LR - 1)) & (Sh::NS - 1);
     float sn, cs;
@@ -146,7 +146,7 @@ template <int LG, int P, int VPT, bool END = (P >= PassShape<LG, P>::NPASS || VP
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             const int q = t + g * BT;
-            if (q < nq) pass_twiddles<LG, P, VPT>(w[g], q);
+            if (q < nq) pass_twiddles<LG, P>(w[g], q);
         }
         next.init(S, t);
     }
@@ -212,7 +212,7 @@ __device__ __forceinline__ void stockham_pass(f2v *z, int S, int t, const Io &io
                     for (int r = 1; r < R; ++r) v[g][r] = cmul(v[g][r], tw.w[g][r - 1]);
                 } else {
                     f2v w[R - 1];
-                    pass_twiddles<LG, P, VPT>(w, q);
+                    pass_twiddles<LG, P>(w, q);
 #pragma unroll
                     for (int r = 1; r < R; ++r) v[g][r] = cmul(v[g][r], w[r - 1]);
                 }
@@ -265,9 +265,9 @@ __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
     fft_passes<LG, 0, VPT, true, false>(z, S, t, io, tw);
 
     // product of the two spectra, stored conjugated for the inverse;
-    // P_{L-k} = conj P_k (real signals)
-    for (int q = t; q < nb * (L / 2 + 1); q += BT) {
-        const int blk = q / (L / 2 + 1), k = q - blk * (L / 2 + 1);
+    // P_{L-k} = conj P_k (real signals): k = 0 .. L/2 - 1 with its partner
+    // L - k (k = 0 is its own), then k = L/2 (its own) of every block
+    auto product = [&](int blk, int k) {
         const int kk = (L - k) & (L - 1);
         const int ik = pad((blk << LG) + k), ikk = pad((blk << LG) + kk);
         const f2v zk = z[ik], zm = conjv(z[ikk]);
@@ -276,7 +276,9 @@ __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
         const f2v P = CORR ? cmul(X, conjv(Yk)) : cmul(X, Yk);
         z[ik] = conjv(P);
         if (kk != k) z[ikk] = P;
-    }
+    };
+    for (int q = t; q < nb * (L / 2); q += BT) product(q >> (LG - 1), q & (L / 2 - 1));
+    for (int blk = t; blk < nb; blk += BT) product(blk, L / 2);
     __syncthreads();
     fft_passes<LG, 0, VPT, false, true>(z, S, t, io, tw);
 }
