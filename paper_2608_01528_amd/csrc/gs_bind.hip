@@ -250,7 +250,8 @@ __global__ void __launch_bounds__(BT) circular_kernel(BindArgs a) {
     const int64_t wpr = (a.nblocks + nbmax - 1) / nbmax;          // work-groups per row
     const int64_t row = (int64_t)blockIdx.x / wpr;
     const int64_t blk0 = ((int64_t)blockIdx.x - row * wpr) * nbmax;
-    const int nb = (int)((a.nblocks - blk0 < nbmax) ? (a.nblocks - blk0) : nbmax);
+    // blocks of 4096 values or more: one per work-group, known here
+    const int nb = (L >= SEG) ? 1 : (int)((a.nblocks - blk0 < nbmax) ? (a.nblocks - blk0) : nbmax);
     const int S = nb * L;                                        // <= VPT * BT
     const int t = threadIdx.x;
     f2v *z = smem;
