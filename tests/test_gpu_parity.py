@@ -1450,11 +1450,15 @@ def test_bind_circular(B, D, L, op, dt):
 @pytest.mark.parametrize("L", [1 << k for k in range(1, 14)])
 @pytest.mark.parametrize("op", ["conv", "corr"])
 @pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
-def test_bind_circular_every_block_length(L, op, dt):
+@pytest.mark.parametrize("split", ["full", "partial"])
+def test_bind_circular_every_block_length(L, op, dt, split):
     # the transform is compiled once per block length: every length from 2 to
-    # 8192, with a row split over two work-groups, the second holding fewer
-    # blocks (6144 values) where blocks are shorter than 4096
-    B, D = 3, (6144 if L <= 2048 else 8192)
+    # 8192, with rows of 8192 values (every work-group holding 4096 values)
+    # and, where blocks are shorter than 4096, rows of 6144 values (the
+    # second work-group of a row holding fewer blocks)
+    if split == "partial" and L > 2048:
+        pytest.skip("blocks of 4096 and more always take one work-group each")
+    B, D = 3, (6144 if split == "partial" else 8192)
     print("bind all L", op, L, D, dt, flush=True)
     rng = np.random.default_rng(1000 + L)
     X = rng.standard_normal((B, D)).astype(np.float32)
