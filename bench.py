@@ -110,6 +110,8 @@ def traffic_sources(kernel: str):
         return ["gs_abi.hip", "gs_gemm.hip", "gs_gemm256.hip", "gs_internal.h"]
     if "soft_" in kernel:
         return ["gs_abi.hip", "gs_internal.h", "gs_small.hip"]
+    if "circular_kernel" in kernel:
+        return ["gs_abi.hip", "gs_bind.hip", "gs_internal.h"]
     return None
 
 
@@ -985,7 +987,8 @@ def bind_workload(args, torch, gsm):
                                "and 256), xor, mul; value: circular convolution over whole rows"},
         "roofline": {"bound": "hbm", "kernel": "circular_kernel", "call": "gs_bind_restored (conv, L=4096)",
                      "achieved": per[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": per[dom]["frac"], "traffic": None, "bytes_per_launch": nbytes,
+                     "frac": per[dom]["frac"], "traffic": load_traffic("circular_kernel", "bind"),
+                     "bytes_per_launch": nbytes,
                      "avg_launch_us": per[dom]["us"]},
         "cpu_baseline": None,
         "extra": {"per_call": per, "kernel_source_hash": kernel_source_hash()},
