@@ -396,6 +396,27 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
                          void *X, gs_dtype xt, int64_t ldx, void *stream);
 
 /*
+ * gs_bind_coords -- binding of two coordinate batches through the original
+ * domain in one pass (Sec. 3.3: a component-wise operator runs after the
+ * restore and its result is projected back; Sec. 2.2 and Table 1:
+ * element-wise product):  Z = ((T Q) .* (T2 Q)) Q^T,  row by row
+ *   z_b = ((t_b Q) .* (t2_b Q)) Q^T.
+ * The restored and bound vectors stay on the chip: the call equals
+ * gs_reconstruct(T, Q, T2, GS_BIND_MUL) followed by gs_project of its result
+ * against Q, without the B x D intermediate.
+ *
+ *   T, T2  in   B x r, f32, ldt, ldt2 >= r; 1 <= r <= 256
+ *   Q      in   r x D, f32, ldq >= D
+ *   Z      out  B x r, f32, ldz >= r; overlaps none of the inputs
+ * fp32 accumulation; each sum over D runs in order over chunks of 32
+ * columns.  tt, qt and zt must be GS_F32 (GS_ERR_DTYPE otherwise); r above
+ * 256 gives GS_ERR_SHAPE (use the two calls).
+ */
+gs_status gs_bind_coords(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                         const void *T2, int64_t ldt2, const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
+                         void *Z, gs_dtype zt, int64_t ldz, void *stream);
+
+/*
  * gs_bind_restored -- binding and unbinding of restored vectors, row by row (Sec. 2.2:
  * the modulo-style component-wise operators run in the original domain,
  * after gs_reconstruct; Sec. 3.3: circular convolution).  For each row b:

@@ -572,6 +572,30 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
                                 (hipStream_t)stream), "gs_reconstruct");
 }
 
+gs_status gs_bind_coords(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
+                         const void *T2, int64_t ldt2, const void *Q, gs_dtype qt, int64_t D, int64_t ldq,
+                         void *Z, gs_dtype zt, int64_t ldz, void *stream) {
+    if (tt != GS_F32 || qt != GS_F32 || zt != GS_F32) return fail(GS_ERR_DTYPE, "gs_bind_coords: T, T2, Q and Z must be f32");
+    if (B < 0 || r < 1 || D < 1) return fail(GS_ERR_SHAPE, "gs_bind_coords: need B >= 0, r >= 1, D >= 1");
+    if (r > BIND_COORDS_MAX_R)
+        return fail(GS_ERR_SHAPE, "gs_bind_coords: r = %lld exceeds %lld", (long long)r, (long long)BIND_COORDS_MAX_R);
+    GS_CHECK(check_matrix(T, "T", B, r, ldt, tt, false));
+    GS_CHECK(check_matrix(T2, "T2", B, r, ldt2, tt, false));
+    GS_CHECK(check_matrix(Q, "Q", r, D, ldq, qt, false));
+    GS_CHECK(check_matrix(Z, "Z", B, r, ldz, zt, false));
+    GS_CHECK(check_overlaps({span(T, B, r, ldt, 4, "T"), span(T2, B, r, ldt2, 4, "T2"), span(Q, r, D, ldq, 4, "Q")},
+                            {span(Z, B, r, ldz, 4, "Z")}));
+    if (B == 0) return ok();
+    GS_CHECK(check_device());
+    BindCoordsArgs a{};
+    a.T = static_cast<const float *>(T); a.ldt = ldt;
+    a.T2 = static_cast<const float *>(T2); a.ldt2 = ldt2;
+    a.Q = static_cast<const float *>(Q); a.ldq = ldq;
+    a.Z = static_cast<float *>(Z); a.ldz = ldz;
+    a.B = B; a.r = r; a.D = D;
+    return launched(launch_bind_coords(a, (hipStream_t)stream), "gs_bind_coords");
+}
+
 gs_status gs_bind_restored(const void *X, gs_dtype xt, int64_t B, int64_t D, int64_t ldx,
                            const void *Y, int64_t ldy, gs_bind_op op, int64_t L,
                            void *Z, gs_dtype zt, int64_t ldz, void *stream) {

@@ -171,6 +171,18 @@ struct BindArgs {
 };
 hipError_t launch_bind(gs_dtype tin, gs_dtype tout, int op, const BindArgs &a, hipStream_t s);
 
+// Z = ((T Q) .* (T2 Q)) Q^T, fp32, r <= BIND_COORDS_MAX_R
+constexpr int64_t BIND_COORDS_MAX_R = 256;
+struct BindCoordsArgs {
+    const float *T; int64_t ldt;
+    const float *T2; int64_t ldt2;
+    const float *Q; int64_t ldq;
+    float *Z; int64_t ldz;
+    int64_t B, r, D;
+    int vec, qvec;      // 16-byte aligned rows of T and T2 / of Q (set by launch_bind_coords)
+};
+hipError_t launch_bind_coords(const BindCoordsArgs &a, hipStream_t s);
+
 // Small-codebook streaming kernels of the separate calls (r <= M <= SMALL_MAX)
 // and of the fused soft selection (r <= M <= SOFT_MAX_M).
 constexpr int SMALL_MAX = 64;

@@ -6,7 +6,7 @@ Two layers with the C names:
   pointers exactly as declared in the header.
 * `gs_compress`, `gs_compress_padded`, `gs_compress_partitioned`, `gs_compress_noalloc`, `gs_project`, `gs_prob2vec`, `gs_prob2vec_sparse`,
   `gs_similarity`,
-  `gs_attention`, `gs_similarity_attention`, `gs_reconstruct`, `gs_soft_select` and `gs_bind_restored`
+  `gs_attention`, `gs_similarity_attention`, `gs_reconstruct`, `gs_bind_coords`, `gs_soft_select` and `gs_bind_restored`
   below take torch tensors on the current
   GPU, allocate the outputs with torch, and pass pointers, sizes and the
   current stream to the library.  They only marshal arguments: every step of
@@ -96,6 +96,9 @@ _SIGS["gs_prob2vec_sparse"] = ([_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _i64, _
 _SIGS["gs_bind_restored"] = ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, ctypes.c_int, _i64,
                      _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
 
+_SIGS["gs_bind_coords"] = ([_vp, ctypes.c_int, _i64, _i64, _i64, _vp, _i64, _vp, ctypes.c_int, _i64, _i64,
+                           _vp, ctypes.c_int, _i64, _vp], ctypes.c_int)
+
 _SIGS["gs_soft_select"] = ([ctypes.POINTER(SoftGroup), ctypes.c_int, ctypes.c_int, ctypes.c_int,
                             ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_int, _vp], ctypes.c_int)
 
@@ -136,6 +139,21 @@ def _mat(t: torch.Tensor, name: str):
     if t.numel() == 0:
         return _DT[t.dtype], max(t.size(1), 1)
     return _DT[t.dtype], max(t.stride(0), t.size(1))
+
+
+def _shape(t, name: str, rows=None, cols=None):
+    """The library reads and writes the sizes it is given: an operand whose
+    shape disagrees with them would be read or written past its end."""
+    if t is None:
+        return
+    if t.dim() != 2 or (rows is not None and t.shape[0] != rows) or (cols is not None and t.shape[1] != cols):
+        raise ValueError("%s must be %s x %s, got %s" % (name, "?" if rows is None else rows,
+                                                         "?" if cols is None else cols, tuple(t.shape)))
+
+
+def _vec(t, name: str, n: int):
+    if t is not None and t.numel() < n:
+        raise ValueError("%s needs at least %d entries, has %d" % (name, n, t.numel()))
 
 
 def alloc_rows(rows: int, cols: int, dtype, device) -> torch.Tensor:
@@ -272,6 +290,10 @@ def gs_compress_noalloc(C: torch.Tensor, tol: float = 1e-10, q_dtype=torch.float
 def gs_project(X: torch.Tensor, Q: torch.Tensor, out_dtype=None, xnorm2: bool = False,
                out: torch.Tensor | None = None, xnorm2_out: torch.Tensor | None = None):
     """T = X Q^T (and ||x_b||^2 if xnorm2)."""
+    _shape(X, "X")
+    _shape(Q, "Q", cols=X.shape[1])
+    _shape(out, "out", X.shape[0], Q.shape[0])
+    _vec(xnorm2_out, "xnorm2_out", X.shape[0])
     xt, ldx = _mat(X, "X")
     qt, ldq = _mat(Q, "Q")
     B, D = X.shape
@@ -291,6 +313,9 @@ def gs_prob2vec(P: torch.Tensor, R: torch.Tensor, out_dtype=None, out: torch.Ten
                 echelon: bool = False):
     """T = P R: Gram-loc of sum_j P[b, j] c_j.  echelon: R is lower echelon
     (as gs_compress returns it), so its zero blocks may be skipped."""
+    _shape(P, "P")
+    _shape(R, "R", rows=P.shape[1])
+    _shape(out, "out", P.shape[0], R.shape[1])
     pt, ldp = _mat(P, "P")
     rt, ldr = _mat(R, "R")
     rt |= GS_ECHELON if echelon else 0
@@ -309,6 +334,10 @@ def gs_prob2vec_sparse(rowptr: torch.Tensor, cols: torch.Tensor, vals: torch.Ten
     cols (int32, nnz), vals (nnz, the type of R)."""
     if rowptr.dtype != torch.int64 or cols.dtype != torch.int32:
         raise ValueError("rowptr must be int64 and cols int32")
+    if vals.numel() != cols.numel():
+        raise ValueError("vals and cols must have the same length")
+    _shape(R, "R")
+    _shape(out, "out", rowptr.numel() - 1, R.shape[1])
     rt, ldr = _mat(R, "R")
     M, r = R.shape
     B = rowptr.numel() - 1
@@ -326,6 +355,12 @@ def gs_similarity(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mod
                   echelon: bool = False):
     """Scores S (B x M, fp32) and row argmax (int32) of T against R
     (echelon: as in gs_prob2vec)."""
+    _shape(T, "T")
+    _shape(R, "R", cols=T.shape[1])
+    _shape(out if scores else None, "out", T.shape[0], R.shape[0])
+    _vec(argmax_out if argmax else None, "argmax_out", T.shape[0])
+    _vec(qnorm2, "qnorm2", T.shape[0])
+    _vec(cnorm, "cnorm", R.shape[0])
     tt, ldt = _mat(T, "T")
     rt, ldr = _mat(R, "R")
     rt |= GS_ECHELON if echelon else 0
@@ -349,6 +384,12 @@ def gs_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm=None, mode
                  echelon: bool = False):
     """Attention weights A = softmax(beta * S) (B x M, fp32) and optionally the
     weighted sum O = A R (B x r) (echelon: as in gs_prob2vec)."""
+    _shape(T, "T")
+    _shape(R, "R", cols=T.shape[1])
+    _shape(out, "out", T.shape[0], R.shape[0])
+    _shape(o_out if weighted_sum else None, "o_out", T.shape[0], T.shape[1])
+    _vec(qnorm2, "qnorm2", T.shape[0])
+    _vec(cnorm, "cnorm", R.shape[0])
     tt, ldt = _mat(T, "T")
     rt, ldr = _mat(R, "R")
     rt |= GS_ECHELON if echelon else 0
@@ -374,6 +415,13 @@ def gs_similarity_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm
     """Scores S, row argmax and attention weights A = softmax(beta * S) from
     one evaluation of the scores; each of the three may be switched off
     (None is returned in its place)."""
+    _shape(T, "T")
+    _shape(R, "R", cols=T.shape[1])
+    _shape(out if scores else None, "out", T.shape[0], R.shape[0])
+    _shape(a_out if attention else None, "a_out", T.shape[0], R.shape[0])
+    _vec(argmax_out if argmax else None, "argmax_out", T.shape[0])
+    _vec(qnorm2, "qnorm2", T.shape[0])
+    _vec(cnorm, "cnorm", R.shape[0])
     tt, ldt = _mat(T, "T")
     rt, ldr = _mat(R, "R")
     rt |= GS_ECHELON if echelon else 0
@@ -397,6 +445,10 @@ def gs_similarity_attention(T: torch.Tensor, R: torch.Tensor, qnorm2=None, cnorm
 def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = None, bind=None,
                    out_dtype=None, out: torch.Tensor | None = None):
     """X = T Q, or (T Q) .* (T2 Q) with bind='mul'."""
+    _shape(T, "T")
+    _shape(Q, "Q", rows=T.shape[1])
+    _shape(T2, "T2", T.shape[0], T.shape[1])
+    _shape(out, "out", T.shape[0], Q.shape[1])
     tt, ldt = _mat(T, "T")
     qt, ldq = _mat(Q, "Q")
     B, r = T.shape
@@ -416,6 +468,25 @@ def gs_reconstruct(T: torch.Tensor, Q: torch.Tensor, T2: torch.Tensor | None = N
     return out
 
 
+def gs_bind_coords(T: torch.Tensor, T2: torch.Tensor, Q: torch.Tensor, out: torch.Tensor | None = None):
+    """Z = ((T Q) .* (T2 Q)) Q^T in one pass (fp32, r <= 256)."""
+    _shape(T, "T")
+    _shape(T2, "T2", T.shape[0], T.shape[1])
+    _shape(Q, "Q", rows=T.shape[1])
+    _shape(out, "out", T.shape[0], T.shape[1])
+    tt, ldt = _mat(T, "T")
+    _, ldt2 = _mat(T2, "T2")
+    qt, ldq = _mat(Q, "Q")
+    B, r = T.shape
+    D = Q.shape[1]
+    if out is None:
+        out = alloc_rows(B, r, T.dtype, T.device)
+    zt, ldz = _mat(out, "Z")
+    _check(lib().gs_bind_coords(_ptr(T), tt, B, r, ldt, _ptr(T2), ldt2, _ptr(Q), qt, D, ldq,
+                                _ptr(out), zt, ldz, _stream()))
+    return out
+
+
 _BINDOPS = {"mul": GS_BINDOP_MUL, "xor": GS_BINDOP_XOR, "conv": GS_BINDOP_CONV, "corr": GS_BINDOP_CORR}
 
 
@@ -424,6 +495,9 @@ def gs_bind_restored(X: torch.Tensor, Y: torch.Tensor, op: str = "conv", L: int 
     """Binding of restored vectors row by row: 'mul' (element-wise product),
     'xor' (binary vectors), 'conv' / 'corr' (blockwise circular convolution /
     correlation over blocks of L values, L = D by default)."""
+    _shape(X, "X")
+    _shape(Y, "Y", X.shape[0], X.shape[1])
+    _shape(out, "out", X.shape[0], X.shape[1])
     xt, ldx = _mat(X, "X")
     _, ldy = _mat(Y, "Y")
     B, D = X.shape

@@ -269,6 +269,51 @@ def test_similarity_attention_validation(L):
              NULL, 5, NULL, 2.0, NULL, 5, NULL) == gsm.GS_OK                          # empty batch
 
 
+def test_bind_coords_validation(L):
+    f = L.gs_bind_coords
+    # T (4 x 5), T2, Q (5 x 8), Z (4 x 5)
+    ok = [A1, gsm.GS_F32, 4, 5, 5, A2, 5, A3, gsm.GS_F32, 8, 8, A4, gsm.GS_F32, 5, NULL]
+    bad = list(ok); bad[1] = gsm.GS_BF16
+    assert f(*bad) == gsm.GS_ERR_DTYPE and "f32" in err(L)                            # bf16 T
+    bad = list(ok); bad[12] = gsm.GS_BF16
+    assert f(*bad) == gsm.GS_ERR_DTYPE                                                # bf16 Z
+    bad = list(ok); bad[3] = 257; bad[4] = 257; bad[6] = 257; bad[13] = 257
+    assert f(*bad) == gsm.GS_ERR_SHAPE and "256" in err(L)                            # r > 256
+    bad = list(ok); bad[4] = 4
+    assert f(*bad) == gsm.GS_ERR_SHAPE                                                # ldt < r
+    bad = list(ok); bad[10] = 7
+    assert f(*bad) == gsm.GS_ERR_SHAPE                                                # ldq < D
+    bad = list(ok); bad[11] = A1
+    assert f(*bad) == gsm.GS_ERR_ARG                                                  # Z aliases T
+    bad = list(ok); bad[5] = NULL
+    assert f(*bad) == gsm.GS_ERR_ARG                                                  # no T2
+    empty = list(ok); empty[0] = NULL; empty[2] = 0; empty[5] = NULL; empty[11] = NULL
+    assert f(*empty) == gsm.GS_OK                                                     # empty batch
+
+
+def test_wrappers_reject_mismatched_shapes():
+    # operands whose shapes disagree with the sizes the wrapper passes would
+    # be read or written past their ends: rejected before any call
+    f = lambda *s: torch.zeros(*s)
+    cases = [
+        lambda: gsm.gs_project(f(4, 8), f(3, 7)),                              # Q columns != D
+        lambda: gsm.gs_project(f(4, 8), f(3, 8), out=f(4, 2)),                 # out columns != r
+        lambda: gsm.gs_prob2vec(f(4, 5), f(6, 3)),                             # R rows != M
+        lambda: gsm.gs_similarity(f(4, 3), f(5, 2)),                           # R columns != r
+        lambda: gsm.gs_similarity(f(4, 3), f(5, 3), qnorm2=f(3)),              # qnorm2 too short
+        lambda: gsm.gs_attention(f(4, 3), f(5, 3), out=f(4, 4)),              # A columns != M
+        lambda: gsm.gs_similarity_attention(f(4, 3), f(5, 3), a_out=f(3, 5)),  # A rows != B
+        lambda: gsm.gs_reconstruct(f(4, 3), f(2, 8)),                          # Q rows != r
+        lambda: gsm.gs_reconstruct(f(4, 3), f(3, 8), T2=f(4, 2), bind="mul"),  # T2 shape
+        lambda: gsm.gs_bind_coords(f(4, 3), f(4, 3), f(2, 8)),                 # Q rows != r
+        lambda: gsm.gs_bind_coords(f(4, 3), f(5, 3), f(3, 8)),                 # T2 shape
+        lambda: gsm.gs_bind_restored(f(4, 8), f(4, 7)),                        # Y shape
+    ]
+    for c in cases:
+        with pytest.raises(ValueError, match="must be|needs at least"):
+            c()
+
+
 def test_errors_are_per_thread(L):
     import threading
     assert compress(L, ct=7) == gsm.GS_ERR_DTYPE

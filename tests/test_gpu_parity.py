@@ -516,6 +516,55 @@ def test_bind_and_reproject(kind):
     assert rowrel(host(Ty), oracle.project(Yo, Qo)) <= TOL_F32
 
 
+def _orthonormal_rows(r, D, seed):
+    q, _ = np.linalg.qr(np.random.default_rng(seed).standard_normal((D, r)))
+    return np.ascontiguousarray(q.T)
+
+
+@pytest.mark.parametrize("B,r,D", [(260, 150, 1100), (129, 256, 4096), (1, 1, 40), (300, 32, 64),
+                                   (257, 33, 1000), (128, 64, 2048), (5, 128, 160), (200, 100, 512)])
+def test_bind_coords(B, r, D):
+    # restore -> bind -> re-project in one pass against the oracle's three
+    # steps in fp64, and against the library's two calls; ragged batch row
+    # blocks (128 rows per work-group), ragged r (padded to 32, 64, 128 or
+    # 256) and ragged column chunks of 32
+    print("bind_coords", B, r, D, flush=True)
+    rng = np.random.default_rng(B + r + D)
+    Q = _orthonormal_rows(r, D, r + D).astype(np.float32)
+    T = rng.standard_normal((B, r)).astype(np.float32)
+    T2 = rng.standard_normal((B, r)).astype(np.float32)
+    Z = gsm.gs_bind_coords(dev(T), dev(T2), dev(Q))
+    X = gsm.gs_reconstruct(dev(T), dev(Q), T2=dev(T2), bind="mul")
+    Zc = gsm.gs_project(X, dev(Q))
+    torch.cuda.synchronize()
+    Zo = oracle.project(oracle.bind(oracle.reconstruct(T, Q), oracle.reconstruct(T2, Q)), Q)
+    assert rowrel(host(Z), Zo) <= TOL_F32
+    assert rowrel(host(Z), host(Zc)) <= TOL_F32
+
+
+def test_bind_coords_codebook_and_strides():
+    # coordinates of codebook rows (the binding of two entries, projected
+    # back), operands with leading dimensions that are not multiples of four
+    # (element loads), and an output with a leading dimension larger than r
+    C = rq_codebook("bipolar", 40, 1000, 17)
+    Qo, Ro, kept, r = oracle.compress(C)
+    ia, ib = np.arange(40), np.roll(np.arange(40), 7)
+    Ta = torch.zeros((40, r + 3), dtype=torch.float32, device="cuda")[:, :r]
+    Tb = torch.zeros((40, r + 1), dtype=torch.float32, device="cuda")[:, :r]
+    Ta.copy_(dev(Ro[ia]))
+    Tb.copy_(dev(Ro[ib]))
+    Qs = torch.zeros((r, 1003), dtype=torch.float32, device="cuda")[:, :1000]
+    Qs.copy_(dev(Qo))
+    out = torch.full((40, r + 9), float("nan"), device="cuda")
+    Z = gsm.gs_bind_coords(Ta, Tb, Qs, out=out[:, :r])
+    torch.cuda.synchronize()
+    Zo = oracle.project(oracle.bind(C[ia], C[ib]), Qo)
+    assert rowrel(host(Z), Zo) <= TOL_F32
+    assert torch.isnan(out[:, r:]).all()                 # nothing past column r is written
+    Z0 = gsm.gs_bind_coords(Ta[:0], Tb[:0], Qs)          # empty batch
+    assert Z0.shape == (0, r)
+
+
 def test_bipolar_self_binding_is_ones():
     C = rq_codebook("bipolar", 30, 512, 5)
     Qo, Ro, kept, r = oracle.compress(C)
