@@ -991,9 +991,56 @@ def bind_workload(args, torch, gsm):
                      "bytes_per_launch": nbytes,
                      "avg_launch_us": per[dom]["us"]},
         "cpu_baseline": None,
-        "extra": {"per_call": per, "kernel_source_hash": kernel_source_hash()},
+        "extra": {"per_call": per, "bind_coords": bind_coords_extra(torch, gsm, reps),
+                  "kernel_source_hash": kernel_source_hash()},
     }
     print(json.dumps(out), flush=True)
+
+
+def bind_coords_extra(torch, gsm, reps):
+    """Restore -> bind -> re-project of coordinate pairs, Z = ((T Q) .* (T2 Q)) Q^T:
+    gs_bind_coords (one pass, the bound vectors kept on chip) against the two
+    calls gs_reconstruct(bind='mul') + gs_project (B x D written and read
+    back), at the large workload's shape (65536 rows, D = 8192, fp32) for
+    r = 32 .. 256; mean device time of `reps` calls each (HIP events)."""
+    B, D = 65536, 8192
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    res = {}
+    stream = torch.cuda.current_stream()
+
+    def timed(f):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+    X = gsm.alloc_rows(B, D, torch.float32, "cuda")
+    for r in (32, 64, 128, 256):
+        q, _ = torch.linalg.qr(torch.randn((D, r), generator=g, device="cuda"))
+        Q = gsm.alloc_rows(r, D, torch.float32, "cuda")
+        Q.copy_(q.T)
+        T = gsm.alloc_rows(B, r, torch.float32, "cuda")
+        T2 = gsm.alloc_rows(B, r, torch.float32, "cuda")
+        T.copy_(torch.randn((B, r), generator=g, device="cuda"))
+        T2.copy_(torch.randn((B, r), generator=g, device="cuda"))
+        Z = gsm.alloc_rows(B, r, torch.float32, "cuda")
+        Zc = gsm.alloc_rows(B, r, torch.float32, "cuda")
+        fused = timed(lambda: gsm.gs_bind_coords(T, T2, Q, out=Z))
+        chain = timed(lambda: (gsm.gs_reconstruct(T, Q, T2=T2, bind="mul", out=X), gsm.gs_project(X, Q, out=Zc)))
+        diff = float(((Z - Zc).norm(dim=1) / Zc.norm(dim=1).clamp_min(1e-30)).max().item())
+        fl = 3 * 2.0 * B * D * r
+        res[str(r)] = {"fused_ms": fused, "two_calls_ms": chain, "speedup": chain / fused,
+                       "fused_TFLOPs": fl / fused / 1e9, "fused_frac_f32_peak": fl / fused / 1e9 / MFMA_PEAK["f32"],
+                       "max_rowrel_vs_two_calls": diff}
+        del Q, T, T2, Z, Zc
+    del X
+    torch.cuda.empty_cache()
+    return {"B": B, "D": D, "per_r": res}
 
 
 def main():

@@ -410,7 +410,10 @@ gs_status gs_reconstruct(const void *T, gs_dtype tt, int64_t B, int64_t r, int64
  *   Z      out  B x r, f32, ldz >= r; overlaps none of the inputs
  * fp32 accumulation; each sum over D runs in order over chunks of 32
  * columns.  tt, qt and zt must be GS_F32 (GS_ERR_DTYPE otherwise); r above
- * 256 gives GS_ERR_SHAPE (use the two calls).
+ * 256 gives GS_ERR_SHAPE (use the two calls).  The pass saves the B x D
+ * write and read of the two calls but holds 128 rows per work-group: it is
+ * the faster form for r up to 128 on batches that fill the GPU (at least
+ * 256 x 128 rows); at r = 256 the two calls run faster.
  */
 gs_status gs_bind_coords(const void *T, gs_dtype tt, int64_t B, int64_t r, int64_t ldt,
                          const void *T2, int64_t ldt2, const void *Q, gs_dtype qt, int64_t D, int64_t ldq,

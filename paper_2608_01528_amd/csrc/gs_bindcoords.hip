@@ -109,14 +109,16 @@ __global__ void __launch_bounds__(BC_THREADS, 2) bind_coords_kernel(BindCoordsAr
         for (int g = 0; g < 16; ++g) y[g] = y1[g] * y2[g];
         // (3) Z[row][n] += sum_d Y[row][d] Q[n][d0 + d]
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
+        for (int a4 = 0; a4 < 4; ++a4) {
+            f4v qv[NB];
 #pragma unroll
-            for (int a4 = 0; a4 < 4; ++a4) {
-                const f4v qv = *reinterpret_cast<const f4v *>(qn + (32 * b + ln) * Ly::QN + 8 * a4 + 4 * h);
+            for (int b = 0; b < NB; ++b)
+                qv[b] = *reinterpret_cast<const f4v *>(qn + (32 * b + ln) * Ly::QN + 8 * a4 + 4 * h);
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    z[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(y[4 * a4 + u], qv[u], z[b], 0, 0, 0);
-            }
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    z[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(y[4 * a4 + u], qv[b][u], z[b], 0, 0, 0);
         }
         __syncthreads();                  // every wave is done with this chunk
     }
