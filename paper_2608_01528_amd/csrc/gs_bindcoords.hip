@@ -59,9 +59,16 @@ __global__ void __launch_bounds__(BC_THREADS, 2) bind_coords_kernel(BindCoordsAr
 #pragma unroll
     for (int b = 0; b < NB; ++b) z[b] = f16v{};
 
-    for (int64_t d0 = 0; d0 < D; d0 += BC_DC) {
-        // stage Q[0..RB)[d0..d0+32) in both layouts
-        for (int i = tid; i < RB * (BC_DC / 4); i += BC_THREADS) {
+    // Q[0..RB)[d0..d0+32): this thread's RB / 32 pieces of four columns,
+    // read into registers (the next chunk's while the current one is
+    // multiplied, when they fit) and written to LDS in both layouts
+    constexpr int NP = RB * (BC_DC / 4) / BC_THREADS;
+    constexpr bool PREFETCH = RB <= 128;
+    f4v pre[NP];
+    auto fetch = [&](int64_t d0) {
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+            const int i = tid + j * BC_THREADS;
             const int k = i / (BC_DC / 4), d4 = 4 * (i % (BC_DC / 4));
             f4v v = f4v{0.f, 0.f, 0.f, 0.f};
             if (k < r) {
@@ -73,11 +80,34 @@ __global__ void __launch_bounds__(BC_THREADS, 2) bind_coords_kernel(BindCoordsAr
                     for (int e = 0; e < 4; ++e) v[e] = (d0 + d4 + e < D) ? q[e] : 0.f;
                 }
             }
-            *reinterpret_cast<f4v *>(qn + k * Ly::QN + d4) = v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) qd[(d4 + e) * Ly::QD + k] = v[e];
+            pre[j] = v;
         }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+            const int i = tid + j * BC_THREADS;
+            const int k = i / (BC_DC / 4), d4 = 4 * (i % (BC_DC / 4));
+            *reinterpret_cast<f4v *>(qn + k * Ly::QN + d4) = pre[j];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) qd[(d4 + e) * Ly::QD + k] = pre[j][e];
+        }
+    };
+    if (PREFETCH) {
+        fetch(0);
+        stage();
         __syncthreads();
+    }
+
+    for (int64_t d0 = 0; d0 < D; d0 += BC_DC) {
+        const bool more = d0 + BC_DC < D;
+        if (!PREFETCH) {
+            fetch(d0);
+            stage();
+            __syncthreads();
+        } else if (more) {
+            fetch(d0 + BC_DC);           // in flight during this chunk's products
+        }
 
         // (1) Y1^T and Y2^T: C[d][row] over k = 8t + 4h + u
         f16v y1 = f16v{}, y2 = f16v{};
@@ -121,6 +151,10 @@ __global__ void __launch_bounds__(BC_THREADS, 2) bind_coords_kernel(BindCoordsAr
                     z[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(y[4 * a4 + u], qv[b][u], z[b], 0, 0, 0);
         }
         __syncthreads();                  // every wave is done with this chunk
+        if (PREFETCH && more) {
+            stage();
+            __syncthreads();
+        }
     }
 
     // register g of block b holds Z[row0 + 8 (g / 4) + 4 h + g % 4][32 b + ln]
