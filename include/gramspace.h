@@ -38,7 +38,13 @@
  * Streams.  `stream` is a hipStream_t passed as void* (NULL = null stream).
  * Every call except gs_compress only enqueues work on that stream and returns
  * without waiting.  gs_compress synchronises the stream before returning
- * because the rank is returned in host memory.
+ * because the rank is returned in host memory.  The allocating compress
+ * calls (gs_compress, gs_compress_partitioned, gs_compress_padded) also run
+ * part of their work on a second stream of the library's (one per GPU,
+ * non-blocking, default priority, created on the first such call on that
+ * GPU and kept until the process ends), forked from and joined back into
+ * `stream` by events within the call; gs_compress_noalloc runs everything on
+ * `stream` and gives the same results bit for bit.
  *
  * Element types.  GS_F32 and GS_BF16 (bfloat16 storage, fp32 arithmetic) for
  * batch data and coordinates; GS_F64 additionally for compress input/outputs.
@@ -148,7 +154,8 @@ size_t gs_compress_workspace(int64_t M, int64_t D);
  *   rank   out  HOST int32
  *   ws          device workspace of >= gs_compress_workspace(M, D) bytes,
  *               256-byte aligned; contents on return are unspecified
- *   stream      synchronised before return
+ *   stream      synchronised before return (part of the work runs on the
+ *               library's second stream, joined back before return)
  * Errors: GS_ERR_NUMERIC if C holds a NaN or infinity (detected on the device;
  * outputs are then undefined), or if the re-orthonormalisation of a panel
  * meets a Gram matrix that is not positive definite (not expected for finite
@@ -240,7 +247,8 @@ gs_status gs_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t
  * workspace, which comes instead from a static array of
  * GS_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
  * (from the first call on that device until the process ends).  The call
- * allocates nothing.  Codebooks whose workspace, gs_compress_workspace(M, D),
+ * allocates nothing and creates no stream or event: its work runs on `stream`
+ * alone.  Codebooks whose workspace, gs_compress_workspace(M, D),
  * exceeds the array are rejected with GS_ERR_WORKSPACE (64 MiB: e.g. up to
  * 1000 x 4096 or 256 x 8192 in fp64 working precision).  All calls on one GPU
  * share its array: calls that overlap in time on the same GPU (other threads,

@@ -202,6 +202,51 @@ gs_status scratch_for_current_device(void **out) {
     return GS_OK;
 }
 
+// The second stream of the allocating compression calls: one per GPU,
+// created on first use with that device current and kept until the process
+// ends, shared by every call on the GPU (its work is ordered against each
+// call's own stream by that call's events).  gs_compress_noalloc does not use
+// it: creating a stream or an event can allocate.
+std::mutex g_aux_mu;
+hipStream_t g_aux_stream[kMaxDevices] = {};
+bool g_aux_made[kMaxDevices] = {};
+
+class OverlapScope {
+public:
+    // Sets up ov for the current device; a failure is reported as an error.
+    gs_status open(const char *fn) {
+        int dev = -1;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: hipGetDevice: %s", fn, hipGetErrorString(e));
+        if (dev < 0 || dev >= kMaxDevices)
+            return fail(GS_ERR_DEVICE, "%s: device %d beyond the %d supported", fn, dev, kMaxDevices);
+        {
+            std::lock_guard<std::mutex> lock(g_aux_mu);
+            if (!g_aux_made[dev]) {
+                hipStream_t st = nullptr;
+                e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+                if (e != hipSuccess)
+                    return fail(GS_ERR_DEVICE, "%s: hipStreamCreateWithFlags: %s", fn, hipGetErrorString(e));
+                g_aux_stream[dev] = st;
+                g_aux_made[dev] = true;
+            }
+            ov_.aux = g_aux_stream[dev];
+        }
+        e = hipEventCreateWithFlags(&ov_.fork, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ov_.join, hipEventDisableTiming);
+        if (e != hipSuccess) return fail(GS_ERR_DEVICE, "%s: hipEventCreateWithFlags: %s", fn, hipGetErrorString(e));
+        return GS_OK;
+    }
+    const gs::CompressOverlap *get() const { return &ov_; }
+    ~OverlapScope() {
+        if (ov_.fork) (void)hipEventDestroy(ov_.fork);
+        if (ov_.join) (void)hipEventDestroy(ov_.join);
+    }
+
+private:
+    gs::CompressOverlap ov_{nullptr, nullptr, nullptr};
+};
+
 }  // namespace
 
 extern "C" {
@@ -226,10 +271,12 @@ gs_status gs_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t 
                                        span(cnorm, 1, M, M, 4, "cnorm")}));
     }
     GS_CHECK(check_device());
+    OverlapScope ovs;
+    GS_CHECK(ovs.open("gs_compress"));
     int nonfinite = 0;
     int32_t r = 0;
     hipError_t e = run_compress(C, ct, M, D, ldc, tol, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
-                                &nonfinite, ws, (hipStream_t)stream);
+                                &nonfinite, ws, (hipStream_t)stream, 0, ovs.get());
     return finish_compress("gs_compress", e, nonfinite, r, rank);
 }
 
@@ -267,10 +314,12 @@ gs_status gs_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t
                                        span(cnorm, 1, M, M, 4, "cnorm")}));
     }
     GS_CHECK(check_device());
+    OverlapScope ovs;
+    GS_CHECK(ovs.open(fn));
     int nonfinite = 0;
     int32_t total = 0;
     hipError_t e = run_compress_partitioned(C, ct, M, D, ldc, tol, subset, Q, qt, ldq, R, rt, ldr, kept, cnorm,
-                                            ranks, &total, &nonfinite, ws, (hipStream_t)stream);
+                                            ranks, &total, &nonfinite, ws, (hipStream_t)stream, ovs.get());
     return finish_compress(fn, e, nonfinite, total, rank);
 }
 
@@ -313,10 +362,12 @@ gs_status gs_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, i
                                        span(kept, 1, M, M, 4, "kept"), span(cnorm, 1, M, M, 4, "cnorm")}));
     }
     GS_CHECK(check_device());
+    OverlapScope ovs;
+    GS_CHECK(ovs.open(fn));
     int nonfinite = 0;
     int32_t r = 0;
     hipError_t e = run_compress_padded(C, ct, M, D, ldc, tol, k, H, ldh, Q, qt, ldq, R, rt, ldr, kept, cnorm, &r,
-                                       &nonfinite, ws, (hipStream_t)stream);
+                                       &nonfinite, ws, (hipStream_t)stream, ovs.get());
     return finish_compress(fn, e, nonfinite, r, rank);
 }
 

@@ -7,7 +7,13 @@
 // order.  For each panel W (pb x D):
 //
 //  1. first pass against the basis Q built from earlier panels (r_old rows):
-//     H1 = W Q^T (its coefficients, into R), W -= H1 Q;
+//     H1 = W Q^T (its coefficients, into R), W -= H1 Q, in two parts: first
+//     against the vectors of the panels before the previous one, then
+//     against the previous panel's (block modified Gram-Schmidt over the two
+//     parts).  The first part needs nothing of the previous panel, so it
+//     runs while that panel is factored (on a second stream when one is
+//     given, otherwise before it on the same stream; the results are the
+//     same bit for bit);
 //  2. the rows of the panel are orthogonalised among themselves in the small
 //     space of the panel's triangular factor: W^T = Q_t R_t by a tree of
 //     Householder factorisations (TSQR), so the columns a_i of R_t have the
@@ -43,6 +49,7 @@ constexpr int NT = 256;       // threads of the panel kernels
 constexpr int TCH = 256;      // rows of a TSQR node: panel columns of a leaf, or 8 stacked factors
 constexpr int TFAN = TCH / PB;
 constexpr int BK = 512;       // D-chunk of the split products W Q^T
+constexpr int BK_PREV = 128;  // D-chunk of the product with the previous panel's vectors (short: two K-steps)
 constexpr int KS = 64;        // K-step staged in LDS by the matrix-core products
 constexpr int BN = 64;        // basis vectors (dots) or columns (update) per work-group
 constexpr int LDK = KS + 1;   // LDS row stride (odd in doubles)
@@ -51,7 +58,9 @@ typedef double d4 __attribute__((ext_vector_type(4)));
 
 // Row-count sources of the panel kernels: the panel's rows, the basis rows
 // built before the panel, or the new basis vectors of the panel.
-enum Rows { ROWS_PANEL = 0, ROWS_OLD = 1, ROWS_NEW = 2, ROWS_OLD_PASS2 = 3 };
+// The earlier basis splits for the first pass: ROWS_OLD_A, the vectors of
+// the panels before the previous one; ROWS_OLD_B, the previous panel's.
+enum Rows { ROWS_PANEL = 0, ROWS_OLD = 1, ROWS_NEW = 2, ROWS_OLD_PASS2 = 3, ROWS_OLD_A = 4, ROWS_OLD_B = 5 };
 
 // Second pass against the earlier basis: needed only where the first pass
 // can have left the new vectors measurably off orthogonal to it.  A new
@@ -63,13 +72,14 @@ enum Rows { ROWS_PANEL = 0, ROWS_OLD = 1, ROWS_NEW = 2, ROWS_OLD_PASS2 = 3 };
 constexpr double PASS2_WEIGHT = 8.0;
 
 struct WsLayout {
-    size_t qm, wp, w2, hc, h2, g2, part, gpart, tsq0, tsq1, x1, c1, lx, cn, rank_after, kept, flag, pass2, total;
+    size_t qm, wp, wp_next, w2, hc, h2, g2, part, part_next, part_prev, gpart, tsq0, tsq1, x1, c1, lx, cn,
+        rank_after, kept, flag, pass2, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int64_t leaf_count(int64_t D) { return (D + TCH - 1) / TCH; }
-int64_t chunk_count(int64_t D) { return (D + BK - 1) / BK; }
+int64_t chunk_count(int64_t D, int64_t bk = BK) { return (D + bk - 1) / bk; }
 
 WsLayout layout(int64_t M, int64_t D) {
     WsLayout L;
@@ -77,11 +87,14 @@ WsLayout layout(int64_t M, int64_t D) {
     size_t o = 0;
     L.qm = o;    o = align256(o + sizeof(double) * M * D);
     L.wp = o;    o = align256(o + sizeof(double) * PB * D);
+    L.wp_next = o; o = align256(o + sizeof(double) * PB * D);
     L.w2 = o;    o = align256(o + sizeof(double) * PB * D);
     L.hc = o;    o = align256(o + sizeof(double) * M * M);
     L.h2 = o;    o = align256(o + sizeof(double) * PB * M);
     L.g2 = o;    o = align256(o + sizeof(double) * PB * PB);
     L.part = o;  o = align256(o + sizeof(double) * nch * PB * (M > PB ? M : PB));
+    L.part_next = o; o = align256(o + sizeof(double) * nch * PB * (M > PB ? M : PB));
+    L.part_prev = o; o = align256(o + sizeof(double) * chunk_count(D, BK_PREV) * PB * PB);
     L.gpart = o; o = align256(o + sizeof(double) * ((D + BN - 1) / BN) * PB * PB);
     L.tsq0 = o;  o = align256(o + sizeof(double) * nl * PB * PB);
     L.tsq1 = o;  o = align256(o + sizeof(double) * nl * PB * PB);
@@ -109,12 +122,24 @@ __device__ __forceinline__ int rank_before(const int32_t *rank_after, int64_t ro
     return row == 0 ? 0 : rank_after[row - 1];
 }
 
+// Rank before the previous panel (0 for the first two panels).
+__device__ __forceinline__ int rank_before_prev(const Panel &p) {
+    return p.i0 >= PB ? rank_before(p.rank_after, p.i0 - PB) : 0;
+}
+
 __device__ __forceinline__ int rows_of(const Panel &p, int which) {
     const int r_old = rank_before(p.rank_after, p.i0);
     if (which == ROWS_PANEL) return p.pb;
     if (which == ROWS_OLD) return r_old;
     if (which == ROWS_OLD_PASS2) return *p.pass2 ? r_old : 0;
+    if (which == ROWS_OLD_A) return rank_before_prev(p);
+    if (which == ROWS_OLD_B) return r_old - rank_before_prev(p);
     return p.rank_after[p.i0 + p.pb - 1] - r_old;   // ROWS_NEW: valid after the panel's rank decisions
+}
+
+// First basis row of a set of basis rows (ROWS_OLD_B starts past ROWS_OLD_A).
+__device__ __forceinline__ int rows_first(const Panel &p, int which) {
+    return which == ROWS_OLD_B ? rank_before_prev(p) : 0;
 }
 
 template <typename T> __device__ __forceinline__ double ld_f64(const T *p, int64_t i);
@@ -146,6 +171,11 @@ __device__ __forceinline__ double dpp_f64(double v) {
     const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xf, 0xf, false);
     return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
+
+// The panel factorisation and the small-space steps are chains of dependent
+// steps on a few work-groups, and the next panel's products may share their
+// CUs; their waves take instruction-issue precedence over those.
+__device__ __forceinline__ void raise_wave_priority() { __builtin_amdgcn_s_setprio(3); }
 
 __global__ void k_init(double *hc, int64_t nhc, int32_t *kept, int32_t *rank_after, int64_t M,
                        int32_t *flag) {
@@ -193,17 +223,19 @@ __global__ void __launch_bounds__(NT) k_load_panel(const T *C, int64_t ldc, int6
 // 0..15 and 16..31).  For v_mfma_f64_16x16x4f64, lane l supplies A[l % 16][l / 16]
 // and B[l / 16][l % 16], and holds D[l / 16 + 4 j][l % 16] in element j.
 
-// part[c][i][kb + n] = sum over the c-th D-chunk of S[i][d] * Qb[kb + n][d]
-// (i < rows(sw), kb + n < rows(qw)).  Grid: (basis blocks of 64, D-chunks).
+// part[c][i][kb + n] = sum over the c-th D-chunk (bk columns, a multiple of
+// KS) of S[i][d] * Qb[kb + n][d] (i < rows(sw), kb + n < rows(qw)).  Grid:
+// (basis blocks of 64, D-chunks).
 __global__ void __launch_bounds__(NT) k_bdots(const double *S, int sw, const double *Qb, int qw, int64_t D,
-                                              Panel p, double *part, int64_t ldp) {
+                                              int64_t bk, Panel p, double *part, int64_t ldp) {
     __shared__ double Ss[PB * LDK];
     __shared__ double Qs[BN * LDK];
     const int ns = rows_of(p, sw), nq = rows_of(p, qw);
     const int kb = blockIdx.x * BN;
     if (kb >= nq || ns == 0) return;
+    Qb += (int64_t)rows_first(p, qw) * D;
     const int64_t c = blockIdx.y;
-    const int64_t d_lo = c * BK, d_hi = (d_lo + BK < D) ? d_lo + BK : D;
+    const int64_t d_lo = c * bk, d_hi = (d_lo + bk < D) ? d_lo + bk : D;
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     // staging: element u of a thread is row (t + 256 u) / 64, column t % 64,
     // so the 64 lanes of a wave read 64 consecutive doubles of one row
@@ -262,25 +294,38 @@ __global__ void __launch_bounds__(NT) k_bdots(const double *S, int sw, const dou
     }
 }
 
-// out[i][k] (leading dimension ldo) = sum over the chunks c (in order) of
-// part[c][i][k], for i < rows(sw), k < rows(qw).
-__global__ void k_breduce(const double *part, int64_t nch, int64_t ldp, int sw, int qw, Panel p,
-                          double *out, int64_t ldo) {
-    const int ns = rows_of(p, sw), nq = rows_of(p, qw);
-    const int64_t e = (int64_t)blockIdx.x * NT + threadIdx.x;
-    const int i = (int)(e / ldp), k = (int)(e % ldp);
-    if (i >= ns || k >= nq) return;
-    // four running sums (chunks c = 4 m + j), added in a fixed order
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+// Sum of the n values p[0], p[st], ..., p[(n - 1) st] in a fixed order:
+// eight running sums (terms 8 m + j, in order of m), so that eight loads are
+// in flight at a time, added pairwise.
+__device__ __forceinline__ double strided_sum(const double *p, int64_t n, int64_t st) {
+    double s[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
     int64_t c = 0;
-    for (; c + 4 <= nch; c += 4) {
-        s0 += part[((c + 0) * PB + i) * ldp + k];
-        s1 += part[((c + 1) * PB + i) * ldp + k];
-        s2 += part[((c + 2) * PB + i) * ldp + k];
-        s3 += part[((c + 3) * PB + i) * ldp + k];
+    for (; c + 8 <= n; c += 8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) s[j] += p[(c + j) * st];
     }
-    for (; c < nch; ++c) s0 += part[(c * PB + i) * ldp + k];
-    out[(int64_t)i * ldo + k] = (s0 + s1) + (s2 + s3);
+    for (int j = 0; c < n; ++c, ++j) s[j] += p[c * st];
+    return ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
+}
+
+// out[i][k] (leading dimension ldo) = sum over the chunks c of part[c][i][k],
+// for i < rows(sw), k < rows(qw).  A work-group of 256 threads for 64
+// entries, each quarter of the threads summing a quarter of the chunks,
+// quarters added in order.
+__global__ void __launch_bounds__(NT) k_breduce(const double *part, int64_t nch, int64_t ldp, int sw, int qw,
+                                                Panel p, double *out, int64_t ldo) {
+    __shared__ double red[4][64];
+    const int ns = rows_of(p, sw), nq = rows_of(p, qw);
+    const int t = threadIdx.x, qt = t >> 6;
+    const int64_t e = (int64_t)blockIdx.x * 64 + (t & 63);
+    const int i = (int)(e / ldp), k = (int)(e % ldp);
+    const bool live = i < ns && k < nq;
+    if (blockIdx.x * (int64_t)64 >= (int64_t)ns * ldp) return;     // the whole group is past the rows
+    const int64_t c0 = nch * qt / 4, c1 = nch * (qt + 1) / 4;
+    red[qt][t & 63] = live ? strided_sum(part + (c0 * PB + i) * ldp + k, c1 - c0, (int64_t)PB * ldp) : 0.0;
+    __syncthreads();
+    if (qt == 0 && live)
+        out[rows_first(p, qw) + (int64_t)i * ldo + k] = (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
 }
 
 // G[i][j] = sum over the column blocks b (in a fixed order) of
@@ -290,14 +335,7 @@ __global__ void __launch_bounds__(NT) k_gram_reduce(const double *gpart, int64_t
     __shared__ double red[4][64];
     const int t = threadIdx.x, e = blockIdx.x * 64 + (t & 63), qt = t >> 6;
     const int64_t b0 = nblk * qt / 4, b1 = nblk * (qt + 1) / 4;
-    double s0 = 0.0, s1 = 0.0;
-    int64_t b = b0;
-    for (; b + 2 <= b1; b += 2) {
-        s0 += gpart[b * PB * PB + e];
-        s1 += gpart[(b + 1) * PB * PB + e];
-    }
-    if (b < b1) s0 += gpart[b * PB * PB + e];
-    red[qt][t & 63] = s0 + s1;
+    red[qt][t & 63] = strided_sum(gpart + b0 * PB * PB + e, b1 - b0, (int64_t)PB * PB);
     __syncthreads();
     if (qt == 0) G[e] = (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
 }
@@ -312,6 +350,9 @@ __global__ void __launch_bounds__(NT) k_bupdate(double *S, int sw, const double 
     __shared__ double Qs[KS * LDK];
     const int ns = rows_of(p, sw), nq = rows_of(p, qw);
     if (ns == 0 || (nq == 0 && !gpart)) return;
+    const int q0 = rows_first(p, qw);
+    H += q0;
+    Qb += (int64_t)q0 * D;
     const int64_t d0 = (int64_t)blockIdx.x * BN;
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
     // staging: element u of a thread is row (t + 256 u) / 64, column t % 64
@@ -441,6 +482,7 @@ __global__ void __launch_bounds__(TSQR_NT) k_tsqr(const double *S, int sw, int64
                                                   int64_t nin, double *Rout, Panel p) {
     __shared__ __attribute__((aligned(16))) double vbuf[2][VST * TG];
     __shared__ double coefs[2][2];
+    raise_wave_priority();
     const int t = threadIdx.x;
     const int k = t / TG, g = t % TG;
     const int64_t c = blockIdx.x;
@@ -576,6 +618,7 @@ __global__ void __launch_bounds__(64) k_small_rank(const double *Rt, const doubl
     __shared__ int kidx[PB];                                     // kept index of each row (-1: dependent)
     __shared__ int krow[PB];                                     // row that made each kept vector
     __shared__ double rinv[PB];                                  // 1 / pivot of each kept vector
+    raise_wave_priority();
     const int l = threadIdx.x;
     const bool act = l < PB;
     const bool row_l = l < p.pb;       // lane l is a row of this panel
@@ -738,6 +781,7 @@ __global__ void __launch_bounds__(64) k_small_chol(const double *G, Panel p, dou
     __shared__ double L[PB][PB + 1];
     __shared__ __attribute__((aligned(16))) double zb[PB];
     __shared__ double rd[PB];          // 1 / L[j][j]
+    raise_wave_priority();
     const int l = threadIdx.x;
     const bool act = l < PB;
     const int n = rows_of(p, ROWS_NEW);
@@ -903,15 +947,17 @@ hipError_t launch_norms(const void *C, int64_t ldc, int64_t M, int64_t D, double
 
 #define GS_TRY(x) do { hipError_t e_ = (x); if (e_ != hipSuccess) return e_; } while (0)
 
-// One pass of the block projection: H = S Qb^T (split over D-chunks, reduced
-// in order into out, leading dimension ldo), then S -= H Qb (with gpart, also
-// the column blocks' shares of the Gram matrix of the updated S).
-hipError_t block_pass(double *S, int sw, const double *Qb, int qw, int64_t max_q, int64_t D, const Panel &p,
-                      double *part, int64_t ldp, double *out, int64_t ldo, double *gpart, hipStream_t s) {
-    const int64_t nch = chunk_count(D);
+// One pass of the block projection: H = S Qb^T (split over D-chunks of bk
+// columns, reduced in a fixed order into out, leading dimension ldo), then
+// S -= H Qb (with gpart, also the column blocks' shares of the Gram matrix
+// of the updated S).  part holds chunk_count(D, bk) x PB x ldp partial sums.
+hipError_t block_pass(double *S, int sw, const double *Qb, int qw, int64_t max_q, int64_t D, int64_t bk,
+                      const Panel &p, double *part, int64_t ldp, double *out, int64_t ldo, double *gpart,
+                      hipStream_t s) {
+    const int64_t nch = chunk_count(D, bk);
     const dim3 gd((unsigned)((max_q + BN - 1) / BN), (unsigned)nch);
-    hipLaunchKernelGGL(k_bdots, gd, dim3(NT), 0, s, (const double *)S, sw, Qb, qw, D, p, part, ldp);
-    const unsigned gr = (unsigned)((PB * ldp + NT - 1) / NT);
+    hipLaunchKernelGGL(k_bdots, gd, dim3(NT), 0, s, (const double *)S, sw, Qb, qw, D, bk, p, part, ldp);
+    const unsigned gr = (unsigned)((PB * ldp + 63) / 64);
     hipLaunchKernelGGL(k_breduce, dim3(gr), dim3(NT), 0, s, (const double *)part, nch, ldp, sw, qw, p, out, ldo);
     if (!gpart) {
         hipLaunchKernelGGL(k_bupdate, dim3((unsigned)((D + BN - 1) / BN)), dim3(NT), 0, s, S, sw,
@@ -949,12 +995,15 @@ size_t compress_workspace(int64_t M, int64_t D) { return layout(M, D).total; }
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                         void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                         int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite, void *ws_,
-                        hipStream_t s, int64_t row_base) {
+                        hipStream_t s, int64_t row_base, const CompressOverlap *ov) {
     const WsLayout L = layout(M, D);
     char *ws = static_cast<char *>(ws_);
-    double *qm = (double *)(ws + L.qm), *wp = (double *)(ws + L.wp), *w2 = (double *)(ws + L.w2);
+    double *qm = (double *)(ws + L.qm), *w2 = (double *)(ws + L.w2);
+    double *wbuf[2] = {(double *)(ws + L.wp), (double *)(ws + L.wp_next)};
     double *hc = (double *)(ws + L.hc), *h2 = (double *)(ws + L.h2), *g2 = (double *)(ws + L.g2);
-    double *part = (double *)(ws + L.part), *tsq0 = (double *)(ws + L.tsq0), *tsq1 = (double *)(ws + L.tsq1);
+    double *part = (double *)(ws + L.part), *part_next = (double *)(ws + L.part_next);
+    double *part_prev = (double *)(ws + L.part_prev);
+    double *tsq0 = (double *)(ws + L.tsq0), *tsq1 = (double *)(ws + L.tsq1);
     double *gpart = (double *)(ws + L.gpart);
     const int64_t nblk = (D + BN - 1) / BN;
     double *x1 = (double *)(ws + L.x1), *c1 = (double *)(ws + L.c1), *lx = (double *)(ws + L.lx);
@@ -962,22 +1011,55 @@ hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_
     int32_t *rank_after = (int32_t *)(ws + L.rank_after), *kept_ws = (int32_t *)(ws + L.kept);
     int32_t *flag = (int32_t *)(ws + L.flag), *pass2 = (int32_t *)(ws + L.pass2);
     const int64_t ldp = M > PB ? M : PB;
+    const int64_t npanels = (M + PB - 1) / PB;
+    auto panel = [&](int64_t q) {
+        const int64_t i0 = q * PB;
+        return Panel{i0, (int)((M - i0 < PB) ? (M - i0) : PB), rank_after, pass2};
+    };
+    // Panel q's rows into its buffer, and the first part of its first pass:
+    // against the vectors of the panels before q - 1 (coefficients into R).
+    // Reads only what panels up to q - 2 produced.
+    auto stage = [&](int64_t q, hipStream_t st) -> hipError_t {
+        const Panel pn = panel(q);
+        double *w = wbuf[q & 1];
+        if (ct == GS_F32) GS_TRY(launch_load<float>(C, ldc, D, pn.i0, pn.pb, w, st));
+        else if (ct == GS_F64) GS_TRY(launch_load<double>(C, ldc, D, pn.i0, pn.pb, w, st));
+        else GS_TRY(launch_load<bf16_t>(C, ldc, D, pn.i0, pn.pb, w, st));
+        if (pn.i0 >= 2 * PB)
+            GS_TRY(block_pass(w, ROWS_PANEL, qm, ROWS_OLD_A, pn.i0 - PB, D, BK, pn, part_next, ldp, hc + pn.i0 * M,
+                              M, nullptr, st));
+        return hipSuccess;
+    };
 
     hipLaunchKernelGGL(k_init, dim3(1024), dim3(NT), 0, s, hc, M * M, kept_ws, rank_after, M, flag);
     GS_TRY(hipGetLastError());
     if (ct == GS_F32) GS_TRY(launch_norms<float>(C, ldc, M, D, cn, flag, s));
     else if (ct == GS_F64) GS_TRY(launch_norms<double>(C, ldc, M, D, cn, flag, s));
     else GS_TRY(launch_norms<bf16_t>(C, ldc, M, D, cn, flag, s));
+    GS_TRY(stage(0, s));
 
-    for (int64_t i0 = 0; i0 < M; i0 += PB) {
-        const int pb = (int)((M - i0 < PB) ? (M - i0) : PB);
-        const Panel p{i0, pb, rank_after, pass2};
-        if (ct == GS_F32) GS_TRY(launch_load<float>(C, ldc, D, i0, pb, wp, s));
-        else if (ct == GS_F64) GS_TRY(launch_load<double>(C, ldc, D, i0, pb, wp, s));
-        else GS_TRY(launch_load<bf16_t>(C, ldc, D, i0, pb, wp, s));
-        // 1. first pass against the earlier basis; its coefficients go to R
-        if (i0 > 0)
-            GS_TRY(block_pass(wp, ROWS_PANEL, qm, ROWS_OLD, i0, D, p, part, ldp, hc + i0 * M, M, nullptr, s));
+    for (int64_t q = 0; q < npanels; ++q) {
+        const Panel p = panel(q);
+        const int64_t i0 = p.i0;
+        double *wp = wbuf[q & 1];
+        // 1. the rest of the first pass: against the previous panel's vectors
+        if (q > 0) {
+            if (ov) GS_TRY(hipStreamWaitEvent(s, ov->join, 0));
+            GS_TRY(block_pass(wp, ROWS_PANEL, qm, ROWS_OLD_B, PB, D, BK_PREV, p, part_prev, PB, hc + i0 * M, M,
+                              nullptr, s));
+        }
+        // the next panel's rows and the first part of its first pass, beside
+        // this panel's factorisation (they touch none of its buffers)
+        if (q + 1 < npanels) {
+            if (ov) {
+                GS_TRY(hipEventRecord(ov->fork, s));
+                GS_TRY(hipStreamWaitEvent(ov->aux, ov->fork, 0));
+                GS_TRY(stage(q + 1, ov->aux));
+                GS_TRY(hipEventRecord(ov->join, ov->aux));
+            } else {
+                GS_TRY(stage(q + 1, s));
+            }
+        }
         // 2. rank decisions in the panel's small space; first-round new vectors
         double *rt_ = nullptr;
         GS_TRY(panel_factor(wp, ROWS_PANEL, D, p, tsq0, tsq1, &rt_, s));
@@ -989,7 +1071,7 @@ hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_
         // 3. second pass on the new vectors, with their Gram matrix, and its
         // Cholesky factor
         if (i0 > 0) {
-            GS_TRY(block_pass(w2, ROWS_NEW, qm, ROWS_OLD_PASS2, i0, D, p, part, ldp, h2, M, gpart, s));
+            GS_TRY(block_pass(w2, ROWS_NEW, qm, ROWS_OLD_PASS2, i0, D, BK, p, part, ldp, h2, M, gpart, s));
         } else {
             hipLaunchKernelGGL(k_bupdate, dim3((unsigned)nblk), dim3(NT), 0, s, w2, (int)ROWS_NEW,
                                (const double *)h2, M, (const double *)qm, (int)ROWS_OLD, D, p, gpart);
@@ -1002,7 +1084,7 @@ hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_
                            (const double *)(lx + PB * PB), (int)ROWS_NEW, (const double *)w2, (int)ROWS_NEW,
                            qm, true, D, p);
         GS_TRY(hipGetLastError());
-        hipLaunchKernelGGL(k_coef, dim3((unsigned)((i0 + PB + NT - 1) / NT), (unsigned)pb), dim3(NT), 0, s,
+        hipLaunchKernelGGL(k_coef, dim3((unsigned)((i0 + PB + NT - 1) / NT), (unsigned)p.pb), dim3(NT), 0, s,
                            (const double *)c1,
                            (const double *)h2, M, i0 > 0, (const double *)lx, hc, M, p);
         GS_TRY(hipGetLastError());
@@ -1128,7 +1210,7 @@ size_t compress_padded_workspace(int64_t M, int64_t D, int64_t k) { return pad_l
 hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                                int64_t k, const double *H, int64_t ldh, void *Q, gs_dtype qt, int64_t ldq,
                                void *R, gs_dtype rt, int64_t ldr, int32_t *kept, float *cnorm, int32_t *rank,
-                               int *nonfinite, void *ws_, hipStream_t s) {
+                               int *nonfinite, void *ws_, hipStream_t s, const CompressOverlap *ov) {
     const PadLayout L = pad_layout(M, D, k);
     char *ws = static_cast<char *>(ws_);
     double *aug = (double *)(ws + L.aug), *qa = (double *)(ws + L.qa), *ra = (double *)(ws + L.ra);
@@ -1144,7 +1226,7 @@ hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D,
     // unit rows then complete the basis (its rank is at least k)
     int32_t ra_rank = 0;
     GS_TRY(run_compress(aug, GS_F64, Ma, D, D, tol, qa, GS_F64, D, ra, GS_F64, Ma, kept_a, cn_a, &ra_rank,
-                        nonfinite, ws + L.cws, s));
+                        nonfinite, ws + L.cws, s, 0, ov));
     // rank of the codebook itself: the kept rows below M (kept is in index order)
     int32_t r = 0;
     GS_TRY(hipMemcpyAsync(&r, ws + L.cws + layout(Ma, D).rank_after + sizeof(int32_t) * (M - 1), sizeof(int32_t),
@@ -1179,7 +1261,7 @@ hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D,
 hipError_t run_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                                     int64_t subset, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt,
                                     int64_t ldr, int32_t *kept, float *cnorm, int32_t *ranks, int32_t *total,
-                                    int *nonfinite, void *ws, hipStream_t s) {
+                                    int *nonfinite, void *ws, hipStream_t s, const CompressOverlap *ov) {
     // R's capacity starts at zero: each subset writes its own block only
     hipLaunchKernelGGL(k_fill, dim3(1024), dim3(NT), 0, s, (char *)R, M, M, ldr, (int)esz(rt), 0);
     GS_TRY(hipGetLastError());
@@ -1192,7 +1274,7 @@ hipError_t run_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64
         GS_TRY(run_compress(static_cast<const char *>(C) + m0 * ldc * (int64_t)esz(ct), ct, mg, D, ldc, tol,
                             static_cast<char *>(Q) + o * ldq * (int64_t)esz(qt), qt, ldq,
                             static_cast<char *>(R) + (m0 * ldr + o) * (int64_t)esz(rt), rt, ldr,
-                            kept ? kept + o : nullptr, cnorm ? cnorm + m0 : nullptr, &rg, &nf, ws, s, m0));
+                            kept ? kept + o : nullptr, cnorm ? cnorm + m0 : nullptr, &rg, &nf, ws, s, m0, ov));
         ranks[g] = rg;
         *nonfinite |= nf;
         end = o + mg;         // rows o .. o + mg - 1 of Q / entries of kept were written

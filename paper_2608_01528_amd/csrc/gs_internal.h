@@ -247,23 +247,34 @@ hipError_t launch_sparse_prob2vec(gs_dtype tv, gs_dtype tt, const SparseArgs &a,
 
 // Compression.
 size_t compress_workspace(int64_t M, int64_t D);
+// A second stream (non-blocking, default priority) on which compression runs
+// the next panel's rows and the first part of its first pass while the
+// current panel is factored, and two events (timing disabled) that fork it
+// from and join it back into the caller's stream.  Without one (null), the
+// same launches run in the same order on the caller's stream alone, with the
+// same results bit for bit.
+struct CompressOverlap {
+    hipStream_t aux;
+    hipEvent_t fork, join;
+};
 // row_base is added to the kept row indices (a subset's first codebook row).
 hipError_t run_compress(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                         void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt, int64_t ldr,
                         int32_t *kept, float *cnorm, int32_t *rank, int *nonfinite,
-                        void *ws, hipStream_t s, int64_t row_base = 0);
+                        void *ws, hipStream_t s, int64_t row_base = 0, const CompressOverlap *ov = nullptr);
 // Basis completed to k vectors by unit vectors (coordinates zero-padded),
 // optionally transformed by an orthogonal k x k matrix H.
 size_t compress_padded_workspace(int64_t M, int64_t D, int64_t k);
 hipError_t run_compress_padded(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                                int64_t k, const double *H, int64_t ldh, void *Q, gs_dtype qt, int64_t ldq,
                                void *R, gs_dtype rt, int64_t ldr, int32_t *kept, float *cnorm, int32_t *rank,
-                               int *nonfinite, void *ws, hipStream_t s);
+                               int *nonfinite, void *ws, hipStream_t s, const CompressOverlap *ov = nullptr);
 // Consecutive subsets of `subset` codebook rows, each compressed on its own;
 // bases stacked in Q, coordinate blocks on R's block diagonal.
 hipError_t run_compress_partitioned(const void *C, gs_dtype ct, int64_t M, int64_t D, int64_t ldc, double tol,
                                     int64_t subset, void *Q, gs_dtype qt, int64_t ldq, void *R, gs_dtype rt,
                                     int64_t ldr, int32_t *kept, float *cnorm, int32_t *ranks, int32_t *total,
-                                    int *nonfinite, void *ws, hipStream_t s);
+                                    int *nonfinite, void *ws, hipStream_t s,
+                                    const CompressOverlap *ov = nullptr);
 
 }  // namespace gs
