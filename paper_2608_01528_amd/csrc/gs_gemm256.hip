@@ -248,6 +248,11 @@ template <> __device__ __forceinline__ bf16_t to_out<bf16_t>(float v) {
     return bf16_t{__builtin_bit_cast(uint16_t, (__bf16)v)};
 }
 
+// Two fp32 values as adjacent bf16 (round to nearest even), the first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
+    return (uint32_t)to_out<bf16_t>(x).bits | ((uint32_t)to_out<bf16_t>(y).bits << 16);
+}
+
 // Row of the output held by accumulator register g of a 32x32 block, for lane l.
 __device__ __forceinline__ int acc_row(int g, int l) { return 8 * (g >> 2) + 4 * (l >> 5) + (g & 3); }
 
@@ -306,7 +311,7 @@ __device__ __forceinline__ uint16_t *stage_slot(uint16_t *lds, int s) { return l
 // memory instructions of this wave that need not be waited for.  Returns once
 // the last MFMA is issued; the stages stay in use until the caller's next
 // barrier.
-template <typename T, bool BNN, bool SQA, bool SQB, int NW>
+template <typename T, bool BNN, bool SQA, bool SQB, int NW, bool SWP = false>
 __device__ __forceinline__ void mma_256(const GemmArgs &g, const TileLoads<T, BNN, NW> &tl, uint16_t *lds,
                                         int slot0, bool preissued, int pending,
                                         f16v acc[4][Waves<NW>::NJ], bool sqa, float sq[4], bool sqb,
@@ -355,12 +360,16 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, const TileLoads<T, BN
             }
     };
     auto mma = [&](const Frags &f) {
+        // SWP: B's fragment is the first operand, so the block comes out
+        // transposed (register g of lane l holds row l % 32, column
+        // 8 (g / 4) + 4 (l / 32) + g % 4 of the block)
         if constexpr (sizeof(T) == 2) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < NJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = SWP ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0)
+                                    : __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -368,7 +377,8 @@ __device__ __forceinline__ void mma_256(const GemmArgs &g, const TileLoads<T, BN
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
                     for (int j = 0; j < NJ; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][e], f.b[j][e], acc[i][j], 0, 0, 0);
+                        acc[i][j] = SWP ? __builtin_amdgcn_mfma_f32_32x32x2f32(f.b[j][e], f.a[i][e], acc[i][j], 0, 0, 0)
+                                        : __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[i][e], f.b[j][e], acc[i][j], 0, 0, 0);
         }
         if (SQA && sqa) {
 #pragma unroll
@@ -478,23 +488,28 @@ __device__ __forceinline__ void k_range(const GemmArgs &g, int64_t n0, bool a_no
 // work-group per CU) it walks its share of the range.
 // When a tile's last MFMAs are issued, the next tile's first stage is loaded
 // into the stage slot the last K-step did not read, and the output is staged
-// through the other slot in passes of PR rows (32 bf16 or 16 fp32 rows of
-// every wave, 36 KiB in all), then written with streaming stores that are not
-// waited for: the next tile waits only for its own first stage (issued before
-// those stores), so the stores drain while it computes.
+// through the other slot, 32 rows of every wave at a time (16 for fp32 output;
+// 36 KiB in all), then written as whole 16-byte row chunks with streaming
+// stores that are not waited for: the next tile waits only for its own first
+// stage (issued before those stores), so the stores drain while it computes.
+// With bf16 output the MFMAs take the B fragment as their first operand, so
+// each lane holds runs of four consecutive columns of one row and stages them
+// with one 8-byte LDS write per run (two-byte writes otherwise).
 template <typename T, typename TO, bool BNN>
 __global__ void __launch_bounds__(Waves<GEMM_NW>::NTHR) __attribute__((amdgpu_waves_per_eu(GEMM_NW / 4, GEMM_NW / 4)))
 gemm256_store_kernel(GemmArgs g) {
     typedef Waves<GEMM_NW> W;
     constexpr int NJ = W::NJ, WTN = W::WTN, TK = Op<T>::TK;
+    constexpr bool SWP = sizeof(TO) == 2;                    // transposed accumulator blocks
     constexpr int PR = sizeof(TO) == 2 ? 32 : 16;            // rows per staging pass
-    constexpr int RP = PR / 2;                               // accumulator registers per pass
+    constexpr int RP = PR / 2;                               // accumulator registers per pass (fp32)
     constexpr int EPC = 16 / (int)sizeof(TO);                // elements per 16-byte chunk
     constexpr int CPR = WTN / EPC;                           // chunks per sub-tile row
     constexpr int STRIDE = ep_stride<TO, GEMM_NW>();         // bytes per staged row
     constexpr int NSTORES = 4 * (32 / PR) * (PR * CPR / 64); // streaming stores per wave per interior tile
     static_assert(NSTORES == 16 || NSTORES == 32, "waits of mma_256");
     static_assert(GEMM_NW * PR * STRIDE <= 2 * OPT * 2, "staging fits one stage slot");
+    static_assert(STRIDE % 16 == 0, "16-byte reads of staged rows");
     extern __shared__ float lds_f[];
     uint16_t *lds = reinterpret_cast<uint16_t *>(lds_f);
     const int64_t nM = (g.M + TM - 1) / TM, nN = (g.N + TN - 1) / TN;
@@ -521,15 +536,15 @@ gemm256_store_kernel(GemmArgs g) {
         // (and spilled) across the product loop
         int tid = threadIdx.x;
         asm volatile("" : "+v"(tid));
-        const int l = tid & 63, w = tid >> 6;
+        const int l = tid & 63, w = tid >> 6, h = l >> 5;
         const int wm = W::wm(w), wn = W::wn(w);
         f16v acc[4][NJ];
         // row norms of A from the fragments (the waves of the left column):
         // the rownorm2 side output of the tiles with n0 == 0
         const bool sqa = a_norms && n0 == 0 && wn == 0;
         float sq[4] = {0.f, 0.f, 0.f, 0.f}, sb[NJ];
-        mma_256<T, BNN, true, false, GEMM_NW>(g, tl, lds, slot0, true, pending, acc, sqa, sq, false, sb, k_lo,
-                                              k_hi, tid);
+        mma_256<T, BNN, true, false, GEMM_NW, SWP>(g, tl, lds, slot0, true, pending, acc, sqa, sq, false, sb,
+                                                   k_lo, k_hi, tid);
         if (sqa) {
             // lanes l and l + 32 hold the two k-halves of row wm + 32 i + l % 32
 #pragma unroll
@@ -552,30 +567,45 @@ gemm256_store_kernel(GemmArgs g) {
             tl1.issue(g, k_lo1 / TK, 0, stage_slot(lds, next_slot), tid);
             tl1.issue(g, k_lo1 / TK, 1, stage_slot(lds, next_slot), tid);
         }
-        __syncthreads();                  // every wave is done reading this tile's stages
 
-        // Epilogue: each wave stages PR rows of its 128 x WTN sub-tile at a
-        // time in its own part of the other slot (rows padded so the
-        // column-wise writes of the accumulator layout do not collide on
-        // banks), then writes whole 16-byte row chunks.
-        unsigned char *region = reinterpret_cast<unsigned char *>(stage_slot(lds, next_slot ^ 1)) + w * (PR * STRIDE);
-        // whole tile inside the output, rows 16-byte aligned: 16-byte stores
+        // whole tile inside the output, rows 16-byte aligned: staged 16-byte stores
         const bool interior = ((reinterpret_cast<uintptr_t>(C) & 15) == 0) && (g.ldc % EPC == 0) &&
                               m0 + TM <= g.M && n0 + TN <= g.N;
+        if (interior) {
+            __syncthreads();              // every wave is done reading this tile's stages
+            // Each wave stages PR rows of its 128 x WTN sub-tile at a time in
+            // its own part of the other slot (rows padded against bank
+            // collisions), then writes whole 16-byte row chunks.
+            unsigned char *region =
+                reinterpret_cast<unsigned char *>(stage_slot(lds, next_slot ^ 1)) + w * (PR * STRIDE);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int hh = 0; hh < 32 / PR; ++hh) {
+                for (int hh = 0; hh < 32 / PR; ++hh) {
+                    if constexpr (SWP) {
+                        // register 4 m + e of block (i, j): row 32 i + l % 32,
+                        // column 32 j + 8 m + 4 h + e of the wave's sub-tile
 #pragma unroll
-                for (int j = 0; j < NJ; ++j)
+                        for (int j = 0; j < NJ; ++j)
 #pragma unroll
-                    for (int gg = 0; gg < RP; ++gg) {
-                        const int row = acc_row(RP * hh + gg, l) - PR * hh, col = 32 * j + (l & 31);
-                        *reinterpret_cast<TO *>(region + row * STRIDE + col * (int)sizeof(TO)) =
-                            to_out<TO>(acc[i][j][RP * hh + gg]);
+                            for (int m = 0; m < 4; ++m) {
+                                const f16v &a = acc[i][j];
+                                const uint2 v = {pack_bf16(a[4 * m], a[4 * m + 1]),
+                                                 pack_bf16(a[4 * m + 2], a[4 * m + 3])};
+                                *reinterpret_cast<uint2 *>(region + (l & 31) * STRIDE +
+                                                           (32 * j + 8 * m + 4 * h) * (int)sizeof(TO)) = v;
+                            }
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                            for (int gg = 0; gg < RP; ++gg) {
+                                const int row = acc_row(RP * hh + gg, l) - PR * hh, col = 32 * j + (l & 31);
+                                *reinterpret_cast<TO *>(region + row * STRIDE + col * (int)sizeof(TO)) =
+                                    to_out<TO>(acc[i][j][RP * hh + gg]);
+                            }
                     }
-                const int64_t rb = m0 + wm + 32 * i + PR * hh;   // first output row of this pass
-                if (interior) {
+                    const int64_t rb = m0 + wm + 32 * i + PR * hh;   // first output row of this pass
 #pragma unroll
                     for (int id = l; id < PR * CPR; id += 64) {
                         const int rr = id / CPR, cc = id % CPR;
@@ -592,21 +622,27 @@ gemm256_store_kernel(GemmArgs g) {
                         // should not displace the operand slices other tiles share in L2
                         __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(dst));
                     }
-                } else {
-                    // edge tiles and unaligned outputs: element stores within bounds
-                    for (int id = l; id < PR * WTN; id += 64) {
-                        const int rr = id / WTN, cc = id % WTN;
-                        const int64_t grow = rb + rr, gcol = n0 + wn + cc;
-                        if (grow < g.M && gcol < g.N) {
-                            TO x = *reinterpret_cast<const TO *>(region + rr * STRIDE + cc * (int)sizeof(TO));
+                }
+        } else {
+            // edge tiles and unaligned outputs: element stores within bounds,
+            // straight from the accumulators
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int64_t row = m0 + wm + 32 * i + (SWP ? (l & 31) : acc_row(e, l));
+                        const int64_t col = n0 + wn + 32 * j + (SWP ? 8 * (e >> 2) + 4 * h + (e & 3) : (l & 31));
+                        if (row < g.M && col < g.N) {
+                            TO x = to_out<TO>(acc[i][j][e]);
                             if constexpr (sizeof(TO) == 4) {
-                                if (g.mul_out) x = x * C[grow * g.ldc + gcol];
+                                if (g.mul_out) x = x * C[row * g.ldc + col];
                             }
-                            C[grow * g.ldc + gcol] = x;
+                            C[row * g.ldc + col] = x;
                         }
                     }
-                }
-            }
+        }
         if (!has_next) break;
         // the stores just issued (a fixed count on interior tiles without
         // loads in the epilogue) need not land before the next tile starts
