@@ -227,6 +227,7 @@ struct SoftArgs {
     int cosine;
     float scale, beta;
     int coords;                                 // form t = p R per row (else scores through R R^T)
+    int t_bf16;                                 // coordinate outputs T in bf16 (else fp32)
 };
 
 int64_t soft_select_tiles(int64_t B);

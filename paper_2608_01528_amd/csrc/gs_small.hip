@@ -443,61 +443,6 @@ __device__ __forceinline__ int soft_group(const SoftArgs &a, int64_t blk) {
     return gi;
 }
 
-// Row ops over RPT rows at once (row u of thread t lives at tile row
-// t + u * SROWS, row stride M).
-template <int MB, class Rows>
-__device__ __forceinline__ void rows_prob2vec(const float *tile, int M, int r, const Rows &R, float out[RPT][MB]) {
-#pragma unroll
-    for (int q = 0; q < RPT; ++q)
-#pragma unroll
-        for (int k = 0; k < MB; ++k) out[q][k] = 0.f;
-#pragma unroll 2
-    for (int j = 0; j < M; ++j) {
-        float p[RPT];
-#pragma unroll
-        for (int q = 0; q < RPT; ++q) p[q] = tile[(threadIdx.x + q * SROWS) * M + j];
-        float rr[MB];
-        R.row(j, rr);
-#pragma unroll
-        for (int k = 0; k < MB; ++k)
-#pragma unroll
-            for (int q = 0; q < RPT; ++q) out[q][k] += p[q] * rr[k];
-    }
-#pragma unroll
-    for (int q = 0; q < RPT; ++q)
-#pragma unroll
-        for (int k = 0; k < MB; ++k)
-            if (k >= r) out[q][k] = 0.f;
-}
-
-template <int MB, class Rows>
-__device__ __forceinline__ void rows_scores(const float x[RPT][MB], int M, const Rows &R, const float *Rn,
-                                            float mul, const float q[RPT], float *tile, float best[RPT],
-                                            int bi[RPT]) {
-#pragma unroll
-    for (int u = 0; u < RPT; ++u) { best[u] = -INFINITY; bi[u] = 0; }
-#pragma unroll 2
-    for (int j = 0; j < M; ++j) {
-        float rr[MB];
-        R.row(j, rr);
-        float d[RPT];
-#pragma unroll
-        for (int u = 0; u < RPT; ++u) d[u] = 0.f;
-#pragma unroll
-        for (int k = 0; k < MB; ++k)
-#pragma unroll
-            for (int u = 0; u < RPT; ++u) d[u] += x[u][k] * rr[k];
-        const float rn = Rn[j];
-#pragma unroll
-        for (int u = 0; u < RPT; ++u) {
-            const float sj = mul * d[u] * q[u] * rn;
-            tile[(threadIdx.x + u * SROWS) * M + j] = sj;
-            if (sj > best[u]) { best[u] = sj; bi[u] = j; }
-        }
-    }
-}
-
-
 // --------------------------------------------- soft selection, Gram form
 //
 // Without a coordinate output the coordinates t = p R are never formed: with
@@ -606,6 +551,35 @@ __device__ __forceinline__ void gram_stage(const float (&rk)[(M + 1) / 2], float
     }
 }
 
+// Coordinate form: wave 0 publishes the codebook coordinates themselves,
+// Rs[j * GS + k] = R[j][k] (zero for k >= r), from the same operand layout,
+// their transpose Rs[MAXK * MAXK + k * GS + j] for codebooks of at most 8
+// entries, and the per-entry factors as gram_stage does.
+template <int M, int GS>
+__device__ __forceinline__ void rows_stage(const float (&rk)[(M + 1) / 2], float *Rs, float *Rn, bool cosine,
+                                           bool given, float cn) {
+    const int l = threadIdx.x;
+    const int row = l & 31, h = l >> 5;
+    float s2 = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < (M + 1) / 2; ++kk) {
+        s2 += rk[kk] * rk[kk];
+        if (row < M) {
+            Rs[row * GS + 2 * kk + h] = rk[kk];
+            if (M <= 8) Rs[MAXK * MAXK + (2 * kk + h) * GS + row] = rk[kk];
+        }
+    }
+    s2 += __shfl_xor(s2, 32);   // ||R_row||^2: even and odd columns
+    if (l < M) {
+        float c = 1.f;
+        if (cosine) {
+            const float n = given ? cn : sqrtf(s2);
+            c = (n > 0.f) ? 1.f / n : 0.f;
+        }
+        Rn[l] = c;
+    }
+}
+
 // LDS accesses of one wave complete in order: fences that keep the compiler
 // from moving this wave's LDS reads and writes across each other.
 __device__ __forceinline__ void wave_lds_fence() {
@@ -618,9 +592,221 @@ __device__ __forceinline__ void wave_lds_fence() {
 // the block, their own part of the tile), so after the one work-group
 // barrier that publishes the Gram matrix the waves go on independently: one
 // wave's arithmetic overlaps another's loads and stores.
-template <typename TI, int M>
-__device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float scale, float beta, int64_t b0,
-                                          int nrow, float *tile, float *Gs, float *Rn) {
+// Coordinate form of step 5 for the wave's 64 rows (rows wrow0 .. + 63 of
+// the block, in wtile): t = p R for each row, stored (bf16 or fp32) when the group
+// asks for T, then the raw scores d_j = <t, R_j> of this thread's row and
+// ||t||^2 in n2.  Rs holds R (row stride GS, zero past r columns).
+//   M <= 8: vector units, each thread its own row (2 M^2 multiply-adds).
+//   9 <= M <= 16: matrix cores, 16 x 16 blocks (below).
+//   M > 16: matrix cores, the wave's rows as two 32-row blocks.  First
+//     T^T = R^T P^T (v_mfma_f32_32x32x2f32, step kk pairing m = kk and
+//     kk + KH over the half-waves): lane l supplies R[m][l % 32] and
+//     P[row l % 32][m], and its register g then holds T[row l % 32][k] for
+//     k = 8 (g / 4) + 4 (l / 32) + g % 4.  Those registers are directly the
+//     A operand of S = T R^T (step s pairing the same k with B = R[l % 32][k]
+//     from registers), whose result block (lane l, register g: row
+//     8 (g / 4) + 4 (l / 32) + g % 4, entry l % 32) goes through the tile to
+//     the threads' rows.
+// The wave's rows of T (row stride r in wtile) to the output, in bf16 or fp32.
+__device__ __forceinline__ void store_coords(const SoftGroup &G, bool t_bf16, int64_t b0, int wrow0, int nroww,
+                                             const float *wtile, int lane) {
+    if (t_bf16) tile_store<bf16_t, 64>(static_cast<bf16_t *>(G.T), G.ldt, b0 + wrow0, nroww, (int)G.r, wtile, lane);
+    else tile_store<float, 64>(static_cast<float *>(G.T), G.ldt, b0 + wrow0, nroww, (int)G.r, wtile, lane);
+}
+
+template <int M, int GS>
+__device__ __forceinline__ void soft_coords(const SoftGroup &G, bool t_bf16, int64_t b0, int wrow0, int nroww,
+                                            float *tile, float *wtile, const float *Rs, float (&d)[M], float &n2) {
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int r = (int)G.r;
+    float *srow = tile + t * M;
+    if constexpr (M <= 8) {
+        float p[M], tk[M];
+#pragma unroll
+        for (int k = 0; k < M; ++k) p[k] = srow[k];
+#pragma unroll
+        for (int k = 0; k < M; ++k) tk[k] = 0.f;
+#pragma unroll
+        for (int j = 0; j < M; ++j) {
+            const f4v *rq = reinterpret_cast<const f4v *>(Rs + j * GS);
+#pragma unroll
+            for (int qq = 0; qq < GS / 4; ++qq) {
+                const f4v v = rq[qq];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * qq + i < M) tk[4 * qq + i] += p[j] * v[i];
+            }
+        }
+        // d_j = sum_k t_k R[j][k], one row of R^T at a time into M
+        // independent sums
+        const float *Rt = Rs + MAXK * MAXK;
+#pragma unroll
+        for (int j = 0; j < M; ++j) d[j] = 0.f;
+#pragma unroll
+        for (int k = 0; k < M; ++k) {
+            const f4v *rq = reinterpret_cast<const f4v *>(Rt + k * GS);
+#pragma unroll
+            for (int qq = 0; qq < GS / 4; ++qq) {
+                const f4v v = rq[qq];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (4 * qq + i < M) d[4 * qq + i] += tk[k] * v[i];
+            }
+        }
+        n2 = 0.f;
+#pragma unroll
+        for (int k = 0; k < M; ++k) n2 += tk[k] * tk[k];
+        if (G.T) {
+            // rows of r values in the wave's tile, after every lane's row reads
+            wave_lds_fence();
+            float *trow = wtile + lane * r;
+#pragma unroll
+            for (int k = 0; k < M; ++k)
+                if (k < r) trow[k] = tk[k];
+            wave_lds_fence();
+            store_coords(G, t_bf16, b0, wrow0, nroww, wtile, lane);
+            wave_lds_fence();
+        }
+    } else if constexpr (M <= 16) {
+        // 16 x 16 blocks (v_mfma_f32_16x16x4f32), the wave's rows as four
+        // 16-row blocks.  T^T = R^T P^T in steps of four entries m = 4 s + q
+        // (q = lane / 16): lane l supplies R[m][l % 16] and P[row l % 16][m],
+        // and its register g then holds T[row l % 16][4 q + g], directly the
+        // A operand of S = T R^T at step g (B = R[l % 16][4 q + g]); the
+        // result (lane l, register g: row 4 q + g, entry l % 16) goes through
+        // the tile to the threads' rows.
+        constexpr int KS = (M + 3) / 4;
+        const int c = lane & 15, qd = lane >> 4;
+        f4v tq[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const float *prow = tile + (wrow0 + 16 * b + c) * M;
+            tq[b] = f4v{};
+#pragma unroll
+            for (int st = 0; st < KS; ++st) {
+                const int m = 4 * st + qd;
+                const float ra = (m < M && c < M) ? Rs[m * GS + c] : 0.f;
+                const float x = (m < M) ? prow[m] : 0.f;
+                tq[b] = __builtin_amdgcn_mfma_f32_16x16x4f32(ra, x, tq[b], 0, 0, 0);
+            }
+        }
+        // ||t||^2 of row l % 16 of each block (coordinates past r are zero)
+        float nb[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            float s2 = tq[b][0] * tq[b][0] + tq[b][1] * tq[b][1] + tq[b][2] * tq[b][2] + tq[b][3] * tq[b][3];
+            s2 += __shfl_xor(s2, 16);
+            nb[b] = s2 + __shfl_xor(s2, 32);
+        }
+        n2 = (qd == 0) ? nb[0] : (qd == 1) ? nb[1] : (qd == 2) ? nb[2] : nb[3];   // block l / 16, row l % 16
+        if (G.T) {
+            // the products consumed every probability read of the wave
+            wave_lds_fence();
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int k = 4 * qd + g;
+                    if (k < r) wtile[(16 * b + c) * r + k] = tq[b][g];
+                }
+            wave_lds_fence();
+            store_coords(G, t_bf16, b0, wrow0, nroww, wtile, lane);
+        }
+        float rb[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int k = 4 * qd + g;
+            rb[g] = (c < M && k < M) ? Rs[c * GS + k] : 0.f;
+        }
+        wave_lds_fence();   // T (or the probabilities) have left the tile
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            f4v acc = {};
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(tq[b][g], rb[g], acc, 0, 0, 0);
+            if (c < M) {
+                float *drow = tile + (wrow0 + 16 * b + 4 * qd) * M + c;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) drow[g * M] = acc[g];
+            }
+        }
+        wave_lds_fence();
+#pragma unroll
+        for (int j = 0; j < M; ++j) d[j] = srow[j];
+    } else {
+        constexpr int KH = (M + 1) / 2;
+        // steps of the second product: s with 8 (s / 4) + s % 4 < M
+        constexpr int NS = 4 * (M / 8) + (M % 8 < 4 ? M % 8 : 4);
+        const int l = lane, c = l & 31, h = l >> 5;
+        gs16v tq[2];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const float *arow = tile + (wrow0 + 32 * b + c) * M + KH * h;
+            tq[b] = gs16v{};
+#pragma unroll
+            for (int kk = 0; kk < KH; ++kk) {
+                const int m = kk + KH * h;
+                const float ra = (m < M && c < M) ? Rs[m * GS + c] : 0.f;
+                float x = arow[kk];
+                if (M % 2 == 1 && kk == KH - 1) x = (h == 0) ? x : 0.f;
+                tq[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(ra, x, tq[b], 0, 0, 0);
+            }
+        }
+        // ||t||^2 of row l % 32 of each block (coordinates past r are zero)
+        float nb[2];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            float s2 = 0.f;
+#pragma unroll
+            for (int g = 0; g < 16; ++g) s2 += tq[b][g] * tq[b][g];
+            nb[b] = s2 + __shfl_xor(s2, 32);
+        }
+        n2 = h ? nb[1] : nb[0];   // this thread's row: block l / 32, row l % 32
+        if (G.T) {
+            // the products consumed every probability read of the wave
+            wave_lds_fence();
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int g = 0; g < 16; ++g) {
+                    const int k = 8 * (g >> 2) + 4 * h + (g & 3);
+                    if (k < r) wtile[(32 * b + c) * r + k] = tq[b][g];
+                }
+            wave_lds_fence();
+            store_coords(G, t_bf16, b0, wrow0, nroww, wtile, lane);
+        }
+        float rb[NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int k = 8 * (s >> 2) + 4 * h + (s & 3);
+            rb[s] = (c < M && k < M) ? Rs[c * GS + k] : 0.f;
+        }
+        wave_lds_fence();   // T (or the probabilities) have left the tile
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            gs16v acc = {};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(tq[b][s], rb[s], acc, 0, 0, 0);
+            if (c < M) {
+                float *drow = tile + (wrow0 + 32 * b + 4 * h) * M + c;
+#pragma unroll
+                for (int g = 0; g < 16; ++g) drow[(8 * (g >> 2) + (g & 3)) * M] = acc[g];
+            }
+        }
+        wave_lds_fence();
+#pragma unroll
+        for (int j = 0; j < M; ++j) d[j] = srow[j];
+    }
+}
+
+// CO (coordinate form): the codebook coordinates go to Gs in place of the
+// Gram matrix, and each row's coordinates t = p R are formed (stored
+// when the group asks for T) and scored against R, 2 M^2 multiply-adds per
+// row (R zero past r columns).
+template <typename TI, int M, bool CO>
+__device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float scale, float beta, bool t_bf16,
+                                          int64_t b0, int nrow, float *tile, float *Gs, float *Rn) {
     constexpr int GS = (M + 3) & ~3;   // row stride of G in LDS (16-byte rows)
     constexpr int KG = (M + 1) / 2;    // steps of the Gram product
     const int t = threadIdx.x;
@@ -653,9 +839,12 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     TileReq<TI> req;
     req.issue(base, contig ? n : 0, lane);   // an empty range issues nothing useful
 
-    // 3. Gram matrix and factors while the tiles are in flight, published to
-    // every wave
-    if (t < 64) gram_stage<M, GS>(rk, Gs, Rn, cosine, G.cnorm != nullptr, cn);
+    // 3. Gram matrix (coordinate form: the coordinates) and factors while the
+    // tiles are in flight, published to every wave
+    if (t < 64) {
+        if constexpr (CO) rows_stage<M, GS>(rk, Gs, Rn, cosine, G.cnorm != nullptr, cn);
+        else gram_stage<M, GS>(rk, Gs, Rn, cosine, G.cnorm != nullptr, cn);
+    }
     lds_barrier();
 
     // 4. this wave's rows to its part of the tile
@@ -668,10 +857,15 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
 
     // 5. scores of the thread's row, in registers
     float *srow = tile + t * M;
+    float d[M];
+    float q;
+    if constexpr (CO) {
+        soft_coords<M, GS>(G, t_bf16, b0, wrow0, nroww, tile, wtile, Gs, d, q);
+        q = cosine ? ((q > 0.f) ? 1.f / sqrtf(q) : 0.f) : 1.f;   // in span: ||v|| = ||t||
+    } else {
     float p[M];
 #pragma unroll
     for (int k = 0; k < M; ++k) p[k] = srow[k];
-    float d[M];
     if constexpr (M > 16) {
         // Matrix cores: the wave's 64 rows as two 32 x M blocks times G
         // (v_mfma_f32_32x32x2f32; step kk pairs k = kk and kk + KH over the
@@ -735,7 +929,8 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     float n2 = 0.f;
 #pragma unroll
     for (int j = 0; j < M; ++j) n2 += p[j] * d[j];
-    const float q = cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;   // in span: ||v|| = ||t||
+    q = cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;   // in span: ||v|| = ||t||
+    }
     const float mq = scale * q;
     float best = -INFINITY, worst = INFINITY;
     int bi = 0;
@@ -776,12 +971,12 @@ __device__ __forceinline__ void soft_gram(const SoftGroup &G, bool cosine, float
     }
 }
 
-template <typename TI, int M>
+template <typename TI, int M, bool CO>
 __device__ __forceinline__ void soft_gram_m(int m, const SoftGroup &G, bool cosine, float scale, float beta,
-                                            int64_t b0, int nrow, float *tile, float *Gs, float *Rn) {
+                                            bool t_bf16, int64_t b0, int nrow, float *tile, float *Gs, float *Rn) {
     if constexpr (M <= MAXK) {
-        if (m == M) soft_gram<TI, M>(G, cosine, scale, beta, b0, nrow, tile, Gs, Rn);
-        else soft_gram_m<TI, M + 1>(m, G, cosine, scale, beta, b0, nrow, tile, Gs, Rn);
+        if (m == M) soft_gram<TI, M, CO>(G, cosine, scale, beta, t_bf16, b0, nrow, tile, Gs, Rn);
+        else soft_gram_m<TI, M + 1, CO>(m, G, cosine, scale, beta, t_bf16, b0, nrow, tile, Gs, Rn);
     }
 }
 
@@ -801,112 +996,24 @@ __global__ void __launch_bounds__(SROWS, 4) soft_gram_kernel(SoftArgs a) {
     const SoftGroup G = a.g[gi];   // by value: the group's descriptor in scalar registers
     const int64_t b0 = (blk - a.tile_start[gi]) * SBLK;
     const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
-    soft_gram_m<TI, 1>((int)G.M, G, a.cosine != 0, a.scale, a.beta, b0, nrow, tile, Gs, Rn);
+    soft_gram_m<TI, 1, false>((int)G.M, G, a.cosine != 0, a.scale, a.beta, false, b0, nrow, tile, Gs, Rn);
 }
 
-template <typename TI, typename TT, int MB, class Rows>
-__device__ __forceinline__ void soft_block(const SoftArgs &a, const SoftGroup &G, int64_t b0, int nrow,
-                                           const Rows &Rsrc, const float *Rn, float *tile) {
-    const int t = threadIdx.x;
-    const int M = (int)G.M, r = (int)G.r;
-    float best[RPT];
-    int bi[RPT];
-    {
-        float x[RPT][MB];
-        rows_prob2vec<MB>(tile, M, r, Rsrc, x);      // Gram-loc of the superposed vectors
-        float q[RPT];
-#pragma unroll
-        for (int u = 0; u < RPT; ++u) {
-            float n2 = 0.f;
-#pragma unroll
-            for (int k = 0; k < MB; ++k) n2 += x[u][k] * x[u][k];   // in span: ||v|| = ||t||
-            q[u] = a.cosine ? ((n2 > 0.f) ? 1.f / sqrtf(n2) : 0.f) : 1.f;
-        }
-        lds_barrier();   // the tile is reused for the outputs
-        if (G.T) {
-#pragma unroll
-            for (int u = 0; u < RPT; ++u)
-#pragma unroll
-                for (int k = 0; k < MB; ++k)
-                    if (k < r) tile[(t + u * SROWS) * r + k] = x[u][k];
-            lds_barrier();
-            tile_store<TT, SROWS>(static_cast<TT *>(G.T), G.ldt, b0, nrow, r, tile);
-            lds_barrier();
-        }
-        rows_scores<MB>(x, M, Rsrc, Rn, a.scale, q, tile, best, bi);
-    }
-    if (G.argmax) {
-#pragma unroll
-        for (int u = 0; u < RPT; ++u)
-            if (t + u * SROWS < nrow) __builtin_nontemporal_store(bi[u], G.argmax + b0 + t + u * SROWS);
-    }
-    if (G.S) {
-        lds_barrier();
-        tile_store<float, SROWS>(G.S, G.lds, b0, nrow, M, tile);
-    }
-    if (G.A) {
-        // attention weights: softmax of beta times the same scores; the
-        // maximum of beta * s is taken after scaling (beta may be negative)
-        if (G.S) lds_barrier();   // S has left the tile before it is overwritten
-#pragma unroll
-        for (int u = 0; u < RPT; ++u) {
-            float *srow = tile + (t + u * SROWS) * M;
-            float mx = -INFINITY;
-            for (int j = 0; j < M; ++j) mx = fmaxf(mx, a.beta * srow[j]);
-            row_softmax(srow, M, a.beta, mx);
-        }
-        lds_barrier();
-        tile_store<float, SROWS>(G.A, G.lda, b0, nrow, M, tile);
-    }
-}
-
-// At least four work-groups per CU (every work-group of the vsa launch in one
-// round): at most 128 registers per lane.
-template <typename TI, typename TT>
+// Fused soft selection in the coordinate form: t = p R is formed for every
+// row (and stored when the group asks for T), then scored against R, on the
+// same frame as the Gram form (specialised on M, waves independent after the
+// barrier that publishes the codebook block).
+template <typename TI>
 __global__ void __launch_bounds__(SROWS, 4) soft_select_kernel(SoftArgs a) {
     __shared__ __attribute__((aligned(16))) float tile[SBLK * MAXK];
-    __shared__ __attribute__((aligned(16))) float Rs[MAXK * MAXK];
+    __shared__ __attribute__((aligned(16))) float Rs[MAXK * MAXK + 8 * 8];   // R, then R^T for M <= 8
     __shared__ float Rn[MAXK];
     const int64_t blk = blockIdx.x;
     const int gi = soft_group(a, blk);
-    const SoftGroup &G = a.g[gi];
+    const SoftGroup G = a.g[gi];   // by value: the group's descriptor in scalar registers
     const int64_t b0 = (blk - a.tile_start[gi]) * SBLK;
-    const int M = (int)G.M, r = (int)G.r;
     const int nrow = (int)((G.B - b0 < SBLK) ? (G.B - b0) : SBLK);
-    const int MB = a.mb[gi];
-    const TI *P = static_cast<const TI *>(G.P);
-    const TI *R = static_cast<const TI *>(G.R);
-
-    // 1. request the probability tile: each wave its own 64 rows, as in the
-    // Gram form (one linear range per wave when rows are contiguous)
-    static_assert(SBLK == SROWS, "one row per thread");
-    const TI *base = P + b0 * G.ldp;
-    const bool contig = G.ldp == G.M && aligned16(base);
-    const int lane = threadIdx.x & 63, wrow0 = threadIdx.x & ~63;
-    const int nroww = (nrow - wrow0 < 0) ? 0 : (nrow - wrow0 < 64) ? nrow - wrow0 : 64;
-    const TI *wbase = base + (int64_t)wrow0 * M;
-    TileReq<TI> req;
-    req.issue(wbase, contig ? nroww * M : 0, lane);
-    // 2. stage the norms and the padded codebook block while the tile is in
-    // flight
-    stage_norms<TI, SROWS>(R, G.ldr, M, r, G.cnorm, a.cosine != 0, MB, Rn);
-    for (int e = threadIdx.x; e < MB * MB; e += SROWS) {
-        const int j = e / MB, k = e - (e / MB) * MB;
-        Rs[e] = (j < M && k < r) ? ld_f32<TI>(R, (int64_t)j * G.ldr + k) : 0.f;
-    }
-    // 3. tile to LDS
-    if (contig) {
-        req.store(tile + wrow0 * M, wbase, nroww * M, lane);
-    } else {
-        tile_load<TI, SROWS>(P, G.ldp, b0, nrow, M, tile);
-    }
-    lds_barrier();
-    switch (MB) {
-        case 8: soft_block<TI, TT, 8>(a, G, b0, nrow, LdsRows<8>{Rs}, Rn, tile); break;
-        case 16: soft_block<TI, TT, 16>(a, G, b0, nrow, LdsRows<16>{Rs}, Rn, tile); break;
-        case 24: soft_block<TI, TT, 24>(a, G, b0, nrow, LdsRows<24>{Rs}, Rn, tile); break;
-        default: soft_block<TI, TT, 32>(a, G, b0, nrow, LdsRows<32>{Rs}, Rn, tile); break;
-    }
+    soft_gram_m<TI, 1, true>((int)G.M, G, a.cosine != 0, a.scale, a.beta, a.t_bf16 != 0, b0, nrow, tile, Rs, Rn);
 }
 
 template <typename TI, typename TO, int MODE>
@@ -958,10 +1065,11 @@ hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipS
         else return hipErrorInvalidValue;
         return hipGetLastError();
     }
-    if (tin == GS_F32 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<float, float>), grid, block, 0, s, a);
-    else if (tin == GS_F32 && tt == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<float, bf16_t>), grid, block, 0, s, a);
-    else if (tin == GS_BF16 && tt == GS_F32) hipLaunchKernelGGL((soft_select_kernel<bf16_t, float>), grid, block, 0, s, a);
-    else if (tin == GS_BF16 && tt == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<bf16_t, bf16_t>), grid, block, 0, s, a);
+    if (tt != GS_F32 && tt != GS_BF16) return hipErrorInvalidValue;
+    SoftArgs b = a;
+    b.t_bf16 = tt == GS_BF16;
+    if (tin == GS_F32) hipLaunchKernelGGL((soft_select_kernel<float>), grid, block, 0, s, b);
+    else if (tin == GS_BF16) hipLaunchKernelGGL((soft_select_kernel<bf16_t>), grid, block, 0, s, b);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

@@ -720,6 +720,39 @@ def test_soft_select(mode, scale, beta, form):
         soft_argmax_exact(g["argmax"], host(b["Pd"]), host(b["Rd"]), None, mode, scale)
 
 
+@pytest.mark.parametrize("tdt", [torch.float32, torch.bfloat16], ids=_name_early)
+@pytest.mark.parametrize("form", ["auto-T", "coords"])
+def test_soft_select_rank_deficient_coordinates(tdt, form):
+    # codebooks with duplicated rows (r < M) on each of the coordinate form's
+    # three paths (vector units up to 8 entries, 16 x 16 matrix blocks up to
+    # 16, 32 x 32 beyond), ragged batches: T has r columns and the scores,
+    # weights and argmax are those of the dense definitions
+    Ms, Bs = [7, 8, 13, 16, 20, 31], [300, 64, 257, 1, 700, 129]
+    books = []
+    for i, (M, B) in enumerate(zip(Ms, Bs)):
+        C = rq_codebook("bipolar", M, 256, 90 + i, dup=0.3)
+        Qo, Ro, kept, r = oracle.compress(C)
+        assert r < M
+        P = wl.softmax_probs(B, M, math.sqrt(2), 90 + i)
+        books.append(dict(C=C, Qo=Qo, Ro=Ro, P=P, Pd=dev(P), Rd=dev(Ro.astype(np.float32)), M=M, B=B, r=r))
+    with_t = form == "auto-T"
+    groups = soft_outputs(books, want=("T", "S", "argmax", "A") if with_t else ("S", "argmax", "A"))
+    if with_t:
+        for g, b in zip(groups, books):
+            g["T"] = torch.full((b["B"], b["r"]), np.nan, device="cuda", dtype=tdt)
+    gsm.gs_soft_select(groups, mode="cosine", scale=1.0, beta=16.0, form=form.split("-")[0])
+    torch.cuda.synchronize()
+    for b, g in zip(books, groups):
+        V = oracle.prob2vec(b["P"], b["C"])
+        So = oracle.similarity(V, b["C"], oracle.COSINE)
+        if with_t:
+            tol = TOL_F32 if tdt == torch.float32 else TOL_BF16
+            assert rowrel(host(g["T"]), oracle.project(V, b["Qo"])) <= tol
+        assert rowrel(host(g["S"]), So) <= TOL_F32
+        assert rowrel(host(g["A"]), oracle.softmax(So, 16.0)) <= TOL_F32
+        soft_argmax_exact(g["argmax"], b["P"], b["Ro"].astype(np.float32), None, "cosine", 1.0)
+
+
 @pytest.mark.parametrize("pdt", [torch.float32, torch.bfloat16], ids=_name_early)
 def test_soft_select_strided_rows(pdt):
     # probabilities and outputs as column slices of wider matrices (row
