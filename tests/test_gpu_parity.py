@@ -1141,6 +1141,43 @@ def test_large_tiles_ragged_columns(op_dtype):
         assert rowrel(Tg, oracle.project(X[rows], Q)) <= tol
 
 
+@pytest.mark.parametrize("op_dtype", OP_DTYPES, ids=_name)
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=_name)
+def test_large_tiles_unaligned_outputs(op_dtype, out_dtype):
+    # outputs whose rows are not 16-byte aligned (a view starting one element
+    # into an odd-strided buffer): every tile leaves through the element
+    # stores; the buffer's columns outside the view stay untouched
+    print("large tiles, unaligned outputs", _name(op_dtype), _name(out_dtype), flush=True)
+    tol = TOL_F32 if out_dtype == torch.float32 else TOL_BF16
+
+    def view(B, N):
+        buf = torch.full((B, N + 3), float("nan"), device="cuda", dtype=out_dtype)
+        return buf, buf[:, 1:N + 1]
+
+    def untouched(buf, N):
+        return torch.isnan(buf[:, 0].float()).all().item() and torch.isnan(buf[:, N + 1:].float()).all().item()
+
+    B, K, N = 16384, 300, 1000            # project: 64 x 4 tiles, ragged last column tile
+    X, Q = _mat(B, K, 91, op_dtype), _mat(N, K, 92, op_dtype, 1 / np.sqrt(K))
+    ldk = _ld(K, op_dtype)
+    buf, T = view(B, N)
+    gsm.gs_project(nan_padded(X, ldk, op_dtype), nan_padded(Q, ldk, op_dtype), out=T)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 93)
+    assert torch.isfinite(T.float()).all().item() and untouched(buf, N)
+    assert rowrel(host(T[rows]), oracle.project(X[rows], Q)) <= tol
+
+    B, r, D = 8192, 45, 2100              # restore: 32 x 9 tiles
+    Tc, Qr = _mat(B, r, 94, op_dtype), _mat(r, D, 95, op_dtype)
+    buf, Xo = view(B, D)
+    gsm.gs_reconstruct(nan_padded(Tc, _ld(r, op_dtype), op_dtype), nan_padded(Qr, _ld(D, op_dtype, 8), op_dtype),
+                       out=Xo)
+    torch.cuda.synchronize()
+    rows = _tile_rows(B, 96)
+    assert torch.isfinite(Xo.float()).all().item() and untouched(buf, D)
+    assert rowrel(host(Xo[rows]), oracle.reconstruct(Tc[rows], Qr)) <= tol
+
+
 # ------------- row sweep / scored products (>= 256 row blocks of 256, 256-column blocks)
 #
 # With Q the identity, coordinates and codebook coordinates are themselves the
