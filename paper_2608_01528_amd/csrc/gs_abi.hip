@@ -722,7 +722,6 @@ gs_status gs_soft_select(const gs_soft_group *groups, int ngroups, gs_dtype pt, 
         d.argmax = g.argmax; d.A = g.A; d.lda = g.lda;
         a.tile_start[k] = tiles;
         tiles += soft_select_tiles(g.B);
-        a.mb[k] = soft_select_pad(g.M);
     }
     a.tile_start[ngroups] = tiles;
     a.ntiles = tiles;

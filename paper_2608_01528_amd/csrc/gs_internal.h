@@ -222,7 +222,6 @@ struct SoftArgs {
     SoftGroup g[SOFT_MAX_GROUPS];
     int64_t tile_start[SOFT_MAX_GROUPS + 1];    // first work-group (row block) of each group
     int64_t ntiles;                             // work-groups in total
-    int mb[SOFT_MAX_GROUPS];                    // padded codebook size of each group
     int ngroups;
     int cosine;
     float scale, beta;
@@ -231,7 +230,6 @@ struct SoftArgs {
 };
 
 int64_t soft_select_tiles(int64_t B);
-int soft_select_pad(int64_t M);
 hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipStream_t s);
 
 // Probability vectorisation of sparse (CSR) probability rows.

@@ -1076,6 +1076,5 @@ hipError_t launch_soft_select(gs_dtype tin, gs_dtype tt, const SoftArgs &a, hipS
 
 int64_t soft_select_tiles(int64_t B) { return (B + SBLK - 1) / SBLK; }
 
-int soft_select_pad(int64_t M) { return pad_of(M); }
 
 }  // namespace gs
