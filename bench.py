@@ -172,7 +172,8 @@ class VsaWorkload:
 
     def fused_bytes(self):
         """Algorithmic bytes of one fused launch: read P, R, norms; write S,
-        argmax, A (the coordinates stay on chip)."""
+        argmax, A (no coordinates are written: the Gram form never forms
+        them, the coordinate form keeps them in registers)."""
         tot = 0
         for b in self.books:
             B, M, r = b["B"], b["M"], b["r"]
